@@ -1,0 +1,194 @@
+/*
+ * cs.h - C ABI of the Complementary Sparsity sparse-sparse layer for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method (Hunter, Spracklen and Ahmad, "Two Sparsities Are Better Than
+ * One", Section 3) overlays N sparse weight kernels whose supports do not
+ * collide into one dense packed kernel that stores, per slot, a weight value
+ * and a Kernel ID (Combine, Sections 3.1-3.2 step 1, Section 3.3.1).  At run
+ * time only the non-zero activations are visited (Select, Section 3.2 step 2);
+ * each is multiplied by the packed weights at its index (Multiply, step 3),
+ * each product goes to the accumulator of its Kernel ID (Route, step 4,
+ * Section 3.3.2) and is summed (Sum, step 5).  k-WTA (Section 3.3.3) then
+ * keeps the k largest outputs, which become the next layer's sparse input.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Status: every function returns a cs_status (0 = success, < 0 = error).
+ *    All argument checks are synchronous, run on the host and happen before
+ *    any HIP call, so a bad argument never launches work and needs no GPU.
+ *    A HIP launch or runtime failure returns CS_ERR_DEVICE; the library clears
+ *    the HIP error state it observed.  No C++ exception crosses this ABI.
+ *  - Ownership: the caller owns every buffer.  The GPU entry points never
+ *    allocate, free or synchronise; they enqueue kernels on `stream` (a
+ *    hipStream_t passed as void*, NULL = the default stream) and return.
+ *    Outputs are completely overwritten.  Inputs and outputs must not alias.
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are GPU memory
+ *    of the current HIP device.
+ *  - Layouts are dense row-major.  Images are NHWC.  Conv weights are OHWI,
+ *    flattened per output channel to r = kh*kw*c_in slots with slot
+ *    i = (ky*kw + kx)*c_in + c (taps major, channels inner; Section 5.1 treats
+ *    a 3x3 conv as nine 1x1 convs).
+ *  - Packed sets: output channel o belongs to set (group) g = o / n and has
+ *    Kernel ID kid = o - g*n; the n kernels of a set are n contiguous output
+ *    channels.  G = d_out / n packed kernels.
+ *  - Integer path: int8 activations and weights, int32 accumulation and bias
+ *    (Section 4: weights and activations quantised to 8 bits).  Float path:
+ *    fp32 throughout.  Integer sums wrap modulo 2^32 on overflow (the
+ *    configurations used stay below 2^31 by a wide margin).
+ */
+#ifndef CS_H_
+#define CS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CS_OK = 0,
+  CS_ERR_ARG = -1,        /* null pointer, negative/zero size, bad enum value   */
+  CS_ERR_SHAPE = -2,      /* sizes inconsistent or beyond the supported limits   */
+  CS_ERR_DTYPE = -3,      /* unsupported dtype or dtype combination              */
+  CS_ERR_COLLISION = -4,  /* cs_pack: two kernels of one set share a slot        */
+  CS_ERR_WORKSPACE = -5,  /* workspace missing or smaller than required          */
+  CS_ERR_DEVICE = -6      /* HIP launch or runtime error                         */
+} cs_status;
+
+typedef enum { CS_I8 = 0, CS_I32 = 1, CS_F32 = 2 } cs_dtype;
+
+/* Supported limits (checked, CS_ERR_SHAPE beyond them). */
+#define CS_MAX_ROW 65535   /* row length / c_in: indices are stored as uint16  */
+#define CS_MAX_N 32        /* kernels per packed set                           */
+#define CS_MAX_KWTA_ROW 2048 /* row length of cs_kwta                           */
+
+/*
+ * cs_pack - Combine (Section 3.1/3.2 step 1, Figure 7; Kernel ID of Section
+ * 3.3.1, local to the set as in Section 3.3.2).  Offline, HOST memory only,
+ * no HIP call.
+ *
+ *  wt      CS_I8 or CS_F32: element type of w and val.
+ *  w       host [d_out][r] dense weights; an exact zero is an absent weight.
+ *  n       complement factor, 1 <= n <= CS_MAX_N, must divide d_out.
+ *  val     host [r][G] out: val[i][g] = w[g*n + kid][i] for the one kernel of
+ *          set g that is non-zero at slot i; 0 where no kernel is (a hole).
+ *  kid     host [r][G] out (uint8): local Kernel ID in [0, n); 0 at holes.
+ *  holes   out (may be NULL): number of (i, g) slots no kernel of g uses.
+ *  bad_g, bad_i  out (may be NULL): on CS_ERR_COLLISION, the first colliding
+ *          (set, slot) in set-major, slot-minor order; -1 otherwise.
+ *  Errors: CS_ERR_ARG (null w/val/kid, d_out/r < 1), CS_ERR_SHAPE (n does not
+ *  divide d_out, n > CS_MAX_N), CS_ERR_DTYPE, CS_ERR_COLLISION (val/kid are
+ *  then unspecified).
+ */
+int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* val, uint8_t* kid,
+            int64_t* holes, int* bad_g, int* bad_i);
+
+/*
+ * cs_compact - the sparse representation of Select (Section 3.2 step 2: the
+ * non-zero activations with their indices; Figure 10 passes winners "along
+ * with their indices").  DEVICE memory.
+ *
+ *  xt      CS_I8 or CS_F32.
+ *  x       device [rows][c] dense activations.
+ *  idx     device [rows][c] out (uint16): per row, the indices of the non-zero
+ *          elements in ascending order in idx[row][0 .. cnt[row]-1]; the rest
+ *          of the row is left untouched.
+ *  val     device [rows][c] out (same dtype as x): the matching values.
+ *  cnt     device [rows] out (int32): number of non-zeros of each row.
+ *  A float -0.0 counts as zero.  rows may be 0 (nothing is launched).
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE (c > CS_MAX_ROW), CS_ERR_DEVICE.
+ */
+int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, void* val,
+               int32_t* cnt, void* stream);
+
+/*
+ * cs_mrs_conv2d - Multiply, Route and Sum (Section 3.2 steps 3-5, Sections
+ * 3.3.1-3.3.2) of a convolution whose input is already in cs_compact form.
+ * DEVICE memory.  For each output pixel and each non-zero (c, v) of every
+ * input pixel under the kernel window at tap (ky, kx), slot
+ * i = (ky*kw + kx)*c_in + c; for each set g the product v * val[i][g] is added
+ * to output channel g*n + kid[i][g].  Then bias, then the optional 2x2
+ * stride-2 max-pool (Table 1), then the NHWC store.
+ *
+ *  xt      CS_I8 (int8 lists and weights, int32 bias and y) or CS_F32.
+ *  idx, lval, cnt  device lists of the b*h*w input pixels as cs_compact
+ *          writes them, with row stride `cap` (cap >= c_in): every index
+ *          < c_in; a count above c_in is read as c_in.
+ *  b, h, w, c_in   input geometry; kh, kw >= 1; stride >= 1; pad >= 0.
+ *          ho = (h + 2*pad - kh)/stride + 1, wo likewise, both >= 1.
+ *  val, kid  device packed kernels [kh*kw*c_in][G] from cs_pack (every
+ *          kid < n).
+ *  c_out, n  n divides c_out, 1 <= n <= CS_MAX_N.
+ *  bias    device [c_out] (int32 / fp32) or NULL for none.
+ *  pool    1 (none) or 2 (2x2 stride-2 max-pool; ho and wo must be even).
+ *  y       device NHWC [b][ho/pool][wo/pool][c_out] out (int32 / fp32).
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE, CS_ERR_DEVICE.
+ */
+int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt, int cap,
+                  int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                  const void* val, const uint8_t* kid, int c_out, int n, const void* bias,
+                  int pool, void* y, void* stream);
+
+/*
+ * cs_linear - a whole sparse-sparse linear layer: cs_compact of x into the
+ * workspace, then Multiply/Route/Sum (a linear layer is the 1x1 convolution
+ * of 1x1 images).  DEVICE memory.
+ *
+ *  x       device [batch][d_in] (int8 or fp32), d_in <= CS_MAX_ROW.
+ *  val,kid device packed kernels [d_in][G] from cs_pack of [d_out][d_in].
+ *  bias    device [d_out] or NULL.   y  device [batch][d_out] out.
+ *  ws      device workspace of at least cs_workspace_bytes(0, xt, batch, d_in)
+ *          bytes, 256-byte aligned; its contents on entry do not matter.
+ *  Errors: as cs_compact and cs_mrs_conv2d, plus CS_ERR_WORKSPACE.
+ */
+int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, const uint8_t* kid,
+              int d_out, int n, const void* bias, void* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * cs_conv2d - a whole sparse-sparse conv layer: cs_compact of the b*h*w input
+ * pixels (rows of c_in) into the workspace, then cs_mrs_conv2d.  Arguments as
+ * cs_mrs_conv2d with x a device NHWC [b][h][w][c_in] tensor; ws must hold at
+ * least cs_workspace_bytes(1, xt, b*h*w, c_in) bytes.
+ */
+int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+              int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
+              const void* bias, int pool, void* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * cs_kwta - k-WTA (Section 2.2.2: exactly the top k activations propagate;
+ * Section 3.3.3: global k-WTA over a vector after linear layers, local k-WTA
+ * along the channels of each pixel after conv layers - both are this call
+ * with one row per vector or per pixel).  DEVICE memory.
+ *
+ *  it      CS_I32 or CS_F32: dtype of `in`.
+ *  in      device [rows][c], 1 <= c <= CS_MAX_KWTA_ROW, 0 <= k <= c.
+ *  Each row keeps exactly k elements: the k largest, equal values going to
+ *  the lower index; fp32 compares numerically (-0.0 ties +0.0; NaN is not
+ *  supported).  Winners keep their value (even if <= 0), the rest become 0.
+ *  ot      == it: out holds the masked values.
+ *          CS_I8 with it == CS_I32: out holds requantised winners
+ *          clamp(v >> shift, -127, 127) (arithmetic shift), 0 elsewhere.
+ *  shift   0..31, used only for CS_I8 output.
+ *  out     device [rows][c] out.  rows may be 0.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE, CS_ERR_DEVICE.
+ */
+int cs_kwta(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,
+            void* out, void* stream);
+
+/*
+ * cs_workspace_bytes - workspace cs_linear (op 0) or cs_conv2d (op 1) needs
+ * for `rows` input rows (batch, or b*h*w pixels) of c_in elements of dtype
+ * xt.  Returns 0 for invalid arguments.  Host only.
+ */
+size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in);
+
+/* cs_status_str - static, never-NULL description of a status code. */
+const char* cs_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CS_H_ */

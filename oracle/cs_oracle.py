@@ -42,6 +42,7 @@ __all__ = [
     "PackCollision",
     "pack",
     "unpack",
+    "compact_rows",
     "linear",
     "conv2d_nhwc",
     "im2col_nhwc",
@@ -115,6 +116,21 @@ def unpack(val: np.ndarray, kid: np.ndarray, n: int) -> np.ndarray:
             if val[i, g] != 0:
                 W[g * n + int(kid[i, g]), i] = val[i, g]
     return W
+
+
+# ---------------------------------------------------------------------------
+# Select's sparse representation (Section 3.2 step 2; Figure 10 sends the
+# winners on "along with their indices").
+# ---------------------------------------------------------------------------
+def compact_rows(x: np.ndarray):
+    """Per row of x [rows][c]: (indices of the non-zero elements in ascending
+    order, their values).  A float -0.0 is a zero."""
+    x = np.asarray(x)
+    out = []
+    for row in x.reshape(-1, x.shape[-1]):
+        nz = np.flatnonzero(row != 0)
+        out.append((nz, row[nz]))
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -1,0 +1,75 @@
+"""ctypes loader for libcs.so (the C ABI declared in include/cs.h).
+
+The library is built in-tree (python -m paper_2112_13896_amd.build).  There is
+no fallback: if it is missing or cannot be loaded, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs.so")
+
+CS_OK = 0
+CS_ERR_ARG = -1
+CS_ERR_SHAPE = -2
+CS_ERR_DTYPE = -3
+CS_ERR_COLLISION = -4
+CS_ERR_WORKSPACE = -5
+CS_ERR_DEVICE = -6
+
+CS_I8, CS_I32, CS_F32 = 0, 1, 2
+
+CS_MAX_ROW = 65535
+CS_MAX_N = 32
+CS_MAX_KWTA_ROW = 2048
+
+# name -> (restype, argtypes), in the order of include/cs.h
+_c = ctypes
+_vp, _i, _i64, _sz = _c.c_void_p, _c.c_int, _c.c_int64, _c.c_size_t
+SIGNATURES = {
+    "cs_pack": (_i, [_i, _vp, _i, _i, _i, _vp, _vp, _c.POINTER(_i64), _c.POINTER(_i), _c.POINTER(_i)]),
+    "cs_compact": (_i, [_i, _vp, _i64, _i, _vp, _vp, _vp, _vp]),
+    "cs_mrs_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i,
+                           _vp, _i, _vp, _vp]),
+    "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
+    "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _vp,
+                       _sz, _vp]),
+    "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),
+    "cs_workspace_bytes": (_sz, [_i, _i, _i64, _i]),
+    "cs_status_str": (_c.c_char_p, [_i]),
+}
+
+
+class CSError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status} ({status_str(status)})")
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it is not built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2112_13896_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def status_str(status: int) -> str:
+    return lib().cs_status_str(int(status)).decode()
+
+
+def check(fn: str, status: int) -> None:
+    if status != CS_OK:
+        raise CSError(fn, status)

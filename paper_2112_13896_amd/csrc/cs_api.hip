@@ -1,0 +1,260 @@
+// C ABI entry points of the sparse-sparse layer (declared in include/cs.h).
+// Every argument is checked on the host before the first HIP call; kernels
+// are enqueued on the caller's stream and nothing is allocated, freed or
+// synchronised here.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "compact_kernels.h"
+#include "cs.h"
+#include "kwta_kernels.h"
+#include "mrs_kernels.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+size_t elem_size(cs_dtype t) { return t == CS_I8 ? 1 : 4; }
+
+bool is_act_dtype(cs_dtype t) { return t == CS_I8 || t == CS_F32; }
+
+int launch_status() {
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? CS_OK : CS_ERR_DEVICE;
+}
+
+int blocks_for(int64_t threads, int bd, int64_t cap = 1 << 20) {
+  int64_t b = (threads + bd - 1) / bd;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (int)b;
+}
+
+// ---------------------------------------------------------------- compaction
+int compact_checked(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, void* val,
+                    int32_t* cnt, hipStream_t stream) {
+  if (rows == 0) return CS_OK;
+  if (c >= 64) {
+    const int64_t threads = rows * 64;
+    const int grid = blocks_for(threads, 256, 65536);
+    if (xt == CS_I8)
+      hipLaunchKernelGGL(cs::compact_wide<int8_t>, dim3(grid), dim3(256), 0, stream,
+                         static_cast<const int8_t*>(x), rows, c, idx, static_cast<int8_t*>(val),
+                         cnt);
+    else
+      hipLaunchKernelGGL(cs::compact_wide<float>, dim3(grid), dim3(256), 0, stream,
+                         static_cast<const float*>(x), rows, c, idx, static_cast<float*>(val),
+                         cnt);
+  } else {
+    int s_log2 = 0;
+    while ((1 << s_log2) < c) ++s_log2;
+    const int64_t rows_per_wave = 64 >> s_log2;
+    const int64_t threads = (rows + rows_per_wave - 1) / rows_per_wave * 64;
+    const int grid = blocks_for(threads, 256, 65536);
+    if (xt == CS_I8)
+      hipLaunchKernelGGL(cs::compact_narrow<int8_t>, dim3(grid), dim3(256), 0, stream,
+                         static_cast<const int8_t*>(x), rows, c, s_log2, idx,
+                         static_cast<int8_t*>(val), cnt);
+    else
+      hipLaunchKernelGGL(cs::compact_narrow<float>, dim3(grid), dim3(256), 0, stream,
+                         static_cast<const float*>(x), rows, c, s_log2, idx,
+                         static_cast<float*>(val), cnt);
+  }
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- MRS
+int conv_geometry(int b, int h, int w, int c_in, int kh, int kw, int stride, int pad, int c_out,
+                  int n, int pool, cs::ConvGeom* g) {
+  if (b < 1 || h < 1 || w < 1 || c_in < 1 || kh < 1 || kw < 1 || stride < 1 || pad < 0 ||
+      c_out < 1 || n < 1)
+    return CS_ERR_ARG;
+  if (c_in > CS_MAX_ROW || n > CS_MAX_N || c_out % n != 0) return CS_ERR_SHAPE;
+  if (pool != 1 && pool != 2) return CS_ERR_ARG;
+  const int64_t ho = ((int64_t)h + 2 * pad - kh) / stride + 1;
+  const int64_t wo = ((int64_t)w + 2 * pad - kw) / stride + 1;
+  if (h + 2 * pad < kh || w + 2 * pad < kw || ho < 1 || wo < 1) return CS_ERR_SHAPE;
+  if (pool == 2 && (ho % 2 != 0 || wo % 2 != 0)) return CS_ERR_SHAPE;
+  if ((int64_t)kh * kw * c_in > INT32_MAX) return CS_ERR_SHAPE;
+  g->B = b; g->H = h; g->W = w; g->C = c_in;
+  g->KH = kh; g->KW = kw; g->S = stride; g->P = pad;
+  g->Ho = (int)ho; g->Wo = (int)wo; g->pool = pool;
+  g->G = c_out / n; g->n = n; g->c_out = c_out;
+  g->cap = c_in;
+  return CS_OK;
+}
+
+int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+               const cs::ConvGeom& geo, const void* val, const uint8_t* kid, const void* bias,
+               void* y, hipStream_t stream) {
+  const int64_t opix = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
+  const int64_t total = opix * geo.G;
+  const bool one = geo.n == 1;
+  const int nacc = one ? 1 : geo.n;
+  const size_t per_thread = (size_t)nacc * 4 * (geo.pool == 2 ? 2 : 1);
+  const int bd = per_thread * 256 <= 32768 ? 256 : 128;
+  const size_t shmem = per_thread * bd;
+  const int64_t nblocks = (total + bd - 1) / bd;
+  if (nblocks > INT32_MAX) return CS_ERR_SHAPE;
+  const dim3 grid((unsigned)nblocks), block(bd);
+  if (xt == CS_I8) {
+    auto* lv = static_cast<const int8_t*>(lval);
+    auto* pv = static_cast<const int8_t*>(val);
+    auto* bs = static_cast<const int32_t*>(bias);
+    auto* yy = static_cast<int32_t*>(y);
+    if (one)
+      hipLaunchKernelGGL((cs::mrs_conv<int8_t, int32_t, true>), grid, block, shmem, stream, idx,
+                         lv, cnt, pv, kid, bs, yy, geo, total);
+    else
+      hipLaunchKernelGGL((cs::mrs_conv<int8_t, int32_t, false>), grid, block, shmem, stream, idx,
+                         lv, cnt, pv, kid, bs, yy, geo, total);
+  } else {
+    auto* lv = static_cast<const float*>(lval);
+    auto* pv = static_cast<const float*>(val);
+    auto* bs = static_cast<const float*>(bias);
+    auto* yy = static_cast<float*>(y);
+    if (one)
+      hipLaunchKernelGGL((cs::mrs_conv<float, float, true>), grid, block, shmem, stream, idx, lv,
+                         cnt, pv, kid, bs, yy, geo, total);
+    else
+      hipLaunchKernelGGL((cs::mrs_conv<float, float, false>), grid, block, shmem, stream, idx,
+                         lv, cnt, pv, kid, bs, yy, geo, total);
+  }
+  return launch_status();
+}
+
+struct WsLayout {
+  size_t idx_off, val_off, cnt_off, total;
+};
+
+WsLayout ws_layout(cs_dtype xt, int64_t rows, int c_in) {
+  WsLayout l;
+  l.idx_off = 0;
+  l.val_off = align_up((size_t)rows * c_in * 2);
+  l.cnt_off = l.val_off + align_up((size_t)rows * c_in * elem_size(xt));
+  l.total = l.cnt_off + align_up((size_t)rows * 4);
+  return l;
+}
+
+// ---------------------------------------------------------------- k-WTA
+template <typename TI, typename TO>
+int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
+                  hipStream_t stream) {
+  if (c <= 64 && k <= 32) {
+    const int64_t nb = (rows + cs::KWTA_LANE_ROWS - 1) / cs::KWTA_LANE_ROWS;
+    if (nb > INT32_MAX) return CS_ERR_SHAPE;
+    const size_t shmem = (size_t)cs::KWTA_LANE_ROWS * (c + 1) * 4;
+    const dim3 grid((unsigned)nb), block(cs::KWTA_LANE_ROWS);
+    if (k <= 8)
+      hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 8>), grid, block, shmem, stream, in, rows, c, k,
+                         out, shift);
+    else if (k <= 16)
+      hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 16>), grid, block, shmem, stream, in, rows, c, k,
+                         out, shift);
+    else
+      hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 32>), grid, block, shmem, stream, in, rows, c, k,
+                         out, shift);
+    return launch_status();
+  }
+  const int m = (c + 63) / 64;
+  const int64_t nb64 = (rows + cs::KWTA_WAVE_WAVES - 1) / cs::KWTA_WAVE_WAVES;
+  const int nb = (int)(nb64 < 65536 ? nb64 : 65536);
+  const dim3 grid(nb), block(64 * cs::KWTA_WAVE_WAVES);
+#define CS_KWTA_WAVE(MM)                                                                  \
+  hipLaunchKernelGGL((cs::kwta_wave<TI, TO, MM>), grid, block, 0, stream, in, rows, c, k, out, \
+                     shift)
+  if (m <= 1) CS_KWTA_WAVE(1);
+  else if (m <= 2) CS_KWTA_WAVE(2);
+  else if (m <= 4) CS_KWTA_WAVE(4);
+  else if (m <= 8) CS_KWTA_WAVE(8);
+  else if (m <= 16) CS_KWTA_WAVE(16);
+  else CS_KWTA_WAVE(32);
+#undef CS_KWTA_WAVE
+  return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, void* val,
+               int32_t* cnt, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  if (rows < 0 || c < 1) return CS_ERR_ARG;
+  if (c > CS_MAX_ROW) return CS_ERR_SHAPE;
+  if (rows > 0 && (!x || !idx || !val || !cnt)) return CS_ERR_ARG;
+  return compact_checked(xt, x, rows, c, idx, val, cnt, static_cast<hipStream_t>(stream));
+}
+
+int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt, int cap,
+                  int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                  const void* val, const uint8_t* kid, int c_out, int n, const void* bias,
+                  int pool, void* y, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (cap < c_in) return CS_ERR_SHAPE;
+  if (!idx || !lval || !cnt || !val || !kid || !y) return CS_ERR_ARG;
+  geo.cap = cap;
+  return mrs_launch(xt, idx, lval, cnt, geo, val, kid, bias, y, static_cast<hipStream_t>(stream));
+}
+
+int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+              int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
+              const void* bias, int pool, void* y, void* ws, size_t ws_bytes, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !val || !kid || !y) return CS_ERR_ARG;
+  const int64_t rows = (int64_t)b * h * w;
+  const WsLayout l = ws_layout(xt, rows, c_in);
+  if (!ws || ws_bytes < l.total) return CS_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return CS_ERR_WORKSPACE;
+  auto* base = static_cast<unsigned char*>(ws);
+  auto* idx = reinterpret_cast<uint16_t*>(base + l.idx_off);
+  void* lv = base + l.val_off;
+  auto* cnt = reinterpret_cast<int32_t*>(base + l.cnt_off);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
+  if (r != CS_OK) return r;
+  return mrs_launch(xt, idx, lv, cnt, geo, val, kid, bias, y, s);
+}
+
+int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, const uint8_t* kid,
+              int d_out, int n, const void* bias, void* y, void* ws, size_t ws_bytes,
+              void* stream) {
+  return cs_conv2d(xt, x, batch, 1, 1, d_in, 1, 1, 1, 0, val, kid, d_out, n, bias, 1, y, ws,
+                   ws_bytes, stream);
+}
+
+int cs_kwta(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,
+            void* out, void* stream) {
+  if (it != CS_I32 && it != CS_F32) return CS_ERR_DTYPE;
+  if (!(ot == it || (it == CS_I32 && ot == CS_I8))) return CS_ERR_DTYPE;
+  if (rows < 0 || c < 1 || k < 0) return CS_ERR_ARG;
+  if (k > c || c > CS_MAX_KWTA_ROW) return CS_ERR_SHAPE;
+  if (shift < 0 || shift > 31) return CS_ERR_ARG;
+  if (rows > 0 && (!in || !out)) return CS_ERR_ARG;
+  if (rows == 0) return CS_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (it == CS_F32)
+    return kwta_dispatch(static_cast<const float*>(in), rows, c, k, static_cast<float*>(out), 0,
+                         s);
+  if (ot == CS_I8)
+    return kwta_dispatch(static_cast<const int32_t*>(in), rows, c, k, static_cast<int8_t*>(out),
+                         shift, s);
+  return kwta_dispatch(static_cast<const int32_t*>(in), rows, c, k, static_cast<int32_t*>(out), 0,
+                       s);
+}
+
+size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in) {
+  if ((op != 0 && op != 1) || !is_act_dtype(xt) || rows < 0 || c_in < 1 || c_in > CS_MAX_ROW)
+    return 0;
+  return ws_layout(xt, rows, c_in).total;
+}
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+// cs_pack: Combine step of Complementary Sparsity (Sections 3.1 and 3.2,
+// step 1; Figure 7).  N kernels whose supports do not collide are overlaid
+// into one packed kernel; every slot keeps the weight value and the Kernel ID
+// of the kernel that owns it (Section 3.3.1), the ID being local to the set
+// (Section 3.3.2).  Host memory only; no HIP call.
+#include <cstdint>
+#include <cstring>
+
+#include "cs.h"
+
+namespace {
+
+template <typename T>
+int pack_impl(const T* w, int d_out, int r, int n, T* val, uint8_t* kid, int64_t* holes,
+              int* bad_g, int* bad_i) {
+  const int G = d_out / n;
+  int64_t nholes = 0;
+  for (int g = 0; g < G; ++g) {
+    for (int i = 0; i < r; ++i) {
+      int owner = -1;
+      for (int j = 0; j < n; ++j) {
+        const T v = w[(int64_t)(g * n + j) * r + i];
+        if (v != T(0)) {
+          if (owner >= 0) {
+            if (bad_g) *bad_g = g;
+            if (bad_i) *bad_i = i;
+            return CS_ERR_COLLISION;
+          }
+          owner = j;
+        }
+      }
+      const int64_t s = (int64_t)i * G + g;
+      if (owner < 0) {
+        val[s] = T(0);
+        kid[s] = 0;
+        ++nholes;
+      } else {
+        val[s] = w[(int64_t)(g * n + owner) * r + i];
+        kid[s] = (uint8_t)owner;
+      }
+    }
+  }
+  if (holes) *holes = nholes;
+  return CS_OK;
+}
+
+}  // namespace
+
+extern "C" int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* val,
+                       uint8_t* kid, int64_t* holes, int* bad_g, int* bad_i) {
+  if (bad_g) *bad_g = -1;
+  if (bad_i) *bad_i = -1;
+  if (holes) *holes = 0;
+  if (!w || !val || !kid || d_out < 1 || r < 1 || n < 1) return CS_ERR_ARG;
+  if (n > CS_MAX_N || d_out % n != 0) return CS_ERR_SHAPE;
+  switch (wt) {
+    case CS_I8:
+      return pack_impl(static_cast<const int8_t*>(w), d_out, r, n, static_cast<int8_t*>(val), kid,
+                       holes, bad_g, bad_i);
+    case CS_F32:
+      return pack_impl(static_cast<const float*>(w), d_out, r, n, static_cast<float*>(val), kid,
+                       holes, bad_g, bad_i);
+    default:
+      return CS_ERR_DTYPE;
+  }
+}
+
+extern "C" const char* cs_status_str(int status) {
+  switch (status) {
+    case CS_OK: return "ok";
+    case CS_ERR_ARG: return "invalid argument (null pointer, size or enum)";
+    case CS_ERR_SHAPE: return "inconsistent or unsupported shape";
+    case CS_ERR_DTYPE: return "unsupported dtype";
+    case CS_ERR_COLLISION: return "two kernels of one packed set share a slot";
+    case CS_ERR_WORKSPACE: return "workspace missing or too small";
+    case CS_ERR_DEVICE: return "HIP device error";
+    default: return "unknown status";
+  }
+}

@@ -1,0 +1,225 @@
+// k-WTA (Section 2.2.2: exactly the top k activations propagate; Section
+// 3.3.3: global k-WTA over a whole vector, local k-WTA along the channels of
+// one pixel).  Both variants are a per-row top-k here; a row is a sample or a
+// pixel.
+//
+// Semantics: exactly k winners per row; equal values go to the lower index;
+// fp32 compares numerically (-0.0 ties +0.0).  A value maps to an unsigned
+// key whose integer order is the value order, so the search runs on integer
+// keys: the threshold T is the k-th largest key, every key > T wins, and the
+// first (k - #{key > T}) keys equal to T in index order win too.
+//
+// Two gfx950 kernels:
+//  * kwta_lane  (row <= 64, k <= 32): one lane owns a row, staged through LDS
+//    with a padded stride so the 64 lanes read 64 different banks.  The lane
+//    keeps a descending top-K list by insertion (a max/min exchange per slot,
+//    no branches), which yields T;
+//  * kwta_wave  (row <= 2048): one wavefront owns a row, each lane holds up to
+//    M keys in registers.  T is found MSB-first, 8 bits per pass, with a
+//    256-bin LDS histogram per wavefront (the histogram search of Section
+//    3.3.3 and Figure 10, refined digit by digit so it is exact for 32-bit
+//    keys); the bin holding the k-th key is found with a wavefront suffix
+//    scan.  Ties are ranked with a ballot + popcount in index order.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cs {
+
+__device__ __forceinline__ uint32_t order_key(int32_t v) { return (uint32_t)v ^ 0x80000000u; }
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t b = __float_as_uint(f);
+  if (b == 0x80000000u) b = 0u;                    // -0.0 -> +0.0
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Winner value to output: same type, or int32 -> int8 requantisation.
+template <typename TI, typename TO>
+__device__ __forceinline__ TO kwta_out(TI v, int shift);
+template <>
+__device__ __forceinline__ int32_t kwta_out<int32_t, int32_t>(int32_t v, int) { return v; }
+template <>
+__device__ __forceinline__ float kwta_out<float, float>(float v, int) { return v; }
+template <>
+__device__ __forceinline__ int8_t kwta_out<int32_t, int8_t>(int32_t v, int shift) {
+  int32_t q = v >> shift;                           // arithmetic shift (floor)
+  q = q < -127 ? -127 : (q > 127 ? 127 : q);
+  return (int8_t)q;
+}
+
+constexpr int KWTA_LANE_ROWS = 128;   // rows (threads) per block of kwta_lane
+
+// LDS tile: KWTA_LANE_ROWS rows of c 32-bit words, stride c + 1.
+template <typename TI, typename TO, int KMAX>
+__global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict__ in,
+                                                            int64_t rows, int c, int k,
+                                                            TO* __restrict__ out, int shift) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  TI* tile = reinterpret_cast<TI*>(smem);
+  const int stride = c + 1;
+  const int tid = threadIdx.x;
+  const int64_t row0 = (int64_t)blockIdx.x * KWTA_LANE_ROWS;
+  const int64_t nrows64 = rows - row0 < KWTA_LANE_ROWS ? rows - row0 : KWTA_LANE_ROWS;
+  const int nrows = (int)nrows64;
+  const int nelem = nrows * c;
+  const TI* src = in + row0 * c;
+  for (int e = tid; e < nelem; e += KWTA_LANE_ROWS) tile[(e / c) * stride + (e % c)] = src[e];
+  __syncthreads();
+
+  uint32_t thr = 0;
+  int need = 0;
+  if (tid < nrows) {
+    const TI* r = tile + tid * stride;
+    uint32_t top[KMAX];
+#pragma unroll
+    for (int s = 0; s < KMAX; ++s) top[s] = 0u;
+    for (int i = 0; i < c; ++i) {
+      uint32_t x = order_key(r[i]);
+#pragma unroll
+      for (int s = 0; s < KMAX; ++s) {
+        const uint32_t hi = top[s] > x ? top[s] : x;
+        x = top[s] > x ? x : top[s];
+        top[s] = hi;
+      }
+    }
+    int gt = 0;
+#pragma unroll
+    for (int s = 0; s < KMAX; ++s) thr = (s == k - 1) ? top[s] : thr;
+#pragma unroll
+    for (int s = 0; s < KMAX; ++s) gt += (s < k && top[s] > thr) ? 1 : 0;
+    need = k - gt;
+  }
+  __syncthreads();
+  // second pass, results written back in place (as TO in a TO-typed view)
+  TO* otile = reinterpret_cast<TO*>(smem);
+  const int ostride = (int)(stride * sizeof(TI) / sizeof(TO));
+  if (tid < nrows) {
+    TI* r = tile + tid * stride;
+    TO* o = otile + tid * ostride;
+    for (int i = 0; i < c; ++i) {
+      const TI v = r[i];
+      const uint32_t x = order_key(v);
+      bool win = false;
+      if (k > 0) {
+        if (x > thr) {
+          win = true;
+        } else if (x == thr && need > 0) {
+          win = true;
+          --need;
+        }
+      }
+      // o[i] never overlaps an r[j] read later: TO is not wider than TI
+      o[i] = win ? kwta_out<TI, TO>(v, shift) : TO(0);
+    }
+  }
+  __syncthreads();
+  TO* dst = out + row0 * c;
+  for (int e = tid; e < nelem; e += KWTA_LANE_ROWS) dst[e] = otile[(e / c) * ostride + (e % c)];
+}
+
+constexpr int KWTA_WAVE_WAVES = 4;   // wavefronts (rows) per block of kwta_wave
+
+template <typename TI, typename TO, int M>
+__global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __restrict__ in,
+                                                                  int64_t rows, int c, int k,
+                                                                  TO* __restrict__ out,
+                                                                  int shift) {
+  __shared__ uint32_t hist[KWTA_WAVE_WAVES][256];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  uint32_t* h = hist[wv];
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  const bool all_win = (k == c);
+  const bool none_win = (k == 0);
+  for (int64_t row0 = (int64_t)blockIdx.x * KWTA_WAVE_WAVES; row0 < rows;
+       row0 += (int64_t)gridDim.x * KWTA_WAVE_WAVES) {           // uniform across the block
+    const int64_t row = row0 + wv;
+    const bool live = row < rows;                                 // uniform across the wave
+    TI v[M];
+    uint32_t key[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const int e = j * 64 + lane;
+      v[j] = (live && e < c) ? in[row * c + e] : TI(0);
+      key[j] = order_key(v[j]);
+    }
+    uint32_t prefix = 0u, pmask = 0u;
+    int need = k;
+    const bool search = live && !all_win && !none_win;
+    for (int sh = 24; sh >= 0; sh -= 8) {
+      for (int b = lane; b < 256; b += 64) h[b] = 0u;
+      __syncthreads();
+      if (search) {
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+          const int e = j * 64 + lane;
+          if (e < c && (key[j] & pmask) == prefix)
+            __hip_atomic_fetch_add(&h[(key[j] >> sh) & 255u], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+      }
+      __syncthreads();
+      if (search) {
+        const uint32_t c0 = h[4 * lane], c1 = h[4 * lane + 1], c2 = h[4 * lane + 2],
+                       c3 = h[4 * lane + 3];
+        const uint32_t s = c0 + c1 + c2 + c3;
+        uint32_t incl = s;                                   // sum over lanes >= this lane
+        for (int off = 1; off < 64; off <<= 1) {
+          const uint32_t t = __shfl_down(incl, off, 64);
+          if (lane + off < 64) incl += t;
+        }
+        const uint32_t excl = incl - s;                      // keys in higher bins
+        const uint32_t un = (uint32_t)need;
+        const bool here = excl < un && un <= incl;
+        int d = 0;
+        uint32_t above = 0;
+        if (here) {
+          uint32_t cum = excl;
+          if (cum + c3 >= un) {
+            d = 4 * lane + 3;
+          } else {
+            cum += c3;
+            if (cum + c2 >= un) {
+              d = 4 * lane + 2;
+            } else {
+              cum += c2;
+              if (cum + c1 >= un) {
+                d = 4 * lane + 1;
+              } else {
+                cum += c1;
+                d = 4 * lane;
+              }
+            }
+          }
+          above = cum;
+        }
+        const uint64_t bal = __ballot(here);
+        const int src = __ffsll((long long)bal) - 1;
+        d = __shfl(d, src, 64);
+        above = __shfl(above, src, 64);
+        need -= (int)above;
+        prefix |= (uint32_t)d << sh;
+        pmask |= 0xFFu << sh;
+      }
+      __syncthreads();
+    }
+    // ranks of the ties in index order (element index = j*64 + lane)
+    int run = 0;
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const int e = j * 64 + lane;
+      const bool valid = live && e < c;
+      const bool eq = search && valid && key[j] == prefix;
+      const uint64_t b = __ballot(eq);
+      const int rank = run + __popcll(b & below);
+      run += __popcll(b);
+      bool win;
+      if (all_win) win = true;
+      else if (none_win) win = false;
+      else win = key[j] > prefix || (eq && rank < need);
+      if (valid) out[row * c + e] = win ? kwta_out<TI, TO>(v[j], shift) : TO(0);
+    }
+  }
+}
+
+}  // namespace cs

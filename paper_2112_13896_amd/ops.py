@@ -1,0 +1,170 @@
+"""Torch-facing wrappers of the C ABI (argument marshalling only).
+
+Every step of the layer runs in the HIP kernels of libcs.so; these functions
+check tensor placement/dtype/shape, allocate outputs with torch and pass raw
+device pointers plus torch's current HIP stream.  They never compute on the
+host and have no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import CS_F32, CS_I8, CS_I32, check, lib
+
+_TORCH_DT = {torch.int8: CS_I8, torch.int32: CS_I32, torch.float32: CS_F32}
+_NP_DT = {np.dtype(np.int8): CS_I8, np.dtype(np.float32): CS_F32}
+
+
+def _dt(t: torch.Tensor) -> int:
+    try:
+        return _TORCH_DT[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}") from None
+
+
+def _dev(t: torch.Tensor, name: str) -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _opt(t: torch.Tensor | None, name: str):
+    return None if t is None else _dev(t, name)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ------------------------------------------------------------------ pack (host)
+def pack(W: np.ndarray, n: int):
+    """Combine on the host: W [d_out][r] (int8 or float32) -> (val [r][G],
+    kid [r][G] uint8, holes).  Raises CSError(CS_ERR_COLLISION) with .bad
+    = (g, i) when two kernels of a set share a slot."""
+    W = np.ascontiguousarray(W)
+    if W.ndim != 2:
+        raise ValueError("W must be [d_out][r]")
+    d_out, r = W.shape
+    wt = _NP_DT.get(W.dtype)
+    if wt is None:
+        raise TypeError(f"unsupported weight dtype {W.dtype}")
+    G = d_out // n if n > 0 else 0
+    val = np.zeros((r, max(G, 1)), dtype=W.dtype)
+    kid = np.zeros((r, max(G, 1)), dtype=np.uint8)
+    holes = ctypes.c_int64(0)
+    bg, bi = ctypes.c_int(0), ctypes.c_int(0)
+    st = lib().cs_pack(wt, W.ctypes.data, d_out, r, n, val.ctypes.data, kid.ctypes.data,
+                       ctypes.byref(holes), ctypes.byref(bg), ctypes.byref(bi))
+    if st != _lib.CS_OK:
+        err = _lib.CSError("cs_pack", st)
+        err.bad = (bg.value, bi.value)
+        raise err
+    return val, kid, int(holes.value)
+
+
+# ------------------------------------------------------------------ device ops
+def compact(x: torch.Tensor):
+    """x [rows][c] (int8/float32) -> (idx uint16-as-int16 [rows][c], val, cnt int32).
+    Only idx[r, :cnt[r]] and val[r, :cnt[r]] are defined."""
+    if x.dim() != 2:
+        raise ValueError("x must be [rows][c]")
+    rows, c = x.shape
+    idx = torch.empty((rows, c), dtype=torch.int16, device=x.device)
+    val = torch.empty_like(x)
+    cnt = torch.empty((rows,), dtype=torch.int32, device=x.device)
+    check("cs_compact", lib().cs_compact(_dt(x), _dev(x, "x"), rows, c, _dev(idx, "idx"),
+                                         _dev(val, "val"), _dev(cnt, "cnt"), _stream()))
+    return idx, val, cnt
+
+
+def conv_out(h: int, k: int, stride: int, pad: int) -> int:
+    return (h + 2 * pad - k) // stride + 1
+
+
+def mrs_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, val, kid,
+               kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None, pool: int = 1,
+               out: torch.Tensor | None = None) -> torch.Tensor:
+    """Multiply/route/sum on compacted lists of the b*h*w input pixels."""
+    b, h, w, c_in = in_shape
+    c_out = val.shape[1] * n
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    ydt = torch.int32 if lval.dtype == torch.int8 else torch.float32
+    if out is None:
+        out = torch.empty((b, ho // pool, wo // pool, c_out), dtype=ydt, device=lval.device)
+    check("cs_mrs_conv2d", lib().cs_mrs_conv2d(
+        _dt(lval), _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
+        b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"), _dev(kid, "kid"), c_out, n,
+        _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
+    return out
+
+
+def workspace_bytes(op: int, dtype: torch.dtype, rows: int, c_in: int) -> int:
+    return int(lib().cs_workspace_bytes(op, _TORCH_DT[dtype], rows, c_in))
+
+
+def workspace(op: int, dtype: torch.dtype, rows: int, c_in: int, device) -> torch.Tensor:
+    nbytes = workspace_bytes(op, dtype, rows, c_in)
+    if nbytes == 0:
+        raise ValueError("invalid workspace request")
+    return torch.empty((nbytes,), dtype=torch.uint8, device=device)
+
+
+def conv2d(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: int, n: int,
+           stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
+           ws: torch.Tensor | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Sparse-sparse conv of NHWC x with packed OHWI kernels (val/kid [kh*kw*c_in][G])."""
+    if x.dim() != 4:
+        raise ValueError("x must be NHWC")
+    b, h, w, c_in = x.shape
+    c_out = val.shape[1] * n
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
+    if out is None:
+        out = torch.empty((b, max(ho, 0) // pool, max(wo, 0) // pool, c_out), dtype=ydt,
+                          device=x.device)
+    if ws is None:
+        ws = workspace(1, x.dtype, b * h * w, c_in, x.device)
+    check("cs_conv2d", lib().cs_conv2d(
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"),
+        _dev(kid, "kid"), c_out, n, _opt(bias, "bias"), pool, _dev(out, "out"), _dev(ws, "ws"),
+        ws.numel(), _stream()))
+    return out
+
+
+def linear(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, n: int,
+           bias: torch.Tensor | None = None, ws: torch.Tensor | None = None,
+           out: torch.Tensor | None = None) -> torch.Tensor:
+    """Sparse-sparse linear layer: x [batch][d_in], packed val/kid [d_in][G]."""
+    if x.dim() != 2:
+        raise ValueError("x must be [batch][d_in]")
+    batch, d_in = x.shape
+    d_out = val.shape[1] * n
+    ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
+    if out is None:
+        out = torch.empty((batch, d_out), dtype=ydt, device=x.device)
+    if ws is None:
+        ws = workspace(0, x.dtype, batch, d_in, x.device)
+    check("cs_linear", lib().cs_linear(
+        _dt(x), _dev(x, "x"), batch, d_in, _dev(val, "val"), _dev(kid, "kid"), d_out, n,
+        _opt(bias, "bias"), _dev(out, "out"), _dev(ws, "ws"), ws.numel(), _stream()))
+    return out
+
+
+def kwta(x: torch.Tensor, k: int, out_dtype: torch.dtype | None = None, shift: int = 0,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    """k-WTA along the last axis.  out_dtype=torch.int8 on int32 input
+    requantises the winners with `shift`."""
+    c = x.shape[-1]
+    rows = x.numel() // c if c else 0
+    odt = x.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty(x.shape, dtype=odt, device=x.device)
+    check("cs_kwta", lib().cs_kwta(_dt(x), _dev(x, "x"), rows, c, k, _TORCH_DT[odt], shift,
+                                   _dev(out, "out"), _stream()))
+    return out

@@ -1,0 +1,201 @@
+"""C ABI checks that need no GPU: exports, host pack, argument validation.
+
+There is no GPU in the build container, so any HIP call made by an entry
+point would come back as CS_ERR_DEVICE.  Getting the specific validation code
+instead shows that every check runs on the host before the first HIP call.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import cs_oracle as o
+from paper_2112_13896_amd import _lib, ops
+from paper_2112_13896_amd._lib import (CS_ERR_ARG, CS_ERR_COLLISION, CS_ERR_DTYPE, CS_ERR_SHAPE,
+                                       CS_ERR_WORKSPACE, CS_F32, CS_I8, CS_I32, CS_OK)
+from workloads import complementary_weights
+
+HEADER = os.path.join(os.path.dirname(__file__), "..", "include", "cs.h")
+FAKE = 0x10000          # a non-null address that must never be dereferenced
+FAKE_WS = 0x100000      # 256-aligned fake workspace
+
+
+@pytest.fixture(scope="module")
+def L():
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(cs_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) == set(_lib.SIGNATURES), names
+    for nm in names:
+        assert hasattr(L, nm)
+
+
+def test_status_strings(L):
+    for code in range(0, -7, -1):
+        s = _lib.status_str(code)
+        assert s and s != "unknown status"
+    assert _lib.status_str(5) == "unknown status"
+
+
+@pytest.mark.parametrize("dtype", ["int8", "float32"])
+def test_pack_matches_oracle(dtype):
+    r = np.random.default_rng(3)
+    for d_out, R, n in [(64, 512, 8), (1500, 1600, 20), (12, 1500, 1), (64, 1600, 16), (9, 7, 3)]:
+        if R % n:
+            W = r.integers(-5, 6, size=(d_out, R)).astype(dtype)
+            W[:, :] = 0
+            for g in range(d_out // n):          # disjoint but not covering: holes
+                for i in range(R):
+                    j = r.integers(0, n + 1)
+                    if j < n:
+                        W[g * n + j, i] = r.integers(1, 100)
+        else:
+            W = complementary_weights(r, r, d_out, R, n, "int8" if dtype == "int8" else "normal")
+        val, kid, holes = ops.pack(W, n)
+        v2, k2, h2 = o.pack(W, n)
+        assert val.dtype == W.dtype
+        assert np.array_equal(val, v2) and np.array_equal(kid, k2) and holes == h2
+
+
+def test_pack_collision_reports_first_offender():
+    W = np.zeros((6, 10), dtype=np.int8)
+    W[3, 4] = 1
+    W[5, 4] = 2      # group 1 collides at slot 4
+    W[4, 9] = 1
+    W[3, 9] = 1      # group 1 collides at slot 9 too (later)
+    with pytest.raises(_lib.CSError) as e:
+        ops.pack(W, 3)
+    assert e.value.status == CS_ERR_COLLISION and e.value.bad == (1, 4)
+    with pytest.raises(o.PackCollision) as e2:
+        o.pack(W, 3)
+    assert (e2.value.g, e2.value.i) == (1, 4)
+
+
+def test_pack_argument_errors(L):
+    w = np.ones((4, 4), dtype=np.int8)
+    out = np.zeros(64, dtype=np.int8)
+    k = np.zeros(64, dtype=np.uint8)
+    p = lambda *a: L.cs_pack(*a)  # noqa: E731
+    assert p(CS_I8, None, 4, 4, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
+    assert p(CS_I8, w.ctypes.data, 4, 4, 3, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_SHAPE
+    assert p(CS_I8, w.ctypes.data, 4, 4, 0, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
+    assert p(CS_I32, w.ctypes.data, 4, 4, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_DTYPE
+    assert p(CS_I8, w.ctypes.data, 64, 4, 64, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_SHAPE
+    assert p(CS_I8, w.ctypes.data, 4, 0, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
+
+
+def test_compact_validation(L):
+    c = L.cs_compact
+    assert c(CS_I32, FAKE, 4, 8, FAKE, FAKE, FAKE, None) == CS_ERR_DTYPE
+    assert c(CS_I8, FAKE, -1, 8, FAKE, FAKE, FAKE, None) == CS_ERR_ARG
+    assert c(CS_I8, FAKE, 4, 0, FAKE, FAKE, FAKE, None) == CS_ERR_ARG
+    assert c(CS_I8, FAKE, 4, 70000, FAKE, FAKE, FAKE, None) == CS_ERR_SHAPE
+    assert c(CS_F32, None, 4, 8, FAKE, FAKE, FAKE, None) == CS_ERR_ARG
+    assert c(CS_F32, FAKE, 4, 8, FAKE, FAKE, None, None) == CS_ERR_ARG
+    assert c(CS_F32, None, 0, 8, None, None, None, None) == CS_OK       # empty: nothing launched
+
+
+def conv_args(**kw):
+    a = dict(xt=CS_I8, x=FAKE, b=2, h=8, w=8, c_in=4, kh=3, kw=3, stride=1, pad=1, val=FAKE,
+             kid=FAKE, c_out=8, n=4, bias=None, pool=1, y=FAKE, ws=FAKE_WS, ws_bytes=1 << 30,
+             stream=None)
+    a.update(kw)
+    return list(a.values())
+
+
+def test_conv2d_validation(L):
+    f = L.cs_conv2d
+    assert f(*conv_args(xt=CS_I32)) == CS_ERR_DTYPE
+    assert f(*conv_args(b=0)) == CS_ERR_ARG
+    assert f(*conv_args(stride=0)) == CS_ERR_ARG
+    assert f(*conv_args(pad=-1)) == CS_ERR_ARG
+    assert f(*conv_args(n=3)) == CS_ERR_SHAPE                  # 3 does not divide 8
+    assert f(*conv_args(n=40, c_out=80)) == CS_ERR_SHAPE       # n > CS_MAX_N
+    assert f(*conv_args(c_in=70000)) == CS_ERR_SHAPE
+    assert f(*conv_args(kh=11, pad=1)) == CS_ERR_SHAPE         # window larger than padded input
+    assert f(*conv_args(pool=3)) == CS_ERR_ARG
+    assert f(*conv_args(pool=2, h=7, w=7)) == CS_ERR_SHAPE     # odd conv output
+    assert f(*conv_args(x=None)) == CS_ERR_ARG
+    assert f(*conv_args(val=None)) == CS_ERR_ARG
+    assert f(*conv_args(y=None)) == CS_ERR_ARG
+    need = L.cs_workspace_bytes(1, CS_I8, 2 * 8 * 8, 4)
+    assert f(*conv_args(ws_bytes=need - 1)) == CS_ERR_WORKSPACE
+    assert f(*conv_args(ws=None)) == CS_ERR_WORKSPACE
+    assert f(*conv_args(ws=FAKE_WS + 8)) == CS_ERR_WORKSPACE   # misaligned
+
+
+def test_mrs_and_linear_validation(L):
+    m = L.cs_mrs_conv2d
+    base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, FAKE, 8, 4, None, 1, FAKE, None]
+    assert m(*base[:4], 3, *base[5:]) == CS_ERR_SHAPE          # cap < c_in
+    bad = list(base)
+    bad[1] = None
+    assert m(*bad) == CS_ERR_ARG
+    bad = list(base)
+    bad[0] = CS_I32
+    assert m(*bad) == CS_ERR_DTYPE
+    lin = L.cs_linear
+    assert lin(CS_I8, FAKE, 16, 512, FAKE, FAKE, 64, 7, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_SHAPE
+    assert lin(CS_I8, FAKE, 0, 512, FAKE, FAKE, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
+    assert lin(CS_I8, FAKE, 16, 512, FAKE, FAKE, 64, 8, None, FAKE, FAKE_WS, 10, None) == CS_ERR_WORKSPACE
+    assert lin(CS_F32, FAKE, 16, 512, None, FAKE, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
+
+
+def test_kwta_validation(L):
+    k = L.cs_kwta
+    assert k(CS_I8, FAKE, 4, 64, 8, CS_I8, 0, FAKE, None) == CS_ERR_DTYPE
+    assert k(CS_F32, FAKE, 4, 64, 8, CS_I8, 0, FAKE, None) == CS_ERR_DTYPE
+    assert k(CS_I32, FAKE, 4, 64, 8, CS_F32, 0, FAKE, None) == CS_ERR_DTYPE
+    assert k(CS_I32, FAKE, 4, 64, 65, CS_I32, 0, FAKE, None) == CS_ERR_SHAPE
+    assert k(CS_I32, FAKE, 4, 3000, 8, CS_I32, 0, FAKE, None) == CS_ERR_SHAPE
+    assert k(CS_I32, FAKE, 4, 64, -1, CS_I32, 0, FAKE, None) == CS_ERR_ARG
+    assert k(CS_I32, FAKE, 4, 0, 0, CS_I32, 0, FAKE, None) == CS_ERR_ARG
+    assert k(CS_I32, FAKE, 4, 64, 8, CS_I8, 32, FAKE, None) == CS_ERR_ARG
+    assert k(CS_I32, None, 4, 64, 8, CS_I8, 3, FAKE, None) == CS_ERR_ARG
+    assert k(CS_I32, None, 0, 64, 8, CS_I8, 3, None, None) == CS_OK     # empty: nothing launched
+
+
+def test_workspace_bytes(L):
+    def al(v):
+        return (v + 255) // 256 * 256
+    for op, xt, rows, c in [(0, CS_I8, 16, 512), (1, CS_F32, 100352, 64), (1, CS_I8, 262144, 1)]:
+        es = 1 if xt == CS_I8 else 4
+        exp = al(rows * c * 2) + al(rows * c * es) + al(rows * 4)
+        assert L.cs_workspace_bytes(op, xt, rows, c) == exp
+    assert L.cs_workspace_bytes(2, CS_I8, 4, 4) == 0
+    assert L.cs_workspace_bytes(0, CS_I32, 4, 4) == 0
+    assert L.cs_workspace_bytes(0, CS_I8, 4, 0) == 0
+    assert L.cs_workspace_bytes(0, CS_I8, -1, 4) == 0
+
+
+def test_product_path_has_no_fallback(monkeypatch, tmp_path):
+    """With the library absent the binding raises instead of computing."""
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(_lib, "_LIB", None)
+    with pytest.raises(RuntimeError):
+        _lib.lib()
+    with pytest.raises(RuntimeError):
+        ops.pack(np.ones((2, 2), dtype=np.int8), 1)
+
+
+def test_ctypes_signatures_match_header():
+    """Each binding signature has as many arguments as the header declares."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for name, (_, args) in _lib.SIGNATURES.items():
+        m = re.search(name + r"\s*\(([^;]*)\)\s*;", text, flags=re.S)
+        assert m, name
+        nargs = len([a for a in m.group(1).split(",") if a.strip()])
+        assert nargs == len(args), (name, nargs, len(args))
+        assert ctypes  # silence unused import warnings in some linters

@@ -415,3 +415,16 @@ def test_requant_shift_rule():
     assert networks.requant_shift(np.array([128])) == 1
     assert networks.requant_shift(np.array([-255, 3])) == 1
     assert networks.requant_shift(np.array([256])) == 2
+
+
+def test_compact_rows_brute_force():
+    r = rng(32)
+    x = r.integers(-3, 4, size=(9, 13)).astype(np.int8)
+    xf = np.where(r.random((4, 7)) < 0.5, 0.0, r.normal(size=(4, 7))).astype(np.float32)
+    xf[0, 0] = -0.0
+    for arr in (x, xf):
+        res = o.compact_rows(arr)
+        for row, (ii, vv) in zip(arr, res):
+            exp_i = [j for j in range(len(row)) if row[j] != 0]
+            assert list(ii) == exp_i
+            assert [row[j] for j in exp_i] == list(vv)
