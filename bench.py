@@ -1,0 +1,257 @@
+#!/usr/bin/env python3
+"""Throughput of the Complementary Sparsity sparse-sparse layer chain on one GPU.
+
+    python bench.py [--steps K] [--warmup W] [--config C]
+
+A step is one pass of the whole chain over one batch: per layer, compaction
+of the activations into (index, value) lists, multiply-route-sum (+ bias,
++ 2x2 max-pool), k-WTA (+ int8 requantisation).  Inputs are resident in HBM
+when the timed region starts; the chain rotates among buffer sets (input +
+every intermediate) totalling more than 512 MiB, so a step does not find the
+previous step's data in the 256 MiB Infinity Cache.
+
+Default workload: the keyword-spotting CNN of Table 1 (config 2, int8, batch
+256).  Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sparse-sparse layer samples/s + dense-equiv GMAC/s; achieved HBM GB/s (1 GPU)"
+HBM_PEAK_GBS = 8000.0               # MI355X HBM3E, published
+INT_VALU_PEAK_TOPS = 78.6           # 256 CU x 64 lanes x 2.4 GHz x (mul+add) int32 VALU
+FP32_VALU_PEAK_TFLOPS = 157.3       # published fp32 vector peak
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def conv_products(cnt_map: np.ndarray, spec) -> int:
+    """Products the multiply-route-sum kernel performs: for every conv output
+    pixel (before pooling), the non-zeros under its window, times G."""
+    b, h, w = cnt_map.shape
+    ho = (h + 2 * spec.pad - spec.kh) // spec.stride + 1
+    wo = (w + 2 * spec.pad - spec.kw) // spec.stride + 1
+    pad = np.zeros((b, h + 2 * spec.pad, w + 2 * spec.pad), dtype=np.int64)
+    pad[:, spec.pad:spec.pad + h, spec.pad:spec.pad + w] = cnt_map
+    tot = 0
+    for ky in range(spec.kh):
+        for kx in range(spec.kw):
+            tot += int(pad[:, ky:ky + spec.stride * (ho - 1) + 1:spec.stride,
+                           kx:kx + spec.stride * (wo - 1) + 1:spec.stride].sum())
+    return tot * (spec.c_out // spec.n)
+
+
+def layer_costs(net, bufs, cfg) -> dict:
+    """Algorithmic bytes (and products) per launch of every kernel, from the
+    actual non-zero counts of this batch."""
+    import torch
+    costs = {}
+    for li, p in enumerate(net.packed):
+        s = p.spec
+        es = 1 if p.val.dtype == torch.int8 else 4
+        rows = net.list_rows[li]
+        cnt = bufs.cnt[li].cpu().numpy().astype(np.int64)
+        nnz = int(cnt.sum())
+        lists = nnz * (2 + es) + rows * 4
+        costs[f"{s.name}.compact"] = {"bytes": rows * s.c_in * es + lists}
+        out_elems = int(np.prod(net.out_shapes[li]))
+        table = p.val.numel() * (es + 1)
+        bias = 0 if p.bias is None else s.c_out * 4
+        mrs_bytes = lists + table + bias + out_elems * 4
+        if s.kind == "conv":
+            b, h, w, _ = net.in_shapes[li]
+            prods = conv_products(cnt.reshape(b, h, w), s)
+        else:
+            prods = nnz * (s.c_out // s.n)
+        costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
+                                  "int": p.val.dtype == torch.int8}
+        if s.k is not None:
+            ob = 1 if s.shift is not None else 4
+            costs[f"{s.name}.kwta"] = {"bytes": out_elems * (4 + ob)}
+    return costs
+
+
+def dense_macs(cfg) -> int:
+    shape = (cfg.batch,) + tuple(cfg.in_shape)
+    tot = 0
+    for s in cfg.layers:
+        if s.kind == "conv":
+            b, h, w, c = shape
+            ho = (h + 2 * s.pad - s.kh) // s.stride + 1
+            wo = (w + 2 * s.pad - s.kw) // s.stride + 1
+            tot += b * ho * wo * s.c_out * s.kh * s.kw * c
+            shape = (b, ho // s.pool, wo // s.pool, s.c_out)
+        else:
+            b = shape[0]
+            tot += b * int(np.prod(shape[1:])) * s.c_out
+            shape = (b, s.c_out)
+    return tot
+
+
+def roofline_for(name: str, cost: dict, ms: float) -> dict:
+    sec = ms * 1e-3
+    gbs = cost["bytes"] / sec / 1e9
+    if "products" in cost:
+        # ridge: products per byte above which the VALU roof is the lower one
+        if cost["int"]:
+            peak_ops = INT_VALU_PEAK_TOPS
+        else:
+            peak_ops = FP32_VALU_PEAK_TFLOPS
+        ops = 2.0 * cost["products"]
+        intensity = ops / cost["bytes"]
+        ridge = peak_ops * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if intensity > ridge:
+            ach = ops / sec / 1e12
+            return {"bound": "alu", "achieved": round(ach, 3), "peak": peak_ops,
+                    "unit": "TOP/s" if cost["int"] else "TFLOP/s", "frac": round(ach / peak_ops, 4),
+                    "traffic": None, "kernel": name, "algorithmic_bytes": cost["bytes"],
+                    "products": cost["products"], "hbm_gbs": round(gbs, 1)}
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": name,
+            "algorithmic_bytes": cost["bytes"], **({"products": cost["products"]} if "products" in cost else {})}
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE and
+    WRITE_SIZE scaled by a copy-kernel calibration), if a record for exactly
+    this kernel source is committed; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        from paper_2112_13896_amd import build as b
+        if rec.get("source_digest") != b.source_digest():
+            return None
+        return rec.get("kernels", {}).get(workload, {}).get(kernel)
+    except Exception:
+        return None
+
+
+def cpu_baseline(cfg, inp, seconds: float) -> dict:
+    """The CPU oracle (as it stands) on the whole batch, repeated until about
+    `seconds` of work; samples/s over all repetitions."""
+    from oracle import networks
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        networks.run_chain(cfg.layers, inp["x"], inp["W"], inp["b"])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 50:
+            break
+    return {"value": round(reps * cfg.batch / el, 2), "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reps} x full batch of {cfg.batch} ({cfg.name}), float64 numpy oracle, "
+                      f"{el:.1f} s on {os.cpu_count()} host CPUs (BLAS threads {threads})"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload id (default 2: keyword-spotting CNN)")
+    ap.add_argument("--rotate-mib", type=float, default=512.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
+              "the sparse-sparse path shards over samples with no exchange, so N GPUs run N "
+              "independent copies of this measurement.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2112_13896_amd.network import EventTimer, Network
+    from workloads import CONFIGS, generate
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        return 1
+    cfg = CONFIGS[args.config]
+    log(f"bench: workload {cfg.name}, batch {cfg.batch}")
+    inp = generate(cfg)
+    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
+    per_set = net.bufs.nbytes() + inp["x"].nbytes
+    nsets = max(8, math.ceil(args.rotate_mib * 2 ** 20 / per_set))
+    sets = [net.bufs] + [net.make_buffers() for _ in range(nsets - 1)]
+    xs = [torch.from_numpy(inp["x"]).cuda() for _ in range(nsets)]
+    log(f"bench: {nsets} rotating buffer sets of {per_set / 2 ** 20:.1f} MiB")
+
+    def step(i, timer=None):
+        j = i % nsets
+        net.forward(xs[j], sets[j], timer)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    # per-kernel breakdown (untimed pass) to find the dominant kernel
+    brk = EventTimer()
+    for i in range(max(nsets, 8)):
+        step(i, brk)
+    breakdown = brk.mean_ms()
+    dominant = max(breakdown, key=breakdown.get)
+    costs = layer_costs(net, sets[0], cfg)
+    log("bench: per-kernel ms " + ", ".join(f"{k}={v:.4f}" for k, v in breakdown.items()))
+
+    timer = EventTimer([dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, timer)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms = timer.mean_ms()[dominant]
+    ms_step = wall * 1e3 / args.steps
+    samples_s = cfg.batch / (ms_step * 1e-3)
+    roof = roofline_for(dominant, costs[dominant], dom_ms)
+    roof["traffic"] = load_traffic(dominant, cfg.name)
+    kernels = {}
+    for k, ms in breakdown.items():
+        c = costs.get(k, {})
+        e = {"us": round(ms * 1e3, 2)}
+        if "bytes" in c:
+            e["GB/s"] = round(c["bytes"] / (ms * 1e-3) / 1e9, 1)
+        if "products" in c:
+            e["Gproducts/s"] = round(c["products"] / (ms * 1e-3) / 1e9, 1)
+        kernels[k] = e
+    res = {
+        "metric": METRIC, "value": round(samples_s, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "i8*i8->i32" if cfg.dtype == "i8" else "f32",
+        "data": "synthetic (seeded; stands in for the paper's dataset)",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "layers": [s.name for s in cfg.layers]},
+        "dense_equiv_gmac_per_s": round(dense_macs(cfg) / (ms_step * 1e-3) / 1e9, 1),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle")
+        res["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

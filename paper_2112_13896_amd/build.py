@@ -34,6 +34,19 @@ def sources() -> list:
     return [os.path.join(CSRC, "cs_api.hip"), os.path.join(CSRC, "cs_pack.cpp")]
 
 
+def source_digest() -> str:
+    """SHA-256 over every native source and header the library is built from."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                   if f.endswith((".hip", ".cpp", ".h")))
+    files.append(os.path.join(INCLUDE, "cs.h"))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def build(verbose: bool = False, extra: list | None = None) -> str:
     """Compile libcs.so (always recompiles).  Returns its path."""
     tmp = LIB + ".tmp"

@@ -2,17 +2,20 @@
 
 Each layer description needs the attributes kind ("conv"/"linear"), c_in,
 c_out, n, kh, kw, stride, pad, pool, k (or None), shift (or None).  Weights
-are packed once on the host (cs_pack), uploaded, and every buffer the chain
-needs (workspaces, per-layer sums and k-WTA outputs) is allocated up front for
-a fixed batch, so forward() only enqueues kernels.
+are packed once on the host (cs_pack) and uploaded.  Buffers (compaction
+lists, per-layer sums, k-WTA outputs) live in a Buffers object allocated up
+front for a fixed batch; several Buffers can share one Network, so a caller
+can rotate among them.  forward() only enqueues kernels, on torch's current
+stream.
 
-Per layer: compaction + multiply/route/sum (+ bias, + 2x2 max-pool), then
-k-WTA (+ int8 requantisation of the winners in int8 chains).  A conv output
-feeding a linear layer is read as [batch][h*w*c] (NHWC flatten, no copy).
+Per layer: cs_compact (Select's (index, value) lists), cs_mrs_conv2d
+(multiply/route/sum + bias + optional 2x2 max-pool), then cs_kwta (+ int8
+requantisation of the winners in int8 chains).  A conv output feeding a
+linear layer is read as [batch][h*w*c] (NHWC flatten, no copy).
 """
 from __future__ import annotations
 
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 
 import numpy as np
 import torch
@@ -30,6 +33,19 @@ class PackedLayer:
     holes: int
 
 
+@dataclass
+class Buffers:
+    idx: list = field(default_factory=list)    # per layer: [rows][c_in] uint16 (as int16)
+    lval: list = field(default_factory=list)   # per layer: [rows][c_in] list values
+    cnt: list = field(default_factory=list)    # per layer: [rows] int32
+    acc: list = field(default_factory=list)    # per layer: sums after pool
+    out: list = field(default_factory=list)    # per layer: k-WTA / requantised output
+
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for lst in
+                   (self.idx, self.lval, self.cnt, self.acc, self.out) for t in lst)
+
+
 class Network:
     def __init__(self, layers, weights, biases, in_shape, batch: int, device="cuda"):
         self.layers = list(layers)
@@ -43,16 +59,23 @@ class Network:
             bias = None if b is None else torch.from_numpy(np.asarray(b)).to(self.device)
             self.packed.append(PackedLayer(spec, torch.from_numpy(val).to(self.device),
                                            torch.from_numpy(kid).to(self.device), bias, holes))
-        self._plan()
+        self._shapes()
+        self.bufs = self.make_buffers()
+
+    @property
+    def acc(self):
+        return self.bufs.acc
+
+    @property
+    def out(self):
+        return self.bufs.out
 
     # shapes and buffers ----------------------------------------------------
-    def _plan(self):
+    def _shapes(self):
         shape = (self.batch,) + self.in_shape
-        self.in_shapes, self.acc, self.out, self.ws = [], [], [], []
+        self.in_shapes, self.out_shapes, self.list_rows = [], [], []
         for p in self.packed:
             s = p.spec
-            dt = torch.int8 if p.val.dtype == torch.int8 else torch.float32
-            acc_dt = torch.int32 if dt == torch.int8 else torch.float32
             if s.kind == "conv":
                 if len(shape) != 4:
                     raise ValueError(f"{s} needs an NHWC input, got {shape}")
@@ -61,47 +84,120 @@ class Network:
                     raise ValueError("channel mismatch")
                 ho, wo = conv_out(h, s.kh, s.stride, s.pad), conv_out(w, s.kw, s.stride, s.pad)
                 oshape = (b, ho // s.pool, wo // s.pool, s.c_out)
-                ws = ops.workspace(1, dt, b * h * w, c, self.device)
+                rows = b * h * w
             else:
                 b = shape[0]
                 d_in = int(np.prod(shape[1:]))
                 if d_in != s.c_in:
                     raise ValueError("input length mismatch")
                 oshape = (b, s.c_out)
-                ws = ops.workspace(0, dt, b, d_in, self.device)
+                rows = b
             self.in_shapes.append(shape)
-            self.ws.append(ws)
-            acc = torch.empty(oshape, dtype=acc_dt, device=self.device)
-            self.acc.append(acc)
-            if s.k is None:
-                self.out.append(acc)
-            else:
-                odt = torch.int8 if s.shift is not None else acc_dt
-                self.out.append(torch.empty(oshape, dtype=odt, device=self.device))
+            self.out_shapes.append(oshape)
+            self.list_rows.append(rows)
             shape = oshape
         self.out_shape = shape
 
+    def make_buffers(self) -> Buffers:
+        B = Buffers()
+        for p, oshape, rows in zip(self.packed, self.out_shapes, self.list_rows):
+            s = p.spec
+            dt = p.val.dtype
+            acc_dt = torch.int32 if dt == torch.int8 else torch.float32
+            B.idx.append(torch.empty((rows, s.c_in), dtype=torch.int16, device=self.device))
+            B.lval.append(torch.empty((rows, s.c_in), dtype=dt, device=self.device))
+            B.cnt.append(torch.empty((rows,), dtype=torch.int32, device=self.device))
+            acc = torch.empty(oshape, dtype=acc_dt, device=self.device)
+            B.acc.append(acc)
+            if s.k is None:
+                B.out.append(acc)
+            else:
+                odt = torch.int8 if s.shift is not None else acc_dt
+                B.out.append(torch.empty(oshape, dtype=odt, device=self.device))
+        return B
+
     # execution -------------------------------------------------------------
-    def forward_layer(self, li: int, x: torch.Tensor) -> torch.Tensor:
+    def forward_layer(self, li: int, x: torch.Tensor, bufs: Buffers | None = None,
+                      timer=None) -> torch.Tensor:
+        B = self.bufs if bufs is None else bufs
         p = self.packed[li]
         s = p.spec
+        rows = self.list_rows[li]
+        xin = x.reshape(rows, s.c_in)
+        t = timer or _NoTimer()
+        t.start(f"{s.name}.compact")
+        ops.compact_into(xin, B.idx[li], B.lval[li], B.cnt[li])
+        t.stop(f"{s.name}.compact")
         if s.kind == "conv":
-            ops.conv2d(x, p.val, p.kid, s.kh, s.kw, s.n, s.stride, s.pad, p.bias, s.pool,
-                       ws=self.ws[li], out=self.acc[li])
+            geo = self.in_shapes[li]
+            kh, kw, stride, pad, pool = s.kh, s.kw, s.stride, s.pad, s.pool
         else:
-            ops.linear(x.reshape(x.shape[0], -1), p.val, p.kid, s.n, p.bias, ws=self.ws[li],
-                       out=self.acc[li])
+            geo = (rows, 1, 1, s.c_in)
+            kh = kw = stride = pool = 1
+            pad = 0
+        acc = B.acc[li]
+        t.start(f"{s.name}.mrs")
+        ops.mrs_conv2d(B.idx[li], B.lval[li], B.cnt[li], geo, p.val, p.kid, kh, kw, s.n,
+                       stride, pad, p.bias, pool, out=acc.reshape(
+                           (geo[0], (conv_out(geo[1], kh, stride, pad)) // pool,
+                            (conv_out(geo[2], kw, stride, pad)) // pool, s.c_out)))
+        t.stop(f"{s.name}.mrs")
         if s.k is not None:
+            t.start(f"{s.name}.kwta")
             if s.shift is not None:
-                ops.kwta(self.acc[li], s.k, torch.int8, s.shift, out=self.out[li])
+                ops.kwta(acc, s.k, torch.int8, s.shift, out=B.out[li])
             else:
-                ops.kwta(self.acc[li], s.k, out=self.out[li])
-        return self.out[li]
+                ops.kwta(acc, s.k, out=B.out[li])
+            t.stop(f"{s.name}.kwta")
+        return B.out[li]
 
-    def forward(self, x: torch.Tensor) -> torch.Tensor:
+    def forward(self, x: torch.Tensor, bufs: Buffers | None = None, timer=None) -> torch.Tensor:
         if tuple(x.shape) != tuple(self.in_shapes[0]):
             raise ValueError(f"input shape {tuple(x.shape)} != planned {self.in_shapes[0]}")
         cur = x
         for li in range(len(self.packed)):
-            cur = self.forward_layer(li, cur)
+            cur = self.forward_layer(li, cur, bufs, timer)
         return cur
+
+    def kernel_names(self) -> list:
+        names = []
+        for p in self.packed:
+            s = p.spec
+            names += [f"{s.name}.compact", f"{s.name}.mrs"]
+            if s.k is not None:
+                names.append(f"{s.name}.kwta")
+        return names
+
+
+class _NoTimer:
+    def start(self, name):
+        pass
+
+    def stop(self, name):
+        pass
+
+
+class EventTimer:
+    """HIP events around selected launches, recorded on torch's current stream
+    (the stream every launch of this package goes to)."""
+
+    def __init__(self, names=None):
+        self.names = None if names is None else set(names)
+        self.pairs = {}
+        self._open = {}
+
+    def start(self, name):
+        if self.names is None or name in self.names:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            self._open[name] = e
+
+    def stop(self, name):
+        if name in self._open:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            self.pairs.setdefault(name, []).append((self._open.pop(name), e))
+
+    def mean_ms(self) -> dict:
+        torch.cuda.synchronize()
+        return {k: sum(a.elapsed_time(b) for a, b in v) / len(v) for k, v in self.pairs.items()}

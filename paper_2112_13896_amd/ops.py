@@ -83,6 +83,17 @@ def compact(x: torch.Tensor):
     return idx, val, cnt
 
 
+def compact_into(x: torch.Tensor, idx: torch.Tensor, val: torch.Tensor, cnt: torch.Tensor) -> None:
+    """cs_compact into caller-provided buffers (idx int16 [rows][c], val like x, cnt int32)."""
+    rows, c = x.shape
+    if idx.shape != (rows, c) or val.shape != (rows, c) or cnt.shape != (rows,):
+        raise ValueError("buffer shapes do not match x")
+    if idx.dtype != torch.int16 or val.dtype != x.dtype or cnt.dtype != torch.int32:
+        raise TypeError("buffer dtypes do not match")
+    check("cs_compact", lib().cs_compact(_dt(x), _dev(x, "x"), rows, c, _dev(idx, "idx"),
+                                         _dev(val, "val"), _dev(cnt, "cnt"), _stream()))
+
+
 def conv_out(h: int, k: int, stride: int, pad: int) -> int:
     return (h + 2 * pad - k) // stride + 1
 
