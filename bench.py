@@ -62,14 +62,20 @@ def layer_costs(net, bufs, cfg) -> dict:
         s = p.spec
         es = 1 if p.val.dtype == torch.int8 else 4
         rows = net.list_rows[li]
-        cnt = bufs.cnt[li].cpu().numpy().astype(np.int64)
-        nnz = int(cnt.sum())
-        lists = nnz * (2 + es) + rows * 4
-        costs[f"{s.name}.compact"] = {"bytes": rows * s.c_in * es + lists}
         out_elems = int(np.prod(net.out_shapes[li]))
         table = p.val.numel() * (es + 1)
         bias = 0 if p.bias is None else s.c_out * 4
-        mrs_bytes = lists + table + bias + out_elems * 4
+        if getattr(s, "dense_input", False):
+            # sparse-dense: every input element is read and multiplied
+            cnt = np.full(rows, s.c_in, dtype=np.int64)
+            mrs_bytes = rows * s.c_in * es + table + bias + out_elems * 4
+        else:
+            cnt = bufs.cnt[li].cpu().numpy().astype(np.int64)
+            nnz = int(cnt.sum())
+            lists = nnz * (2 + es) + rows * 4
+            costs[f"{s.name}.compact"] = {"bytes": rows * s.c_in * es + lists}
+            mrs_bytes = lists + table + bias + out_elems * 4
+        nnz = int(cnt.sum())
         if s.kind == "conv":
             b, h, w, _ = net.in_shapes[li]
             prods = conv_products(cnt.reshape(b, h, w), s)

@@ -157,6 +157,20 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
               const void* bias, int pool, void* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
+ * Route, Sum with dense activations; Section 4 runs the first layer of the
+ * keyword-spotting network this way because its input is dense).  DEVICE
+ * memory.  Same arguments and result as cs_conv2d, but x is read densely (no
+ * compaction, no workspace).  Supported shapes (else CS_ERR_SHAPE): n == 1
+ * (every set holds one dense kernel), c_out == 64, kh*kw*c_in <= 32 and an
+ * input patch per output item ((pool-1)*stride + kh) * ((pool-1)*stride + kw)
+ * * c_in <= 64 values.
+ */
+int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                    int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
+                    const void* bias, int pool, void* y, void* stream);
+
+/*
  * cs_kwta - k-WTA (Section 2.2.2: exactly the top k activations propagate;
  * Section 3.3.3: global k-WTA over a vector after linear layers, local k-WTA
  * along the channels of each pixel after conv layers - both are this call

@@ -35,6 +35,8 @@ SIGNATURES = {
     "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _vp,
                        _sz, _vp]),
+    "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i,
+                             _vp, _vp]),
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),
     "cs_workspace_bytes": (_sz, [_i, _i, _i64, _i]),
     "cs_status_str": (_c.c_char_p, [_i]),

@@ -9,6 +9,7 @@
 #include "cs.h"
 #include "kwta_kernels.h"
 #include "mrs_kernels.h"
+#include "mrs_tiled.h"
 
 namespace {
 
@@ -86,9 +87,31 @@ int conv_geometry(int b, int h, int w, int c_in, int kh, int kw, int stride, int
   return CS_OK;
 }
 
-int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
-               const cs::ConvGeom& geo, const void* val, const uint8_t* kid, const void* bias,
-               void* y, hipStream_t stream) {
+int device_cus(int* cus) {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CS_ERR_DEVICE;
+  if (dev >= 0 && dev < 64 && cached[dev] > 0) {
+    *cus = cached[dev];
+    return CS_OK;
+  }
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v < 1)
+    return CS_ERR_DEVICE;
+  if (dev >= 0 && dev < 64) cached[dev] = v;
+  *cus = v;
+  return CS_OK;
+}
+
+constexpr size_t kBlockLds = 64 * 1024;   // LDS budget of one workgroup
+constexpr size_t kCuLds = 160 * 1024;     // LDS of one compute unit (gfx950)
+
+// First version: one lane per (output item, set), packed kernels read from
+// global memory.  Used when the lists cannot be read four entries at a time
+// (row stride not a multiple of 4) or a table slice cannot fit in LDS.
+int mrs_launch_simple(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                      const cs::ConvGeom& geo, const void* val, const uint8_t* kid,
+                      const void* bias, void* y, hipStream_t stream) {
   const int64_t opix = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
   const int64_t total = opix * geo.G;
   const bool one = geo.n == 1;
@@ -121,6 +144,80 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
     else
       hipLaunchKernelGGL((cs::mrs_conv<float, float, false>), grid, block, shmem, stream, idx,
                          lv, cnt, pv, kid, bs, yy, geo, total);
+  }
+  return launch_status();
+}
+
+template <typename T, typename A, bool ONE>
+void launch_tiled(dim3 grid, size_t shmem, hipStream_t stream, const uint16_t* idx,
+                  const void* lval, const int32_t* cnt, const void* val, const uint8_t* kid,
+                  const void* bias, void* y, const cs::ConvGeom& geo, const cs::TiledArgs& ta) {
+  hipLaunchKernelGGL((cs::mrs_tiled<T, A, ONE>), grid, dim3(cs::MRS_BD), shmem, stream, idx,
+                     static_cast<const T*>(lval), cnt, static_cast<const T*>(val), kid,
+                     static_cast<const A*>(bias), static_cast<A*>(y), geo, ta);
+}
+
+int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+               const cs::ConvGeom& geo, const void* val, const uint8_t* kid, const void* bias,
+               void* y, hipStream_t stream) {
+  const bool one = geo.n == 1;
+  const int nacc = one ? 1 : geo.n;
+  const int T = geo.KH * geo.KW;
+  const int R = T * geo.C;
+  const size_t esz = xt == CS_I8 ? (one ? 1 : 2) : (one ? 4 : 8);
+  const size_t acc_bytes = (size_t)nacc * cs::MRS_BD * 4;
+  int Gs = 0;
+  if (acc_bytes < kBlockLds) {
+    const size_t fit = (kBlockLds - acc_bytes) / ((size_t)R * esz);
+    Gs = (int)(fit < (size_t)geo.G ? fit : (size_t)geo.G);
+  }
+  cs::TiledArgs ta;
+  ta.chunk_mode = T == 1 ? 1 : 0;
+  ta.log2Q = geo.pool == 2 ? 2 : 0;
+  // tap mode: each lane walks at most MRS_TAPS taps
+  int log2S = 0;
+  if (!ta.chunk_mode)
+    while (((T + (1 << log2S) - 1) >> log2S) > cs::MRS_TAPS) ++log2S;
+  if (geo.cap % 4 != 0 || Gs < 1 || log2S + ta.log2Q > 6)
+    return mrs_launch_simple(xt, idx, lval, cnt, geo, val, kid, bias, y, stream);
+  int cus = 0;
+  const int st = device_cus(&cus);
+  if (st != CS_OK) return st;
+  ta.gslices = (geo.G + Gs - 1) / Gs;
+  ta.Gs = (geo.G + ta.gslices - 1) / ta.gslices;        // even split over the slices
+  ta.items = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
+  const size_t shmem = acc_bytes + (size_t)R * ta.Gs * esz;
+  int bpc = (int)(kCuLds / shmem);
+  bpc = bpc < 1 ? 1 : (bpc > 4 ? 4 : bpc);              // 4 x 512 threads fill a compute unit
+  const int64_t grid_lanes = (int64_t)cus * bpc * cs::MRS_BD;
+  // more slices while the grid is not covered twice: up to one slice per tap
+  // (tap mode) or per 64 list slots (chunk mode), and 64 lanes per group
+  const int64_t max_s = ta.chunk_mode ? (geo.C >= 128 ? geo.C / 64 : 1) : T;
+  while (log2S + ta.log2Q < 6 && (2LL << log2S) <= max_s &&
+         ta.items * geo.G * ((int64_t)1 << (log2S + ta.log2Q)) < 2 * grid_lanes)
+    ++log2S;
+  ta.log2S = log2S;
+  ta.S = 1 << log2S;
+  const int64_t lanes_per_slice = ta.items * ta.Gs * ((int64_t)1 << (log2S + ta.log2Q));
+  int64_t blocks_per_slice = (lanes_per_slice + cs::MRS_BD - 1) / cs::MRS_BD;
+  const int64_t cap_blocks = ((int64_t)cus * bpc + ta.gslices - 1) / ta.gslices;
+  if (blocks_per_slice > cap_blocks) blocks_per_slice = cap_blocks;
+  if (blocks_per_slice < 1) blocks_per_slice = 1;
+  const dim3 grid((unsigned)(blocks_per_slice * ta.gslices));
+  if (xt == CS_I8) {
+    if (one)
+      launch_tiled<int8_t, int32_t, true>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
+                                          geo, ta);
+    else
+      launch_tiled<int8_t, int32_t, false>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
+                                           geo, ta);
+  } else {
+    if (one)
+      launch_tiled<float, float, true>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo,
+                                       ta);
+    else
+      launch_tiled<float, float, false>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
+                                        geo, ta);
   }
   return launch_status();
 }
@@ -222,6 +319,52 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
   int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
   if (r != CS_OK) return r;
   return mrs_launch(xt, idx, lv, cnt, geo, val, kid, bias, y, s);
+}
+
+int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                    int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
+                    const void* bias, int pool, void* y, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !val || !kid || !y) return CS_ERR_ARG;
+  const int R = kh * kw * c_in;
+  const int ph = (pool - 1) * stride + kh, pw = (pool - 1) * stride + kw;
+  if (n != 1 || c_out != 64 || R > 32 || (int64_t)ph * pw * c_in > 64) return CS_ERR_SHAPE;
+  const int64_t items = (int64_t)b * (geo.Ho / pool) * (geo.Wo / pool);
+  int cus = 0;
+  const int dst = device_cus(&cus);
+  if (dst != CS_OK) return dst;
+  const int64_t nb64 = (items + 3) / 4;                    // 4 wavefronts per block
+  const int64_t cap = (int64_t)cus * 8;                    // persistent: 32 wavefronts per CU
+  const int nb = (int)(nb64 < cap ? nb64 : cap);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool gsc = kh == 5 && kw == 5 && c_in == 1 && stride == 1 && pool == 2;
+  if (xt == CS_I8) {
+    auto* xx = static_cast<const int8_t*>(x);
+    auto* pv = static_cast<const int8_t*>(val);
+    auto* bs = static_cast<const int32_t*>(bias);
+    auto* yy = static_cast<int32_t*>(y);
+    if (gsc)
+      hipLaunchKernelGGL((cs::conv_dense_n1<int8_t, int32_t, 5, 5, 1, 1, 2>), dim3(nb), dim3(256),
+                         0, s, xx, pv, bs, yy, geo, items);
+    else
+      hipLaunchKernelGGL((cs::conv_dense_n1_rt<int8_t, int32_t>), dim3(nb), dim3(256), 0, s, xx,
+                         pv, bs, yy, geo, items);
+  } else {
+    auto* xx = static_cast<const float*>(x);
+    auto* pv = static_cast<const float*>(val);
+    auto* bs = static_cast<const float*>(bias);
+    auto* yy = static_cast<float*>(y);
+    if (gsc)
+      hipLaunchKernelGGL((cs::conv_dense_n1<float, float, 5, 5, 1, 1, 2>), dim3(nb), dim3(256), 0,
+                         s, xx, pv, bs, yy, geo, items);
+    else
+      hipLaunchKernelGGL((cs::conv_dense_n1_rt<float, float>), dim3(nb), dim3(256), 0, s, xx, pv,
+                         bs, yy, geo, items);
+  }
+  return launch_status();
 }
 
 int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, const uint8_t* kid,

@@ -104,9 +104,10 @@ class Network:
             s = p.spec
             dt = p.val.dtype
             acc_dt = torch.int32 if dt == torch.int8 else torch.float32
-            B.idx.append(torch.empty((rows, s.c_in), dtype=torch.int16, device=self.device))
-            B.lval.append(torch.empty((rows, s.c_in), dtype=dt, device=self.device))
-            B.cnt.append(torch.empty((rows,), dtype=torch.int32, device=self.device))
+            lr = 0 if getattr(s, "dense_input", False) else rows
+            B.idx.append(torch.empty((lr, s.c_in), dtype=torch.int16, device=self.device))
+            B.lval.append(torch.empty((lr, s.c_in), dtype=dt, device=self.device))
+            B.cnt.append(torch.empty((lr,), dtype=torch.int32, device=self.device))
             acc = torch.empty(oshape, dtype=acc_dt, device=self.device)
             B.acc.append(acc)
             if s.k is None:
@@ -123,8 +124,15 @@ class Network:
         p = self.packed[li]
         s = p.spec
         rows = self.list_rows[li]
-        xin = x.reshape(rows, s.c_in)
         t = timer or _NoTimer()
+        if getattr(s, "dense_input", False):
+            # sparse-dense variant: dense activations, no compaction
+            t.start(f"{s.name}.mrs")
+            ops.conv2d_dense(x, p.val, p.kid, s.kh, s.kw, s.n, s.stride, s.pad, p.bias, s.pool,
+                             out=B.acc[li])
+            t.stop(f"{s.name}.mrs")
+            return self._select(li, s, B, t)
+        xin = x.reshape(rows, s.c_in)
         t.start(f"{s.name}.compact")
         ops.compact_into(xin, B.idx[li], B.lval[li], B.cnt[li])
         t.stop(f"{s.name}.compact")
@@ -142,6 +150,10 @@ class Network:
                            (geo[0], (conv_out(geo[1], kh, stride, pad)) // pool,
                             (conv_out(geo[2], kw, stride, pad)) // pool, s.c_out)))
         t.stop(f"{s.name}.mrs")
+        return self._select(li, s, B, t)
+
+    def _select(self, li, s, B, t):
+        acc = B.acc[li]
         if s.k is not None:
             t.start(f"{s.name}.kwta")
             if s.shift is not None:
@@ -163,7 +175,9 @@ class Network:
         names = []
         for p in self.packed:
             s = p.spec
-            names += [f"{s.name}.compact", f"{s.name}.mrs"]
+            if not getattr(s, "dense_input", False):
+                names.append(f"{s.name}.compact")
+            names.append(f"{s.name}.mrs")
             if s.k is not None:
                 names.append(f"{s.name}.kwta")
         return names

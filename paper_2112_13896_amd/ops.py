@@ -148,6 +148,26 @@ def conv2d(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: i
     return out
 
 
+def conv2d_dense(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: int, n: int,
+                 stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
+                 out: torch.Tensor | None = None) -> torch.Tensor:
+    """Sparse-dense conv (dense NHWC input, no compaction); see cs_conv2d_dense for the
+    supported shapes."""
+    if x.dim() != 4:
+        raise ValueError("x must be NHWC")
+    b, h, w, c_in = x.shape
+    c_out = val.shape[1] * n
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
+    if out is None:
+        out = torch.empty((b, max(ho, 0) // pool, max(wo, 0) // pool, c_out), dtype=ydt,
+                          device=x.device)
+    check("cs_conv2d_dense", lib().cs_conv2d_dense(
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"),
+        _dev(kid, "kid"), c_out, n, _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
+    return out
+
+
 def linear(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, n: int,
            bias: torch.Tensor | None = None, ws: torch.Tensor | None = None,
            out: torch.Tensor | None = None) -> torch.Tensor:

@@ -136,6 +136,24 @@ def test_conv2d_validation(L):
     assert f(*conv_args(ws=FAKE_WS + 8)) == CS_ERR_WORKSPACE   # misaligned
 
 
+def test_conv2d_dense_validation(L):
+    f = L.cs_conv2d_dense
+    ok = dict(xt=CS_I8, x=FAKE, b=2, h=32, w=32, c_in=1, kh=5, kw=5, stride=1, pad=0, val=FAKE,
+              kid=FAKE, c_out=64, n=1, bias=None, pool=2, y=FAKE, stream=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(*a.values())
+    assert call(xt=CS_I32) == CS_ERR_DTYPE
+    assert call(n=2) == CS_ERR_SHAPE              # only dense kernels (n == 1)
+    assert call(c_out=32) == CS_ERR_SHAPE         # one wavefront of 64 channels
+    assert call(c_in=2) == CS_ERR_SHAPE           # 50 weights per channel > 32
+    assert call(kh=7, kw=7) == CS_ERR_SHAPE
+    assert call(x=None) == CS_ERR_ARG
+    assert call(pool=2, h=33, w=33) == CS_ERR_SHAPE
+
+
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, FAKE, 8, 4, None, 1, FAKE, None]

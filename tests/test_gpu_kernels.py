@@ -114,6 +114,7 @@ LINEAR_CASES = [
     (9, 64, 64, 32, 64),       # dense input rows
     (4, 33, 6, 3, 0),          # all-zero input: output = bias
     (130, 256, 256, 16, 26),
+    (2, 8192, 16, 2, 300),     # packed table too large for one workgroup's LDS
 ]
 
 
@@ -188,6 +189,44 @@ def test_conv2d(case, dtype):
         if pool == 2:
             S = pool_S(S)
         assert_f32_close(y, ref, S, f"conv {case}")
+
+
+DENSE_CASES = [
+    # b, h, w, c_in, kh, kw, stride, pad, pool
+    (3, 32, 32, 1, 5, 5, 1, 0, 2),
+    (2, 9, 11, 3, 3, 3, 1, 1, 1),
+    (2, 12, 12, 2, 3, 3, 2, 1, 2),
+    (1, 7, 6, 8, 2, 2, 1, 0, 1),
+]
+
+
+@pytest.mark.parametrize("case", DENSE_CASES)
+@pytest.mark.parametrize("dtype", ["i8", "f32"])
+def test_conv2d_dense(case, dtype):
+    """Sparse-dense variant (dense input, dense kernels) against the oracle."""
+    b, h, w, c_in, kh, kw, stride, pad, pool = case
+    r = rng(sum(case) + (dtype == "f32"))
+    R = kh * kw * c_in
+    W = complementary_weights(r, r, 64, R, 1, "int8" if dtype == "i8" else "normal")
+    W = W.reshape(64, kh, kw, c_in)
+    x = sparse_rows(r, b * h * w, c_in, None,
+                    "u_m127_127" if dtype == "i8" else "absnormal").reshape(b, h, w, c_in)
+    bias = (r.integers(-1000, 1001, size=64).astype(np.int32) if dtype == "i8"
+            else r.normal(size=64).astype(np.float32)) if b != 2 else None
+    val, kid, _ = ops.pack(W.reshape(64, -1), 1)
+    y = host(ops.conv2d_dense(dev(x), dev(val), dev(kid), kh, kw, 1, stride, pad,
+                              None if bias is None else dev(bias), pool))
+    ref = o.conv2d_nhwc(x, W, stride, pad, bias)
+    if pool == 2:
+        ref = o.maxpool2x2_nhwc(ref)
+    assert y.shape == ref.shape
+    if dtype == "i8":
+        assert np.array_equal(y.astype(np.int64), ref)
+    else:
+        S = o.abs_sum_conv(x, W, stride, pad) + (0 if bias is None else np.abs(bias.astype(np.float64)))
+        if pool == 2:
+            S = pool_S(S)
+        assert_f32_close(y, ref, S, f"dense conv {case}")
 
 
 def test_mrs_on_compacted_lists_matches_conv2d():

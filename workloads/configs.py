@@ -36,6 +36,7 @@ class LayerSpec:
     shift: int | None = None  # int chains: requantise winners with this shift
     bias: bool = False
     weight_dist: str = "int8"  # "int8": uniform non-zero in [-127,127]; "normal": N(0, 2/nnz_k)
+    dense_input: bool = False  # the layer's input is dense: run it sparse-dense (no compaction)
 
     @property
     def r(self) -> int:
@@ -87,7 +88,8 @@ CONFIGS = {
         cid=2, name="gsc_cnn_i8_b256", dtype="i8", batch=256, in_shape=(32, 32, 1),
         in_nnz=None, in_dist="u_m127_127",
         layers=(
-            LayerSpec("conv1", "conv", 1, 64, n=1, kh=5, kw=5, pool=2, k=8, shift=_C2_S1),
+            LayerSpec("conv1", "conv", 1, 64, n=1, kh=5, kw=5, pool=2, k=8, shift=_C2_S1,
+                      dense_input=True),
             LayerSpec("conv2", "conv", 64, 64, n=16, kh=5, kw=5, pool=2, k=8, shift=_C2_S2),
             LayerSpec("linear1", "linear", 1600, 1500, n=20, k=75, shift=_C2_S3),
             LayerSpec("output", "linear", 1500, 12, n=1),
