@@ -13,6 +13,8 @@
 
 namespace cs {
 
+constexpr int COMPACT_BATCH = 8;   // 64-element chunks of a row in flight together
+
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
@@ -37,17 +39,26 @@ __global__ __launch_bounds__(256) void compact_wide(const T* __restrict__ x, int
     uint16_t* ir = idx + row * c;
     T* vr = val + row * c;
     int run = 0;
-    for (int base = 0; base < c; base += 64) {
-      const int j = base + lane;
-      const T v = j < c ? xr[j] : T(0);
-      const bool nz = j < c && is_nonzero(v);
-      const uint64_t m = __ballot(nz);
-      if (nz) {
-        const int pos = run + __popcll(m & below);
-        ir[pos] = (uint16_t)j;
-        vr[pos] = v;
+    // COMPACT_BATCH chunks of 64 are loaded before any is used
+    for (int b0 = 0; b0 < c; b0 += 64 * COMPACT_BATCH) {
+      T v[COMPACT_BATCH];
+#pragma unroll
+      for (int u = 0; u < COMPACT_BATCH; ++u) {
+        const int j = b0 + u * 64 + lane;
+        v[u] = j < c ? xr[j] : T(0);
       }
-      run += __popcll(m);
+#pragma unroll
+      for (int u = 0; u < COMPACT_BATCH; ++u) {
+        const int j = b0 + u * 64 + lane;
+        const bool nz = j < c && is_nonzero(v[u]);
+        const uint64_t m = __ballot(nz);
+        if (nz) {
+          const int pos = run + __popcll(m & below);
+          ir[pos] = (uint16_t)j;
+          vr[pos] = v[u];
+        }
+        run += __popcll(m);
+      }
     }
     if (lane == 0) cnt[row] = run;
   }

@@ -148,13 +148,44 @@ int mrs_launch_simple(cs_dtype xt, const uint16_t* idx, const void* lval, const 
   return launch_status();
 }
 
-template <typename T, typename A, bool ONE>
+template <typename T, typename A, bool ONE, int GB>
 void launch_tiled(dim3 grid, size_t shmem, hipStream_t stream, const uint16_t* idx,
                   const void* lval, const int32_t* cnt, const void* val, const uint8_t* kid,
                   const void* bias, void* y, const cs::ConvGeom& geo, const cs::TiledArgs& ta) {
-  hipLaunchKernelGGL((cs::mrs_tiled<T, A, ONE>), grid, dim3(cs::MRS_BD), shmem, stream, idx,
+  hipLaunchKernelGGL((cs::mrs_tiled<T, A, ONE, GB>), grid, dim3(cs::MRS_BD), shmem, stream, idx,
                      static_cast<const T*>(lval), cnt, static_cast<const T*>(val), kid,
                      static_cast<const A*>(bias), static_cast<A*>(y), geo, ta);
+}
+
+template <typename T, typename A>
+void launch_tiled_any(bool one, int gb, dim3 grid, size_t shmem, hipStream_t stream,
+                      const uint16_t* idx, const void* lval, const int32_t* cnt, const void* val,
+                      const uint8_t* kid, const void* bias, void* y, const cs::ConvGeom& geo,
+                      const cs::TiledArgs& ta) {
+  if (one) {
+    if (gb == 2)
+      launch_tiled<T, A, true, 2>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+    else
+      launch_tiled<T, A, true, 1>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+  } else {
+    if (gb == 2)
+      launch_tiled<T, A, false, 2>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+    else
+      launch_tiled<T, A, false, 1>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+  }
+}
+
+// Sets per table slice: the largest divisor of G that is a multiple of gb and
+// whose table fits the workgroup's LDS next to the accumulators; 0 if none.
+int table_slice(const cs::ConvGeom& geo, size_t esz, int nacc, int gb) {
+  const size_t acc_bytes = (size_t)gb * nacc * cs::MRS_BD * 4;
+  if (acc_bytes >= kBlockLds) return 0;
+  const size_t R = (size_t)geo.KH * geo.KW * geo.C;
+  for (int gs = geo.G; gs >= gb; --gs)                 // table + bias of the slice
+    if (geo.G % gs == 0 && gs % gb == 0 &&
+        acc_bytes + R * esz * gs + (size_t)gs * nacc * 4 + 16 <= kBlockLds)
+      return gs;
+  return 0;
 }
 
 int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
@@ -163,13 +194,14 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   const bool one = geo.n == 1;
   const int nacc = one ? 1 : geo.n;
   const int T = geo.KH * geo.KW;
-  const int R = T * geo.C;
+  const int64_t R = (int64_t)T * geo.C;
   const size_t esz = xt == CS_I8 ? (one ? 1 : 2) : (one ? 4 : 8);
-  const size_t acc_bytes = (size_t)nacc * cs::MRS_BD * 4;
-  int Gs = 0;
-  if (acc_bytes < kBlockLds) {
-    const size_t fit = (kBlockLds - acc_bytes) / ((size_t)R * esz);
-    Gs = (int)(fit < (size_t)geo.G ? fit : (size_t)geo.G);
+  // two sets per lane when they split evenly and fit; else one
+  int gb = 2;
+  int Gs = geo.G % 2 == 0 ? table_slice(geo, esz, nacc, 2) : 0;
+  if (Gs < 2) {
+    gb = 1;
+    Gs = table_slice(geo, esz, nacc, 1);
   }
   cs::TiledArgs ta;
   ta.chunk_mode = T == 1 ? 1 : 0;
@@ -178,47 +210,50 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   int log2S = 0;
   if (!ta.chunk_mode)
     while (((T + (1 << log2S) - 1) >> log2S) > cs::MRS_TAPS) ++log2S;
-  if (geo.cap % 4 != 0 || Gs < 1 || log2S + ta.log2Q > 6)
+  const int64_t items = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
+  const int64_t in_rows = (int64_t)geo.B * geo.H * geo.W;
+  // 32-bit offsets inside the kernel: element offsets and lane counts below 2^31
+  const bool fits32 = in_rows * geo.cap < INT32_MAX && items * geo.c_out < INT32_MAX &&
+                      R * geo.G < INT32_MAX && items * geo.G * 64 < INT32_MAX;
+  if (geo.cap % 4 != 0 || Gs < 1 || log2S + ta.log2Q > 6 || !fits32)
     return mrs_launch_simple(xt, idx, lval, cnt, geo, val, kid, bias, y, stream);
   int cus = 0;
   const int st = device_cus(&cus);
   if (st != CS_OK) return st;
-  ta.gslices = (geo.G + Gs - 1) / Gs;
-  ta.Gs = (geo.G + ta.gslices - 1) / ta.gslices;        // even split over the slices
-  ta.items = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
-  const size_t shmem = acc_bytes + (size_t)R * ta.Gs * esz;
+  ta.Gs = Gs;
+  ta.gslices = geo.G / Gs;
+  ta.items = (int)items;
+  ta.fd_gs = cs::make_fastdiv((uint32_t)Gs);
+  ta.fd_units = cs::make_fastdiv((uint32_t)(Gs / gb));
+  ta.fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / geo.pool));
+  ta.fd_hp = cs::make_fastdiv((uint32_t)(geo.Ho / geo.pool));
+  ta.fd_kw = cs::make_fastdiv((uint32_t)geo.KW);
+  const size_t tab_bytes = ((size_t)R * Gs * esz + 15) / 16 * 16;
+  const size_t shmem = (size_t)gb * nacc * cs::MRS_BD * 4 + tab_bytes + (size_t)Gs * nacc * 4;
   int bpc = (int)(kCuLds / shmem);
-  bpc = bpc < 1 ? 1 : (bpc > 4 ? 4 : bpc);              // 4 x 512 threads fill a compute unit
+  bpc = bpc < 1 ? 1 : (bpc > 8 ? 8 : bpc);              // 8 x 256 threads fill a compute unit
   const int64_t grid_lanes = (int64_t)cus * bpc * cs::MRS_BD;
+  const int64_t units = items * (geo.G / gb);
   // more slices while the grid is not covered twice: up to one slice per tap
   // (tap mode) or per 64 list slots (chunk mode), and 64 lanes per group
   const int64_t max_s = ta.chunk_mode ? (geo.C >= 128 ? geo.C / 64 : 1) : T;
   while (log2S + ta.log2Q < 6 && (2LL << log2S) <= max_s &&
-         ta.items * geo.G * ((int64_t)1 << (log2S + ta.log2Q)) < 2 * grid_lanes)
+         units * ((int64_t)1 << (log2S + ta.log2Q)) < 2 * grid_lanes)
     ++log2S;
   ta.log2S = log2S;
   ta.S = 1 << log2S;
-  const int64_t lanes_per_slice = ta.items * ta.Gs * ((int64_t)1 << (log2S + ta.log2Q));
+  const int64_t lanes_per_slice = items * (Gs / gb) * ((int64_t)1 << (log2S + ta.log2Q));
   int64_t blocks_per_slice = (lanes_per_slice + cs::MRS_BD - 1) / cs::MRS_BD;
   const int64_t cap_blocks = ((int64_t)cus * bpc + ta.gslices - 1) / ta.gslices;
   if (blocks_per_slice > cap_blocks) blocks_per_slice = cap_blocks;
   if (blocks_per_slice < 1) blocks_per_slice = 1;
   const dim3 grid((unsigned)(blocks_per_slice * ta.gslices));
-  if (xt == CS_I8) {
-    if (one)
-      launch_tiled<int8_t, int32_t, true>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
-                                          geo, ta);
-    else
-      launch_tiled<int8_t, int32_t, false>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
-                                           geo, ta);
-  } else {
-    if (one)
-      launch_tiled<float, float, true>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo,
-                                       ta);
-    else
-      launch_tiled<float, float, false>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y,
-                                        geo, ta);
-  }
+  if (xt == CS_I8)
+    launch_tiled_any<int8_t, int32_t>(one, gb, grid, shmem, stream, idx, lval, cnt, val, kid,
+                                      bias, y, geo, ta);
+  else
+    launch_tiled_any<float, float>(one, gb, grid, shmem, stream, idx, lval, cnt, val, kid, bias,
+                                   y, geo, ta);
   return launch_status();
 }
 
@@ -244,15 +279,16 @@ int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
     if (nb > INT32_MAX) return CS_ERR_SHAPE;
     const size_t shmem = (size_t)cs::KWTA_LANE_ROWS * (c + 1) * 4;
     const dim3 grid((unsigned)nb), block(cs::KWTA_LANE_ROWS);
+    const cs::FastDiv fd_c = cs::make_fastdiv((uint32_t)c);
     if (k <= 8)
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 8>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift);
+                         out, shift, fd_c);
     else if (k <= 16)
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 16>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift);
+                         out, shift, fd_c);
     else
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 32>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift);
+                         out, shift, fd_c);
     return launch_status();
   }
   const int m = (c + 63) / 64;
@@ -332,11 +368,15 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
   const int R = kh * kw * c_in;
   const int ph = (pool - 1) * stride + kh, pw = (pool - 1) * stride + kw;
   if (n != 1 || c_out != 64 || R > 32 || (int64_t)ph * pw * c_in > 64) return CS_ERR_SHAPE;
-  const int64_t items = (int64_t)b * (geo.Ho / pool) * (geo.Wo / pool);
+  const int64_t items64 = (int64_t)b * (geo.Ho / pool) * (geo.Wo / pool);
+  if (items64 * 64 >= INT32_MAX || (int64_t)b * h * w * c_in >= INT32_MAX) return CS_ERR_SHAPE;
+  const int items = (int)items64;
+  const cs::FastDiv fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / pool));
+  const cs::FastDiv fd_hp = cs::make_fastdiv((uint32_t)(geo.Ho / pool));
   int cus = 0;
   const int dst = device_cus(&cus);
   if (dst != CS_OK) return dst;
-  const int64_t nb64 = (items + 3) / 4;                    // 4 wavefronts per block
+  const int64_t nb64 = (items64 + 3) / 4;                  // 4 wavefronts per block
   const int64_t cap = (int64_t)cus * 8;                    // persistent: 32 wavefronts per CU
   const int nb = (int)(nb64 < cap ? nb64 : cap);
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -348,10 +388,10 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
     auto* yy = static_cast<int32_t*>(y);
     if (gsc)
       hipLaunchKernelGGL((cs::conv_dense_n1<int8_t, int32_t, 5, 5, 1, 1, 2>), dim3(nb), dim3(256),
-                         0, s, xx, pv, bs, yy, geo, items);
+                         0, s, xx, pv, bs, yy, geo, items, fd_wp, fd_hp);
     else
       hipLaunchKernelGGL((cs::conv_dense_n1_rt<int8_t, int32_t>), dim3(nb), dim3(256), 0, s, xx,
-                         pv, bs, yy, geo, items);
+                         pv, bs, yy, geo, items, fd_wp, fd_hp);
   } else {
     auto* xx = static_cast<const float*>(x);
     auto* pv = static_cast<const float*>(val);
@@ -359,10 +399,10 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
     auto* yy = static_cast<float*>(y);
     if (gsc)
       hipLaunchKernelGGL((cs::conv_dense_n1<float, float, 5, 5, 1, 1, 2>), dim3(nb), dim3(256), 0,
-                         s, xx, pv, bs, yy, geo, items);
+                         s, xx, pv, bs, yy, geo, items, fd_wp, fd_hp);
     else
       hipLaunchKernelGGL((cs::conv_dense_n1_rt<float, float>), dim3(nb), dim3(256), 0, s, xx, pv,
-                         bs, yy, geo, items);
+                         bs, yy, geo, items, fd_wp, fd_hp);
   }
   return launch_status();
 }

@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fastdiv.h"
+
 namespace cs {
 
 __device__ __forceinline__ uint32_t order_key(int32_t v) { return (uint32_t)v ^ 0x80000000u; }
@@ -48,12 +50,14 @@ __device__ __forceinline__ int8_t kwta_out<int32_t, int8_t>(int32_t v, int shift
 }
 
 constexpr int KWTA_LANE_ROWS = 128;   // rows (threads) per block of kwta_lane
+constexpr int KWTA_BATCH = 16;        // tile elements a thread loads per batch
 
 // LDS tile: KWTA_LANE_ROWS rows of c 32-bit words, stride c + 1.
 template <typename TI, typename TO, int KMAX>
 __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict__ in,
                                                             int64_t rows, int c, int k,
-                                                            TO* __restrict__ out, int shift) {
+                                                            TO* __restrict__ out, int shift,
+                                                            FastDiv fd_c) {
   extern __shared__ __align__(16) unsigned char smem[];
   TI* tile = reinterpret_cast<TI*>(smem);
   const int stride = c + 1;
@@ -63,7 +67,22 @@ __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict
   const int nrows = (int)nrows64;
   const int nelem = nrows * c;
   const TI* src = in + row0 * c;
-  for (int e = tid; e < nelem; e += KWTA_LANE_ROWS) tile[(e / c) * stride + (e % c)] = src[e];
+  for (int b0 = 0; b0 < nelem; b0 += KWTA_LANE_ROWS * KWTA_BATCH) {   // loads in flight together
+    TI v[KWTA_BATCH];
+#pragma unroll
+    for (int u = 0; u < KWTA_BATCH; ++u) {
+      const int e = b0 + u * KWTA_LANE_ROWS + tid;
+      v[u] = e < nelem ? src[e] : TI(0);
+    }
+#pragma unroll
+    for (int u = 0; u < KWTA_BATCH; ++u) {
+      const int e = b0 + u * KWTA_LANE_ROWS + tid;
+      if (e < nelem) {
+        const int rr = (int)fdiv((uint32_t)e, fd_c);
+        tile[rr * stride + (e - rr * c)] = v[u];
+      }
+    }
+  }
   __syncthreads();
 
   uint32_t thr = 0;
@@ -114,7 +133,10 @@ __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict
   }
   __syncthreads();
   TO* dst = out + row0 * c;
-  for (int e = tid; e < nelem; e += KWTA_LANE_ROWS) dst[e] = otile[(e / c) * ostride + (e % c)];
+  for (int e = tid; e < nelem; e += KWTA_LANE_ROWS) {
+    const int rr = (int)fdiv((uint32_t)e, fd_c);
+    dst[e] = otile[rr * ostride + (e - rr * c)];
+  }
 }
 
 constexpr int KWTA_WAVE_WAVES = 4;   // wavefronts (rows) per block of kwta_wave

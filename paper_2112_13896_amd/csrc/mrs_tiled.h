@@ -25,13 +25,16 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fastdiv.h"
 #include "mrs_kernels.h"
 
 namespace cs {
 
-constexpr int MRS_BD = 512;     // threads per workgroup
+constexpr int MRS_BD = 256;     // threads per workgroup
 constexpr int MRS_TAPS = 9;     // most taps one lane walks (host picks S accordingly)
 constexpr int MRS_AHEAD = 2;    // taps prefetched ahead of the one being processed
+constexpr int MRS_STAGE = 16;   // table entries a lane loads per batch while staging
+constexpr int MRS_CHUNKS = 4;   // list chunks loaded together in single-tap layers
 
 template <typename T, bool ONE>
 struct TabEntry;
@@ -47,10 +50,15 @@ struct TabEntry<float, true> { using type = float; };
 struct TiledArgs {
   int S, log2S;      // slices per (item, set, sub-pixel), power of two
   int log2Q;         // sub-pixels on separate lanes: 0 (none) or 2 (2x2 pool)
-  int Gs;            // sets per table slice
+  int Gs;            // sets per table slice (divides G, multiple of the sets per lane)
   int gslices;       // number of table slices; gridDim.x is a multiple of it
   int chunk_mode;    // 1: a single tap, slices split its list chunks
-  int64_t items;     // output items (pooled pixels when pooling)
+  int items;         // output items (pooled pixels when pooling)
+  FastDiv fd_gs;     // / Gs
+  FastDiv fd_units;  // / (Gs / sets per lane)
+  FastDiv fd_wp;     // / pooled output width
+  FastDiv fd_hp;     // / pooled output height
+  FastDiv fd_kw;     // / kernel width
 };
 
 template <typename T>
@@ -88,30 +96,60 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <typename T, typename A, bool ONE>
-__device__ __forceinline__ void mrs_chunk(const Chunk<T>& ch, int lim, int sbase,
-                                          const typename TabEntry<T, ONE>::type* trow,
-                                          int gcount, A* acc_lane, A& accr) {
-  using E = typename TabEntry<T, ONE>::type;
+// Entries of the staged table a lane reads at once: GB consecutive sets.
+template <typename T, bool ONE, int GB>
+struct __attribute__((aligned(GB * sizeof(typename TabEntry<T, ONE>::type)))) TabVec {
+  typename TabEntry<T, ONE>::type e[GB];
+};
+
+// One 4-entry chunk of a list against the lane's GB sets.  All table reads of
+// the chunk are issued before any is used; tail entries beyond the list
+// (e >= lim) read row 0 and contribute a zero product, so there is no branch.
+template <typename T, typename A, bool ONE, int GB>
+__device__ __forceinline__ void mrs_chunk(const Chunk<T>& ch, int lim,
+                                          const unsigned char* tbase, uint32_t row_bytes,
+                                          A* acc_lane, A (&accr)[GB]) {
+  using V = TabVec<T, ONE, GB>;
+  V tv[4];
+  A xv[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    if (e < lim) {
-      const E te = trow[(sbase + chunk_idx(ch.idx, e)) * gcount];     // Multiply: packed row
-      if constexpr (ONE) {
-        accr += (A)ch.v(e) * (A)te;                                      // Sum
-      } else if constexpr (sizeof(T) == 1) {
-        __hip_atomic_fetch_add(acc_lane + (int)(te >> 8) * MRS_BD,       // Route + Sum
-                               ch.v(e) * (int32_t)(int8_t)(te & 0xFFu), __ATOMIC_RELAXED,
+    const bool ok = e < lim;
+    const uint32_t c = ok ? (uint32_t)chunk_idx(ch.idx, e) : 0u;
+    tv[e] = *reinterpret_cast<const V*>(tbase + __umul24(c, row_bytes));   // Multiply: row c
+    xv[e] = ok ? (A)ch.v(e) : A(0);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if constexpr (ONE) {
+#pragma unroll
+      for (int j = 0; j < GB; ++j) accr[j] += xv[e] * (A)tv[e].e[j];      // Sum
+    } else if constexpr (sizeof(T) == 1) {
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        // Route + Sum: the entry's high byte is the accumulator (set j, kernel id)
+        const auto te = tv[e].e[j];
+        __hip_atomic_fetch_add(acc_lane + (int)(te >> 8) * MRS_BD,
+                               xv[e] * (int32_t)(int8_t)(te & 0xFFu), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_WORKGROUP);
-      } else {
-        A* p = reinterpret_cast<A*>(reinterpret_cast<unsigned char*>(acc_lane) + te.y);
-        *p = *p + ch.v(e) * __uint_as_float(te.x);                       // Route + Sum
       }
+    } else {
+      // Route + Sum: the GB sets' accumulators are disjoint, so all GB reads
+      // are issued before the writes
+      A* p[GB];
+      A a[GB];
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        p[j] = reinterpret_cast<A*>(reinterpret_cast<unsigned char*>(acc_lane) + tv[e].e[j].y);
+        a[j] = *p[j];
+      }
+#pragma unroll
+      for (int j = 0; j < GB; ++j) *p[j] = a[j] + xv[e] * __uint_as_float(tv[e].e[j].x);
     }
   }
 }
 
-template <typename T, typename A, bool ONE>
+template <typename T, typename A, bool ONE, int GB>
 __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__ lidx,
                                                     const T* __restrict__ lval,
                                                     const int32_t* __restrict__ lcnt,
@@ -130,36 +168,62 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
   const int gsl = blockIdx.x % ta.gslices;
   const int bis = blockIdx.x / ta.gslices;              // block index within the set slice
   const int nbs = gridDim.x / ta.gslices;               // blocks per set slice
-  const int g0 = gsl * ta.Gs;
-  const int gcount = min(ta.Gs, G - g0);
+  const int gcount = ta.Gs;
+  const int g0 = gsl * gcount;
+  const int gunits = gcount / GB;
 
-  A* acc = reinterpret_cast<A*>(smem);                  // [n][MRS_BD]
-  E* tab = reinterpret_cast<E*>(smem + (size_t)n * MRS_BD * sizeof(A));
+  A* acc = reinterpret_cast<A*>(smem);                  // [GB * n][MRS_BD]
+  unsigned char* tab = smem + (size_t)GB * n * MRS_BD * sizeof(A);
+  const uint32_t row_bytes = (uint32_t)(gcount * sizeof(E));
 
-  // stage the augmented table of sets [g0, g0 + gcount): tab[i * gcount + gl]
-  for (int e = tid; e < R * gcount; e += MRS_BD) {
-    const int i = e / gcount, gl = e - i * gcount;
-    const int64_t src = (int64_t)i * G + g0 + gl;
-    if constexpr (ONE) {
-      tab[e] = pval[src];
-    } else if constexpr (sizeof(T) == 1) {
-      tab[e] = (uint16_t)((uint8_t)pval[src] | ((uint16_t)pkid[src] << 8));
-    } else {
-      tab[e] = make_uint2(__float_as_uint((float)pval[src]),
-                          (uint32_t)pkid[src] * MRS_BD * (uint32_t)sizeof(A));
+  // stage the augmented table of sets [g0, g0 + gcount): row i, column gl.
+  // Loads go out in batches of MRS_STAGE per lane so their latencies overlap.
+  const int total = R * gcount;
+  for (int base = 0; base < total; base += MRS_BD * MRS_STAGE) {
+    T wv[MRS_STAGE];
+    uint8_t kv[MRS_STAGE];
+#pragma unroll
+    for (int u = 0; u < MRS_STAGE; ++u) {
+      const int e = base + u * MRS_BD + tid;
+      if (e < total) {
+        const int i = (int)fdiv((uint32_t)e, ta.fd_gs), gl = e - i * gcount;
+        const int src = i * G + g0 + gl;
+        wv[u] = pval[src];
+        kv[u] = ONE ? (uint8_t)0 : pkid[src];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < MRS_STAGE; ++u) {
+      const int e = base + u * MRS_BD + tid;
+      if (e < total) {
+        const int gl = e - (int)fdiv((uint32_t)e, ta.fd_gs) * gcount;
+        E* dst = reinterpret_cast<E*>(tab) + e;
+        const int slot = (gl % GB) * n + (int)kv[u];     // accumulator of the entry
+        if constexpr (ONE) {
+          *dst = wv[u];
+        } else if constexpr (sizeof(T) == 1) {
+          *dst = (uint16_t)((uint8_t)wv[u] | ((uint16_t)slot << 8));
+        } else {
+          *dst = make_uint2(__float_as_uint((float)wv[u]),
+                            (uint32_t)slot * MRS_BD * (uint32_t)sizeof(A));
+        }
+      }
     }
   }
+  // the slice's bias values next to the table (so the epilogue reads LDS)
+  A* bias_s = reinterpret_cast<A*>(tab + ((size_t)R * gcount * sizeof(E) + 15) / 16 * 16);
+  for (int k = tid; k < gcount * n; k += MRS_BD) bias_s[k] = bias ? bias[g0 * n + k] : A(0);
   __syncthreads();                                      // the only workgroup barrier
 
   const int S = ta.S;
   const int log2QS = ta.log2S + ta.log2Q;
-  const int QS = 1 << log2QS;                           // lanes per (item, set)
+  const int QS = 1 << log2QS;                           // lanes per (item, set unit)
   const int nq = 1 << ta.log2Q;
-  const int64_t work = ta.items * gcount * QS;
-  const int64_t stride = (int64_t)nbs * MRS_BD;
-  const int Hp = geo.Ho / geo.pool, Wp = geo.Wo / geo.pool;
+  const int nacc = GB * n;
+  const int work = ta.items * gunits * QS;              // < 2^31 (host)
+  const int stride = nbs * MRS_BD;
   A* acc_lane = acc + tid;
-  const int gbase_lane = tid & ~(QS - 1);               // first lane of this (item, set)
+  const int gbase_lane = tid & ~(QS - 1);               // first lane of this (item, set unit)
   const int r = tid & (QS - 1);                         // rank inside the group
   const int s = r & (S - 1);                            // slice
   const int q = r >> ta.log2S;                          // 2x2 pool sub-pixel
@@ -168,32 +232,34 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
   const int c0 = ta.chunk_mode ? s : 0;                 // first chunk of a tap
   const int cstep = ta.chunk_mode ? S : 1;
   const int jfirst = c0 * 4 < geo.cap ? c0 * 4 : 0;    // speculative first chunk, in the row
+  const bool vec_out = QS == 1 && (nacc & 3) == 0 && (geo.c_out & 3) == 0;
 
-  // every lane runs the same number of rounds (whole wavefronts reduce together)
-  const int64_t rounds = (work + stride - 1) / stride;
-  for (int64_t rd = 0; rd < rounds; ++rd) {
-    const int64_t w = rd * stride + (int64_t)bis * MRS_BD + tid;
+  const int rounds = (work + stride - 1) / stride;      // same for every lane of the block
+  for (int rd = 0; rd < rounds; ++rd) {
+    const int w = rd * stride + bis * MRS_BD + tid;
     const bool active = w < work;
-    const int64_t grp = active ? (w >> log2QS) : 0;     // (item, set) index
-    const int64_t item = grp / gcount;
-    const int gl = (int)(grp - item * gcount);
-    const int g = g0 + gl;
-    const int wp = (int)(item % Wp);
-    const int64_t tmp = item / Wp;
-    const int hp = (int)(tmp % Hp);
-    const int bb = (int)(tmp / Hp);
-    const int ho = hp * geo.pool + q / geo.pool;
-    const int wo = wp * geo.pool + q % geo.pool;
-    const E* trow = tab + gl;
+    const uint32_t grp = active ? (uint32_t)(w >> log2QS) : 0u;   // (item, set unit)
+    const uint32_t item = fdiv(grp, ta.fd_units);
+    const int gu = (int)(grp - item * (uint32_t)gunits);
+    const int gfirst = g0 + gu * GB;                    // first set of the lane
+    const uint32_t tmp = fdiv(item, ta.fd_wp);
+    const int wp = (int)(item - tmp * ta.fd_wp.d);
+    const uint32_t bbu = fdiv(tmp, ta.fd_hp);
+    const int hp = (int)(tmp - bbu * ta.fd_hp.d);
+    const int bb = (int)bbu;
+    const int ho = hp * geo.pool + (q >> 1) * (geo.pool >> 1);
+    const int wo = wp * geo.pool + (q & 1) * (geo.pool >> 1);
+    const unsigned char* tcol = tab + (size_t)gu * GB * sizeof(E);
 
-    A accr = A(0);
+    A accr[GB];
+#pragma unroll
+    for (int j = 0; j < GB; ++j) accr[j] = A(0);
     if (!ONE)
-      for (int k = 0; k < n; ++k) acc_lane[k * MRS_BD] = A(0);
+      for (int k = 0; k < nacc; ++k) acc_lane[k * MRS_BD] = A(0);
     if (active) {
-      // the lane's taps t0, t0 + tstep, ... walked with a rolling prefetch: the
-      // count and first chunk of the next MRS_AHEAD taps are in flight while a
-      // tap is processed (ring slots are compile-time after unrolling)
-      int64_t prow[MRS_AHEAD + 1];
+      // taps t0, t0 + tstep, ... with a rolling prefetch: the count and first
+      // chunk of the next MRS_AHEAD taps are in flight while one is processed
+      int prow[MRS_AHEAD + 1];
       int pcnt[MRS_AHEAD + 1];
       Chunk<T> first[MRS_AHEAD + 1];
       auto prefetch = [&](int u, int slot) {
@@ -201,27 +267,69 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
         prow[slot] = -1;
         pcnt[slot] = 0;
         if (t < T_) {
-          const int ky = t / geo.KW, kx = t - ky * geo.KW;
+          const int ky = (int)fdiv((uint32_t)t, ta.fd_kw), kx = t - ky * geo.KW;
           const int hy = ho * geo.S + ky - geo.P, wx = wo * geo.S + kx - geo.P;
           if (hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W) {
-            const int64_t pr = ((int64_t)bb * geo.H + hy) * geo.W + wx;
+            const int pr = (bb * geo.H + hy) * geo.W + wx;       // < 2^31 (host)
             prow[slot] = pr;
             pcnt[slot] = min(lcnt[pr], geo.C);
             // the row holds cap >= 4*ceil(C/4) entries: this chunk is in bounds
-            first[slot].load(lidx + pr * geo.cap, lval + pr * geo.cap, jfirst);
+            const int off = pr * geo.cap;                      // < 2^31 (host)
+            first[slot].load(lidx + off, lval + off, jfirst);
           }
         }
       };
 #pragma unroll
       for (int u = 0; u < MRS_AHEAD; ++u) prefetch(u, u);
+      if (ta.chunk_mode) {
+        // one tap: its count and the lane's first MRS_CHUNKS chunks (c0, c0 + S, ...)
+        // go out together; chunks past the row's capacity are not read
+        const int pr = prow[0];
+        if (pr >= 0) {
+          const int off = pr * geo.cap;
+          const uint16_t* li = lidx + off;
+          const T* lv = lval + off;
+          Chunk<T> ch[MRS_CHUNKS];
+          ch[0] = first[0];
+#pragma unroll
+          for (int z = 1; z < MRS_CHUNKS; ++z) {
+            const int j = (c0 + z * cstep) * 4;
+            if (j < geo.cap) ch[z].load(li, lv, j);
+          }
+          const int m = pcnt[0];
+#pragma unroll
+          for (int z = 0; z < MRS_CHUNKS; ++z) {
+            const int cz = c0 + z * cstep;
+            if (cz * 4 < m)
+              mrs_chunk<T, A, ONE, GB>(ch[z], m - cz * 4, tcol, row_bytes, acc_lane, accr);
+          }
+          // the rest of a long list, one chunk ahead
+          int c = c0 + MRS_CHUNKS * cstep;
+          if (c * 4 < m) {
+            Chunk<T> cur;
+            cur.load(li, lv, c * 4);
+            while (true) {
+              const int cn = c + cstep;
+              const bool more = cn * 4 < m;
+              Chunk<T> nxt;
+              if (more) nxt.load(li, lv, cn * 4);
+              mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tcol, row_bytes, acc_lane, accr);
+              if (!more) break;
+              cur = nxt;
+              c = cn;
+            }
+          }
+        }
+      } else
 #pragma unroll
       for (int u = 0; u < MRS_TAPS; ++u) {
         if (u + MRS_AHEAD < MRS_TAPS) prefetch(u + MRS_AHEAD, (u + MRS_AHEAD) % (MRS_AHEAD + 1));
         const int sl = u % (MRS_AHEAD + 1);
         if (prow[sl] >= 0 && c0 * 4 < pcnt[sl]) {
-          const uint16_t* li = lidx + prow[sl] * geo.cap;
-          const T* lv = lval + prow[sl] * geo.cap;
-          const int sbase = (t0 + u * tstep) * geo.C;
+          const int off = prow[sl] * geo.cap;
+          const uint16_t* li = lidx + off;
+          const T* lv = lval + off;
+          const unsigned char* tbase = tcol + (uint32_t)((t0 + u * tstep) * geo.C) * row_bytes;
           const int m = pcnt[sl];
           Chunk<T> cur = first[sl];
           int c = c0;
@@ -230,7 +338,7 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
             const bool more = cn * 4 < m;
             Chunk<T> nxt;
             if (more) nxt.load(li, lv, cn * 4);          // next chunk in flight
-            mrs_chunk<T, A, ONE>(cur, m - c * 4, sbase, trow, gcount, acc_lane, accr);
+            mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tbase, row_bytes, acc_lane, accr);
             if (!more) break;
             cur = nxt;
             c = cn;
@@ -238,20 +346,42 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
         }
       }
     }
-    if (ONE) acc_lane[0] = accr;
+    if (ONE) {
+#pragma unroll
+      for (int j = 0; j < GB; ++j) acc_lane[j * MRS_BD] = accr[j];
+    }
     wave_sync();                                        // partial sums of the group visible
-    // lane r of the group finishes kids k = r, r + QS, ...: sum the slices of
-    // each sub-pixel, take the max over the sub-pixels, add the bias
-    for (int k = r; k < n; k += QS) {
-      A m = A(0);
-      for (int qq = 0; qq < nq; ++qq) {
-        A a = A(0);
-        for (int t = 0; t < S; ++t) a += acc[k * MRS_BD + gbase_lane + qq * S + t];
-        m = (qq == 0 || a > m) ? a : m;
+    A* yrow = y + (item * (uint32_t)geo.c_out + (uint32_t)(gfirst * n));   // GB*n contiguous outputs
+    if (vec_out) {
+      // one lane per (item, set unit): 16-byte stores of 4 consecutive outputs
+      for (int k = 0; k < nacc; k += 4) {
+        A v4[4];
+#pragma unroll
+        for (int z = 0; z < 4; ++z) {
+          v4[z] = acc_lane[(k + z) * MRS_BD];
+          v4[z] += bias_s[(gfirst - g0) * n + k + z];
+        }
+        if (active) {
+          if constexpr (sizeof(A) == 4 && sizeof(T) == 1)
+            *reinterpret_cast<int4*>(yrow + k) = make_int4(v4[0], v4[1], v4[2], v4[3]);
+          else
+            *reinterpret_cast<float4*>(yrow + k) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+        }
       }
-      if (active) {
-        if (bias) m += bias[g * n + k];
-        y[item * geo.c_out + g * n + k] = m;
+    } else {
+      // lane r of the group finishes outputs kk = r, r + QS, ...: sum the slices
+      // of each sub-pixel, max over the sub-pixels, add the bias
+      for (int kk = r; kk < nacc; kk += QS) {
+        A mv = A(0);
+        for (int qq = 0; qq < nq; ++qq) {
+          A a = A(0);
+          for (int t = 0; t < S; ++t) a += acc[kk * MRS_BD + gbase_lane + qq * S + t];
+          mv = (qq == 0 || a > mv) ? a : mv;
+        }
+        if (active) {
+          mv += bias_s[(gfirst - g0) * n + kk];
+          yrow[kk] = mv;
+        }
       }
     }
     wave_sync();                                        // before the accumulators are reused
@@ -270,7 +400,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
                                                      const T* __restrict__ pval,
                                                      const A* __restrict__ bias,
                                                      A* __restrict__ y, ConvGeom geo,
-                                                     int64_t items) {
+                                                     int items, FastDiv fd_wp, FastDiv fd_hp) {
   constexpr int R = KH * KW * C;
   constexpr int PH = (POOL - 1) * STR + KH;
   constexpr int PW = (POOL - 1) * STR + KW;
@@ -282,17 +412,17 @@ __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
 #pragma unroll
   for (int i = 0; i < R; ++i) w[i] = (A)pval[i * 64 + lane];
   const A b = bias ? bias[lane] : A(0);
-  const int Hp = geo.Ho / POOL, Wp = geo.Wo / POOL;
   const int c = lane % C, pp = lane / C, py = pp / PW, px = pp % PW;
-  for (int64_t it = wave; it < items; it += nwaves) {
-    const int wp = (int)(it % Wp);
-    const int64_t tmp = it / Wp;
-    const int hp = (int)(tmp % Hp);
-    const int bb = (int)(tmp / Hp);
+  for (int it = (int)wave; it < items; it += (int)nwaves) {
+    const uint32_t tmp = fdiv((uint32_t)it, fd_wp);
+    const int wp = it - (int)(tmp * fd_wp.d);
+    const uint32_t bbu = fdiv(tmp, fd_hp);
+    const int hp = (int)(tmp - bbu * fd_hp.d);
+    const int bb = (int)bbu;
     const int hy = hp * POOL * STR - geo.P + py, wx = wp * POOL * STR - geo.P + px;
     A xv = A(0);
     if (pp < PH * PW && hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W)
-      xv = (A)x[(((int64_t)bb * geo.H + hy) * geo.W + wx) * C + c];
+      xv = (A)x[((bb * geo.H + hy) * geo.W + wx) * C + c];
     A best = A(0);
 #pragma unroll
     for (int q = 0; q < POOL * POOL; ++q) {
@@ -307,7 +437,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
       }
       best = (q == 0 || a > best) ? a : best;
     }
-    y[it * 64 + lane] = best;
+    y[it * 64 + lane] = best;                             // items * 64 < 2^31 (host)
   }
 }
 
@@ -318,7 +448,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1_rt(const T* __restrict__ x,
                                                         const T* __restrict__ pval,
                                                         const A* __restrict__ bias,
                                                         A* __restrict__ y, ConvGeom geo,
-                                                        int64_t items) {
+                                                        int items, FastDiv fd_wp, FastDiv fd_hp) {
   const int lane = threadIdx.x & 63;
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
@@ -326,17 +456,17 @@ __global__ __launch_bounds__(256) void conv_dense_n1_rt(const T* __restrict__ x,
   const int ph = (geo.pool - 1) * geo.S + geo.KH;
   const int pw = (geo.pool - 1) * geo.S + geo.KW;
   const A b = bias ? bias[lane] : A(0);
-  const int Hp = geo.Ho / geo.pool, Wp = geo.Wo / geo.pool;
   const int c = lane % geo.C, pp = lane / geo.C, py = pp / pw, px = pp % pw;
-  for (int64_t it = wave; it < items; it += nwaves) {
-    const int wp = (int)(it % Wp);
-    const int64_t tmp = it / Wp;
-    const int hp = (int)(tmp % Hp);
-    const int bb = (int)(tmp / Hp);
+  for (int it = (int)wave; it < items; it += (int)nwaves) {
+    const uint32_t tmp = fdiv((uint32_t)it, fd_wp);
+    const int wp = it - (int)(tmp * fd_wp.d);
+    const uint32_t bbu = fdiv(tmp, fd_hp);
+    const int hp = (int)(tmp - bbu * fd_hp.d);
+    const int bb = (int)bbu;
     const int hy = hp * geo.pool * geo.S - geo.P + py, wx = wp * geo.pool * geo.S - geo.P + px;
     A xv = A(0);
     if (pp < ph * pw && hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W)
-      xv = (A)x[(((int64_t)bb * geo.H + hy) * geo.W + wx) * geo.C + c];
+      xv = (A)x[((bb * geo.H + hy) * geo.W + wx) * geo.C + c];
     A best = A(0);
     for (int q = 0; q < geo.pool * geo.pool; ++q) {
       const int oy = (q / geo.pool) * geo.S, ox = (q % geo.pool) * geo.S;
@@ -349,7 +479,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1_rt(const T* __restrict__ x,
       }
       best = (q == 0 || a > best) ? a : best;
     }
-    y[it * 64 + lane] = best;
+    y[it * 64 + lane] = best;                             // items * 64 < 2^31 (host)
   }
 }
 

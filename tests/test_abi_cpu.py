@@ -217,3 +217,17 @@ def test_ctypes_signatures_match_header():
         nargs = len([a for a in m.group(1).split(",") if a.strip()])
         assert nargs == len(args), (name, nargs, len(args))
         assert ctypes  # silence unused import warnings in some linters
+
+
+def test_fast_division_formula():
+    """The kernels divide by launch-time constants with the round-up
+    reciprocal m = floor(2^32 (2^s - d) / d) + 1, s = ceil(log2 d):
+    floor(n / d) == (mulhi(n, m) + n) >> s for every 32-bit n."""
+    rng = np.random.default_rng(5)
+    for d in list(range(1, 3000)) + [65535, 65536, 100352, 2 ** 31 - 1, 2 ** 32 - 1]:
+        s = (d - 1).bit_length() if d > 1 else 0
+        m = (((1 << 32) * ((1 << s) - d)) // d + 1) if d > 1 else 0
+        ns = [0, 1, d - 1, d, d + 1, 2 ** 32 - 1] + [int(v) for v in rng.integers(0, 2 ** 32, 50)]
+        for n in ns:
+            if 0 <= n < 2 ** 32:
+                assert (((n * m) >> 32) + n) >> s == n // d
