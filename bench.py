@@ -177,6 +177,9 @@ def main() -> int:
     ap.add_argument("--rotate-mib", type=float, default=512.0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer --steps times (reference kernel "
+                         "for scaling the HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -194,6 +197,20 @@ def main() -> int:
     if not torch.cuda.is_available():
         log("bench.py needs a GPU")
         return 1
+    if args.calibrate_copy > 0:
+        nbytes = int(args.calibrate_copy * 2 ** 20) // 16 * 16
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes,
+                          "launches": args.steps,
+                          "GB/s": round(2 * nbytes * args.steps / el / 1e9, 1)}), flush=True)
+        return 0
     cfg = CONFIGS[args.config]
     log(f"bench: workload {cfg.name}, batch {cfg.batch}")
     inp = generate(cfg)
