@@ -37,20 +37,20 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def conv_products(cnt_map: np.ndarray, spec) -> int:
+def conv_products(cnt_map: np.ndarray, pl, groups: int) -> int:
     """Products the multiply-route-sum kernel performs: for every conv output
     pixel (before pooling), the non-zeros under its window, times G."""
     b, h, w = cnt_map.shape
-    ho = (h + 2 * spec.pad - spec.kh) // spec.stride + 1
-    wo = (w + 2 * spec.pad - spec.kw) // spec.stride + 1
-    pad = np.zeros((b, h + 2 * spec.pad, w + 2 * spec.pad), dtype=np.int64)
-    pad[:, spec.pad:spec.pad + h, spec.pad:spec.pad + w] = cnt_map
+    ho = (h + 2 * pl.pad - pl.kh) // pl.stride + 1
+    wo = (w + 2 * pl.pad - pl.kw) // pl.stride + 1
+    pad = np.zeros((b, h + 2 * pl.pad, w + 2 * pl.pad), dtype=np.int64)
+    pad[:, pl.pad:pl.pad + h, pl.pad:pl.pad + w] = cnt_map
     tot = 0
-    for ky in range(spec.kh):
-        for kx in range(spec.kw):
-            tot += int(pad[:, ky:ky + spec.stride * (ho - 1) + 1:spec.stride,
-                           kx:kx + spec.stride * (wo - 1) + 1:spec.stride].sum())
-    return tot * (spec.c_out // spec.n)
+    for ky in range(pl.kh):
+        for kx in range(pl.kw):
+            tot += int(pad[:, ky:ky + pl.stride * (ho - 1) + 1:pl.stride,
+                           kx:kx + pl.stride * (wo - 1) + 1:pl.stride].sum())
+    return tot * groups
 
 
 def layer_costs(net, bufs, cfg) -> dict:
@@ -58,34 +58,37 @@ def layer_costs(net, bufs, cfg) -> dict:
     actual non-zero counts of this batch."""
     import torch
     costs = {}
-    for li, p in enumerate(net.packed):
+    for li, (p, pl) in enumerate(zip(net.packed, net.plans)):
         s = p.spec
         es = 1 if p.val.dtype == torch.int8 else 4
-        rows = net.list_rows[li]
-        out_elems = int(np.prod(net.out_shapes[li]))
+        b, h, w, c = pl.geo
+        rows = b * h * w
+        out_elems = int(np.prod(pl.out_shape))
         table = p.val.numel() * (es + 1)
         bias = 0 if p.bias is None else s.c_out * 4
-        if getattr(s, "dense_input", False):
+        if pl.dense_kernel:
             # sparse-dense: every input element is read and multiplied
-            cnt = np.full(rows, s.c_in, dtype=np.int64)
-            mrs_bytes = rows * s.c_in * es + table + bias + out_elems * 4
+            cnt = np.full(rows, c, dtype=np.int64)
+            mrs_bytes = rows * c * es + table + bias + out_elems * 4
         else:
-            cnt = bufs.cnt[li].cpu().numpy().astype(np.int64)
+            src = bufs.lists[li - 1][2] if pl.in_lists else bufs.cnt[li]
+            cnt = src.cpu().numpy().astype(np.int64)
             nnz = int(cnt.sum())
             lists = nnz * (2 + es) + rows * 4
-            costs[f"{s.name}.compact"] = {"bytes": rows * s.c_in * es + lists}
+            if not pl.in_lists:
+                costs[f"{s.name}.compact"] = {"bytes": rows * c * es + lists}
             mrs_bytes = lists + table + bias + out_elems * 4
-        nnz = int(cnt.sum())
-        if s.kind == "conv":
-            b, h, w, _ = net.in_shapes[li]
-            prods = conv_products(cnt.reshape(b, h, w), s)
-        else:
-            prods = nnz * (s.c_out // s.n)
+        prods = conv_products(cnt.reshape(b, h, w), pl, s.c_out // s.n)
         costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
                                   "int": p.val.dtype == torch.int8}
         if s.k is not None:
-            ob = 1 if s.shift is not None else 4
-            costs[f"{s.name}.kwta"] = {"bytes": out_elems * (4 + ob)}
+            if pl.emit_lists:
+                lc = bufs.lists[li][2].cpu().numpy().astype(np.int64)
+                ob = 1 if s.shift is not None else 4
+                costs[f"{s.name}.kwta"] = {"bytes": out_elems * 4 + int(lc.sum()) * (2 + ob) + len(lc) * 4}
+            else:
+                ob = 1 if s.shift is not None else 4
+                costs[f"{s.name}.kwta"] = {"bytes": out_elems * (4 + ob)}
     return costs
 
 

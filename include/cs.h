@@ -113,9 +113,10 @@ int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, v
  * stride-2 max-pool (Table 1), then the NHWC store.
  *
  *  xt      CS_I8 (int8 lists and weights, int32 bias and y) or CS_F32.
- *  idx, lval, cnt  device lists of the b*h*w input pixels as cs_compact
- *          writes them, with row stride `cap` (cap >= c_in): every index
- *          < c_in; a count above c_in is read as c_in.
+ *  idx, lval, cnt  device lists of the b*h*w input pixels as cs_compact or
+ *          cs_kwta_lists write them, row stride `cap` (cap >= 1 entries): every
+ *          index < c_in; a count above cap is read as cap.  Row strides that
+ *          are multiples of 4 take the fast path (4 entries per load).
  *  b, h, w, c_in   input geometry; kh, kw >= 1; stride >= 1; pad >= 0.
  *          ho = (h + 2*pad - kh)/stride + 1, wo likewise, both >= 1.
  *  val, kid  device packed kernels [kh*kw*c_in][G] from cs_pack (every
@@ -190,6 +191,21 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
  */
 int cs_kwta(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,
             void* out, void* stream);
+
+/*
+ * cs_kwta_lists - k-WTA whose winners go to the next layer as (index, value)
+ * lists (Figure 10: the values that pass are sent on "along with their
+ * indices"; Section 3.2: the next layer's Select is this list).  DEVICE memory.
+ * Same selection and dtype rules as cs_kwta (exactly k, ties to the lower
+ * index, optional int8 requantisation), but instead of a dense row it writes,
+ * per row, the winners whose output value is non-zero in ascending index
+ * order: idx[row][0 .. cnt[row]-1] (uint16), val[row][..] (dtype ot),
+ * cnt[row] (int32), row stride `cap` >= k.  Entries past cnt are untouched.
+ * These lists feed cs_mrs_conv2d directly (its cap argument = this cap).
+ *  Errors: as cs_kwta; CS_ERR_SHAPE if cap < k.
+ */
+int cs_kwta_lists(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,
+                  uint16_t* idx, void* val, int32_t* cnt, int cap, void* stream);
 
 /*
  * cs_workspace_bytes - workspace cs_linear (op 0) or cs_conv2d (op 1) needs

@@ -38,6 +38,7 @@ SIGNATURES = {
     "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i,
                              _vp, _vp]),
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),
+    "cs_kwta_lists": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp]),
     "cs_workspace_bytes": (_sz, [_i, _i, _i64, _i]),
     "cs_status_str": (_c.c_char_p, [_i]),
 }

@@ -273,7 +273,7 @@ WsLayout ws_layout(cs_dtype xt, int64_t rows, int c_in) {
 // ---------------------------------------------------------------- k-WTA
 template <typename TI, typename TO>
 int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
-                  hipStream_t stream) {
+                  hipStream_t stream, cs::ListOut lo = cs::ListOut{nullptr, nullptr, nullptr, 0}) {
   if (c <= 64 && k <= 32) {
     const int64_t nb = (rows + cs::KWTA_LANE_ROWS - 1) / cs::KWTA_LANE_ROWS;
     if (nb > INT32_MAX) return CS_ERR_SHAPE;
@@ -282,13 +282,13 @@ int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
     const cs::FastDiv fd_c = cs::make_fastdiv((uint32_t)c);
     if (k <= 8)
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 8>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift, fd_c);
+                         out, shift, fd_c, lo);
     else if (k <= 16)
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 16>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift, fd_c);
+                         out, shift, fd_c, lo);
     else
       hipLaunchKernelGGL((cs::kwta_lane<TI, TO, 32>), grid, block, shmem, stream, in, rows, c, k,
-                         out, shift, fd_c);
+                         out, shift, fd_c, lo);
     return launch_status();
   }
   const int m = (c + 63) / 64;
@@ -297,7 +297,7 @@ int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
   const dim3 grid(nb), block(64 * cs::KWTA_WAVE_WAVES);
 #define CS_KWTA_WAVE(MM)                                                                  \
   hipLaunchKernelGGL((cs::kwta_wave<TI, TO, MM>), grid, block, 0, stream, in, rows, c, k, out, \
-                     shift)
+                     shift, lo)
   if (m <= 1) CS_KWTA_WAVE(1);
   else if (m <= 2) CS_KWTA_WAVE(2);
   else if (m <= 4) CS_KWTA_WAVE(4);
@@ -329,7 +329,7 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
   cs::ConvGeom geo;
   const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
   if (st != CS_OK) return st;
-  if (cap < c_in) return CS_ERR_SHAPE;
+  if (cap < 1) return CS_ERR_SHAPE;
   if (!idx || !lval || !cnt || !val || !kid || !y) return CS_ERR_ARG;
   geo.cap = cap;
   return mrs_launch(xt, idx, lval, cnt, geo, val, kid, bias, y, static_cast<hipStream_t>(stream));
@@ -432,6 +432,27 @@ int cs_kwta(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot
                          shift, s);
   return kwta_dispatch(static_cast<const int32_t*>(in), rows, c, k, static_cast<int32_t*>(out), 0,
                        s);
+}
+
+int cs_kwta_lists(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,
+                  uint16_t* idx, void* val, int32_t* cnt, int cap, void* stream) {
+  if (it != CS_I32 && it != CS_F32) return CS_ERR_DTYPE;
+  if (!(ot == it || (it == CS_I32 && ot == CS_I8))) return CS_ERR_DTYPE;
+  if (rows < 0 || c < 1 || k < 0 || cap < 1) return CS_ERR_ARG;
+  if (k > c || c > CS_MAX_KWTA_ROW || cap < k) return CS_ERR_SHAPE;
+  if (shift < 0 || shift > 31) return CS_ERR_ARG;
+  if (rows > 0 && (!in || !idx || !val || !cnt)) return CS_ERR_ARG;
+  if (rows == 0) return CS_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const cs::ListOut lo{idx, val, cnt, cap};
+  if (it == CS_F32)
+    return kwta_dispatch(static_cast<const float*>(in), rows, c, k, static_cast<float*>(nullptr),
+                         0, s, lo);
+  if (ot == CS_I8)
+    return kwta_dispatch(static_cast<const int32_t*>(in), rows, c, k,
+                         static_cast<int8_t*>(nullptr), shift, s, lo);
+  return kwta_dispatch(static_cast<const int32_t*>(in), rows, c, k, static_cast<int32_t*>(nullptr),
+                       0, s, lo);
 }
 
 size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in) {

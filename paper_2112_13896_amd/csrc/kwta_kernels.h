@@ -49,6 +49,18 @@ __device__ __forceinline__ int8_t kwta_out<int32_t, int8_t>(int32_t v, int shift
   return (int8_t)q;
 }
 
+// Optional list output: the winners of each row as (index, value) pairs in
+// ascending index order, capacity `cap` per row, with winners whose output
+// value is 0 left out (they contribute nothing downstream) - the form the
+// next layer's multiply-route-sum reads (Figure 10: winners go on "along with
+// their indices").  idx == nullptr selects the dense masked output instead.
+struct ListOut {
+  uint16_t* idx;
+  void* val;
+  int32_t* cnt;
+  int cap;
+};
+
 constexpr int KWTA_LANE_ROWS = 128;   // rows (threads) per block of kwta_lane
 constexpr int KWTA_BATCH = 16;        // tile elements a thread loads per batch
 
@@ -57,7 +69,7 @@ template <typename TI, typename TO, int KMAX>
 __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict__ in,
                                                             int64_t rows, int c, int k,
                                                             TO* __restrict__ out, int shift,
-                                                            FastDiv fd_c) {
+                                                            FastDiv fd_c, ListOut lo) {
   extern __shared__ __align__(16) unsigned char smem[];
   TI* tile = reinterpret_cast<TI*>(smem);
   const int stride = c + 1;
@@ -108,6 +120,37 @@ __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict
     for (int s = 0; s < KMAX; ++s) gt += (s < k && top[s] > thr) ? 1 : 0;
     need = k - gt;
   }
+  if (lo.idx) {
+    // list output: each lane writes its row's winners in index order
+    if (tid < nrows) {
+      const TI* r = tile + tid * stride;
+      const int64_t row = row0 + tid;
+      uint16_t* li = lo.idx + row * lo.cap;
+      TO* lv = static_cast<TO*>(lo.val) + row * lo.cap;
+      int pos = 0;
+      for (int i = 0; i < c; ++i) {
+        const TI v = r[i];
+        const uint32_t x = order_key(v);
+        bool win = false;
+        if (k > 0) {
+          if (x > thr) {
+            win = true;
+          } else if (x == thr && need > 0) {
+            win = true;
+            --need;
+          }
+        }
+        const TO ov = kwta_out<TI, TO>(v, shift);
+        if (win && ov != TO(0)) {
+          li[pos] = (uint16_t)i;
+          lv[pos] = ov;
+          ++pos;
+        }
+      }
+      lo.cnt[row] = pos;
+    }
+    return;                                             // no barrier follows
+  }
   __syncthreads();
   // second pass, results written back in place (as TO in a TO-typed view)
   TO* otile = reinterpret_cast<TO*>(smem);
@@ -145,7 +188,7 @@ template <typename TI, typename TO, int M>
 __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __restrict__ in,
                                                                   int64_t rows, int c, int k,
                                                                   TO* __restrict__ out,
-                                                                  int shift) {
+                                                                  int shift, ListOut lo) {
   __shared__ uint32_t hist[KWTA_WAVE_WAVES][256];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
@@ -226,7 +269,7 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
       __syncthreads();
     }
     // ranks of the ties in index order (element index = j*64 + lane)
-    int run = 0;
+    int run = 0, lrun = 0;
 #pragma unroll
     for (int j = 0; j < M; ++j) {
       const int e = j * 64 + lane;
@@ -239,8 +282,22 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
       if (all_win) win = true;
       else if (none_win) win = false;
       else win = key[j] > prefix || (eq && rank < need);
-      if (valid) out[row * c + e] = win ? kwta_out<TI, TO>(v[j], shift) : TO(0);
+      const TO ov = kwta_out<TI, TO>(v[j], shift);
+      if (lo.idx) {
+        // list output: non-zero winners, ranked in index order by ballot + popcount
+        const bool put = valid && win && ov != TO(0);
+        const uint64_t pb = __ballot(put);
+        if (put) {
+          const int pos = lrun + __popcll(pb & below);
+          lo.idx[row * lo.cap + pos] = (uint16_t)e;
+          static_cast<TO*>(lo.val)[row * lo.cap + pos] = ov;
+        }
+        lrun += __popcll(pb);
+      } else if (valid) {
+        out[row * c + e] = win ? ov : TO(0);
+      }
     }
+    if (lo.idx && live && lane == 0) lo.cnt[row] = lrun;
   }
 }
 

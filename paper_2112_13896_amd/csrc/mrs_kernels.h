@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void mrs_conv(const uint16_t* __restrict__ lid
         const int wx = wo * geo.S + kx - geo.P;
         if (wx < 0 || wx >= geo.W) continue;
         const int64_t pix = ((int64_t)bb * geo.H + hy) * geo.W + wx;
-        const int m = min(lcnt[pix], geo.C);        // never read past a list row
+        const int m = min(lcnt[pix], geo.cap);      // never read past a list row
         const uint16_t* li = lidx + pix * geo.cap;
         const T* lv = lval + pix * geo.cap;
         const int64_t sbase = (int64_t)(ky * geo.KW + kx) * geo.C;

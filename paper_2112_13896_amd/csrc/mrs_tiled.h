@@ -272,7 +272,7 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
           if (hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W) {
             const int pr = (bb * geo.H + hy) * geo.W + wx;       // < 2^31 (host)
             prow[slot] = pr;
-            pcnt[slot] = min(lcnt[pr], geo.C);
+            pcnt[slot] = min(lcnt[pr], geo.cap);
             // the row holds cap >= 4*ceil(C/4) entries: this chunk is in bounds
             const int off = pr * geo.cap;                      // < 2^31 (host)
             first[slot].load(lidx + off, lval + off, jfirst);

@@ -1,17 +1,25 @@
 """A chain of sparse-sparse layers run through the C ABI.
 
-Each layer description needs the attributes kind ("conv"/"linear"), c_in,
-c_out, n, kh, kw, stride, pad, pool, k (or None), shift (or None).  Weights
-are packed once on the host (cs_pack) and uploaded.  Buffers (compaction
-lists, per-layer sums, k-WTA outputs) live in a Buffers object allocated up
-front for a fixed batch; several Buffers can share one Network, so a caller
-can rotate among them.  forward() only enqueues kernels, on torch's current
-stream.
+Each layer description needs the attributes name, kind ("conv"/"linear"),
+c_in, c_out, n, kh, kw, stride, pad, pool, k (or None), shift (or None) and
+optionally dense_input.  Weights are packed once on the host (cs_pack) and
+uploaded.  Buffers live in a Buffers object allocated up front for a fixed
+batch; several Buffers can share one Network so a caller can rotate among
+them.  forward() only enqueues kernels, on torch's current stream.
 
-Per layer: cs_compact (Select's (index, value) lists), cs_mrs_conv2d
-(multiply/route/sum + bias + optional 2x2 max-pool), then cs_kwta (+ int8
-requantisation of the winners in int8 chains).  A conv output feeding a
-linear layer is read as [batch][h*w*c] (NHWC flatten, no copy).
+Data flow (Section 3.2; Figure 10 sends the k-WTA winners on "along with
+their indices"):
+  * the first layer's dense input is compacted into (index, value) lists
+    (cs_compact), or read densely by the sparse-dense kernel when the layer
+    is marked dense_input (cs_conv2d_dense);
+  * multiply/route/sum (cs_mrs_conv2d: + bias + optional 2x2 max-pool) reads
+    the lists and writes the layer's sums;
+  * a k-WTA that feeds another layer emits that layer's lists directly
+    (cs_kwta_lists, capacity k rounded up to 4, winners requantised to int8
+    in int8 chains); the last layer's k-WTA writes a dense masked output.
+A linear layer that follows a conv layer reads the conv output's per-pixel
+lists as a convolution whose window is the whole h x w map: its slots
+(h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
 """
 from __future__ import annotations
 
@@ -34,16 +42,35 @@ class PackedLayer:
 
 
 @dataclass
+class Plan:
+    """How one layer runs: list geometry and kernel parameters."""
+    in_lists: bool           # input arrives as the previous layer's k-WTA lists
+    dense_kernel: bool       # sparse-dense kernel on a dense input
+    geo: tuple               # (b, h, w, c_in) of the list rows / dense input
+    kh: int
+    kw: int
+    stride: int
+    pad: int
+    pool: int
+    out_shape: tuple         # sums after pool
+    emit_lists: bool         # k-WTA writes lists for the next layer
+    cap_out: int             # capacity of the emitted lists
+
+
+@dataclass
 class Buffers:
-    idx: list = field(default_factory=list)    # per layer: [rows][c_in] uint16 (as int16)
-    lval: list = field(default_factory=list)   # per layer: [rows][c_in] list values
-    cnt: list = field(default_factory=list)    # per layer: [rows] int32
-    acc: list = field(default_factory=list)    # per layer: sums after pool
-    out: list = field(default_factory=list)    # per layer: k-WTA / requantised output
+    idx: list = field(default_factory=list)     # per layer: compaction lists (dense input only)
+    lval: list = field(default_factory=list)
+    cnt: list = field(default_factory=list)
+    acc: list = field(default_factory=list)     # per layer: sums after pool
+    out: list = field(default_factory=list)     # per layer: dense k-WTA output, or None
+    lists: list = field(default_factory=list)   # per layer: (idx, val, cnt) emitted, or None
 
     def nbytes(self) -> int:
-        return sum(t.numel() * t.element_size() for lst in
-                   (self.idx, self.lval, self.cnt, self.acc, self.out) for t in lst)
+        ts = [t for lst in (self.idx, self.lval, self.cnt, self.acc, self.out) for t in lst
+              if t is not None]
+        ts += [t for trip in self.lists if trip is not None for t in trip]
+        return sum(t.numel() * t.element_size() for t in ts)
 
 
 class Network:
@@ -59,7 +86,7 @@ class Network:
             bias = None if b is None else torch.from_numpy(np.asarray(b)).to(self.device)
             self.packed.append(PackedLayer(spec, torch.from_numpy(val).to(self.device),
                                            torch.from_numpy(kid).to(self.device), bias, holes))
-        self._shapes()
+        self._plan()
         self.bufs = self.make_buffers()
 
     @property
@@ -70,112 +97,150 @@ class Network:
     def out(self):
         return self.bufs.out
 
-    # shapes and buffers ----------------------------------------------------
-    def _shapes(self):
+    # plan ------------------------------------------------------------------
+    def _plan(self):
         shape = (self.batch,) + self.in_shape
-        self.in_shapes, self.out_shapes, self.list_rows = [], [], []
-        for p in self.packed:
+        self.plans = []
+        self.in_shapes = []
+        nl = len(self.packed)
+        prev_k = None
+        for li, p in enumerate(self.packed):
             s = p.spec
+            in_lists = prev_k is not None
             if s.kind == "conv":
-                if len(shape) != 4:
-                    raise ValueError(f"{s} needs an NHWC input, got {shape}")
+                if len(shape) != 4 or shape[3] != s.c_in:
+                    raise ValueError(f"layer {s.name}: NHWC input with {s.c_in} channels expected")
                 b, h, w, c = shape
-                if c != s.c_in:
-                    raise ValueError("channel mismatch")
-                ho, wo = conv_out(h, s.kh, s.stride, s.pad), conv_out(w, s.kw, s.stride, s.pad)
-                oshape = (b, ho // s.pool, wo // s.pool, s.c_out)
-                rows = b * h * w
+                geo = (b, h, w, c)
+                kh, kw, st, pad, pool = s.kh, s.kw, s.stride, s.pad, s.pool
+                ho, wo = conv_out(h, kh, st, pad), conv_out(w, kw, st, pad)
+                oshape = (b, ho // pool, wo // pool, s.c_out)
             else:
                 b = shape[0]
-                d_in = int(np.prod(shape[1:]))
-                if d_in != s.c_in:
-                    raise ValueError("input length mismatch")
+                if int(np.prod(shape[1:])) != s.c_in:
+                    raise ValueError(f"layer {s.name}: input length {s.c_in} expected")
+                if len(shape) == 4:
+                    # linear after conv: a convolution whose window is the whole map
+                    geo = shape
+                    kh, kw = shape[1], shape[2]
+                else:
+                    geo = (b, 1, 1, s.c_in)
+                    kh = kw = 1
+                st, pad, pool = 1, 0, 1
                 oshape = (b, s.c_out)
-                rows = b
+            dense_kernel = bool(getattr(s, "dense_input", False)) and not in_lists
+            emit = s.k is not None and li + 1 < nl
+            self.plans.append(Plan(in_lists, dense_kernel, geo, kh, kw, st, pad, pool, oshape,
+                                   emit, ops.list_capacity(s.k) if emit else 0))
             self.in_shapes.append(shape)
-            self.out_shapes.append(oshape)
-            self.list_rows.append(rows)
+            prev_k = s.k
             shape = oshape
         self.out_shape = shape
 
     def make_buffers(self) -> Buffers:
         B = Buffers()
-        for p, oshape, rows in zip(self.packed, self.out_shapes, self.list_rows):
+        for p, pl in zip(self.packed, self.plans):
             s = p.spec
             dt = p.val.dtype
             acc_dt = torch.int32 if dt == torch.int8 else torch.float32
-            lr = 0 if getattr(s, "dense_input", False) else rows
-            B.idx.append(torch.empty((lr, s.c_in), dtype=torch.int16, device=self.device))
-            B.lval.append(torch.empty((lr, s.c_in), dtype=dt, device=self.device))
-            B.cnt.append(torch.empty((lr,), dtype=torch.int32, device=self.device))
-            acc = torch.empty(oshape, dtype=acc_dt, device=self.device)
+            b, h, w, c = pl.geo
+            rows = b * h * w
+            if not pl.in_lists and not pl.dense_kernel:
+                B.idx.append(torch.empty((rows, c), dtype=torch.int16, device=self.device))
+                B.lval.append(torch.empty((rows, c), dtype=dt, device=self.device))
+                B.cnt.append(torch.empty((rows,), dtype=torch.int32, device=self.device))
+            else:
+                B.idx.append(None)
+                B.lval.append(None)
+                B.cnt.append(None)
+            acc = torch.empty(pl.out_shape, dtype=acc_dt, device=self.device)
             B.acc.append(acc)
             if s.k is None:
                 B.out.append(acc)
+                B.lists.append(None)
+            elif pl.emit_lists:
+                orow = int(np.prod(pl.out_shape[:-1]))
+                odt = torch.int8 if s.shift is not None else acc_dt
+                B.out.append(None)
+                B.lists.append((torch.empty((orow, pl.cap_out), dtype=torch.int16, device=self.device),
+                                torch.empty((orow, pl.cap_out), dtype=odt, device=self.device),
+                                torch.empty((orow,), dtype=torch.int32, device=self.device)))
             else:
                 odt = torch.int8 if s.shift is not None else acc_dt
-                B.out.append(torch.empty(oshape, dtype=odt, device=self.device))
+                B.out.append(torch.empty(pl.out_shape, dtype=odt, device=self.device))
+                B.lists.append(None)
         return B
 
     # execution -------------------------------------------------------------
-    def forward_layer(self, li: int, x: torch.Tensor, bufs: Buffers | None = None,
-                      timer=None) -> torch.Tensor:
+    def forward_layer(self, li: int, x, bufs: Buffers | None = None, timer=None):
+        """x: the dense input tensor (first layer) or None (lists of layer li-1)."""
         B = self.bufs if bufs is None else bufs
         p = self.packed[li]
         s = p.spec
-        rows = self.list_rows[li]
+        pl = self.plans[li]
         t = timer or _NoTimer()
-        if getattr(s, "dense_input", False):
+        b, h, w, c = pl.geo
+        acc = B.acc[li]
+        acc4 = acc.reshape(b, -1, 1, s.c_out) if acc.dim() == 2 else acc
+        if pl.dense_kernel:
             # sparse-dense variant: dense activations, no compaction
             t.start(f"{s.name}.mrs")
-            ops.conv2d_dense(x, p.val, p.kid, s.kh, s.kw, s.n, s.stride, s.pad, p.bias, s.pool,
-                             out=B.acc[li])
+            ops.conv2d_dense(x, p.val, p.kid, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                             pl.pool, out=acc)
             t.stop(f"{s.name}.mrs")
-            return self._select(li, s, B, t)
-        xin = x.reshape(rows, s.c_in)
-        t.start(f"{s.name}.compact")
-        ops.compact_into(xin, B.idx[li], B.lval[li], B.cnt[li])
-        t.stop(f"{s.name}.compact")
-        if s.kind == "conv":
-            geo = self.in_shapes[li]
-            kh, kw, stride, pad, pool = s.kh, s.kw, s.stride, s.pad, s.pool
         else:
-            geo = (rows, 1, 1, s.c_in)
-            kh = kw = stride = pool = 1
-            pad = 0
-        acc = B.acc[li]
-        t.start(f"{s.name}.mrs")
-        ops.mrs_conv2d(B.idx[li], B.lval[li], B.cnt[li], geo, p.val, p.kid, kh, kw, s.n,
-                       stride, pad, p.bias, pool, out=acc.reshape(
-                           (geo[0], (conv_out(geo[1], kh, stride, pad)) // pool,
-                            (conv_out(geo[2], kw, stride, pad)) // pool, s.c_out)))
-        t.stop(f"{s.name}.mrs")
-        return self._select(li, s, B, t)
-
-    def _select(self, li, s, B, t):
-        acc = B.acc[li]
-        if s.k is not None:
-            t.start(f"{s.name}.kwta")
-            if s.shift is not None:
-                ops.kwta(acc, s.k, torch.int8, s.shift, out=B.out[li])
+            if pl.in_lists:
+                idx, lval, cnt = B.lists[li - 1]
             else:
-                ops.kwta(acc, s.k, out=B.out[li])
+                t.start(f"{s.name}.compact")
+                ops.compact_into(x.reshape(b * h * w, c), B.idx[li], B.lval[li], B.cnt[li])
+                t.stop(f"{s.name}.compact")
+                idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
+            t.start(f"{s.name}.mrs")
+            ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.val, p.kid, pl.kh, pl.kw, s.n, pl.stride,
+                           pl.pad, p.bias, pl.pool, out=acc4)
+            t.stop(f"{s.name}.mrs")
+        if s.k is not None:
+            odt = torch.int8 if s.shift is not None else None
+            shift = s.shift if s.shift is not None else 0
+            t.start(f"{s.name}.kwta")
+            if pl.emit_lists:
+                ops.kwta_lists(acc, s.k, odt, shift, pl.cap_out, out=B.lists[li])
+            else:
+                ops.kwta(acc, s.k, odt, shift, out=B.out[li])
             t.stop(f"{s.name}.kwta")
         return B.out[li]
 
-    def forward(self, x: torch.Tensor, bufs: Buffers | None = None, timer=None) -> torch.Tensor:
+    def forward(self, x: torch.Tensor, bufs: Buffers | None = None, timer=None):
         if tuple(x.shape) != tuple(self.in_shapes[0]):
             raise ValueError(f"input shape {tuple(x.shape)} != planned {self.in_shapes[0]}")
-        cur = x
+        out = None
         for li in range(len(self.packed)):
-            cur = self.forward_layer(li, cur, bufs, timer)
-        return cur
+            out = self.forward_layer(li, x if li == 0 else None, bufs, timer)
+        return out
+
+    def dense_output(self, li: int, bufs: Buffers | None = None) -> torch.Tensor:
+        """Layer li's k-WTA output as a dense tensor (scattered back from its
+        lists when the layer emits lists).  For checks, not the timed path."""
+        B = self.bufs if bufs is None else bufs
+        if B.lists[li] is None:
+            return B.out[li]
+        idx, val, cnt = B.lists[li]
+        pl = self.plans[li]
+        rows, cap = idx.shape
+        dense = torch.zeros((rows, pl.out_shape[-1]), dtype=val.dtype, device=val.device)
+        pos = torch.arange(cap, device=val.device)[None, :]
+        keep = pos < cnt[:, None].to(torch.int64)
+        r = torch.arange(rows, device=val.device)[:, None].expand(rows, cap)
+        ii = idx.to(torch.int64) & 0xFFFF
+        dense[r[keep], ii[keep]] = val[keep]
+        return dense.reshape(pl.out_shape)
 
     def kernel_names(self) -> list:
         names = []
-        for p in self.packed:
+        for pl, p in zip(self.plans, self.packed):
             s = p.spec
-            if not getattr(s, "dense_input", False):
+            if not pl.in_lists and not pl.dense_kernel:
                 names.append(f"{s.name}.compact")
             names.append(f"{s.name}.mrs")
             if s.k is not None:

@@ -199,3 +199,28 @@ def kwta(x: torch.Tensor, k: int, out_dtype: torch.dtype | None = None, shift: i
     check("cs_kwta", lib().cs_kwta(_dt(x), _dev(x, "x"), rows, c, k, _TORCH_DT[odt], shift,
                                    _dev(out, "out"), _stream()))
     return out
+
+
+def list_capacity(k: int) -> int:
+    """Row stride for k-entry lists: k rounded up to a multiple of 4 (vector reads)."""
+    return max(4, (k + 3) // 4 * 4)
+
+
+def kwta_lists(x: torch.Tensor, k: int, out_dtype: torch.dtype | None = None, shift: int = 0,
+               cap: int | None = None, out=None):
+    """k-WTA along the last axis, winners emitted as (idx, val, cnt) lists of
+    capacity `cap` (default: list_capacity(k)).  Rows are all leading axes."""
+    c = x.shape[-1]
+    rows = x.numel() // c if c else 0
+    odt = x.dtype if out_dtype is None else out_dtype
+    cap = list_capacity(k) if cap is None else cap
+    if out is None:
+        idx = torch.empty((rows, cap), dtype=torch.int16, device=x.device)
+        val = torch.empty((rows, cap), dtype=odt, device=x.device)
+        cnt = torch.empty((rows,), dtype=torch.int32, device=x.device)
+    else:
+        idx, val, cnt = out
+    check("cs_kwta_lists", lib().cs_kwta_lists(
+        _dt(x), _dev(x, "x"), rows, c, k, _TORCH_DT[odt], shift, _dev(idx, "idx"),
+        _dev(val, "val"), _dev(cnt, "cnt"), cap, _stream()))
+    return idx, val, cnt

@@ -157,7 +157,7 @@ def test_conv2d_dense_validation(L):
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, FAKE, 8, 4, None, 1, FAKE, None]
-    assert m(*base[:4], 3, *base[5:]) == CS_ERR_SHAPE          # cap < c_in
+    assert m(*base[:4], 0, *base[5:]) == CS_ERR_SHAPE          # list capacity 0
     bad = list(base)
     bad[1] = None
     assert m(*bad) == CS_ERR_ARG
@@ -183,6 +183,25 @@ def test_kwta_validation(L):
     assert k(CS_I32, FAKE, 4, 64, 8, CS_I8, 32, FAKE, None) == CS_ERR_ARG
     assert k(CS_I32, None, 4, 64, 8, CS_I8, 3, FAKE, None) == CS_ERR_ARG
     assert k(CS_I32, None, 0, 64, 8, CS_I8, 3, None, None) == CS_OK     # empty: nothing launched
+
+
+def test_kwta_lists_validation(L):
+    k = L.cs_kwta_lists
+    ok = [CS_I32, FAKE, 4, 64, 8, CS_I8, 3, FAKE, FAKE, FAKE, 8, None]
+
+    def call(**kw):
+        a = list(ok)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return k(*a)
+    assert call(a0=CS_I8) == CS_ERR_DTYPE
+    assert call(a0=CS_F32) == CS_ERR_DTYPE              # f32 input cannot requantise
+    assert call(a10=7) == CS_ERR_SHAPE                  # capacity below k
+    assert call(a10=0) == CS_ERR_ARG
+    assert call(a4=65) == CS_ERR_SHAPE
+    assert call(a7=None) == CS_ERR_ARG
+    assert call(a6=40) == CS_ERR_ARG
+    assert call(a2=0, a1=None, a7=None, a8=None, a9=None) == CS_OK
 
 
 def test_workspace_bytes(L):

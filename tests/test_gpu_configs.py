@@ -27,14 +27,15 @@ def run_gpu(cfg, inp):
     net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
     net.forward(dev(inp["x"]))
     torch.cuda.synchronize()
-    return net, [host(a) for a in net.acc], [host(a) for a in net.out]
+    outs = [host(net.dense_output(li)) for li in range(len(cfg.layers))]
+    return net, [host(a) for a in net.acc], outs
 
 
 @pytest.mark.parametrize("cid", [1, 2, 5])
 def test_int_config_bit_exact(cid):
     cfg = CONFIGS[cid]
     inp = generate(cfg)
-    _, acc, out = run_gpu(cfg, inp)
+    net, acc, out = run_gpu(cfg, inp)
     ref = networks.run_chain(cfg.layers, inp["x"], inp["W"], inp["b"])
     for li, spec in enumerate(cfg.layers):
         assert acc[li].dtype == np.int32
@@ -43,6 +44,15 @@ def test_int_config_bit_exact(cid):
             f"layer {spec.name} output"
         if spec.k is not None:
             assert ((out[li].reshape(-1, out[li].shape[-1]) != 0).sum(axis=1) <= spec.k).all()
+        if net.bufs.lists[li] is not None:
+            # the emitted lists hold exactly the non-zero outputs, in index order
+            idx, val, cnt = (host(t) for t in net.bufs.lists[li])
+            dense = ref[li]["out"].reshape(len(cnt), -1)
+            for r in range(0, len(cnt), max(1, len(cnt) // 500)):
+                nz = np.flatnonzero(dense[r])
+                assert cnt[r] == len(nz)
+                assert np.array_equal(idx[r, :cnt[r]].view(np.uint16), nz)
+                assert np.array_equal(val[r, :cnt[r]].astype(np.int64), dense[r, nz])
 
 
 @pytest.mark.parametrize("cid", [3, 4])
@@ -78,6 +88,8 @@ def test_repeated_forward_identical():
     inp = generate(cfg, batch=4)
     net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, 4)
     x = dev(inp["x"])
-    a = host(net.forward(x)).copy()
-    b = host(net.forward(x)).copy()
+    net.forward(x)
+    a = host(net.dense_output(0)).copy()
+    net.forward(x)
+    b = host(net.dense_output(0)).copy()
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))

@@ -103,6 +103,33 @@ def test_kwta_requant(c, k, shift):
     assert out.dtype == np.int8 and np.array_equal(out, exp)
 
 
+@pytest.mark.parametrize("c,k", [(64, 8), (64, 16), (64, 32), (256, 26), (576, 72), (1500, 75), (7, 3), (1, 1), (2048, 300)])
+@pytest.mark.parametrize("mode", ["i32", "i32->i8", "f32"])
+def test_kwta_lists(c, k, mode):
+    """k-WTA emitting (index, value) lists: exactly the non-zero entries of the
+    dense k-WTA (or requantised) row, in index order."""
+    r = rng(c * 3 + k + len(mode))
+    rows = 301
+    if mode == "f32":
+        v = np.round(r.normal(size=(rows, c)), 2).astype(np.float32)
+        v[:, ::5] = 0.0
+    else:
+        v = r.integers(-3000, 3001, size=(rows, c)).astype(np.int32)
+        v[::7] = 5
+    shift = 4 if mode == "i32->i8" else 0
+    odt = torch.int8 if mode == "i32->i8" else None
+    from paper_2112_13896_amd.ops import list_capacity
+    cap = list_capacity(k) + (4 if c == 64 else 0)
+    idx, val, cnt = (host(t) for t in ops.kwta_lists(dev(v), k, odt, shift, cap))
+    win = o.kwta_winners(v, k)
+    dense = o.requant(v, shift, win) if mode == "i32->i8" else np.where(win, v, np.zeros_like(v))
+    for row in range(rows):
+        nz = np.flatnonzero(dense[row])
+        assert cnt[row] == len(nz) and cnt[row] <= k
+        assert np.array_equal(idx[row, :cnt[row]].view(np.uint16), nz)
+        assert np.array_equal(val[row, :cnt[row]], dense[row, nz])
+
+
 # ------------------------------------------------------------------ linear
 LINEAR_CASES = [
     # batch, d_in, d_out, n, nnz per row
@@ -239,6 +266,32 @@ def test_mrs_on_compacted_lists_matches_conv2d():
     idx, lv, cnt = ops.compact(xd.reshape(-1, 64))
     y2 = ops.mrs_conv2d(idx, lv, cnt, x.shape, vd, kd, 3, 3, 8, 1, 1)
     assert torch.equal(y1, y2)
+
+
+@pytest.mark.parametrize("dtype", ["i8", "f32"])
+def test_mrs_reads_kwta_lists(dtype):
+    """A conv whose input is the previous k-WTA's capacity-k lists, and a
+    linear layer over a whole conv map read as a window-sized conv."""
+    r = rng(33 + (dtype == "f32"))
+    b, h, w, c = 3, 6, 7, 64
+    k = 9
+    acc_prev = (r.integers(-500, 500, size=(b, h, w, c)).astype(np.int32) if dtype == "i8"
+                else r.normal(size=(b, h, w, c)).astype(np.float32))
+    shift = 2
+    odt = torch.int8 if dtype == "i8" else None
+    lists = ops.kwta_lists(dev(acc_prev), k, odt, shift if dtype == "i8" else 0)
+    win = o.kwta_winners(acc_prev, k)
+    x_ref = o.requant(acc_prev, shift, win) if dtype == "i8" else np.where(win, acc_prev, np.float32(0))
+    wd = "int8" if dtype == "i8" else "normal"
+    for (kh, kw, pad, n, c_out) in [(3, 3, 1, 8, 64), (h, w, 0, 16, 48)]:
+        W = complementary_weights(r, r, c_out, kh * kw * c, n, wd).reshape(c_out, kh, kw, c)
+        val, kid, _ = ops.pack(W.reshape(c_out, -1), n)
+        y = host(ops.mrs_conv2d(*lists, (b, h, w, c), dev(val), dev(kid), kh, kw, n, 1, pad))
+        ref = o.conv2d_nhwc(x_ref, W, 1, pad)
+        if dtype == "i8":
+            assert np.array_equal(y.astype(np.int64), ref)
+        else:
+            assert_f32_close(y, ref, o.abs_sum_conv(x_ref, W, 1, pad), "mrs on k-WTA lists")
 
 
 def test_fp32_bitwise_reproducible():
