@@ -60,11 +60,12 @@ def layer_costs(net, bufs, cfg) -> dict:
     costs = {}
     for li, (p, pl) in enumerate(zip(net.packed, net.plans)):
         s = p.spec
-        es = 1 if p.val.dtype == torch.int8 else 4
+        is_int = p.aug.dtype == torch.int16          # int8 weights/activations
+        es = 1 if is_int else 4
         b, h, w, c = pl.geo
         rows = b * h * w
         out_elems = int(np.prod(pl.out_shape))
-        table = p.val.numel() * (es + 1)
+        table = p.aug.numel() * p.aug.element_size()   # the augmented tensor
         bias = 0 if p.bias is None else s.c_out * 4
         if pl.dense_kernel:
             # sparse-dense: every input element is read and multiplied
@@ -80,7 +81,7 @@ def layer_costs(net, bufs, cfg) -> dict:
             mrs_bytes = lists + table + bias + out_elems * 4
         prods = conv_products(cnt.reshape(b, h, w), pl, s.c_out // s.n)
         costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
-                                  "int": p.val.dtype == torch.int8}
+                                  "int": is_int}
         if s.k is not None:
             if pl.emit_lists:
                 lc = bufs.lists[li][2].cpu().numpy().astype(np.int64)

@@ -65,25 +65,38 @@ typedef enum { CS_I8 = 0, CS_I32 = 1, CS_F32 = 2 } cs_dtype;
 #define CS_MAX_KWTA_ROW 2048 /* row length of cs_kwta                           */
 
 /*
- * cs_pack - Combine (Section 3.1/3.2 step 1, Figure 7; Kernel ID of Section
- * 3.3.1, local to the set as in Section 3.3.2).  Offline, HOST memory only,
- * no HIP call.
+ * Augmented packed tensor (Section 3.3.1: each packed weight carries the
+ * Kernel ID that routes its products; Figure 8(b)).  aug[i][g], i < r slots,
+ * g < G sets, row-major, one entry per (slot, set):
+ *   CS_I8 : uint16_t  = (uint8_t)value | (kid << 8)
+ *   CS_F32: cs_aug_f32 {float value; uint32_t kid;}   (8 bytes)
+ * kid is local to the set, in [0, n).  A slot no kernel of the set uses (a
+ * hole) holds value 0, kid 0.
+ */
+typedef struct {
+  float value;
+  uint32_t kid;
+} cs_aug_f32;
+
+/*
+ * cs_pack - Combine (Section 3.1/3.2 step 1, Figure 7): overlay each set of n
+ * kernels into one packed kernel with its Kernel IDs.  Offline, HOST memory
+ * only, no HIP call.
  *
- *  wt      CS_I8 or CS_F32: element type of w and val.
+ *  wt      CS_I8 or CS_F32: element type of w.
  *  w       host [d_out][r] dense weights; an exact zero is an absent weight.
  *  n       complement factor, 1 <= n <= CS_MAX_N, must divide d_out.
- *  val     host [r][G] out: val[i][g] = w[g*n + kid][i] for the one kernel of
- *          set g that is non-zero at slot i; 0 where no kernel is (a hole).
- *  kid     host [r][G] out (uint8): local Kernel ID in [0, n); 0 at holes.
+ *  aug     host [r][G] out, G = d_out / n, augmented entries as above:
+ *          value = w[g*n + kid][i] for the one kernel of set g non-zero at i.
  *  holes   out (may be NULL): number of (i, g) slots no kernel of g uses.
  *  bad_g, bad_i  out (may be NULL): on CS_ERR_COLLISION, the first colliding
  *          (set, slot) in set-major, slot-minor order; -1 otherwise.
- *  Errors: CS_ERR_ARG (null w/val/kid, d_out/r < 1), CS_ERR_SHAPE (n does not
- *  divide d_out, n > CS_MAX_N), CS_ERR_DTYPE, CS_ERR_COLLISION (val/kid are
- *  then unspecified).
+ *  Errors: CS_ERR_ARG (null w/aug, d_out/r < 1), CS_ERR_SHAPE (n does not
+ *  divide d_out, n > CS_MAX_N), CS_ERR_DTYPE, CS_ERR_COLLISION (aug is then
+ *  unspecified).
  */
-int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* val, uint8_t* kid,
-            int64_t* holes, int* bad_g, int* bad_i);
+int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* aug, int64_t* holes,
+            int* bad_g, int* bad_i);
 
 /*
  * cs_compact - the sparse representation of Select (Section 3.2 step 2: the
@@ -108,8 +121,8 @@ int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, v
  * 3.3.1-3.3.2) of a convolution whose input is already in cs_compact form.
  * DEVICE memory.  For each output pixel and each non-zero (c, v) of every
  * input pixel under the kernel window at tap (ky, kx), slot
- * i = (ky*kw + kx)*c_in + c; for each set g the product v * val[i][g] is added
- * to output channel g*n + kid[i][g].  Then bias, then the optional 2x2
+ * i = (ky*kw + kx)*c_in + c; for each set g the product v * aug[i][g].value
+ * is added to output channel g*n + aug[i][g].kid.  Then bias, the optional 2x2
  * stride-2 max-pool (Table 1), then the NHWC store.
  *
  *  xt      CS_I8 (int8 lists and weights, int32 bias and y) or CS_F32.
@@ -119,8 +132,8 @@ int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, v
  *          are multiples of 4 take the fast path (4 entries per load).
  *  b, h, w, c_in   input geometry; kh, kw >= 1; stride >= 1; pad >= 0.
  *          ho = (h + 2*pad - kh)/stride + 1, wo likewise, both >= 1.
- *  val, kid  device packed kernels [kh*kw*c_in][G] from cs_pack (every
- *          kid < n).
+ *  aug     device augmented packed tensor [kh*kw*c_in][G] from cs_pack
+ *          (every kid < n), element type of xt.
  *  c_out, n  n divides c_out, 1 <= n <= CS_MAX_N.
  *  bias    device [c_out] (int32 / fp32) or NULL for none.
  *  pool    1 (none) or 2 (2x2 stride-2 max-pool; ho and wo must be even).
@@ -129,8 +142,8 @@ int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, v
  */
 int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt, int cap,
                   int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
-                  const void* val, const uint8_t* kid, int c_out, int n, const void* bias,
-                  int pool, void* y, void* stream);
+                  const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                  void* stream);
 
 /*
  * cs_linear - a whole sparse-sparse linear layer: cs_compact of x into the
@@ -138,14 +151,14 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
  * of 1x1 images).  DEVICE memory.
  *
  *  x       device [batch][d_in] (int8 or fp32), d_in <= CS_MAX_ROW.
- *  val,kid device packed kernels [d_in][G] from cs_pack of [d_out][d_in].
+ *  aug     device augmented packed tensor [d_in][G] from cs_pack of [d_out][d_in].
  *  bias    device [d_out] or NULL.   y  device [batch][d_out] out.
  *  ws      device workspace of at least cs_workspace_bytes(0, xt, batch, d_in)
  *          bytes, 256-byte aligned; its contents on entry do not matter.
  *  Errors: as cs_compact and cs_mrs_conv2d, plus CS_ERR_WORKSPACE.
  */
-int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, const uint8_t* kid,
-              int d_out, int n, const void* bias, void* y, void* ws, size_t ws_bytes, void* stream);
+int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* aug, int d_out, int n,
+              const void* bias, void* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * cs_conv2d - a whole sparse-sparse conv layer: cs_compact of the b*h*w input
@@ -154,8 +167,8 @@ int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, 
  * least cs_workspace_bytes(1, xt, b*h*w, c_in) bytes.
  */
 int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
-              int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
-              const void* bias, int pool, void* y, void* ws, size_t ws_bytes, void* stream);
+              int stride, int pad, const void* aug, int c_out, int n, const void* bias, int pool,
+              void* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
@@ -168,8 +181,8 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
  * * c_in <= 64 values.
  */
 int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
-                    int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
-                    const void* bias, int pool, void* y, void* stream);
+                    int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                    int pool, void* y, void* stream);
 
 /*
  * cs_kwta - k-WTA (Section 2.2.2: exactly the top k activations propagate;

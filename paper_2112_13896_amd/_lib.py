@@ -28,14 +28,14 @@ CS_MAX_KWTA_ROW = 2048
 _c = ctypes
 _vp, _i, _i64, _sz = _c.c_void_p, _c.c_int, _c.c_int64, _c.c_size_t
 SIGNATURES = {
-    "cs_pack": (_i, [_i, _vp, _i, _i, _i, _vp, _vp, _c.POINTER(_i64), _c.POINTER(_i), _c.POINTER(_i)]),
+    "cs_pack": (_i, [_i, _vp, _i, _i, _i, _vp, _c.POINTER(_i64), _c.POINTER(_i), _c.POINTER(_i)]),
     "cs_compact": (_i, [_i, _vp, _i64, _i, _vp, _vp, _vp, _vp]),
-    "cs_mrs_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i,
+    "cs_mrs_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
                            _vp, _i, _vp, _vp]),
-    "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
-    "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _vp,
+    "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
+    "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i, _vp, _vp,
                        _sz, _vp]),
-    "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp, _i,
+    "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                              _vp, _vp]),
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),
     "cs_kwta_lists": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp]),

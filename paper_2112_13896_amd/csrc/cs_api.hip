@@ -110,8 +110,8 @@ constexpr size_t kCuLds = 160 * 1024;     // LDS of one compute unit (gfx950)
 // global memory.  Used when the lists cannot be read four entries at a time
 // (row stride not a multiple of 4) or a table slice cannot fit in LDS.
 int mrs_launch_simple(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
-                      const cs::ConvGeom& geo, const void* val, const uint8_t* kid,
-                      const void* bias, void* y, hipStream_t stream) {
+                      const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
+                      hipStream_t stream) {
   const int64_t opix = (int64_t)geo.B * (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
   const int64_t total = opix * geo.G;
   const bool one = geo.n == 1;
@@ -124,54 +124,55 @@ int mrs_launch_simple(cs_dtype xt, const uint16_t* idx, const void* lval, const 
   const dim3 grid((unsigned)nblocks), block(bd);
   if (xt == CS_I8) {
     auto* lv = static_cast<const int8_t*>(lval);
-    auto* pv = static_cast<const int8_t*>(val);
+    auto* pa = static_cast<const uint16_t*>(aug);
     auto* bs = static_cast<const int32_t*>(bias);
     auto* yy = static_cast<int32_t*>(y);
     if (one)
       hipLaunchKernelGGL((cs::mrs_conv<int8_t, int32_t, true>), grid, block, shmem, stream, idx,
-                         lv, cnt, pv, kid, bs, yy, geo, total);
+                         lv, cnt, pa, bs, yy, geo, total);
     else
       hipLaunchKernelGGL((cs::mrs_conv<int8_t, int32_t, false>), grid, block, shmem, stream, idx,
-                         lv, cnt, pv, kid, bs, yy, geo, total);
+                         lv, cnt, pa, bs, yy, geo, total);
   } else {
     auto* lv = static_cast<const float*>(lval);
-    auto* pv = static_cast<const float*>(val);
+    auto* pa = static_cast<const uint2*>(aug);
     auto* bs = static_cast<const float*>(bias);
     auto* yy = static_cast<float*>(y);
     if (one)
       hipLaunchKernelGGL((cs::mrs_conv<float, float, true>), grid, block, shmem, stream, idx, lv,
-                         cnt, pv, kid, bs, yy, geo, total);
+                         cnt, pa, bs, yy, geo, total);
     else
       hipLaunchKernelGGL((cs::mrs_conv<float, float, false>), grid, block, shmem, stream, idx,
-                         lv, cnt, pv, kid, bs, yy, geo, total);
+                         lv, cnt, pa, bs, yy, geo, total);
   }
   return launch_status();
 }
 
 template <typename T, typename A, bool ONE, int GB>
 void launch_tiled(dim3 grid, size_t shmem, hipStream_t stream, const uint16_t* idx,
-                  const void* lval, const int32_t* cnt, const void* val, const uint8_t* kid,
-                  const void* bias, void* y, const cs::ConvGeom& geo, const cs::TiledArgs& ta) {
+                  const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                  void* y, const cs::ConvGeom& geo, const cs::TiledArgs& ta) {
   hipLaunchKernelGGL((cs::mrs_tiled<T, A, ONE, GB>), grid, dim3(cs::MRS_BD), shmem, stream, idx,
-                     static_cast<const T*>(lval), cnt, static_cast<const T*>(val), kid,
+                     static_cast<const T*>(lval), cnt,
+                     static_cast<const typename cs::Aug<T>::type*>(aug),
                      static_cast<const A*>(bias), static_cast<A*>(y), geo, ta);
 }
 
 template <typename T, typename A>
 void launch_tiled_any(bool one, int gb, dim3 grid, size_t shmem, hipStream_t stream,
-                      const uint16_t* idx, const void* lval, const int32_t* cnt, const void* val,
-                      const uint8_t* kid, const void* bias, void* y, const cs::ConvGeom& geo,
+                      const uint16_t* idx, const void* lval, const int32_t* cnt, const void* aug,
+                      const void* bias, void* y, const cs::ConvGeom& geo,
                       const cs::TiledArgs& ta) {
   if (one) {
     if (gb == 2)
-      launch_tiled<T, A, true, 2>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+      launch_tiled<T, A, true, 2>(grid, shmem, stream, idx, lval, cnt, aug, bias, y, geo, ta);
     else
-      launch_tiled<T, A, true, 1>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+      launch_tiled<T, A, true, 1>(grid, shmem, stream, idx, lval, cnt, aug, bias, y, geo, ta);
   } else {
     if (gb == 2)
-      launch_tiled<T, A, false, 2>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+      launch_tiled<T, A, false, 2>(grid, shmem, stream, idx, lval, cnt, aug, bias, y, geo, ta);
     else
-      launch_tiled<T, A, false, 1>(grid, shmem, stream, idx, lval, cnt, val, kid, bias, y, geo, ta);
+      launch_tiled<T, A, false, 1>(grid, shmem, stream, idx, lval, cnt, aug, bias, y, geo, ta);
   }
 }
 
@@ -189,13 +190,13 @@ int table_slice(const cs::ConvGeom& geo, size_t esz, int nacc, int gb) {
 }
 
 int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
-               const cs::ConvGeom& geo, const void* val, const uint8_t* kid, const void* bias,
-               void* y, hipStream_t stream) {
+               const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
+               hipStream_t stream) {
   const bool one = geo.n == 1;
   const int nacc = one ? 1 : geo.n;
   const int T = geo.KH * geo.KW;
   const int64_t R = (int64_t)T * geo.C;
-  const size_t esz = xt == CS_I8 ? (one ? 1 : 2) : (one ? 4 : 8);
+  const size_t esz = xt == CS_I8 ? 2 : 8;               // augmented entry bytes
   // two sets per lane when they split evenly and fit; else one
   int gb = 2;
   int Gs = geo.G % 2 == 0 ? table_slice(geo, esz, nacc, 2) : 0;
@@ -216,13 +217,15 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   const bool fits32 = in_rows * geo.cap < INT32_MAX && items * geo.c_out < INT32_MAX &&
                       R * geo.G < INT32_MAX && items * geo.G * 64 < INT32_MAX;
   if (geo.cap % 4 != 0 || Gs < 1 || log2S + ta.log2Q > 6 || !fits32)
-    return mrs_launch_simple(xt, idx, lval, cnt, geo, val, kid, bias, y, stream);
+    return mrs_launch_simple(xt, idx, lval, cnt, geo, aug, bias, y, stream);
   int cus = 0;
   const int st = device_cus(&cus);
   if (st != CS_OK) return st;
   ta.Gs = Gs;
   ta.gslices = geo.G / Gs;
   ta.items = (int)items;
+  ta.vec_stage = ta.gslices == 1 && (R * Gs * esz) % 16 == 0 &&
+                 reinterpret_cast<uintptr_t>(aug) % 16 == 0;
   ta.fd_gs = cs::make_fastdiv((uint32_t)Gs);
   ta.fd_units = cs::make_fastdiv((uint32_t)(Gs / gb));
   ta.fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / geo.pool));
@@ -249,11 +252,11 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   if (blocks_per_slice < 1) blocks_per_slice = 1;
   const dim3 grid((unsigned)(blocks_per_slice * ta.gslices));
   if (xt == CS_I8)
-    launch_tiled_any<int8_t, int32_t>(one, gb, grid, shmem, stream, idx, lval, cnt, val, kid,
-                                      bias, y, geo, ta);
+    launch_tiled_any<int8_t, int32_t>(one, gb, grid, shmem, stream, idx, lval, cnt, aug, bias,
+                                      y, geo, ta);
   else
-    launch_tiled_any<float, float>(one, gb, grid, shmem, stream, idx, lval, cnt, val, kid, bias,
-                                   y, geo, ta);
+    launch_tiled_any<float, float>(one, gb, grid, shmem, stream, idx, lval, cnt, aug, bias, y,
+                                   geo, ta);
   return launch_status();
 }
 
@@ -323,26 +326,26 @@ int cs_compact(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, v
 
 int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt, int cap,
                   int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
-                  const void* val, const uint8_t* kid, int c_out, int n, const void* bias,
-                  int pool, void* y, void* stream) {
+                  const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                  void* stream) {
   if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
   cs::ConvGeom geo;
   const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
   if (st != CS_OK) return st;
   if (cap < 1) return CS_ERR_SHAPE;
-  if (!idx || !lval || !cnt || !val || !kid || !y) return CS_ERR_ARG;
+  if (!idx || !lval || !cnt || !aug || !y) return CS_ERR_ARG;
   geo.cap = cap;
-  return mrs_launch(xt, idx, lval, cnt, geo, val, kid, bias, y, static_cast<hipStream_t>(stream));
+  return mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, static_cast<hipStream_t>(stream));
 }
 
 int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
-              int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
-              const void* bias, int pool, void* y, void* ws, size_t ws_bytes, void* stream) {
+              int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+              int pool, void* y, void* ws, size_t ws_bytes, void* stream) {
   if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
   cs::ConvGeom geo;
   const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
   if (st != CS_OK) return st;
-  if (!x || !val || !kid || !y) return CS_ERR_ARG;
+  if (!x || !aug || !y) return CS_ERR_ARG;
   const int64_t rows = (int64_t)b * h * w;
   const WsLayout l = ws_layout(xt, rows, c_in);
   if (!ws || ws_bytes < l.total) return CS_ERR_WORKSPACE;
@@ -354,17 +357,17 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
   const hipStream_t s = static_cast<hipStream_t>(stream);
   int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
   if (r != CS_OK) return r;
-  return mrs_launch(xt, idx, lv, cnt, geo, val, kid, bias, y, s);
+  return mrs_launch(xt, idx, lv, cnt, geo, aug, bias, y, s);
 }
 
 int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
-                    int stride, int pad, const void* val, const uint8_t* kid, int c_out, int n,
-                    const void* bias, int pool, void* y, void* stream) {
+                    int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                    int pool, void* y, void* stream) {
   if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
   cs::ConvGeom geo;
   const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
   if (st != CS_OK) return st;
-  if (!x || !val || !kid || !y) return CS_ERR_ARG;
+  if (!x || !aug || !y) return CS_ERR_ARG;
   const int R = kh * kw * c_in;
   const int ph = (pool - 1) * stride + kh, pw = (pool - 1) * stride + kw;
   if (n != 1 || c_out != 64 || R > 32 || (int64_t)ph * pw * c_in > 64) return CS_ERR_SHAPE;
@@ -383,7 +386,7 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
   const bool gsc = kh == 5 && kw == 5 && c_in == 1 && stride == 1 && pool == 2;
   if (xt == CS_I8) {
     auto* xx = static_cast<const int8_t*>(x);
-    auto* pv = static_cast<const int8_t*>(val);
+    auto* pv = static_cast<const uint16_t*>(aug);
     auto* bs = static_cast<const int32_t*>(bias);
     auto* yy = static_cast<int32_t*>(y);
     if (gsc)
@@ -394,7 +397,7 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
                          pv, bs, yy, geo, items, fd_wp, fd_hp);
   } else {
     auto* xx = static_cast<const float*>(x);
-    auto* pv = static_cast<const float*>(val);
+    auto* pv = static_cast<const uint2*>(aug);
     auto* bs = static_cast<const float*>(bias);
     auto* yy = static_cast<float*>(y);
     if (gsc)
@@ -407,11 +410,10 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
   return launch_status();
 }
 
-int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* val, const uint8_t* kid,
-              int d_out, int n, const void* bias, void* y, void* ws, size_t ws_bytes,
-              void* stream) {
-  return cs_conv2d(xt, x, batch, 1, 1, d_in, 1, 1, 1, 0, val, kid, d_out, n, bias, 1, y, ws,
-                   ws_bytes, stream);
+int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* aug, int d_out, int n,
+              const void* bias, void* y, void* ws, size_t ws_bytes, void* stream) {
+  return cs_conv2d(xt, x, batch, 1, 1, d_in, 1, 1, 1, 0, aug, d_out, n, bias, 1, y, ws, ws_bytes,
+                   stream);
 }
 
 int cs_kwta(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dtype ot, int shift,

@@ -10,9 +10,17 @@
 
 namespace {
 
-template <typename T>
-int pack_impl(const T* w, int d_out, int r, int n, T* val, uint8_t* kid, int64_t* holes,
-              int* bad_g, int* bad_i) {
+inline void put(uint16_t* aug, int64_t s, int8_t v, int kid) {
+  aug[s] = (uint16_t)((uint8_t)v | ((uint16_t)kid << 8));
+}
+inline void put(cs_aug_f32* aug, int64_t s, float v, int kid) {
+  aug[s].value = v;
+  aug[s].kid = (uint32_t)kid;
+}
+
+template <typename T, typename E>
+int pack_impl(const T* w, int d_out, int r, int n, E* aug, int64_t* holes, int* bad_g,
+              int* bad_i) {
   const int G = d_out / n;
   int64_t nholes = 0;
   for (int g = 0; g < G; ++g) {
@@ -31,12 +39,10 @@ int pack_impl(const T* w, int d_out, int r, int n, T* val, uint8_t* kid, int64_t
       }
       const int64_t s = (int64_t)i * G + g;
       if (owner < 0) {
-        val[s] = T(0);
-        kid[s] = 0;
+        put(aug, s, T(0), 0);
         ++nholes;
       } else {
-        val[s] = w[(int64_t)(g * n + owner) * r + i];
-        kid[s] = (uint8_t)owner;
+        put(aug, s, w[(int64_t)(g * n + owner) * r + i], owner);
       }
     }
   }
@@ -46,19 +52,19 @@ int pack_impl(const T* w, int d_out, int r, int n, T* val, uint8_t* kid, int64_t
 
 }  // namespace
 
-extern "C" int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* val,
-                       uint8_t* kid, int64_t* holes, int* bad_g, int* bad_i) {
+extern "C" int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void* aug,
+                       int64_t* holes, int* bad_g, int* bad_i) {
   if (bad_g) *bad_g = -1;
   if (bad_i) *bad_i = -1;
   if (holes) *holes = 0;
-  if (!w || !val || !kid || d_out < 1 || r < 1 || n < 1) return CS_ERR_ARG;
+  if (!w || !aug || d_out < 1 || r < 1 || n < 1) return CS_ERR_ARG;
   if (n > CS_MAX_N || d_out % n != 0) return CS_ERR_SHAPE;
   switch (wt) {
     case CS_I8:
-      return pack_impl(static_cast<const int8_t*>(w), d_out, r, n, static_cast<int8_t*>(val), kid,
+      return pack_impl(static_cast<const int8_t*>(w), d_out, r, n, static_cast<uint16_t*>(aug),
                        holes, bad_g, bad_i);
     case CS_F32:
-      return pack_impl(static_cast<const float*>(w), d_out, r, n, static_cast<float*>(val), kid,
+      return pack_impl(static_cast<const float*>(w), d_out, r, n, static_cast<cs_aug_f32*>(aug),
                        holes, bad_g, bad_i);
     default:
       return CS_ERR_DTYPE;

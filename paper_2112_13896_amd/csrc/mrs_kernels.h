@@ -36,6 +36,23 @@ struct ConvGeom {
   int cap;                 // list row stride
 };
 
+// Entry of the augmented packed tensor (Section 3.3.1): value + Kernel ID.
+// int8: one 16-bit word (uint8 value | kid << 8); fp32: (value bits, kid).
+template <typename T>
+struct Aug;
+template <>
+struct Aug<int8_t> {
+  using type = uint16_t;
+  static __device__ __forceinline__ int32_t value(uint16_t e) { return (int32_t)(int8_t)(e & 0xFFu); }
+  static __device__ __forceinline__ int kid(uint16_t e) { return (int)(e >> 8); }
+};
+template <>
+struct Aug<float> {
+  using type = uint2;
+  static __device__ __forceinline__ float value(uint2 e) { return __uint_as_float(e.x); }
+  static __device__ __forceinline__ int kid(uint2 e) { return (int)e.y; }
+};
+
 template <typename A>
 __device__ __forceinline__ void route_add(A* p, A v);
 
@@ -54,8 +71,7 @@ template <typename T, typename A, bool ONE>
 __global__ __launch_bounds__(256) void mrs_conv(const uint16_t* __restrict__ lidx,
                                                 const T* __restrict__ lval,
                                                 const int32_t* __restrict__ lcnt,
-                                                const T* __restrict__ pval,
-                                                const uint8_t* __restrict__ pkid,
+                                                const typename Aug<T>::type* __restrict__ aug,
                                                 const A* __restrict__ bias, A* __restrict__ y,
                                                 ConvGeom geo, int64_t total) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -99,11 +115,12 @@ __global__ __launch_bounds__(256) void mrs_conv(const uint16_t* __restrict__ lid
         const int64_t sbase = (int64_t)(ky * geo.KW + kx) * geo.C;
         for (int j = 0; j < m; ++j) {
           const int64_t i = sbase + li[j];
-          const A prod = (A)lv[j] * (A)pval[i * G + g];      // Multiply
+          const auto e = aug[i * G + g];
+          const A prod = (A)lv[j] * (A)Aug<T>::value(e);       // Multiply
           if (ONE) {
             accr += prod;                                       // Sum
           } else {
-            route_add<A>(&acc[(int)pkid[i * G + g] * bd + tid], prod);  // Route + Sum
+            route_add<A>(&acc[Aug<T>::kid(e) * bd + tid], prod);  // Route + Sum
           }
         }
       }

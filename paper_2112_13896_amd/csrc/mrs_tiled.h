@@ -36,16 +36,11 @@ constexpr int MRS_AHEAD = 2;    // taps prefetched ahead of the one being proces
 constexpr int MRS_STAGE = 16;   // table entries a lane loads per batch while staging
 constexpr int MRS_CHUNKS = 4;   // list chunks loaded together in single-tap layers
 
+// The staged table keeps the global augmented entries unchanged (a copy).
 template <typename T, bool ONE>
-struct TabEntry;
-template <>
-struct TabEntry<int8_t, false> { using type = uint16_t; };
-template <>
-struct TabEntry<int8_t, true> { using type = int8_t; };
-template <>
-struct TabEntry<float, false> { using type = uint2; };        // x: value bits, y: acc byte offset
-template <>
-struct TabEntry<float, true> { using type = float; };
+struct TabEntry {
+  using type = typename Aug<T>::type;
+};
 
 struct TiledArgs {
   int S, log2S;      // slices per (item, set, sub-pixel), power of two
@@ -54,6 +49,7 @@ struct TiledArgs {
   int gslices;       // number of table slices; gridDim.x is a multiple of it
   int chunk_mode;    // 1: a single tap, slices split its list chunks
   int items;         // output items (pooled pixels when pooling)
+  int vec_stage;     // 1: one slice, table bytes a multiple of 16, 16-byte aligned
   FastDiv fd_gs;     // / Gs
   FastDiv fd_units;  // / (Gs / sets per lane)
   FastDiv fd_wp;     // / pooled output width
@@ -105,10 +101,11 @@ struct __attribute__((aligned(GB * sizeof(typename TabEntry<T, ONE>::type)))) Ta
 // One 4-entry chunk of a list against the lane's GB sets.  All table reads of
 // the chunk are issued before any is used; tail entries beyond the list
 // (e >= lim) read row 0 and contribute a zero product, so there is no branch.
+// The accumulator of (set j of the lane, kid) is acc[(j*n + kid)][lane].
 template <typename T, typename A, bool ONE, int GB>
 __device__ __forceinline__ void mrs_chunk(const Chunk<T>& ch, int lim,
                                           const unsigned char* tbase, uint32_t row_bytes,
-                                          A* acc_lane, A (&accr)[GB]) {
+                                          int n, A* acc_lane, A (&accr)[GB]) {
   using V = TabVec<T, ONE, GB>;
   V tv[4];
   A xv[4];
@@ -123,14 +120,14 @@ __device__ __forceinline__ void mrs_chunk(const Chunk<T>& ch, int lim,
   for (int e = 0; e < 4; ++e) {
     if constexpr (ONE) {
 #pragma unroll
-      for (int j = 0; j < GB; ++j) accr[j] += xv[e] * (A)tv[e].e[j];      // Sum
+      for (int j = 0; j < GB; ++j) accr[j] += xv[e] * (A)Aug<T>::value(tv[e].e[j]);   // Sum
     } else if constexpr (sizeof(T) == 1) {
 #pragma unroll
       for (int j = 0; j < GB; ++j) {
-        // Route + Sum: the entry's high byte is the accumulator (set j, kernel id)
+        // Route + Sum: LDS integer atomic into the entry's accumulator
         const auto te = tv[e].e[j];
-        __hip_atomic_fetch_add(acc_lane + (int)(te >> 8) * MRS_BD,
-                               xv[e] * (int32_t)(int8_t)(te & 0xFFu), __ATOMIC_RELAXED,
+        __hip_atomic_fetch_add(acc_lane + (Aug<T>::kid(te) + j * n) * MRS_BD,
+                               xv[e] * Aug<T>::value(te), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_WORKGROUP);
       }
     } else {
@@ -140,11 +137,11 @@ __device__ __forceinline__ void mrs_chunk(const Chunk<T>& ch, int lim,
       A a[GB];
 #pragma unroll
       for (int j = 0; j < GB; ++j) {
-        p[j] = reinterpret_cast<A*>(reinterpret_cast<unsigned char*>(acc_lane) + tv[e].e[j].y);
+        p[j] = acc_lane + (Aug<T>::kid(tv[e].e[j]) + j * n) * MRS_BD;
         a[j] = *p[j];
       }
 #pragma unroll
-      for (int j = 0; j < GB; ++j) *p[j] = a[j] + xv[e] * __uint_as_float(tv[e].e[j].x);
+      for (int j = 0; j < GB; ++j) *p[j] = a[j] + xv[e] * Aug<T>::value(tv[e].e[j]);
     }
   }
 }
@@ -153,8 +150,7 @@ template <typename T, typename A, bool ONE, int GB>
 __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__ lidx,
                                                     const T* __restrict__ lval,
                                                     const int32_t* __restrict__ lcnt,
-                                                    const T* __restrict__ pval,
-                                                    const uint8_t* __restrict__ pkid,
+                                                    const typename Aug<T>::type* __restrict__ aug,
                                                     const A* __restrict__ bias,
                                                     A* __restrict__ y, ConvGeom geo,
                                                     TiledArgs ta) {
@@ -176,37 +172,42 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
   unsigned char* tab = smem + (size_t)GB * n * MRS_BD * sizeof(A);
   const uint32_t row_bytes = (uint32_t)(gcount * sizeof(E));
 
-  // stage the augmented table of sets [g0, g0 + gcount): row i, column gl.
-  // Loads go out in batches of MRS_STAGE per lane so their latencies overlap.
+  // stage the augmented table of sets [g0, g0 + gcount): a copy of the rows'
+  // slices, loads in batches of MRS_STAGE per lane so their latencies overlap
   const int total = R * gcount;
-  for (int base = 0; base < total; base += MRS_BD * MRS_STAGE) {
-    T wv[MRS_STAGE];
-    uint8_t kv[MRS_STAGE];
+  if (ta.vec_stage) {
+    // the whole table, contiguous: 16-byte copies
+    const uint4* src4 = reinterpret_cast<const uint4*>(aug);
+    uint4* dst4 = reinterpret_cast<uint4*>(tab);
+    const int n16 = R * gcount * (int)sizeof(E) / 16;
+    for (int base = 0; base < n16; base += MRS_BD * MRS_STAGE) {
+      uint4 v[MRS_STAGE];
 #pragma unroll
-    for (int u = 0; u < MRS_STAGE; ++u) {
-      const int e = base + u * MRS_BD + tid;
-      if (e < total) {
-        const int i = (int)fdiv((uint32_t)e, ta.fd_gs), gl = e - i * gcount;
-        const int src = i * G + g0 + gl;
-        wv[u] = pval[src];
-        kv[u] = ONE ? (uint8_t)0 : pkid[src];
+      for (int u = 0; u < MRS_STAGE; ++u) {
+        const int e = base + u * MRS_BD + tid;
+        if (e < n16) v[u] = src4[e];
+      }
+#pragma unroll
+      for (int u = 0; u < MRS_STAGE; ++u) {
+        const int e = base + u * MRS_BD + tid;
+        if (e < n16) dst4[e] = v[u];
       }
     }
+  } else {
+    for (int base = 0; base < total; base += MRS_BD * MRS_STAGE) {
+      E v[MRS_STAGE];
 #pragma unroll
-    for (int u = 0; u < MRS_STAGE; ++u) {
-      const int e = base + u * MRS_BD + tid;
-      if (e < total) {
-        const int gl = e - (int)fdiv((uint32_t)e, ta.fd_gs) * gcount;
-        E* dst = reinterpret_cast<E*>(tab) + e;
-        const int slot = (gl % GB) * n + (int)kv[u];     // accumulator of the entry
-        if constexpr (ONE) {
-          *dst = wv[u];
-        } else if constexpr (sizeof(T) == 1) {
-          *dst = (uint16_t)((uint8_t)wv[u] | ((uint16_t)slot << 8));
-        } else {
-          *dst = make_uint2(__float_as_uint((float)wv[u]),
-                            (uint32_t)slot * MRS_BD * (uint32_t)sizeof(A));
+      for (int u = 0; u < MRS_STAGE; ++u) {
+        const int e = base + u * MRS_BD + tid;
+        if (e < total) {
+          const int i = (int)fdiv((uint32_t)e, ta.fd_gs), gl = e - i * gcount;
+          v[u] = aug[i * G + g0 + gl];
         }
+      }
+#pragma unroll
+      for (int u = 0; u < MRS_STAGE; ++u) {
+        const int e = base + u * MRS_BD + tid;
+        if (e < total) reinterpret_cast<E*>(tab)[e] = v[u];
       }
     }
   }
@@ -279,29 +280,32 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
           }
         }
       };
-#pragma unroll
-      for (int u = 0; u < MRS_AHEAD; ++u) prefetch(u, u);
       if (ta.chunk_mode) {
-        // one tap: its count and the lane's first MRS_CHUNKS chunks (c0, c0 + S, ...)
-        // go out together; chunks past the row's capacity are not read
-        const int pr = prow[0];
+        // one tap: the count and the lane's first MRS_CHUNKS chunks (c0, c0 + S,
+        // ...) are all issued before any of them is used (one round trip);
+        // chunks past the row's capacity are not read
+        int pr = -1;
+        {
+          const int hy = ho * geo.S - geo.P, wx = wo * geo.S - geo.P;
+          if (hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W) pr = (bb * geo.H + hy) * geo.W + wx;
+        }
         if (pr >= 0) {
           const int off = pr * geo.cap;
           const uint16_t* li = lidx + off;
           const T* lv = lval + off;
+          const int mraw = lcnt[pr];
           Chunk<T> ch[MRS_CHUNKS];
-          ch[0] = first[0];
 #pragma unroll
-          for (int z = 1; z < MRS_CHUNKS; ++z) {
+          for (int z = 0; z < MRS_CHUNKS; ++z) {
             const int j = (c0 + z * cstep) * 4;
             if (j < geo.cap) ch[z].load(li, lv, j);
           }
-          const int m = pcnt[0];
+          const int m = min(mraw, geo.cap);
 #pragma unroll
           for (int z = 0; z < MRS_CHUNKS; ++z) {
             const int cz = c0 + z * cstep;
             if (cz * 4 < m)
-              mrs_chunk<T, A, ONE, GB>(ch[z], m - cz * 4, tcol, row_bytes, acc_lane, accr);
+              mrs_chunk<T, A, ONE, GB>(ch[z], m - cz * 4, tcol, row_bytes, n, acc_lane, accr);
           }
           // the rest of a long list, one chunk ahead
           int c = c0 + MRS_CHUNKS * cstep;
@@ -313,14 +317,16 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
               const bool more = cn * 4 < m;
               Chunk<T> nxt;
               if (more) nxt.load(li, lv, cn * 4);
-              mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tcol, row_bytes, acc_lane, accr);
+              mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tcol, row_bytes, n, acc_lane, accr);
               if (!more) break;
               cur = nxt;
               c = cn;
             }
           }
         }
-      } else
+      } else {
+#pragma unroll
+      for (int u = 0; u < MRS_AHEAD; ++u) prefetch(u, u);
 #pragma unroll
       for (int u = 0; u < MRS_TAPS; ++u) {
         if (u + MRS_AHEAD < MRS_TAPS) prefetch(u + MRS_AHEAD, (u + MRS_AHEAD) % (MRS_AHEAD + 1));
@@ -338,12 +344,13 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
             const bool more = cn * 4 < m;
             Chunk<T> nxt;
             if (more) nxt.load(li, lv, cn * 4);          // next chunk in flight
-            mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tbase, row_bytes, acc_lane, accr);
+            mrs_chunk<T, A, ONE, GB>(cur, m - c * 4, tbase, row_bytes, n, acc_lane, accr);
             if (!more) break;
             cur = nxt;
             c = cn;
           }
         }
+      }
       }
     }
     if (ONE) {
@@ -397,7 +404,7 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
 // operand of the multiply-adds.  Geometry is compile-time.
 template <typename T, typename A, int KH, int KW, int C, int STR, int POOL>
 __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
-                                                     const T* __restrict__ pval,
+                                                     const typename Aug<T>::type* __restrict__ aug,
                                                      const A* __restrict__ bias,
                                                      A* __restrict__ y, ConvGeom geo,
                                                      int items, FastDiv fd_wp, FastDiv fd_hp) {
@@ -410,7 +417,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   A w[R];
 #pragma unroll
-  for (int i = 0; i < R; ++i) w[i] = (A)pval[i * 64 + lane];
+  for (int i = 0; i < R; ++i) w[i] = (A)Aug<T>::value(aug[i * 64 + lane]);
   const A b = bias ? bias[lane] : A(0);
   const int c = lane % C, pp = lane / C, py = pp / PW, px = pp % PW;
   for (int it = (int)wave; it < items; it += (int)nwaves) {
@@ -445,7 +452,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1(const T* __restrict__ x,
 // host checks: n == 1, 64 channels, r <= 32, patch <= 64 values).
 template <typename T, typename A>
 __global__ __launch_bounds__(256) void conv_dense_n1_rt(const T* __restrict__ x,
-                                                        const T* __restrict__ pval,
+                                                        const typename Aug<T>::type* __restrict__ aug,
                                                         const A* __restrict__ bias,
                                                         A* __restrict__ y, ConvGeom geo,
                                                         int items, FastDiv fd_wp, FastDiv fd_hp) {
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(256) void conv_dense_n1_rt(const T* __restrict__ x,
         const int ci = i % geo.C, t = i / geo.C;
         const int src = ((oy + t / geo.KW) * pw + (ox + t % geo.KW)) * geo.C + ci;
         const A xs = __builtin_bit_cast(A, __builtin_amdgcn_readlane(__builtin_bit_cast(int, xv), src));
-        a += xs * (A)pval[i * 64 + lane];
+        a += xs * (A)Aug<T>::value(aug[i * 64 + lane]);
       }
       best = (q == 0 || a > best) ? a : best;
     }

@@ -35,8 +35,7 @@ from .ops import conv_out
 @dataclass
 class PackedLayer:
     spec: object
-    val: torch.Tensor        # [r][G] device
-    kid: torch.Tensor        # [r][G] uint8 device
+    aug: torch.Tensor        # augmented packed tensor [r][G] on the device
     bias: torch.Tensor | None
     holes: int
 
@@ -82,10 +81,9 @@ class Network:
         self.packed = []
         for spec, W, b in zip(self.layers, weights, biases):
             W2 = np.asarray(W).reshape(spec.c_out, -1)
-            val, kid, holes = ops.pack(W2, spec.n)
+            aug, holes = ops.pack(W2, spec.n)
             bias = None if b is None else torch.from_numpy(np.asarray(b)).to(self.device)
-            self.packed.append(PackedLayer(spec, torch.from_numpy(val).to(self.device),
-                                           torch.from_numpy(kid).to(self.device), bias, holes))
+            self.packed.append(PackedLayer(spec, ops.aug_to_device(aug, self.device), bias, holes))
         self._plan()
         self.bufs = self.make_buffers()
 
@@ -141,7 +139,7 @@ class Network:
         B = Buffers()
         for p, pl in zip(self.packed, self.plans):
             s = p.spec
-            dt = p.val.dtype
+            dt = torch.int8 if p.aug.dtype == torch.int16 else torch.float32
             acc_dt = torch.int32 if dt == torch.int8 else torch.float32
             b, h, w, c = pl.geo
             rows = b * h * w
@@ -185,7 +183,7 @@ class Network:
         if pl.dense_kernel:
             # sparse-dense variant: dense activations, no compaction
             t.start(f"{s.name}.mrs")
-            ops.conv2d_dense(x, p.val, p.kid, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+            ops.conv2d_dense(x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
                              pl.pool, out=acc)
             t.stop(f"{s.name}.mrs")
         else:
@@ -197,8 +195,8 @@ class Network:
                 t.stop(f"{s.name}.compact")
                 idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
             t.start(f"{s.name}.mrs")
-            ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.val, p.kid, pl.kh, pl.kw, s.n, pl.stride,
-                           pl.pad, p.bias, pl.pool, out=acc4)
+            ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad,
+                           p.bias, pl.pool, out=acc4)
             t.stop(f"{s.name}.mrs")
         if s.k is not None:
             odt = torch.int8 if s.shift is not None else None

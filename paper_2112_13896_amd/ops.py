@@ -44,9 +44,13 @@ def _stream() -> int:
 
 # ------------------------------------------------------------------ pack (host)
 def pack(W: np.ndarray, n: int):
-    """Combine on the host: W [d_out][r] (int8 or float32) -> (val [r][G],
-    kid [r][G] uint8, holes).  Raises CSError(CS_ERR_COLLISION) with .bad
-    = (g, i) when two kernels of a set share a slot."""
+    """Combine on the host: W [d_out][r] (int8 or float32) -> (aug, holes).
+
+    aug is the augmented packed tensor [r][G] (G = d_out / n): for int8
+    weights a uint16 array, entry = uint8(value) | kid << 8; for float32
+    weights a uint32 array [r][G][2] holding (value bits, kid).  Raises
+    CSError(CS_ERR_COLLISION) with .bad = (g, i) when two kernels of a set
+    share a slot."""
     W = np.ascontiguousarray(W)
     if W.ndim != 2:
         raise ValueError("W must be [d_out][r]")
@@ -55,17 +59,48 @@ def pack(W: np.ndarray, n: int):
     if wt is None:
         raise TypeError(f"unsupported weight dtype {W.dtype}")
     G = d_out // n if n > 0 else 0
-    val = np.zeros((r, max(G, 1)), dtype=W.dtype)
-    kid = np.zeros((r, max(G, 1)), dtype=np.uint8)
+    if wt == CS_I8:
+        aug = np.zeros((r, max(G, 1)), dtype=np.uint16)
+    else:
+        aug = np.zeros((r, max(G, 1), 2), dtype=np.uint32)
     holes = ctypes.c_int64(0)
     bg, bi = ctypes.c_int(0), ctypes.c_int(0)
-    st = lib().cs_pack(wt, W.ctypes.data, d_out, r, n, val.ctypes.data, kid.ctypes.data,
+    st = lib().cs_pack(wt, W.ctypes.data, d_out, r, n, aug.ctypes.data,
                        ctypes.byref(holes), ctypes.byref(bg), ctypes.byref(bi))
     if st != _lib.CS_OK:
         err = _lib.CSError("cs_pack", st)
         err.bad = (bg.value, bi.value)
         raise err
-    return val, kid, int(holes.value)
+    return aug, int(holes.value)
+
+
+def unpack_aug(aug: np.ndarray):
+    """Split a host augmented tensor into (values [r][G], kernel IDs [r][G])."""
+    if aug.dtype == np.uint16:
+        return (aug & 0xFF).astype(np.uint8).view(np.int8), (aug >> 8).astype(np.int64)
+    if aug.dtype == np.uint32 and aug.ndim == 3 and aug.shape[2] == 2:
+        return aug[..., 0].copy().view(np.float32), aug[..., 1].astype(np.int64)
+    raise TypeError("not an augmented tensor")
+
+
+def aug_to_device(aug: np.ndarray, device="cuda") -> torch.Tensor:
+    """Upload an augmented tensor: int16 [r][G] (int8 weights) or int32
+    [r][G][2] (float32 weights), bit patterns unchanged."""
+    if aug.dtype == np.uint16:
+        return torch.from_numpy(aug.view(np.int16)).to(device)
+    if aug.dtype == np.uint32:
+        return torch.from_numpy(aug.view(np.int32)).to(device)
+    raise TypeError("not an augmented tensor")
+
+
+def _aug(aug: torch.Tensor, xdt: torch.dtype, n: int):
+    """Device pointer and c_out of an augmented tensor that matches activations of dtype xdt."""
+    ok = (xdt == torch.int8 and aug.dtype == torch.int16 and aug.dim() == 2) or \
+         (xdt == torch.float32 and aug.dtype == torch.int32 and aug.dim() == 3 and
+          aug.shape[2] == 2)
+    if not ok:
+        raise TypeError(f"augmented tensor {aug.dtype}{tuple(aug.shape)} does not match {xdt}")
+    return _dev(aug, "aug"), aug.shape[1] * n
 
 
 # ------------------------------------------------------------------ device ops
@@ -98,19 +133,19 @@ def conv_out(h: int, k: int, stride: int, pad: int) -> int:
     return (h + 2 * pad - k) // stride + 1
 
 
-def mrs_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, val, kid,
+def mrs_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, aug,
                kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None, pool: int = 1,
                out: torch.Tensor | None = None) -> torch.Tensor:
     """Multiply/route/sum on compacted lists of the b*h*w input pixels."""
     b, h, w, c_in = in_shape
-    c_out = val.shape[1] * n
+    pa, c_out = _aug(aug, lval.dtype, n)
     ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
     ydt = torch.int32 if lval.dtype == torch.int8 else torch.float32
     if out is None:
         out = torch.empty((b, ho // pool, wo // pool, c_out), dtype=ydt, device=lval.device)
     check("cs_mrs_conv2d", lib().cs_mrs_conv2d(
         _dt(lval), _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
-        b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"), _dev(kid, "kid"), c_out, n,
+        b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n,
         _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
     return out
 
@@ -126,14 +161,14 @@ def workspace(op: int, dtype: torch.dtype, rows: int, c_in: int, device) -> torc
     return torch.empty((nbytes,), dtype=torch.uint8, device=device)
 
 
-def conv2d(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: int, n: int,
+def conv2d(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
            stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
            ws: torch.Tensor | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
-    """Sparse-sparse conv of NHWC x with packed OHWI kernels (val/kid [kh*kw*c_in][G])."""
+    """Sparse-sparse conv of NHWC x with packed OHWI kernels (aug [kh*kw*c_in][G])."""
     if x.dim() != 4:
         raise ValueError("x must be NHWC")
     b, h, w, c_in = x.shape
-    c_out = val.shape[1] * n
+    pa, c_out = _aug(aug, x.dtype, n)
     ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
     ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
     if out is None:
@@ -142,13 +177,12 @@ def conv2d(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: i
     if ws is None:
         ws = workspace(1, x.dtype, b * h * w, c_in, x.device)
     check("cs_conv2d", lib().cs_conv2d(
-        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"),
-        _dev(kid, "kid"), c_out, n, _opt(bias, "bias"), pool, _dev(out, "out"), _dev(ws, "ws"),
-        ws.numel(), _stream()))
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n,
+        _opt(bias, "bias"), pool, _dev(out, "out"), _dev(ws, "ws"), ws.numel(), _stream()))
     return out
 
 
-def conv2d_dense(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int, kw: int, n: int,
+def conv2d_dense(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
                  stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
                  out: torch.Tensor | None = None) -> torch.Tensor:
     """Sparse-dense conv (dense NHWC input, no compaction); see cs_conv2d_dense for the
@@ -156,33 +190,33 @@ def conv2d_dense(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, kh: int,
     if x.dim() != 4:
         raise ValueError("x must be NHWC")
     b, h, w, c_in = x.shape
-    c_out = val.shape[1] * n
+    pa, c_out = _aug(aug, x.dtype, n)
     ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
     ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
     if out is None:
         out = torch.empty((b, max(ho, 0) // pool, max(wo, 0) // pool, c_out), dtype=ydt,
                           device=x.device)
     check("cs_conv2d_dense", lib().cs_conv2d_dense(
-        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, _dev(val, "val"),
-        _dev(kid, "kid"), c_out, n, _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n,
+        _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
     return out
 
 
-def linear(x: torch.Tensor, val: torch.Tensor, kid: torch.Tensor, n: int,
+def linear(x: torch.Tensor, aug: torch.Tensor, n: int,
            bias: torch.Tensor | None = None, ws: torch.Tensor | None = None,
            out: torch.Tensor | None = None) -> torch.Tensor:
-    """Sparse-sparse linear layer: x [batch][d_in], packed val/kid [d_in][G]."""
+    """Sparse-sparse linear layer: x [batch][d_in], packed aug [d_in][G]."""
     if x.dim() != 2:
         raise ValueError("x must be [batch][d_in]")
     batch, d_in = x.shape
-    d_out = val.shape[1] * n
+    pa, d_out = _aug(aug, x.dtype, n)
     ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
     if out is None:
         out = torch.empty((batch, d_out), dtype=ydt, device=x.device)
     if ws is None:
         ws = workspace(0, x.dtype, batch, d_in, x.device)
     check("cs_linear", lib().cs_linear(
-        _dt(x), _dev(x, "x"), batch, d_in, _dev(val, "val"), _dev(kid, "kid"), d_out, n,
+        _dt(x), _dev(x, "x"), batch, d_in, pa, d_out, n,
         _opt(bias, "bias"), _dev(out, "out"), _dev(ws, "ws"), ws.numel(), _stream()))
     return out
 

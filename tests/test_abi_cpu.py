@@ -63,10 +63,20 @@ def test_pack_matches_oracle(dtype):
                         W[g * n + j, i] = r.integers(1, 100)
         else:
             W = complementary_weights(r, r, d_out, R, n, "int8" if dtype == "int8" else "normal")
-        val, kid, holes = ops.pack(W, n)
+        aug, holes = ops.pack(W, n)
         v2, k2, h2 = o.pack(W, n)
-        assert val.dtype == W.dtype
-        assert np.array_equal(val, v2) and np.array_equal(kid, k2) and holes == h2
+        assert holes == h2
+        # augmented entry layout: int8 -> uint8(value) | kid << 8; fp32 -> (value bits, kid)
+        if W.dtype == np.int8:
+            assert aug.dtype == np.uint16
+            want = v2.view(np.uint8).astype(np.uint16) | (k2.astype(np.uint16) << 8)
+            assert np.array_equal(aug, want)
+        else:
+            assert aug.dtype == np.uint32 and aug.shape == v2.shape + (2,)
+            assert np.array_equal(aug[..., 0], v2.astype(np.float32).view(np.uint32))
+            assert np.array_equal(aug[..., 1], k2.astype(np.uint32))
+        val, kid = ops.unpack_aug(aug)
+        assert np.array_equal(val, v2) and np.array_equal(kid, k2)
 
 
 def test_pack_collision_reports_first_offender():
@@ -85,15 +95,15 @@ def test_pack_collision_reports_first_offender():
 
 def test_pack_argument_errors(L):
     w = np.ones((4, 4), dtype=np.int8)
-    out = np.zeros(64, dtype=np.int8)
-    k = np.zeros(64, dtype=np.uint8)
+    out = np.zeros(64, dtype=np.uint16)
     p = lambda *a: L.cs_pack(*a)  # noqa: E731
-    assert p(CS_I8, None, 4, 4, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
-    assert p(CS_I8, w.ctypes.data, 4, 4, 3, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_SHAPE
-    assert p(CS_I8, w.ctypes.data, 4, 4, 0, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
-    assert p(CS_I32, w.ctypes.data, 4, 4, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_DTYPE
-    assert p(CS_I8, w.ctypes.data, 64, 4, 64, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_SHAPE
-    assert p(CS_I8, w.ctypes.data, 4, 0, 2, out.ctypes.data, k.ctypes.data, None, None, None) == CS_ERR_ARG
+    assert p(CS_I8, None, 4, 4, 2, out.ctypes.data, None, None, None) == CS_ERR_ARG
+    assert p(CS_I8, w.ctypes.data, 4, 4, 2, None, None, None, None) == CS_ERR_ARG
+    assert p(CS_I8, w.ctypes.data, 4, 4, 3, out.ctypes.data, None, None, None) == CS_ERR_SHAPE
+    assert p(CS_I8, w.ctypes.data, 4, 4, 0, out.ctypes.data, None, None, None) == CS_ERR_ARG
+    assert p(CS_I32, w.ctypes.data, 4, 4, 2, out.ctypes.data, None, None, None) == CS_ERR_DTYPE
+    assert p(CS_I8, w.ctypes.data, 64, 4, 64, out.ctypes.data, None, None, None) == CS_ERR_SHAPE
+    assert p(CS_I8, w.ctypes.data, 4, 0, 2, out.ctypes.data, None, None, None) == CS_ERR_ARG
 
 
 def test_compact_validation(L):
@@ -108,8 +118,8 @@ def test_compact_validation(L):
 
 
 def conv_args(**kw):
-    a = dict(xt=CS_I8, x=FAKE, b=2, h=8, w=8, c_in=4, kh=3, kw=3, stride=1, pad=1, val=FAKE,
-             kid=FAKE, c_out=8, n=4, bias=None, pool=1, y=FAKE, ws=FAKE_WS, ws_bytes=1 << 30,
+    a = dict(xt=CS_I8, x=FAKE, b=2, h=8, w=8, c_in=4, kh=3, kw=3, stride=1, pad=1, aug=FAKE,
+             c_out=8, n=4, bias=None, pool=1, y=FAKE, ws=FAKE_WS, ws_bytes=1 << 30,
              stream=None)
     a.update(kw)
     return list(a.values())
@@ -128,7 +138,7 @@ def test_conv2d_validation(L):
     assert f(*conv_args(pool=3)) == CS_ERR_ARG
     assert f(*conv_args(pool=2, h=7, w=7)) == CS_ERR_SHAPE     # odd conv output
     assert f(*conv_args(x=None)) == CS_ERR_ARG
-    assert f(*conv_args(val=None)) == CS_ERR_ARG
+    assert f(*conv_args(aug=None)) == CS_ERR_ARG
     assert f(*conv_args(y=None)) == CS_ERR_ARG
     need = L.cs_workspace_bytes(1, CS_I8, 2 * 8 * 8, 4)
     assert f(*conv_args(ws_bytes=need - 1)) == CS_ERR_WORKSPACE
@@ -138,8 +148,8 @@ def test_conv2d_validation(L):
 
 def test_conv2d_dense_validation(L):
     f = L.cs_conv2d_dense
-    ok = dict(xt=CS_I8, x=FAKE, b=2, h=32, w=32, c_in=1, kh=5, kw=5, stride=1, pad=0, val=FAKE,
-              kid=FAKE, c_out=64, n=1, bias=None, pool=2, y=FAKE, stream=None)
+    ok = dict(xt=CS_I8, x=FAKE, b=2, h=32, w=32, c_in=1, kh=5, kw=5, stride=1, pad=0, aug=FAKE,
+              c_out=64, n=1, bias=None, pool=2, y=FAKE, stream=None)
 
     def call(**kw):
         a = dict(ok)
@@ -151,24 +161,28 @@ def test_conv2d_dense_validation(L):
     assert call(c_in=2) == CS_ERR_SHAPE           # 50 weights per channel > 32
     assert call(kh=7, kw=7) == CS_ERR_SHAPE
     assert call(x=None) == CS_ERR_ARG
+    assert call(aug=None) == CS_ERR_ARG
     assert call(pool=2, h=33, w=33) == CS_ERR_SHAPE
 
 
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
-    base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, FAKE, 8, 4, None, 1, FAKE, None]
+    base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, 8, 4, None, 1, FAKE, None]
     assert m(*base[:4], 0, *base[5:]) == CS_ERR_SHAPE          # list capacity 0
     bad = list(base)
     bad[1] = None
     assert m(*bad) == CS_ERR_ARG
     bad = list(base)
+    bad[13] = None                                              # no augmented tensor
+    assert m(*bad) == CS_ERR_ARG
+    bad = list(base)
     bad[0] = CS_I32
     assert m(*bad) == CS_ERR_DTYPE
     lin = L.cs_linear
-    assert lin(CS_I8, FAKE, 16, 512, FAKE, FAKE, 64, 7, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_SHAPE
-    assert lin(CS_I8, FAKE, 0, 512, FAKE, FAKE, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
-    assert lin(CS_I8, FAKE, 16, 512, FAKE, FAKE, 64, 8, None, FAKE, FAKE_WS, 10, None) == CS_ERR_WORKSPACE
-    assert lin(CS_F32, FAKE, 16, 512, None, FAKE, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
+    assert lin(CS_I8, FAKE, 16, 512, FAKE, 64, 7, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_SHAPE
+    assert lin(CS_I8, FAKE, 0, 512, FAKE, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
+    assert lin(CS_I8, FAKE, 16, 512, FAKE, 64, 8, None, FAKE, FAKE_WS, 10, None) == CS_ERR_WORKSPACE
+    assert lin(CS_F32, FAKE, 16, 512, None, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
 
 
 def test_kwta_validation(L):

@@ -163,8 +163,8 @@ def test_linear(case, dtype, with_bias):
     if with_bias:
         b = r.integers(-1000, 1001, size=d_out).astype(np.int32) if dtype == "i8" else \
             r.normal(size=d_out).astype(np.float32)
-    val, kid, _ = ops.pack(W, n)
-    y = host(ops.linear(dev(x), dev(val), dev(kid), n, None if b is None else dev(b)))
+    aug, _ = ops.pack(W, n)
+    y = host(ops.linear(dev(x), ops.aug_to_device(aug), n, None if b is None else dev(b)))
     ref = o.linear(x, W, b)
     if dtype == "i8":
         assert y.dtype == np.int32 and np.array_equal(y.astype(np.int64), ref)
@@ -202,8 +202,8 @@ def test_conv2d(case, dtype):
                         "u_m127_127" if dtype == "i8" else "absnormal").reshape(b, h, w, c_in)
     bias = (r.integers(-1000, 1001, size=c_out).astype(np.int32) if dtype == "i8"
             else r.normal(size=c_out).astype(np.float32)) if b % 2 else None
-    val, kid, _ = ops.pack(W.reshape(c_out, -1), n)
-    y = host(ops.conv2d(dev(x), dev(val), dev(kid), kh, kw, n, stride, pad,
+    aug, _ = ops.pack(W.reshape(c_out, -1), n)
+    y = host(ops.conv2d(dev(x), ops.aug_to_device(aug), kh, kw, n, stride, pad,
                         None if bias is None else dev(bias), pool))
     ref = o.conv2d_nhwc(x, W, stride, pad, bias)
     if pool == 2:
@@ -240,8 +240,8 @@ def test_conv2d_dense(case, dtype):
                     "u_m127_127" if dtype == "i8" else "absnormal").reshape(b, h, w, c_in)
     bias = (r.integers(-1000, 1001, size=64).astype(np.int32) if dtype == "i8"
             else r.normal(size=64).astype(np.float32)) if b != 2 else None
-    val, kid, _ = ops.pack(W.reshape(64, -1), 1)
-    y = host(ops.conv2d_dense(dev(x), dev(val), dev(kid), kh, kw, 1, stride, pad,
+    aug, _ = ops.pack(W.reshape(64, -1), 1)
+    y = host(ops.conv2d_dense(dev(x), ops.aug_to_device(aug), kh, kw, 1, stride, pad,
                               None if bias is None else dev(bias), pool))
     ref = o.conv2d_nhwc(x, W, stride, pad, bias)
     if pool == 2:
@@ -260,11 +260,11 @@ def test_mrs_on_compacted_lists_matches_conv2d():
     r = rng(5)
     W = complementary_weights(r, r, 64, 576, 8, "normal").reshape(64, 3, 3, 64)
     x = sparse_rows(r, 2 * 10 * 12, 64, 7, "absnormal").reshape(2, 10, 12, 64)
-    val, kid, _ = ops.pack(W.reshape(64, -1), 8)
-    xd, vd, kd = dev(x), dev(val), dev(kid)
-    y1 = ops.conv2d(xd, vd, kd, 3, 3, 8, 1, 1)
+    aug, _ = ops.pack(W.reshape(64, -1), 8)
+    xd, ad = dev(x), ops.aug_to_device(aug)
+    y1 = ops.conv2d(xd, ad, 3, 3, 8, 1, 1)
     idx, lv, cnt = ops.compact(xd.reshape(-1, 64))
-    y2 = ops.mrs_conv2d(idx, lv, cnt, x.shape, vd, kd, 3, 3, 8, 1, 1)
+    y2 = ops.mrs_conv2d(idx, lv, cnt, x.shape, ad, 3, 3, 8, 1, 1)
     assert torch.equal(y1, y2)
 
 
@@ -285,8 +285,8 @@ def test_mrs_reads_kwta_lists(dtype):
     wd = "int8" if dtype == "i8" else "normal"
     for (kh, kw, pad, n, c_out) in [(3, 3, 1, 8, 64), (h, w, 0, 16, 48)]:
         W = complementary_weights(r, r, c_out, kh * kw * c, n, wd).reshape(c_out, kh, kw, c)
-        val, kid, _ = ops.pack(W.reshape(c_out, -1), n)
-        y = host(ops.mrs_conv2d(*lists, (b, h, w, c), dev(val), dev(kid), kh, kw, n, 1, pad))
+        aug, _ = ops.pack(W.reshape(c_out, -1), n)
+        y = host(ops.mrs_conv2d(*lists, (b, h, w, c), ops.aug_to_device(aug), kh, kw, n, 1, pad))
         ref = o.conv2d_nhwc(x_ref, W, 1, pad)
         if dtype == "i8":
             assert np.array_equal(y.astype(np.int64), ref)
@@ -298,8 +298,8 @@ def test_fp32_bitwise_reproducible():
     r = rng(6)
     W = complementary_weights(r, r, 256, 2304, 16, "normal").reshape(256, 3, 3, 256)
     x = sparse_rows(r, 2 * 14 * 14, 256, 26, "absnormal").reshape(2, 14, 14, 256)
-    val, kid, _ = ops.pack(W.reshape(256, -1), 16)
-    xd, vd, kd = dev(x), dev(val), dev(kid)
-    a = host(ops.conv2d(xd, vd, kd, 3, 3, 16, 1, 1))
-    b = host(ops.conv2d(xd, vd, kd, 3, 3, 16, 1, 1))
+    aug, _ = ops.pack(W.reshape(256, -1), 16)
+    xd, ad = dev(x), ops.aug_to_device(aug)
+    a = host(ops.conv2d(xd, ad, 3, 3, 16, 1, 1))
+    b = host(ops.conv2d(xd, ad, 3, 3, 16, 1, 1))
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
