@@ -4,8 +4,10 @@
     python bench.py [--steps K] [--warmup W] [--config C]
 
 A step is one pass of the whole chain over one batch: per layer, compaction
-of the activations into (index, value) lists, multiply-route-sum (+ bias,
-+ 2x2 max-pool), k-WTA (+ int8 requantisation).  Inputs are resident in HBM
+of the activations into (index, value) lists (dense inputs only),
+multiply-route-sum (+ bias, + 2x2 max-pool), k-WTA (+ int8 requantisation)
+emitting the next layer's lists; where a layer's packed table fits one
+workgroup the last three are one kernel and the sums never reach HBM.  Inputs are resident in HBM
 when the timed region starts; the chain rotates among buffer sets (input +
 every intermediate) totalling more than 512 MiB, so a step does not find the
 previous step's data in the 256 MiB Infinity Cache.
@@ -80,6 +82,19 @@ def layer_costs(net, bufs, cfg) -> dict:
                 costs[f"{s.name}.compact"] = {"bytes": rows * c * es + lists}
             mrs_bytes = lists + table + bias + out_elems * 4
         prods = conv_products(cnt.reshape(b, h, w), pl, s.c_out // s.n)
+        if s.k is not None and not pl.dense_kernel:
+            # one launch: lists in, table, bias, the k-WTA output (lists or
+            # dense); the sums are written only when the network keeps them
+            ob = 1 if s.shift is not None else 4
+            if pl.emit_lists:
+                lc = bufs.lists[li][2].cpu().numpy().astype(np.int64)
+                obytes = int(lc.sum()) * (2 + ob) + len(lc) * 4
+            else:
+                obytes = out_elems * ob
+            sums = out_elems * 4 if net.keep_sums else 0
+            costs[f"{s.name}.mrs_kwta"] = {"bytes": mrs_bytes - out_elems * 4 + sums + obytes,
+                                           "products": prods, "int": is_int}
+            continue
         costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
                                   "int": is_int}
         if s.k is not None:
@@ -218,7 +233,7 @@ def main() -> int:
     cfg = CONFIGS[args.config]
     log(f"bench: workload {cfg.name}, batch {cfg.batch}")
     inp = generate(cfg)
-    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
+    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, keep_sums=False)
     per_set = net.bufs.nbytes() + inp["x"].nbytes
     nsets = max(8, math.ceil(args.rotate_mib * 2 ** 20 / per_set))
     sets = [net.bufs] + [net.make_buffers() for _ in range(nsets - 1)]

@@ -146,6 +146,62 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
                   void* stream);
 
 /*
+ * cs_mrs_kwta_conv2d - one whole layer: cs_mrs_conv2d followed by k-WTA along
+ * the channels of every output pixel (Section 2.2.2: exactly the top k
+ * activations propagate; Section 3.3.3 local k-WTA), with the winners sent on
+ * as (index, value) lists (Figure 10) or as a dense masked tensor.  DEVICE
+ * memory.  Where the layer's packed table fits one workgroup's LDS the sums,
+ * the selection and the output are produced by one kernel and the sums need
+ * not reach HBM; otherwise cs_mrs_conv2d and cs_kwta / cs_kwta_lists run
+ * back to back on `stream`.
+ *
+ *  xt .. pool   as cs_mrs_conv2d.
+ *  y       device NHWC [b][ho/pool][wo/pool][c_out] (int32 / fp32), always
+ *          required: with keep_sums = 1 it holds the sums after pool and bias
+ *          on return; with keep_sums = 0 it is scratch and its contents are
+ *          unspecified.
+ *  k       winners per output pixel, 0 <= k <= c_out; ties go to the lower
+ *          channel index; fp32 compares numerically (-0.0 == +0.0).
+ *  ot      output dtype: CS_F32 for fp32 input; CS_I32 (the sums themselves)
+ *          or CS_I8 (requantised, clamp(v >> shift, -127, 127)) for int8.
+ *  shift   0 .. 31, used with ot == CS_I8.
+ *  out     device [b][ho/pool][wo/pool][c_out] of ot: winners kept, the rest
+ *          zero.  NULL when lists are written instead.
+ *  oidx, oval, ocnt, ocap  list output (NULL when out is given): per output
+ *          pixel, oidx/oval [rows][ocap] (uint16 / ot) hold the winners whose
+ *          output value is non-zero in ascending channel order and ocnt[row]
+ *          their number; ocap >= k.
+ *  Exactly one of out and oidx must be non-NULL.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE (k > c_out, ocap < k, or
+ *  c_out > CS_MAX_KWTA_ROW), CS_ERR_DEVICE.
+ */
+int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, void* out, uint16_t* oidx,
+                       void* oval, int32_t* ocnt, int ocap, void* stream);
+
+/*
+ * cs_mrs_plan - how cs_mrs_conv2d / cs_mrs_kwta_conv2d would run a layer with
+ * these sizes (operands assumed aligned as torch allocates them).  Host only;
+ * no HIP call.  For tests and tuning.
+ *
+ *  xt .. pool  as cs_mrs_kwta_conv2d; cap: list row stride; k: winners, or -1
+ *          for cs_mrs_conv2d (sums only).
+ *  info    host int64[11] out: [0] path (0 one lane per output, 1 table-slice
+ *          kernel, 2 fused layer kernel); for path 2: [1] tile mode (0 rows of
+ *          items, 1 image rectangles), [2] items (mode 0) or pooled rows
+ *          (mode 1) per tile, [3] pooled columns per tile (mode 1), [4] list
+ *          chunks staged in LDS at most, [5] input pixels per tile at most,
+ *          [6] workgroups, [7] LDS bytes per workgroup, [8] log2 of the lanes
+ *          sharing one output's taps or chunks, [9] k-WTA selection variant;
+ *          [10] 1 when k-WTA runs as a kernel of its own after the sums.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE.
+ */
+int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int kw, int stride,
+                int pad, int c_out, int n, int pool, int k, int64_t* info);
+
+/*
  * cs_linear - a whole sparse-sparse linear layer: cs_compact of x into the
  * workspace, then Multiply/Route/Sum (a linear layer is the 1x1 convolution
  * of 1x1 images).  DEVICE memory.

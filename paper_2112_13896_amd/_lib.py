@@ -32,6 +32,10 @@ SIGNATURES = {
     "cs_compact": (_i, [_i, _vp, _i64, _i, _vp, _vp, _vp, _vp]),
     "cs_mrs_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
                            _vp, _i, _vp, _vp]),
+    "cs_mrs_kwta_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
+                                _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
+    "cs_mrs_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
+                         _c.POINTER(_i64)]),
     "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i, _vp, _vp,
                        _sz, _vp]),

@@ -5,9 +5,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cmath>
+
 #include "compact_kernels.h"
 #include "cs.h"
 #include "kwta_kernels.h"
+#include "mrs_fused.h"
 #include "mrs_kernels.h"
 #include "mrs_tiled.h"
 
@@ -189,9 +192,276 @@ int table_slice(const cs::ConvGeom& geo, size_t esz, int nacc, int gb) {
   return 0;
 }
 
+// ---------------------------------------------------------------- fused layer
+constexpr size_t kFusedLds = 80 * 1024;   // two workgroups per compute unit
+constexpr size_t kFusedLds3 = 53 * 1024;  // three
+
+size_t round16(size_t v) { return (v + 15) / 16 * 16; }
+
+bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }   // NULL: yes
+
+// Lists can be read 4 entries at a time: row stride a multiple of 4 and the
+// arrays aligned for 8-byte index and 4- or 16-byte value loads.
+bool lists_vectorisable(cs_dtype xt, const uint16_t* idx, const void* lval, int cap) {
+  return cap % 4 == 0 && aligned(idx, 8) && aligned(lval, xt == CS_I8 ? 4 : 16);
+}
+
+struct FusedPlan {
+  cs::FusedArgs fa;
+  size_t shmem;
+  int64_t blocks;
+  int gb;
+};
+
+// Tiles for the fused kernel, or false when the layer does not suit it (the
+// table does not fit the LDS next to the accumulators, too many lanes per
+// item, misaligned operands, a row too long for the selection).
+//
+// Candidates (LDS budget for three or two workgroups per compute unit, tile
+// shape, slices) are compared with a simple model of the time: workgroups per
+// concurrently resident workgroup slot of 256 compute units, times (a fixed
+// cost per workgroup for staging and the epilogue + rounds x the list chunks
+// one lane walks + the group reduction).
+constexpr int kPlanCus = 256;          // MI355X compute units (the model only)
+constexpr double kCostFixed = 40.0;    // per workgroup, in list-chunk units
+constexpr int kMaxPlanSlices = 4;
+
+bool fused_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const void* y, int k,
+                int shift, int write_sums, int ocap, int osz, FusedPlan* pl) {
+  const bool one = geo.n == 1;
+  const int n = one ? 1 : geo.n;
+  const size_t esz = xt == CS_I8 ? 2 : 8;                 // augmented entry
+  const size_t chunk_b = xt == CS_I8 ? 12 : 24;           // 4 indices + 4 values
+  const int T = geo.KH * geo.KW;
+  const int64_t R = (int64_t)T * geo.C;
+  const int64_t ntab = R * geo.G;
+  if (ntab * (int64_t)esz >= INT32_MAX || geo.cap % 4 != 0 || geo.c_out % 4 != 0) return false;
+  if (!aligned(aug, 16) || !aligned(y, 16)) return false;
+  // k-WTA in the epilogue: one lane per item, rows of at most 128 channels
+  if (k >= 0 && (geo.c_out > 128 || k > 32)) return false;
+  // sets per lane: two when they split evenly and the lane's accumulators fit
+  const int gb = (geo.G % 2 == 0 && 2 * n <= cs::FUSED_NACC) ? 2 : 1;
+  if (gb * n > cs::FUSED_NACC) return false;
+  const int units = geo.G / gb;
+  const int log2Q = geo.pool == 2 ? 2 : 0;
+  if ((units << log2Q) > cs::MRS_BD) return false;
+  const size_t acc_b = (size_t)((gb * n + 7) & ~7) * cs::MRS_BD * 4;   // rows rounded up to 8
+  const bool lists = k >= 0 && ocap > 0;
+  const size_t fixed = acc_b + round16((size_t)ntab * esz) + round16((size_t)geo.c_out * 4) + 64;
+  const bool lane_sel = k >= 0;
+  const int ostride = lane_sel ? geo.c_out + 1 : geo.c_out;   // odd: conflict-free lane reads
+  const int64_t worst_ch = geo.cap / 4;                  // chunks of a full row
+  const size_t min_ch = (size_t)(worst_ch < 4 ? worst_ch : 4);   // planned per pixel, at least
+  const bool mode0 = T == 1 && geo.S == 1 && geo.P == 0 && geo.pool == 1;
+  const int Hp = geo.Ho / geo.pool, Wp = geo.Wo / geo.pool;
+  // list chunks one lane walks for one tap, on average (unknown for dense inputs)
+  const double ch_tap = (double)(worst_ch < 4 ? worst_ch : 4);
+  auto tile_bytes = [&](int sl, int np, size_t chunks) {
+    return fixed + round16((size_t)sl * ostride * 4) + (k >= 0 ? round16((size_t)sl * 8) : 0) +
+           (lists ? round16((size_t)sl * ocap * 2) + round16((size_t)sl * ocap * osz) : 0) +
+           round16((size_t)np * 8) + chunks * chunk_b + 2 * chunk_b + 32;
+  };
+  bool found = false;
+  double best = 0.0;
+  cs::FusedArgs bfa{};
+  int64_t bblocks = 0;
+  size_t bbudget = 0;
+  auto consider = [&](size_t budget, int sl, int np, int64_t blocks, int log2S,
+                      const cs::FusedArgs& f) {
+    const size_t lds = tile_bytes(sl, np, (size_t)np * min_ch);
+    if (lds > budget || np > cs::MRS_BD * cs::FUSED_PPT || blocks < 1 || blocks > INT32_MAX)
+      return;
+    const int lpi = units << (log2Q + log2S);
+    if (lpi > cs::MRS_BD) return;
+    const int ipr = cs::MRS_BD / lpi;
+    const int rounds = (sl + ipr - 1) / ipr;
+    const int S = 1 << log2S;
+    const double work = T == 1 ? std::ceil(ch_tap / S) : std::ceil((double)T / S) * ch_tap;
+    // the group reduction: one shuffle per accumulator and slice/sub-pixel step
+    const double red = (double)gb * n * (log2S + log2Q) / 16.0;
+    int bpc = (int)(kCuLds / budget);
+    bpc = bpc > 8 ? 8 : (bpc < 1 ? 1 : bpc);
+    double waves = (double)blocks / ((double)kPlanCus * bpc);   // fractional, at least one
+    waves = waves < 1.0 ? 1.0 : waves;
+    const double cost = waves * (kCostFixed + rounds * (work + red));
+    if (!found || cost < best) {
+      found = true;
+      best = cost;
+      bfa = f;
+      bfa.log2S = log2S;
+      bfa.LPI = lpi;
+      bfa.IPR = ipr;
+      bfa.npix_cap = np;
+      bblocks = blocks;
+      bbudget = budget;
+    }
+  };
+  const int max_log2S_tap = [&] {
+    int l = 0;
+    while ((2 << l) <= T && (2 << l) <= kMaxPlanSlices && l + log2Q < 6) ++l;
+    return l;
+  }();
+  const int max_log2S_chunk = [&] {
+    int l = 0;
+    while ((2 << l) <= worst_ch && (2 << l) <= kMaxPlanSlices && l + log2Q < 6) ++l;
+    return l;
+  }();
+  const int max_log2S = T == 1 ? max_log2S_chunk : max_log2S_tap;
+  for (size_t budget : {kFusedLds3, kFusedLds}) {
+    if (fixed >= budget) continue;
+    for (int log2S = 0; log2S <= max_log2S; ++log2S) {
+      const int lpi = units << (log2Q + log2S);
+      if (lpi > cs::MRS_BD) break;
+      const int ipr = cs::MRS_BD / lpi;
+      if (mode0) {
+        const int64_t items = (int64_t)geo.B * geo.Ho * geo.Wo;
+        for (int r = 1; r <= 4; ++r) {
+          const int ti = ipr * r;
+          cs::FusedArgs f{};
+          f.tile_mode = 0;
+          f.TI = ti;
+          consider(budget, ti, ti, (items + ti - 1) / ti, log2S, f);
+        }
+      } else {
+        for (int tw = Wp; tw >= 1; tw = (tw > 1 ? (tw + 1) / 2 : 0)) {
+          const int iw = (tw * geo.pool - 1) * geo.S + geo.KW;
+          for (int tpr = 1; tpr <= Hp; ++tpr) {
+            const int ih = (tpr * geo.pool - 1) * geo.S + geo.KH;
+            const int64_t np = (int64_t)ih * iw;
+            if (np > cs::MRS_BD * cs::FUSED_PPT) break;
+            const int sl = tpr * tw;
+            if (sl > ipr * 8) break;
+            cs::FusedArgs f{};
+            f.tile_mode = 1;
+            f.TPR = tpr;
+            f.TW = tw;
+            f.tiles_x = (Wp + tw - 1) / tw;
+            f.tiles_img = ((Hp + tpr - 1) / tpr) * f.tiles_x;
+            f.IW = iw;
+            consider(budget, sl, (int)np, (int64_t)geo.B * f.tiles_img, log2S, f);
+          }
+          if (tw == 1) break;
+        }
+      }
+    }
+  }
+  if (!found) return false;
+  cs::FusedArgs fa = bfa;
+  const int slots = fa.tile_mode == 0 ? fa.TI : fa.TPR * fa.TW;
+  if (fa.tile_mode == 1) {
+    fa.fd_tw = cs::make_fastdiv((uint32_t)fa.TW);
+    fa.fd_iw = cs::make_fastdiv((uint32_t)fa.IW);
+    fa.fd_tx = cs::make_fastdiv((uint32_t)fa.tiles_x);
+    fa.fd_timg = cs::make_fastdiv((uint32_t)fa.tiles_img);
+  }
+  // list budget: what is left of the LDS, at most every chunk of every pixel
+  const size_t base = tile_bytes(slots, fa.npix_cap, 0);
+  if (base >= bbudget) return false;
+  int64_t lc = (int64_t)((bbudget - base) / chunk_b);
+  if (lc > (int64_t)fa.npix_cap * worst_ch) lc = (int64_t)fa.npix_cap * worst_ch;
+  fa.units = units;
+  fa.log2Q = log2Q;
+  fa.list_cap = (int)lc;
+  fa.k = k;
+  fa.shift = shift;
+  fa.write_sums = write_sums;
+  fa.ostride = ostride;
+  fa.kmode = k <= 8 ? 1 : (k <= 16 ? 2 : 3);               // one lane per item
+  fa.fd_lpi = cs::make_fastdiv((uint32_t)fa.LPI);
+  fa.fd_kw = cs::make_fastdiv((uint32_t)geo.KW);
+  fa.fd_cout = cs::make_fastdiv((uint32_t)geo.c_out);
+  fa.fd_ochunks = cs::make_fastdiv((uint32_t)(lists ? ocap / 4 : 1));
+  // LDS layout
+  size_t o = acc_b;
+  fa.off_tab = (uint32_t)o;
+  o += round16((size_t)ntab * esz);
+  fa.off_bias = (uint32_t)o;
+  o += round16((size_t)geo.c_out * 4);
+  fa.off_out = (uint32_t)o;
+  o += round16((size_t)slots * fa.ostride * 4);
+  fa.off_sel = (uint32_t)o;
+  o += k >= 0 ? round16((size_t)slots * 8) : 0;
+  fa.off_lidx = (uint32_t)o;
+  o += lists ? round16((size_t)slots * ocap * 2) : 0;
+  fa.off_lval = (uint32_t)o;
+  o += lists ? round16((size_t)slots * ocap * osz) : 0;
+  fa.off_pix = (uint32_t)o;
+  o += round16((size_t)fa.npix_cap * 8);
+  fa.off_cidx = (uint32_t)o;                             // lc chunks + the spare slot
+  o += round16((size_t)(lc + 1) * 8);
+  fa.off_cval = (uint32_t)o;
+  o += round16((size_t)(lc + 1) * (chunk_b - 8));
+  fa.off_misc = (uint32_t)o;
+  o += 64;
+  if (o > bbudget) return false;
+  pl->fa = fa;
+  pl->shmem = o;
+  pl->blocks = bblocks;
+  pl->gb = gb;
+  return true;
+}
+
+template <typename T, typename A, typename TO>
+void launch_fused_t(const FusedPlan& pl, hipStream_t stream, const uint16_t* idx,
+                    const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                    void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  const dim3 grid((unsigned)pl.blocks), block(cs::MRS_BD);
+  const T* lv = static_cast<const T*>(lval);
+  const auto* pa = static_cast<const typename cs::Aug<T>::type*>(aug);
+  const A* bs = static_cast<const A*>(bias);
+  A* yy = static_cast<A*>(y);
+  TO* oo = static_cast<TO*>(out);
+#define CS_FUSED(ONE_, GB_)                                                                  \
+  hipLaunchKernelGGL((cs::mrs_fused<T, A, TO, ONE_, GB_>), grid, block, pl.shmem, stream, idx, \
+                     lv, cnt, pa, bs, yy, oo, lo, geo, pl.fa)
+  if (geo.n == 1) {
+    if (pl.gb == 2) CS_FUSED(true, 2);
+    else CS_FUSED(true, 1);
+  } else {
+    if (pl.gb == 2) CS_FUSED(false, 2);
+    else CS_FUSED(false, 1);
+  }
+#undef CS_FUSED
+}
+
+// Launch a planned fused layer.  ot: output dtype of the k-WTA (ignored when
+// fa.k < 0).
+int launch_fused(const FusedPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stream,
+                 const uint16_t* idx, const void* lval, const int32_t* cnt, const void* aug,
+                 const void* bias, void* y, void* out, const cs::ListOut& lo,
+                 const cs::ConvGeom& geo) {
+  if (xt == CS_F32)
+    launch_fused_t<float, float, float>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  else if (ot == CS_I8)
+    launch_fused_t<int8_t, int32_t, int8_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
+                                           geo);
+  else
+    launch_fused_t<int8_t, int32_t, int32_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
+                                            geo);
+  return launch_status();
+}
+
+int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                     const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
+                     hipStream_t stream);
+
+// Sums of a layer: the fused kernel (lists staged in LDS) when the layer suits
+// it, else the table-slice kernel, else the one-lane-per-output kernel.
 int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
                const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                hipStream_t stream) {
+  if (lists_vectorisable(xt, idx, lval, geo.cap)) {
+    FusedPlan fp;
+    if (fused_plan(geo, xt, aug, y, -1, 0, 1, 0, 0, &fp))
+      return launch_fused(fp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                          cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
+  }
+  return mrs_launch_tiled(xt, idx, lval, cnt, geo, aug, bias, y, stream);
+}
+
+int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                     const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
+                     hipStream_t stream) {
   const bool one = geo.n == 1;
   const int nacc = one ? 1 : geo.n;
   const int T = geo.KH * geo.KW;
@@ -216,7 +486,7 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   // 32-bit offsets inside the kernel: element offsets and lane counts below 2^31
   const bool fits32 = in_rows * geo.cap < INT32_MAX && items * geo.c_out < INT32_MAX &&
                       R * geo.G < INT32_MAX && items * geo.G * 64 < INT32_MAX;
-  if (geo.cap % 4 != 0 || Gs < 1 || log2S + ta.log2Q > 6 || !fits32)
+  if (!lists_vectorisable(xt, idx, lval, geo.cap) || Gs < 1 || log2S + ta.log2Q > 6 || !fits32)
     return mrs_launch_simple(xt, idx, lval, cnt, geo, aug, bias, y, stream);
   int cus = 0;
   const int st = device_cus(&cus);
@@ -336,6 +606,88 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
   if (!idx || !lval || !cnt || !aug || !y) return CS_ERR_ARG;
   geo.cap = cap;
   return mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, static_cast<hipStream_t>(stream));
+}
+
+int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, void* out, uint16_t* oidx,
+                       void* oval, int32_t* ocnt, int ocap, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  const cs_dtype at = xt == CS_I8 ? CS_I32 : CS_F32;
+  if (!(ot == at || (xt == CS_I8 && ot == CS_I8))) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (cap < 1) return CS_ERR_SHAPE;
+  if (!idx || !lval || !cnt || !aug || !y) return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0 || shift < 0 || shift > 31) return CS_ERR_ARG;
+  if (k > c_out || c_out > CS_MAX_KWTA_ROW) return CS_ERR_SHAPE;
+  const bool lists = oidx != nullptr;
+  if (lists == (out != nullptr)) return CS_ERR_ARG;        // exactly one output form
+  if (lists && (!oval || !ocnt || ocap < 1)) return CS_ERR_ARG;
+  if (lists && ocap < k) return CS_ERR_SHAPE;
+  geo.cap = cap;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const cs::ListOut lo{oidx, oval, ocnt, lists ? ocap : 0};
+  // the fused kernel writes lists 4 entries at a time
+  const int osz = ot == CS_I8 ? 1 : 4;
+  const bool lists_ok = !lists || (ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, osz * 4));
+  if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
+    FusedPlan fp;
+    if (fused_plan(geo, xt, aug, y, k, shift, keep_sums, lists ? ocap : 0, osz, &fp))
+      return launch_fused(fp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
+  // two kernels: the sums into y, then k-WTA from y
+  st = mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, s);
+  if (st != CS_OK) return st;
+  const int64_t rows = (int64_t)b * (geo.Ho / pool) * (geo.Wo / pool);
+  if (xt == CS_F32)
+    return kwta_dispatch(static_cast<const float*>(y), rows, c_out, k, static_cast<float*>(out),
+                         0, s, lo);
+  if (ot == CS_I8)
+    return kwta_dispatch(static_cast<const int32_t*>(y), rows, c_out, k,
+                         static_cast<int8_t*>(out), shift, s, lo);
+  return kwta_dispatch(static_cast<const int32_t*>(y), rows, c_out, k, static_cast<int32_t*>(out),
+                       0, s, lo);
+}
+
+int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int kw, int stride,
+                int pad, int c_out, int n, int pool, int k, int64_t* info) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  if (!info) return CS_ERR_ARG;
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (cap < 1 || k < -1 || k > c_out) return CS_ERR_SHAPE;
+  geo.cap = cap;
+  for (int i = 0; i < 11; ++i) info[i] = 0;
+  FusedPlan fp;
+  const int ocap = k >= 0 ? (k + 3) / 4 * 4 : 0;        // lists as the k-WTA emits them
+  bool fused = cap % 4 == 0 && fused_plan(geo, xt, nullptr, nullptr, k, 0, 1,
+                                          ocap < 4 ? 4 : ocap, xt == CS_I8 ? 1 : 4, &fp);
+  if (!fused && k >= 0 && cap % 4 == 0) {
+    // the sums in the fused kernel, k-WTA in its own kernel
+    fused = fused_plan(geo, xt, nullptr, nullptr, -1, 0, 1, 0, 0, &fp);
+    info[10] = 1;
+  } else if (k >= 0 && !fused) {
+    info[10] = 1;
+  }
+  if (fused) {
+    info[0] = 2;
+    info[1] = fp.fa.tile_mode;
+    info[2] = fp.fa.tile_mode == 0 ? fp.fa.TI : fp.fa.TPR;
+    info[3] = fp.fa.tile_mode == 0 ? 0 : fp.fa.TW;
+    info[4] = fp.fa.list_cap;
+    info[5] = fp.fa.npix_cap;
+    info[6] = fp.blocks;
+    info[7] = (int64_t)fp.shmem;
+    info[8] = fp.fa.log2S;
+    info[9] = fp.fa.kmode;
+  } else {
+    info[0] = cap % 4 == 0 ? 1 : 0;
+  }
+  return CS_OK;
 }
 
 int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,

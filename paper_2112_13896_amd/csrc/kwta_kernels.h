@@ -15,11 +15,12 @@
 //    keeps a descending top-K list by insertion (a max/min exchange per slot,
 //    no branches), which yields T;
 //  * kwta_wave  (row <= 2048): one wavefront owns a row, each lane holds up to
-//    M keys in registers.  T is found MSB-first, 8 bits per pass, with a
-//    256-bin LDS histogram per wavefront (the histogram search of Section
-//    3.3.3 and Figure 10, refined digit by digit so it is exact for 32-bit
-//    keys); the bin holding the k-th key is found with a wavefront suffix
-//    scan.  Ties are ranked with a ballot + popcount in index order.
+//    M keys in registers.  T is found MSB-first, one bit per step below the
+//    bits every key of the row shares, counting the keys above a candidate
+//    with ballots (the threshold search of Section 3.3.3 and Figure 10,
+//    refined bit by bit so it is exact for 32-bit keys).  No LDS histogram:
+//    sums that cluster (many equal to the bias) would pile its atomics onto
+//    a few bins.  Ties are ranked with a ballot + popcount in index order.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -27,6 +28,12 @@
 #include "fastdiv.h"
 
 namespace cs {
+
+__device__ __forceinline__ void wave_sync_kwta() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ __forceinline__ uint32_t order_key(int32_t v) { return (uint32_t)v ^ 0x80000000u; }
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -60,6 +67,53 @@ struct ListOut {
   int32_t* cnt;
   int cap;
 };
+
+// k-th largest of a row's keys, searched by one wavefront: lane l holds keys
+// key[j] of elements j*64 + l (elements >= c are not part of the row).  The
+// search starts below the bits all keys share (from the row's min and max)
+// and fixes one bit per step, MSB first: T | bit is kept while at least k keys
+// are >= it, counted with a ballot per key.  No memory traffic; the result is
+// wavefront-uniform.  Requires 1 <= k < c.  Returns T; *need = k - #{key > T},
+// the number of keys equal to T that win (the lowest indices).
+template <int M>
+__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[M], int c, int k,
+                                                     int* need) {
+  const int lane = threadIdx.x & 63;
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    if (j * 64 + lane < c) {
+      kmin = key[j] < kmin ? key[j] : kmin;
+      kmax = key[j] > kmax ? key[j] : kmax;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t a = __shfl_xor(kmin, off, 64), b = __shfl_xor(kmax, off, 64);
+    kmin = a < kmin ? a : kmin;
+    kmax = b > kmax ? b : kmax;
+  }
+  const uint32_t diff = kmin ^ kmax;
+  uint32_t T = kmax;
+  if (diff != 0u) {
+    const int hb = 31 - __builtin_clz(diff);
+    const uint32_t low = hb == 31 ? 0xFFFFFFFFu : ((2u << hb) - 1u);
+    T = kmax & ~low;                                   // the shared prefix, zeros below
+    for (int b = hb; b >= 0; --b) {
+      const uint32_t cand = T | (1u << b);
+      int cnt = 0;
+#pragma unroll
+      for (int j = 0; j < M; ++j)                      // keys outside the row are 0 < cand
+        if (j * 64 < c) cnt += __popcll(__ballot(key[j] >= cand));
+      if (cnt >= k) T = cand;
+    }
+  }
+  int gt = 0;
+#pragma unroll
+  for (int j = 0; j < M; ++j) gt += __popcll(__ballot(j * 64 + lane < c && key[j] > T));
+  *need = k - gt;
+  return T;
+}
 
 constexpr int KWTA_LANE_ROWS = 128;   // rows (threads) per block of kwta_lane
 constexpr int KWTA_BATCH = 16;        // tile elements a thread loads per batch
@@ -189,103 +243,42 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
                                                                   int64_t rows, int c, int k,
                                                                   TO* __restrict__ out,
                                                                   int shift, ListOut lo) {
-  __shared__ uint32_t hist[KWTA_WAVE_WAVES][256];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
-  uint32_t* h = hist[wv];
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
   const bool all_win = (k == c);
   const bool none_win = (k == 0);
-  for (int64_t row0 = (int64_t)blockIdx.x * KWTA_WAVE_WAVES; row0 < rows;
-       row0 += (int64_t)gridDim.x * KWTA_WAVE_WAVES) {           // uniform across the block
-    const int64_t row = row0 + wv;
-    const bool live = row < rows;                                 // uniform across the wave
+  for (int64_t row = (int64_t)blockIdx.x * KWTA_WAVE_WAVES + wv; row < rows;
+       row += (int64_t)gridDim.x * KWTA_WAVE_WAVES) {            // uniform across the wave
     TI v[M];
     uint32_t key[M];
 #pragma unroll
     for (int j = 0; j < M; ++j) {
       const int e = j * 64 + lane;
-      v[j] = (live && e < c) ? in[row * c + e] : TI(0);
-      key[j] = order_key(v[j]);
+      v[j] = e < c ? in[row * c + e] : TI(0);
+      key[j] = e < c ? order_key(v[j]) : 0u;
     }
-    uint32_t prefix = 0u, pmask = 0u;
-    int need = k;
-    const bool search = live && !all_win && !none_win;
-    for (int sh = 24; sh >= 0; sh -= 8) {
-      for (int b = lane; b < 256; b += 64) h[b] = 0u;
-      __syncthreads();
-      if (search) {
-#pragma unroll
-        for (int j = 0; j < M; ++j) {
-          const int e = j * 64 + lane;
-          if (e < c && (key[j] & pmask) == prefix)
-            __hip_atomic_fetch_add(&h[(key[j] >> sh) & 255u], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_WORKGROUP);
-        }
-      }
-      __syncthreads();
-      if (search) {
-        const uint32_t c0 = h[4 * lane], c1 = h[4 * lane + 1], c2 = h[4 * lane + 2],
-                       c3 = h[4 * lane + 3];
-        const uint32_t s = c0 + c1 + c2 + c3;
-        uint32_t incl = s;                                   // sum over lanes >= this lane
-        for (int off = 1; off < 64; off <<= 1) {
-          const uint32_t t = __shfl_down(incl, off, 64);
-          if (lane + off < 64) incl += t;
-        }
-        const uint32_t excl = incl - s;                      // keys in higher bins
-        const uint32_t un = (uint32_t)need;
-        const bool here = excl < un && un <= incl;
-        int d = 0;
-        uint32_t above = 0;
-        if (here) {
-          uint32_t cum = excl;
-          if (cum + c3 >= un) {
-            d = 4 * lane + 3;
-          } else {
-            cum += c3;
-            if (cum + c2 >= un) {
-              d = 4 * lane + 2;
-            } else {
-              cum += c2;
-              if (cum + c1 >= un) {
-                d = 4 * lane + 1;
-              } else {
-                cum += c1;
-                d = 4 * lane;
-              }
-            }
-          }
-          above = cum;
-        }
-        const uint64_t bal = __ballot(here);
-        const int src = __ffsll((long long)bal) - 1;
-        d = __shfl(d, src, 64);
-        above = __shfl(above, src, 64);
-        need -= (int)above;
-        prefix |= (uint32_t)d << sh;
-        pmask |= 0xFFu << sh;
-      }
-      __syncthreads();
-    }
+    int need = 0;
+    uint32_t thr = 0u;
+    if (!all_win && !none_win) thr = wave_kth_largest<M>(key, c, k, &need);
     // ranks of the ties in index order (element index = j*64 + lane)
     int run = 0, lrun = 0;
 #pragma unroll
     for (int j = 0; j < M; ++j) {
       const int e = j * 64 + lane;
-      const bool valid = live && e < c;
-      const bool eq = search && valid && key[j] == prefix;
+      const bool valid = e < c;
+      const bool eq = !all_win && !none_win && valid && key[j] == thr;
       const uint64_t b = __ballot(eq);
       const int rank = run + __popcll(b & below);
       run += __popcll(b);
       bool win;
-      if (all_win) win = true;
+      if (all_win) win = valid;
       else if (none_win) win = false;
-      else win = key[j] > prefix || (eq && rank < need);
+      else win = valid && (key[j] > thr || (eq && rank < need));
       const TO ov = kwta_out<TI, TO>(v[j], shift);
       if (lo.idx) {
         // list output: non-zero winners, ranked in index order by ballot + popcount
-        const bool put = valid && win && ov != TO(0);
+        const bool put = win && ov != TO(0);
         const uint64_t pb = __ballot(put);
         if (put) {
           const int pos = lrun + __popcll(pb & below);
@@ -297,7 +290,7 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
         out[row * c + e] = win ? ov : TO(0);
       }
     }
-    if (lo.idx && live && lane == 0) lo.cnt[row] = lrun;
+    if (lo.idx && lane == 0) lo.cnt[row] = lrun;
   }
 }
 

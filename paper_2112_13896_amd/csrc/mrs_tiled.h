@@ -57,6 +57,28 @@ struct TiledArgs {
   FastDiv fd_kw;     // / kernel width
 };
 
+// Copy n16 16-byte words from global memory to LDS with MRS_COPY loads in
+// flight per lane.  Every load is unconditional (a lane past the end reads the
+// last word again), so the batch stays in registers and the loads overlap.
+constexpr int MRS_COPY = 10;
+__device__ __forceinline__ void copy16_to_lds(const uint4* __restrict__ src, uint4* dst, int n16) {
+  if (n16 <= 0) return;
+  const int tid = threadIdx.x;
+  for (int base = 0; base < n16; base += MRS_BD * MRS_COPY) {
+    uint4 v[MRS_COPY];
+#pragma unroll
+    for (int u = 0; u < MRS_COPY; ++u) {
+      const int e = base + u * MRS_BD + tid;
+      v[u] = src[e < n16 ? e : n16 - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < MRS_COPY; ++u) {
+      const int e = base + u * MRS_BD + tid;
+      if (e < n16) dst[e] = v[u];
+    }
+  }
+}
+
 template <typename T>
 struct Chunk;
 template <>
@@ -177,32 +199,17 @@ __global__ __launch_bounds__(MRS_BD) void mrs_tiled(const uint16_t* __restrict__
   const int total = R * gcount;
   if (ta.vec_stage) {
     // the whole table, contiguous: 16-byte copies
-    const uint4* src4 = reinterpret_cast<const uint4*>(aug);
-    uint4* dst4 = reinterpret_cast<uint4*>(tab);
-    const int n16 = R * gcount * (int)sizeof(E) / 16;
-    for (int base = 0; base < n16; base += MRS_BD * MRS_STAGE) {
-      uint4 v[MRS_STAGE];
-#pragma unroll
-      for (int u = 0; u < MRS_STAGE; ++u) {
-        const int e = base + u * MRS_BD + tid;
-        if (e < n16) v[u] = src4[e];
-      }
-#pragma unroll
-      for (int u = 0; u < MRS_STAGE; ++u) {
-        const int e = base + u * MRS_BD + tid;
-        if (e < n16) dst4[e] = v[u];
-      }
-    }
+    copy16_to_lds(reinterpret_cast<const uint4*>(aug), reinterpret_cast<uint4*>(tab),
+                  R * gcount * (int)sizeof(E) / 16);
   } else {
     for (int base = 0; base < total; base += MRS_BD * MRS_STAGE) {
       E v[MRS_STAGE];
 #pragma unroll
       for (int u = 0; u < MRS_STAGE; ++u) {
-        const int e = base + u * MRS_BD + tid;
-        if (e < total) {
-          const int i = (int)fdiv((uint32_t)e, ta.fd_gs), gl = e - i * gcount;
-          v[u] = aug[i * G + g0 + gl];
-        }
+        const int e0 = base + u * MRS_BD + tid;
+        const int e = e0 < total ? e0 : total - 1;            // always a valid entry
+        const int i = (int)fdiv((uint32_t)e, ta.fd_gs), gl = e - i * gcount;
+        v[u] = aug[i * G + g0 + gl];
       }
 #pragma unroll
       for (int u = 0; u < MRS_STAGE; ++u) {

@@ -12,11 +12,15 @@ their indices"):
   * the first layer's dense input is compacted into (index, value) lists
     (cs_compact), or read densely by the sparse-dense kernel when the layer
     is marked dense_input (cs_conv2d_dense);
-  * multiply/route/sum (cs_mrs_conv2d: + bias + optional 2x2 max-pool) reads
-    the lists and writes the layer's sums;
-  * a k-WTA that feeds another layer emits that layer's lists directly
-    (cs_kwta_lists, capacity k rounded up to 4, winners requantised to int8
-    in int8 chains); the last layer's k-WTA writes a dense masked output.
+  * multiply/route/sum + bias + optional 2x2 max-pool + k-WTA run as one
+    call (cs_mrs_kwta_conv2d) that reads the lists and emits the next layer's
+    lists directly (capacity k rounded up to 4, winners requantised to int8
+    in int8 chains), or a dense masked output for the last layer; the sums
+    reach HBM only when keep_sums is set (tests) - a layer whose packed table
+    is too large for one workgroup falls back inside the library to separate
+    sum and k-WTA kernels;
+  * a layer without k-WTA writes its sums (cs_mrs_conv2d); after the dense
+    sparse-dense first layer, k-WTA is a separate call (cs_kwta_lists).
 A linear layer that follows a conv layer reads the conv output's per-pixel
 lists as a convolution whose window is the whole h x w map: its slots
 (h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
@@ -73,8 +77,10 @@ class Buffers:
 
 
 class Network:
-    def __init__(self, layers, weights, biases, in_shape, batch: int, device="cuda"):
+    def __init__(self, layers, weights, biases, in_shape, batch: int, device="cuda",
+                 keep_sums: bool = True):
         self.layers = list(layers)
+        self.keep_sums = keep_sums
         self.device = torch.device(device)
         self.batch = batch
         self.in_shape = tuple(in_shape)
@@ -180,6 +186,8 @@ class Network:
         b, h, w, c = pl.geo
         acc = B.acc[li]
         acc4 = acc.reshape(b, -1, 1, s.c_out) if acc.dim() == 2 else acc
+        odt = torch.int8 if s.shift is not None else None
+        shift = s.shift if s.shift is not None else 0
         if pl.dense_kernel:
             # sparse-dense variant: dense activations, no compaction
             t.start(f"{s.name}.mrs")
@@ -194,13 +202,21 @@ class Network:
                 ops.compact_into(x.reshape(b * h * w, c), B.idx[li], B.lval[li], B.cnt[li])
                 t.stop(f"{s.name}.compact")
                 idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
+            if s.k is not None:
+                # one call: sums, pool, k-WTA, requantisation, lists or dense output
+                t.start(f"{s.name}.mrs_kwta")
+                ops.mrs_kwta_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride,
+                                    pl.pad, p.bias, pl.pool, k=s.k, out_dtype=odt, shift=shift,
+                                    y=acc4, keep_sums=self.keep_sums,
+                                    lists=B.lists[li] if pl.emit_lists else None,
+                                    out=None if pl.emit_lists else B.out[li])
+                t.stop(f"{s.name}.mrs_kwta")
+                return B.out[li]
             t.start(f"{s.name}.mrs")
             ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad,
                            p.bias, pl.pool, out=acc4)
             t.stop(f"{s.name}.mrs")
         if s.k is not None:
-            odt = torch.int8 if s.shift is not None else None
-            shift = s.shift if s.shift is not None else 0
             t.start(f"{s.name}.kwta")
             if pl.emit_lists:
                 ops.kwta_lists(acc, s.k, odt, shift, pl.cap_out, out=B.lists[li])
@@ -240,6 +256,9 @@ class Network:
             s = p.spec
             if not pl.in_lists and not pl.dense_kernel:
                 names.append(f"{s.name}.compact")
+            if s.k is not None and not pl.dense_kernel:
+                names.append(f"{s.name}.mrs_kwta")
+                continue
             names.append(f"{s.name}.mrs")
             if s.k is not None:
                 names.append(f"{s.name}.kwta")

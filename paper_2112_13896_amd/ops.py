@@ -150,6 +150,66 @@ def mrs_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shap
     return out
 
 
+def mrs_kwta_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, aug,
+                    kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None,
+                    pool: int = 1, *, k: int, out_dtype: torch.dtype | None = None,
+                    shift: int = 0, y: torch.Tensor | None = None, keep_sums: bool = True,
+                    cap: int | None = None, lists=None, out: torch.Tensor | None = None):
+    """One layer: multiply/route/sum (+ bias, pool) and k-WTA over each output
+    pixel's channels.  Returns (y, result) where y holds the sums (when
+    keep_sums) and result is the dense masked output, or the (idx, val, cnt)
+    lists when `cap` or `lists` is given."""
+    b, h, w, c_in = in_shape
+    pa, c_out = _aug(aug, lval.dtype, n)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    acc_dt = torch.int32 if lval.dtype == torch.int8 else torch.float32
+    odt = acc_dt if out_dtype is None else out_dtype
+    oshape = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    if y is None:
+        y = torch.empty(oshape, dtype=acc_dt, device=lval.device)
+    if lists is None and cap is not None:
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=lval.device),
+                 torch.empty((rows, cap), dtype=odt, device=lval.device),
+                 torch.empty((rows,), dtype=torch.int32, device=lval.device))
+    if lists is not None:
+        oi, ov, oc = lists
+        if oi.dtype != torch.int16 or ov.dtype != odt or oc.dtype != torch.int32:
+            raise TypeError("list buffer dtypes do not match")
+        if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+            raise ValueError("list buffer shapes do not match the output")
+        args = (None, _dev(oi, "oidx"), _dev(ov, "oval"), _dev(oc, "ocnt"), oi.shape[1])
+        result = lists
+    else:
+        if out is None:
+            out = torch.empty(oshape, dtype=odt, device=lval.device)
+        if out.dtype != odt or out.numel() != rows * c_out:
+            raise ValueError("out does not match the output")
+        args = (_dev(out, "out"), None, None, None, 0)
+        result = out
+    check("cs_mrs_kwta_conv2d", lib().cs_mrs_kwta_conv2d(
+        _dt(lval), _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
+        b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n, _opt(bias, "bias"), pool,
+        _dev(y, "y"), 1 if keep_sums else 0, k, _TORCH_DT[odt], shift, *args, _stream()))
+    return y, result
+
+
+def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: int, pad: int,
+             c_out: int, n: int, pool: int = 1, k: int = -1) -> dict:
+    """The launch plan the library picks for a layer (host only)."""
+    b, h, w, c_in = in_shape
+    info = (ctypes.c_int64 * 11)()
+    check("cs_mrs_plan", lib().cs_mrs_plan(_TORCH_DT[dtype], cap, b, h, w, c_in, kh, kw, stride,
+                                           pad, c_out, n, pool, k, info))
+    path = ("simple", "tiled", "fused")[info[0]]
+    kwta = None if k < 0 else ("separate" if info[10] else "fused")
+    if path != "fused":
+        return {"path": path, "kwta": kwta}
+    return {"path": path, "tile_mode": info[1], "tile": info[2], "tile_cols": info[3],
+            "list_cap": info[4], "npix_cap": info[5], "blocks": info[6], "lds": info[7],
+            "log2_slices": info[8], "select": info[9], "kwta": kwta}
+
+
 def workspace_bytes(op: int, dtype: torch.dtype, rows: int, c_in: int) -> int:
     return int(lib().cs_workspace_bytes(op, _TORCH_DT[dtype], rows, c_in))
 

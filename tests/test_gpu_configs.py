@@ -16,6 +16,7 @@ import torch
 
 from oracle import cs_oracle as o
 from oracle import networks
+from paper_2112_13896_amd import ops
 from paper_2112_13896_amd.network import Network
 from tests.gpu_util import assert_f32_close, check_kwta_f32, dev, host
 from workloads import CONFIGS, generate
@@ -24,11 +25,20 @@ pytestmark = pytest.mark.gpu
 
 
 def run_gpu(cfg, inp):
+    """The chain with the sums kept (checked below), then as the benchmark runs
+    it (sums not kept): every layer's output must be the same bits."""
     net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
     net.forward(dev(inp["x"]))
     torch.cuda.synchronize()
     outs = [host(net.dense_output(li)) for li in range(len(cfg.layers))]
-    return net, [host(a) for a in net.acc], outs
+    acc = [host(a) for a in net.acc]
+    bench = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, keep_sums=False)
+    bench.forward(dev(inp["x"]))
+    for li in range(len(cfg.layers)):
+        o2 = host(bench.dense_output(li))
+        assert np.array_equal(o2.view(np.uint8), outs[li].view(np.uint8)), \
+            f"layer {li}: output differs when the sums are not kept"
+    return net, acc, outs
 
 
 @pytest.mark.parametrize("cid", [1, 2, 5])
@@ -71,6 +81,26 @@ def test_fp32_config_layerwise(cid):
         layer_in = out[li]            # the next layer checks against the GPU's own input
     rows = sum(a.size // a.shape[-1] for a in acc)
     assert near <= max(1, rows // 1000), f"{near} near-tie rows"
+
+
+@pytest.mark.parametrize("cid,layer,path", [(1, "linear", "fused"), (2, "conv2", "fused"),
+                                             (2, "linear1", "tiled"), (2, "output", "fused"),
+                                             (3, "conv3x3", "fused"), (4, "conv1x1", "tiled"),
+                                             (4, "conv3x3", "tiled"), (5, "expand", "fused"),
+                                             (5, "project", "fused")])
+def test_config_launch_paths(cid, layer, path):
+    """Which kernel runs each layer at full size (the benchmark's launches)."""
+    cfg = CONFIGS[cid]
+    inp = generate(cfg, batch=1)
+    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
+    li = [s.name for s in cfg.layers].index(layer)
+    pl = net.plans[li]
+    s = cfg.layers[li]
+    cap = net.bufs.lists[li - 1][0].shape[1] if pl.in_lists else pl.geo[3]
+    dt = torch.int8 if cfg.dtype == "i8" else torch.float32
+    plan = ops.mrs_plan(dt, cap, pl.geo, pl.kh, pl.kw, pl.stride, pl.pad, s.c_out, s.n, pl.pool,
+                        s.k if s.k is not None else -1)
+    assert plan["path"] == path, plan
 
 
 def test_config_product_counts_match_closed_form():

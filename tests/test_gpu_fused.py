@@ -1,0 +1,214 @@
+"""GPU parity of the one-kernel layer (cs_mrs_kwta_conv2d): multiply, route,
+sum, bias, 2x2 max-pool, k-WTA, requantisation, list or dense output.
+
+Every case is checked against the oracle (dense convolution of the unpacked
+weights, full-sort k-WTA): int8 bit for bit (sums, winners, requantised
+values, list order and counts); fp32 sums within 1e-5 * sum|products| and the
+winners as the exact top-k of the kernel's own sums, differing from the
+oracle's only at near-ties.  Each case runs twice, keeping the sums (checked)
+and not keeping them (the benchmark's setting), and both outputs must be
+identical.  The launch plan is asserted so that every tiling path (rows of
+items, full-width image rows, column tiles, partial LDS staging with global
+reads, the two-kernel fallback) is known to run.
+"""
+from __future__ import annotations
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import cs_oracle as o
+from paper_2112_13896_amd import ops
+from tests.gpu_util import assert_f32_close, check_kwta_f32, dev, host, pool_S
+from workloads import complementary_weights
+
+pytestmark = pytest.mark.gpu
+
+
+def sparse_input(r, shape, nnz, dtype, low_range=False):
+    """NHWC input with exactly `nnz` non-zero channels per pixel."""
+    b, h, w, c = shape
+    rows = b * h * w
+    x = np.zeros((rows, c), dtype=np.int8 if dtype == "i8" else np.float32)
+    for i in range(rows):
+        pos = r.choice(c, size=min(nnz, c), replace=False)
+        if dtype == "i8":
+            x[i, pos] = 1 if low_range else r.integers(1, 128, size=len(pos))
+        else:
+            x[i, pos] = np.abs(r.normal(size=len(pos))).astype(np.float32)
+    if rows > 3:
+        x[2] = 0                                   # an empty pixel
+    return x.reshape(shape)
+
+
+def weights(r, c_out, kh, kw, c_in, n, dtype, low_range=False):
+    W = complementary_weights(r, r, c_out, kh * kw * c_in, n,
+                              "int8" if dtype == "i8" else "normal")
+    if low_range and dtype == "i8":
+        W = np.sign(W).astype(np.int8)             # +-1: many equal sums (ties)
+    return W.reshape(c_out, kh, kw, c_in)
+
+
+def dense_from_lists(idx, val, cnt, c):
+    rows, cap = idx.shape
+    out = np.zeros((rows, c), dtype=val.dtype)
+    for row in range(rows):
+        m = cnt[row]
+        ii = idx[row, :m].view(np.uint16).astype(np.int64)
+        assert (np.diff(ii) > 0).all(), f"row {row}: list indices not ascending"
+        out[row, ii] = val[row, :m]
+    return out
+
+
+# dtype, (b, h, w, c_in), nnz, kh, kw, stride, pad, c_out, n, pool, k, bias, shift,
+# out ("lists"/"dense"), expected plan (path, tile mode or None)
+CASES = [
+    # keyword-spotting conv2 shape: 5x5, 2x2 pool, whole image per tile
+    ("i8", (3, 14, 14, 64), 8, 5, 5, 1, 0, 64, 16, 2, 8, False, 9, "lists", ("fused", 1)),
+    # 3x3 pad 1, ragged image against the tiles, fp32 dense output
+    ("f32", (2, 19, 13, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "dense", ("fused", 1)),
+    # wide image: column tiles
+    ("f32", (1, 9, 150, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "lists", ("fused", 1)),
+    # 1x1 expand: rows of items, bias, requantised lists, ragged last tile
+    ("i8", (2, 7, 9, 96), 12, 1, 1, 1, 0, 576, 8, 1, 72, True, 9, "lists", ("fused", 0)),
+    # linear, int32 dense output, bias
+    ("i8", (37, 1, 1, 512), 64, 1, 1, 1, 0, 64, 8, 1, 16, True, None, "dense", ("fused", 0)),
+    # dense kernels (n = 1), one accumulator per set in registers
+    ("i8", (29, 1, 1, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("fused", 0)),
+    ("f32", (3, 6, 5, 40), 9, 3, 3, 1, 1, 16, 1, 1, 5, True, None, "dense", ("fused", 1)),
+    # stride 2, odd input
+    ("f32", (2, 17, 17, 32), 5, 3, 3, 2, 1, 32, 4, 1, 4, False, None, "lists", ("fused", 1)),
+    # 5x5 pad 2 with pool, odd number of sets (one set per lane)
+    ("f32", (2, 12, 10, 16), 4, 5, 5, 1, 2, 24, 8, 2, 6, True, None, "dense", ("fused", 1)),
+    # k = 0 and k = c_out
+    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 0, False, 3, "lists", ("fused", 1)),
+    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 32, True, None, "dense", ("fused", 1)),
+    # ties everywhere: +-1 weights, all-one inputs
+    ("i8", (4, 9, 9, 64), 8, 3, 3, 1, 1, 64, 16, 1, 8, False, 0, "lists", ("fused", 1)),
+    # lists that do not fit the LDS budget: some pixels are read from global memory
+    ("f32", (2, 24, 24, 128), 100, 3, 3, 1, 1, 16, 4, 1, 4, False, None, "lists", ("fused", 1)),
+    # c_out not a multiple of 4: two kernels (sums, then k-WTA)
+    ("i8", (3, 6, 6, 24), 5, 3, 3, 1, 1, 6, 2, 1, 2, True, 2, "lists", ("tiled", None)),
+    # a table too large for LDS: two kernels
+    ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("tiled", None)),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"{c[0]}-{c[1]}-{c[3]}x{c[4]}-n{c[8]}-k{c[10]}-{c[13]}"
+                                             for c in CASES])
+def test_fused_layer(case):
+    (dtype, shape, nnz, kh, kw, stride, pad, c_out, n, pool, k, has_bias, shift, mode,
+     want) = case
+    r = np.random.default_rng(zlib.crc32(repr(case[:13]).encode()))
+    b, h, w, c_in = shape
+    ties = shift == 0
+    x = sparse_input(r, shape, nnz, dtype, low_range=ties)
+    W = weights(r, c_out, kh, kw, c_in, n, dtype, low_range=ties)
+    bias = None
+    if has_bias:
+        bias = (r.integers(-1000, 1001, size=c_out).astype(np.int32) if dtype == "i8"
+                else r.normal(size=c_out).astype(np.float32))
+    aug, _ = ops.pack(W.reshape(c_out, -1), n)
+    ad = ops.aug_to_device(aug)
+    xd = dev(x)
+    idx, lv, cnt = ops.compact(xd.reshape(-1, c_in))
+    tdt = torch.int8 if dtype == "i8" else torch.float32
+    plan = ops.mrs_plan(tdt, c_in, shape, kh, kw, stride, pad, c_out, n, pool, k)
+    assert plan["path"] == want[0], plan
+    if want[1] is not None:
+        assert plan["tile_mode"] == want[1], plan
+    odt = torch.int8 if shift is not None and dtype == "i8" else None
+    cap = ops.list_capacity(k) if mode == "lists" else None
+    bd = None if bias is None else dev(bias)
+
+    def run(keep):
+        y, res = ops.mrs_kwta_conv2d(idx, lv, cnt, shape, ad, kh, kw, n, stride, pad, bd, pool,
+                                     k=k, out_dtype=odt, shift=shift or 0, keep_sums=keep,
+                                     cap=cap)
+        if mode == "lists":
+            res = tuple(host(t) for t in res)
+        else:
+            res = host(res)
+        return host(y), res
+
+    y, res = run(True)
+    _, res2 = run(False)
+    if mode == "lists":
+        # entries past a row's count are unspecified; the rest must agree
+        assert np.array_equal(res[2], res2[2]), "keep_sums changed the counts"
+        live = np.arange(res[0].shape[1])[None, :] < res[2][:, None]
+        for a, b2 in zip(res[:2], res2[:2]):
+            assert np.array_equal(a[live], b2[live]), "keep_sums changed the output"
+        out = dense_from_lists(*res, c_out)
+    else:
+        assert np.array_equal(res, res2), "keep_sums changed the output"
+        out = res.reshape(-1, c_out)
+
+    ref = o.conv2d_nhwc(x, W, stride, pad, bias)
+    if pool == 2:
+        ref = o.maxpool2x2_nhwc(ref)
+    assert y.shape == ref.shape
+    win = o.kwta_winners(ref, k)
+    if dtype == "i8":
+        assert np.array_equal(y.astype(np.int64), ref), "sums"
+        if odt == torch.int8:
+            want_out = o.requant(ref, shift, win).reshape(-1, c_out)
+        else:
+            want_out = np.where(win, ref, 0).reshape(-1, c_out)
+        assert np.array_equal(out.astype(np.int64), want_out.astype(np.int64)), "k-WTA output"
+        if mode == "lists":
+            # the lists hold exactly the non-zero outputs
+            assert np.array_equal(res[2], (want_out != 0).sum(axis=1))
+    else:
+        S = o.abs_sum_conv(x, W, stride, pad)
+        if pool == 2:
+            S = pool_S(S)
+        if bias is not None:
+            S = S + np.abs(bias.astype(np.float64))
+        assert_f32_close(y, ref, S, "fused sums")
+        near = check_kwta_f32(y, out, ref, S, k)
+        assert near <= max(1, out.shape[0] // 100)
+
+
+def test_fused_partial_staging_plan():
+    """The budget case above really leaves pixels unstaged: its lists need
+    more chunks than the LDS list budget of a tile."""
+    plan = ops.mrs_plan(torch.float32, 128, (2, 24, 24, 128), 3, 3, 1, 1, 16, 4, 1, 4)
+    assert plan["path"] == "fused"
+    need = plan["npix_cap"] * 25                 # 100 entries per pixel = 25 chunks
+    assert plan["list_cap"] < need, plan
+
+
+def test_fused_column_tiles_plan():
+    plan = ops.mrs_plan(torch.float32, 64, (1, 9, 150, 64), 3, 3, 1, 1, 64, 8, 1, 8)
+    assert plan["path"] == "fused" and plan["tile_mode"] == 1
+    assert 0 < plan["tile_cols"] < 150, plan
+
+
+def test_fused_repeatable_and_overwrites():
+    """Two calls give identical bits, and stale data in the outputs is
+    overwritten (lists beyond the count are not read)."""
+    r = np.random.default_rng(77)
+    shape = (2, 11, 11, 64)
+    x = sparse_input(r, shape, 7, "f32")
+    W = weights(r, 64, 3, 3, 64, 8, "f32")
+    aug, _ = ops.pack(W.reshape(64, -1), 8)
+    ad = ops.aug_to_device(aug)
+    idx, lv, cnt = ops.compact(dev(x).reshape(-1, 64))
+    cap = ops.list_capacity(8)
+    rows = 2 * 11 * 11
+    lists = (torch.full((rows, cap), -1, dtype=torch.int16, device="cuda"),
+             torch.full((rows, cap), 7.0, dtype=torch.float32, device="cuda"),
+             torch.full((rows,), 99, dtype=torch.int32, device="cuda"))
+    y = torch.full((2, 11, 11, 64), 3.0, device="cuda")
+    ops.mrs_kwta_conv2d(idx, lv, cnt, shape, ad, 3, 3, 8, 1, 1, k=8, y=y, lists=lists)
+    a = [host(t).copy() for t in lists] + [host(y).copy()]
+    ops.mrs_kwta_conv2d(idx, lv, cnt, shape, ad, 3, 3, 8, 1, 1, k=8, y=y, lists=lists)
+    b = [host(t).copy() for t in lists] + [host(y).copy()]
+    assert (a[2] <= 8).all() and (a[2] >= 0).all()
+    assert np.array_equal(a[2], b[2]) and np.array_equal(a[3].view(np.uint32), b[3].view(np.uint32))
+    live = np.arange(cap)[None, :] < a[2][:, None]
+    assert np.array_equal(a[0][live], b[0][live])
+    assert np.array_equal(a[1][live].view(np.uint32), b[1][live].view(np.uint32))
