@@ -82,6 +82,18 @@ def layer_costs(net, bufs, cfg) -> dict:
                 costs[f"{s.name}.compact"] = {"bytes": rows * c * es + lists}
             mrs_bytes = lists + table + bias + out_elems * 4
         prods = conv_products(cnt.reshape(b, h, w), pl, s.c_out // s.n)
+        if s.k is not None and pl.dense_kernel:
+            # one launch: dense input, weights, the k-WTA output (lists or dense)
+            ob = 1 if s.shift is not None else 4
+            if pl.emit_lists:
+                lc = bufs.lists[li][2].cpu().numpy().astype(np.int64)
+                obytes = int(lc.sum()) * (2 + ob) + len(lc) * 4
+            else:
+                obytes = out_elems * ob
+            sums = out_elems * 4 if net.keep_sums else 0
+            costs[f"{s.name}.dense_kwta"] = {"bytes": rows * c * es + table + bias + sums + obytes,
+                                             "products": prods, "int": is_int}
+            continue
         if s.k is not None and not pl.dense_kernel:
             # one launch: lists in, table, bias, the k-WTA output (lists or
             # dense); the sums are written only when the network keeps them

@@ -241,6 +241,28 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
                     int pool, void* y, void* stream);
 
 /*
+ * cs_conv2d_dense_kwta - the whole dense-input first layer: cs_conv2d_dense
+ * followed by k-WTA along the channels of every output pixel, with the
+ * winners emitted as lists or densely, as cs_mrs_kwta_conv2d does for a
+ * sparse input.  DEVICE memory.  For int8 with k <= 32 the convolution runs
+ * on the matrix cores (int8 MFMA; the dense contraction of Section 3.1's
+ * sparse-dense case) in the same kernel as the pool, the selection and the
+ * output, and the sums need not reach HBM; otherwise cs_conv2d_dense and
+ * cs_kwta / cs_kwta_lists run back to back on `stream`.
+ *
+ *  xt .. pool   as cs_conv2d_dense (n == 1, c_out == 64, kh*kw*c_in <= 32; the
+ *          two-kernel path, taken for fp32 or k > 32, also needs the pooled
+ *          window to hold at most 64 values, else CS_ERR_SHAPE).
+ *  y, keep_sums, k, ot, shift, out, oidx, oval, ocnt, ocap   as
+ *          cs_mrs_kwta_conv2d.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE, CS_ERR_DEVICE.
+ */
+int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                         int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                         int pool, void* y, int keep_sums, int k, cs_dtype ot, int shift, void* out,
+                         uint16_t* oidx, void* oval, int32_t* ocnt, int ocap, void* stream);
+
+/*
  * cs_kwta - k-WTA (Section 2.2.2: exactly the top k activations propagate;
  * Section 3.3.3: global k-WTA over a vector after linear layers, local k-WTA
  * along the channels of each pixel after conv layers - both are this call

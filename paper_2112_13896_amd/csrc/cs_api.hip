@@ -8,6 +8,7 @@
 #include <cmath>
 
 #include "compact_kernels.h"
+#include "conv_dense_mfma.h"
 #include "cs.h"
 #include "kwta_kernels.h"
 #include "mrs_fused.h"
@@ -760,6 +761,108 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
                          bs, yy, geo, items, fd_wp, fd_hp);
   }
   return launch_status();
+}
+
+int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                         int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                         int pool, void* y, int keep_sums, int k, cs_dtype ot, int shift, void* out,
+                         uint16_t* oidx, void* oval, int32_t* ocnt, int ocap, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  const cs_dtype at = xt == CS_I8 ? CS_I32 : CS_F32;
+  if (!(ot == at || (xt == CS_I8 && ot == CS_I8))) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !aug || !y) return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0 || shift < 0 || shift > 31) return CS_ERR_ARG;
+  if (k > c_out || c_out > CS_MAX_KWTA_ROW) return CS_ERR_SHAPE;
+  const bool lists = oidx != nullptr;
+  if (lists == (out != nullptr)) return CS_ERR_ARG;
+  if (lists && (!oval || !ocnt || ocap < 1)) return CS_ERR_ARG;
+  if (lists && ocap < k) return CS_ERR_SHAPE;
+  const int R = kh * kw * c_in;
+  if (n != 1 || c_out != 64 || R > 32) return CS_ERR_SHAPE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int osz = ot == CS_I8 ? 1 : 4;
+  const cs::ListOut lo{oidx, oval, ocnt, lists ? ocap : 0};
+  const int Hp = geo.Ho / pool, Wp = geo.Wo / pool;
+  const int64_t items = (int64_t)b * Hp * Wp;
+  const bool lists_ok = !lists || (ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, osz * 4));
+  if (xt == CS_I8 && k <= 32 && lists_ok && items * 64 < INT32_MAX) {
+    // matrix-core kernel: pooled rows per workgroup for about 512 workgroups
+    int tiles = (int)((512 + b - 1) / b);
+    tiles = tiles < 1 ? 1 : (tiles > Hp ? Hp : tiles);
+    int tpr = (Hp + tiles - 1) / tiles;
+    size_t shmem = 0;
+    cs::DenseArgs da{};
+    for (; tpr >= 1; --tpr) {
+      const int rows_in = (tpr * pool - 1) * stride + kh;
+      const size_t items_t = (size_t)tpr * Wp;
+      size_t o = round16((size_t)rows_in * w * c_in);
+      da.off_out = (uint32_t)o;
+      o += round16(items_t * 65 * 4);
+      da.off_sel = (uint32_t)o;
+      o += round16(items_t * 8);
+      da.off_lidx = (uint32_t)o;
+      o += lists ? round16(items_t * ocap * 2) : 0;
+      da.off_lval = (uint32_t)o;
+      o += lists ? round16(items_t * ocap * osz) : 0;
+      if (o <= kFusedLds) {
+        shmem = o;
+        break;
+      }
+    }
+    if (tpr >= 1) {
+      da.TPR = tpr;
+      da.tiles_img = (Hp + tpr - 1) / tpr;
+      da.R = R;
+      da.k = k;
+      da.shift = shift;
+      da.kmode = k <= 8 ? 1 : (k <= 16 ? 2 : 3);
+      da.write_sums = keep_sums;
+      da.ostride = 65;
+      da.fd_wp = cs::make_fastdiv((uint32_t)Wp);
+      da.fd_timg = cs::make_fastdiv((uint32_t)da.tiles_img);
+      da.fd_cout = cs::make_fastdiv(64u);
+      da.fd_ochunks = cs::make_fastdiv((uint32_t)(lists ? ocap / 4 : 1));
+      const int64_t nb = (int64_t)b * da.tiles_img;
+      if (nb < INT32_MAX) {
+        const dim3 grid((unsigned)nb), block(256);
+        const auto* xx = static_cast<const int8_t*>(x);
+        const auto* pa = static_cast<const uint16_t*>(aug);
+        const auto* bs = static_cast<const int32_t*>(bias);
+        auto* yy = static_cast<int32_t*>(y);
+        if (pool == 2) {
+          if (ot == CS_I8)
+            hipLaunchKernelGGL((cs::conv_dense_mfma<2, int8_t>), grid, block, shmem, s, xx, pa, bs,
+                               yy, static_cast<int8_t*>(out), lo, geo, da);
+          else
+            hipLaunchKernelGGL((cs::conv_dense_mfma<2, int32_t>), grid, block, shmem, s, xx, pa,
+                               bs, yy, static_cast<int32_t*>(out), lo, geo, da);
+        } else {
+          if (ot == CS_I8)
+            hipLaunchKernelGGL((cs::conv_dense_mfma<1, int8_t>), grid, block, shmem, s, xx, pa, bs,
+                               yy, static_cast<int8_t*>(out), lo, geo, da);
+          else
+            hipLaunchKernelGGL((cs::conv_dense_mfma<1, int32_t>), grid, block, shmem, s, xx, pa,
+                               bs, yy, static_cast<int32_t*>(out), lo, geo, da);
+        }
+        return launch_status();
+      }
+    }
+  }
+  // two kernels: the sums into y (pooled window of at most 64 values), then k-WTA from y
+  st = cs_conv2d_dense(xt, x, b, h, w, c_in, kh, kw, stride, pad, aug, c_out, n, bias, pool, y,
+                       stream);
+  if (st != CS_OK) return st;
+  if (xt == CS_F32)
+    return kwta_dispatch(static_cast<const float*>(y), items, c_out, k, static_cast<float*>(out),
+                         0, s, lo);
+  if (ot == CS_I8)
+    return kwta_dispatch(static_cast<const int32_t*>(y), items, c_out, k,
+                         static_cast<int8_t*>(out), shift, s, lo);
+  return kwta_dispatch(static_cast<const int32_t*>(y), items, c_out, k, static_cast<int32_t*>(out),
+                       0, s, lo);
 }
 
 int cs_linear(cs_dtype xt, const void* x, int batch, int d_in, const void* aug, int d_out, int n,

@@ -107,38 +107,93 @@ struct RowMap {
   }
 };
 
-// k-WTA with one lane per item: the lane inserts its item's c keys into a
-// descending top-KMAX list (a max/min exchange per slot, no branches); the
-// k-th entry is the threshold key T.  A second pass over the row finds the
-// index of the last tie that still wins (ties go to the lower index; -1 if
-// none) and, for list output, writes the winners with a non-zero output value
-// to the tile's LDS lists in index order and their count to cnt.  Rows are
-// read with an odd stride, so the 64 lanes of a wavefront hit 64 banks.
-// k == 0 and k >= c need no search (none / every element wins).
+// Exchanges within a quad of lanes (DPP quad permutations, no LDS).
+__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);   // [1,0,3,2]
+}
+__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);   // [2,3,0,1]
+}
+__device__ __forceinline__ int quad_excl_sum(int v, int qd) {
+  // Hillis-Steele over the 4 lanes: from lane qd-1, then from lane qd-2
+  int x = v;
+  const int t1 = __builtin_amdgcn_update_dpp(0, x, 0x90, 0xF, 0xF, false);        // [0,0,1,2]
+  x += qd >= 1 ? t1 : 0;
+  const int t2 = __builtin_amdgcn_update_dpp(0, x, 0x40, 0xF, 0xF, false);        // [0,0,0,1]
+  x += qd >= 2 ? t2 : 0;
+  return x - v;
+}
+
+// Insert x into the descending list top[] (a max/min exchange per slot).
+template <int KMAX>
+__device__ __forceinline__ void topk_insert(uint32_t (&top)[KMAX], uint32_t x) {
+#pragma unroll
+  for (int s = 0; s < KMAX; ++s) {
+    const uint32_t hi = top[s] > x ? top[s] : x;
+    x = top[s] > x ? x : top[s];
+    top[s] = hi;
+  }
+}
+
+// k-WTA with four lanes per item (a quad): each lane inserts the keys of its
+// quarter of the row into a descending top-KMAX list, the quad merges the four
+// lists (two exchange steps) and reads the threshold key T = the k-th largest.
+// The winners are key > T and the first `need` keys equal to T in index
+// order (ties go to the lower index); a quad prefix sum gives each lane its
+// ties' ranks and its winners' positions in the row's list.  List output: the
+// winners with a non-zero output value go to the tile's LDS lists in index
+// order and their count to cnt.  sel[it] = (T, index of the last winning tie
+// or -1).  Rows are read with an odd stride (bank-conflict free).
 template <typename A, typename TO, int KMAX>
-__device__ void kwta_lane_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
+__device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
                                 int c, int k, int shift, uint2* sel, uint16_t* tl_idx,
                                 TO* tl_val, int cap, int32_t* gcnt) {
-  for (int it = threadIdx.x; it < sm.nslots; it += MRS_BD) {
-    if (!sm.live(it)) continue;
-    const A* v = otile + it * ostride;
+  constexpr int BK = 16;                               // keys read per batch (loads issued together)
+  const int qd = threadIdx.x & 3;
+  const int L = (c + 3) >> 2;                          // row quarter of a lane
+  const int i_lo = qd * L, i_hi = min(c, i_lo + L);
+  const int nsl = (sm.nslots + 3) & ~3;
+  for (int base = 0; base < ((nsl + MRS_BD / 4 - 1) / (MRS_BD / 4)) * (MRS_BD / 4);
+       base += MRS_BD / 4) {
+    const int it = base + (threadIdx.x >> 2);
+    const bool live = sm.live(it);                     // the same for the 4 lanes of the quad
+    const A* v = otile + (live ? it : 0) * ostride;
+    // --- the threshold: per-lane top-KMAX of the quarter, merged over the quad
+    uint32_t top[KMAX];
+#pragma unroll
+    for (int s = 0; s < KMAX; ++s) top[s] = 0u;
+    const bool search = live && k > 0 && k < c;
+    if (search) {
+      for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
+        uint32_t xs[BK];
+#pragma unroll
+        for (int j = 0; j < BK; ++j) {
+          const int i = i0 + j;
+          const uint32_t kx = order_key(v[i < i_hi ? i : i_hi - 1]);
+          xs[j] = i < i_hi ? kx : 0u;                  // a 0 never changes the k-th largest
+        }
+#pragma unroll
+        for (int j = 0; j < BK; ++j) topk_insert<KMAX>(top, xs[j]);
+      }
+    }
+    // merge with the neighbour at distance 1, then 2 (all four lanes end equal);
+    // executed by every lane of the wavefront (DPP reads the partner's registers)
+    {
+      uint32_t px[KMAX];
+#pragma unroll
+      for (int s = 0; s < KMAX; ++s) px[s] = quad_xor1(top[s]);
+#pragma unroll
+      for (int s = 0; s < KMAX; ++s) topk_insert<KMAX>(top, px[s]);
+#pragma unroll
+      for (int s = 0; s < KMAX; ++s) px[s] = quad_xor2(top[s]);
+#pragma unroll
+      for (int s = 0; s < KMAX; ++s) topk_insert<KMAX>(top, px[s]);
+    }
     uint32_t thr = 0u;
     int need = 0;
     if (k >= c) {
-      need = c;                                          // every element: key >= 0, all "ties"
+      need = c;                                        // every element wins (key >= 0)
     } else if (k > 0) {
-      uint32_t top[KMAX];
-#pragma unroll
-      for (int s = 0; s < KMAX; ++s) top[s] = 0u;
-      for (int i = 0; i < c; ++i) {
-        uint32_t x = order_key(v[i]);
-#pragma unroll
-        for (int s = 0; s < KMAX; ++s) {
-          const uint32_t hi = top[s] > x ? top[s] : x;
-          x = top[s] > x ? x : top[s];
-          top[s] = hi;
-        }
-      }
 #pragma unroll
       for (int s = 0; s < KMAX; ++s) thr = (s == k - 1) ? top[s] : thr;
       int gt = 0;
@@ -146,33 +201,74 @@ __device__ void kwta_lane_items(const A* otile, int ostride, const SlotMap& sm, 
       for (int s = 0; s < KMAX; ++s) gt += (s < k && top[s] > thr) ? 1 : 0;
       need = k - gt;
     }
-    // winners: key > T, or key == T among the first `need` ties
-    int last_tie = -1, ties = 0, pos = 0;
-    const bool any = k > 0;
-    for (int i = 0; i < c; ++i) {
-      const A a = v[i];
-      const uint32_t key = order_key(a);
-      bool win = false;
-      if (any) {
-        if (key > thr) {
-          win = true;
-        } else if (key == thr && ties < need) {
-          win = true;
-          ++ties;
-          last_tie = i;
-        }
-      }
-      if (tl_idx) {
-        const TO ov = kwta_out<A, TO>(a, shift);
-        if (win && ov != TO(0)) {
-          tl_idx[it * cap + pos] = (uint16_t)i;
-          tl_val[it * cap + pos] = ov;
-          ++pos;
+    // --- counts of this lane's quarter: ties with T, then winners with output != 0
+    int ties_l = 0;
+    if (live && k > 0) {
+      for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
+#pragma unroll
+        for (int j = 0; j < BK; ++j) {
+          const int i = i0 + j;
+          const uint32_t key = order_key(v[i < i_hi ? i : i_hi - 1]);
+          ties_l += (i < i_hi && key == thr) ? 1 : 0;
         }
       }
     }
-    sel[it] = make_uint2(thr, (uint32_t)last_tie);
-    if (tl_idx) gcnt[rm.row(it)] = pos;
+    const int tie0 = quad_excl_sum(ties_l, qd);          // ties in the quarters before
+    int win_l = 0, last_tie = -1;
+    {
+      int tr = tie0;
+      if (live && k > 0) {
+        for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
+#pragma unroll
+          for (int j = 0; j < BK; ++j) {
+            const int i = i0 + j;
+            const A a = v[i < i_hi ? i : i_hi - 1];
+            const uint32_t key = order_key(a);
+            const bool in = i < i_hi;
+            const bool tie = in && key == thr && tr < need;
+            tr += (in && key == thr) ? 1 : 0;
+            last_tie = tie ? i : last_tie;
+            const bool win = (in && key > thr) || tie;
+            win_l += (win && kwta_out<A, TO>(a, shift) != TO(0)) ? 1 : 0;
+          }
+        }
+      }
+    }
+    const int pos0 = quad_excl_sum(win_l, qd);           // list position of the first winner
+    // the last winning tie of the row: the largest over the quad
+    {
+      uint32_t lt = (uint32_t)(last_tie + 1);
+      uint32_t o1 = quad_xor1(lt);
+      lt = o1 > lt ? o1 : lt;
+      uint32_t o2 = quad_xor2(lt);
+      lt = o2 > lt ? o2 : lt;
+      last_tie = (int)lt - 1;
+    }
+    if (live) {
+      if (tl_idx && win_l > 0) {
+        int tr = tie0, pos = pos0;
+        for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
+#pragma unroll
+          for (int j = 0; j < BK; ++j) {
+            const int i = i0 + j;
+            const A a = v[i < i_hi ? i : i_hi - 1];
+            const uint32_t key = order_key(a);
+            const bool in = i < i_hi;
+            const bool tie = in && key == thr && tr < need;
+            tr += (in && key == thr) ? 1 : 0;
+            const bool win = k > 0 && ((in && key > thr) || tie);
+            const TO ov = kwta_out<A, TO>(a, shift);
+            if (win && ov != TO(0)) {
+              tl_idx[it * cap + pos] = (uint16_t)i;
+              tl_val[it * cap + pos] = ov;
+              ++pos;
+            }
+          }
+        }
+      }
+      if (qd == 0) sel[it] = make_uint2(thr, (uint32_t)last_tie);
+      if (tl_idx && qd == 3) gcnt[rm.row(it)] = pos0 + win_l;
+    }
   }
 }
 
@@ -607,15 +703,15 @@ __global__ __launch_bounds__(MRS_BD) void mrs_fused(const uint16_t* __restrict__
     TO* tl_val = reinterpret_cast<TO*>(smem + fa.off_lval);     // [slots][cap] lists of the tile
     switch (fa.kmode) {
       case 1:
-        kwta_lane_items<A, TO, 8>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
+        kwta_quad_items<A, TO, 8>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
                                   tl_val, lo.cap, lo.cnt);
         break;
       case 2:
-        kwta_lane_items<A, TO, 16>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
+        kwta_quad_items<A, TO, 16>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
                                    tl_val, lo.cap, lo.cnt);
         break;
       default:
-        kwta_lane_items<A, TO, 32>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
+        kwta_quad_items<A, TO, 32>(otile, ostride, sm, rm, c_out, fa.k, fa.shift, sel, tl_idx,
                                    tl_val, lo.cap, lo.cnt);
         break;
     }

@@ -19,8 +19,9 @@ their indices"):
     reach HBM only when keep_sums is set (tests) - a layer whose packed table
     is too large for one workgroup falls back inside the library to separate
     sum and k-WTA kernels;
-  * a layer without k-WTA writes its sums (cs_mrs_conv2d); after the dense
-    sparse-dense first layer, k-WTA is a separate call (cs_kwta_lists).
+  * a dense first layer runs as the sparse-dense variant (dense input, dense
+    weights), with k-WTA in the same call (cs_conv2d_dense_kwta);
+  * a layer without k-WTA writes its sums (cs_mrs_conv2d / cs_conv2d_dense).
 A linear layer that follows a conv layer reads the conv output's per-pixel
 lists as a convolution whose window is the whole h x w map: its slots
 (h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
@@ -188,6 +189,17 @@ class Network:
         acc4 = acc.reshape(b, -1, 1, s.c_out) if acc.dim() == 2 else acc
         odt = torch.int8 if s.shift is not None else None
         shift = s.shift if s.shift is not None else 0
+        if pl.dense_kernel and s.k is not None:
+            # sparse-dense variant with k-WTA: dense activations, no compaction,
+            # one call (the convolution on the matrix cores where it applies)
+            t.start(f"{s.name}.dense_kwta")
+            ops.conv2d_dense_kwta(x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                                  pl.pool, k=s.k, out_dtype=odt, shift=shift, y=acc,
+                                  keep_sums=self.keep_sums,
+                                  lists=B.lists[li] if pl.emit_lists else None,
+                                  out=None if pl.emit_lists else B.out[li])
+            t.stop(f"{s.name}.dense_kwta")
+            return B.out[li]
         if pl.dense_kernel:
             # sparse-dense variant: dense activations, no compaction
             t.start(f"{s.name}.mrs")
@@ -256,8 +268,8 @@ class Network:
             s = p.spec
             if not pl.in_lists and not pl.dense_kernel:
                 names.append(f"{s.name}.compact")
-            if s.k is not None and not pl.dense_kernel:
-                names.append(f"{s.name}.mrs_kwta")
+            if s.k is not None:
+                names.append(f"{s.name}.dense_kwta" if pl.dense_kernel else f"{s.name}.mrs_kwta")
                 continue
             names.append(f"{s.name}.mrs")
             if s.k is not None:

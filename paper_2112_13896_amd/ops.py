@@ -262,6 +262,50 @@ def conv2d_dense(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
     return out
 
 
+def conv2d_dense_kwta(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
+                      stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None,
+                      pool: int = 1, *, k: int, out_dtype: torch.dtype | None = None,
+                      shift: int = 0, y: torch.Tensor | None = None, keep_sums: bool = True,
+                      cap: int | None = None, lists=None, out: torch.Tensor | None = None):
+    """The dense-input first layer with k-WTA (cs_conv2d_dense_kwta).  Returns
+    (y, result) as mrs_kwta_conv2d does."""
+    if x.dim() != 4:
+        raise ValueError("x must be NHWC")
+    b, h, w, c_in = x.shape
+    pa, c_out = _aug(aug, x.dtype, n)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    acc_dt = torch.int32 if x.dtype == torch.int8 else torch.float32
+    odt = acc_dt if out_dtype is None else out_dtype
+    oshape = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    if y is None:
+        y = torch.empty(oshape, dtype=acc_dt, device=x.device)
+    if lists is None and cap is not None:
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=x.device),
+                 torch.empty((rows, cap), dtype=odt, device=x.device),
+                 torch.empty((rows,), dtype=torch.int32, device=x.device))
+    if lists is not None:
+        oi, ov, oc = lists
+        if oi.dtype != torch.int16 or ov.dtype != odt or oc.dtype != torch.int32:
+            raise TypeError("list buffer dtypes do not match")
+        if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+            raise ValueError("list buffer shapes do not match the output")
+        args = (None, _dev(oi, "oidx"), _dev(ov, "oval"), _dev(oc, "ocnt"), oi.shape[1])
+        result = lists
+    else:
+        if out is None:
+            out = torch.empty(oshape, dtype=odt, device=x.device)
+        if out.dtype != odt or out.numel() != rows * c_out:
+            raise ValueError("out does not match the output")
+        args = (_dev(out, "out"), None, None, None, 0)
+        result = out
+    check("cs_conv2d_dense_kwta", lib().cs_conv2d_dense_kwta(
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n,
+        _opt(bias, "bias"), pool, _dev(y, "y"), 1 if keep_sums else 0, k, _TORCH_DT[odt], shift,
+        *args, _stream()))
+    return y, result
+
+
 def linear(x: torch.Tensor, aug: torch.Tensor, n: int,
            bias: torch.Tensor | None = None, ws: torch.Tensor | None = None,
            out: torch.Tensor | None = None) -> torch.Tensor:

@@ -212,3 +212,82 @@ def test_fused_repeatable_and_overwrites():
     live = np.arange(cap)[None, :] < a[2][:, None]
     assert np.array_equal(a[0][live], b[0][live])
     assert np.array_equal(a[1][live].view(np.uint32), b[1][live].view(np.uint32))
+
+
+# ------------------------------------------------------------------ dense first layer
+# dtype, (b, h, w, c_in), kh, kw, stride, pad, pool, k, bias, shift, out
+DENSE_KWTA_CASES = [
+    ("i8", (5, 32, 32, 1), 5, 5, 1, 0, 2, 8, False, 11, "lists"),     # keyword-spotting conv1
+    ("i8", (3, 20, 18, 1), 5, 5, 1, 0, 2, 8, True, 7, "dense"),
+    ("i8", (2, 13, 11, 2), 3, 3, 1, 1, 1, 12, True, None, "lists"),   # no pool, pad, 2 channels
+    ("i8", (2, 16, 16, 3), 3, 3, 2, 1, 2, 5, False, 4, "lists"),      # stride 2
+    ("i8", (2, 12, 12, 1), 5, 5, 1, 2, 2, 0, False, 3, "lists"),      # k = 0
+    ("i8", (4, 12, 12, 1), 3, 3, 1, 1, 2, 8, False, 0, "lists"),      # ties: +-1 weights, 0/1 input
+    ("i8", (2, 12, 12, 1), 5, 5, 1, 0, 2, 40, False, 6, "lists"),     # k > 32: two kernels
+    ("f32", (2, 14, 14, 1), 5, 5, 1, 0, 2, 8, True, None, "dense"),   # fp32: two kernels
+]
+
+
+@pytest.mark.parametrize("case", DENSE_KWTA_CASES,
+                         ids=[f"{c[0]}-{c[1]}-{c[2]}x{c[3]}-p{c[6]}-k{c[7]}-{c[10]}"
+                              for c in DENSE_KWTA_CASES])
+def test_dense_kwta_layer(case):
+    dtype, shape, kh, kw, stride, pad, pool, k, has_bias, shift, mode = case
+    r = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    b, h, w, c_in = shape
+    ties = shift == 0
+    if dtype == "i8":
+        x = (r.integers(0, 2, size=shape) if ties else r.integers(-127, 128, size=shape)).astype(np.int8)
+        W = r.integers(-127, 128, size=(64, kh, kw, c_in)).astype(np.int8)
+        W[W == 0] = 1
+        if ties:
+            W = np.sign(W).astype(np.int8)
+    else:
+        x = r.normal(size=shape).astype(np.float32)
+        W = r.normal(size=(64, kh, kw, c_in)).astype(np.float32)
+    bias = None
+    if has_bias:
+        bias = (r.integers(-1000, 1001, size=64).astype(np.int32) if dtype == "i8"
+                else r.normal(size=64).astype(np.float32))
+    aug, _ = ops.pack(W.reshape(64, -1), 1)
+    ad = ops.aug_to_device(aug)
+    odt = torch.int8 if shift is not None and dtype == "i8" else None
+    cap = ops.list_capacity(k) if mode == "lists" else None
+    bd = None if bias is None else dev(bias)
+
+    def run(keep):
+        y, res = ops.conv2d_dense_kwta(dev(x), ad, kh, kw, 1, stride, pad, bd, pool, k=k,
+                                       out_dtype=odt, shift=shift or 0, keep_sums=keep, cap=cap)
+        res = tuple(host(t) for t in res) if mode == "lists" else host(res)
+        return host(y), res
+
+    y, res = run(True)
+    _, res2 = run(False)
+    if mode == "lists":
+        assert np.array_equal(res[2], res2[2])
+        live = np.arange(res[0].shape[1])[None, :] < res[2][:, None]
+        for a, b2 in zip(res[:2], res2[:2]):
+            assert np.array_equal(a[live], b2[live]), "keep_sums changed the output"
+        out = dense_from_lists(*res, 64)
+    else:
+        assert np.array_equal(res, res2)
+        out = res.reshape(-1, 64)
+    ref = o.conv2d_nhwc(x, W, stride, pad, bias)
+    if pool == 2:
+        ref = o.maxpool2x2_nhwc(ref)
+    win = o.kwta_winners(ref, k)
+    if dtype == "i8":
+        assert np.array_equal(y.astype(np.int64), ref), "sums"
+        want = (o.requant(ref, shift, win) if odt == torch.int8
+                else np.where(win, ref, 0)).reshape(-1, 64)
+        assert np.array_equal(out.astype(np.int64), want.astype(np.int64)), "k-WTA output"
+        if mode == "lists":
+            assert np.array_equal(res[2], (want != 0).sum(axis=1))
+    else:
+        S = o.abs_sum_conv(x, W, stride, pad)
+        if pool == 2:
+            S = pool_S(S)
+        if bias is not None:
+            S = S + np.abs(bias.astype(np.float64))
+        assert_f32_close(y, ref, S, "dense sums")
+        check_kwta_f32(y, out, ref, S, k)
