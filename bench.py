@@ -7,10 +7,15 @@ A step is one pass of the whole chain over one batch: per layer, compaction
 of the activations into (index, value) lists (dense inputs only),
 multiply-route-sum (+ bias, + 2x2 max-pool), k-WTA (+ int8 requantisation)
 emitting the next layer's lists; where a layer's packed table fits one
-workgroup the last three are one kernel and the sums never reach HBM.  Inputs are resident in HBM
-when the timed region starts; the chain rotates among buffer sets (input +
-every intermediate) totalling more than 512 MiB, so a step does not find the
-previous step's data in the 256 MiB Infinity Cache.
+workgroup the last three are one kernel and the sums never reach HBM.  Inputs
+are resident in HBM when the timed region starts; the chain rotates among
+buffer sets (input + every intermediate) totalling more than 512 MiB, so a
+step does not find the previous step's data in the 256 MiB Infinity Cache.
+Each buffer set's pass is recorded once into a HIP graph and a timed step is
+one graph replay, so the step time is the kernels' time, not Python's launch
+overhead.  Per-kernel durations (and the roofline of the dominant kernel) come
+from graphs holding 20 launches of that one kernel, timed with HIP events on
+the replaying stream.
 
 Default workload: the keyword-spotting CNN of Table 1 (config 2, int8, batch
 256).  Prints ONE JSON line on stdout; progress goes to stderr.
@@ -31,6 +36,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "sparse-sparse layer samples/s + dense-equiv GMAC/s; achieved HBM GB/s (1 GPU)"
 HBM_PEAK_GBS = 8000.0               # MI355X HBM3E, published
+KREP = 20                           # launches per graph when timing one kernel
 INT_VALU_PEAK_TOPS = 78.6           # 256 CU x 64 lanes x 2.4 GHz x (mul+add) int32 VALU
 FP32_VALU_PEAK_TFLOPS = 157.3       # published fp32 vector peak
 
@@ -222,7 +228,7 @@ def main() -> int:
 
     import torch
 
-    from paper_2112_13896_amd.network import EventTimer, Network
+    from paper_2112_13896_amd.network import Network
     from workloads import CONFIGS, generate
 
     if not torch.cuda.is_available():
@@ -252,32 +258,49 @@ def main() -> int:
     xs = [torch.from_numpy(inp["x"]).cuda() for _ in range(nsets)]
     log(f"bench: {nsets} rotating buffer sets of {per_set / 2 ** 20:.1f} MiB")
 
-    def step(i, timer=None):
-        j = i % nsets
-        net.forward(xs[j], sets[j], timer)
-
     for i in range(args.warmup):
-        step(i)
+        net.forward(xs[i % nsets], sets[i % nsets])
     torch.cuda.synchronize()
-    # per-kernel breakdown (untimed pass) to find the dominant kernel
-    brk = EventTimer()
-    for i in range(max(nsets, 8)):
-        step(i, brk)
-    breakdown = brk.mean_ms()
+    # one HIP graph per buffer set: a step is one replay (every layer's kernels,
+    # no per-launch host work)
+    graphs = [net.capture(xs[j], sets[j]) for j in range(nsets)]
+    for i in range(args.warmup):
+        graphs[i % nsets].replay()
+    torch.cuda.synchronize()
+
+    # per-kernel durations: each launch recorded KREP times into a graph of its
+    # own, replayed with HIP events on the replaying stream around it
+    def kernel_ms(call, reps=4):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(KREP):
+                call()
+        g.replay()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * KREP)
+
+    launches = [nc for li in range(len(net.packed)) for nc in net.launches(
+        li, xs[0] if li == 0 else None, sets[0])]
+    breakdown = {name: kernel_ms(call) for name, call in launches}
     dominant = max(breakdown, key=breakdown.get)
     costs = layer_costs(net, sets[0], cfg)
     log("bench: per-kernel ms " + ", ".join(f"{k}={v:.4f}" for k, v in breakdown.items()))
 
-    timer = EventTimer([dominant])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i, timer)
+        graphs[i % nsets].replay()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    dom_ms = timer.mean_ms()[dominant]
     ms_step = wall * 1e3 / args.steps
     samples_s = cfg.batch / (ms_step * 1e-3)
+    # the dominant kernel again, right after the timed steps
+    dom_ms = kernel_ms(dict(launches)[dominant], reps=max(4, args.steps // KREP))
     roof = roofline_for(dominant, costs[dominant], dom_ms)
     roof["traffic"] = load_traffic(dominant, cfg.name)
     kernels = {}

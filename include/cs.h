@@ -152,8 +152,11 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
  * as (index, value) lists (Figure 10) or as a dense masked tensor.  DEVICE
  * memory.  Where the layer's packed table fits one workgroup's LDS the sums,
  * the selection and the output are produced by one kernel and the sums need
- * not reach HBM; otherwise cs_mrs_conv2d and cs_kwta / cs_kwta_lists run
- * back to back on `stream`.
+ * not reach HBM; so they are too for a layer with one output vector per
+ * sample (a linear layer: window = the whole unpadded map, output 1 x 1, no
+ * pool; at most 1024 input pixels) whose table is larger, one workgroup per
+ * sample reading the table from global memory; otherwise cs_mrs_conv2d and
+ * cs_kwta / cs_kwta_lists run back to back on `stream`.
  *
  *  xt .. pool   as cs_mrs_conv2d.
  *  y       device NHWC [b][ho/pool][wo/pool][c_out] (int32 / fp32), always
@@ -189,7 +192,10 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
  *  xt .. pool  as cs_mrs_kwta_conv2d; cap: list row stride; k: winners, or -1
  *          for cs_mrs_conv2d (sums only).
  *  info    host int64[11] out: [0] path (0 one lane per output, 1 table-slice
- *          kernel, 2 fused layer kernel); for path 2: [1] tile mode (0 rows of
+ *          kernel, 2 fused layer kernel, 3 one workgroup per sample: a layer
+ *          whose window is the whole unpadded input map, output 1 x 1, no
+ *          pool - a linear layer); for path 3: [6] workgroups, [7] LDS bytes
+ *          per workgroup, [8] entry slices per packed set; for path 2: [1] tile mode (0 rows of
  *          items, 1 image rectangles), [2] items (mode 0) or pooled rows
  *          (mode 1) per tile, [3] pooled columns per tile (mode 1), [4] list
  *          chunks staged in LDS at most, [5] input pixels per tile at most,

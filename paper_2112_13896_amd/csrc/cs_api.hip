@@ -13,6 +13,7 @@
 #include "kwta_kernels.h"
 #include "mrs_fused.h"
 #include "mrs_kernels.h"
+#include "mrs_sample.h"
 #include "mrs_tiled.h"
 
 namespace {
@@ -442,6 +443,87 @@ int launch_fused(const FusedPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stre
   return launch_status();
 }
 
+// ------------------------------------------------ one sample per workgroup
+// A layer whose output is one vector per sample (a linear layer, or a
+// convolution whose window is the whole unpadded input map) runs with one
+// workgroup per sample when its table is too large for the fused kernel.
+struct SamplePlan {
+  cs::SampleArgs sa;
+  size_t shmem;
+};
+
+bool sample_plan(const cs::ConvGeom& geo, cs_dtype xt, int k, int shift, int write_sums,
+                 SamplePlan* pl) {
+  if (geo.Ho != 1 || geo.Wo != 1 || geo.pool != 1 || geo.KH != geo.H || geo.KW != geo.W ||
+      geo.P != 0)
+    return false;
+  const int npix = geo.H * geo.W;
+  if (npix > cs::SAMPLE_BD || geo.c_out > cs::SAMPLE_MAX_ROW) return false;
+  const int64_t ents = (int64_t)npix * geo.cap;
+  if ((int64_t)geo.B * ents >= INT32_MAX || (int64_t)geo.B * geo.c_out >= INT32_MAX) return false;
+  const size_t asz = 4;                                  // int32 / fp32 sums
+  const size_t fixed = round16((size_t)geo.c_out * asz) + round16((size_t)ents * 8) +
+                       round16((size_t)npix * 8) + 256 * 4 + cs::SAMPLE_MISC * 4;
+  const size_t slice = (size_t)geo.c_out * asz;
+  if (fixed + slice > kFusedLds) return false;
+  int S = cs::SAMPLE_BD / geo.G;
+  S = S < 1 ? 1 : S;
+  const int smax = (int)((kFusedLds - fixed) / slice);
+  S = S > smax ? smax : S;
+  S = S > cs::SAMPLE_MAX_SLICES ? cs::SAMPLE_MAX_SLICES : S;
+  S = S > ents ? (int)ents : S;                          // no more slices than entries
+  S = S < 1 ? 1 : S;
+  cs::SampleArgs& sa = pl->sa;
+  sa.npix = npix;
+  sa.S = S;
+  sa.jobs = S * geo.G;
+  sa.k = k;
+  sa.shift = shift;
+  sa.write_sums = write_sums;
+  size_t o = round16((size_t)S * slice);
+  sa.off_row = (uint32_t)o;
+  o += round16((size_t)geo.c_out * asz);
+  sa.off_ent = (uint32_t)o;
+  o += round16((size_t)ents * 4);
+  sa.off_val = (uint32_t)o;
+  o += round16((size_t)ents * 4);
+  sa.off_pix = (uint32_t)o;
+  o += round16((size_t)npix * 8);
+  sa.off_hist = (uint32_t)o;
+  o += 256 * 4;
+  sa.off_misc = (uint32_t)o;
+  o += cs::SAMPLE_MISC * 4;
+  pl->shmem = o;
+  (void)xt;
+  return o <= kFusedLds;
+}
+
+template <typename T, typename A, typename TO>
+void launch_sample_t(const SamplePlan& pl, hipStream_t stream, const uint16_t* idx,
+                     const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                     void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  using E = typename cs::Aug<T>::type;
+  hipLaunchKernelGGL((cs::mrs_sample<T, A, TO>), dim3(geo.B), dim3(cs::SAMPLE_BD), pl.shmem,
+                     stream, idx, static_cast<const T*>(lval), cnt, static_cast<const E*>(aug),
+                     static_cast<const A*>(bias), static_cast<A*>(y), static_cast<TO*>(out), lo,
+                     geo, pl.sa);
+}
+
+int launch_sample(const SamplePlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stream,
+                  const uint16_t* idx, const void* lval, const int32_t* cnt, const void* aug,
+                  const void* bias, void* y, void* out, const cs::ListOut& lo,
+                  const cs::ConvGeom& geo) {
+  if (xt == CS_F32)
+    launch_sample_t<float, float, float>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  else if (ot == CS_I8)
+    launch_sample_t<int8_t, int32_t, int8_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
+                                             geo);
+  else
+    launch_sample_t<int8_t, int32_t, int32_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
+                                              geo);
+  return launch_status();
+}
+
 int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
                      const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                      hipStream_t stream);
@@ -457,6 +539,10 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
       return launch_fused(fp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
                           cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   }
+  SamplePlan sp;
+  if (sample_plan(geo, xt, -1, 0, 1, &sp))
+    return launch_sample(sp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                         cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   return mrs_launch_tiled(xt, idx, lval, cnt, geo, aug, bias, y, stream);
 }
 
@@ -639,6 +725,11 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
     if (fused_plan(geo, xt, aug, y, k, shift, keep_sums, lists ? ocap : 0, osz, &fp))
       return launch_fused(fp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
+  {
+    SamplePlan sp;
+    if (sample_plan(geo, xt, k, shift, keep_sums, &sp))
+      return launch_sample(sp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
   // two kernels: the sums into y, then k-WTA from y
   st = mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, s);
   if (st != CS_OK) return st;
@@ -667,6 +758,14 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
   const int ocap = k >= 0 ? (k + 3) / 4 * 4 : 0;        // lists as the k-WTA emits them
   bool fused = cap % 4 == 0 && fused_plan(geo, xt, nullptr, nullptr, k, 0, 1,
                                           ocap < 4 ? 4 : ocap, xt == CS_I8 ? 1 : 4, &fp);
+  SamplePlan sp;
+  if (!fused && sample_plan(geo, xt, k, 0, 1, &sp)) {
+    info[0] = 3;
+    info[6] = geo.B;
+    info[7] = (int64_t)sp.shmem;
+    info[8] = sp.sa.S;
+    return CS_OK;
+  }
   if (!fused && k >= 0 && cap % 4 == 0) {
     // the sums in the fused kernel, k-WTA in its own kernel
     fused = fused_plan(geo, xt, nullptr, nullptr, -1, 0, 1, 0, 0, &fp);

@@ -536,7 +536,6 @@ __global__ __launch_bounds__(MRS_BD) void mrs_fused(const uint16_t* __restrict__
 
   // ---- compute: lanes (item of the round, set unit, sub-pixel q, slice s);
   // the Q*S lanes of one (item, set unit) are consecutive in one wavefront
-  const int Q = 1 << fa.log2Q;
   const int S = 1 << fa.log2S;
   const int log2QS = fa.log2Q + fa.log2S;
   const int QS = 1 << log2QS;
@@ -551,7 +550,6 @@ __global__ __launch_bounds__(MRS_BD) void mrs_fused(const uint16_t* __restrict__
   const int sl = r & (S - 1);                             // slice
   const int q = r >> fa.log2S;                            // 2x2 pool sub-pixel
   const int gfirst = unit * GB;                           // first set of the lane
-  const int gbase_lane = tid & ~(QS - 1);
   A* acc_lane = acc + tid;
   const unsigned char* tcol = tab + (size_t)gfirst * sizeof(E);
   const int c0 = chunk_mode ? sl : 0, cstep = chunk_mode ? S : 1;

@@ -177,64 +177,62 @@ class Network:
         return B
 
     # execution -------------------------------------------------------------
-    def forward_layer(self, li: int, x, bufs: Buffers | None = None, timer=None):
-        """x: the dense input tensor (first layer) or None (lists of layer li-1)."""
+    def launches(self, li: int, x, bufs: Buffers | None = None) -> list:
+        """The kernel launches of layer li as (name, call) pairs in order; each
+        call enqueues one library call on torch's current stream, reading and
+        writing only preallocated buffers, so a call can be replayed alone or
+        recorded into a HIP graph.  x: the dense input (first layer) or None
+        (the lists of layer li-1)."""
         B = self.bufs if bufs is None else bufs
         p = self.packed[li]
         s = p.spec
         pl = self.plans[li]
-        t = timer or _NoTimer()
         b, h, w, c = pl.geo
         acc = B.acc[li]
         acc4 = acc.reshape(b, -1, 1, s.c_out) if acc.dim() == 2 else acc
         odt = torch.int8 if s.shift is not None else None
         shift = s.shift if s.shift is not None else 0
-        if pl.dense_kernel and s.k is not None:
-            # sparse-dense variant with k-WTA: dense activations, no compaction,
-            # one call (the convolution on the matrix cores where it applies)
-            t.start(f"{s.name}.dense_kwta")
-            ops.conv2d_dense_kwta(x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
-                                  pl.pool, k=s.k, out_dtype=odt, shift=shift, y=acc,
-                                  keep_sums=self.keep_sums,
-                                  lists=B.lists[li] if pl.emit_lists else None,
-                                  out=None if pl.emit_lists else B.out[li])
-            t.stop(f"{s.name}.dense_kwta")
-            return B.out[li]
+        lists_out = B.lists[li] if pl.emit_lists else None
+        out = None if pl.emit_lists else B.out[li]
+        calls = []
         if pl.dense_kernel:
-            # sparse-dense variant: dense activations, no compaction
-            t.start(f"{s.name}.mrs")
-            ops.conv2d_dense(x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
-                             pl.pool, out=acc)
-            t.stop(f"{s.name}.mrs")
-        else:
-            if pl.in_lists:
-                idx, lval, cnt = B.lists[li - 1]
-            else:
-                t.start(f"{s.name}.compact")
-                ops.compact_into(x.reshape(b * h * w, c), B.idx[li], B.lval[li], B.cnt[li])
-                t.stop(f"{s.name}.compact")
-                idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
             if s.k is not None:
-                # one call: sums, pool, k-WTA, requantisation, lists or dense output
-                t.start(f"{s.name}.mrs_kwta")
-                ops.mrs_kwta_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride,
-                                    pl.pad, p.bias, pl.pool, k=s.k, out_dtype=odt, shift=shift,
-                                    y=acc4, keep_sums=self.keep_sums,
-                                    lists=B.lists[li] if pl.emit_lists else None,
-                                    out=None if pl.emit_lists else B.out[li])
-                t.stop(f"{s.name}.mrs_kwta")
-                return B.out[li]
-            t.start(f"{s.name}.mrs")
-            ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad,
-                           p.bias, pl.pool, out=acc4)
-            t.stop(f"{s.name}.mrs")
-        if s.k is not None:
-            t.start(f"{s.name}.kwta")
-            if pl.emit_lists:
-                ops.kwta_lists(acc, s.k, odt, shift, pl.cap_out, out=B.lists[li])
+                # sparse-dense variant with k-WTA: dense activations, no
+                # compaction, one call (on the matrix cores where it applies)
+                calls.append((f"{s.name}.dense_kwta", lambda: ops.conv2d_dense_kwta(
+                    x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, k=s.k,
+                    out_dtype=odt, shift=shift, y=acc, keep_sums=self.keep_sums,
+                    lists=lists_out, out=out)))
             else:
-                ops.kwta(acc, s.k, odt, shift, out=B.out[li])
-            t.stop(f"{s.name}.kwta")
+                calls.append((f"{s.name}.mrs", lambda: ops.conv2d_dense(
+                    x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, out=acc)))
+            return calls
+        if pl.in_lists:
+            idx, lval, cnt = B.lists[li - 1]
+        else:
+            idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
+            calls.append((f"{s.name}.compact", lambda: ops.compact_into(
+                x.reshape(b * h * w, c), idx, lval, cnt)))
+        if s.k is not None:
+            # one call: sums, pool, k-WTA, requantisation, lists or dense output
+            calls.append((f"{s.name}.mrs_kwta", lambda: ops.mrs_kwta_conv2d(
+                idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                pl.pool, k=s.k, out_dtype=odt, shift=shift, y=acc4, keep_sums=self.keep_sums,
+                lists=lists_out, out=out)))
+        else:
+            calls.append((f"{s.name}.mrs", lambda: ops.mrs_conv2d(
+                idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                pl.pool, out=acc4)))
+        return calls
+
+    def forward_layer(self, li: int, x, bufs: Buffers | None = None, timer=None):
+        """x: the dense input tensor (first layer) or None (lists of layer li-1)."""
+        B = self.bufs if bufs is None else bufs
+        t = timer or _NoTimer()
+        for name, call in self.launches(li, x, B):
+            t.start(name)
+            call()
+            t.stop(name)
         return B.out[li]
 
     def forward(self, x: torch.Tensor, bufs: Buffers | None = None, timer=None):
@@ -244,6 +242,16 @@ class Network:
         for li in range(len(self.packed)):
             out = self.forward_layer(li, x if li == 0 else None, bufs, timer)
         return out
+
+    def capture(self, x: torch.Tensor, bufs: Buffers | None = None) -> torch.cuda.CUDAGraph:
+        """Record one forward pass over x into a HIP graph: replaying it runs
+        every layer's kernels on the same buffers with no per-launch host
+        work (no library call inside allocates, synchronises or clears memory
+        with a memset node)."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.forward(x, bufs)
+        return g
 
     def dense_output(self, li: int, bufs: Buffers | None = None) -> torch.Tensor:
         """Layer li's k-WTA output as a dense tensor (scattered back from its
@@ -263,18 +271,7 @@ class Network:
         return dense.reshape(pl.out_shape)
 
     def kernel_names(self) -> list:
-        names = []
-        for pl, p in zip(self.plans, self.packed):
-            s = p.spec
-            if not pl.in_lists and not pl.dense_kernel:
-                names.append(f"{s.name}.compact")
-            if s.k is not None:
-                names.append(f"{s.name}.dense_kwta" if pl.dense_kernel else f"{s.name}.mrs_kwta")
-                continue
-            names.append(f"{s.name}.mrs")
-            if s.k is not None:
-                names.append(f"{s.name}.kwta")
-        return names
+        return [name for li in range(len(self.packed)) for name, _ in self.launches(li, None)]
 
 
 class _NoTimer:

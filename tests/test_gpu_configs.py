@@ -84,7 +84,7 @@ def test_fp32_config_layerwise(cid):
 
 
 @pytest.mark.parametrize("cid,layer,path", [(1, "linear", "fused"), (2, "conv2", "fused"),
-                                             (2, "linear1", "tiled"), (2, "output", "fused"),
+                                             (2, "linear1", "sample"), (2, "output", "fused"),
                                              (3, "conv3x3", "fused"), (4, "conv1x1", "tiled"),
                                              (4, "conv3x3", "tiled"), (5, "expand", "fused"),
                                              (5, "project", "fused")])

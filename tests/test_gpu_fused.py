@@ -9,7 +9,8 @@ oracle's only at near-ties.  Each case runs twice, keeping the sums (checked)
 and not keeping them (the benchmark's setting), and both outputs must be
 identical.  The launch plan is asserted so that every tiling path (rows of
 items, full-width image rows, column tiles, partial LDS staging with global
-reads, the two-kernel fallback) is known to run.
+reads, one workgroup per sample for large-table linear layers, the two-kernel
+fallback) is known to run.
 """
 from __future__ import annotations
 
@@ -91,8 +92,21 @@ CASES = [
     ("f32", (2, 24, 24, 128), 100, 3, 3, 1, 1, 16, 4, 1, 4, False, None, "lists", ("fused", 1)),
     # c_out not a multiple of 4: two kernels (sums, then k-WTA)
     ("i8", (3, 6, 6, 24), 5, 3, 3, 1, 1, 6, 2, 1, 2, True, 2, "lists", ("tiled", None)),
-    # a table too large for LDS: two kernels
-    ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("tiled", None)),
+    # a table too large for LDS, one output vector per sample: one workgroup
+    # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
+    ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
+    # plain linear layers: fp32 with bias, int32 dense output at the 2048 row limit
+    ("f32", (6, 1, 1, 2000), 200, 1, 1, 1, 0, 1024, 8, 1, 50, True, None, "dense", ("sample", None)),
+    ("i8", (5, 1, 1, 1600), 150, 1, 1, 1, 0, 2048, 16, 1, 200, True, None, "dense", ("sample", None)),
+    # odd set count (G = 167), k not a multiple of 4, requantised lists
+    ("i8", (3, 1, 1, 1200), 90, 1, 1, 1, 0, 1002, 6, 1, 33, True, 10, "lists", ("sample", None)),
+    # k = 0 and k = c_out
+    ("i8", (3, 1, 1, 1200), 100, 1, 1, 1, 0, 1536, 12, 1, 0, False, 9, "lists", ("sample", None)),
+    ("f32", (3, 1, 1, 1200), 100, 1, 1, 1, 0, 1536, 12, 1, 1536, False, None, "lists", ("sample", None)),
+    # ties everywhere: +-1 weights, all-one inputs, whole-map 3x3 window
+    ("i8", (4, 3, 3, 256), 20, 3, 3, 1, 0, 1000, 8, 1, 60, False, 0, "lists", ("sample", None)),
+    # 256 taps per sample (16x16 map), fp32 whole-map window
+    ("f32", (2, 16, 16, 32), 4, 16, 16, 1, 0, 512, 8, 1, 20, False, None, "lists", ("sample", None)),
 ]
 
 
@@ -170,6 +184,30 @@ def test_fused_layer(case):
         assert_f32_close(y, ref, S, "fused sums")
         near = check_kwta_f32(y, out, ref, S, k)
         assert near <= max(1, out.shape[0] // 100)
+
+
+@pytest.mark.parametrize("dtype", ["i8", "f32"])
+def test_sample_sums_only(dtype):
+    """cs_mrs_conv2d (no k-WTA) of a large-table linear layer takes the
+    one-workgroup-per-sample kernel; the sums match the oracle."""
+    r = np.random.default_rng(4242 if dtype == "i8" else 4243)
+    shape, c_out, n = (7, 1, 1, 1600), 1500, 20
+    x = sparse_input(r, shape, 160, dtype)
+    W = weights(r, c_out, 1, 1, 1600, n, dtype)
+    bias = (r.integers(-1000, 1001, size=c_out).astype(np.int32) if dtype == "i8"
+            else r.normal(size=c_out).astype(np.float32))
+    tdt = torch.int8 if dtype == "i8" else torch.float32
+    assert ops.mrs_plan(tdt, 1600, shape, 1, 1, 1, 0, c_out, n, 1, -1)["path"] == "sample"
+    aug, _ = ops.pack(W.reshape(c_out, -1), n)
+    idx, lv, cnt = ops.compact(dev(x).reshape(-1, 1600))
+    y = host(ops.mrs_conv2d(idx, lv, cnt, shape, ops.aug_to_device(aug), 1, 1, n, 1, 0,
+                            dev(bias), 1))
+    ref = o.conv2d_nhwc(x, W, 1, 0, bias)
+    if dtype == "i8":
+        assert np.array_equal(y.astype(np.int64), ref)
+    else:
+        S = o.abs_sum_conv(x, W, 1, 0) + np.abs(bias.astype(np.float64))
+        assert_f32_close(y, ref, S, "sample sums")
 
 
 def test_fused_partial_staging_plan():
