@@ -150,13 +150,13 @@ int cs_mrs_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const int3
  * the channels of every output pixel (Section 2.2.2: exactly the top k
  * activations propagate; Section 3.3.3 local k-WTA), with the winners sent on
  * as (index, value) lists (Figure 10) or as a dense masked tensor.  DEVICE
- * memory.  Where the layer's packed table fits one workgroup's LDS the sums,
- * the selection and the output are produced by one kernel and the sums need
- * not reach HBM; so they are too for a layer with one output vector per
- * sample (a linear layer: window = the whole unpadded map, output 1 x 1, no
- * pool; at most 1024 input pixels) whose table is larger, one workgroup per
- * sample reading the table from global memory; otherwise cs_mrs_conv2d and
- * cs_kwta / cs_kwta_lists run back to back on `stream`.
+ * memory.  A layer with one output vector per sample (a linear layer: window
+ * = the whole unpadded map, output 1 x 1, no pool; at most 1024 input pixels)
+ * runs as one kernel with one workgroup per sample, the table read from
+ * global memory; a layer whose packed table fits one workgroup's LDS runs as
+ * one kernel with the table in LDS; in both the sums need not reach HBM.
+ * Otherwise cs_mrs_conv2d and cs_kwta / cs_kwta_lists run back to back on
+ * `stream`.
  *
  *  xt .. pool   as cs_mrs_conv2d.
  *  y       device NHWC [b][ho/pool][wo/pool][c_out] (int32 / fp32), always

@@ -446,7 +446,7 @@ int launch_fused(const FusedPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stre
 // ------------------------------------------------ one sample per workgroup
 // A layer whose output is one vector per sample (a linear layer, or a
 // convolution whose window is the whole unpadded input map) runs with one
-// workgroup per sample when its table is too large for the fused kernel.
+// workgroup per sample, whatever the size of its table.
 struct SamplePlan {
   cs::SampleArgs sa;
   size_t shmem;
@@ -461,41 +461,44 @@ bool sample_plan(const cs::ConvGeom& geo, cs_dtype xt, int k, int shift, int wri
   if (npix > cs::SAMPLE_BD || geo.c_out > cs::SAMPLE_MAX_ROW) return false;
   const int64_t ents = (int64_t)npix * geo.cap;
   if ((int64_t)geo.B * ents >= INT32_MAX || (int64_t)geo.B * geo.c_out >= INT32_MAX) return false;
+  // all workgroups resident at once: the whole LDS of a compute unit; else
+  // two workgroups per compute unit
+  const size_t budget = geo.B <= kPlanCus ? kCuLds : kFusedLds;
   const size_t asz = 4;                                  // int32 / fp32 sums
-  const size_t fixed = round16((size_t)geo.c_out * asz) + round16((size_t)ents * 8) +
-                       round16((size_t)npix * 8) + 256 * 4 + cs::SAMPLE_MISC * 4;
-  const size_t slice = (size_t)geo.c_out * asz;
-  if (fixed + slice > kFusedLds) return false;
+  const size_t hist_b = k >= 0 ? 2 * cs::SAMPLE_BINS * 4 : 0;
+  const size_t ent_b = round16((size_t)(ents + cs::SAMPLE_ENT_PAD) * 4);
+  const size_t fixed = round16((size_t)geo.c_out * asz) + 2 * ent_b +
+                       round16((size_t)npix * 8) + hist_b + cs::SAMPLE_MISC * 4;
+  const size_t slice = round16((size_t)geo.c_out * asz);
+  if (fixed + slice > budget) return false;
   int S = cs::SAMPLE_BD / geo.G;
-  S = S < 1 ? 1 : S;
-  const int smax = (int)((kFusedLds - fixed) / slice);
+  // int32 sums share one accumulator row (LDS atomics); fp32 slices own one each
+  const int smax = xt == CS_I8 ? cs::SAMPLE_MAX_SLICES : (int)((budget - fixed) / slice);
   S = S > smax ? smax : S;
   S = S > cs::SAMPLE_MAX_SLICES ? cs::SAMPLE_MAX_SLICES : S;
-  S = S > ents ? (int)ents : S;                          // no more slices than entries
   S = S < 1 ? 1 : S;
+  const int acc_rows = xt == CS_I8 ? 1 : S;
   cs::SampleArgs& sa = pl->sa;
   sa.npix = npix;
   sa.S = S;
-  sa.jobs = S * geo.G;
   sa.k = k;
   sa.shift = shift;
   sa.write_sums = write_sums;
-  size_t o = round16((size_t)S * slice);
+  size_t o = (size_t)acc_rows * slice;
   sa.off_row = (uint32_t)o;
   o += round16((size_t)geo.c_out * asz);
   sa.off_ent = (uint32_t)o;
-  o += round16((size_t)ents * 4);
+  o += ent_b;
   sa.off_val = (uint32_t)o;
-  o += round16((size_t)ents * 4);
+  o += ent_b;
   sa.off_pix = (uint32_t)o;
   o += round16((size_t)npix * 8);
   sa.off_hist = (uint32_t)o;
-  o += 256 * 4;
+  o += hist_b;
   sa.off_misc = (uint32_t)o;
   o += cs::SAMPLE_MISC * 4;
   pl->shmem = o;
-  (void)xt;
-  return o <= kFusedLds;
+  return o <= budget;
 }
 
 template <typename T, typename A, typename TO>
@@ -528,21 +531,22 @@ int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const i
                      const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                      hipStream_t stream);
 
-// Sums of a layer: the fused kernel (lists staged in LDS) when the layer suits
-// it, else the table-slice kernel, else the one-lane-per-output kernel.
+// Sums of a layer: one workgroup per sample for a linear layer, else the fused
+// kernel (lists staged in LDS) when the layer suits it, else the table-slice
+// kernel, else the one-lane-per-output kernel.
 int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
                const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                hipStream_t stream) {
+  SamplePlan sp;
+  if (sample_plan(geo, xt, -1, 0, 1, &sp))
+    return launch_sample(sp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                         cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   if (lists_vectorisable(xt, idx, lval, geo.cap)) {
     FusedPlan fp;
     if (fused_plan(geo, xt, aug, y, -1, 0, 1, 0, 0, &fp))
       return launch_fused(fp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
                           cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   }
-  SamplePlan sp;
-  if (sample_plan(geo, xt, -1, 0, 1, &sp))
-    return launch_sample(sp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
-                         cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   return mrs_launch_tiled(xt, idx, lval, cnt, geo, aug, bias, y, stream);
 }
 
@@ -720,15 +724,15 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
   // the fused kernel writes lists 4 entries at a time
   const int osz = ot == CS_I8 ? 1 : 4;
   const bool lists_ok = !lists || (ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, osz * 4));
-  if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
-    FusedPlan fp;
-    if (fused_plan(geo, xt, aug, y, k, shift, keep_sums, lists ? ocap : 0, osz, &fp))
-      return launch_fused(fp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
-  }
   {
     SamplePlan sp;
     if (sample_plan(geo, xt, k, shift, keep_sums, &sp))
       return launch_sample(sp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
+  if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
+    FusedPlan fp;
+    if (fused_plan(geo, xt, aug, y, k, shift, keep_sums, lists ? ocap : 0, osz, &fp))
+      return launch_fused(fp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
   // two kernels: the sums into y, then k-WTA from y
   st = mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, s);
@@ -754,18 +758,18 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
   if (cap < 1 || k < -1 || k > c_out) return CS_ERR_SHAPE;
   geo.cap = cap;
   for (int i = 0; i < 11; ++i) info[i] = 0;
-  FusedPlan fp;
-  const int ocap = k >= 0 ? (k + 3) / 4 * 4 : 0;        // lists as the k-WTA emits them
-  bool fused = cap % 4 == 0 && fused_plan(geo, xt, nullptr, nullptr, k, 0, 1,
-                                          ocap < 4 ? 4 : ocap, xt == CS_I8 ? 1 : 4, &fp);
   SamplePlan sp;
-  if (!fused && sample_plan(geo, xt, k, 0, 1, &sp)) {
+  if (sample_plan(geo, xt, k, 0, 1, &sp)) {
     info[0] = 3;
     info[6] = geo.B;
     info[7] = (int64_t)sp.shmem;
     info[8] = sp.sa.S;
     return CS_OK;
   }
+  FusedPlan fp;
+  const int ocap = k >= 0 ? (k + 3) / 4 * 4 : 0;        // lists as the k-WTA emits them
+  bool fused = cap % 4 == 0 && fused_plan(geo, xt, nullptr, nullptr, k, 0, 1,
+                                          ocap < 4 ? 4 : ocap, xt == CS_I8 ? 1 : 4, &fp);
   if (!fused && k >= 0 && cap % 4 == 0) {
     // the sums in the fused kernel, k-WTA in its own kernel
     fused = fused_plan(geo, xt, nullptr, nullptr, -1, 0, 1, 0, 0, &fp);

@@ -74,10 +74,11 @@ CASES = [
     ("f32", (1, 9, 150, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "lists", ("fused", 1)),
     # 1x1 expand: rows of items, bias, requantised lists, ragged last tile
     ("i8", (2, 7, 9, 96), 12, 1, 1, 1, 0, 576, 8, 1, 72, True, 9, "lists", ("fused", 0)),
-    # linear, int32 dense output, bias
-    ("i8", (37, 1, 1, 512), 64, 1, 1, 1, 0, 64, 8, 1, 16, True, None, "dense", ("fused", 0)),
+    # linear, int32 dense output, bias: one workgroup per sample
+    ("i8", (37, 1, 1, 512), 64, 1, 1, 1, 0, 64, 8, 1, 16, True, None, "dense", ("sample", None)),
+    ("i8", (29, 1, 1, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("sample", None)),
     # dense kernels (n = 1), one accumulator per set in registers
-    ("i8", (29, 1, 1, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("fused", 0)),
+    ("i8", (3, 4, 5, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("fused", 0)),
     ("f32", (3, 6, 5, 40), 9, 3, 3, 1, 1, 16, 1, 1, 5, True, None, "dense", ("fused", 1)),
     # stride 2, odd input
     ("f32", (2, 17, 17, 32), 5, 3, 3, 2, 1, 32, 4, 1, 4, False, None, "lists", ("fused", 1)),
