@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "compact_kernels.h"
@@ -14,6 +15,7 @@
 #include "mrs_fused.h"
 #include "mrs_kernels.h"
 #include "mrs_sample.h"
+#include "mrs_scatter.h"
 #include "mrs_tiled.h"
 
 namespace {
@@ -527,6 +529,115 @@ int launch_sample(const SamplePlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t st
   return launch_status();
 }
 
+// ------------------------------------------- input-stationary int8 layer
+// An int8 convolution with stride 1 whose band of output rows (every column
+// and channel, int32) fits in LDS runs input-stationary: each non-zero
+// scatters its products into the band's shared accumulators.
+struct ScatterPlan {
+  cs::ScatterArgs sc;
+  size_t shmem;
+  int64_t blocks;
+  int gpl, m;
+};
+
+bool scatter_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int shift,
+                  int write_sums, ScatterPlan* pl) {
+  if (xt != CS_I8 || geo.S != 1 || geo.KH > cs::SCAT_MAX_KH) return false;
+  if (geo.KW != 3 && geo.KW != 5 && geo.KW != 7) return false;
+  if (geo.c_out > 128 || geo.W > 255 || geo.C > 65535 || !aligned(aug, 4)) return false;
+  const int64_t R = (int64_t)geo.KH * geo.KW * geo.C;
+  if ((R * geo.G) % 2 != 0 || R * geo.G * 2 >= INT32_MAX) return false;
+  const int gpl = geo.G % 2 == 0 ? 2 : 1;
+  const int ostride = geo.c_out + 16;
+  const int guard = (geo.KW * ostride + 64 + 3) & ~3;
+  const size_t tab_b = round16((size_t)R * geo.G * 2);
+  for (size_t budget : {kFusedLds, kCuLds}) {
+    for (int BR = geo.Ho; BR >= geo.pool; BR -= geo.pool) {
+      if (BR % geo.pool != 0) continue;
+      const int rows_in = std::min(BR + geo.KH - 1, geo.H);
+      const int64_t npix = (int64_t)rows_in * geo.W;
+      if (npix > cs::SCAT_BD || rows_in > 255) continue;
+      const int64_t ne = npix * geo.cap;
+      if (ne >= INT32_MAX / 2) continue;
+      const size_t acc_b = round16((size_t)(2 * guard + (int64_t)BR * geo.Wo * ostride) * 4);
+      const size_t o_tab = acc_b;
+      const size_t o_ent = o_tab + tab_b;
+      const size_t o_pix = o_ent + round16((size_t)ne * 8);
+      const size_t o_bias = o_pix + round16((size_t)npix * 8);
+      const size_t o_misc = o_bias + round16((size_t)geo.c_out * 4);
+      const size_t total = o_misc + cs::SAMPLE_MISC * 4;
+      if (total > budget) continue;
+      const int bands = (geo.Ho + BR - 1) / BR;
+      cs::ScatterArgs& sc = pl->sc;
+      sc.BR = BR;
+      sc.bands = bands;
+      sc.guard = guard;
+      sc.ostride = ostride;
+      sc.k = k;
+      sc.shift = shift;
+      sc.write_sums = write_sums;
+      sc.off_tab = (uint32_t)o_tab;
+      sc.off_ent = (uint32_t)o_ent;
+      sc.off_pix = (uint32_t)o_pix;
+      sc.off_bias = (uint32_t)o_bias;
+      sc.off_misc = (uint32_t)o_misc;
+      sc.fd_gpc = cs::make_fastdiv((uint32_t)(geo.G / gpl));
+      sc.fd_bands = cs::make_fastdiv((uint32_t)bands);
+      sc.fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / geo.pool));
+      pl->shmem = total;
+      pl->blocks = (int64_t)geo.B * bands;
+      pl->gpl = gpl;
+      pl->m = geo.c_out > 64 ? 2 : 1;
+      return pl->blocks <= INT32_MAX;
+    }
+  }
+  return false;
+}
+
+template <typename TO, int KW, int GPL, int M>
+void launch_scatter_t(const ScatterPlan& pl, hipStream_t stream, const uint16_t* idx,
+                      const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                      void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  hipLaunchKernelGGL((cs::mrs_scatter<TO, KW, GPL, M>), dim3((unsigned)pl.blocks),
+                     dim3(cs::SCAT_BD), pl.shmem, stream, idx, static_cast<const int8_t*>(lval),
+                     cnt, static_cast<const uint16_t*>(aug), static_cast<const int32_t*>(bias),
+                     static_cast<int32_t*>(y), static_cast<TO*>(out), lo, geo, pl.sc);
+}
+
+template <typename TO, int KW>
+void launch_scatter_kw(const ScatterPlan& pl, hipStream_t s, const uint16_t* idx, const void* lval,
+                       const int32_t* cnt, const void* aug, const void* bias, void* y, void* out,
+                       const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  if (pl.gpl == 2) {
+    if (pl.m == 1) launch_scatter_t<TO, KW, 2, 1>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    else launch_scatter_t<TO, KW, 2, 2>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  } else {
+    if (pl.m == 1) launch_scatter_t<TO, KW, 1, 1>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    else launch_scatter_t<TO, KW, 1, 2>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
+}
+
+template <typename TO>
+void launch_scatter_to(const ScatterPlan& pl, hipStream_t s, const uint16_t* idx,
+                       const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                       void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  switch (geo.KW) {
+    case 3: launch_scatter_kw<TO, 3>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    case 5: launch_scatter_kw<TO, 5>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    default: launch_scatter_kw<TO, 7>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+  }
+}
+
+int launch_scatter(const ScatterPlan& pl, cs_dtype ot, hipStream_t s, const uint16_t* idx,
+                   const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                   void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  if (ot == CS_I8)
+    launch_scatter_to<int8_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  else
+    launch_scatter_to<int32_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  return launch_status();
+}
+
 int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
                      const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                      hipStream_t stream);
@@ -541,6 +652,10 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   if (sample_plan(geo, xt, -1, 0, 1, &sp))
     return launch_sample(sp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
                          cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
+  ScatterPlan scp;
+  if (scatter_plan(geo, xt, aug, -1, 0, 1, &scp))
+    return launch_scatter(scp, CS_I32, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                          cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   if (lists_vectorisable(xt, idx, lval, geo.cap)) {
     FusedPlan fp;
     if (fused_plan(geo, xt, aug, y, -1, 0, 1, 0, 0, &fp))
@@ -728,6 +843,9 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
     SamplePlan sp;
     if (sample_plan(geo, xt, k, shift, keep_sums, &sp))
       return launch_sample(sp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    ScatterPlan scp;
+    if (scatter_plan(geo, xt, aug, k, shift, keep_sums, &scp))
+      return launch_scatter(scp, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
   if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
     FusedPlan fp;
@@ -764,6 +882,15 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
     info[6] = geo.B;
     info[7] = (int64_t)sp.shmem;
     info[8] = sp.sa.S;
+    return CS_OK;
+  }
+  ScatterPlan scp;
+  if (scatter_plan(geo, xt, nullptr, k, 0, 1, &scp)) {
+    info[0] = 4;
+    info[2] = scp.sc.BR;
+    info[6] = scp.blocks;
+    info[7] = (int64_t)scp.shmem;
+    info[8] = scp.gpl;
     return CS_OK;
   }
   FusedPlan fp;

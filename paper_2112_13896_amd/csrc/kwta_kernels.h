@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "fastdiv.h"
+#include "wave_ops.h"
 
 namespace cs {
 
@@ -87,12 +88,8 @@ __device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[M], i
       kmax = key[j] > kmax ? key[j] : kmax;
     }
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t a = __shfl_xor(kmin, off, 64), b = __shfl_xor(kmax, off, 64);
-    kmin = a < kmin ? a : kmin;
-    kmax = b > kmax ? b : kmax;
-  }
+  kmin = wave_min_u32(kmin);
+  kmax = wave_max_u32(kmax);
   const uint32_t diff = kmin ^ kmax;
   uint32_t T = kmax;
   if (diff != 0u) {
@@ -236,6 +233,147 @@ __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict
   }
 }
 
+// k-WTA of one row held by one wavefront: lane l holds v[j] = element
+// j*64 + l (elements >= c are not part of the row).  Winners: the k largest
+// keys, ties to the lower index; written as the row's list (non-zero outputs
+// in index order, ranked by ballot + popcount, and the count) or densely.
+template <typename TI, typename TO, int M>
+__device__ __forceinline__ void kwta_wave_row(const TI (&v)[M], int c, int k, int shift,
+                                              const ListOut& lo, TO* __restrict__ out,
+                                              int64_t row) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  const bool all_win = (k >= c);
+  const bool none_win = (k == 0);
+  uint32_t key[M];
+#pragma unroll
+  for (int j = 0; j < M; ++j) key[j] = j * 64 + lane < c ? order_key(v[j]) : 0u;
+  int need = 0;
+  uint32_t thr = 0u;
+  if (!all_win && !none_win) thr = wave_kth_largest<M>(key, c, k, &need);
+  // ranks of the ties in index order (element index = j*64 + lane)
+  int run = 0, lrun = 0;
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    const int e = j * 64 + lane;
+    const bool valid = e < c;
+    const bool eq = !all_win && !none_win && valid && key[j] == thr;
+    const uint64_t b = __ballot(eq);
+    const int rank = run + __popcll(b & below);
+    run += __popcll(b);
+    bool win;
+    if (all_win) win = valid;
+    else if (none_win) win = false;
+    else win = valid && (key[j] > thr || (eq && rank < need));
+    const TO ov = kwta_out<TI, TO>(v[j], shift);
+    if (lo.idx) {
+      // list output: non-zero winners, ranked in index order by ballot + popcount
+      const bool put = win && ov != TO(0);
+      const uint64_t pb = __ballot(put);
+      if (put) {
+        const int pos = lrun + __popcll(pb & below);
+        lo.idx[row * lo.cap + pos] = (uint16_t)e;
+        static_cast<TO*>(lo.val)[row * lo.cap + pos] = ov;
+      }
+      lrun += __popcll(pb);
+    } else if (valid) {
+      out[row * c + e] = win ? ov : TO(0);
+    }
+  }
+  if (lo.idx && lane == 0) lo.cnt[row] = lrun;
+}
+
+// k-WTA of one row held by one row of 16 lanes (lanes 16q .. 16q + 15 of a
+// wavefront hold one row each): lane r holds v[j] = element r*KPL + j
+// (elements >= c are not part of the row).  The threshold is found bit by
+// bit below the row's range (keys offset by the row minimum), counting with
+// 16-lane DPP sums; ties go to the lower index; the winners are written as the
+// row's list (non-zero outputs in index order, and the count) or densely.
+// Every lane of the wavefront must be active; `live` rows write.
+template <typename TI, typename TO, int KPL>
+__device__ __forceinline__ void kwta_row16(const TI (&v)[KPL], int c, int k, int shift, bool live,
+                                           const ListOut& lo, TO* __restrict__ out, int64_t row) {
+  const int r = threadIdx.x & 15;
+  const int i0 = r * KPL;
+  uint32_t key[KPL];
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    key[j] = order_key(v[j]);
+    if (i0 + j < c) {
+      kmin = key[j] < kmin ? key[j] : kmin;
+      kmax = key[j] > kmax ? key[j] : kmax;
+    }
+  }
+  kmin = row16_reduce(kmin, OpMin{});
+  kmax = row16_reduce(kmax, OpMax{});
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) key[j] = i0 + j < c ? key[j] - kmin : 0u;
+  const uint32_t range = kmax - kmin;
+  // winners: key > thr, and the first `need` keys (lowest indices) == thr
+  uint32_t thr = 0u;
+  int need = 0;
+  if (k == 0) {
+    thr = 0xFFFFFFFFu;
+  } else if (k >= c) {
+    need = c;
+  } else if (range == 0u) {
+    need = k;
+  } else {
+    uint32_t T = 0u;
+    for (int b = 31 - __builtin_clz(range); b >= 0; --b) {         // uniform within a row
+      const uint32_t cand = T | (1u << b);
+      int cnt = 0;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) cnt += (i0 + j < c && key[j] >= cand) ? 1 : 0;
+      cnt = (int)row16_reduce((uint32_t)cnt, OpAdd{});
+      if (cnt >= k) T = cand;
+    }
+    int gt = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) gt += (i0 + j < c && key[j] > T) ? 1 : 0;
+    thr = T;
+    need = k - (int)row16_reduce((uint32_t)gt, OpAdd{});
+  }
+  // ranks of the ties and list positions, in index order
+  int eq_l = 0;
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) eq_l += (i0 + j < c && key[j] == thr) ? 1 : 0;
+  int rank = row16_incl_sum(eq_l) - eq_l;
+  bool win[KPL];
+  TO ov[KPL];
+  int put_l = 0;
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const bool in = i0 + j < c;
+    const bool eq = in && key[j] == thr;
+    win[j] = in && (key[j] > thr || (eq && rank < need));
+    rank += eq ? 1 : 0;
+    ov[j] = kwta_out<TI, TO>(v[j], shift);
+    put_l += (win[j] && ov[j] != TO(0)) ? 1 : 0;
+  }
+  if (lo.idx) {
+    const int incl = row16_incl_sum(put_l);
+    const int total = (int)row16_reduce((uint32_t)put_l, OpAdd{});
+    if (live) {
+      int pos = incl - put_l;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        if (win[j] && ov[j] != TO(0)) {
+          lo.idx[row * lo.cap + pos] = (uint16_t)(i0 + j);
+          static_cast<TO*>(lo.val)[row * lo.cap + pos] = ov[j];
+          ++pos;
+        }
+      }
+      if (r == 0) lo.cnt[row] = total;
+    }
+  } else if (live) {
+#pragma unroll
+    for (int j = 0; j < KPL; ++j)
+      if (i0 + j < c) out[row * c + i0 + j] = win[j] ? ov[j] : TO(0);
+  }
+}
+
 constexpr int KWTA_WAVE_WAVES = 4;   // wavefronts (rows) per block of kwta_wave
 
 template <typename TI, typename TO, int M>
@@ -245,52 +383,15 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
                                                                   int shift, ListOut lo) {
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
-  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  const bool all_win = (k == c);
-  const bool none_win = (k == 0);
   for (int64_t row = (int64_t)blockIdx.x * KWTA_WAVE_WAVES + wv; row < rows;
        row += (int64_t)gridDim.x * KWTA_WAVE_WAVES) {            // uniform across the wave
     TI v[M];
-    uint32_t key[M];
 #pragma unroll
     for (int j = 0; j < M; ++j) {
       const int e = j * 64 + lane;
       v[j] = e < c ? in[row * c + e] : TI(0);
-      key[j] = e < c ? order_key(v[j]) : 0u;
     }
-    int need = 0;
-    uint32_t thr = 0u;
-    if (!all_win && !none_win) thr = wave_kth_largest<M>(key, c, k, &need);
-    // ranks of the ties in index order (element index = j*64 + lane)
-    int run = 0, lrun = 0;
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-      const int e = j * 64 + lane;
-      const bool valid = e < c;
-      const bool eq = !all_win && !none_win && valid && key[j] == thr;
-      const uint64_t b = __ballot(eq);
-      const int rank = run + __popcll(b & below);
-      run += __popcll(b);
-      bool win;
-      if (all_win) win = valid;
-      else if (none_win) win = false;
-      else win = valid && (key[j] > thr || (eq && rank < need));
-      const TO ov = kwta_out<TI, TO>(v[j], shift);
-      if (lo.idx) {
-        // list output: non-zero winners, ranked in index order by ballot + popcount
-        const bool put = win && ov != TO(0);
-        const uint64_t pb = __ballot(put);
-        if (put) {
-          const int pos = lrun + __popcll(pb & below);
-          lo.idx[row * lo.cap + pos] = (uint16_t)e;
-          static_cast<TO*>(lo.val)[row * lo.cap + pos] = ov;
-        }
-        lrun += __popcll(pb);
-      } else if (valid) {
-        out[row * c + e] = win ? ov : TO(0);
-      }
-    }
-    if (lo.idx && lane == 0) lo.cnt[row] = lrun;
+    kwta_wave_row<TI, TO, M>(v, c, k, shift, lo, out, row);
   }
 }
 

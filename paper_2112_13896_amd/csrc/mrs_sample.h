@@ -28,6 +28,7 @@
 
 #include "kwta_kernels.h"
 #include "mrs_kernels.h"
+#include "wave_ops.h"
 
 namespace cs {
 
@@ -49,32 +50,6 @@ struct SampleArgs {
   int shift;
   int write_sums;
   uint32_t off_row, off_ent, off_val, off_pix, off_hist, off_misc;   // LDS byte offsets (acc at 0)
-};
-
-// Inclusive scan over the 64 lanes of a wavefront with DPP: shifts by 1, 2,
-// 4, 8 inside each row of 16 lanes, then row 0's and row 2's last lane to
-// rows 1 and 3, then lane 31 to rows 2 and 3.  Lanes without a source take
-// the identity.  Every lane of the wavefront must be active.
-template <typename Op>
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, uint32_t id, Op op) {
-  const int iv = (int)id;
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x111, 0xf, 0xf, false));
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x112, 0xf, 0xf, false));
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x114, 0xf, 0xf, false));
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x118, 0xf, 0xf, false));
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x142, 0xa, 0xf, false));
-  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(iv, (int)v, 0x143, 0xc, 0xf, false));
-  return v;
-}
-
-struct OpAdd {
-  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; }
-};
-struct OpMin {
-  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a < b ? a : b; }
-};
-struct OpMax {
-  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; }
 };
 
 // Exclusive prefix sum of one int per thread over the workgroup; *total gets
@@ -246,8 +221,8 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
     }
   }
   if (sa.k < 0) return;                                             // uniform
-  kmin = __builtin_amdgcn_readlane(wave_incl_scan(kmin, 0xFFFFFFFFu, OpMin{}), 63);
-  kmax = __builtin_amdgcn_readlane(wave_incl_scan(kmax, 0u, OpMax{}), 63);
+  kmin = wave_min_u32(kmin);
+  kmax = wave_max_u32(kmax);
   uint32_t* wmm = reinterpret_cast<uint32_t*>(misc) + SAMPLE_BD / 64;   // [2][waves]
   if (lane == 0) {
     wmm[wv] = kmin;

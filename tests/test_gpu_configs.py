@@ -83,7 +83,7 @@ def test_fp32_config_layerwise(cid):
     assert near <= max(1, rows // 1000), f"{near} near-tie rows"
 
 
-@pytest.mark.parametrize("cid,layer,path", [(1, "linear", "sample"), (2, "conv2", "fused"),
+@pytest.mark.parametrize("cid,layer,path", [(1, "linear", "sample"), (2, "conv2", "scatter"),
                                              (2, "linear1", "sample"), (2, "output", "sample"),
                                              (3, "conv3x3", "fused"), (4, "conv1x1", "tiled"),
                                              (4, "conv3x3", "tiled"), (5, "expand", "fused"),

@@ -9,8 +9,8 @@ oracle's only at near-ties.  Each case runs twice, keeping the sums (checked)
 and not keeping them (the benchmark's setting), and both outputs must be
 identical.  The launch plan is asserted so that every tiling path (rows of
 items, full-width image rows, column tiles, partial LDS staging with global
-reads, one workgroup per sample for large-table linear layers, the two-kernel
-fallback) is known to run.
+reads, one workgroup per sample for linear layers, input-stationary int8
+convolutions, the two-kernel fallback) is known to run.
 """
 from __future__ import annotations
 
@@ -66,8 +66,10 @@ def dense_from_lists(idx, val, cnt, c):
 # dtype, (b, h, w, c_in), nnz, kh, kw, stride, pad, c_out, n, pool, k, bias, shift,
 # out ("lists"/"dense"), expected plan (path, tile mode or None)
 CASES = [
-    # keyword-spotting conv2 shape: 5x5, 2x2 pool, whole image per tile
-    ("i8", (3, 14, 14, 64), 8, 5, 5, 1, 0, 64, 16, 2, 8, False, 9, "lists", ("fused", 1)),
+    # keyword-spotting conv2 shape: 5x5, 2x2 pool, int8: input-stationary, whole image
+    ("i8", (3, 14, 14, 64), 8, 5, 5, 1, 0, 64, 16, 2, 8, False, 9, "lists", ("scatter", None)),
+    # the same layer with stride 2: the gather kernel (rectangle tiles)
+    ("i8", (2, 17, 17, 64), 8, 5, 5, 2, 2, 64, 16, 1, 8, False, 9, "lists", ("fused", 1)),
     # 3x3 pad 1, ragged image against the tiles, fp32 dense output
     ("f32", (2, 19, 13, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "dense", ("fused", 1)),
     # wide image: column tiles
@@ -85,14 +87,24 @@ CASES = [
     # 5x5 pad 2 with pool, odd number of sets (one set per lane)
     ("f32", (2, 12, 10, 16), 4, 5, 5, 1, 2, 24, 8, 2, 6, True, None, "dense", ("fused", 1)),
     # k = 0 and k = c_out
-    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 0, False, 3, "lists", ("fused", 1)),
-    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 32, True, None, "dense", ("fused", 1)),
+    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 0, False, 3, "lists", ("scatter", None)),
+    ("i8", (2, 8, 8, 32), 6, 3, 3, 1, 1, 32, 4, 1, 32, True, None, "dense", ("scatter", None)),
     # ties everywhere: +-1 weights, all-one inputs
-    ("i8", (4, 9, 9, 64), 8, 3, 3, 1, 1, 64, 16, 1, 8, False, 0, "lists", ("fused", 1)),
+    ("i8", (4, 9, 9, 64), 8, 3, 3, 1, 1, 64, 16, 1, 8, False, 0, "lists", ("scatter", None)),
     # lists that do not fit the LDS budget: some pixels are read from global memory
     ("f32", (2, 24, 24, 128), 100, 3, 3, 1, 1, 16, 4, 1, 4, False, None, "lists", ("fused", 1)),
-    # c_out not a multiple of 4: two kernels (sums, then k-WTA)
-    ("i8", (3, 6, 6, 24), 5, 3, 3, 1, 1, 6, 2, 1, 2, True, 2, "lists", ("tiled", None)),
+    # c_out not a multiple of 4, odd set count (one set per lane): input-stationary
+    ("i8", (3, 6, 6, 24), 5, 3, 3, 1, 1, 6, 2, 1, 2, True, 2, "lists", ("scatter", None)),
+    # the same with stride 2: two kernels (sums, then k-WTA)
+    ("i8", (3, 7, 7, 24), 5, 3, 3, 2, 1, 6, 2, 1, 2, True, 2, "lists", ("tiled", None)),
+    # input-stationary: 7x7 pad 3 with pool; 128 channels (two keys per lane);
+    # a map wider than one band (several bands per image); a map too wide
+    # for the byte-sized column field (the gather kernel)
+    ("i8", (2, 12, 12, 16), 5, 7, 7, 1, 3, 32, 4, 2, 6, True, 8, "lists", ("scatter", None)),
+    ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, True, None, "dense", ("scatter", None)),
+    ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, False, 10, "lists", ("scatter", None)),
+    ("i8", (1, 40, 40, 32), 6, 3, 3, 1, 1, 64, 8, 2, 8, True, 9, "lists", ("scatter", None)),
+    ("i8", (1, 6, 300, 16), 4, 3, 3, 1, 1, 16, 4, 1, 4, False, 5, "lists", ("fused", 1)),
     # a table too large for LDS, one output vector per sample: one workgroup
     # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
     ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
