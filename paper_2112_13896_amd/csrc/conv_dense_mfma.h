@@ -14,7 +14,7 @@
 //  * the B operand (the 64 channels' weights, 4 N tiles of 16) stays in
 //    registers for the whole workgroup;
 //  * the pooled sums + bias go to an LDS tile [items][64 + 1]; k-WTA and the
-//    output run as in the fused sparse layer (one lane per item).
+//    output run as in the fused sparse layer (four lanes per item).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -26,6 +26,9 @@
 
 namespace cs {
 
+constexpr int DENSE_BD = 512;     // threads per workgroup
+constexpr int DENSE_STAGE = 8;   // input bytes per thread in flight while staging
+
 struct DenseArgs {
   int TPR;            // pooled rows per workgroup
   int tiles_img;      // workgroups per image
@@ -34,18 +37,21 @@ struct DenseArgs {
   int shift;
   int kmode;          // 1/2/3: top-8/16/32 insertion
   int write_sums;
+  int vec_rows;       // 1: no padding, rows of W*C bytes a multiple of 16, input 16-byte aligned
   int ostride;        // c_out + 1
-  uint32_t off_out, off_sel, off_lidx, off_lval;   // LDS byte offsets (image rows at 0)
+  uint32_t off_w, off_out, off_sel, off_lidx, off_lval;   // LDS byte offsets (image rows at 0)
   FastDiv fd_wp;      // / pooled width
   FastDiv fd_timg;    // / tiles_img
   FastDiv fd_cout;    // / c_out
   FastDiv fd_ochunks; // / (list capacity / 4)
+  FastDiv fd_rowb;    // / staged row bytes ((W + 2P) * C)
+  FastDiv fd_c;       // / C
 };
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 
 template <int POOL, typename TO>
-__global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict__ x,
+__global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __restrict__ x,
                                                        const uint16_t* __restrict__ aug,
                                                        const int32_t* __restrict__ bias,
                                                        int32_t* __restrict__ y,
@@ -61,73 +67,125 @@ __global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict_
   const int nitems = npr * Wp;
   const int64_t item0 = ((int64_t)img * Hp + pr0) * Wp;
 
-  // input rows the tile reads, clipped to the image, staged whole (W * C bytes each)
+  // the input rows the tile reads, staged zero-padded (columns -P .. W+P-1,
+  // rows outside the image as zeros), so that the im2col gather below needs
+  // no bounds checks
+  const int Wpad = W + 2 * geo.P;
+  const int rowb = Wpad * C;
   const int iy0 = pr0 * POOL * geo.S - geo.P;
-  const int ry0 = max(iy0, 0);
-  const int ry1 = min(((pr0 + npr) * POOL - 1) * geo.S - geo.P + geo.KH, geo.H);
-  const int rowb = W * C;
-  const int nbytes = max(ry1 - ry0, 0) * rowb;
+  const int rows_in = (npr * POOL - 1) * geo.S + geo.KH;
+  const int nbytes = rows_in * rowb;                        // <= the LDS allocation (host)
   int8_t* rows = reinterpret_cast<int8_t*>(smem);
-  {
-    const int8_t* src = x + ((int64_t)img * geo.H + ry0) * rowb;
-    for (int e = tid; e < nbytes; e += 256) rows[e] = src[e];
-  }
 
-  // B operands: lane holds channel 16*nt + lane%16, slots 8*(lane/16) .. +7
+  // the weights ([R][64] 16-bit entries, value in the low byte) are staged in
+  // LDS with 16-byte loads issued together with the input's
   const int g = lane >> 4, col = lane & 15;
+  uint16_t* wts = reinterpret_cast<uint16_t*>(smem + da.off_w);
+  int32_t bch[4];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) bch[nt] = bias ? bias[16 * nt + col] : 0;
+  {
+    const int n16 = da.R * 64 * 2 / 16;                   // R * 64 entries: whole 16-byte pieces
+    uint4 wv = {0u, 0u, 0u, 0u};
+    if (tid < n16) wv = reinterpret_cast<const uint4*>(aug)[tid];   // n16 <= 256 < DENSE_BD
+    const int8_t* ximg = x + (int64_t)img * geo.H * W * C;
+    if (da.vec_rows && iy0 >= 0 && iy0 + rows_in <= geo.H) {
+      // unpadded rows inside the image: one contiguous run, 16 bytes per load
+      const uint4* src = reinterpret_cast<const uint4*>(ximg + (int64_t)iy0 * W * C);
+      uint4* dst = reinterpret_cast<uint4*>(rows);
+      for (int b0 = 0; b0 < nbytes / 16; b0 += DENSE_BD * 2) {
+        uint4 v[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = b0 + u * DENSE_BD + tid;
+          if (e < nbytes / 16) v[u] = src[e];
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = b0 + u * DENSE_BD + tid;
+          if (e < nbytes / 16) dst[e] = v[u];
+        }
+      }
+    } else
+    for (int b0 = 0; b0 < nbytes; b0 += DENSE_BD * DENSE_STAGE) {
+      int8_t v[DENSE_STAGE];
+#pragma unroll
+      for (int u = 0; u < DENSE_STAGE; ++u) {
+        const int e = b0 + u * DENSE_BD + tid;
+        const int r = (int)fdiv((uint32_t)e, da.fd_rowb);
+        const int cb = e - r * rowb;
+        const int px = (int)fdiv((uint32_t)cb, da.fd_c);
+        const int iy = iy0 + r, ix = px - geo.P;
+        const bool ok = e < nbytes && iy >= 0 && iy < geo.H && ix >= 0 && ix < W;
+        v[u] = ximg[ok ? ((int64_t)iy * W + ix) * C + (cb - px * C) : 0];
+        v[u] = ok ? v[u] : int8_t(0);
+      }
+#pragma unroll
+      for (int u = 0; u < DENSE_STAGE; ++u) {
+        const int e = b0 + u * DENSE_BD + tid;
+        if (e < nbytes) rows[e] = v[u];
+      }
+    }
+    if (tid < n16) reinterpret_cast<uint4*>(wts)[tid] = wv;
+  }
+  __syncthreads();
+  // B operands: lane holds channel 16*nt + lane%16, slots 8*(lane/16) .. +7
+  uint32_t bw[4][8];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int kk = 8 * g + j;
+      bw[nt][j] = wts[(kk < da.R ? kk : 0) * 64 + 16 * nt + col];
+    }
   int64_t bop[4];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
     uint64_t b8 = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int kk = 8 * g + j;
-      const uint32_t v = kk < da.R ? (uint32_t)(aug[kk * 64 + 16 * nt + col] & 0xFFu) : 0u;
+      const uint32_t v = 8 * g + j < da.R ? (bw[nt][j] & 0xFFu) : 0u;
       b8 |= (uint64_t)v << (8 * j);
     }
     bop[nt] = (int64_t)b8;
   }
-  int32_t bch[4];
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt) bch[nt] = bias ? bias[16 * nt + col] : 0;
 
-  // this lane's 8 slots of a window: input offset relative to the window's
-  // top-left corner, or -1 past r
-  int dy[8], dx[8], dc[8];
+  // this lane's 8 slots of a window: byte offset from the window's top-left
+  // corner in the staged rows (slots past R read offset 0 and are masked)
+  int offs[8];
+  uint32_t kmask[2] = {0u, 0u};                             // bytes of slots < R
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int kk = 8 * g + j;
     const int t = kk / C, c = kk - (kk / C) * C;
-    dy[j] = kk < da.R ? t / geo.KW : -1;
-    dx[j] = t - (t / geo.KW) * geo.KW;
-    dc[j] = c;
+    const int ky = t / geo.KW, kx = t - (t / geo.KW) * geo.KW;
+    offs[j] = kk < da.R ? ky * rowb + kx * C + c : 0;
+    kmask[j >> 2] |= kk < da.R ? (0xFFu << (8 * (j & 3))) : 0u;
   }
-  __syncthreads();
 
   int32_t* otile = reinterpret_cast<int32_t*>(smem + da.off_out);
   const int ostride = da.ostride;
   constexpr int IPM = 16 / (POOL * POOL);                  // items per M tile
   const int mtiles = (nitems + IPM - 1) / IPM;
-  for (int mt = wv; mt < mtiles; mt += 4) {
-    // this lane's im2col row: item and sub-pixel
+  for (int mt = wv; mt < mtiles; mt += DENSE_BD / 64) {
+    // this lane's im2col row: item and sub-pixel (past the tile's last item
+    // the last item is gathered again; its results are not stored)
     const int r = lane & 15;
-    const int item = mt * IPM + r / (POOL * POOL);
+    int item = mt * IPM + r / (POOL * POOL);
+    item = item < nitems ? item : nitems - 1;
     const int q = r % (POOL * POOL);
-    uint64_t a8 = 0;
-    if (item < nitems) {
-      const int pr = (int)fdiv((uint32_t)item, da.fd_wp);
-      const int pc = item - pr * Wp;
-      const int oy = (pr0 + pr) * POOL + q / POOL, ox = pc * POOL + q % POOL;
-      const int by = oy * geo.S - geo.P, bx = ox * geo.S - geo.P;
+    const int pr = (int)fdiv((uint32_t)item, da.fd_wp);
+    const int pc = item - pr * Wp;
+    const int oyl = pr * POOL + q / POOL, ox = pc * POOL + q % POOL;   // conv row in the tile
+    const unsigned char* wb = reinterpret_cast<const unsigned char*>(rows) +
+                              oyl * geo.S * rowb + ox * geo.S * C;
+    uint32_t lo4 = 0u, hi4 = 0u;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int iy = by + dy[j], ix = bx + dx[j];
-        uint32_t v = 0u;
-        if (dy[j] >= 0 && iy >= ry0 && iy < ry1 && ix >= 0 && ix < W)
-          v = (uint8_t)rows[(iy - ry0) * rowb + ix * C + dc[j]];
-        a8 |= (uint64_t)v << (8 * j);
-      }
+    for (int j = 0; j < 4; ++j) {
+      lo4 |= (uint32_t)wb[offs[j]] << (8 * j);
+      hi4 |= (uint32_t)wb[offs[4 + j]] << (8 * j);
     }
+    const uint64_t a8 = (uint64_t)(lo4 & kmask[0]) | ((uint64_t)(hi4 & kmask[1]) << 32);
     const v4i_t zero = {0, 0, 0, 0};
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
@@ -155,7 +213,7 @@ __global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict_
   const int c_out = 64;
   if (da.write_sums) {
     const int tot = nitems * c_out;
-    for (int e = tid; e < tot; e += 256) {
+    for (int e = tid; e < tot; e += DENSE_BD) {
       const int it = (int)fdiv((uint32_t)e, da.fd_cout);
       y[item0 * c_out + e] = otile[it * ostride + (e - it * c_out)];
     }
@@ -168,15 +226,15 @@ __global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict_
     TO* tl_val = reinterpret_cast<TO*>(smem + da.off_lval);
     switch (da.kmode) {
       case 1:
-        kwta_quad_items<int32_t, TO, 8>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
+        kwta_quad_items<int32_t, TO, 8, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
                                         tl_val, lo.cap, lo.cnt);
         break;
       case 2:
-        kwta_quad_items<int32_t, TO, 16>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 16, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
       default:
-        kwta_quad_items<int32_t, TO, 32>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 32, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
     }
@@ -184,7 +242,7 @@ __global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict_
     if (lo.idx) {
       using OV = typename ChunkVal<TO>::type;
       const int cq = lo.cap >> 2;
-      for (int e = tid; e < nitems * cq; e += 256) {
+      for (int e = tid; e < nitems * cq; e += DENSE_BD) {
         const int it = (int)fdiv((uint32_t)e, da.fd_ochunks);
         const int j = e - it * cq;
         const int64_t gofs = (item0 + it) * lo.cap + 4 * j;
@@ -194,7 +252,7 @@ __global__ __launch_bounds__(256) void conv_dense_mfma(const int8_t* __restrict_
       }
     } else {
       const bool none = da.k == 0;
-      for (int e = tid; e < nitems * c_out; e += 256) {
+      for (int e = tid; e < nitems * c_out; e += DENSE_BD) {
         const int it = (int)fdiv((uint32_t)e, da.fd_cout);
         const int ch = e - it * c_out;
         const int32_t a = otile[it * ostride + ch];

@@ -1018,7 +1018,7 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
   const int Hp = geo.Ho / pool, Wp = geo.Wo / pool;
   const int64_t items = (int64_t)b * Hp * Wp;
   const bool lists_ok = !lists || (ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, osz * 4));
-  if (xt == CS_I8 && k <= 32 && lists_ok && items * 64 < INT32_MAX) {
+  if (xt == CS_I8 && k <= 32 && lists_ok && aligned(aug, 16) && items * 64 < INT32_MAX) {
     // matrix-core kernel: pooled rows per workgroup for about 512 workgroups
     int tiles = (int)((512 + b - 1) / b);
     tiles = tiles < 1 ? 1 : (tiles > Hp ? Hp : tiles);
@@ -1028,7 +1028,9 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
     for (; tpr >= 1; --tpr) {
       const int rows_in = (tpr * pool - 1) * stride + kh;
       const size_t items_t = (size_t)tpr * Wp;
-      size_t o = round16((size_t)rows_in * w * c_in);
+      size_t o = round16((size_t)rows_in * (w + 2 * pad) * c_in);   // zero-padded rows
+      da.off_w = (uint32_t)o;
+      o += round16((size_t)R * 64 * 2);                              // the weights
       da.off_out = (uint32_t)o;
       o += round16(items_t * 65 * 4);
       da.off_sel = (uint32_t)o;
@@ -1055,9 +1057,12 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
       da.fd_timg = cs::make_fastdiv((uint32_t)da.tiles_img);
       da.fd_cout = cs::make_fastdiv(64u);
       da.fd_ochunks = cs::make_fastdiv((uint32_t)(lists ? ocap / 4 : 1));
+      da.fd_rowb = cs::make_fastdiv((uint32_t)((w + 2 * pad) * c_in));
+      da.vec_rows = pad == 0 && (w * c_in) % 16 == 0 && aligned(x, 16) ? 1 : 0;
+      da.fd_c = cs::make_fastdiv((uint32_t)c_in);
       const int64_t nb = (int64_t)b * da.tiles_img;
       if (nb < INT32_MAX) {
-        const dim3 grid((unsigned)nb), block(256);
+        const dim3 grid((unsigned)nb), block(cs::DENSE_BD);
         const auto* xx = static_cast<const int8_t*>(x);
         const auto* pa = static_cast<const uint16_t*>(aug);
         const auto* bs = static_cast<const int32_t*>(bias);

@@ -124,27 +124,60 @@ __device__ __forceinline__ int quad_excl_sum(int v, int qd) {
   return x - v;
 }
 
-// Insert x into the descending list top[] (a max/min exchange per slot).
-template <int KMAX>
-__device__ __forceinline__ void topk_insert(uint32_t (&top)[KMAX], uint32_t x) {
+// Bitonic networks in registers (all indices compile-time): sort N keys
+// descending; sort a bitonic sequence of N keys descending; and keep in a[]
+// the N largest of two descending lists (a max against the reversed other
+// list leaves a bitonic sequence holding them, which is then sorted).
+template <int N>
+__device__ __forceinline__ void bitonic_sort_desc(uint32_t (&a)[N]) {
 #pragma unroll
-  for (int s = 0; s < KMAX; ++s) {
-    const uint32_t hi = top[s] > x ? top[s] : x;
-    x = top[s] > x ? x : top[s];
-    top[s] = hi;
-  }
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint32_t x = a[i], y = a[l];
+          const uint32_t hi = x > y ? x : y, lo = x > y ? y : x;
+          const bool desc = (i & k) == 0;
+          a[i] = desc ? hi : lo;
+          a[l] = desc ? lo : hi;
+        }
+      }
+}
+template <int N>
+__device__ __forceinline__ void bitonic_clean_desc(uint32_t (&a)[N]) {
+#pragma unroll
+  for (int j = N >> 1; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int l = i ^ j;
+      if (l > i) {
+        const uint32_t x = a[i], y = a[l];
+        a[i] = x > y ? x : y;
+        a[l] = x > y ? y : x;
+      }
+    }
+}
+template <int N>
+__device__ __forceinline__ void top_merge_desc(uint32_t (&a)[N], const uint32_t (&b)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) a[i] = a[i] > b[N - 1 - i] ? a[i] : b[N - 1 - i];
+  bitonic_clean_desc<N>(a);
 }
 
-// k-WTA with four lanes per item (a quad): each lane inserts the keys of its
-// quarter of the row into a descending top-KMAX list, the quad merges the four
-// lists (two exchange steps) and reads the threshold key T = the k-th largest.
+// k-WTA with four lanes per item (a quad): each lane keeps the KMAX largest
+// keys of its quarter of the row, sorted (blocks of KMAX keys sorted and
+// merged with bitonic networks), the quad merges the four lists (two exchange
+// steps) and reads the threshold key T = the k-th largest.
 // The winners are key > T and the first `need` keys equal to T in index
 // order (ties go to the lower index); a quad prefix sum gives each lane its
 // ties' ranks and its winners' positions in the row's list.  List output: the
 // winners with a non-zero output value go to the tile's LDS lists in index
 // order and their count to cnt.  sel[it] = (T, index of the last winning tie
 // or -1).  Rows are read with an odd stride (bank-conflict free).
-template <typename A, typename TO, int KMAX>
+template <typename A, typename TO, int KMAX, int BD = MRS_BD>
 __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
                                 int c, int k, int shift, uint2* sel, uint16_t* tl_idx,
                                 TO* tl_val, int cap, int32_t* gcnt) {
@@ -153,27 +186,27 @@ __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, 
   const int L = (c + 3) >> 2;                          // row quarter of a lane
   const int i_lo = qd * L, i_hi = min(c, i_lo + L);
   const int nsl = (sm.nslots + 3) & ~3;
-  for (int base = 0; base < ((nsl + MRS_BD / 4 - 1) / (MRS_BD / 4)) * (MRS_BD / 4);
-       base += MRS_BD / 4) {
+  for (int base = 0; base < ((nsl + BD / 4 - 1) / (BD / 4)) * (BD / 4); base += BD / 4) {
     const int it = base + (threadIdx.x >> 2);
     const bool live = sm.live(it);                     // the same for the 4 lanes of the quad
     const A* v = otile + (live ? it : 0) * ostride;
     // --- the threshold: per-lane top-KMAX of the quarter, merged over the quad
+    // (keys past the quarter are 0: a 0 never changes the k-th largest)
     uint32_t top[KMAX];
 #pragma unroll
     for (int s = 0; s < KMAX; ++s) top[s] = 0u;
     const bool search = live && k > 0 && k < c;
     if (search) {
-      for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
-        uint32_t xs[BK];
+      for (int i0 = i_lo; i0 < i_hi; i0 += KMAX) {
+        uint32_t blk[KMAX];
 #pragma unroll
-        for (int j = 0; j < BK; ++j) {
+        for (int j = 0; j < KMAX; ++j) {
           const int i = i0 + j;
           const uint32_t kx = order_key(v[i < i_hi ? i : i_hi - 1]);
-          xs[j] = i < i_hi ? kx : 0u;                  // a 0 never changes the k-th largest
+          blk[j] = i < i_hi ? kx : 0u;
         }
-#pragma unroll
-        for (int j = 0; j < BK; ++j) topk_insert<KMAX>(top, xs[j]);
+        bitonic_sort_desc<KMAX>(blk);
+        top_merge_desc<KMAX>(top, blk);
       }
     }
     // merge with the neighbour at distance 1, then 2 (all four lanes end equal);
@@ -182,12 +215,10 @@ __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, 
       uint32_t px[KMAX];
 #pragma unroll
       for (int s = 0; s < KMAX; ++s) px[s] = quad_xor1(top[s]);
-#pragma unroll
-      for (int s = 0; s < KMAX; ++s) topk_insert<KMAX>(top, px[s]);
+      top_merge_desc<KMAX>(top, px);
 #pragma unroll
       for (int s = 0; s < KMAX; ++s) px[s] = quad_xor2(top[s]);
-#pragma unroll
-      for (int s = 0; s < KMAX; ++s) topk_insert<KMAX>(top, px[s]);
+      top_merge_desc<KMAX>(top, px);
     }
     uint32_t thr = 0u;
     int need = 0;
