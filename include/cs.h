@@ -194,8 +194,12 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
  *  info    host int64[11] out: [0] path (0 one lane per output, 1 table-slice
  *          kernel, 2 fused layer kernel, 3 one workgroup per sample: a layer
  *          whose window is the whole unpadded input map, output 1 x 1, no
- *          pool - a linear layer); for path 3: [6] workgroups, [7] LDS bytes
- *          per workgroup, [8] entry slices per packed set; for path 2: [1] tile mode (0 rows of
+ *          pool - a linear layer; 4 input-stationary int8 convolution; 5 one
+ *          wavefront per item: a 1x1 layer with many items and a k-WTA over
+ *          rows of more than 128 or k > 32); for paths 3 and
+ *          5: [6] workgroups, [7] LDS bytes per workgroup, [8] entry slices
+ *          per packed set; for path 4: [2] output rows per band, [6]
+ *          workgroups, [7] LDS bytes, [8] sets per lane; for path 2: [1] tile mode (0 rows of
  *          items, 1 image rectangles), [2] items (mode 0) or pooled rows
  *          (mode 1) per tile, [3] pooled columns per tile (mode 1), [4] list
  *          chunks staged in LDS at most, [5] input pixels per tile at most,

@@ -15,6 +15,7 @@
 #include "mrs_fused.h"
 #include "mrs_kernels.h"
 #include "mrs_sample.h"
+#include "mrs_rows.h"
 #include "mrs_scatter.h"
 #include "mrs_tiled.h"
 
@@ -638,6 +639,81 @@ int launch_scatter(const ScatterPlan& pl, cs_dtype ot, hipStream_t s, const uint
   return launch_status();
 }
 
+// ------------------------------------------------- one wavefront per item
+// A one-tap layer (1x1 conv with stride 1, or linear) with many items, a
+// table that fits LDS and a k-WTA over long rows: each wavefront takes whole
+// items.
+constexpr int64_t kRowsMinItems = 4096;   // fewer items: too few wavefronts to fill the chip
+constexpr size_t kRowsTabLds = 48 * 1024;
+
+struct RowsPlan {
+  cs::RowsArgs ra;
+  size_t shmem;
+  int64_t blocks, items;
+};
+
+bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int shift,
+               int write_sums, RowsPlan* pl) {
+  if (geo.KH != 1 || geo.KW != 1 || geo.S != 1 || geo.P != 0 || geo.pool != 1) return false;
+  // only for a k-WTA the fused kernel's epilogue cannot take (rows over 128
+  // or k over 32), which would otherwise need its own kernel and the sums in HBM
+  if (k < 0 || (geo.c_out <= 128 && k <= 32)) return false;
+  if (geo.c_out > 2048 || !aligned(aug, 16)) return false;
+  const int64_t items = (int64_t)geo.B * geo.H * geo.W;
+  if (items < kRowsMinItems || items * geo.cap >= INT32_MAX * 4LL) return false;
+  const size_t esz = xt == CS_I8 ? 2 : 8;
+  const size_t tab_b = (size_t)geo.C * geo.G * esz;
+  if (tab_b > kRowsTabLds) return false;
+  cs::RowsArgs& ra = pl->ra;
+  ra.S = geo.G <= 64 ? 64 / geo.G : 1;
+  ra.gpl = geo.G <= 64 ? 1 : (geo.G + 63) / 64;
+  const uint32_t accw = (uint32_t)(((int64_t)ra.S * geo.c_out + 3) & ~3LL);
+  ra.acc_words = accw;
+  ra.k = k;
+  ra.shift = shift;
+  ra.write_sums = write_sums;
+  ra.off_acc = (uint32_t)round16(tab_b);
+  ra.off_ent = ra.off_acc + (uint32_t)(cs::ROWS_WAVES * accw * 4);
+  ra.fd_g = cs::make_fastdiv((uint32_t)geo.G);
+  ra.fd_n = cs::make_fastdiv((uint32_t)geo.n);
+  ra.off_hist = ra.off_ent + cs::ROWS_WAVES * cs::ROWS_ENT * 8;
+  ra.off_row = ra.off_hist + (k >= 0 ? cs::ROWS_WAVES * 512 * 4 : 0);
+  ra.row_words = (uint32_t)((geo.c_out + 3) & ~3);
+  ra.off_bias = ra.off_row + cs::ROWS_WAVES * ra.row_words * 4;
+  pl->shmem = ra.off_bias + ra.row_words * 4;
+  if (pl->shmem > kFusedLds) return false;
+  // about four workgroups per compute unit, whole wavefront rounds of items
+  int64_t ipw = (items + 4 * kPlanCus - 1) / (4 * kPlanCus);
+  ipw = (ipw + cs::ROWS_WAVES - 1) / cs::ROWS_WAVES * cs::ROWS_WAVES;
+  ra.ipw = (int)ipw;
+  pl->items = items;
+  pl->blocks = (items + ipw - 1) / ipw;
+  return pl->blocks <= INT32_MAX;
+}
+
+template <typename T, typename A, typename TO>
+void launch_rows_t(const RowsPlan& pl, hipStream_t s, const uint16_t* idx, const void* lval,
+                   const int32_t* cnt, const void* aug, const void* bias, void* y, void* out,
+                   const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  using E = typename cs::Aug<T>::type;
+  hipLaunchKernelGGL((cs::mrs_rows<T, A, TO>), dim3((unsigned)pl.blocks), dim3(cs::ROWS_BD),
+                     pl.shmem, s, idx, static_cast<const T*>(lval), cnt, static_cast<const E*>(aug),
+                     static_cast<const A*>(bias), static_cast<A*>(y), static_cast<TO*>(out), lo,
+                     geo, pl.ra, pl.items);
+}
+
+int launch_rows(const RowsPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t s, const uint16_t* idx,
+                const void* lval, const int32_t* cnt, const void* aug, const void* bias, void* y,
+                void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  if (xt == CS_F32)
+    launch_rows_t<float, float, float>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  else if (ot == CS_I8)
+    launch_rows_t<int8_t, int32_t, int8_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  else
+    launch_rows_t<int8_t, int32_t, int32_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  return launch_status();
+}
+
 int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
                      const cs::ConvGeom& geo, const void* aug, const void* bias, void* y,
                      hipStream_t stream);
@@ -846,6 +922,9 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
     ScatterPlan scp;
     if (scatter_plan(geo, xt, aug, k, shift, keep_sums, &scp))
       return launch_scatter(scp, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    RowsPlan rp;
+    if (rows_plan(geo, xt, aug, k, shift, keep_sums, &rp))
+      return launch_rows(rp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
   if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
     FusedPlan fp;
@@ -891,6 +970,14 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
     info[6] = scp.blocks;
     info[7] = (int64_t)scp.shmem;
     info[8] = scp.gpl;
+    return CS_OK;
+  }
+  RowsPlan rp;
+  if (rows_plan(geo, xt, nullptr, k, 0, 1, &rp)) {
+    info[0] = 5;
+    info[6] = rp.blocks;
+    info[7] = (int64_t)rp.shmem;
+    info[8] = rp.ra.S;
     return CS_OK;
   }
   FusedPlan fp;

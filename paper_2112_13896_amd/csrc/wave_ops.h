@@ -33,6 +33,17 @@ struct OpMax {
   __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; }
 };
 
+// Make this wavefront's LDS writes visible to its other lanes: wait for the
+// wavefront's LDS operations only (not for its global stores, which a fence
+// would also wait for) and keep the compiler from moving memory accesses
+// across.
+__device__ __forceinline__ void wave_lds_sync() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);                               // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // Wavefront minimum / maximum, the same in every lane (all lanes active).
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(v, 0xFFFFFFFFu, OpMin{}), 63);

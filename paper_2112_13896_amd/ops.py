@@ -201,8 +201,10 @@ def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: i
     info = (ctypes.c_int64 * 11)()
     check("cs_mrs_plan", lib().cs_mrs_plan(_TORCH_DT[dtype], cap, b, h, w, c_in, kh, kw, stride,
                                            pad, c_out, n, pool, k, info))
-    path = ("simple", "tiled", "fused", "sample", "scatter")[info[0]]
+    path = ("simple", "tiled", "fused", "sample", "scatter", "rows")[info[0]]
     kwta = None if k < 0 else ("separate" if info[10] else "fused")
+    if path == "rows":
+        return {"path": path, "kwta": kwta, "blocks": info[6], "lds": info[7], "slices": info[8]}
     if path == "scatter":
         return {"path": path, "kwta": kwta, "band_rows": info[2], "blocks": info[6],
                 "lds": info[7], "sets_per_lane": info[8]}

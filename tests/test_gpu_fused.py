@@ -10,7 +10,8 @@ and not keeping them (the benchmark's setting), and both outputs must be
 identical.  The launch plan is asserted so that every tiling path (rows of
 items, full-width image rows, column tiles, partial LDS staging with global
 reads, one workgroup per sample for linear layers, input-stationary int8
-convolutions, the two-kernel fallback) is known to run.
+convolutions, one wavefront per item for 1x1 layers, the two-kernel fallback)
+is known to run.
 """
 from __future__ import annotations
 
@@ -105,6 +106,12 @@ CASES = [
     ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, False, 10, "lists", ("scatter", None)),
     ("i8", (1, 40, 40, 32), 6, 3, 3, 1, 1, 64, 8, 2, 8, True, 9, "lists", ("scatter", None)),
     ("i8", (1, 6, 300, 16), 4, 3, 3, 1, 1, 16, 4, 1, 4, False, 5, "lists", ("fused", 1)),
+    # 1x1 layers with many items: one wavefront per item (config 5's expand
+    # shape; more sets than lanes; ties; fp32)
+    ("i8", (8, 24, 24, 96), 12, 1, 1, 1, 0, 576, 8, 1, 72, True, 9, "lists", ("rows", None)),
+    ("i8", (1, 64, 64, 32), 4, 1, 1, 1, 0, 1600, 8, 1, 100, True, 6, "lists", ("rows", None)),
+    ("i8", (2, 48, 48, 64), 8, 1, 1, 1, 0, 192, 16, 1, 40, False, 0, "lists", ("rows", None)),
+    ("f32", (4, 32, 32, 64), 7, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "dense", ("rows", None)),
     # a table too large for LDS, one output vector per sample: one workgroup
     # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
     ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
