@@ -650,10 +650,19 @@ struct RowsPlan {
   cs::RowsArgs ra;
   size_t shmem;
   int64_t blocks, items;
+  int cpl, waves;
 };
+
+// channels per lane of the row kernel's k-WTA (odd, 64 * cpl >= c_out)
+int rows_cpl(int c_out) {
+  for (int cpl : {3, 5, 9, 17, 33})
+    if (64 * cpl >= c_out) return cpl;
+  return 0;
+}
 
 bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int shift,
                int write_sums, RowsPlan* pl) {
+  if (xt != CS_I8) return false;
   if (geo.KH != 1 || geo.KW != 1 || geo.S != 1 || geo.P != 0 || geo.pool != 1) return false;
   // only for a k-WTA the fused kernel's epilogue cannot take (rows over 128
   // or k over 32), which would otherwise need its own kernel and the sums in HBM
@@ -661,56 +670,86 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
   if (geo.c_out > 2048 || !aligned(aug, 16)) return false;
   const int64_t items = (int64_t)geo.B * geo.H * geo.W;
   if (items < kRowsMinItems || items * geo.cap >= INT32_MAX * 4LL) return false;
-  const size_t esz = xt == CS_I8 ? 2 : 8;
-  const size_t tab_b = (size_t)geo.C * geo.G * esz;
-  if (tab_b > kRowsTabLds) return false;
+  const size_t tab_b = (size_t)geo.C * geo.G * 2;
+  if (tab_b > kRowsTabLds || (int64_t)geo.C * geo.G >= (1 << 24)) return false;
+  const int cpl = rows_cpl(geo.c_out);
+  if (cpl == 0) return false;
   cs::RowsArgs& ra = pl->ra;
-  ra.S = geo.G <= 64 ? 64 / geo.G : 1;
-  ra.gpl = geo.G <= 64 ? 1 : (geo.G + 63) / 64;
-  const uint32_t accw = (uint32_t)(((int64_t)ra.S * geo.c_out + 3) & ~3LL);
-  ra.acc_words = accw;
   ra.k = k;
   ra.shift = shift;
   ra.write_sums = write_sums;
-  ra.off_acc = (uint32_t)round16(tab_b);
-  ra.off_ent = ra.off_acc + (uint32_t)(cs::ROWS_WAVES * accw * 4);
+  ra.S = geo.G <= 32 ? 64 / geo.G : 1;
+  ra.gpl = geo.G <= 32 ? 1 : (geo.G + 63) / 64;
+  ra.acc_words = (uint32_t)std::max(64 * cpl, cs::ROWS_HIST);
+  ra.acc_words = (ra.acc_words + 3) & ~3u;
   ra.fd_g = cs::make_fastdiv((uint32_t)geo.G);
-  ra.fd_n = cs::make_fastdiv((uint32_t)geo.n);
-  ra.off_hist = ra.off_ent + cs::ROWS_WAVES * cs::ROWS_ENT * 8;
-  ra.off_row = ra.off_hist + (k >= 0 ? cs::ROWS_WAVES * 512 * 4 : 0);
-  ra.row_words = (uint32_t)((geo.c_out + 3) & ~3);
-  ra.off_bias = ra.off_row + cs::ROWS_WAVES * ra.row_words * 4;
-  pl->shmem = ra.off_bias + ra.row_words * 4;
-  if (pl->shmem > kFusedLds) return false;
-  // about four workgroups per compute unit, whole wavefront rounds of items
-  int64_t ipw = (items + 4 * kPlanCus - 1) / (4 * kPlanCus);
-  ipw = (ipw + cs::ROWS_WAVES - 1) / cs::ROWS_WAVES * cs::ROWS_WAVES;
-  ra.ipw = (int)ipw;
+  // wavefronts per workgroup: the most wavefronts per compute unit (at most
+  // 32) within its LDS; fewer per workgroup only when that gives more
+  size_t best_sh = 0;
+  int best_w = 0, best_cu = 0;
+  for (int w : {16, 8, 4}) {
+    const size_t sh = round16(tab_b) + (size_t)w * ra.acc_words * 4 + 16 +
+                      round16((size_t)geo.c_out * 4);
+    if (sh > kCuLds) continue;
+    const int per_cu = std::min<int>((int)(kCuLds / sh) * w, 32);
+    if (per_cu > best_cu) {
+      best_cu = per_cu;
+      best_w = w;
+      best_sh = sh;
+    }
+  }
+  if (best_w == 0) return false;
+  ra.off_acc = (uint32_t)round16(tab_b);
+  ra.off_next = ra.off_acc + best_w * ra.acc_words * 4;
+  ra.off_bias = ra.off_next + 16;
+  pl->shmem = best_sh;
+  pl->waves = best_w;
+  // as many workgroups as fit the chip at once, each with an even share of the items
+  const int64_t wgs = std::min<int64_t>((int64_t)kPlanCus * (best_cu / best_w),
+                                        (items + best_w - 1) / best_w);
+  ra.per_wg = (items + wgs - 1) / wgs;
   pl->items = items;
-  pl->blocks = (items + ipw - 1) / ipw;
-  return pl->blocks <= INT32_MAX;
+  pl->blocks = (items + ra.per_wg - 1) / ra.per_wg;
+  pl->cpl = cpl;
+  return true;
 }
 
-template <typename T, typename A, typename TO>
+template <typename TO, int CPL>
+void launch_rows_c(const RowsPlan& pl, hipStream_t s, const uint16_t* idx, const void* lval,
+                   const int32_t* cnt, const void* aug, const void* bias, void* y, void* out,
+                   const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3((unsigned)pl.blocks), dim3(64 * pl.waves), pl.shmem, s, idx,
+                       static_cast<const int8_t*>(lval), cnt, static_cast<const uint16_t*>(aug),
+                       static_cast<const int32_t*>(bias), static_cast<int32_t*>(y),
+                       static_cast<TO*>(out), lo, geo, pl.ra, pl.items);
+  };
+  if (geo.c_out == 64 * CPL)
+    go(cs::mrs_rows<TO, CPL, true>);
+  else
+    go(cs::mrs_rows<TO, CPL, false>);
+}
+
+template <typename TO>
 void launch_rows_t(const RowsPlan& pl, hipStream_t s, const uint16_t* idx, const void* lval,
                    const int32_t* cnt, const void* aug, const void* bias, void* y, void* out,
                    const cs::ListOut& lo, const cs::ConvGeom& geo) {
-  using E = typename cs::Aug<T>::type;
-  hipLaunchKernelGGL((cs::mrs_rows<T, A, TO>), dim3((unsigned)pl.blocks), dim3(cs::ROWS_BD),
-                     pl.shmem, s, idx, static_cast<const T*>(lval), cnt, static_cast<const E*>(aug),
-                     static_cast<const A*>(bias), static_cast<A*>(y), static_cast<TO*>(out), lo,
-                     geo, pl.ra, pl.items);
+  switch (pl.cpl) {
+    case 3: launch_rows_c<TO, 3>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    case 5: launch_rows_c<TO, 5>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    case 9: launch_rows_c<TO, 9>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    case 17: launch_rows_c<TO, 17>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+    default: launch_rows_c<TO, 33>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo); break;
+  }
 }
 
-int launch_rows(const RowsPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t s, const uint16_t* idx,
+int launch_rows(const RowsPlan& pl, cs_dtype ot, hipStream_t s, const uint16_t* idx,
                 const void* lval, const int32_t* cnt, const void* aug, const void* bias, void* y,
                 void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
-  if (xt == CS_F32)
-    launch_rows_t<float, float, float>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
-  else if (ot == CS_I8)
-    launch_rows_t<int8_t, int32_t, int8_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  if (ot == CS_I8)
+    launch_rows_t<int8_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   else
-    launch_rows_t<int8_t, int32_t, int32_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    launch_rows_t<int32_t>(pl, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   return launch_status();
 }
 
@@ -924,7 +963,7 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
       return launch_scatter(scp, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
     RowsPlan rp;
     if (rows_plan(geo, xt, aug, k, shift, keep_sums, &rp))
-      return launch_rows(rp, xt, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+      return launch_rows(rp, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
   if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
     FusedPlan fp;
@@ -977,7 +1016,7 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
     info[0] = 5;
     info[6] = rp.blocks;
     info[7] = (int64_t)rp.shmem;
-    info[8] = rp.ra.S;
+    info[8] = rp.cpl;
     return CS_OK;
   }
   FusedPlan fp;

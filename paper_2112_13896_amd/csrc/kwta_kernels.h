@@ -374,129 +374,6 @@ __device__ __forceinline__ void kwta_row16(const TI (&v)[KPL], int c, int k, int
   }
 }
 
-// k-WTA of one row by one wavefront, the row (c values) in LDS: threshold by
-// radix select - keys offset by the row minimum, 8 bits per pass from the top
-// of the row's range, each pass counting the keys still in the running into a
-// 256-bin histogram in LDS (hist: 512 words of this wavefront's own, two
-// buffers used alternately) and finding the digit of the k-th largest with
-// one 16-byte read per lane and a DPP scan.  Ties go to the lower index; the
-// winners are written as the row's list (non-zero outputs in index order) or
-// densely.  Runtime loops over the row in steps of 64 (no per-key registers).
-// Every lane of the wavefront must be active; the row must be visible to the
-// whole wavefront.
-template <typename TI, typename TO>
-__device__ __forceinline__ void kwta_wave_radix(const TI* row_s, int c, int k, int shift,
-                                                const ListOut& lo, TO* __restrict__ out,
-                                                int64_t row, uint32_t* hist) {
-  typedef uint32_t h4_t __attribute__((ext_vector_type(4)));
-  const int lane = threadIdx.x & 63;
-  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-  for (int e = lane; e < c; e += 64) {
-    const uint32_t kx = order_key(row_s[e]);
-    kmin = kx < kmin ? kx : kmin;
-    kmax = kx > kmax ? kx : kmax;
-  }
-  kmin = wave_min_u32(kmin);
-  kmax = wave_max_u32(kmax);
-  const uint32_t range = kmax - kmin;
-  constexpr int RB = 4;   // keys a lane reads before it counts them (reads ahead of atomics)
-  uint32_t thr = 0u;   // an offset key
-  int need = 0;
-  if (k == 0) {
-    thr = 0xFFFFFFFFu;
-  } else if (k >= c) {
-    need = c;
-  } else if (range == 0u) {
-    need = k;
-  } else {
-    int rem = 32 - __builtin_clz(range);
-    uint32_t prefix = 0u;
-    int nd = k;
-    const h4_t z = {0u, 0u, 0u, 0u};
-    reinterpret_cast<h4_t*>(hist)[lane] = z;                        // first pass's bins
-    for (int pass = 0; rem > 0; ++pass) {                           // uniform
-      const int width = rem < 8 ? rem : 8;
-      const int sh = rem - width;
-      const uint32_t dmask = (1u << width) - 1u;
-      uint32_t* h = hist + (pass & 1) * 256;
-      wave_lds_sync();                                             // the zeroed bins
-      for (int e0 = 0; e0 < c; e0 += 64 * RB) {
-        uint32_t kx[RB];
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-          const int e = e0 + u * 64 + lane;
-          kx[u] = order_key(row_s[e < c ? e : 0]) - kmin;
-        }
-#pragma unroll
-        for (int u = 0; u < RB; ++u)
-          if (e0 + u * 64 + lane < c && (uint32_t)((uint64_t)kx[u] >> rem) == prefix)
-            __hip_atomic_fetch_add(&h[(kx[u] >> sh) & dmask], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_WORKGROUP);
-      }
-      reinterpret_cast<h4_t*>(hist + ((pass + 1) & 1) * 256)[lane] = z;   // the next pass's bins
-      wave_lds_sync();                                             // the counts
-      // lane l holds the 4 bins at 4*(63 - l): an inclusive scan counts the
-      // keys in a lane's bins and above
-      const int b0 = 4 * (63 - lane);
-      const h4_t hb = *reinterpret_cast<const h4_t*>(h + b0);
-      const int ls = (int)(hb.x + hb.y + hb.z + hb.w);
-      const int incl = (int)wave_incl_scan((uint32_t)ls, 0u, OpAdd{});
-      const int above = incl - ls;
-      int run = above, bin = b0;
-      if (run + (int)hb.w >= nd) {
-        bin = b0 + 3;
-      } else {
-        run += (int)hb.w;
-        if (run + (int)hb.z >= nd) {
-          bin = b0 + 2;
-        } else {
-          run += (int)hb.z;
-          if (run + (int)hb.y >= nd) {
-            bin = b0 + 1;
-          } else {
-            run += (int)hb.y;
-          }
-        }
-      }
-      const uint64_t fb = __ballot(above < nd && nd <= incl);       // exactly one lane
-      const int f = __ffsll((unsigned long long)fb) - 1;
-      prefix = (prefix << width) | (uint32_t)__builtin_amdgcn_readlane(bin, f);
-      nd -= __builtin_amdgcn_readlane(run, f);
-      rem = sh;
-    }
-    thr = prefix;
-    need = nd;
-  }
-  // winners in index order: key > thr, or key == thr among the first `need`
-  int rank0 = 0, lrun = 0;
-  for (int e0 = 0; e0 < c; e0 += 64) {                              // uniform
-    const int e = e0 + lane;
-    const bool valid = e < c;
-    const TI a = row_s[valid ? e : 0];
-    const uint32_t kx = order_key(a) - kmin;
-    const bool eq = valid && kx == thr;
-    const uint64_t b = __ballot(eq);
-    const int rank = rank0 + __popcll(b & below);
-    rank0 += __popcll(b);
-    const bool win = valid && (kx > thr || (eq && rank < need));
-    const TO ov = kwta_out<TI, TO>(a, shift);
-    if (lo.idx) {
-      const bool put = win && ov != TO(0);
-      const uint64_t pb = __ballot(put);
-      if (put) {
-        const int pos = lrun + __popcll(pb & below);
-        lo.idx[row * lo.cap + pos] = (uint16_t)e;
-        static_cast<TO*>(lo.val)[row * lo.cap + pos] = ov;
-      }
-      lrun += __popcll(pb);
-    } else if (valid) {
-      out[row * c + e] = win ? ov : TO(0);
-    }
-  }
-  if (lo.idx && lane == 0) lo.cnt[row] = lrun;
-}
-
 constexpr int KWTA_WAVE_WAVES = 4;   // wavefronts (rows) per block of kwta_wave
 
 template <typename TI, typename TO, int M>

@@ -33,13 +33,12 @@ struct OpMax {
   __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; }
 };
 
-// Make this wavefront's LDS writes visible to its other lanes: wait for the
-// wavefront's LDS operations only (not for its global stores, which a fence
-// would also wait for) and keep the compiler from moving memory accesses
-// across.
-__device__ __forceinline__ void wave_lds_sync() {
+// Compiler-only ordering of a wavefront's LDS accesses: the LDS runs one
+// wavefront's instructions in issue order, so a write by one lane is seen by a
+// later read of another lane of the same wavefront once the compiler keeps
+// the two in order.
+__device__ __forceinline__ void wave_lds_order() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0xC07F);                               // lgkmcnt(0)
   __builtin_amdgcn_wave_barrier();
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }

@@ -204,7 +204,8 @@ def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: i
     path = ("simple", "tiled", "fused", "sample", "scatter", "rows")[info[0]]
     kwta = None if k < 0 else ("separate" if info[10] else "fused")
     if path == "rows":
-        return {"path": path, "kwta": kwta, "blocks": info[6], "lds": info[7], "slices": info[8]}
+        return {"path": path, "kwta": kwta, "blocks": info[6], "lds": info[7],
+                "channels_per_lane": info[8]}
     if path == "scatter":
         return {"path": path, "kwta": kwta, "band_rows": info[2], "blocks": info[6],
                 "lds": info[7], "sets_per_lane": info[8]}

@@ -106,12 +106,18 @@ CASES = [
     ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, False, 10, "lists", ("scatter", None)),
     ("i8", (1, 40, 40, 32), 6, 3, 3, 1, 1, 64, 8, 2, 8, True, 9, "lists", ("scatter", None)),
     ("i8", (1, 6, 300, 16), 4, 3, 3, 1, 1, 16, 4, 1, 4, False, 5, "lists", ("fused", 1)),
-    # 1x1 layers with many items: one wavefront per item (config 5's expand
-    # shape; more sets than lanes; ties; fp32)
+    # int8 1x1 layers with many items and a k-WTA over long rows: one
+    # wavefront per item (config 5's expand shape; more sets than lanes; ties
+    # with fewer sets than lanes; lists longer than one 64-entry chunk with
+    # int32 dense output; eight sets with k = 0 and k = c_out)
     ("i8", (8, 24, 24, 96), 12, 1, 1, 1, 0, 576, 8, 1, 72, True, 9, "lists", ("rows", None)),
     ("i8", (1, 64, 64, 32), 4, 1, 1, 1, 0, 1600, 8, 1, 100, True, 6, "lists", ("rows", None)),
     ("i8", (2, 48, 48, 64), 8, 1, 1, 1, 0, 192, 16, 1, 40, False, 0, "lists", ("rows", None)),
-    ("f32", (4, 32, 32, 64), 7, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "dense", ("rows", None)),
+    ("i8", (2, 48, 48, 128), 100, 1, 1, 1, 0, 1000, 8, 1, 120, True, None, "dense", ("rows", None)),
+    ("i8", (1, 70, 70, 64), 3, 1, 1, 1, 0, 256, 32, 1, 0, False, 9, "lists", ("rows", None)),
+    ("i8", (1, 70, 70, 64), 3, 1, 1, 1, 0, 256, 32, 1, 256, True, None, "dense", ("rows", None)),
+    # the same shape in fp32: the gather kernel's sums, then a k-WTA kernel
+    ("f32", (4, 32, 32, 64), 7, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "dense", ("fused", 0)),
     # a table too large for LDS, one output vector per sample: one workgroup
     # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
     ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
