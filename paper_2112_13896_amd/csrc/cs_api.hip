@@ -664,9 +664,10 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
                int write_sums, RowsPlan* pl) {
   if (xt != CS_I8) return false;
   if (geo.KH != 1 || geo.KW != 1 || geo.S != 1 || geo.P != 0 || geo.pool != 1) return false;
-  // only for a k-WTA the fused kernel's epilogue cannot take (rows over 128
-  // or k over 32), which would otherwise need its own kernel and the sums in HBM
-  if (k < 0 || (geo.c_out <= 128 && k <= 32)) return false;
+  // sums only, or a k-WTA the fused kernel's epilogue cannot take (rows over
+  // 128 or k over 32), which would otherwise need its own kernel and the sums in HBM
+  if (k >= 0 && geo.c_out <= 128 && k <= 32) return false;
+  if (k < 0 && !write_sums) return false;
   if (geo.c_out > 2048 || !aligned(aug, 16)) return false;
   const int64_t items = (int64_t)geo.B * geo.H * geo.W;
   if (items < kRowsMinItems || items * geo.cap >= INT32_MAX * 4LL) return false;
@@ -688,7 +689,7 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
   size_t best_sh = 0;
   int best_w = 0, best_cu = 0;
   for (int w : {16, 8, 4}) {
-    const size_t sh = round16(tab_b) + (size_t)w * ra.acc_words * 4 + 16 +
+    const size_t sh = round16(tab_b) + (size_t)w * (ra.acc_words * 4 + cs::ROWS_ENT_STRIDE * 8) + 16 +
                       round16((size_t)geo.c_out * 4);
     if (sh > kCuLds) continue;
     const int per_cu = std::min<int>((int)(kCuLds / sh) * w, 32);
@@ -702,6 +703,7 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
   ra.off_acc = (uint32_t)round16(tab_b);
   ra.off_next = ra.off_acc + best_w * ra.acc_words * 4;
   ra.off_bias = ra.off_next + 16;
+  ra.off_ent = ra.off_bias + (uint32_t)round16((size_t)geo.c_out * 4);
   pl->shmem = best_sh;
   pl->waves = best_w;
   // as many workgroups as fit the chip at once, each with an even share of the items
@@ -771,6 +773,10 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
   if (scatter_plan(geo, xt, aug, -1, 0, 1, &scp))
     return launch_scatter(scp, CS_I32, stream, idx, lval, cnt, aug, bias, y, nullptr,
                           cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
+  RowsPlan rp;
+  if (rows_plan(geo, xt, aug, -1, 0, 1, &rp))
+    return launch_rows(rp, CS_I32, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                       cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   if (lists_vectorisable(xt, idx, lval, geo.cap)) {
     FusedPlan fp;
     if (fused_plan(geo, xt, aug, y, -1, 0, 1, 0, 0, &fp))

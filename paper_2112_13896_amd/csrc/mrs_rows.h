@@ -36,6 +36,7 @@ namespace cs {
 
 constexpr int ROWS_BD = 1024;             // most threads per workgroup (16 wavefronts)
 constexpr int ROWS_BATCH = 4;             // table entries a lane reads before it adds
+constexpr int ROWS_ENT_STRIDE = 66;       // int2 slots per wavefront entry copy (64 + zero + pad)
 constexpr int ROWS_DIGIT = 9;             // bits per radix pass
 constexpr int ROWS_BINS = 1 << ROWS_DIGIT;
 constexpr int ROWS_HIST = ROWS_BINS + 64; // bins + one spare bin per lane
@@ -50,6 +51,7 @@ struct RowsArgs {
   uint32_t acc_words;  // words per wavefront row (>= c_out and >= ROWS_HIST)
   uint32_t off_next;   // LDS byte offset of the workgroup's item counter
   uint32_t off_bias;   // LDS byte offset of the bias (c_out words)
+  uint32_t off_ent;    // LDS byte offset of the wavefronts' entry copies (S > 1 only)
   int64_t per_wg;      // items per workgroup
   FastDiv fd_g;        // / G
 };
@@ -76,6 +78,8 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
   uint32_t* hist = reinterpret_cast<uint32_t*>(acc);                      // the same words
   int* next = reinterpret_cast<int*>(smem + ra.off_next);
   int32_t* bias_s = reinterpret_cast<int32_t*>(smem + ra.off_bias);     // [c_out]
+  // (row offset, value) of up to 64 entries, then a (0, 0) entry for slots past the list
+  int2* ent = reinterpret_cast<int2*>(smem + ra.off_ent) + wv * ROWS_ENT_STRIDE;
 
   // ---- the table into LDS (16-byte pieces), once per workgroup
   {
@@ -105,6 +109,7 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
   const int nv = FULL ? CPL : (c - ch0 < 0 ? 0 : (c - ch0 < CPL ? c - ch0 : CPL));
   for (int o = tid; o < c; o += nthr) bias_s[o] = bias != nullptr ? bias[o] : 0;
   if (tid == 0) *next = nwv;
+  if (lane == 0) ent[64] = make_int2(0, 0);
   __syncthreads();
   // a lane's slots past c_out (pads) take part as the row's smallest keys and
   // never win; their row words are scratch
@@ -185,30 +190,52 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
             }
           }
         }
-      } else if (job) {
-        // S slices of G sets: lane (s, g0) takes the entries s, s + S, ...
-        const int S = ra.S;
-        int32_t* ag = acc + g0 * n;
-        for (int e = 0; e < nb; e += S * ROWS_BATCH) {              // uniform
-          int p[ROWS_BATCH], x[ROWS_BATCH];
+      } else {
+        // S slices of G sets: lane (s, g0) takes the entries s, s + S, ...,
+        // read from a wavefront-private copy of the entries in LDS
+        ent[lane] = make_int2(pre, xv);
+        wave_lds_order();
+        if (job) {
+          const int S = ra.S;
+          int32_t* ag = acc + g0 * n;
+          for (int e = 0; e < nb; e += S * ROWS_BATCH) {            // uniform
+            int2 en[ROWS_BATCH];
 #pragma unroll
-          for (int u = 0; u < ROWS_BATCH; ++u) {
-            const int el = e + s + S * u;
-            const int es = el < nb ? el : 0;
-            p[u] = __shfl(pre, es);
-            x[u] = __shfl(xv, es);
-            x[u] = el < nb ? x[u] : 0;
+            for (int u = 0; u < ROWS_BATCH; ++u) {
+              const int el = e + s + S * u;
+              en[u] = ent[el < nb ? el : 64];
+            }
+            uint32_t w[ROWS_BATCH];
+#pragma unroll
+            for (int u = 0; u < ROWS_BATCH; ++u)
+              w[u] = *reinterpret_cast<const uint16_t*>(smem + en[u].x + 2 * g0);
+#pragma unroll
+            for (int u = 0; u < ROWS_BATCH; ++u)
+              __hip_atomic_fetch_add(ag + (int)(w[u] >> 8),
+                                     __mul24(en[u].y, (int)(int8_t)(w[u] & 0xFFu)),
+                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
           }
-          uint32_t w[ROWS_BATCH];
-#pragma unroll
-          for (int u = 0; u < ROWS_BATCH; ++u)
-            w[u] = *reinterpret_cast<const uint16_t*>(smem + p[u] + 2 * g0);
-#pragma unroll
-          for (int u = 0; u < ROWS_BATCH; ++u)
-            __hip_atomic_fetch_add(ag + (int)(w[u] >> 8), __mul24(x[u], (int)(int8_t)(w[u] & 0xFFu)),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
+        wave_lds_order();                                           // before the buffer is rewritten
       }
+    }
+
+    if (ra.k < 0) {
+      // ---- sums only: the row to HBM (16-byte stores when c_out allows),
+      // then back to the bias
+      wave_lds_order();
+      if ((c & 3) == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {
+        typedef int32_t i4_t __attribute__((ext_vector_type(4)));
+        i4_t* y4 = reinterpret_cast<i4_t*>(y + it * c);
+        for (int o = lane; o < (c >> 2); o += 64) y4[o] = reinterpret_cast<const i4_t*>(acc)[o];
+      } else {
+        for (int o = lane; o < c; o += 64) y[it * c + o] = acc[o];
+      }
+      wave_lds_order();
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) acc[ch0 + i] = bias_s[ch0 + i < c ? ch0 + i : c - 1];
+      li = lnext;
+      continue;
     }
 
     // ---- the row into registers; its memory becomes the histogram

@@ -87,7 +87,7 @@ def test_fp32_config_layerwise(cid):
                                              (2, "linear1", "sample"), (2, "output", "sample"),
                                              (3, "conv3x3", "fused"), (4, "conv1x1", "tiled"),
                                              (4, "conv3x3", "tiled"), (5, "expand", "rows"),
-                                             (5, "project", "fused")])
+                                             (5, "project", "rows")])
 def test_config_launch_paths(cid, layer, path):
     """Which kernel runs each layer at full size (the benchmark's launches)."""
     cfg = CONFIGS[cid]

@@ -236,6 +236,35 @@ def test_sample_sums_only(dtype):
         assert_f32_close(y, ref, S, "sample sums")
 
 
+# (b, h, w, c_in), nnz, c_out, n, bias: int8 1x1 sums only, one wavefront per
+# item (config 5's project shape: G = 12, slices of sets; G = 72, one set per
+# lane; c_out not a multiple of 4; lists longer than 64 entries)
+ROWS_SUMS_CASES = [
+    ((4, 32, 32, 576), 72, 96, 8, True),
+    ((2, 48, 48, 96), 12, 576, 8, False),
+    ((1, 70, 70, 120), 15, 150, 10, True),
+    ((2, 48, 48, 256), 100, 200, 8, True),
+]
+
+
+@pytest.mark.parametrize("case", ROWS_SUMS_CASES, ids=[str(c[0]) + f"-{c[2]}" for c in ROWS_SUMS_CASES])
+def test_rows_sums_only(case):
+    """cs_mrs_conv2d (no k-WTA) of an int8 1x1 layer with many items takes
+    the one-wavefront-per-item kernel; the sums match the oracle exactly."""
+    shape, nnz, c_out, n, has_bias = case
+    r = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    c_in = shape[3]
+    x = sparse_input(r, shape, nnz, "i8")
+    W = weights(r, c_out, 1, 1, c_in, n, "i8")
+    bias = r.integers(-1000, 1001, size=c_out).astype(np.int32) if has_bias else None
+    assert ops.mrs_plan(torch.int8, c_in, shape, 1, 1, 1, 0, c_out, n, 1, -1)["path"] == "rows"
+    aug, _ = ops.pack(W.reshape(c_out, -1), n)
+    idx, lv, cnt = ops.compact(dev(x).reshape(-1, c_in))
+    y = host(ops.mrs_conv2d(idx, lv, cnt, shape, ops.aug_to_device(aug), 1, 1, n, 1, 0,
+                            None if bias is None else dev(bias), 1))
+    assert np.array_equal(y.astype(np.int64), o.conv2d_nhwc(x, W, 1, 0, bias))
+
+
 def test_fused_partial_staging_plan():
     """The budget case above really leaves pixels unstaged: its lists need
     more chunks than the LDS list budget of a tile."""
