@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 
 #include "compact_kernels.h"
@@ -648,10 +649,33 @@ constexpr size_t kRowsTabLds = 48 * 1024;
 
 struct RowsPlan {
   cs::RowsArgs ra;
-  size_t shmem;
+  size_t shmem, tab_b;
   int64_t blocks, items;
   int cpl, waves;
 };
+
+// LDS bytes of the row kernel with w wavefronts per workgroup
+size_t rows_shmem(const RowsPlan& pl, int w, int c_out) {
+  return round16(pl.tab_b) + (size_t)w * (pl.ra.acc_words * 4 + cs::ROWS_ENT_STRIDE * 8) +
+         round16((size_t)c_out * 4);
+}
+
+// w wavefronts per workgroup, wcu of them resident per compute unit: LDS
+// offsets, and as many workgroups as fit the chip at once, each with an even
+// share of the items
+bool rows_layout(RowsPlan* pl, int w, int wcu, int c_out) {
+  if (wcu < w) return false;
+  cs::RowsArgs& ra = pl->ra;
+  ra.off_acc = (uint32_t)round16(pl->tab_b);
+  ra.off_bias = ra.off_acc + w * ra.acc_words * 4;
+  ra.off_ent = ra.off_bias + (uint32_t)round16((size_t)c_out * 4);
+  pl->shmem = rows_shmem(*pl, w, c_out);
+  pl->waves = w;
+  const int64_t wgs = std::min<int64_t>((int64_t)kPlanCus * (wcu / w), (pl->items + w - 1) / w);
+  ra.per_wg = (pl->items + wgs - 1) / wgs;
+  pl->blocks = (pl->items + ra.per_wg - 1) / ra.per_wg;
+  return pl->shmem <= kCuLds;
+}
 
 // channels per lane of the row kernel's k-WTA (odd, 64 * cpl >= c_out)
 int rows_cpl(int c_out) {
@@ -679,48 +703,72 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
   ra.k = k;
   ra.shift = shift;
   ra.write_sums = write_sums;
-  ra.S = geo.G <= 32 ? 64 / geo.G : 1;
-  ra.gpl = geo.G <= 32 ? 1 : (geo.G + 63) / 64;
+  // groups of 64 sets with wavefront-uniform entries; a rest of at most 32
+  // sets as slices, a larger rest as one more (partial) group
+  int qf = geo.G / 64, rest = geo.G % 64;
+  ra.gbase = 64 * qf;
+  if (rest > 32) {
+    ++qf;
+    rest = 0;
+  }
+  ra.qf = qf;
+  ra.S = rest > 0 ? 64 / rest : 0;
   ra.acc_words = (uint32_t)std::max(64 * cpl, cs::ROWS_HIST);
   ra.acc_words = (ra.acc_words + 3) & ~3u;
-  ra.fd_g = cs::make_fastdiv((uint32_t)geo.G);
-  // wavefronts per workgroup: the most wavefronts per compute unit (at most
-  // 32) within its LDS; fewer per workgroup only when that gives more
-  size_t best_sh = 0;
-  int best_w = 0, best_cu = 0;
-  for (int w : {16, 8, 4}) {
-    const size_t sh = round16(tab_b) + (size_t)w * (ra.acc_words * 4 + cs::ROWS_ENT_STRIDE * 8) + 16 +
-                      round16((size_t)geo.c_out * 4);
-    if (sh > kCuLds) continue;
-    const int per_cu = std::min<int>((int)(kCuLds / sh) * w, 32);
-    if (per_cu > best_cu) {
-      best_cu = per_cu;
-      best_w = w;
-      best_sh = sh;
-    }
-  }
-  if (best_w == 0) return false;
-  ra.off_acc = (uint32_t)round16(tab_b);
-  ra.off_next = ra.off_acc + best_w * ra.acc_words * 4;
-  ra.off_bias = ra.off_next + 16;
-  ra.off_ent = ra.off_bias + (uint32_t)round16((size_t)geo.c_out * 4);
-  pl->shmem = best_sh;
-  pl->waves = best_w;
-  // as many workgroups as fit the chip at once, each with an even share of the items
-  const int64_t wgs = std::min<int64_t>((int64_t)kPlanCus * (best_cu / best_w),
-                                        (items + best_w - 1) / best_w);
-  ra.per_wg = (items + wgs - 1) / wgs;
+  ra.fd_g = cs::make_fastdiv((uint32_t)(rest > 0 ? rest : 1));
   pl->items = items;
-  pl->blocks = (items + ra.per_wg - 1) / ra.per_wg;
+  pl->tab_b = tab_b;
+  // an estimate for the plan report (LDS only); the launch sizes the
+  // workgroups and the grid from the kernel's actual occupancy
   pl->cpl = cpl;
-  return true;
+  for (int w : {16, 8, 4}) {
+    const size_t sh = rows_shmem(*pl, w, geo.c_out);
+    if (sh <= kCuLds)
+      return rows_layout(pl, w, std::min<int>(32, (int)(kCuLds / sh) * w), geo.c_out);
+  }
+  return false;
+}
+
+// Resident workgroups per compute unit of a kernel at a block size and LDS
+// size (0 when the query fails).
+int occupancy(const void* kern, int threads, size_t shmem) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, threads, shmem) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return nb;
 }
 
 template <typename TO, int CPL>
-void launch_rows_c(const RowsPlan& pl, hipStream_t s, const uint16_t* idx, const void* lval,
+void launch_rows_c(RowsPlan pl, hipStream_t s, const uint16_t* idx, const void* lval,
                    const int32_t* cnt, const void* aug, const void* bias, void* y, void* out,
                    const cs::ListOut& lo, const cs::ConvGeom& geo) {
   auto go = [&](auto kern) {
+    // the workgroup size with the most resident wavefronts per compute unit
+    // (registers and LDS), the larger on a tie
+    // resident workgroups per LDS size class, cached per kernel (-1: not yet asked)
+    static std::atomic<int> occ_cache[3][2] = {{{-1}, {-1}}, {{-1}, {-1}}, {{-1}, {-1}}};
+    int best_w = 0, best_cu = 0;
+    int wi = 0;
+    for (int w : {16, 8, 4}) {
+      const size_t sh = rows_shmem(pl, w, geo.c_out);
+      const int slot = wi++;
+      if (sh > kCuLds) continue;
+      int occ = -1;
+      if ((size_t)occ_cache[slot][0].load() == sh) occ = occ_cache[slot][1].load();
+      if (occ < 0) {
+        occ = occupancy(reinterpret_cast<const void*>(kern), 64 * w, sh);
+        occ_cache[slot][1].store(occ);
+        occ_cache[slot][0].store((int)sh);
+      }
+      const int wcu = occ * w;
+      if (wcu > best_cu) {
+        best_cu = wcu;
+        best_w = w;
+      }
+    }
+    if (best_w > 0) rows_layout(&pl, best_w, best_cu, geo.c_out);   // else the plan's layout
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.blocks), dim3(64 * pl.waves), pl.shmem, s, idx,
                        static_cast<const int8_t*>(lval), cnt, static_cast<const uint16_t*>(aug),
                        static_cast<const int32_t*>(bias), static_cast<int32_t*>(y),

@@ -5,7 +5,7 @@
 //
 //  * the workgroup stages the packed table (value + Kernel ID per slot) in LDS
 //    once; after that its wavefronts work without workgroup barriers, each
-//    taking whole items from a workgroup-local counter;
+//    on its own items;
 //  * a wavefront's accumulator row is in output-channel order and starts at
 //    the bias; lane j holds entry j of the item's list (its table row offset
 //    and value); when G > 32 each lane takes the sets g = lane + 64 q and the
@@ -45,16 +45,23 @@ struct RowsArgs {
   int k;
   int shift;
   int write_sums;
-  int S;              // entry slices: 64 / G when G <= 32, else 1
-  int gpl;            // sets per lane when S = 1: ceil(G / 64)
+  int qf;             // groups of 64 sets with wavefront-uniform entries (the last may be partial)
+  int S;              // slices of the remaining Gs sets (0: none)
+  int gbase;          // first of the remaining sets (64 qf)
   uint32_t off_acc;    // LDS byte offset of the wavefronts' rows (table at 0)
   uint32_t acc_words;  // words per wavefront row (>= c_out and >= ROWS_HIST)
-  uint32_t off_next;   // LDS byte offset of the workgroup's item counter
   uint32_t off_bias;   // LDS byte offset of the bias (c_out words)
   uint32_t off_ent;    // LDS byte offset of the wavefronts' entry copies (S > 1 only)
   int64_t per_wg;      // items per workgroup
-  FastDiv fd_g;        // / G
+  FastDiv fd_g;        // / Gs
 };
+
+// A value the compiler must treat as unknown where it is used: keeps it from
+// hoisting per-slot copies of a lane constant out of the item loop.
+__device__ __forceinline__ int opaque_int(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 
 template <typename TO, int CPL, bool FULL>
 __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__ lidx,
@@ -76,7 +83,6 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
   // the packed table [C][G] is at LDS offset 0
   int32_t* acc = reinterpret_cast<int32_t*>(smem + ra.off_acc) + wv * ra.acc_words;
   uint32_t* hist = reinterpret_cast<uint32_t*>(acc);                      // the same words
-  int* next = reinterpret_cast<int*>(smem + ra.off_next);
   int32_t* bias_s = reinterpret_cast<int32_t*>(smem + ra.off_bias);     // [c_out]
   // (row offset, value) of up to 64 entries, then a (0, 0) entry for slots past the list
   int2* ent = reinterpret_cast<int2*>(smem + ra.off_ent) + wv * ROWS_ENT_STRIDE;
@@ -108,7 +114,6 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
   // FULL: c_out = 64 CPL, every lane's slots are channels
   const int nv = FULL ? CPL : (c - ch0 < 0 ? 0 : (c - ch0 < CPL ? c - ch0 : CPL));
   for (int o = tid; o < c; o += nthr) bias_s[o] = bias != nullptr ? bias[o] : 0;
-  if (tid == 0) *next = nwv;
   if (lane == 0) ent[64] = make_int2(0, 0);
   __syncthreads();
   // a lane's slots past c_out (pads) take part as the row's smallest keys and
@@ -118,9 +123,10 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
 
   const int64_t ib = (int64_t)blockIdx.x * ra.per_wg;
   const int nit = (int)(items - ib < ra.per_wg ? items - ib : ra.per_wg);
-  // with S > 1 slices: this lane's slice s and set g0 (lanes past S*G idle)
+  // the remaining sets as slices: this lane's slice s and set gbase + g0
+  // (lanes past S * Gs idle)
   const int s = (int)fdiv((uint32_t)lane, ra.fd_g);
-  const int g0 = lane - s * G;
+  const int g0 = lane - s * (int)ra.fd_g.d;
   const bool job = s < ra.S;
 
   // the next item's count and first 64 list entries (one per lane) are loaded while
@@ -140,10 +146,9 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
   int li = wv;                                                      // uniform
   prefetch(li);
   while (li < nit) {
-    int lnext = 0;
-    if (lane == 0)
-      lnext = __hip_atomic_fetch_add(next, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    lnext = __builtin_amdgcn_readfirstlane(lnext);
+    // the lane's first channel, recomputed per item (not held in registers per slot)
+    const int cl = opaque_int(ch0);
+    const int lnext = li + nwv;
     const int64_t it = ib + li;
     int cnt = __builtin_amdgcn_readfirstlane(cnt_n);
     cnt = cnt < 0 ? 0 : (cnt > cap ? cap : cnt);
@@ -164,40 +169,42 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
         pre = (int)ix * G * 2;
         xv = lane < nb ? (int)v : 0;
       }
-      if (ra.S == 1) {
-        // every lane one set (g = lane + 64 q), entries wavefront-uniform
-        for (int e = 0; e < nb; e += ROWS_BATCH) {                  // uniform
-          int sp[ROWS_BATCH], sx[ROWS_BATCH];
+      // groups of 64 sets: lane l takes set 64 q + l, the entries one after
+      // another (wavefront-uniform, read from their lanes)
+      for (int e = 0; ra.qf > 0 && e < nb; e += ROWS_BATCH) {       // uniform
+        int sp[ROWS_BATCH], sx[ROWS_BATCH];
 #pragma unroll
-          for (int u = 0; u < ROWS_BATCH; ++u) {
-            const int eu = e + u < nb ? e + u : nb - 1;
-            sp[u] = __builtin_amdgcn_readlane(pre, eu);
-            sx[u] = e + u < nb ? __builtin_amdgcn_readlane(xv, eu) : 0;
-          }
-          for (int q = 0; q < ra.gpl; ++q) {                        // uniform
-            const int g = lane + 64 * q;
-            if (g < G) {
-              uint32_t w[ROWS_BATCH];
+        for (int u = 0; u < ROWS_BATCH; ++u) {
+          const int eu = e + u < nb ? e + u : nb - 1;
+          sp[u] = __builtin_amdgcn_readlane(pre, eu);
+          sx[u] = e + u < nb ? __builtin_amdgcn_readlane(xv, eu) : 0;
+        }
+        for (int q = 0; q < ra.qf; ++q) {                           // uniform
+          const int g = lane + 64 * q;
+          if (g < G) {                                              // all lanes but in a last partial group
+            uint32_t w[ROWS_BATCH];
 #pragma unroll
-              for (int u = 0; u < ROWS_BATCH; ++u)
-                w[u] = *reinterpret_cast<const uint16_t*>(smem + sp[u] + 2 * g);
-              int32_t* ag = acc + g * n;
+            for (int u = 0; u < ROWS_BATCH; ++u)
+              w[u] = *reinterpret_cast<const uint16_t*>(smem + sp[u] + 2 * g);
+            int32_t* ag = acc + g * n;
 #pragma unroll
-              for (int u = 0; u < ROWS_BATCH; ++u)
-                __hip_atomic_fetch_add(ag + (int)(w[u] >> 8),
-                                       __mul24(sx[u], (int)(int8_t)(w[u] & 0xFFu)),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
+            for (int u = 0; u < ROWS_BATCH; ++u)
+              __hip_atomic_fetch_add(ag + (int)(w[u] >> 8),
+                                     __mul24(sx[u], (int)(int8_t)(w[u] & 0xFFu)),
+                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
           }
         }
-      } else {
-        // S slices of G sets: lane (s, g0) takes the entries s, s + S, ...,
-        // read from a wavefront-private copy of the entries in LDS
+      }
+      // the remaining Gs sets (from gbase on) as S slices: lane (s, g0) takes
+      // set gbase + g0 and the entries s, s + S, ..., read from a
+      // wavefront-private copy of the entries in LDS
+      if (ra.S > 0) {
         ent[lane] = make_int2(pre, xv);
         wave_lds_order();
         if (job) {
           const int S = ra.S;
-          int32_t* ag = acc + g0 * n;
+          const int g = ra.gbase + g0;
+          int32_t* ag = acc + g * n;
           for (int e = 0; e < nb; e += S * ROWS_BATCH) {            // uniform
             int2 en[ROWS_BATCH];
 #pragma unroll
@@ -208,7 +215,7 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
             uint32_t w[ROWS_BATCH];
 #pragma unroll
             for (int u = 0; u < ROWS_BATCH; ++u)
-              w[u] = *reinterpret_cast<const uint16_t*>(smem + en[u].x + 2 * g0);
+              w[u] = *reinterpret_cast<const uint16_t*>(smem + en[u].x + 2 * g);
 #pragma unroll
             for (int u = 0; u < ROWS_BATCH; ++u)
               __hip_atomic_fetch_add(ag + (int)(w[u] >> 8),
@@ -233,7 +240,7 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
       }
       wave_lds_order();
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) acc[ch0 + i] = bias_s[ch0 + i < c ? ch0 + i : c - 1];
+      for (int i = 0; i < CPL; ++i) acc[cl + i] = bias_s[cl + i < c ? cl + i : c - 1];
       li = lnext;
       continue;
     }
@@ -241,11 +248,11 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
     // ---- the row into registers; its memory becomes the histogram
     uint32_t key[CPL];
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) key[i] = order_key(acc[ch0 + i]);
+    for (int i = 0; i < CPL; ++i) key[i] = order_key(acc[cl + i]);
     if (ra.write_sums) {
 #pragma unroll
       for (int i = 0; i < CPL; ++i)
-        if (i < nv) y[it * c + ch0 + i] = (int32_t)(key[i] ^ 0x80000000u);
+        if (i < nv) y[it * c + cl + i] = (int32_t)(key[i] ^ 0x80000000u);
     }
     uint32_t kmn = 0xFFFFFFFFu, kmx = 0u;
 #pragma unroll
@@ -323,11 +330,6 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
       thr = prefix;
       need = nd;
     }
-    // ---- the row back to the bias for the next item
-    wave_lds_order();
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) acc[ch0 + i] = bias_s[ch0 + i < c ? ch0 + i : c - 1];
-
     // ---- winners in channel order: key > thr, or key == thr among the first `need`
     int gt_l = 0, eq_l = 0;
 #pragma unroll
@@ -338,6 +340,12 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
     const uint32_t pk = (uint32_t)eq_l | ((uint32_t)gt_l << 16);
     const uint32_t pincl = wave_incl_scan(pk, 0u, OpAdd{});
     int eqb = (int)((pincl - pk) & 0xFFFFu);                        // ties in lower lanes
+    // the list of the non-zero winners staged in the row's memory (positions
+    // in channel order, the other slots to spare entries k + lane) and copied
+    // out with consecutive lanes on consecutive entries, when it fits there
+    const int sidx_b = ((k + 64) * 2 + 3) & ~3;
+    const bool stage = lo.idx != nullptr && k >= 0 &&
+                       sidx_b + (k + 64) * (int)sizeof(TO) <= 4 * (int)ra.acc_words;
     if (lo.idx) {
       // the non-zero winners: counted first (bit i of pb), then written at
       // their list positions
@@ -358,13 +366,34 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
       // row base pointers (uniform) and 32-bit byte offsets per lane
       unsigned char* lv = reinterpret_cast<unsigned char*>(static_cast<TO*>(lo.val) + it * lo.cap);
       unsigned char* lx = reinterpret_cast<unsigned char*>(lo.idx + it * lo.cap);
+      if (stage) {
+        uint16_t* sx = reinterpret_cast<uint16_t*>(acc);
+        TO* sv = reinterpret_cast<TO*>(reinterpret_cast<unsigned char*>(acc) + sidx_b);
+        wave_lds_order();                                           // after the histogram reads
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-        if ((pb >> i) & Mask(1)) {
-          *reinterpret_cast<uint16_t*>(lx + 2u * pos) = (uint16_t)(ch0 + i);
-          *reinterpret_cast<TO*>(lv + (uint32_t)sizeof(TO) * pos) =
-              kwta_out<int32_t, TO>((int32_t)((key[i] + kmn) ^ 0x80000000u), ra.shift);
-          ++pos;
+        for (int i = 0; i < CPL; ++i) {
+          const bool put = (pb >> i) & Mask(1);
+          const int p = put ? (int)pos : k + lane;
+          sx[p] = (uint16_t)(cl + i);
+          sv[p] = kwta_out<int32_t, TO>((int32_t)((key[i] + kmn) ^ 0x80000000u), ra.shift);
+          pos += put ? 1u : 0u;
+        }
+        wave_lds_order();
+        const int total = __builtin_amdgcn_readlane(pin, 63);
+        for (int j = lane; j < total; j += 64) {
+          *reinterpret_cast<uint16_t*>(lx + 2u * (uint32_t)j) = sx[j];
+          *reinterpret_cast<TO*>(lv + (uint32_t)sizeof(TO) * (uint32_t)j) = sv[j];
+        }
+        wave_lds_order();                                           // before the row is reset
+      } else {
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+          if ((pb >> i) & Mask(1)) {
+            *reinterpret_cast<uint16_t*>(lx + 2u * pos) = (uint16_t)(cl + i);
+            *reinterpret_cast<TO*>(lv + (uint32_t)sizeof(TO) * pos) =
+                kwta_out<int32_t, TO>((int32_t)((key[i] + kmn) ^ 0x80000000u), ra.shift);
+            ++pos;
+          }
         }
       }
       if (lane == 63) lo.cnt[it] = pin;
@@ -375,9 +404,13 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
         const bool win = key[i] > thr || (eq && eqb < need);
         eqb += eq ? 1 : 0;
         const TO ov = kwta_out<int32_t, TO>((int32_t)((key[i] + kmn) ^ 0x80000000u), ra.shift);
-        if (i < nv) out[it * c + ch0 + i] = win ? ov : TO(0);
+        if (i < nv) out[it * c + cl + i] = win ? ov : TO(0);
       }
     }
+    // ---- the row back to the bias for the next item
+    wave_lds_order();
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) acc[cl + i] = bias_s[cl + i < c ? cl + i : c - 1];
     li = lnext;
   }
 }
