@@ -205,6 +205,38 @@ def cpu_baseline(cfg, inp, seconds: float) -> dict:
                       f"{el:.1f} s on {os.cpu_count()} host CPUs (BLAS threads {threads})"}
 
 
+def ab_reorder(cfg, inp, x, kernel_ms, breakdown) -> dict:
+    """The first layer by reordering (cs_conv2d_reorder_kwta, the support of
+    every output gathered from the dense input) against the routed launches
+    of the same layer (compaction + multiply-route-sum with k-WTA)."""
+    import torch
+    from paper_2112_13896_amd import ops
+
+    spec = cfg.layers[0]
+    if not (cfg.dtype == "f32" and spec.kind == "conv" and spec.c_out == 64 and spec.stride == 1
+            and spec.pool == 1 and spec.k is not None and spec.k <= 32):
+        return {"layer": spec.name, "supported": False}
+    W = inp["W"][0]
+    aug, _ = ops.pack(W.reshape(spec.c_out, -1), spec.n)
+    table = torch.from_numpy(ops.reorder_table(aug, spec.kh, spec.kw, spec.c_in, spec.c_out,
+                                               spec.n)).cuda()
+    bias = None if inp["b"][0] is None else torch.from_numpy(inp["b"][0]).cuda()
+    rows = x.shape[0] * x.shape[1] * x.shape[2]
+    cap = ops.list_capacity(spec.k)
+    lists = (torch.empty((rows, cap), dtype=torch.int16, device="cuda"),
+             torch.empty((rows, cap), dtype=torch.float32, device="cuda"),
+             torch.empty((rows,), dtype=torch.int32, device="cuda"))
+    y = torch.empty(x.shape[:3] + (spec.c_out,), dtype=torch.float32, device="cuda")
+
+    def call():
+        ops.conv2d_reorder_kwta(x, table, spec.kh, spec.kw, spec.pad, bias, k=spec.k, y=y,
+                                keep_sums=False, lists=lists)
+    call()
+    routed = sum(v for k, v in breakdown.items() if k.startswith(spec.name + "."))
+    return {"layer": spec.name, "supported": True, "reorder_us": round(kernel_ms(call) * 1e3, 2),
+            "routed_us": round(routed * 1e3, 2), "table_entries_per_output": int(table.shape[1])}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,6 +246,9 @@ def main() -> int:
     ap.add_argument("--rotate-mib", type=float, default=512.0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ab-reorder", action="store_true",
+                    help="also time the first layer by reordering the activations instead of "
+                         "routing the products (fp32 dense-input 64-channel layers)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
                     help="only copy a MIB-sized device buffer --steps times (reference kernel "
                          "for scaling the HBM byte counters)")
@@ -323,6 +358,8 @@ def main() -> int:
         "roofline": roof,
         "kernels": kernels,
     }
+    if args.ab_reorder:
+        res["ab_reorder"] = ab_reorder(cfg, inp, xs[0], kernel_ms, breakdown)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)

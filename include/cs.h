@@ -272,6 +272,61 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
                          int pool, void* y, int keep_sums, int k, cs_dtype ot, int shift, void* out,
                          uint16_t* oidx, void* oval, int32_t* ocnt, int ocap, void* stream);
 
+/* Output tile side of the reordering kernel (CS_REORDER_TILE^2 pixels). */
+#define CS_REORDER_TILE 8
+
+/*
+ * cs_reorder_table - the packed kernel in Kernel-ID order, for reordering
+ * the activations instead of routing the products (Section 3.2: reordering
+ * the incoming activations as the alternative to routing the element-wise
+ * products).  Offline, HOST memory only, no HIP call.  For every output
+ * o = g*n + kid the table lists the slots i of set g with kid[i][g] == kid and
+ * a non-zero value (the support of kernel o), in ascending slot order, as
+ * pairs (byte offset of slot i in cs_conv2d_reorder_kwta's input tile,
+ * value bits): slot i = (ky*kw + kx)*c_in + c has offset
+ * 4*((ky*(CS_REORDER_TILE + kw - 1) + kx)*(c_in + 1) + c).
+ *
+ *  aug     host [kh*kw*c_in][c_out/n] cs_aug_f32 entries (cs_pack, CS_F32).
+ *  smax    in/out: with table == NULL, receives the longest support (>= 1);
+ *          else the entries per output the table has room for (>= that).
+ *  table   host [c_out][smax][2] int32 out (may be NULL), outputs shorter
+ *          than smax padded with (0, 0.0f).
+ *  Errors: CS_ERR_ARG (null aug/smax, sizes < 1, a kid >= n), CS_ERR_SHAPE
+ *  (n does not divide c_out, n > CS_MAX_N, kh*kw*c_in > CS_MAX_ROW, smax too
+ *  small).
+ */
+int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c_out, int n, int* smax,
+                     int32_t* table);
+
+/*
+ * cs_conv2d_reorder_kwta - a dense-input fp32 conv layer computed by
+ * reordering instead of routing: every output reads the activations at its
+ * kernel's support (cs_reorder_table) and sums their products in a register;
+ * then k-WTA along the channels of every output pixel as cs_mrs_kwta_conv2d.
+ * Same sums as cs_conv2d_dense_kwta / cs_conv2d + cs_mrs_kwta_conv2d up to
+ * fp32 rounding order.  DEVICE memory (except the scalars).
+ *
+ *  xt      CS_F32.  x device NHWC [b][h][w][c_in] dense activations.
+ *  kh, kw, pad   window and zero padding; stride 1, no pooling.
+ *  table, smax   device copy of cs_reorder_table's table for this layer, with
+ *          smax a multiple of 8 (CS_ERR_SHAPE otherwise).
+ *  c_out   must be 64; c_in <= 64.
+ *  bias    device [c_out] (may be NULL).
+ *  y, keep_sums  device [b][ho][wo][c_out] sums, written when keep_sums == 1
+ *          (16-byte aligned).
+ *  k       winners per pixel, 0 <= k <= 32 or k == c_out; ot CS_F32.
+ *  out | (oidx, oval, ocnt, ocap)   exactly one: dense [b][ho][wo][c_out]
+ *          output (winners keep their value, the rest 0; 16-byte aligned), or
+ *          lists as cs_mrs_kwta_conv2d with ocap >= k and a multiple of 4,
+ *          oidx 8-byte and oval 16-byte aligned.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE, CS_ERR_DEVICE.
+ */
+int cs_conv2d_reorder_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
+                           int kw, int pad, const int32_t* table, int smax, int c_out,
+                           const void* bias, void* y, int keep_sums, int k, cs_dtype ot,
+                           void* out, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap,
+                           void* stream);
+
 /*
  * cs_kwta - k-WTA (Section 2.2.2: exactly the top k activations propagate;
  * Section 3.3.3: global k-WTA over a vector after linear layers, local k-WTA

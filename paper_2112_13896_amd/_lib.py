@@ -38,6 +38,9 @@ SIGNATURES = {
                          _c.POINTER(_i64)]),
     "cs_conv2d_dense_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                                   _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
+    "cs_reorder_table": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),
+    "cs_conv2d_reorder_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _vp,
+                                    _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i, _vp, _vp,
                        _sz, _vp]),

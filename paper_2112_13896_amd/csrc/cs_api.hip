@@ -14,6 +14,7 @@
 #include "cs.h"
 #include "kwta_kernels.h"
 #include "mrs_fused.h"
+#include "mrs_reorder.h"
 #include "mrs_kernels.h"
 #include "mrs_sample.h"
 #include "mrs_rows.h"
@@ -1334,3 +1335,53 @@ size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in) {
 }
 
 }  // extern "C"
+
+int cs_conv2d_reorder_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
+                           int kw, int pad, const int32_t* table, int smax, int c_out,
+                           const void* bias, void* y, int keep_sums, int k, cs_dtype ot,
+                           void* out, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap,
+                           void* stream) {
+  if (xt != CS_F32 || ot != CS_F32) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, 1, pad, c_out, 1, 1, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !table || !y || smax < 1) return CS_ERR_ARG;
+  if (smax % 8 != 0) return CS_ERR_SHAPE;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0) return CS_ERR_ARG;
+  if (c_out != cs::RO_COUT || c_in > 64 || k > c_out || (k > 32 && k != c_out)) return CS_ERR_SHAPE;
+  const bool lists = oidx != nullptr;
+  if (lists == (out != nullptr)) return CS_ERR_ARG;
+  if (lists && (!oval || !ocnt || ocap < 1)) return CS_ERR_ARG;
+  if (lists && (ocap < k || ocap % 4 != 0 || !aligned(oidx, 8) || !aligned(oval, 16)))
+    return CS_ERR_SHAPE;
+  if (!aligned(y, 16) || !aligned(out, 16)) return CS_ERR_ARG;
+  const int tiles_w = (geo.Wo + cs::RO_T - 1) / cs::RO_T, tiles_h = (geo.Ho + cs::RO_T - 1) / cs::RO_T;
+  const int64_t nb = (int64_t)b * tiles_w * tiles_h;
+  if (nb >= INT32_MAX || (int64_t)smax * c_out * 2 >= INT32_MAX) return CS_ERR_SHAPE;
+  // the input tile, reused afterwards for the per-lane list staging
+  const size_t halo = (size_t)(cs::RO_T + kh - 1) * (cs::RO_T + kw - 1) * (c_in + 1) * 4;
+  const size_t stage = lists ? (size_t)64 * ocap * 6 : 0;
+  const size_t shmem = round16(std::max(halo, stage));
+  if (shmem > kCuLds) return CS_ERR_SHAPE;
+  cs::ReorderArgs ra{};
+  ra.smax = smax;
+  ra.tiles_w = tiles_w;
+  ra.tiles_img = tiles_w * tiles_h;
+  ra.k = k;
+  ra.write_sums = keep_sums;
+  ra.vec4 = (c_in % 4 == 0 && aligned(x, 16)) ? 1 : 0;
+  const cs::ListOut lo{oidx, oval, ocnt, lists ? ocap : 0};
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3((unsigned)nb), dim3(64), shmem, s, static_cast<const float*>(x),
+                       reinterpret_cast<const int2*>(table), static_cast<const float*>(bias),
+                       static_cast<float*>(y), static_cast<float*>(out), lo, geo, ra);
+  };
+  if (k <= 8)
+    go(cs::conv_reorder_f32<8>);
+  else if (k <= 16)
+    go(cs::conv_reorder_f32<16>);
+  else
+    go(cs::conv_reorder_f32<32>);
+  return launch_status();
+}

@@ -71,6 +71,55 @@ extern "C" int cs_pack(cs_dtype wt, const void* w, int d_out, int r, int n, void
   }
 }
 
+extern "C" int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c_out, int n,
+                                int* smax, int32_t* table) {
+  if (!aug || !smax || kh < 1 || kw < 1 || c_in < 1 || c_out < 1 || n < 1) return CS_ERR_ARG;
+  if (n > CS_MAX_N || c_out % n != 0) return CS_ERR_SHAPE;
+  if ((int64_t)kh * kw * c_in > CS_MAX_ROW) return CS_ERR_SHAPE;
+  const int G = c_out / n, R = kh * kw * c_in;
+  const cs_aug_f32* a = static_cast<const cs_aug_f32*>(aug);
+  // the support of every kernel: its non-zero slots (holes and zero weights
+  // add nothing and are left out)
+  int longest = 0;
+  for (int o = 0; o < c_out; ++o) {
+    const int g = o / n, kid = o - g * n;
+    int cnt = 0;
+    for (int i = 0; i < R; ++i) {
+      const cs_aug_f32& e = a[(int64_t)i * G + g];
+      if (e.kid >= (uint32_t)n) return CS_ERR_ARG;
+      cnt += (e.value != 0.f && (int)e.kid == kid) ? 1 : 0;
+    }
+    longest = cnt > longest ? cnt : longest;
+  }
+  const int sm = longest > 0 ? longest : 1;
+  if (!table) {
+    *smax = sm;
+    return CS_OK;
+  }
+  if (*smax < sm) return CS_ERR_SHAPE;
+  const int hw = CS_REORDER_TILE + kw - 1, cp = c_in + 1;
+  for (int o = 0; o < c_out; ++o) {
+    const int g = o / n, kid = o - g * n;
+    int32_t* t = table + (int64_t)o * *smax * 2;
+    int j = 0;
+    for (int i = 0; i < R; ++i) {
+      const cs_aug_f32& e = a[(int64_t)i * G + g];
+      if (e.value == 0.f || (int)e.kid != kid) continue;
+      // slot i = (ky * kw + kx) * c_in + c -> byte offset in the input tile
+      const int tap = i / c_in, c = i - tap * c_in;
+      const int ky = tap / kw, kx = tap - ky * kw;
+      t[2 * j] = 4 * ((ky * hw + kx) * cp + c);
+      std::memcpy(&t[2 * j + 1], &e.value, 4);
+      ++j;
+    }
+    for (; j < *smax; ++j) {                                      // padding: offset 0, weight 0
+      t[2 * j] = 0;
+      t[2 * j + 1] = 0;
+    }
+  }
+  return CS_OK;
+}
+
 extern "C" const char* cs_status_str(int status) {
   switch (status) {
     case CS_OK: return "ok";

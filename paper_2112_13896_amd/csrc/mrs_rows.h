@@ -56,13 +56,6 @@ struct RowsArgs {
   FastDiv fd_g;        // / Gs
 };
 
-// A value the compiler must treat as unknown where it is used: keeps it from
-// hoisting per-slot copies of a lane constant out of the item loop.
-__device__ __forceinline__ int opaque_int(int v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
-
 template <typename TO, int CPL, bool FULL>
 __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__ lidx,
                                                     const int8_t* __restrict__ lval,

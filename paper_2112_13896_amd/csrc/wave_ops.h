@@ -71,4 +71,12 @@ __device__ __forceinline__ int row16_incl_sum(int v) {
   return v;
 }
 
+// A value the compiler must treat as unknown where it is used: keeps it from
+// hoisting per-slot copies of a lane constant out of a loop, or (a lane's
+// own zero) makes a wavefront-uniform address a vector one.
+__device__ __forceinline__ int opaque_int(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 }  // namespace cs

@@ -315,6 +315,66 @@ def conv2d_dense_kwta(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: i
     return y, result
 
 
+def reorder_table(aug: np.ndarray, kh: int, kw: int, c_in: int, c_out: int, n: int) -> np.ndarray:
+    """cs_reorder_table: the fp32 packed kernel (host, from pack) in Kernel-ID
+    order, int32 [c_out][smax][2] (tile byte offset, value bits), smax the
+    longest support rounded up to a multiple of 8."""
+    if not (aug.dtype == np.uint32 and aug.ndim == 3 and aug.shape[2] == 2):
+        raise TypeError("reorder_table takes an fp32 packed kernel (uint32 [r][G][2])")
+    aug = np.ascontiguousarray(aug)
+    smax = ctypes.c_int(0)
+    check("cs_reorder_table", lib().cs_reorder_table(aug.ctypes.data, kh, kw, c_in, c_out, n,
+                                                     ctypes.byref(smax), None))
+    smax.value = (smax.value + 7) // 8 * 8           # the kernel reads 8 entries at a time
+    table = np.zeros((c_out, smax.value, 2), dtype=np.int32)
+    check("cs_reorder_table", lib().cs_reorder_table(aug.ctypes.data, kh, kw, c_in, c_out, n,
+                                                     ctypes.byref(smax), table.ctypes.data))
+    return table
+
+
+def conv2d_reorder_kwta(x: torch.Tensor, table: torch.Tensor, kh: int, kw: int, pad: int = 0,
+                        bias: torch.Tensor | None = None, *, k: int,
+                        y: torch.Tensor | None = None, keep_sums: bool = True,
+                        cap: int | None = None, lists=None, out: torch.Tensor | None = None):
+    """A dense-input fp32 conv layer by reordering (cs_conv2d_reorder_kwta);
+    table is reorder_table's result on the device.  Returns (y, result) as
+    mrs_kwta_conv2d does."""
+    if x.dim() != 4:
+        raise ValueError("x must be NHWC")
+    if table.dim() != 3 or table.dtype != torch.int32 or table.shape[2] != 2:
+        raise ValueError("table must be int32 [c_out][smax][2]")
+    b, h, w, c_in = x.shape
+    c_out, smax = table.shape[0], table.shape[1]
+    ho, wo = conv_out(h, kh, 1, pad), conv_out(w, kw, 1, pad)
+    oshape = (b, max(ho, 0), max(wo, 0), c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    if y is None:
+        y = torch.empty(oshape, dtype=torch.float32, device=x.device)
+    if lists is None and cap is not None:
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=x.device),
+                 torch.empty((rows, cap), dtype=torch.float32, device=x.device),
+                 torch.empty((rows,), dtype=torch.int32, device=x.device))
+    if lists is not None:
+        oi, ov, oc = lists
+        if oi.dtype != torch.int16 or ov.dtype != torch.float32 or oc.dtype != torch.int32:
+            raise TypeError("list buffer dtypes do not match")
+        if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+            raise ValueError("list buffer shapes do not match the output")
+        args = (None, _dev(oi, "oidx"), _dev(ov, "oval"), _dev(oc, "ocnt"), oi.shape[1])
+        result = lists
+    else:
+        if out is None:
+            out = torch.empty(oshape, dtype=torch.float32, device=x.device)
+        if out.dtype != torch.float32 or out.numel() != rows * c_out:
+            raise ValueError("out does not match the output")
+        args = (_dev(out, "out"), None, None, None, 0)
+        result = out
+    check("cs_conv2d_reorder_kwta", lib().cs_conv2d_reorder_kwta(
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, pad, _dev(table, "table"), smax, c_out,
+        _opt(bias, "bias"), _dev(y, "y"), 1 if keep_sums else 0, k, CS_F32, *args, _stream()))
+    return y, result
+
+
 def linear(x: torch.Tensor, aug: torch.Tensor, n: int,
            bias: torch.Tensor | None = None, ws: torch.Tensor | None = None,
            out: torch.Tensor | None = None) -> torch.Tensor:

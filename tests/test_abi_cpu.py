@@ -165,6 +165,108 @@ def test_conv2d_dense_validation(L):
     assert call(pool=2, h=33, w=33) == CS_ERR_SHAPE
 
 
+def _reorder_eval(x, table, kh, kw, pad, bias):
+    """The reordering kernel's sums, evaluated on the CPU in float64 from the
+    table: each output tile's zero-padded input halo laid out as the kernel
+    stages it (rows of tile + kw - 1 pixels of c_in + 1 words), every output
+    the sum of halo[pixel offset + table offset] * value over its entries."""
+    T = 8
+    b, h, w, c = x.shape
+    ho, wo = h + 2 * pad - kh + 1, w + 2 * pad - kw + 1
+    hw, hh, cp = T + kw - 1, T + kh - 1, c + 1
+    off = table[..., 0] // 4
+    val = table[..., 1].copy().view(np.float32).astype(np.float64)
+    y = np.zeros((b, ho, wo, table.shape[0]))
+    for bi in range(b):
+        for ty in range(0, ho, T):
+            for tx in range(0, wo, T):
+                halo = np.zeros((hh, hw, cp))
+                for yy in range(hh):
+                    for xx in range(hw):
+                        iy, ix = ty + yy - pad, tx + xx - pad
+                        if 0 <= iy < h and 0 <= ix < w:
+                            halo[yy, xx, :c] = x[bi, iy, ix]
+                flat = halo.reshape(-1)
+                for py in range(min(T, ho - ty)):
+                    for px in range(min(T, wo - tx)):
+                        base = (py * hw + px) * cp
+                        y[bi, ty + py, tx + px] = (flat[base + off] * val).sum(axis=1)
+    if bias is not None:
+        y += bias
+    return y
+
+
+def test_reorder_table_lists_each_support():
+    """Every output's table entries are exactly its kernel's non-zero weights,
+    each once, with the slot's (ky, kx, c) recoverable from the offset."""
+    r = np.random.default_rng(11)
+    for c_out, kh, kw, c_in, n in [(64, 3, 3, 64, 8), (64, 1, 1, 30, 2), (64, 5, 5, 16, 2)]:
+        W = complementary_weights(r, r, c_out, kh * kw * c_in, n, "normal")
+        aug, _ = ops.pack(W, n)
+        t = ops.reorder_table(aug, kh, kw, c_in, c_out, n)
+        hw, cp = 8 + kw - 1, c_in + 1
+        longest = max(np.count_nonzero(W, axis=1).max(), 1)
+        assert t.shape[0] == c_out and t.shape[1] == (longest + 7) // 8 * 8
+        for oi in range(c_out):
+            got = {}
+            for off, vb in t[oi]:
+                v = np.array([vb], np.int32).view(np.float32)[0]
+                if v == 0:
+                    assert off == 0                    # padding
+                    continue
+                wrd = off // 4
+                pix, ch = divmod(wrd, cp)
+                ky, kx = divmod(pix, hw)
+                slot = (ky * kw + kx) * c_in + ch
+                assert slot not in got
+                got[slot] = v
+            want = {i: W[oi, i] for i in np.flatnonzero(W[oi])}
+            assert got == want
+
+
+def test_reorder_table_sums_match_oracle():
+    """The table evaluated the way the kernel reads it (tile halos in its LDS
+    layout) gives the oracle's convolution, including ragged edge tiles."""
+    r = np.random.default_rng(12)
+    for shape, kh, pad, n in [((1, 11, 13, 16), 3, 1, 4), ((2, 9, 10, 8), 5, 2, 2)]:
+        b, h, w, c = shape
+        x = np.where(r.random(shape) < 0.2, np.abs(r.normal(size=shape)), 0).astype(np.float32)
+        W = complementary_weights(r, r, 64, kh * kh * c, n, "normal").reshape(64, kh, kh, c)
+        bias = r.normal(size=64).astype(np.float32)
+        aug, _ = ops.pack(W.reshape(64, -1), n)
+        t = ops.reorder_table(aug, kh, kh, c, 64, n)
+        np.testing.assert_allclose(_reorder_eval(x, t, kh, kh, pad, bias),
+                                   o.conv2d_nhwc(x, W, 1, pad, bias), rtol=1e-12, atol=1e-12)
+
+
+def test_reorder_validation(L):
+    f = L.cs_reorder_table
+    sm = ctypes.c_int(0)
+    assert f(None, 3, 3, 64, 64, 8, ctypes.byref(sm), None) == CS_ERR_ARG
+    assert f(FAKE, 3, 3, 64, 64, 7, ctypes.byref(sm), None) == CS_ERR_SHAPE   # 7 does not divide 64
+    assert f(FAKE, 3, 3, 64, 64, 40, ctypes.byref(sm), None) == CS_ERR_SHAPE  # n > CS_MAX_N
+    g = L.cs_conv2d_reorder_kwta
+    ok = dict(xt=CS_F32, x=FAKE, b=1, h=8, w=8, c_in=64, kh=3, kw=3, pad=1, table=FAKE, smax=72,
+              c_out=64, bias=None, y=FAKE, keep_sums=0, k=8, ot=CS_F32, out=None, oidx=FAKE,
+              oval=FAKE, ocnt=FAKE, ocap=8, stream=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return g(*a.values())
+    assert call(xt=CS_I8) == CS_ERR_DTYPE
+    assert call(c_out=32) == CS_ERR_SHAPE
+    assert call(c_in=65) == CS_ERR_SHAPE
+    assert call(k=40, ocap=40) == CS_ERR_SHAPE      # 32 < k < c_out
+    assert call(ocap=6) == CS_ERR_SHAPE             # not a multiple of 4
+    assert call(ocap=4) == CS_ERR_SHAPE             # < k
+    assert call(table=None) == CS_ERR_ARG
+    assert call(smax=70) == CS_ERR_SHAPE            # not a multiple of 8
+    assert call(out=FAKE) == CS_ERR_ARG             # both output forms
+    assert call(oidx=None, oval=None, ocnt=None, ocap=0) == CS_ERR_ARG   # neither
+    assert call(y=FAKE + 4) == CS_ERR_ARG           # y not 16-byte aligned
+
+
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, 8, 4, None, 1, FAKE, None]
