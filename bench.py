@@ -114,7 +114,7 @@ def layer_costs(net, bufs, cfg) -> dict:
                                            "products": prods, "int": is_int}
             continue
         costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
-                                  "int": is_int}
+                                  "int": is_int, "lists_in": 0 if pl.dense_kernel else lists}
         if s.k is not None:
             if pl.emit_lists:
                 lc = bufs.lists[li][2].cpu().numpy().astype(np.int64)
@@ -123,6 +123,15 @@ def layer_costs(net, bufs, cfg) -> dict:
             else:
                 ob = 1 if s.shift is not None else 4
                 costs[f"{s.name}.kwta"] = {"bytes": out_elems * (4 + ob)}
+    # a call that runs two layers (a layer and the last layer on its winners):
+    # both layers' bytes, less the second one's list reads (they stay on chip)
+    for li, pl in enumerate(net.plans):
+        if pl.fuse_next:
+            a = costs[f"{net.packed[li].spec.name}.mrs_kwta"]
+            z = costs[f"{net.packed[li + 1].spec.name}.mrs"]
+            costs[f"{net.packed[li].spec.name}.mrs_kwta+{net.packed[li + 1].spec.name}.mrs"] = {
+                "bytes": a["bytes"] + z["bytes"] - z["lists_in"],
+                "products": a["products"] + z["products"], "int": a["int"]}
     return costs
 
 

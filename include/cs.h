@@ -237,6 +237,32 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
               void* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * cs_mrs_kwta_chain2 - two layers of a chain's tail: a layer with k-WTA whose
+ * output is one vector per sample (a linear layer, or a conv whose pooled map
+ * is 1 x 1), then a linear layer without k-WTA on its requantised winners
+ * (Figure 10: the winners go on with their indices).  When the first layer
+ * runs one workgroup per sample (as cs_mrs_plan reports, path 3) both run in
+ * one kernel: every winner (channel i, value v) adds v times the second
+ * layer's packed row i into LDS accumulators, and the winners never leave the
+ * chip (their lists are still written); otherwise cs_mrs_kwta_conv2d and
+ * cs_mrs_conv2d run back to back on `stream`.  DEVICE memory.
+ *
+ *  xt .. ocap   as cs_mrs_kwta_conv2d, with xt == ot == CS_I8 and list
+ *          output (oidx, oval, ocnt, ocap; no dense out).
+ *  aug2, c_out2, n2, bias2   the second layer (cs_pack of [c_out2][c_out]
+ *          int8 weights; bias2 int32 [c_out2] or NULL).
+ *  y2      device int32 [b][c_out2] out: the second layer's sums.
+ *  Errors: as cs_mrs_kwta_conv2d; CS_ERR_SHAPE when the first layer's output
+ *  is not one vector per sample.
+ */
+int cs_mrs_kwta_chain2(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, uint16_t* oidx, void* oval,
+                       int32_t* ocnt, int ocap, const void* aug2, int c_out2, int n2,
+                       const void* bias2, void* y2, void* stream);
+
+/*
  * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
  * Route, Sum with dense activations; Section 4 runs the first layer of the
  * keyword-spotting network this way because its input is dense).  DEVICE

@@ -36,6 +36,9 @@ SIGNATURES = {
                                 _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_mrs_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
                          _c.POINTER(_i64)]),
+    "cs_mrs_kwta_chain2": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
+                                _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp,
+                                _vp, _vp]),
     "cs_conv2d_dense_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                                   _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_reorder_table": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),

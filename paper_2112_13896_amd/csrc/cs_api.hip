@@ -509,26 +509,29 @@ bool sample_plan(const cs::ConvGeom& geo, cs_dtype xt, int k, int shift, int wri
 template <typename T, typename A, typename TO>
 void launch_sample_t(const SamplePlan& pl, hipStream_t stream, const uint16_t* idx,
                      const void* lval, const int32_t* cnt, const void* aug, const void* bias,
-                     void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+                     void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo,
+                     const cs::NextLayer& nx) {
   using E = typename cs::Aug<T>::type;
-  hipLaunchKernelGGL((cs::mrs_sample<T, A, TO>), dim3(geo.B), dim3(cs::SAMPLE_BD), pl.shmem,
+  const size_t shmem = nx.aug ? (size_t)nx.off_acc + round16((size_t)nx.c_out * 4) : pl.shmem;
+  hipLaunchKernelGGL((cs::mrs_sample<T, A, TO>), dim3(geo.B), dim3(cs::SAMPLE_BD), shmem,
                      stream, idx, static_cast<const T*>(lval), cnt, static_cast<const E*>(aug),
                      static_cast<const A*>(bias), static_cast<A*>(y), static_cast<TO*>(out), lo,
-                     geo, pl.sa);
+                     geo, pl.sa, nx);
 }
 
 int launch_sample(const SamplePlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stream,
                   const uint16_t* idx, const void* lval, const int32_t* cnt, const void* aug,
                   const void* bias, void* y, void* out, const cs::ListOut& lo,
-                  const cs::ConvGeom& geo) {
+                  const cs::ConvGeom& geo, const cs::NextLayer& nx = cs::NextLayer{}) {
   if (xt == CS_F32)
-    launch_sample_t<float, float, float>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo, geo);
+    launch_sample_t<float, float, float>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo, geo,
+                                         nx);
   else if (ot == CS_I8)
     launch_sample_t<int8_t, int32_t, int8_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
-                                             geo);
+                                             geo, nx);
   else
     launch_sample_t<int8_t, int32_t, int32_t>(pl, stream, idx, lval, cnt, aug, bias, y, out, lo,
-                                              geo);
+                                              geo, nx);
   return launch_status();
 }
 
@@ -1384,4 +1387,48 @@ int cs_conv2d_reorder_kwta(cs_dtype xt, const void* x, int b, int h, int w, int 
   else
     go(cs::conv_reorder_f32<32>);
   return launch_status();
+}
+
+int cs_mrs_kwta_chain2(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, uint16_t* oidx, void* oval,
+                       int32_t* ocnt, int ocap, const void* aug2, int c_out2, int n2,
+                       const void* bias2, void* y2, void* stream) {
+  if (xt != CS_I8 || ot != CS_I8) return CS_ERR_DTYPE;
+  if (!aug2 || !y2 || !oidx) return CS_ERR_ARG;
+  if (c_out2 < 1 || n2 < 1) return CS_ERR_ARG;
+  if (n2 > CS_MAX_N || c_out2 % n2 != 0) return CS_ERR_SHAPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  // the first layer as cs_mrs_kwta_conv2d checks it, the second as a linear
+  // layer over the first one's output vector (one per sample when the first
+  // layer's map is 1 x 1)
+  const bool vec = geo.Ho / pool == 1 && geo.Wo / pool == 1;
+  if (!vec) return CS_ERR_SHAPE;
+  if (cap < 1) return CS_ERR_SHAPE;
+  if (!idx || !lval || !cnt || !aug || !y || !oval || !ocnt || ocap < 1) return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0 || shift < 0 || shift > 31) return CS_ERR_ARG;
+  if (k > c_out || c_out > CS_MAX_KWTA_ROW || ocap < k) return CS_ERR_SHAPE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  geo.cap = cap;
+  SamplePlan sp;
+  if (sample_plan(geo, xt, k, shift, keep_sums, &sp)) {
+    // one kernel: the first layer's winners feed the second layer in LDS
+    cs::NextLayer nx{static_cast<const uint16_t*>(aug2), static_cast<const int32_t*>(bias2),
+                     static_cast<int32_t*>(y2), c_out2 / n2, n2, c_out2,
+                     (uint32_t)round16(sp.shmem)};
+    if ((size_t)nx.off_acc + round16((size_t)c_out2 * 4) <= kCuLds) {
+      const cs::ListOut lo{oidx, oval, ocnt, ocap};
+      return launch_sample(sp, xt, ot, s, idx, lval, cnt, aug, bias, y, nullptr, lo, geo, nx);
+    }
+  }
+  // two launches: the layer with its lists, then the linear layer on them
+  st = cs_mrs_kwta_conv2d(xt, idx, lval, cnt, cap, b, h, w, c_in, kh, kw, stride, pad, aug, c_out,
+                          n, bias, pool, y, keep_sums, k, ot, shift, nullptr, oidx, oval, ocnt,
+                          ocap, stream);
+  if (st != CS_OK) return st;
+  return cs_mrs_conv2d(CS_I8, oidx, oval, ocnt, ocap, b, 1, 1, c_out, 1, 1, 1, 0, aug2, c_out2, n2,
+                       bias2, 1, y2, stream);
 }

@@ -52,6 +52,20 @@ struct SampleArgs {
   uint32_t off_row, off_ent, off_val, off_pix, off_hist, off_misc;   // LDS byte offsets (acc at 0)
 };
 
+// An optional linear layer without k-WTA fed by this layer's winners (the
+// last layer of a chain): its packed table aug [c_out of this layer][G]
+// (int8 entries), bias [c_out] and sums y [rows][c_out].  aug == nullptr:
+// none.  int8 chains only.
+constexpr int NX_MAXG = 16;   // next-layer sets whose rows a thread loads ahead
+
+struct NextLayer {
+  const uint16_t* aug;
+  const int32_t* bias;
+  int32_t* y;
+  int G, n, c_out;
+  uint32_t off_acc;  // LDS byte offset of its c_out accumulators
+};
+
 // Exclusive prefix sum of one int per thread over the workgroup; *total gets
 // the sum.  ws: SAMPLE_BD / 64 ints.  Barriers inside (call uniformly, with
 // every thread active).
@@ -88,7 +102,8 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
                                                         const typename Aug<T>::type* __restrict__ aug,
                                                         const A* __restrict__ bias,
                                                         A* __restrict__ y, TO* __restrict__ out,
-                                                        ListOut lo, ConvGeom geo, SampleArgs sa) {
+                                                        ListOut lo, ConvGeom geo, SampleArgs sa,
+                                                        NextLayer nx) {
   using E = typename Aug<T>::type;
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -316,6 +331,25 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
     need = nd;
   }
 
+  // the next layer's accumulators start at zero (the scan's barriers order
+  // this before its adds); the packed rows of the keys that can win (key >=
+  // T) are loaded now, their latency hidden behind the scan and the lists
+  int32_t* acc2 = reinterpret_cast<int32_t*>(smem + nx.off_acc);
+  uint16_t pw[SAMPLE_KEYS][NX_MAXG];
+  if (nx.aug != nullptr) {
+    for (int o = tid; o < nx.c_out; o += SAMPLE_BD) acc2[o] = 0;
+    if (nx.G <= NX_MAXG) {
+#pragma unroll
+      for (int j = 0; j < SAMPLE_KEYS; ++j) {
+        if (i0 + j < c_out && key[j] >= thr) {
+          const uint16_t* r = nx.aug + (int64_t)(i0 + j) * nx.G;
+#pragma unroll
+          for (int g = 0; g < NX_MAXG; ++g) pw[j][g] = g < nx.G ? r[g] : (uint16_t)0;
+        }
+      }
+    }
+  }
+
   // ---- one scan: keys above the threshold (with a non-zero output, for
   // lists) and keys equal to it, packed as two 16-bit counts
   int gt_t = 0, eq_t = 0;
@@ -329,6 +363,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
   int tot2 = 0;
   const int pre = sample_scan(gt_t | (eq_t << 16), misc, &tot2);
   int gt_before = pre & 0xFFFF, eq_before = pre >> 16;
+  bool wins[SAMPLE_KEYS];
   if (lo.idx) {
     // keys equal to thr hold one value, so their outputs are all zero or all
     // non-zero: the thread holding the first tie tells the others through LDS
@@ -351,6 +386,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
       const bool eq = in && key[j] == thr;
       const bool win = in && (key[j] > thr || (eq && eq_before < need));
       const TO ov = kwta_out<A, TO>(rv[j], sa.shift);
+      wins[j] = win;
       if (win && ov != TO(0)) {
         const int pos = gt_before + (ntie_nz ? (eq_before < need ? eq_before : need) : 0);
         lo.idx[ob + pos] = (uint16_t)(i0 + j);
@@ -369,8 +405,43 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
       const int i = i0 + j;
       const bool eq = i < c_out && key[j] == thr;
       const bool win = i < c_out && (key[j] > thr || (eq && eq_before < need));
+      wins[j] = win;
       if (i < c_out) out[item * c_out + i] = win ? kwta_out<A, TO>(rv[j], sa.shift) : TO(0);
       eq_before += eq ? 1 : 0;
+    }
+  }
+  // ---- the next layer on the winners: a winner (channel i, output v) adds
+  // v * value to the next layer's output g*n + kid for every set g of its
+  // packed row i (integer sums: exact in any order)
+  if constexpr (std::is_same<T, int8_t>::value) {
+    if (nx.aug != nullptr) {
+#pragma unroll
+      for (int j = 0; j < SAMPLE_KEYS; ++j) {
+        const int32_t ov = (int32_t)kwta_out<A, TO>(rv[j], sa.shift);
+        if (wins[j] && ov != 0) {
+          if (nx.G <= NX_MAXG) {
+#pragma unroll
+            for (int g = 0; g < NX_MAXG; ++g) {
+              const uint32_t w = pw[j][g];
+              if (g < nx.G)
+                __hip_atomic_fetch_add(acc2 + g * nx.n + (int)(w >> 8),
+                                       ov * (int)(int8_t)(w & 0xFFu), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+          } else {
+            const uint16_t* r = nx.aug + (int64_t)(i0 + j) * nx.G;
+            for (int g = 0; g < nx.G; ++g) {
+              const uint32_t w = r[g];
+              __hip_atomic_fetch_add(acc2 + g * nx.n + (int)(w >> 8),
+                                     ov * (int)(int8_t)(w & 0xFFu), __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+          }
+        }
+      }
+      __syncthreads();
+      for (int o = tid; o < nx.c_out; o += SAMPLE_BD)
+        nx.y[item * nx.c_out + o] = acc2[o] + (nx.bias != nullptr ? nx.bias[o] : 0);
     }
   }
 }

@@ -21,7 +21,10 @@ their indices"):
     sum and k-WTA kernels;
   * a dense first layer runs as the sparse-dense variant (dense input, dense
     weights), with k-WTA in the same call (cs_conv2d_dense_kwta);
-  * a layer without k-WTA writes its sums (cs_mrs_conv2d / cs_conv2d_dense).
+  * a layer without k-WTA writes its sums (cs_mrs_conv2d / cs_conv2d_dense);
+  * the last layer, a linear layer without k-WTA on the int8 winners of a
+    layer with one output vector per sample, runs in that layer's call
+    (cs_mrs_kwta_chain2: the winners feed it on chip) unless fuse_tail is off.
 A linear layer that follows a conv layer reads the conv output's per-pixel
 lists as a convolution whose window is the whole h x w map: its slots
 (h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
@@ -59,6 +62,7 @@ class Plan:
     out_shape: tuple         # sums after pool
     emit_lists: bool         # k-WTA writes lists for the next layer
     cap_out: int             # capacity of the emitted lists
+    fuse_next: bool = False  # the next (last) layer runs in this layer's call
 
 
 @dataclass
@@ -79,9 +83,10 @@ class Buffers:
 
 class Network:
     def __init__(self, layers, weights, biases, in_shape, batch: int, device="cuda",
-                 keep_sums: bool = True):
+                 keep_sums: bool = True, fuse_tail: bool = True):
         self.layers = list(layers)
         self.keep_sums = keep_sums
+        self.fuse_tail = fuse_tail
         self.device = torch.device(device)
         self.batch = batch
         self.in_shape = tuple(in_shape)
@@ -141,6 +146,16 @@ class Network:
             prev_k = s.k
             shape = oshape
         self.out_shape = shape
+        # the tail: a last linear layer without k-WTA on the int8 winners of a
+        # layer whose output is one vector per sample
+        if self.fuse_tail and nl >= 2:
+            a, z = self.plans[nl - 2], self.plans[nl - 1]
+            sa, sz = self.packed[nl - 2].spec, self.packed[nl - 1].spec
+            int8 = self.packed[nl - 2].aug.dtype == torch.int16 and self.packed[nl - 1].aug.dtype == torch.int16
+            if (int8 and sa.k is not None and sa.shift is not None and a.emit_lists and
+                    not a.dense_kernel and len(a.out_shape) == 2 and sz.kind == "linear" and
+                    sz.k is None and z.in_lists):
+                a.fuse_next = True
 
     def make_buffers(self) -> Buffers:
         B = Buffers()
@@ -207,13 +222,23 @@ class Network:
                 calls.append((f"{s.name}.mrs", lambda: ops.conv2d_dense(
                     x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, out=acc)))
             return calls
+        if li > 0 and self.plans[li - 1].fuse_next:
+            return []                                   # run by the previous layer's call
         if pl.in_lists:
             idx, lval, cnt = B.lists[li - 1]
         else:
             idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
             calls.append((f"{s.name}.compact", lambda: ops.compact_into(
                 x.reshape(b * h * w, c), idx, lval, cnt)))
-        if s.k is not None:
+        if pl.fuse_next:
+            # one call: this layer with its k-WTA, then the last layer on its winners
+            q = self.packed[li + 1]
+            acc2 = B.acc[li + 1]
+            calls.append((f"{s.name}.mrs_kwta+{q.spec.name}.mrs", lambda: ops.mrs_kwta_chain2(
+                idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                pl.pool, k=s.k, shift=shift, aug2=q.aug, n2=q.spec.n, bias2=q.bias, y=acc4,
+                keep_sums=self.keep_sums, lists=lists_out, y2=acc2)))
+        elif s.k is not None:
             # one call: sums, pool, k-WTA, requantisation, lists or dense output
             calls.append((f"{s.name}.mrs_kwta", lambda: ops.mrs_kwta_conv2d(
                 idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,

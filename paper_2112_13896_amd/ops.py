@@ -194,6 +194,48 @@ def mrs_kwta_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in
     return y, result
 
 
+def mrs_kwta_chain2(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, aug,
+                    kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None,
+                    pool: int = 1, *, k: int, shift: int, aug2, n2: int, bias2=None,
+                    y: torch.Tensor | None = None, keep_sums: bool = True, cap: int | None = None,
+                    lists=None, y2: torch.Tensor | None = None):
+    """An int8 layer with k-WTA (one output vector per sample) and the linear
+    layer on its requantised winners (cs_mrs_kwta_chain2).  Returns
+    (y, lists, y2): the first layer's sums (when keep_sums), its winners'
+    lists and the second layer's int32 sums [b][c_out2]."""
+    if lval.dtype != torch.int8:
+        raise TypeError("mrs_kwta_chain2 takes int8 lists")
+    b, h, w, c_in = in_shape
+    pa, c_out = _aug(aug, lval.dtype, n)
+    pa2, c_out2 = _aug(aug2, torch.int8, n2)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    oshape = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    if y is None:
+        y = torch.empty(oshape, dtype=torch.int32, device=lval.device)
+    if lists is None:
+        cap = list_capacity(k) if cap is None else cap
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=lval.device),
+                 torch.empty((rows, cap), dtype=torch.int8, device=lval.device),
+                 torch.empty((rows,), dtype=torch.int32, device=lval.device))
+    oi, ov, oc = lists
+    if oi.dtype != torch.int16 or ov.dtype != torch.int8 or oc.dtype != torch.int32:
+        raise TypeError("list buffer dtypes do not match")
+    if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+        raise ValueError("list buffer shapes do not match the output")
+    if y2 is None:
+        y2 = torch.empty((b, c_out2), dtype=torch.int32, device=lval.device)
+    if y2.dtype != torch.int32 or y2.numel() != b * c_out2:
+        raise ValueError("y2 does not match the second layer's output")
+    check("cs_mrs_kwta_chain2", lib().cs_mrs_kwta_chain2(
+        CS_I8, _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
+        b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n, _opt(bias, "bias"), pool,
+        _dev(y, "y"), 1 if keep_sums else 0, k, CS_I8, shift, _dev(oi, "oidx"), _dev(ov, "oval"),
+        _dev(oc, "ocnt"), oi.shape[1], pa2, c_out2, n2, _opt(bias2, "bias2"), _dev(y2, "y2"),
+        _stream()))
+    return y, lists, y2
+
+
 def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: int, pad: int,
              c_out: int, n: int, pool: int = 1, k: int = -1) -> dict:
     """The launch plan the library picks for a layer (host only)."""

@@ -267,6 +267,28 @@ def test_reorder_validation(L):
     assert call(y=FAKE + 4) == CS_ERR_ARG           # y not 16-byte aligned
 
 
+def test_chain2_validation(L):
+    f = L.cs_mrs_kwta_chain2
+    ok = dict(xt=CS_I8, idx=FAKE, lval=FAKE, cnt=FAKE, cap=8, b=4, h=5, w=5, c_in=64, kh=5, kw=5,
+              stride=1, pad=0, aug=FAKE, c_out=1500, n=20, bias=None, pool=1, y=FAKE, keep_sums=0,
+              k=75, ot=CS_I8, shift=8, oidx=FAKE, oval=FAKE, ocnt=FAKE, ocap=76, aug2=FAKE,
+              c_out2=12, n2=1, bias2=None, y2=FAKE, stream=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(*a.values())
+    assert call(xt=CS_F32) == CS_ERR_DTYPE
+    assert call(ot=CS_I32) == CS_ERR_DTYPE
+    assert call(aug2=None) == CS_ERR_ARG
+    assert call(y2=None) == CS_ERR_ARG
+    assert call(oidx=None) == CS_ERR_ARG            # list output only
+    assert call(n2=5) == CS_ERR_SHAPE               # 5 does not divide 12
+    assert call(kh=3, kw=3) == CS_ERR_SHAPE         # a 3 x 3 output map: not one vector per sample
+    assert call(k=80) == CS_ERR_SHAPE               # more winners than the list holds
+    assert call(shift=40) == CS_ERR_ARG
+
+
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, 8, 4, None, 1, FAKE, None]

@@ -65,6 +65,32 @@ def test_int_config_bit_exact(cid):
                 assert np.array_equal(val[r, :cnt[r]].astype(np.int64), dense[r, nz])
 
 
+def test_tail_fusion_matches_two_launches():
+    """Config 2's last two layers (linear1 with k-WTA, then the output layer on
+    its winners) in one call (cs_mrs_kwta_chain2) and as two calls: the same
+    bits in every buffer, one launch fewer."""
+    cfg = CONFIGS[2]
+    inp = generate(cfg)
+    fused = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
+    plain = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, fuse_tail=False)
+    assert fused.plans[-2].fuse_next and not plain.plans[-2].fuse_next
+    names_f, names_p = fused.kernel_names(), plain.kernel_names()
+    assert len(names_f) == len(names_p) - 1 and "linear1.mrs_kwta+output.mrs" in names_f
+    x = dev(inp["x"])
+    fused.forward(x)
+    plain.forward(x)
+    torch.cuda.synchronize()
+    for li in range(len(cfg.layers)):
+        assert np.array_equal(host(fused.acc[li]), host(plain.acc[li])), f"layer {li} sums"
+        assert np.array_equal(host(fused.dense_output(li)), host(plain.dense_output(li))), \
+            f"layer {li} output"
+    # with the sums of linear1 not kept, the output layer's sums are unchanged
+    bench = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, keep_sums=False)
+    bench.forward(x)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(bench.acc[-1]), host(plain.acc[-1]))
+
+
 @pytest.mark.parametrize("cid", [3, 4])
 def test_fp32_config_layerwise(cid):
     cfg = CONFIGS[cid]
