@@ -325,6 +325,43 @@ int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c_out, int n
                      int32_t* table);
 
 /*
+ * cs_pack_channels - Combine along the channel dimension (Section 3.1: sets
+ * of kernels can be overlaid in the filter or in the channel dimension).  In
+ * every filter, each group of n consecutive input channels holds n kh x kw
+ * slices with disjoint supports; they are overlaid into one dense kh x kw
+ * slice whose slots keep the weight and the channel ID (which slice, 0..n-1).
+ * Offline, HOST memory only, no HIP call.
+ *
+ *  wt      CS_F32.  w host [c_out][kh][kw][c_in] dense filters (0 = absent).
+ *  n       channels per group, 1 <= n <= CS_MAX_N, dividing c_in.
+ *  packed  host [c_out][c_in/n][kh][kw] cs_aug_f32 out (kid = channel ID):
+ *          value = w[o][y][x][q*n + cid] for the one channel of group q that
+ *          is non-zero at (y, x); holes hold 0, 0.
+ *  holes   out (may be NULL): packed slots no channel uses.
+ *  bad_o, bad_i  out (may be NULL): on CS_ERR_COLLISION the first colliding
+ *          filter and packed slot (q*kh + y)*kw + x, in that order; else -1.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE (n does not divide c_in,
+ *  n > CS_MAX_N), CS_ERR_COLLISION (packed then unspecified).
+ */
+int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, int kw, int c_in, int n,
+                     void* packed, int64_t* holes, int* bad_o, int* bad_i);
+
+/*
+ * cs_reorder_table_channels - cs_reorder_table for a channel-overlaid layer
+ * (cs_pack_channels): every filter's packed slots (q, y, x) with a non-zero
+ * value read channel q*n + cid at tap (y, x), so the filter's table lists
+ * them with that slot's byte offset in cs_conv2d_reorder_kwta's input tile;
+ * the layer then runs as any reordered layer.  Offline, HOST memory only.
+ *  packed  host [c_out][c_in/n][kh][kw] cs_aug_f32 (cs_pack_channels).
+ *  smax, table   as cs_reorder_table.
+ *  Errors: CS_ERR_ARG (null packed/smax, sizes < 1, a channel ID >= n),
+ *  CS_ERR_SHAPE (n does not divide c_in, n > CS_MAX_N, kh*kw*c_in >
+ *  CS_MAX_ROW, smax too small).
+ */
+int cs_reorder_table_channels(const void* packed, int kh, int kw, int c_in, int c_out, int n,
+                              int* smax, int32_t* table);
+
+/*
  * cs_conv2d_reorder_kwta - a dense-input fp32 conv layer computed by
  * reordering instead of routing: every output reads the activations at its
  * kernel's support (cs_reorder_table) and sums their products in a register;

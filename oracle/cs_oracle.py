@@ -119,6 +119,57 @@ def unpack(val: np.ndarray, kid: np.ndarray, n: int) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
+# Combine along the channel dimension (Section 3.1: sets of kernels can be
+# overlaid in the filter or in the channel dimension).  For one filter
+# W[o] (kh x kw x C), the n channel slices of a group q (channels q*n ..
+# q*n+n-1) have disjoint kh x kw supports and are overlaid into one dense
+# kh x kw slice whose every slot keeps its weight and the channel ID (the
+# slice it came from) - the channel-dimension counterpart of the Kernel ID.
+# ---------------------------------------------------------------------------
+def pack_channels(W4: np.ndarray, n: int):
+    """W4 : [c_out][kh][kw][C] dense weights (zero = absent).
+    Returns (val[c_out][C/n][kh][kw], cid[..] uint8, holes): val[o][q][y][x] =
+    W4[o][y][x][q*n + cid] for the unique channel of group q non-zero at
+    (y, x) in filter o; holes hold 0, 0.  Raises PackCollision(o, slot) with
+    slot = (q*kh + y)*kw + x at the first collision in (o, q, y, x) order."""
+    W4 = np.asarray(W4)
+    c_out, kh, kw, C = W4.shape
+    if n <= 0 or C % n != 0:
+        raise ValueError("n must divide the channels")
+    Q = C // n
+    val = np.zeros((c_out, Q, kh, kw), dtype=W4.dtype)
+    cid = np.zeros((c_out, Q, kh, kw), dtype=np.uint8)
+    holes = 0
+    for o in range(c_out):
+        for q in range(Q):
+            block = W4[o, :, :, q * n:(q + 1) * n]       # [kh][kw][n]
+            nz = block != 0
+            count = nz.sum(axis=2)
+            bad = np.argwhere(count > 1)
+            if bad.size:
+                y, x = bad[0]
+                raise PackCollision(o, int((q * kh + y) * kw + x))
+            holes += int((count == 0).sum())
+            owner = nz.argmax(axis=2)
+            cid[o, q] = owner.astype(np.uint8)
+            val[o, q] = np.take_along_axis(block, owner[..., None], axis=2)[..., 0]
+    return val, cid, holes
+
+
+def unpack_channels(val: np.ndarray, cid: np.ndarray, n: int) -> np.ndarray:
+    """Inverse of pack_channels: the dense [c_out][kh][kw][C] weights."""
+    c_out, Q, kh, kw = val.shape
+    W4 = np.zeros((c_out, kh, kw, Q * n), dtype=val.dtype)
+    for o in range(c_out):
+        for q in range(Q):
+            for y in range(kh):
+                for x in range(kw):
+                    if val[o, q, y, x] != 0:
+                        W4[o, y, x, q * n + int(cid[o, q, y, x])] = val[o, q, y, x]
+    return W4
+
+
+# ---------------------------------------------------------------------------
 # Select's sparse representation (Section 3.2 step 2; Figure 10 sends the
 # winners on "along with their indices").
 # ---------------------------------------------------------------------------

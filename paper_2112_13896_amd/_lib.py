@@ -42,6 +42,9 @@ SIGNATURES = {
     "cs_conv2d_dense_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                                   _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_reorder_table": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),
+    "cs_pack_channels": (_i, [_i, _vp, _i, _i, _i, _i, _i, _vp, _c.POINTER(_i64), _c.POINTER(_i),
+                              _c.POINTER(_i)]),
+    "cs_reorder_table_channels": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),
     "cs_conv2d_reorder_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _vp,
                                     _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),

@@ -120,6 +120,89 @@ extern "C" int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c
   return CS_OK;
 }
 
+extern "C" int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, int kw, int c_in,
+                                int n, void* packed, int64_t* holes, int* bad_o, int* bad_i) {
+  if (bad_o) *bad_o = -1;
+  if (bad_i) *bad_i = -1;
+  if (holes) *holes = 0;
+  if (!w || !packed || c_out < 1 || kh < 1 || kw < 1 || c_in < 1 || n < 1) return CS_ERR_ARG;
+  if (wt != CS_F32) return CS_ERR_DTYPE;
+  if (n > CS_MAX_N || c_in % n != 0) return CS_ERR_SHAPE;
+  const float* W = static_cast<const float*>(w);
+  cs_aug_f32* P = static_cast<cs_aug_f32*>(packed);
+  const int Q = c_in / n;
+  int64_t nh = 0;
+  for (int o = 0; o < c_out; ++o)
+    for (int q = 0; q < Q; ++q)
+      for (int y = 0; y < kh; ++y)
+        for (int x = 0; x < kw; ++x) {
+          const float* wp = W + (((int64_t)o * kh + y) * kw + x) * c_in + q * n;
+          int owner = -1;
+          for (int j = 0; j < n; ++j) {
+            if (wp[j] != 0.f) {
+              if (owner >= 0) {
+                if (bad_o) *bad_o = o;
+                if (bad_i) *bad_i = (q * kh + y) * kw + x;
+                return CS_ERR_COLLISION;
+              }
+              owner = j;
+            }
+          }
+          cs_aug_f32& e = P[(((int64_t)o * Q + q) * kh + y) * kw + x];
+          e.value = owner >= 0 ? wp[owner] : 0.f;
+          e.kid = owner >= 0 ? (uint32_t)owner : 0u;
+          nh += owner < 0 ? 1 : 0;
+        }
+  if (holes) *holes = nh;
+  return CS_OK;
+}
+
+extern "C" int cs_reorder_table_channels(const void* packed, int kh, int kw, int c_in, int c_out,
+                                         int n, int* smax, int32_t* table) {
+  if (!packed || !smax || kh < 1 || kw < 1 || c_in < 1 || c_out < 1 || n < 1) return CS_ERR_ARG;
+  if (n > CS_MAX_N || c_in % n != 0) return CS_ERR_SHAPE;
+  if ((int64_t)kh * kw * c_in > CS_MAX_ROW) return CS_ERR_SHAPE;
+  const cs_aug_f32* P = static_cast<const cs_aug_f32*>(packed);
+  const int Q = c_in / n, S = Q * kh * kw;                        // packed slots per filter
+  int longest = 0;
+  for (int o = 0; o < c_out; ++o) {
+    int cnt = 0;
+    for (int i = 0; i < S; ++i) {
+      const cs_aug_f32& e = P[(int64_t)o * S + i];
+      if (e.kid >= (uint32_t)n) return CS_ERR_ARG;
+      cnt += e.value != 0.f ? 1 : 0;
+    }
+    longest = cnt > longest ? cnt : longest;
+  }
+  const int sm = longest > 0 ? longest : 1;
+  if (!table) {
+    *smax = sm;
+    return CS_OK;
+  }
+  if (*smax < sm) return CS_ERR_SHAPE;
+  const int hw = CS_REORDER_TILE + kw - 1, cp = c_in + 1;
+  for (int o = 0; o < c_out; ++o) {
+    int32_t* t = table + (int64_t)o * *smax * 2;
+    int j = 0;
+    // packed slot (q, y, x) with channel ID cid reads channel q*n + cid at tap (y, x)
+    for (int q = 0; q < Q; ++q)
+      for (int y = 0; y < kh; ++y)
+        for (int x = 0; x < kw; ++x) {
+          const cs_aug_f32& e = P[(((int64_t)o * Q + q) * kh + y) * kw + x];
+          if (e.value == 0.f) continue;
+          const int c = q * n + (int)e.kid;
+          t[2 * j] = 4 * ((y * hw + x) * cp + c);
+          std::memcpy(&t[2 * j + 1], &e.value, 4);
+          ++j;
+        }
+    for (; j < *smax; ++j) {
+      t[2 * j] = 0;
+      t[2 * j + 1] = 0;
+    }
+  }
+  return CS_OK;
+}
+
 extern "C" const char* cs_status_str(int status) {
   switch (status) {
     case CS_OK: return "ok";

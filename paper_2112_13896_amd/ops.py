@@ -374,6 +374,43 @@ def reorder_table(aug: np.ndarray, kh: int, kw: int, c_in: int, c_out: int, n: i
     return table
 
 
+def pack_channels(W4: np.ndarray, n: int):
+    """Combine along the channel dimension on the host (cs_pack_channels):
+    W4 fp32 [c_out][kh][kw][c_in] -> (packed uint32 [c_out][c_in/n][kh][kw][2]
+    holding (value bits, channel ID), holes).  Raises CSError
+    (CS_ERR_COLLISION) with .bad = (o, slot) on a collision."""
+    W4 = np.ascontiguousarray(W4, dtype=np.float32)
+    if W4.ndim != 4:
+        raise ValueError("W4 must be [c_out][kh][kw][c_in]")
+    c_out, kh, kw, c_in = W4.shape
+    q = c_in // n if n > 0 else 0
+    packed = np.zeros((c_out, max(q, 1), kh, kw, 2), dtype=np.uint32)
+    holes = ctypes.c_int64(0)
+    bo, bi = ctypes.c_int(0), ctypes.c_int(0)
+    st = lib().cs_pack_channels(CS_F32, W4.ctypes.data, c_out, kh, kw, c_in, n, packed.ctypes.data,
+                                ctypes.byref(holes), ctypes.byref(bo), ctypes.byref(bi))
+    if st != _lib.CS_OK:
+        err = _lib.CSError("cs_pack_channels", st)
+        err.bad = (bo.value, bi.value)
+        raise err
+    return packed, int(holes.value)
+
+
+def reorder_table_channels(packed: np.ndarray, kh: int, kw: int, c_in: int, c_out: int,
+                           n: int) -> np.ndarray:
+    """cs_reorder_table_channels: a channel-overlaid layer's table for
+    conv2d_reorder_kwta, int32 [c_out][smax][2] (smax a multiple of 8)."""
+    packed = np.ascontiguousarray(packed)
+    smax = ctypes.c_int(0)
+    check("cs_reorder_table_channels", lib().cs_reorder_table_channels(
+        packed.ctypes.data, kh, kw, c_in, c_out, n, ctypes.byref(smax), None))
+    smax.value = (smax.value + 7) // 8 * 8
+    table = np.zeros((c_out, smax.value, 2), dtype=np.int32)
+    check("cs_reorder_table_channels", lib().cs_reorder_table_channels(
+        packed.ctypes.data, kh, kw, c_in, c_out, n, ctypes.byref(smax), table.ctypes.data))
+    return table
+
+
 def conv2d_reorder_kwta(x: torch.Tensor, table: torch.Tensor, kh: int, kw: int, pad: int = 0,
                         bias: torch.Tensor | None = None, *, k: int,
                         y: torch.Tensor | None = None, keep_sums: bool = True,

@@ -239,12 +239,56 @@ def test_reorder_table_sums_match_oracle():
                                    o.conv2d_nhwc(x, W, 1, pad, bias), rtol=1e-12, atol=1e-12)
 
 
+def test_pack_channels_matches_oracle():
+    from workloads import channel_complementary_weights
+    r = np.random.default_rng(13)
+    for c_out, kh, kw, c, n in [(8, 3, 3, 12, 3), (4, 5, 5, 10, 5), (3, 1, 2, 6, 2)]:
+        W4 = channel_complementary_weights(r, r, c_out, kh, kw, c, n)
+        W4[0, 0, 0, :] = 0                                # a few holes
+        packed, holes = ops.pack_channels(W4, n)
+        val, cid, oh = o.pack_channels(W4, n)
+        assert holes == oh
+        assert np.array_equal(packed[..., 0].view(np.float32), val)
+        assert np.array_equal(packed[..., 1], cid.astype(np.uint32))
+    W4 = channel_complementary_weights(r, r, 2, 3, 3, 6, 3)
+    W4[1, 2, 0, 4] = 1.0                                  # a second channel of group 1 at tap (2, 0)
+    if W4[1, 2, 0, 3] == 0 and W4[1, 2, 0, 5] == 0:
+        W4[1, 2, 0, 5] = 2.0
+    with pytest.raises(_lib.CSError) as e:
+        ops.pack_channels(W4, 3)
+    assert e.value.status == CS_ERR_COLLISION and e.value.bad == (1, (1 * 3 + 2) * 3 + 0)
+
+
+def test_reorder_table_channels_sums_match_oracle():
+    """A channel-overlaid layer's table, evaluated the way the reordering
+    kernel reads it, gives the oracle's convolution of the dense filters."""
+    from workloads import channel_complementary_weights
+    r = np.random.default_rng(14)
+    for shape, kh, pad, n in [((1, 9, 11, 12), 3, 1, 3), ((1, 8, 7, 10), 5, 2, 5)]:
+        b, h, w, c = shape
+        x = np.where(r.random(shape) < 0.3, np.abs(r.normal(size=shape)), 0).astype(np.float32)
+        W4 = channel_complementary_weights(r, r, 64, kh, kh, c, n)
+        packed, _ = ops.pack_channels(W4, n)
+        t = ops.reorder_table_channels(packed, kh, kh, c, 64, n)
+        assert t.shape[1] == (kh * kh * c // n + 7) // 8 * 8
+        np.testing.assert_allclose(_reorder_eval(x, t, kh, kh, pad, None),
+                                   o.conv2d_nhwc(x, W4, 1, pad, None), rtol=1e-12, atol=1e-12)
+
+
 def test_reorder_validation(L):
     f = L.cs_reorder_table
     sm = ctypes.c_int(0)
     assert f(None, 3, 3, 64, 64, 8, ctypes.byref(sm), None) == CS_ERR_ARG
     assert f(FAKE, 3, 3, 64, 64, 7, ctypes.byref(sm), None) == CS_ERR_SHAPE   # 7 does not divide 64
     assert f(FAKE, 3, 3, 64, 64, 40, ctypes.byref(sm), None) == CS_ERR_SHAPE  # n > CS_MAX_N
+    pc = L.cs_pack_channels
+    hz = ctypes.c_int64(0)
+    assert pc(CS_I8, FAKE, 4, 3, 3, 6, 3, FAKE, ctypes.byref(hz), None, None) == CS_ERR_DTYPE
+    assert pc(CS_F32, None, 4, 3, 3, 6, 3, FAKE, None, None, None) == CS_ERR_ARG
+    assert pc(CS_F32, FAKE, 4, 3, 3, 6, 4, FAKE, None, None, None) == CS_ERR_SHAPE   # 4 does not divide 6
+    tc = L.cs_reorder_table_channels
+    assert tc(None, 3, 3, 6, 4, 3, ctypes.byref(sm), None) == CS_ERR_ARG
+    assert tc(FAKE, 3, 3, 6, 4, 4, ctypes.byref(sm), None) == CS_ERR_SHAPE
     g = L.cs_conv2d_reorder_kwta
     ok = dict(xt=CS_F32, x=FAKE, b=1, h=8, w=8, c_in=64, kh=3, kw=3, pad=1, table=FAKE, smax=72,
               c_out=64, bias=None, y=FAKE, keep_sums=0, k=8, ot=CS_F32, out=None, oidx=FAKE,

@@ -105,3 +105,29 @@ def test_reorder_rejects():
         ops.conv2d_reorder_kwta(x, t, 3, 3, 1, None, k=40, cap=40)     # 32 < k < c_out
     with pytest.raises(ops._lib.CSError):
         ops.conv2d_reorder_kwta(x, t, 3, 3, 1, None, k=8, cap=6)      # cap not a multiple of 4
+
+
+@pytest.mark.parametrize("shape,kh,pad,n,k", [((2, 20, 20, 48), 3, 1, 3, 8),
+                                              ((1, 12, 13, 40), 5, 2, 5, 16)])
+def test_channel_overlay_layer(shape, kh, pad, n, k):
+    """Complementary Sparsity in the channel dimension (cs_pack_channels): the
+    layer runs by reordering (cs_reorder_table_channels + the reordering
+    kernel) and matches the oracle's convolution of the dense filters."""
+    from workloads import channel_complementary_weights
+    r = np.random.default_rng(zlib.crc32(repr((shape, kh, n)).encode()))
+    c_in = shape[3]
+    x = sparse_input(r, shape, c_in // 6, "f32")
+    W4 = channel_complementary_weights(r, r, 64, kh, kh, c_in, n)
+    bias = r.normal(size=64).astype(np.float32)
+    packed, holes = ops.pack_channels(W4, n)
+    assert holes == 0
+    table = dev(ops.reorder_table_channels(packed, kh, kh, c_in, 64, n))
+    y, lists = ops.conv2d_reorder_kwta(dev(x), table, kh, kh, pad, dev(bias), k=k,
+                                       cap=ops.list_capacity(k))
+    y = host(y)
+    out = dense_from_lists(*(host(t) for t in lists), 64)
+    ref = o.conv2d_nhwc(x, W4, 1, pad, bias)
+    S = o.abs_sum_conv(x, W4, 1, pad) + np.abs(bias.astype(np.float64))
+    assert_f32_close(y, ref, S, "channel-overlay sums")
+    near = check_kwta_f32(y, out, ref, S, k)
+    assert near <= max(1, out.shape[0] // 100)

@@ -264,6 +264,41 @@ def test_pack_collision_and_holes():
     assert (e.value.g, e.value.i) == (0, 1)
 
 
+def test_pack_channels_hand_example():
+    """One 1 x 2 filter over 2 channels, n = 2: channel 0 holds the left tap,
+    channel 1 the right one; the overlay is one dense 1 x 2 slice."""
+    W4 = np.zeros((1, 1, 2, 2), dtype=np.float32)
+    W4[0, 0, 0, 0] = 1.5
+    W4[0, 0, 1, 1] = -2.0
+    val, cid, holes = o.pack_channels(W4, 2)
+    assert val.shape == (1, 1, 1, 2) and holes == 0
+    assert val[0, 0, 0].tolist() == [1.5, -2.0] and cid[0, 0, 0].tolist() == [0, 1]
+
+
+def test_pack_channels_roundtrip_collision_holes():
+    from workloads import channel_complementary_weights
+    r = rng(19)
+    for c_out, kh, kw, c, n in [(4, 3, 3, 6, 3), (3, 5, 5, 10, 5), (2, 1, 1, 4, 1)]:
+        W4 = channel_complementary_weights(r, r, c_out, kh, kw, c, n)
+        nz = (W4 != 0).reshape(c_out, kh * kw, c // n, n)
+        assert (nz.sum(axis=3) == 1).all()            # each tap: exactly one channel per group
+        val, cid, holes = o.pack_channels(W4, n)
+        assert holes == 0 and (val != 0).all() and cid.max() < n
+        assert np.array_equal(o.unpack_channels(val, cid, n), W4)
+    # holes: brute-force count of the (filter, group, tap) with no channel
+    W4 = np.zeros((2, 2, 2, 4), dtype=np.float32)
+    W4[0, 0, 0, 1] = 1.0
+    W4[1, 1, 1, 2] = 2.0
+    W4[1, 0, 1, 3] = 3.0
+    val, cid, holes = o.pack_channels(W4, 2)
+    assert holes == 2 * 2 * 4 - 3
+    assert np.array_equal(o.unpack_channels(val, cid, 2), W4)
+    W4[1, 1, 1, 3] = 4.0                      # channels 2 and 3 of filter 1 at tap (1, 1)
+    with pytest.raises(o.PackCollision) as e:
+        o.pack_channels(W4, 2)
+    assert (e.value.g, e.value.i) == (1, (1 * 2 + 1) * 2 + 1)
+
+
 def test_pack_factors_from_paper():
     """Section 3 / Figure 7: 80% sparse kernels pack 5 to one dense kernel and
     20 channels give 4 sets; 66% sparse 3x3 kernels pack 3 to one."""

@@ -66,6 +66,30 @@ def complementary_weights(rng_part: np.random.Generator, rng_val: np.random.Gene
     return W
 
 
+def channel_complementary_weights(rng_part: np.random.Generator, rng_val: np.random.Generator,
+                                  c_out: int, kh: int, kw: int, c: int, n: int) -> np.ndarray:
+    """Dense fp32 [c_out][kh][kw][c] filters whose channel slices form
+    complementary sets: for every filter and every group of n consecutive
+    channels, a random permutation of the kh*kw positions is cut into n
+    pieces, one per channel of the group.  Values N(0, 2/nnz) per filter,
+    drawn in float64 and rounded once to float32."""
+    t = kh * kw
+    if c % n or t % n:
+        raise ValueError("n must divide the channels and kh*kw")
+    per = t // n
+    mask = np.zeros((c_out, t, c), dtype=bool)
+    for o in range(c_out):
+        for q in range(c // n):
+            perm = rng_part.permutation(t)
+            for j in range(n):
+                mask[o, perm[j * per:(j + 1) * per], q * n + j] = True
+    nnz = t * c // n
+    vals = rng_val.normal(0.0, np.sqrt(2.0 / nnz), size=mask.shape).astype(np.float32)
+    if np.any(vals[mask] == 0):
+        raise RuntimeError("a support weight rounded to zero")
+    return np.where(mask, vals, np.float32(0)).astype(np.float32).reshape(c_out, kh, kw, c)
+
+
 def sparse_rows(rng: np.random.Generator, rows: int, c: int, nnz: int | None, dist: str):
     """[rows][c] activations with exactly `nnz` non-zeros per row at uniform
     positions (without replacement); nnz=None gives a dense draw.
