@@ -325,6 +325,29 @@ int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c_out, int n
                      int32_t* table);
 
 /*
+ * cs_pack_blocks - Combine for Complementary Sparsity with blocks of
+ * non-zeros (Section 3.1: complementary patterns made of blocks; Section 5's
+ * stem treats a pixel's 3 RGB inputs as one block).  Slots j*b .. j*b+b-1 form
+ * block j (for conv weights in (tap, channel) slot order and b dividing c_in,
+ * a block is b consecutive channels of one tap); every kernel's support must
+ * be a union of whole blocks, complementary within each set block by block.
+ * Offline, HOST memory only, no HIP call.
+ *
+ *  wt, w, d_out, r, n, aug   as cs_pack (aug is the per-slot augmented
+ *          tensor every layer call reads); b divides r.
+ *  kidb    host [r/b][G] uint8 out: the Kernel ID of each (block, set) - one
+ *          routing decision for the block's b products (0 for a hole).
+ *  holes   out (may be NULL): (block, set) pairs no kernel uses.
+ *  bad_g, bad_i  out (may be NULL): on CS_ERR_SHAPE for a split block, the
+ *          kernel and the block; on CS_ERR_COLLISION, the set and the block.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE, CS_ERR_SHAPE (n does not divide d_out,
+ *  n > CS_MAX_N, b does not divide r, a support splits a block),
+ *  CS_ERR_COLLISION.
+ */
+int cs_pack_blocks(cs_dtype wt, const void* w, int d_out, int r, int n, int b, void* aug,
+                   uint8_t* kidb, int64_t* holes, int* bad_g, int* bad_i);
+
+/*
  * cs_pack_channels - Combine along the channel dimension (Section 3.1: sets
  * of kernels can be overlaid in the filter or in the channel dimension).  In
  * every filter, each group of n consecutive input channels holds n kh x kw

@@ -170,6 +170,58 @@ def unpack_channels(val: np.ndarray, cid: np.ndarray, n: int) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
+# Complementary Sparsity with blocks of non-zeros (Section 3.1: complementary
+# patterns whose non-zero elements come in blocks; the stem of Section 5 treats
+# a pixel's 3 RGB values as one block, all non-zero or all zero).  Slots
+# i*b .. i*b+b-1 form block i; every kernel's support is a union of whole
+# blocks, and the kernels of a set are complementary block by block, so one
+# Kernel ID per block routes all b of its products.
+# ---------------------------------------------------------------------------
+class BlockViolation(ValueError):
+    """A kernel's support covers part of a block."""
+
+    def __init__(self, o: int, blk: int):
+        super().__init__(f"kernel {o} covers part of block {blk}")
+        self.o = o
+        self.blk = blk
+
+
+def pack_blocks(W: np.ndarray, n: int, b: int):
+    """W : [d_out][r] dense weights, r a multiple of b.  Returns
+    (val[r][G], kidb[r/b][G] uint8, holes) - val as pack() gives it, kidb the
+    Kernel ID of each block (0 for a block no kernel of the set uses), holes
+    the number of such (block, set) pairs.  Raises BlockViolation(o, block)
+    for the first kernel (in output order) whose support splits a block, or
+    PackCollision(g, block) at the first block two kernels of a set share."""
+    W = np.asarray(W)
+    d_out, r = W.shape
+    if b <= 0 or r % b != 0:
+        raise ValueError("b must divide the slots")
+    if n <= 0 or d_out % n != 0:
+        raise ValueError("n must divide d_out")
+    nb = r // b
+    nzb = (W != 0).reshape(d_out, nb, b)
+    part = nzb.any(axis=2) & ~nzb.all(axis=2)
+    for o_ in range(d_out):
+        bad = np.nonzero(part[o_])[0]
+        if bad.size:
+            raise BlockViolation(o_, int(bad[0]))
+    G = d_out // n
+    kidb = np.zeros((nb, G), dtype=np.uint8)
+    holes = 0
+    for g in range(G):
+        present = nzb[g * n:(g + 1) * n].any(axis=2)   # [n][nb]
+        count = present.sum(axis=0)
+        bad = np.nonzero(count > 1)[0]
+        if bad.size:
+            raise PackCollision(g, int(bad[0]))
+        holes += int((count == 0).sum())
+        kidb[:, g] = present.argmax(axis=0).astype(np.uint8)
+    val, _, _ = pack(W, n)
+    return val, kidb, holes
+
+
+# ---------------------------------------------------------------------------
 # Select's sparse representation (Section 3.2 step 2; Figure 10 sends the
 # winners on "along with their indices").
 # ---------------------------------------------------------------------------
@@ -290,6 +342,19 @@ def kwta(v: np.ndarray, k: int) -> np.ndarray:
     """Winners keep their value, every other element becomes zero."""
     v = np.asarray(v)
     return np.where(kwta_winners(v, k), v, np.zeros_like(v))
+
+
+def kwta_units_winners(v: np.ndarray, k: int, unit: int = 64) -> np.ndarray:
+    """k-WTA in units (Section 5: the k-WTA operator takes a convolution's
+    output in units of 64 elements, so that wide layers are built from [64:64]
+    modules): the last axis is cut into consecutive units of `unit` elements
+    and each unit keeps its own k winners (ties to the lower index)."""
+    v = np.asarray(v)
+    c = v.shape[-1]
+    if unit <= 0 or c % unit != 0:
+        raise ValueError("unit must divide the row length")
+    units = v.reshape(v.shape[:-1] + (c // unit, unit))
+    return kwta_winners(units, k).reshape(v.shape)
 
 
 def requant(a: np.ndarray, shift: int, winners: np.ndarray | None = None) -> np.ndarray:

@@ -42,6 +42,8 @@ SIGNATURES = {
     "cs_conv2d_dense_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                                   _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
     "cs_reorder_table": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),
+    "cs_pack_blocks": (_i, [_i, _vp, _i, _i, _i, _i, _vp, _vp, _c.POINTER(_i64), _c.POINTER(_i),
+                            _c.POINTER(_i)]),
     "cs_pack_channels": (_i, [_i, _vp, _i, _i, _i, _i, _i, _vp, _c.POINTER(_i64), _c.POINTER(_i),
                               _c.POINTER(_i)]),
     "cs_reorder_table_channels": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),

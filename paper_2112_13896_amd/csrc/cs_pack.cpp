@@ -120,6 +120,57 @@ extern "C" int cs_reorder_table(const void* aug, int kh, int kw, int c_in, int c
   return CS_OK;
 }
 
+extern "C" int cs_pack_blocks(cs_dtype wt, const void* w, int d_out, int r, int n, int b,
+                              void* aug, uint8_t* kidb, int64_t* holes, int* bad_g, int* bad_i) {
+  if (bad_g) *bad_g = -1;
+  if (bad_i) *bad_i = -1;
+  if (holes) *holes = 0;
+  if (!w || !aug || !kidb || d_out < 1 || r < 1 || n < 1 || b < 1) return CS_ERR_ARG;
+  if (wt != CS_I8 && wt != CS_F32) return CS_ERR_DTYPE;
+  if (n > CS_MAX_N || d_out % n != 0 || r % b != 0) return CS_ERR_SHAPE;
+  const int nb = r / b, G = d_out / n;
+  const size_t es = wt == CS_I8 ? 1 : 4;
+  auto nz = [&](int o, int i) {
+    const unsigned char* p = static_cast<const unsigned char*>(w) + ((int64_t)o * r + i) * es;
+    if (wt == CS_I8) return *reinterpret_cast<const int8_t*>(p) != 0;
+    float v;
+    std::memcpy(&v, p, 4);
+    return v != 0.f;
+  };
+  // every support a union of whole blocks
+  for (int o = 0; o < d_out; ++o)
+    for (int j = 0; j < nb; ++j) {
+      int c = 0;
+      for (int t = 0; t < b; ++t) c += nz(o, j * b + t) ? 1 : 0;
+      if (c != 0 && c != b) {
+        if (bad_g) *bad_g = o;
+        if (bad_i) *bad_i = j;
+        return CS_ERR_SHAPE;
+      }
+    }
+  // complementary block by block: one Kernel ID per (block, set)
+  int64_t nh = 0;
+  for (int g = 0; g < G; ++g)
+    for (int j = 0; j < nb; ++j) {
+      int owner = -1;
+      for (int k = 0; k < n; ++k) {
+        if (nz(g * n + k, j * b)) {
+          if (owner >= 0) {
+            if (bad_g) *bad_g = g;
+            if (bad_i) *bad_i = j;
+            return CS_ERR_COLLISION;
+          }
+          owner = k;
+        }
+      }
+      kidb[(int64_t)j * G + g] = (uint8_t)(owner >= 0 ? owner : 0);
+      nh += owner < 0 ? 1 : 0;
+    }
+  if (holes) *holes = nh;
+  // the per-slot augmented tensor every layer kernel reads
+  return cs_pack(wt, w, d_out, r, n, aug, nullptr, nullptr, nullptr);
+}
+
 extern "C" int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, int kw, int c_in,
                                 int n, void* packed, int64_t* holes, int* bad_o, int* bad_i) {
   if (bad_o) *bad_o = -1;

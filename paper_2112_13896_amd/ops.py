@@ -374,6 +374,34 @@ def reorder_table(aug: np.ndarray, kh: int, kw: int, c_in: int, c_out: int, n: i
     return table
 
 
+def pack_blocks(W: np.ndarray, n: int, b: int):
+    """Combine with blocks of b slots on the host (cs_pack_blocks): W [d_out][r]
+    int8/float32 -> (aug as pack gives it, kidb uint8 [r/b][G], holes).
+    Raises CSError with .bad = (kernel or set, block) when a support splits a
+    block (CS_ERR_SHAPE) or two kernels of a set share one (CS_ERR_COLLISION)."""
+    W = np.ascontiguousarray(W)
+    if W.ndim != 2:
+        raise ValueError("W must be [d_out][r]")
+    d_out, r = W.shape
+    wt = _NP_DT.get(W.dtype)
+    if wt is None:
+        raise TypeError(f"unsupported weight dtype {W.dtype}")
+    G = d_out // n if n > 0 else 0
+    aug = (np.zeros((r, max(G, 1)), dtype=np.uint16) if wt == CS_I8
+           else np.zeros((r, max(G, 1), 2), dtype=np.uint32))
+    kidb = np.zeros((max(r // b, 1) if b > 0 else 1, max(G, 1)), dtype=np.uint8)
+    holes = ctypes.c_int64(0)
+    bg, bi = ctypes.c_int(0), ctypes.c_int(0)
+    st = lib().cs_pack_blocks(wt, W.ctypes.data, d_out, r, n, b, aug.ctypes.data,
+                              kidb.ctypes.data, ctypes.byref(holes), ctypes.byref(bg),
+                              ctypes.byref(bi))
+    if st != _lib.CS_OK:
+        err = _lib.CSError("cs_pack_blocks", st)
+        err.bad = (bg.value, bi.value)
+        raise err
+    return aug, kidb, int(holes.value)
+
+
 def pack_channels(W4: np.ndarray, n: int):
     """Combine along the channel dimension on the host (cs_pack_channels):
     W4 fp32 [c_out][kh][kw][c_in] -> (packed uint32 [c_out][c_in/n][kh][kw][2]

@@ -239,6 +239,35 @@ def test_reorder_table_sums_match_oracle():
                                    o.conv2d_nhwc(x, W, 1, pad, bias), rtol=1e-12, atol=1e-12)
 
 
+def test_pack_blocks_matches_oracle():
+    from workloads import block_complementary_weights
+    r = np.random.default_rng(15)
+    for d_out, R, n, b, dt in [(64, 147, 4, 3, np.float32), (12, 40, 3, 4, np.int8)]:
+        W = block_complementary_weights(r, r, d_out, R, n, b)
+        if dt == np.int8:
+            W = (np.sign(W) * r.integers(1, 128, size=W.shape)).astype(np.int8)
+        W[:n, :b] = 0                                     # a hole: block 0 of set 0
+        aug, kidb, holes = ops.pack_blocks(W, n, b)
+        val, okidb, oholes = o.pack_blocks(W, n, b)
+        assert holes == oholes == 1
+        assert np.array_equal(kidb, okidb)
+        v, kid = ops.unpack_aug(aug)
+        assert np.array_equal(v, val)
+    W = block_complementary_weights(r, r, 8, 12, 2, 3)
+    W[1, 4] = 0                                           # kernel 1 splits block 1
+    if not (W[1, 3:6] != 0).any():
+        W[1, 3] = 1.0
+    with pytest.raises(_lib.CSError) as e:
+        ops.pack_blocks(W, 2, 3)
+    assert e.value.status == CS_ERR_SHAPE
+    W = block_complementary_weights(r, r, 8, 12, 2, 3)
+    owner = int(np.nonzero(W[:2, 0])[0][0])
+    W[1 - owner, 0:3] = 2.0                               # both kernels of set 0 own block 0
+    with pytest.raises(_lib.CSError) as e:
+        ops.pack_blocks(W, 2, 3)
+    assert e.value.status == CS_ERR_COLLISION and e.value.bad == (0, 0)
+
+
 def test_pack_channels_matches_oracle():
     from workloads import channel_complementary_weights
     r = np.random.default_rng(13)

@@ -303,3 +303,22 @@ def test_fp32_bitwise_reproducible():
     a = host(ops.conv2d(xd, ad, 3, 3, 16, 1, 1))
     b = host(ops.conv2d(xd, ad, 3, 3, 16, 1, 1))
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_kwta_in_units_of_64():
+    """k-WTA in units of 64 channels (wide layers as [64:64] modules): cs_kwta
+    on the [rows * c/64][64] view of a [rows][c] tensor keeps each unit's own
+    k winners, as the oracle's unit k-WTA does; lists per unit likewise."""
+    r = rng(4242)
+    v = r.integers(-3000, 3000, size=(333, 256)).astype(np.int32)
+    k = 6
+    out = host(ops.kwta(dev(v).reshape(-1, 64), k)).reshape(333, 256)
+    win = o.kwta_units_winners(v, k)
+    assert np.array_equal(out, np.where(win, v, 0))
+    idx, val, cnt = (host(t) for t in ops.kwta_lists(dev(v).reshape(-1, 64), k))
+    units = np.where(win, v, 0).reshape(-1, 64)
+    for ri in range(units.shape[0]):
+        nz = np.flatnonzero(units[ri])
+        assert cnt[ri] == len(nz)
+        assert np.array_equal(idx[ri, :cnt[ri]].view(np.uint16), nz)
+

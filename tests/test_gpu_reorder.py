@@ -131,3 +131,26 @@ def test_channel_overlay_layer(shape, kh, pad, n, k):
     assert_f32_close(y, ref, S, "channel-overlay sums")
     near = check_kwta_f32(y, out, ref, S, k)
     assert near <= max(1, out.shape[0] // 100)
+
+
+def test_block_cs_stem_layer():
+    """Block Complementary Sparsity on a 7 x 7 stem over RGB input (the 3
+    values of a pixel form one block, Section 5): cs_pack_blocks, then the
+    layer routed (dense input compacted, stride 2) and reordered (stride 1),
+    both against the oracle's convolution of the dense filters."""
+    from workloads import block_complementary_weights
+    r = np.random.default_rng(91)
+    b, h, w, c, n, kh = 2, 32, 32, 3, 4, 7
+    x = np.abs(r.normal(size=(b, h, w, c))).astype(np.float32)      # dense image
+    W = block_complementary_weights(r, r, 64, kh * kh * c, n, 3).reshape(64, kh, kh, c)
+    aug, kidb, holes = ops.pack_blocks(W.reshape(64, -1), n, 3)
+    assert holes == 0 and kidb.shape == (kh * kh, 64 // n)
+    y = host(ops.conv2d(dev(x), ops.aug_to_device(aug), kh, kh, n, 2, 3))
+    ref = o.conv2d_nhwc(x, W, 2, 3, None)
+    assert_f32_close(y, ref, o.abs_sum_conv(x, W, 2, 3), "block-CS stem, routed")
+    table = dev(ops.reorder_table(aug, kh, kh, c, 64, n))
+    y1, out1 = ops.conv2d_reorder_kwta(dev(x), table, kh, kh, 3, None, k=64)
+    ref1 = o.conv2d_nhwc(x, W, 1, 3, None)
+    S1 = o.abs_sum_conv(x, W, 1, 3)
+    assert_f32_close(host(y1), ref1, S1, "block-CS stem, reordered")
+    assert np.array_equal(host(out1), host(y1))                      # k = c_out: all win

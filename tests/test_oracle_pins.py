@@ -224,6 +224,27 @@ def test_kwta_invariants_random():
 
 
 # ---------------------------------------------------------------- requantisation
+def test_kwta_units_brute_force():
+    """k-WTA in units of 64: each unit of a 256-wide row keeps exactly its own
+    k largest (brute force over the unit by repeated maximum, ties to the
+    lower index); k = 64 keeps everything."""
+    r = rng(21)
+    v = r.integers(-5, 6, size=(7, 256)).astype(np.int32)
+    m = o.kwta_units_winners(v, 3)
+    for row in range(7):
+        for u in range(4):
+            seg = v[row, 64 * u:64 * (u + 1)].astype(np.int64).tolist()
+            want = set()
+            for _ in range(3):
+                best = max(i for i in range(64) if i not in want and
+                           all(seg[i] > seg[j] or (seg[i] == seg[j] and i < j)
+                               for j in range(64) if j not in want and j != i))
+                want.add(best)
+            assert set(np.flatnonzero(m[row, 64 * u:64 * (u + 1)]).tolist()) == want
+    assert o.kwta_units_winners(v, 64).all()
+    assert (o.kwta_units_winners(v, 5).reshape(7, 4, 64).sum(axis=2) == 5).all()
+
+
 def test_requant_values():
     a = np.array([0, 1, -1, 255, 256, 257, -256, -257, 10 ** 6, -10 ** 6, 127, -128, 32767])
     got = o.requant(a, 1)
@@ -297,6 +318,31 @@ def test_pack_channels_roundtrip_collision_holes():
     with pytest.raises(o.PackCollision) as e:
         o.pack_channels(W4, 2)
     assert (e.value.g, e.value.i) == (1, (1 * 2 + 1) * 2 + 1)
+
+
+def test_pack_blocks_hand_example_and_invariants():
+    """Two kernels over two blocks of 2 slots: kernel 0 owns block 0, kernel 1
+    block 1; one Kernel ID per block.  Random block-complementary weights:
+    the per-slot Kernel IDs are the block IDs repeated, the supports are whole
+    blocks; a support splitting a block is refused."""
+    from workloads import block_complementary_weights
+    W = np.array([[1, 2, 0, 0], [0, 0, 3, 4]], dtype=np.int8)
+    val, kidb, holes = o.pack_blocks(W, 2, 2)
+    assert kidb[:, 0].tolist() == [0, 1] and holes == 0
+    assert val[:, 0].tolist() == [1, 2, 3, 4]
+    r = rng(20)
+    for d_out, R, n, b in [(64, 147, 4, 3), (12, 40, 3, 4), (8, 6, 2, 3)]:
+        W = block_complementary_weights(r, r, d_out, R, n, b)
+        val, kidb, holes = o.pack_blocks(W, n, b)
+        v2, kid, h2 = o.pack(W, n)
+        assert np.array_equal(val, v2) and np.array_equal(np.repeat(kidb, b, axis=0), kid)
+        assert holes == 0 and h2 == 0
+        nzb = (W != 0).reshape(d_out, R // b, b)
+        assert (nzb.all(axis=2) | ~nzb.any(axis=2)).all()
+    W = np.array([[1, 0, 0, 0], [0, 0, 3, 4]], dtype=np.int8)
+    with pytest.raises(o.BlockViolation) as e:
+        o.pack_blocks(W, 2, 2)
+    assert (e.value.o, e.value.blk) == (0, 0)
 
 
 def test_pack_factors_from_paper():

@@ -7,6 +7,7 @@ GPU path and the CPU oracle consume what it produces.
 """
 from .configs import CONFIGS, Config, LayerSpec, get_config  # noqa: F401
 from .generate import (  # noqa: F401
+    block_complementary_weights,
     channel_complementary_weights,
     complementary_weights,
     generate,

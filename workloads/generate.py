@@ -90,6 +90,27 @@ def channel_complementary_weights(rng_part: np.random.Generator, rng_val: np.ran
     return np.where(mask, vals, np.float32(0)).astype(np.float32).reshape(c_out, kh, kw, c)
 
 
+def block_complementary_weights(rng_part: np.random.Generator, rng_val: np.random.Generator,
+                                d_out: int, r: int, n: int, b: int) -> np.ndarray:
+    """Dense fp32 [d_out][r] weights, complementary in blocks of b slots: for
+    every set, a random permutation of the r/b blocks is split into n nearly
+    equal pieces, one per kernel; a kernel is non-zero on all slots of its
+    blocks.  Values N(0, 2/nnz) per kernel, float64 rounded once to float32."""
+    if r % b or d_out % n:
+        raise ValueError("b must divide r and n must divide d_out")
+    nb = r // b
+    mask = np.zeros((d_out, nb), dtype=bool)
+    for g in range(d_out // n):
+        for j, piece in enumerate(np.array_split(rng_part.permutation(nb), n)):
+            mask[g * n + j, piece] = True
+    mask = np.repeat(mask, b, axis=1)
+    nnz = np.maximum(mask.sum(axis=1, keepdims=True), 1)
+    vals = (rng_val.normal(size=mask.shape) * np.sqrt(2.0 / nnz)).astype(np.float32)
+    if np.any(vals[mask] == 0):
+        raise RuntimeError("a support weight rounded to zero")
+    return np.where(mask, vals, np.float32(0)).astype(np.float32)
+
+
 def sparse_rows(rng: np.random.Generator, rows: int, c: int, nnz: int | None, dist: str):
     """[rows][c] activations with exactly `nnz` non-zeros per row at uniform
     positions (without replacement); nnz=None gives a dense draw.
