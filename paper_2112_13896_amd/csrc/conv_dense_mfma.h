@@ -46,6 +46,7 @@ struct DenseArgs {
   FastDiv fd_ochunks; // / (list capacity / 4)
   FastDiv fd_rowb;    // / staged row bytes ((W + 2P) * C)
   FastDiv fd_c;       // / C
+  FastDiv fd_kw;      // / KW
 };
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
@@ -157,8 +158,8 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int kk = 8 * g + j;
-    const int t = kk / C, c = kk - (kk / C) * C;
-    const int ky = t / geo.KW, kx = t - (t / geo.KW) * geo.KW;
+    const int t = (int)fdiv((uint32_t)kk, da.fd_c), c = kk - t * C;
+    const int ky = (int)fdiv((uint32_t)t, da.fd_kw), kx = t - ky * geo.KW;
     offs[j] = kk < da.R ? ky * rowb + kx * C + c : 0;
     kmask[j >> 2] |= kk < da.R ? (0xFFu << (8 * (j & 3))) : 0u;
   }

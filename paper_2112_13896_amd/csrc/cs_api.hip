@@ -489,6 +489,9 @@ bool sample_plan(const cs::ConvGeom& geo, cs_dtype xt, int k, int shift, int wri
   sa.k = k;
   sa.shift = shift;
   sa.write_sums = write_sums;
+  sa.fd_cap = cs::make_fastdiv((uint32_t)geo.cap);
+  sa.fd_g = cs::make_fastdiv((uint32_t)geo.G);
+  sa.fd_n = cs::make_fastdiv((uint32_t)geo.n);
   size_t o = (size_t)acc_rows * slice;
   sa.off_row = (uint32_t)o;
   o += round16((size_t)geo.c_out * asz);
@@ -590,6 +593,8 @@ bool scatter_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, 
       sc.fd_gpc = cs::make_fastdiv((uint32_t)(geo.G / gpl));
       sc.fd_bands = cs::make_fastdiv((uint32_t)bands);
       sc.fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / geo.pool));
+      sc.fd_cap = cs::make_fastdiv((uint32_t)geo.cap);
+      sc.fd_w = cs::make_fastdiv((uint32_t)geo.W);
       pl->shmem = total;
       pl->blocks = (int64_t)geo.B * bands;
       pl->gpl = gpl;
@@ -1244,6 +1249,7 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
       da.fd_rowb = cs::make_fastdiv((uint32_t)((w + 2 * pad) * c_in));
       da.vec_rows = pad == 0 && (w * c_in) % 16 == 0 && aligned(x, 16) ? 1 : 0;
       da.fd_c = cs::make_fastdiv((uint32_t)c_in);
+      da.fd_kw = cs::make_fastdiv((uint32_t)kw);
       const int64_t nb = (int64_t)b * da.tiles_img;
       if (nb < INT32_MAX) {
         const dim3 grid((unsigned)nb), block(cs::DENSE_BD);
@@ -1373,6 +1379,8 @@ int cs_conv2d_reorder_kwta(cs_dtype xt, const void* x, int b, int h, int w, int 
   ra.k = k;
   ra.write_sums = keep_sums;
   ra.vec4 = (c_in % 4 == 0 && aligned(x, 16)) ? 1 : 0;
+  ra.fd_cq = cs::make_fastdiv((uint32_t)(ra.vec4 ? c_in / 4 : c_in));
+  ra.fd_hw = cs::make_fastdiv((uint32_t)(cs::RO_T + kw - 1));
   const cs::ListOut lo{oidx, oval, ocnt, lists ? ocap : 0};
   const hipStream_t s = static_cast<hipStream_t>(stream);
   auto go = [&](auto kern) {

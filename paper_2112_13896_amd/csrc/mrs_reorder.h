@@ -41,6 +41,8 @@ struct ReorderArgs {
   int k;           // k-WTA winners (< 0: sums only)
   int write_sums;
   int vec4;        // 1: C % 4 == 0 and the input 16-byte aligned (float4 staging)
+  FastDiv fd_cq;   // / staged pieces per pixel (C / 4 with vec4, else C)
+  FastDiv fd_hw;   // / halo width (8 + KW - 1)
 };
 
 template <int KMAX>
@@ -65,8 +67,8 @@ __global__ __launch_bounds__(64) void conv_reorder_f32(const float* __restrict__
   if (ra.vec4) {
     const int c4 = C >> 2, n4 = HH * HW * c4;
     for (int e = lane; e < n4; e += 64) {
-      const int p = e / c4, q = e - p * c4;
-      const int hy = p / HW, hx = p - (p / HW) * HW;
+      const int p = (int)fdiv((uint32_t)e, ra.fd_cq), q = e - p * c4;
+      const int hy = (int)fdiv((uint32_t)p, ra.fd_hw), hx = p - hy * HW;
       const int iy = iy0 + hy, ix = ix0 + hx;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (iy >= 0 && iy < H && ix >= 0 && ix < W)
@@ -80,8 +82,8 @@ __global__ __launch_bounds__(64) void conv_reorder_f32(const float* __restrict__
   } else {
     const int n1 = HH * HW * C;
     for (int e = lane; e < n1; e += 64) {
-      const int p = e / C, c = e - p * C;
-      const int hy = p / HW, hx = p - (p / HW) * HW;
+      const int p = (int)fdiv((uint32_t)e, ra.fd_cq), c = e - p * C;
+      const int hy = (int)fdiv((uint32_t)p, ra.fd_hw), hx = p - hy * HW;
       const int iy = iy0 + hy, ix = ix0 + hx;
       float v = 0.f;
       if (iy >= 0 && iy < H && ix >= 0 && ix < W) v = ximg[((int64_t)iy * W + ix) * C + c];

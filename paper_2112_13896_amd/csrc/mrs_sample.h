@@ -50,6 +50,9 @@ struct SampleArgs {
   int shift;
   int write_sums;
   uint32_t off_row, off_ent, off_val, off_pix, off_hist, off_misc;   // LDS byte offsets (acc at 0)
+  FastDiv fd_cap;    // / list capacity
+  FastDiv fd_g;      // / G
+  FastDiv fd_n;      // / n
 };
 
 // An optional linear layer without k-WTA fed by this layer's winners (the
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
   for (int u = 0; u < SAMPLE_PRE; ++u) {
     const int e = u * SAMPLE_BD + tid;
     if (e < ne) {
-      const int p = e / cap, j = e - (e / cap) * cap;
+      const int p = (int)fdiv((uint32_t)e, sa.fd_cap), j = e - p * cap;
       const int2 pc = pix[p];
       if (j < pc.y) {
         erow[pc.x + j] = p * C + pidx[u];
@@ -171,7 +174,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
     }
   }
   for (int e = SAMPLE_PRE * SAMPLE_BD + tid; e < ne; e += SAMPLE_BD) {
-    const int p = e / cap, j = e - (e / cap) * cap;
+    const int p = (int)fdiv((uint32_t)e, sa.fd_cap), j = e - p * cap;
     const int2 pc = pix[p];
     if (j < pc.y) {
       erow[pc.x + j] = p * C + lidx[base + e];
@@ -186,7 +189,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
   int per = (tot + Sr - 1) / Sr;
   per = (per + 3) & ~3;
   for (int jb = tid; jb < Sr * G; jb += SAMPLE_BD) {
-    const int s = jb / G, g = jb - (jb / G) * G;
+    const int s = (int)fdiv((uint32_t)jb, sa.fd_g), g = jb - s * G;
     A* accj = acc + (kShared ? 0 : s * c_out) + g;                  // + kid * G
     const int eb = s * per;
     const int ee = eb + per < tot ? eb + per : tot;
@@ -225,7 +228,7 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
   for (int j = 0; j < SAMPLE_KEYS; ++j) {
     const int o = tid + j * SAMPLE_BD;
     if (o < c_out) {
-      const int g = o / n, kd = o - (o / n) * n;
+      const int g = (int)fdiv((uint32_t)o, sa.fd_n), kd = o - g * n;
       A v = bv[j];
       for (int s = 0; s < nrows; ++s) v += acc[s * c_out + kd * G + g];
       row[o] = v;

@@ -57,6 +57,8 @@ struct ScatterArgs {
   FastDiv fd_gpc;    // / (G / GPL)
   FastDiv fd_bands;  // / bands
   FastDiv fd_wp;     // / pooled width
+  FastDiv fd_cap;    // / list capacity
+  FastDiv fd_w;      // / input width
 };
 
 template <typename TO, int KW, int GPL, int M>
@@ -149,10 +151,10 @@ __global__ __launch_bounds__(SCAT_BD) void mrs_scatter(const uint16_t* __restric
   __syncthreads();
   // ---- the entries into LDS in (pixel, list) order
   auto put = [&](int e, int ix16, int x) {
-    const int p = e / cap, j = e - (e / cap) * cap;
+    const int p = (int)fdiv((uint32_t)e, sc.fd_cap), j = e - p * cap;
     const int2 pc = pix[p];
     if (j < pc.y) {
-      const int ly = p / W, lx = p - (p / W) * W;
+      const int ly = (int)fdiv((uint32_t)p, sc.fd_w), lx = p - ly * W;
       ent[pc.x + j] = make_int2((ly << 24) | (lx << 16) | ix16, x);
     }
   };
