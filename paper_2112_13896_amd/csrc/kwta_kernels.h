@@ -283,13 +283,86 @@ __device__ __forceinline__ void kwta_wave_row(const TI (&v)[M], int c, int k, in
   if (lo.idx && lane == 0) lo.cnt[row] = lrun;
 }
 
+// Exchanges within a quad of lanes (DPP quad permutations, no LDS).
+__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);   // [1,0,3,2]
+}
+__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);   // [2,3,0,1]
+}
+__device__ __forceinline__ int quad_excl_sum(int v, int qd) {
+  // Hillis-Steele over the 4 lanes: from lane qd-1, then from lane qd-2
+  int x = v;
+  const int t1 = __builtin_amdgcn_update_dpp(0, x, 0x90, 0xF, 0xF, false);        // [0,0,1,2]
+  x += qd >= 1 ? t1 : 0;
+  const int t2 = __builtin_amdgcn_update_dpp(0, x, 0x40, 0xF, 0xF, false);        // [0,0,0,1]
+  x += qd >= 2 ? t2 : 0;
+  return x - v;
+}
+
+// Bitonic networks in registers (all indices compile-time): sort N keys
+// descending; sort a bitonic sequence of N keys descending; and keep in a[]
+// the N largest of two descending lists (a max against the reversed other
+// list leaves a bitonic sequence holding them, which is then sorted).
+template <int N>
+__device__ __forceinline__ void bitonic_sort_desc(uint32_t (&a)[N]) {
+#pragma unroll
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint32_t x = a[i], y = a[l];
+          const uint32_t hi = x > y ? x : y, lo = x > y ? y : x;
+          const bool desc = (i & k) == 0;
+          a[i] = desc ? hi : lo;
+          a[l] = desc ? lo : hi;
+        }
+      }
+}
+template <int N>
+__device__ __forceinline__ void bitonic_clean_desc(uint32_t (&a)[N]) {
+#pragma unroll
+  for (int j = N >> 1; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int l = i ^ j;
+      if (l > i) {
+        const uint32_t x = a[i], y = a[l];
+        a[i] = x > y ? x : y;
+        a[l] = x > y ? y : x;
+      }
+    }
+}
+template <int N>
+__device__ __forceinline__ void top_merge_desc(uint32_t (&a)[N], const uint32_t (&b)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) a[i] = a[i] > b[N - 1 - i] ? a[i] : b[N - 1 - i];
+  bitonic_clean_desc<N>(a);
+}
+// Keep the N largest of this lane's list and that of its DPP partner (CTRL: a
+// permutation within each row of 16 lanes); both lists sorted descending.
+template <int N, int CTRL>
+__device__ __forceinline__ void row16_top_merge(uint32_t (&a)[N]) {
+  uint32_t p[N];
+#pragma unroll
+  for (int s = 0; s < N; ++s) p[s] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)a[s], CTRL, 0xF, 0xF, false);
+  top_merge_desc<N>(a, p);
+}
+
 // k-WTA of one row held by one row of 16 lanes (lanes 16q .. 16q + 15 of a
 // wavefront hold one row each): lane r holds v[j] = element r*KPL + j
-// (elements >= c are not part of the row).  The threshold is found bit by
-// bit below the row's range (keys offset by the row minimum), counting with
-// 16-lane DPP sums; ties go to the lower index; the winners are written as the
-// row's list (non-zero outputs in index order, and the count) or densely.
-// Every lane of the wavefront must be active; `live` rows write.
+// (elements >= c are not part of the row).  The threshold T, the k-th largest
+// key (keys offset by the row minimum), comes for k <= ROW16_TOPK from the
+// lanes' sorted top lists merged over the row (partners at distance 1 and 2,
+// then the mirrored lane of the half row and of the row: four DPP exchanges),
+// else bit by bit below the row's range, counting with 16-lane DPP sums.
+// Ties go to the lower index; the winners are written as the row's list
+// (non-zero outputs in index order, and the count) or densely.  Every lane of
+// the wavefront must be active; `live` rows write.
+constexpr int ROW16_TOPK = 8;
 template <typename TI, typename TO, int KPL>
 __device__ __forceinline__ void kwta_row16(const TI (&v)[KPL], int c, int k, int shift, bool live,
                                            const ListOut& lo, TO* __restrict__ out, int64_t row) {
@@ -319,6 +392,30 @@ __device__ __forceinline__ void kwta_row16(const TI (&v)[KPL], int c, int k, int
     need = c;
   } else if (range == 0u) {
     need = k;
+  } else if (k <= ROW16_TOPK) {
+    // keys outside the row are 0, the smallest key: with k < c they never
+    // change the k-th largest
+    uint32_t top[ROW16_TOPK];
+#pragma unroll
+    for (int s = 0; s < ROW16_TOPK; ++s) top[s] = 0u;
+#pragma unroll
+    for (int b0 = 0; b0 < KPL; b0 += ROW16_TOPK) {
+      uint32_t blk[ROW16_TOPK];
+#pragma unroll
+      for (int s = 0; s < ROW16_TOPK; ++s) blk[s] = b0 + s < KPL ? key[b0 + s] : 0u;
+      bitonic_sort_desc<ROW16_TOPK>(blk);
+      top_merge_desc<ROW16_TOPK>(top, blk);
+    }
+    row16_top_merge<ROW16_TOPK, 0xB1>(top);                         // quad [1,0,3,2]
+    row16_top_merge<ROW16_TOPK, 0x4E>(top);                         // quad [2,3,0,1]
+    row16_top_merge<ROW16_TOPK, 0x141>(top);                        // half-row mirror
+    row16_top_merge<ROW16_TOPK, 0x140>(top);                        // row mirror
+#pragma unroll
+    for (int s = 0; s < ROW16_TOPK; ++s) thr = (s == k - 1) ? top[s] : thr;
+    int gt = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) gt += (i0 + j < c && key[j] > thr) ? 1 : 0;
+    need = k - (int)row16_reduce((uint32_t)gt, OpAdd{});
   } else {
     uint32_t T = 0u;
     for (int b = 31 - __builtin_clz(range); b >= 0; --b) {         // uniform within a row

@@ -107,66 +107,6 @@ struct RowMap {
   }
 };
 
-// Exchanges within a quad of lanes (DPP quad permutations, no LDS).
-__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);   // [1,0,3,2]
-}
-__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);   // [2,3,0,1]
-}
-__device__ __forceinline__ int quad_excl_sum(int v, int qd) {
-  // Hillis-Steele over the 4 lanes: from lane qd-1, then from lane qd-2
-  int x = v;
-  const int t1 = __builtin_amdgcn_update_dpp(0, x, 0x90, 0xF, 0xF, false);        // [0,0,1,2]
-  x += qd >= 1 ? t1 : 0;
-  const int t2 = __builtin_amdgcn_update_dpp(0, x, 0x40, 0xF, 0xF, false);        // [0,0,0,1]
-  x += qd >= 2 ? t2 : 0;
-  return x - v;
-}
-
-// Bitonic networks in registers (all indices compile-time): sort N keys
-// descending; sort a bitonic sequence of N keys descending; and keep in a[]
-// the N largest of two descending lists (a max against the reversed other
-// list leaves a bitonic sequence holding them, which is then sorted).
-template <int N>
-__device__ __forceinline__ void bitonic_sort_desc(uint32_t (&a)[N]) {
-#pragma unroll
-  for (int k = 2; k <= N; k <<= 1)
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1)
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        const int l = i ^ j;
-        if (l > i) {
-          const uint32_t x = a[i], y = a[l];
-          const uint32_t hi = x > y ? x : y, lo = x > y ? y : x;
-          const bool desc = (i & k) == 0;
-          a[i] = desc ? hi : lo;
-          a[l] = desc ? lo : hi;
-        }
-      }
-}
-template <int N>
-__device__ __forceinline__ void bitonic_clean_desc(uint32_t (&a)[N]) {
-#pragma unroll
-  for (int j = N >> 1; j > 0; j >>= 1)
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int l = i ^ j;
-      if (l > i) {
-        const uint32_t x = a[i], y = a[l];
-        a[i] = x > y ? x : y;
-        a[l] = x > y ? y : x;
-      }
-    }
-}
-template <int N>
-__device__ __forceinline__ void top_merge_desc(uint32_t (&a)[N], const uint32_t (&b)[N]) {
-#pragma unroll
-  for (int i = 0; i < N; ++i) a[i] = a[i] > b[N - 1 - i] ? a[i] : b[N - 1 - i];
-  bitonic_clean_desc<N>(a);
-}
-
 // k-WTA with four lanes per item (a quad): each lane keeps the KMAX largest
 // keys of its quarter of the row, sorted (blocks of KMAX keys sorted and
 // merged with bitonic networks), the quad merges the four lists (two exchange

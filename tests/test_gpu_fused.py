@@ -105,6 +105,10 @@ CASES = [
     ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, True, None, "dense", ("scatter", None)),
     ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 20, False, 10, "lists", ("scatter", None)),
     ("i8", (1, 40, 40, 32), 6, 3, 3, 1, 1, 64, 8, 2, 8, True, 9, "lists", ("scatter", None)),
+    # k-WTA by merged top lists (k <= 8): 8 channels per lane with ties, and
+    # 96 channels (lanes past the row) with pooling
+    ("i8", (2, 9, 9, 32), 6, 3, 3, 1, 1, 128, 16, 1, 7, False, 0, "lists", ("scatter", None)),
+    ("i8", (2, 10, 10, 32), 6, 3, 3, 1, 1, 96, 16, 2, 5, True, 0, "lists", ("scatter", None)),
     ("i8", (1, 6, 300, 16), 4, 3, 3, 1, 1, 16, 4, 1, 4, False, 5, "lists", ("fused", 1)),
     # int8 1x1 layers with many items and a k-WTA over long rows: one
     # wavefront per item (config 5's expand shape; more sets than lanes; ties
