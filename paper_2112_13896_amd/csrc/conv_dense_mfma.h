@@ -94,17 +94,18 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       // unpadded rows inside the image: one contiguous run, 16 bytes per load
       const uint4* src = reinterpret_cast<const uint4*>(ximg + (int64_t)iy0 * W * C);
       uint4* dst = reinterpret_cast<uint4*>(rows);
-      for (int b0 = 0; b0 < nbytes / 16; b0 += DENSE_BD * 2) {
+      const int n16 = nbytes / 16;                         // >= 1
+      for (int b0 = 0; b0 < n16; b0 += DENSE_BD * 2) {
         uint4 v[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const int e = b0 + u * DENSE_BD + tid;
-          if (e < nbytes / 16) v[u] = src[e];
+          v[u] = src[e < n16 ? e : n16 - 1];               // in range: no branch
         }
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const int e = b0 + u * DENSE_BD + tid;
-          if (e < nbytes / 16) dst[e] = v[u];
+          if (e < n16) dst[e] = v[u];
         }
       }
     } else

@@ -172,39 +172,41 @@ __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, 
       for (int s = 0; s < KMAX; ++s) gt += (s < k && top[s] > thr) ? 1 : 0;
       need = k - gt;
     }
-    // --- counts of this lane's quarter: ties with T, then winners with output != 0
-    int ties_l = 0;
+    // --- the lane's quarter as bit masks (bit j: element i_lo + j; c <= 128,
+    // so a quarter has at most 32 elements): keys above T and keys equal to T
+    uint32_t gtm = 0u, eqm = 0u;
     if (live && k > 0) {
       for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
 #pragma unroll
         for (int j = 0; j < BK; ++j) {
           const int i = i0 + j;
           const uint32_t key = order_key(v[i < i_hi ? i : i_hi - 1]);
-          ties_l += (i < i_hi && key == thr) ? 1 : 0;
+          const uint32_t bit = i < i_hi ? 1u << (i - i_lo) : 0u;
+          gtm |= key > thr ? bit : 0u;
+          eqm |= key == thr ? bit : 0u;
         }
       }
     }
-    const int tie0 = quad_excl_sum(ties_l, qd);          // ties in the quarters before
-    int win_l = 0, last_tie = -1;
-    {
-      int tr = tie0;
-      if (live && k > 0) {
-        for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
-#pragma unroll
-          for (int j = 0; j < BK; ++j) {
-            const int i = i0 + j;
-            const A a = v[i < i_hi ? i : i_hi - 1];
-            const uint32_t key = order_key(a);
-            const bool in = i < i_hi;
-            const bool tie = in && key == thr && tr < need;
-            tr += (in && key == thr) ? 1 : 0;
-            last_tie = tie ? i : last_tie;
-            const bool win = (in && key > thr) || tie;
-            win_l += (win && kwta_out<A, TO>(a, shift) != TO(0)) ? 1 : 0;
-          }
-        }
-      }
+    // the winning ties are the first `need` equal keys of the row: this lane's
+    // first need - (ties in the quarters before) of its own
+    const int ties_l = __popc(eqm);
+    const int tie0 = quad_excl_sum(ties_l, qd);
+    int m = need - tie0;
+    m = m < 0 ? 0 : (m > ties_l ? ties_l : m);
+    uint32_t tm = 0u;
+    for (uint32_t e2 = eqm; m > 0; --m) {
+      const uint32_t lb = e2 & (0u - e2);
+      tm |= lb;
+      e2 ^= lb;
     }
+    int last_tie = tm ? i_lo + 31 - __builtin_clz(tm) : -1;
+    // winners with a non-zero output value: their list positions
+    uint32_t putm = 0u;
+    for (uint32_t w = gtm | tm; w != 0u; w &= w - 1u) {
+      const int j = __builtin_ctz(w);
+      putm |= kwta_out<A, TO>(v[i_lo + j], shift) != TO(0) ? 1u << j : 0u;
+    }
+    const int win_l = __popc(putm);
     const int pos0 = quad_excl_sum(win_l, qd);           // list position of the first winner
     // the last winning tie of the row: the largest over the quad
     {
@@ -216,25 +218,13 @@ __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, 
       last_tie = (int)lt - 1;
     }
     if (live) {
-      if (tl_idx && win_l > 0) {
-        int tr = tie0, pos = pos0;
-        for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
-#pragma unroll
-          for (int j = 0; j < BK; ++j) {
-            const int i = i0 + j;
-            const A a = v[i < i_hi ? i : i_hi - 1];
-            const uint32_t key = order_key(a);
-            const bool in = i < i_hi;
-            const bool tie = in && key == thr && tr < need;
-            tr += (in && key == thr) ? 1 : 0;
-            const bool win = k > 0 && ((in && key > thr) || tie);
-            const TO ov = kwta_out<A, TO>(a, shift);
-            if (win && ov != TO(0)) {
-              tl_idx[it * cap + pos] = (uint16_t)i;
-              tl_val[it * cap + pos] = ov;
-              ++pos;
-            }
-          }
+      if (tl_idx) {
+        int pos = pos0;
+        for (uint32_t w = putm; w != 0u; w &= w - 1u) {
+          const int i = i_lo + __builtin_ctz(w);
+          tl_idx[it * cap + pos] = (uint16_t)i;
+          tl_val[it * cap + pos] = kwta_out<A, TO>(v[i], shift);
+          ++pos;
         }
       }
       if (qd == 0) sel[it] = make_uint2(thr, (uint32_t)last_tie);
