@@ -12,7 +12,11 @@
 //    (rows 4*(lane/16) .. +3, column lane%16) are the 2x2 window of one pooled
 //    pixel and the max-pool is a max over the lane's own 4 values;
 //  * the B operand (the 64 channels' weights, 4 N tiles of 16) stays in
-//    registers for the whole workgroup;
+//    registers for the whole workgroup; it is staged transposed ([channel][32
+//    slots] bytes, zero past R), so a lane's 8 slots are one 8-byte read, and
+//    the zero slots make the A operand's bytes past R irrelevant;
+//  * the byte offsets of the 32 slots in the staged rows are a table built
+//    once per workgroup;
 //  * the pooled sums + bias go to an LDS tile [items][64 + 1]; k-WTA and the
 //    output run as in the fused sparse layer (four lanes per item).
 #pragma once
@@ -78,17 +82,25 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
   const int nbytes = rows_in * rowb;                        // <= the LDS allocation (host)
   int8_t* rows = reinterpret_cast<int8_t*>(smem);
 
-  // the weights ([R][64] 16-bit entries, value in the low byte) are staged in
-  // LDS with 16-byte loads issued together with the input's
+  // the weights ([R][64] 16-bit entries, value in the low byte) are staged
+  // transposed, wt[channel][slot] bytes with slots R .. 31 zero: thread t
+  // gathers slots 4*(t%8) .. +3 of channel t/8, loads issued together with
+  // the input's
   const int g = lane >> 4, col = lane & 15;
-  uint16_t* wts = reinterpret_cast<uint16_t*>(smem + da.off_w);
+  unsigned char* wt = smem + da.off_w;                     // [64][32] bytes
+  int* offt = reinterpret_cast<int*>(smem + da.off_w + 64 * 32);   // [32] slot offsets
   int32_t bch[4];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) bch[nt] = bias ? bias[16 * nt + col] : 0;
   {
-    const int n16 = da.R * 64 * 2 / 16;                   // R * 64 entries: whole 16-byte pieces
-    uint4 wv = {0u, 0u, 0u, 0u};
-    if (tid < n16) wv = reinterpret_cast<const uint4*>(aug)[tid];   // n16 <= 256 < DENSE_BD
+    static_assert(DENSE_BD == 64 * 8, "one thread per (channel, 4 slots)");
+    const int wch = tid >> 3, wk0 = (tid & 7) * 4;
+    uint32_t wb4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int kk = wk0 + i;
+      wb4[i] = aug[(kk < da.R ? kk : 0) * 64 + wch];
+    }
     const int8_t* ximg = x + (int64_t)img * geo.H * W * C;
     if (da.vec_rows && iy0 >= 0 && iy0 + rows_in <= geo.H) {
       // unpadded rows inside the image: one contiguous run, 16 bytes per load
@@ -128,41 +140,32 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
         if (e < nbytes) rows[e] = v[u];
       }
     }
-    if (tid < n16) reinterpret_cast<uint4*>(wts)[tid] = wv;
+    uint32_t w4 = 0u;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w4 |= (wk0 + i < da.R ? wb4[i] & 0xFFu : 0u) << (8 * i);
+    reinterpret_cast<uint32_t*>(wt)[tid] = w4;               // wt + wch * 32 + wk0
+    if (tid < 32) {
+      // slot kk = (ky * KW + kx) * C + c: byte offset from a window's corner
+      const int kk = tid;
+      const int t = (int)fdiv((uint32_t)kk, da.fd_c), c = kk - t * C;
+      const int ky = (int)fdiv((uint32_t)t, da.fd_kw), kx = t - ky * geo.KW;
+      offt[kk] = kk < da.R ? ky * rowb + kx * C + c : 0;
+    }
   }
   __syncthreads();
   // B operands: lane holds channel 16*nt + lane%16, slots 8*(lane/16) .. +7
-  uint32_t bw[4][8];
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int kk = 8 * g + j;
-      bw[nt][j] = wts[(kk < da.R ? kk : 0) * 64 + 16 * nt + col];
-    }
   int64_t bop[4];
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    uint64_t b8 = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t v = 8 * g + j < da.R ? (bw[nt][j] & 0xFFu) : 0u;
-      b8 |= (uint64_t)v << (8 * j);
-    }
-    bop[nt] = (int64_t)b8;
-  }
-
-  // this lane's 8 slots of a window: byte offset from the window's top-left
-  // corner in the staged rows (slots past R read offset 0 and are masked)
+  for (int nt = 0; nt < 4; ++nt)
+    bop[nt] = *reinterpret_cast<const int64_t*>(wt + (16 * nt + col) * 32 + 8 * g);
+  // this lane's 8 slots of a window: byte offsets from the window's top-left
+  // corner in the staged rows (slots past R read offset 0; their B is zero)
   int offs[8];
-  uint32_t kmask[2] = {0u, 0u};                             // bytes of slots < R
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int kk = 8 * g + j;
-    const int t = (int)fdiv((uint32_t)kk, da.fd_c), c = kk - t * C;
-    const int ky = (int)fdiv((uint32_t)t, da.fd_kw), kx = t - ky * geo.KW;
-    offs[j] = kk < da.R ? ky * rowb + kx * C + c : 0;
-    kmask[j >> 2] |= kk < da.R ? (0xFFu << (8 * (j & 3))) : 0u;
+  {
+    const int4 o0 = reinterpret_cast<const int4*>(offt)[2 * g];
+    const int4 o1 = reinterpret_cast<const int4*>(offt)[2 * g + 1];
+    offs[0] = o0.x; offs[1] = o0.y; offs[2] = o0.z; offs[3] = o0.w;
+    offs[4] = o1.x; offs[5] = o1.y; offs[6] = o1.z; offs[7] = o1.w;
   }
 
   int32_t* otile = reinterpret_cast<int32_t*>(smem + da.off_out);
@@ -187,11 +190,15 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       lo4 |= (uint32_t)wb[offs[j]] << (8 * j);
       hi4 |= (uint32_t)wb[offs[4 + j]] << (8 * j);
     }
-    const uint64_t a8 = (uint64_t)(lo4 & kmask[0]) | ((uint64_t)(hi4 & kmask[1]) << 32);
+    const uint64_t a8 = (uint64_t)lo4 | ((uint64_t)hi4 << 32);
     const v4i_t zero = {0, 0, 0, 0};
+    v4i_t dd[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)   // independent products, issued back to back
+      dd[nt] = __builtin_amdgcn_mfma_i32_16x16x32_i8((int64_t)a8, bop[nt], zero, 0, 0, 0);
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      const v4i_t d = __builtin_amdgcn_mfma_i32_16x16x32_i8((int64_t)a8, bop[nt], zero, 0, 0, 0);
+      const v4i_t d = dd[nt];
       // lane holds rows 4g .. 4g+3 of column col
       if constexpr (POOL == 2) {
         const int it = mt * IPM + g;                      // the 4 rows are its 2x2 window

@@ -1219,7 +1219,7 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
       const size_t items_t = (size_t)tpr * Wp;
       size_t o = round16((size_t)rows_in * (w + 2 * pad) * c_in);   // zero-padded rows
       da.off_w = (uint32_t)o;
-      o += round16((size_t)R * 64 * 2);                              // the weights
+      o += 64 * 32 + 32 * 4;                              // weights [64][32] bytes, slot offsets
       da.off_out = (uint32_t)o;
       o += round16(items_t * 65 * 4);
       da.off_sel = (uint32_t)o;
