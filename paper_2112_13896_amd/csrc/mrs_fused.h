@@ -117,18 +117,18 @@ struct RowMap {
 // winners with a non-zero output value go to the tile's LDS lists in index
 // order and their count to cnt.  sel[it] = (T, index of the last winning tie
 // or -1).  Rows are read with an odd stride (bank-conflict free).
-template <typename A, typename TO, int KMAX, int BD = MRS_BD>
-__device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
-                                int c, int k, int shift, uint2* sel, uint16_t* tl_idx,
-                                TO* tl_val, int cap, int32_t* gcnt) {
+// One item (tile slot `it`) per quad; every lane of the wavefront takes part
+// (the DPP exchanges), `live` quads write.
+template <typename A, typename TO, int KMAX>
+__device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int it, bool live,
+                                               const RowMap& rm, int c, int k, int shift,
+                                               uint2* sel, uint16_t* tl_idx, TO* tl_val, int cap,
+                                               int32_t* gcnt) {
   constexpr int BK = 16;                               // keys read per batch (loads issued together)
   const int qd = threadIdx.x & 3;
   const int L = (c + 3) >> 2;                          // row quarter of a lane
   const int i_lo = qd * L, i_hi = min(c, i_lo + L);
-  const int nsl = (sm.nslots + 3) & ~3;
-  for (int base = 0; base < ((nsl + BD / 4 - 1) / (BD / 4)) * (BD / 4); base += BD / 4) {
-    const int it = base + (threadIdx.x >> 2);
-    const bool live = sm.live(it);                     // the same for the 4 lanes of the quad
+  {
     const A* v = otile + (live ? it : 0) * ostride;
     // --- the threshold: per-lane top-KMAX of the quarter, merged over the quad
     // (keys past the quarter are 0: a 0 never changes the k-th largest)
@@ -230,6 +230,19 @@ __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, 
       if (qd == 0) sel[it] = make_uint2(thr, (uint32_t)last_tie);
       if (tl_idx && qd == 3) gcnt[rm.row(it)] = pos0 + win_l;
     }
+  }
+}
+
+// All the tile's slots, one per quad of the workgroup's BD threads.
+template <typename A, typename TO, int KMAX, int BD = MRS_BD>
+__device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
+                                int c, int k, int shift, uint2* sel, uint16_t* tl_idx,
+                                TO* tl_val, int cap, int32_t* gcnt) {
+  const int nsl = (sm.nslots + 3) & ~3;
+  for (int base = 0; base < ((nsl + BD / 4 - 1) / (BD / 4)) * (BD / 4); base += BD / 4) {
+    const int it = base + (threadIdx.x >> 2);
+    kwta_quad_item<A, TO, KMAX>(otile, ostride, it, sm.live(it), rm, c, k, shift, sel, tl_idx,
+                                tl_val, cap, gcnt);
   }
 }
 

@@ -321,6 +321,8 @@ DENSE_KWTA_CASES = [
     ("i8", (2, 12, 12, 1), 5, 5, 1, 2, 2, 0, False, 3, "lists"),      # k = 0
     ("i8", (4, 12, 12, 1), 3, 3, 1, 1, 2, 8, False, 0, "lists"),      # ties: +-1 weights, 0/1 input
     ("i8", (2, 12, 12, 1), 5, 5, 1, 0, 2, 40, False, 6, "lists"),     # k > 32: two kernels
+    ("i8", (3, 10, 12, 1), 3, 3, 1, 1, 1, 20, True, 5, "lists"),      # top-32 networks, no pool
+    ("i8", (520, 36, 36, 1), 5, 5, 1, 0, 2, 3, True, 9, "lists"),     # 256 items per workgroup
     ("f32", (2, 14, 14, 1), 5, 5, 1, 0, 2, 8, True, None, "dense"),   # fp32: two kernels
 ]
 
