@@ -263,6 +263,42 @@ int cs_mrs_kwta_chain2(cs_dtype xt, const uint16_t* idx, const void* lval, const
                        const void* bias2, void* y2, void* stream);
 
 /*
+ * cs_mrs_kwta_chain3 - three layers of a chain's tail (Figure 10: every
+ * layer's winners go on to the next with their indices): an int8 convolution
+ * with k-WTA and lists, a layer with k-WTA whose window is that layer's whole
+ * pooled map (one output vector per sample), and a linear layer without k-WTA
+ * on its winners.  The result is that of cs_mrs_kwta_conv2d on the first
+ * layer followed by cs_mrs_kwta_chain2 on its lists (input shape b x hp x wp x
+ * c_out, window hp x wp, stride 1, no padding, no pool, where hp x wp is the
+ * first layer's pooled map).  When the first layer runs input-stationary with
+ * one workgroup per image and the second one workgroup per sample, the three
+ * run in one kernel: each workgroup writes its image's lists, then (after a
+ * workgroup barrier) reads them back as the second layer's input and feeds
+ * the third layer on chip; otherwise the two calls run back to back on
+ * `stream`.  DEVICE memory.
+ *
+ *  xt .. ocap   the first layer as cs_mrs_kwta_conv2d, with xt == ot == CS_I8
+ *          and list output (oidx, oval, ocnt, ocap).
+ *  aug2, c_out2, n2, bias2, y2, k2, shift2, oidx2, oval2, ocnt2, ocap2   the
+ *          second layer (cs_pack of [c_out2][hp*wp*c_out] int8 weights in the
+ *          (y, x, channel) slot order; bias2 int32 or NULL; y2 int32
+ *          [b][c_out2] sums, written when keep_sums; k-WTA k2 with
+ *          requantisation shift2, lists of capacity ocap2 >= k2).
+ *  aug3, c_out3, n3, bias3, y3   the third layer as cs_mrs_kwta_chain2's
+ *          second (y3: int32 [b][c_out3]).
+ *  Errors: as cs_mrs_kwta_conv2d and cs_mrs_kwta_chain2 (CS_ERR_ARG for a
+ *  missing buffer or a bad k, shift or keep_sums; CS_ERR_SHAPE for sizes).
+ */
+int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, uint16_t* oidx, void* oval,
+                       int32_t* ocnt, int ocap, const void* aug2, int c_out2, int n2,
+                       const void* bias2, void* y2, int k2, int shift2, uint16_t* oidx2,
+                       void* oval2, int32_t* ocnt2, int ocap2, const void* aug3, int c_out3,
+                       int n3, const void* bias3, void* y3, void* stream);
+
+/*
  * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
  * Route, Sum with dense activations; Section 4 runs the first layer of the
  * keyword-spotting network this way because its input is dense).  DEVICE

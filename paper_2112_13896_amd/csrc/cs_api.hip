@@ -1440,3 +1440,110 @@ int cs_mrs_kwta_chain2(cs_dtype xt, const uint16_t* idx, const void* lval, const
   return cs_mrs_conv2d(CS_I8, oidx, oval, ocnt, ocap, b, 1, 1, c_out, 1, 1, 1, 0, aug2, c_out2, n2,
                        bias2, 1, y2, stream);
 }
+
+template <int KW, int GPL, int M>
+void launch_scatter_sample_t(const ScatterPlan& scp, const SamplePlan& sp, size_t shmem,
+                             hipStream_t s, const uint16_t* idx, const void* lval,
+                             const int32_t* cnt, const void* aug, const void* bias, void* y,
+                             const cs::ListOut& lo, const cs::ConvGeom& geo, const void* aug2,
+                             const void* bias2, void* y2, const cs::ListOut& lo2,
+                             const cs::ConvGeom& geo2, const cs::NextLayer& nx) {
+  hipLaunchKernelGGL((cs::mrs_scatter_sample<KW, GPL, M>), dim3((unsigned)scp.blocks),
+                     dim3(cs::SCAT_BD), shmem, s, idx, static_cast<const int8_t*>(lval), cnt,
+                     static_cast<const uint16_t*>(aug), static_cast<const int32_t*>(bias),
+                     static_cast<int32_t*>(y), lo, geo, scp.sc,
+                     static_cast<const uint16_t*>(aug2), static_cast<const int32_t*>(bias2),
+                     static_cast<int32_t*>(y2), lo2, geo2, sp.sa, nx);
+}
+
+template <int KW>
+void launch_scatter_sample_kw(const ScatterPlan& scp, const SamplePlan& sp, size_t shmem,
+                              hipStream_t s, const uint16_t* idx, const void* lval,
+                              const int32_t* cnt, const void* aug, const void* bias, void* y,
+                              const cs::ListOut& lo, const cs::ConvGeom& geo, const void* aug2,
+                              const void* bias2, void* y2, const cs::ListOut& lo2,
+                              const cs::ConvGeom& geo2, const cs::NextLayer& nx) {
+#define CS_SCS(GPL_, M_)                                                                       \
+  launch_scatter_sample_t<KW, GPL_, M_>(scp, sp, shmem, s, idx, lval, cnt, aug, bias, y, lo, geo, \
+                                        aug2, bias2, y2, lo2, geo2, nx)
+  if (scp.gpl == 2) {
+    if (scp.m == 1) CS_SCS(2, 1);
+    else CS_SCS(2, 2);
+  } else {
+    if (scp.m == 1) CS_SCS(1, 1);
+    else CS_SCS(1, 2);
+  }
+#undef CS_SCS
+}
+
+int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t* cnt,
+                       int cap, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+                       const void* aug, int c_out, int n, const void* bias, int pool, void* y,
+                       int keep_sums, int k, cs_dtype ot, int shift, uint16_t* oidx, void* oval,
+                       int32_t* ocnt, int ocap, const void* aug2, int c_out2, int n2,
+                       const void* bias2, void* y2, int k2, int shift2, uint16_t* oidx2,
+                       void* oval2, int32_t* ocnt2, int ocap2, const void* aug3, int c_out3,
+                       int n3, const void* bias3, void* y3, void* stream) {
+  if (xt != CS_I8 || ot != CS_I8) return CS_ERR_DTYPE;
+  if (!idx || !lval || !cnt || !aug || !y || !oidx || !oval || !ocnt) return CS_ERR_ARG;
+  if (!aug2 || !y2 || !oidx2 || !oval2 || !ocnt2 || !aug3 || !y3) return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0 || shift < 0 || shift > 31 || k2 < 0 ||
+      shift2 < 0 || shift2 > 31)
+    return CS_ERR_ARG;
+  if (cap < 1 || ocap < 1 || ocap2 < 1 || c_out2 < 1 || n2 < 1 || c_out3 < 1 || n3 < 1)
+    return CS_ERR_SHAPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (k > c_out || c_out > CS_MAX_KWTA_ROW || ocap < k) return CS_ERR_SHAPE;
+  // the second layer: a window over the whole pooled map of the first
+  const int hp = geo.Ho / pool, wp = geo.Wo / pool;
+  cs::ConvGeom geo2;
+  st = conv_geometry(b, hp, wp, c_out, hp, wp, 1, 0, c_out2, n2, 1, &geo2);
+  if (st != CS_OK) return st;
+  if (k2 > c_out2 || c_out2 > CS_MAX_KWTA_ROW || ocap2 < k2) return CS_ERR_SHAPE;
+  if (n3 > CS_MAX_N || c_out3 % n3 != 0) return CS_ERR_SHAPE;
+  geo.cap = cap;
+  geo2.cap = ocap;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  // one kernel when the first layer runs one workgroup per image (its band
+  // is the whole image) and the second one workgroup per sample
+  ScatterPlan scp;
+  SamplePlan sp;
+  if (!sample_plan(geo, xt, k, shift, keep_sums, &sp) &&
+      scatter_plan(geo, xt, aug, k, shift, keep_sums, &scp) && scp.sc.bands == 1 &&
+      scp.blocks == b && sample_plan(geo2, xt, k2, shift2, keep_sums, &sp)) {
+    const cs::NextLayer nx{static_cast<const uint16_t*>(aug3), static_cast<const int32_t*>(bias3),
+                           static_cast<int32_t*>(y3), c_out3 / n3, n3, c_out3,
+                           (uint32_t)round16(sp.shmem)};
+    const size_t shmem2 = (size_t)nx.off_acc + round16((size_t)c_out3 * 4);
+    const size_t shmem = std::max(scp.shmem, shmem2);
+    if (shmem <= kCuLds) {
+      const cs::ListOut lo{oidx, oval, ocnt, ocap};
+      const cs::ListOut lo2{oidx2, oval2, ocnt2, ocap2};
+      switch (geo.KW) {
+        case 3:
+          launch_scatter_sample_kw<3>(scp, sp, shmem, s, idx, lval, cnt, aug, bias, y, lo, geo,
+                                      aug2, bias2, y2, lo2, geo2, nx);
+          break;
+        case 5:
+          launch_scatter_sample_kw<5>(scp, sp, shmem, s, idx, lval, cnt, aug, bias, y, lo, geo,
+                                      aug2, bias2, y2, lo2, geo2, nx);
+          break;
+        default:
+          launch_scatter_sample_kw<7>(scp, sp, shmem, s, idx, lval, cnt, aug, bias, y, lo, geo,
+                                      aug2, bias2, y2, lo2, geo2, nx);
+          break;
+      }
+      return launch_status();
+    }
+  }
+  // otherwise: the first layer, then the two-layer tail on its lists
+  st = cs_mrs_kwta_conv2d(xt, idx, lval, cnt, cap, b, h, w, c_in, kh, kw, stride, pad, aug, c_out,
+                          n, bias, pool, y, keep_sums, k, ot, shift, nullptr, oidx, oval, ocnt,
+                          ocap, stream);
+  if (st != CS_OK) return st;
+  return cs_mrs_kwta_chain2(xt, oidx, oval, ocnt, ocap, b, hp, wp, c_out, hp, wp, 1, 0, aug2,
+                            c_out2, n2, bias2, 1, y2, keep_sums, k2, ot, shift2, oidx2, oval2,
+                            ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, stream);
+}

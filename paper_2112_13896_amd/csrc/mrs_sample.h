@@ -98,21 +98,21 @@ __device__ __forceinline__ float acc_from_bits<float>(uint32_t b) { return __uin
 
 typedef uint32_t su32x4 __attribute__((ext_vector_type(4)));
 
+// The workgroup body for sample `item` (SAMPLE_BD threads).
 template <typename T, typename A, typename TO>
-__global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restrict__ lidx,
-                                                        const T* __restrict__ lval,
-                                                        const int32_t* __restrict__ lcnt,
-                                                        const typename Aug<T>::type* __restrict__ aug,
-                                                        const A* __restrict__ bias,
-                                                        A* __restrict__ y, TO* __restrict__ out,
-                                                        ListOut lo, ConvGeom geo, SampleArgs sa,
-                                                        NextLayer nx) {
+__device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
+                                            const T* __restrict__ lval,
+                                            const int32_t* __restrict__ lcnt,
+                                            const typename Aug<T>::type* __restrict__ aug,
+                                            const A* __restrict__ bias, A* __restrict__ y,
+                                            TO* __restrict__ out, const ListOut& lo,
+                                            const ConvGeom& geo, const SampleArgs& sa,
+                                            const NextLayer& nx, int64_t item) {
   using E = typename Aug<T>::type;
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = geo.n, G = geo.G, C = geo.C, c_out = geo.c_out, cap = geo.cap;
   const int npix = sa.npix, ne = npix * cap;
-  const int64_t item = blockIdx.x;
   A* acc = reinterpret_cast<A*>(smem);                              // [S][n][G]
   A* row = reinterpret_cast<A*>(smem + sa.off_row);                 // [c_out]
   int* erow = reinterpret_cast<int*>(smem + sa.off_ent);            // [ne + pad]
@@ -447,6 +447,18 @@ __global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restri
         nx.y[item * nx.c_out + o] = acc2[o] + (nx.bias != nullptr ? nx.bias[o] : 0);
     }
   }
+}
+
+template <typename T, typename A, typename TO>
+__global__ __launch_bounds__(SAMPLE_BD) void mrs_sample(const uint16_t* __restrict__ lidx,
+                                                        const T* __restrict__ lval,
+                                                        const int32_t* __restrict__ lcnt,
+                                                        const typename Aug<T>::type* __restrict__ aug,
+                                                        const A* __restrict__ bias,
+                                                        A* __restrict__ y, TO* __restrict__ out,
+                                                        ListOut lo, ConvGeom geo, SampleArgs sa,
+                                                        NextLayer nx) {
+  sample_body<T, A, TO>(lidx, lval, lcnt, aug, bias, y, out, lo, geo, sa, nx, blockIdx.x);
 }
 
 }  // namespace cs

@@ -61,21 +61,22 @@ struct ScatterArgs {
   FastDiv fd_w;      // / input width
 };
 
+// The workgroup body for workgroup index blk (SCAT_BD threads).
 template <typename TO, int KW, int GPL, int M>
-__global__ __launch_bounds__(SCAT_BD) void mrs_scatter(const uint16_t* __restrict__ lidx,
-                                                       const int8_t* __restrict__ lval,
-                                                       const int32_t* __restrict__ lcnt,
-                                                       const uint16_t* __restrict__ aug,
-                                                       const int32_t* __restrict__ bias,
-                                                       int32_t* __restrict__ y,
-                                                       TO* __restrict__ out, ListOut lo,
-                                                       ConvGeom geo, ScatterArgs sc) {
+__device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
+                                             const int8_t* __restrict__ lval,
+                                             const int32_t* __restrict__ lcnt,
+                                             const uint16_t* __restrict__ aug,
+                                             const int32_t* __restrict__ bias,
+                                             int32_t* __restrict__ y, TO* __restrict__ out,
+                                             const ListOut& lo, const ConvGeom& geo,
+                                             const ScatterArgs& sc, uint32_t blk) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int H = geo.H, W = geo.W, C = geo.C, G = geo.G, n = geo.n, P = geo.P;
   const int Wo = geo.Wo, c_out = geo.c_out, cap = geo.cap, pool = geo.pool;
-  const uint32_t img = fdiv(blockIdx.x, sc.fd_bands);
-  const int band = (int)(blockIdx.x - img * (uint32_t)sc.bands);
+  const uint32_t img = fdiv(blk, sc.fd_bands);
+  const int band = (int)(blk - img * (uint32_t)sc.bands);
   const int oy0 = band * sc.BR;
   const int nrows = min(sc.BR, geo.Ho - oy0);
   const int iy0 = max(oy0 - P, 0);
@@ -287,6 +288,38 @@ __global__ __launch_bounds__(SCAT_BD) void mrs_scatter(const uint16_t* __restric
     }
     if (sc.k >= 0) kwta_row16<int32_t, TO, KPL>(v, c_out, sc.k, sc.shift, live, lo, out, row);
   }
+}
+
+template <typename TO, int KW, int GPL, int M>
+__global__ __launch_bounds__(SCAT_BD) void mrs_scatter(const uint16_t* __restrict__ lidx,
+                                                       const int8_t* __restrict__ lval,
+                                                       const int32_t* __restrict__ lcnt,
+                                                       const uint16_t* __restrict__ aug,
+                                                       const int32_t* __restrict__ bias,
+                                                       int32_t* __restrict__ y,
+                                                       TO* __restrict__ out, ListOut lo,
+                                                       ConvGeom geo, ScatterArgs sc) {
+  scatter_body<TO, KW, GPL, M>(lidx, lval, lcnt, aug, bias, y, out, lo, geo, sc, blockIdx.x);
+}
+
+// Two layers and a third in one launch, one workgroup per image: a convolution
+// whose band is the whole image writes its k-WTA lists (int8) to lo; after a
+// workgroup barrier (which orders the workgroup's global stores before its
+// loads) the same workgroup runs the next layer, a window over the whole
+// pooled map (one output vector per image), on those lists, with its own
+// k-WTA lists lo2 and the last linear layer nx on its winners.
+template <int KW, int GPL, int M>
+__global__ __launch_bounds__(SCAT_BD) void mrs_scatter_sample(
+    const uint16_t* __restrict__ lidx, const int8_t* __restrict__ lval,
+    const int32_t* __restrict__ lcnt, const uint16_t* __restrict__ aug,
+    const int32_t* __restrict__ bias, int32_t* __restrict__ y, ListOut lo, ConvGeom geo,
+    ScatterArgs sc, const uint16_t* __restrict__ aug2, const int32_t* __restrict__ bias2,
+    int32_t* __restrict__ y2, ListOut lo2, ConvGeom geo2, SampleArgs sa2, NextLayer nx) {
+  scatter_body<int8_t, KW, GPL, M>(lidx, lval, lcnt, aug, bias, y, nullptr, lo, geo, sc,
+                                   blockIdx.x);
+  __syncthreads();
+  sample_body<int8_t, int32_t, int8_t>(lo.idx, static_cast<const int8_t*>(lo.val), lo.cnt, aug2,
+                                       bias2, y2, nullptr, lo2, geo2, sa2, nx, blockIdx.x);
 }
 
 }  // namespace cs

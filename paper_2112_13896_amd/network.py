@@ -24,7 +24,9 @@ their indices"):
   * a layer without k-WTA writes its sums (cs_mrs_conv2d / cs_conv2d_dense);
   * the last layer, a linear layer without k-WTA on the int8 winners of a
     layer with one output vector per sample, runs in that layer's call
-    (cs_mrs_kwta_chain2: the winners feed it on chip) unless fuse_tail is off.
+    (cs_mrs_kwta_chain2: the winners feed it on chip) unless fuse_tail is off;
+    when that pair reads a conv layer's lists as a window over its whole
+    pooled map, the three run in the conv layer's call (cs_mrs_kwta_chain3).
 A linear layer that follows a conv layer reads the conv output's per-pixel
 lists as a convolution whose window is the whole h x w map: its slots
 (h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
@@ -63,6 +65,7 @@ class Plan:
     emit_lists: bool         # k-WTA writes lists for the next layer
     cap_out: int             # capacity of the emitted lists
     fuse_next: bool = False  # the next (last) layer runs in this layer's call
+    fuse_next2: bool = False  # the next two (last) layers run in this layer's call
 
 
 @dataclass
@@ -156,6 +159,17 @@ class Network:
                     not a.dense_kernel and len(a.out_shape) == 2 and sz.kind == "linear" and
                     sz.k is None and z.in_lists):
                 a.fuse_next = True
+        # a conv layer whose lists feed that pair as a window over its whole
+        # pooled map: the three run in one call (cs_mrs_kwta_chain3)
+        if self.fuse_tail and nl >= 3 and self.plans[nl - 2].fuse_next:
+            c, a = self.plans[nl - 3], self.plans[nl - 2]
+            sc = self.packed[nl - 3].spec
+            int8 = self.packed[nl - 3].aug.dtype == torch.int16
+            if (int8 and sc.k is not None and sc.shift is not None and c.emit_lists and
+                    not c.dense_kernel and len(c.out_shape) == 4 and a.in_lists and
+                    tuple(a.geo) == tuple(c.out_shape) and a.kh == c.out_shape[1] and
+                    a.kw == c.out_shape[2] and a.stride == 1 and a.pad == 0 and a.pool == 1):
+                c.fuse_next2 = True
 
     def make_buffers(self) -> Buffers:
         B = Buffers()
@@ -222,15 +236,28 @@ class Network:
                 calls.append((f"{s.name}.mrs", lambda: ops.conv2d_dense(
                     x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, out=acc)))
             return calls
-        if li > 0 and self.plans[li - 1].fuse_next:
-            return []                                   # run by the previous layer's call
+        if ((li > 0 and (self.plans[li - 1].fuse_next or self.plans[li - 1].fuse_next2)) or
+                (li > 1 and self.plans[li - 2].fuse_next2)):
+            return []                                   # run by an earlier layer's call
         if pl.in_lists:
             idx, lval, cnt = B.lists[li - 1]
         else:
             idx, lval, cnt = B.idx[li], B.lval[li], B.cnt[li]
             calls.append((f"{s.name}.compact", lambda: ops.compact_into(
                 x.reshape(b * h * w, c), idx, lval, cnt)))
-        if pl.fuse_next:
+        if pl.fuse_next2:
+            # one call: this layer with its k-WTA and lists, the next layer over
+            # them with its k-WTA, and the last layer on its winners
+            q, r = self.packed[li + 1], self.packed[li + 2]
+            sq = q.spec
+            calls.append((f"{s.name}.mrs_kwta+{sq.name}.mrs_kwta+{r.spec.name}.mrs",
+                          lambda: ops.mrs_kwta_chain3(
+                idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias,
+                pl.pool, k=s.k, shift=shift, aug2=q.aug, n2=sq.n, bias2=q.bias, k2=sq.k,
+                shift2=sq.shift, aug3=r.aug, n3=r.spec.n, bias3=r.bias,
+                keep_sums=self.keep_sums, y=acc4, lists=lists_out,
+                y2=B.acc[li + 1].reshape(b, -1), lists2=B.lists[li + 1], y3=B.acc[li + 2])))
+        elif pl.fuse_next:
             # one call: this layer with its k-WTA, then the last layer on its winners
             q = self.packed[li + 1]
             acc2 = B.acc[li + 1]

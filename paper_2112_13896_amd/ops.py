@@ -236,6 +236,64 @@ def mrs_kwta_chain2(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in
     return y, lists, y2
 
 
+def _list_buffers(rows: int, cap: int, device, lists=None):
+    if lists is None:
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=device),
+                 torch.empty((rows, cap), dtype=torch.int8, device=device),
+                 torch.empty((rows,), dtype=torch.int32, device=device))
+    oi, ov, oc = lists
+    if oi.dtype != torch.int16 or ov.dtype != torch.int8 or oc.dtype != torch.int32:
+        raise TypeError("list buffer dtypes do not match")
+    if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+        raise ValueError("list buffer shapes do not match the output")
+    return lists
+
+
+def mrs_kwta_chain3(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, aug,
+                    kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None,
+                    pool: int = 1, *, k: int, shift: int, aug2, n2: int, bias2=None, k2: int,
+                    shift2: int, aug3, n3: int, bias3=None, keep_sums: bool = True,
+                    y: torch.Tensor | None = None, cap: int | None = None, lists=None,
+                    y2: torch.Tensor | None = None, cap2: int | None = None, lists2=None,
+                    y3: torch.Tensor | None = None):
+    """An int8 conv layer with k-WTA and lists, a layer with k-WTA over its
+    whole pooled map, and a linear layer on the second one's winners
+    (cs_mrs_kwta_chain3).  aug2 packs [c_out2][hp*wp*c_out] weights in the
+    (y, x, channel) slot order of the first layer's NHWC output.  Returns
+    (y, lists, y2, lists2, y3)."""
+    if lval.dtype != torch.int8:
+        raise TypeError("mrs_kwta_chain3 takes int8 lists")
+    b, h, w, c_in = in_shape
+    pa, c_out = _aug(aug, lval.dtype, n)
+    pa2, c_out2 = _aug(aug2, torch.int8, n2)
+    pa3, c_out3 = _aug(aug3, torch.int8, n3)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    oshape = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    dev = lval.device
+    if y is None:
+        y = torch.empty(oshape, dtype=torch.int32, device=dev)
+    lists = _list_buffers(rows, list_capacity(k) if cap is None else cap, dev, lists)
+    if y2 is None:
+        y2 = torch.empty((b, c_out2), dtype=torch.int32, device=dev)
+    lists2 = _list_buffers(b, list_capacity(k2) if cap2 is None else cap2, dev, lists2)
+    if y3 is None:
+        y3 = torch.empty((b, c_out3), dtype=torch.int32, device=dev)
+    for t, nm, m in ((y2, "y2", c_out2), (y3, "y3", c_out3)):
+        if t.dtype != torch.int32 or t.numel() != b * m:
+            raise ValueError(f"{nm} does not match its layer's output")
+    oi, ov, oc = lists
+    oi2, ov2, oc2 = lists2
+    check("cs_mrs_kwta_chain3", lib().cs_mrs_kwta_chain3(
+        CS_I8, _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
+        b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n, _opt(bias, "bias"), pool,
+        _dev(y, "y"), 1 if keep_sums else 0, k, CS_I8, shift, _dev(oi, "oidx"), _dev(ov, "oval"),
+        _dev(oc, "ocnt"), oi.shape[1], pa2, c_out2, n2, _opt(bias2, "bias2"), _dev(y2, "y2"),
+        k2, shift2, _dev(oi2, "oidx2"), _dev(ov2, "oval2"), _dev(oc2, "ocnt2"), oi2.shape[1],
+        pa3, c_out3, n3, _opt(bias3, "bias3"), _dev(y3, "y3"), _stream()))
+    return y, lists, y2, lists2, y3
+
+
 def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: int, pad: int,
              c_out: int, n: int, pool: int = 1, k: int = -1) -> dict:
     """The launch plan the library picks for a layer (host only)."""

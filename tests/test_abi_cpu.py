@@ -362,6 +362,33 @@ def test_chain2_validation(L):
     assert call(shift=40) == CS_ERR_ARG
 
 
+def test_chain3_validation(L):
+    f = L.cs_mrs_kwta_chain3
+    ok = dict(xt=CS_I8, idx=FAKE, lval=FAKE, cnt=FAKE, cap=8, b=4, h=14, w=14, c_in=64, kh=5,
+              kw=5, stride=1, pad=0, aug=FAKE, c_out=64, n=16, bias=None, pool=2, y=FAKE,
+              keep_sums=0, k=8, ot=CS_I8, shift=9, oidx=FAKE, oval=FAKE, ocnt=FAKE, ocap=8,
+              aug2=FAKE, c_out2=1500, n2=20, bias2=None, y2=FAKE, k2=75, shift2=8, oidx2=FAKE,
+              oval2=FAKE, ocnt2=FAKE, ocap2=76, aug3=FAKE, c_out3=12, n3=1, bias3=None, y3=FAKE,
+              stream=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(*a.values())
+    assert call(xt=CS_F32) == CS_ERR_DTYPE
+    assert call(ot=CS_I32) == CS_ERR_DTYPE
+    for name in ("idx", "aug", "oidx", "aug2", "y2", "oidx2", "ocnt2", "aug3", "y3"):
+        assert call(**{name: None}) == CS_ERR_ARG, name
+    assert call(k=-1) == CS_ERR_ARG
+    assert call(shift2=32) == CS_ERR_ARG
+    assert call(keep_sums=2) == CS_ERR_ARG
+    assert call(k=9) == CS_ERR_SHAPE                # more winners than the first list holds
+    assert call(k2=80) == CS_ERR_SHAPE              # more winners than the second list holds
+    assert call(n2=7) == CS_ERR_SHAPE               # 7 does not divide 1500
+    assert call(n3=5) == CS_ERR_SHAPE               # 5 does not divide 12
+    assert call(ocap2=0) == CS_ERR_SHAPE
+
+
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, 8, 4, None, 1, FAKE, None]

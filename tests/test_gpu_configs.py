@@ -66,16 +66,19 @@ def test_int_config_bit_exact(cid):
 
 
 def test_tail_fusion_matches_two_launches():
-    """Config 2's last two layers (linear1 with k-WTA, then the output layer on
-    its winners) in one call (cs_mrs_kwta_chain2) and as two calls: the same
-    bits in every buffer, one launch fewer."""
+    """Config 2's last three layers (conv2 with k-WTA, linear1 with k-WTA over
+    conv2's whole map, the output layer on its winners) in one call
+    (cs_mrs_kwta_chain3) and as three calls: the same bits in every buffer,
+    two launches fewer."""
     cfg = CONFIGS[2]
     inp = generate(cfg)
     fused = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
     plain = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, fuse_tail=False)
     assert fused.plans[-2].fuse_next and not plain.plans[-2].fuse_next
+    assert fused.plans[-3].fuse_next2 and not plain.plans[-3].fuse_next2
     names_f, names_p = fused.kernel_names(), plain.kernel_names()
-    assert len(names_f) == len(names_p) - 1 and "linear1.mrs_kwta+output.mrs" in names_f
+    assert len(names_f) == len(names_p) - 2
+    assert "conv2.mrs_kwta+linear1.mrs_kwta+output.mrs" in names_f
     x = dev(inp["x"])
     fused.forward(x)
     plain.forward(x)
@@ -84,11 +87,14 @@ def test_tail_fusion_matches_two_launches():
         assert np.array_equal(host(fused.acc[li]), host(plain.acc[li])), f"layer {li} sums"
         assert np.array_equal(host(fused.dense_output(li)), host(plain.dense_output(li))), \
             f"layer {li} output"
-    # with the sums of linear1 not kept, the output layer's sums are unchanged
+    # without the intermediate sums kept, every layer's output is unchanged
     bench = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, keep_sums=False)
     bench.forward(x)
     torch.cuda.synchronize()
     assert np.array_equal(host(bench.acc[-1]), host(plain.acc[-1]))
+    for li in range(len(cfg.layers)):
+        assert np.array_equal(host(bench.dense_output(li)), host(plain.dense_output(li))), \
+            f"layer {li} output without sums"
 
 
 @pytest.mark.parametrize("cid", [3, 4])

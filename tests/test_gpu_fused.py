@@ -390,3 +390,59 @@ def test_dense_kwta_layer(case):
             S = S + np.abs(bias.astype(np.float64))
         assert_f32_close(y, ref, S, "dense sums")
         check_kwta_f32(y, out, ref, S, k)
+
+
+# ------------------------------------------------------------- three-layer tail
+# (b, h, w, c_in), nnz, kh, kw, pad, c_out, n, pool, k, shift, c_out2, n2, k2, shift2,
+# c_out3, n3, ties
+CHAIN3_CASES = [
+    # keyword-spotting shape at a small batch: one kernel
+    ((6, 14, 14, 64), 8, 5, 5, 0, 64, 16, 2, 8, 9, 1500, 20, 75, 8, 12, 1, False),
+    # 3x3 pad 1 without pool, 96 channels, ties everywhere: one kernel
+    ((3, 6, 7, 32), 5, 3, 3, 1, 96, 8, 1, 7, 0, 200, 8, 20, 0, 10, 2, True),
+    # an image wider than one band: the two-call fallback
+    ((2, 64, 64, 16), 3, 3, 3, 1, 32, 4, 2, 4, 6, 64, 4, 10, 4, 8, 1, False),
+]
+
+
+@pytest.mark.parametrize("case", CHAIN3_CASES, ids=[f"{c[0]}-{c[1]}x{c[2]}-to{c[10]}" for c in CHAIN3_CASES])
+def test_chain3_matches_separate_calls(case):
+    """cs_mrs_kwta_chain3 against cs_mrs_kwta_conv2d followed by
+    cs_mrs_kwta_chain2 on its lists: the same bits in every output."""
+    (shape, nnz, kh, kw, pad, c_out, n, pool, k, shift, c_out2, n2, k2, shift2, c_out3, n3,
+     ties) = case
+    r = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    b, h, w, c_in = shape
+    x = sparse_input(r, shape, nnz, "i8", low_range=ties)
+    ho, wo = h + 2 * pad - kh + 1, w + 2 * pad - kw + 1
+    hp, wp = ho // pool, wo // pool
+    W1 = weights(r, c_out, kh, kw, c_in, n, "i8", low_range=ties)
+    W2 = weights(r, c_out2, hp, wp, c_out, n2, "i8", low_range=ties)
+    W3 = weights(r, c_out3, 1, 1, c_out2, n3, "i8")
+    b1, b2, b3 = (dev(r.integers(-1000, 1001, size=m).astype(np.int32)) for m in (c_out, c_out2, c_out3))
+    a1, a2, a3 = (ops.aug_to_device(ops.pack(Wx.reshape(Wx.shape[0], -1), nx)[0])
+                  for Wx, nx in ((W1, n), (W2, n2), (W3, n3)))
+    idx, lv, cnt = ops.compact(dev(x).reshape(-1, c_in))
+    cap1, cap2 = ops.list_capacity(k), ops.list_capacity(k2)
+    got = ops.mrs_kwta_chain3(idx, lv, cnt, shape, a1, kh, kw, n, 1, pad, b1, pool, k=k,
+                              shift=shift, aug2=a2, n2=n2, bias2=b2, k2=k2, shift2=shift2,
+                              aug3=a3, n3=n3, bias3=b3, keep_sums=True, cap=cap1, cap2=cap2)
+    y, lists = ops.mrs_kwta_conv2d(idx, lv, cnt, shape, a1, kh, kw, n, 1, pad, b1, pool, k=k,
+                                   out_dtype=torch.int8, shift=shift, keep_sums=True, cap=cap1)
+    y2, lists2, y3 = ops.mrs_kwta_chain2(*lists, (b, hp, wp, c_out), a2, hp, wp, n2, 1, 0, b2, 1,
+                                         k=k2, shift=shift2, aug2=a3, n2=n3, bias2=b3,
+                                         keep_sums=True, cap=cap2)
+    torch.cuda.synchronize()
+    for nm, g, e in (("y", got[0], y), ("y2", got[2], y2), ("y3", got[4], y3)):
+        assert np.array_equal(host(g).reshape(-1), host(e).reshape(-1)), nm
+    for nm, g, e in (("lists", got[1], lists), ("lists2", got[3], lists2)):
+        gi, gv, gc = (host(t) for t in g)
+        ei, ev, ec = (host(t) for t in e)
+        assert np.array_equal(gc, ec), nm + " counts"
+        live = np.arange(gi.shape[1])[None, :] < ec[:, None]
+        assert np.array_equal(gi[live], ei[live]) and np.array_equal(gv[live], ev[live]), nm
+    # the sums of the first layer against the oracle, so that both sides are pinned
+    ref = o.conv2d_nhwc(x, W1, 1, pad, host(b1))
+    if pool == 2:
+        ref = o.maxpool2x2_nhwc(ref)
+    assert np.array_equal(host(got[0]).astype(np.int64), ref), "first layer sums"
