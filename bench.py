@@ -11,11 +11,15 @@ workgroup the last three are one kernel and the sums never reach HBM.  Inputs
 are resident in HBM when the timed region starts; the chain rotates among
 buffer sets (input + every intermediate) totalling more than 512 MiB, so a
 step does not find the previous step's data in the 256 MiB Infinity Cache.
-The passes over all buffer sets, one after another, are recorded once into a
-HIP graph (a serving loop's batches in one launch): the timed K steps are K //
-sets replays of it plus single-pass graphs for the rest, so the step time is
-the kernels' time, not Python's or the graph launch's overhead; the time with
-one graph launch per step is reported beside it.  Per-kernel durations (and the roofline of the dominant kernel) come
+The K timed passes (K <= 256; else one pass per buffer set) are recorded once
+into a HIP graph (a serving loop's batches in one launch), pass i on buffer set
+i mod sets, in two schedules: one after another, or each pass's first kernel
+on one stream and the rest on a second, so that the next batch's first kernel
+runs beside the current batch's later ones (a buffer set is written again only
+after the passes that read it).  The faster in a few warm-up replays is timed
+(`schedule`), so the step time is the kernels' time, not Python's or the graph
+launch's overhead; the same K passes with one graph launch each (no overlap)
+are timed after and reported beside it.  Per-kernel durations (and the roofline of the dominant kernel) come
 from graphs holding 20 launches of that one kernel, timed with HIP events on
 the replaying stream.
 
@@ -146,6 +150,34 @@ def layer_costs(net, bufs, cfg) -> dict:
                 "bytes": a["bytes"] + z["bytes"] - z["lists_in"],
                 "products": a["products"] + z["products"], "int": a["int"]}
     return costs
+
+
+def capture_passes(net, xs, sets, steps: int, overlap: bool):
+    """One graph of `steps` passes, pass i on buffer set i % len(sets)."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()                      # default priority
+    nsets = len(sets)
+    with torch.cuda.graph(g):
+        main = torch.cuda.current_stream()
+        for i in range(steps):
+            j = i % nsets
+            calls = [c for li in range(len(net.packed))
+                     for _, c in net.launches(li, xs[j] if li == 0 else None, sets[j])]
+            if not overlap:
+                for c in calls:
+                    c()
+                continue
+            if i > 0 and j == 0:
+                main.wait_stream(side)              # set 0 .. are written again
+            calls[0]()
+            if len(calls) > 1:
+                side.wait_stream(main)
+                with torch.cuda.stream(side):
+                    for c in calls[1:]:
+                        c()
+        main.wait_stream(side)
+    return g
 
 
 def dense_macs(cfg) -> int:
@@ -321,15 +353,28 @@ def main() -> int:
     # one HIP graph per buffer set: a step is one replay (every layer's kernels,
     # no per-launch host work)
     graphs = [net.capture(xs[j], sets[j]) for j in range(nsets)]
-    # and one graph of the passes over all the sets in turn
-    g_all = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_all):
-        for j in range(nsets):
-            net.forward(xs[j], sets[j])
+    # and one graph of the passes over all the sets in turn, two streams:
+    # a pass's first launch on the capture stream, the rest on a second
+    # stream after it, so that the next pass's first launch (another buffer
+    # set) can run beside the rest of this one
+    gsteps = args.steps if args.steps <= 256 else nsets
+    g_pipe = capture_passes(net, xs, sets, gsteps, overlap=True)
+    g_seq = capture_passes(net, xs, sets, gsteps, overlap=False)
     for i in range(args.warmup):
         graphs[i % nsets].replay()
-    g_all.replay()
-    torch.cuda.synchronize()
+    # the faster of the two schedules of the all-sets graph (a few replays each)
+    sched = {}
+    for name, g in (("overlapped", g_pipe), ("sequential", g_seq)):
+        g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        sched[name] = time.perf_counter() - t0
+    schedule = min(sched, key=sched.get)
+    g_all = g_pipe if schedule == "overlapped" else g_seq
+    log(f"bench: schedule {schedule} ({', '.join(f'{k} {v * 1e6 / (3 * gsteps):.1f} us' for k, v in sched.items())} per step)")
 
     # per-kernel durations: each launch recorded KREP times into a graph of its
     # own, replayed with HIP events on the replaying stream around it
@@ -356,10 +401,10 @@ def main() -> int:
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps // nsets):
+    for _ in range(args.steps // gsteps):
         g_all.replay()
-    for i in range(args.steps % nsets):
-        graphs[i].replay()
+    for i in range(args.steps % gsteps):
+        graphs[i % nsets].replay()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
@@ -392,6 +437,7 @@ def main() -> int:
         "config": {"workload": cfg.name, "batch": cfg.batch, "layers": [s.name for s in cfg.layers]},
         "dense_equiv_gmac_per_s": round(dense_macs(cfg) / (ms_step * 1e-3) / 1e9, 1),
         "ms_per_step_one_launch_per_step": round(ms_step_1, 4),
+        "schedule": schedule,
         "roofline": roof,
         "kernels": kernels,
     }

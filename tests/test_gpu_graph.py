@@ -54,3 +54,46 @@ def test_graph_replay_matches_eager(cid):
         net.forward(x2, side)
         scratch.mul_(1.0001).add_(rep)
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("cid,overlap", [(2, False), (2, True), (3, True), (5, True)])
+def test_multi_pass_graph_matches_eager(cid, overlap):
+    """The benchmark's graph of several passes over rotating buffer sets (seven
+    passes over three sets, so sets are written again inside one replay), in
+    the sequential and the two-stream schedule: after each replay every set
+    holds the eager pass's bits for its own input."""
+    from bench import capture_passes
+    cfg = CONFIGS[cid]
+    batch = min(cfg.batch, 16)
+    inp = generate(cfg, batch=batch)
+    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, batch, keep_sums=False)
+    nsets = 3
+    sets = [net.bufs] + [net.make_buffers() for _ in range(nsets - 1)]
+    # a different input per set: the first one and two scaled/rolled copies
+    xs = []
+    for j in range(nsets):
+        xj = np.roll(inp["x"], j, axis=0).copy()
+        xs.append(dev(xj))
+    want = []
+    for j in range(nsets):
+        net.forward(xs[j], sets[j])
+        want.append(snapshot(net, sets[j])[0])
+    for j in range(nsets):                               # scribble over every output
+        for a in sets[j].acc:
+            a.zero_()
+        for o in sets[j].out:
+            if o is not None:
+                o.zero_()
+        for lst in sets[j].lists:
+            if lst is not None:
+                for t in lst:
+                    t.fill_(-1)
+    g = capture_passes(net, xs, sets, 7, overlap=overlap)
+    for rep in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        for j in range(nsets):
+            got = snapshot(net, sets[j])[0]
+            for li in range(len(net.packed)):
+                assert np.array_equal(got[li], want[j][li]), f"replay {rep} set {j} layer {li}"
+        torch.zeros(1 << 20, device="cuda").add_(1)      # unrelated eager work between replays
