@@ -13,13 +13,15 @@ buffer sets (input + every intermediate) totalling more than 512 MiB, so a
 step does not find the previous step's data in the 256 MiB Infinity Cache.
 The K timed passes (K <= 256; else one pass per buffer set) are recorded once
 into a HIP graph (a serving loop's batches in one launch), pass i on buffer set
-i mod sets, in two schedules: one after another, or each pass's first kernel
+i mod sets, in three schedules: one after another; each pass's first kernel
 on one stream and the rest on a second, so that the next batch's first kernel
-runs beside the current batch's later ones (a buffer set is written again only
-after the passes that read it).  The faster in a few warm-up replays is timed
-(`schedule`), so the step time is the kernels' time, not Python's or the graph
-launch's overhead; the same K passes with one graph launch each (no overlap)
-are timed after and reported beside it.  Per-kernel durations (and the roofline of the dominant kernel) come
+runs beside the current batch's later ones; or whole passes on the two streams
+in turn, so that one batch's last workgroups and the next one's first overlap
+(a buffer set is written again only after the passes that read it).  The
+fastest in a few warm-up replays is timed (`schedule`), so the step time is
+the kernels' time, not Python's or the graph launch's overhead; the same K
+passes with one graph launch each (no overlap) are timed after and reported
+beside it.  Per-kernel durations (and the roofline of the dominant kernel) come
 from graphs holding 20 launches of that one kernel, timed with HIP events on
 the replaying stream.
 
@@ -143,6 +145,17 @@ def layer_costs(net, bufs, cfg) -> dict:
                 "bytes": c["bytes"] + a["bytes"] + z["bytes"] - z["lists_in"],
                 "products": c["products"] + a["products"] + z["products"], "int": c["int"]}
     for li, pl in enumerate(net.plans):
+        if pl.fuse_next3:
+            # the dense first layer and the three-layer tail: bytes of both;
+            # the products counted are the routed ones (VALU work), the first
+            # layer's dense multiply-adds run on the matrix cores
+            names = [net.packed[li + i].spec.name for i in range(4)]
+            d = costs[f"{names[0]}.dense_kwta"]
+            t = costs[f"{names[1]}.mrs_kwta+{names[2]}.mrs_kwta+{names[3]}.mrs"]
+            costs[f"{names[0]}.dense_kwta+{names[1]}.mrs_kwta+{names[2]}.mrs_kwta+{names[3]}.mrs"] = {
+                "bytes": d["bytes"] + t["bytes"], "products": t["products"], "int": t["int"],
+                "mfma_macs": d["products"]}
+    for li, pl in enumerate(net.plans):
         if pl.fuse_next:
             a = costs[f"{net.packed[li].spec.name}.mrs_kwta"]
             z = costs[f"{net.packed[li + 1].spec.name}.mrs"]
@@ -152,24 +165,36 @@ def layer_costs(net, bufs, cfg) -> dict:
     return costs
 
 
-def capture_passes(net, xs, sets, steps: int, overlap: bool):
-    """One graph of `steps` passes, pass i on buffer set i % len(sets)."""
+def capture_passes(net, xs, sets, steps: int, mode: str):
+    """One graph of `steps` passes, pass i on buffer set i % len(sets), in one
+    of three schedules: "sequential" (one stream), "overlapped" (a pass's
+    first launch on the capture stream, the rest after it on a second stream)
+    or "alternate" (whole passes on the two streams in turn).  Two passes in
+    flight at once always use different buffer sets: at each wrap of the sets
+    the two streams wait for each other."""
     import torch
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()                      # default priority
     nsets = len(sets)
     with torch.cuda.graph(g):
         main = torch.cuda.current_stream()
+        side.wait_stream(main)
         for i in range(steps):
             j = i % nsets
             calls = [c for li in range(len(net.packed))
                      for _, c in net.launches(li, xs[j] if li == 0 else None, sets[j])]
-            if not overlap:
+            if mode == "sequential":
                 for c in calls:
                     c()
                 continue
-            if i > 0 and j == 0:
-                main.wait_stream(side)              # set 0 .. are written again
+            if i > 0 and j == 0:                    # set 0 .. are written again
+                main.wait_stream(side)
+                side.wait_stream(main)
+            if mode == "alternate":
+                with torch.cuda.stream(main if i % 2 == 0 else side):
+                    for c in calls:
+                        c()
+                continue
             calls[0]()
             if len(calls) > 1:
                 side.wait_stream(main)
@@ -214,7 +239,8 @@ def roofline_for(name: str, cost: dict, ms: float) -> dict:
             return {"bound": "alu", "achieved": round(ach, 3), "peak": peak_ops,
                     "unit": "TOP/s" if cost["int"] else "TFLOP/s", "frac": round(ach / peak_ops, 4),
                     "traffic": None, "kernel": name, "algorithmic_bytes": cost["bytes"],
-                    "products": cost["products"], "hbm_gbs": round(gbs, 1)}
+                    "products": cost["products"], "hbm_gbs": round(gbs, 1),
+                    **({"mfma_macs": cost["mfma_macs"]} if "mfma_macs" in cost else {})}
     return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": name,
             "algorithmic_bytes": cost["bytes"], **({"products": cost["products"]} if "products" in cost else {})}
@@ -358,13 +384,13 @@ def main() -> int:
     # stream after it, so that the next pass's first launch (another buffer
     # set) can run beside the rest of this one
     gsteps = args.steps if args.steps <= 256 else nsets
-    g_pipe = capture_passes(net, xs, sets, gsteps, overlap=True)
-    g_seq = capture_passes(net, xs, sets, gsteps, overlap=False)
+    g_mode = {m: capture_passes(net, xs, sets, gsteps, m)
+              for m in ("sequential", "overlapped", "alternate")}
     for i in range(args.warmup):
         graphs[i % nsets].replay()
     # the faster of the two schedules of the all-sets graph (a few replays each)
     sched = {}
-    for name, g in (("overlapped", g_pipe), ("sequential", g_seq)):
+    for name, g in g_mode.items():
         g.replay()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -373,7 +399,7 @@ def main() -> int:
         torch.cuda.synchronize()
         sched[name] = time.perf_counter() - t0
     schedule = min(sched, key=sched.get)
-    g_all = g_pipe if schedule == "overlapped" else g_seq
+    g_all = g_mode[schedule]
     log(f"bench: schedule {schedule} ({', '.join(f'{k} {v * 1e6 / (3 * gsteps):.1f} us' for k, v in sched.items())} per step)")
 
     # per-kernel durations: each launch recorded KREP times into a graph of its

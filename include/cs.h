@@ -299,6 +299,39 @@ int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const
                        int n3, const void* bias3, void* y3, void* stream);
 
 /*
+ * cs_conv2d_dense_kwta_chain3 - a whole chain shaped like the keyword-spotting
+ * network of Section 4: the dense-input first layer (as cs_conv2d_dense_kwta,
+ * int8, list output), then the three layers of cs_mrs_kwta_chain3 on its lists
+ * (input shape b x hp x wp x c_out, where hp x wp is the first layer's pooled
+ * map).  The result is that of those two calls.  When the first layer's
+ * matrix-core kernel can take a whole image per workgroup and the three-layer
+ * tail runs in one kernel (cs_mrs_kwta_chain3's condition), all four layers
+ * run in one kernel, one workgroup per image, the phases separated by
+ * workgroup barriers and the lists between them read back from L2; otherwise
+ * the two calls run back to back on `stream`.  DEVICE memory.
+ *
+ *  xt .. ocap   the first layer as cs_conv2d_dense_kwta (xt == ot == CS_I8,
+ *          list output oidx/oval/ocnt/ocap, no dense out).
+ *  kh2 .. ocap2   the second layer (a conv over the first one's lists) as the
+ *          first layer of cs_mrs_kwta_chain3: window, stride, padding, packed
+ *          table, c_out2, n2, bias, pool, sums y2, k-WTA k2 / shift2 and lists.
+ *  aug3 .. ocap3   the third layer (window = the second one's whole pooled map)
+ *          as cs_mrs_kwta_chain3's second.
+ *  aug4, c_out4, n4, bias4, y4   the last linear layer, as its third.
+ *  keep_sums applies to the first three layers' sums y, y2, y3.
+ *  Errors: as cs_conv2d_dense_kwta and cs_mrs_kwta_chain3.
+ */
+int cs_conv2d_dense_kwta_chain3(
+    cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+    const void* aug, int c_out, int n, const void* bias, int pool, void* y, int keep_sums, int k,
+    cs_dtype ot, int shift, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap, int kh2, int kw2,
+    int stride2, int pad2, const void* aug2, int c_out2, int n2, const void* bias2, int pool2,
+    void* y2, int k2, int shift2, uint16_t* oidx2, void* oval2, int32_t* ocnt2, int ocap2,
+    const void* aug3, int c_out3, int n3, const void* bias3, void* y3, int k3, int shift3,
+    uint16_t* oidx3, void* oval3, int32_t* ocnt3, int ocap3, const void* aug4, int c_out4, int n4,
+    const void* bias4, void* y4, void* stream);
+
+/*
  * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
  * Route, Sum with dense activations; Section 4 runs the first layer of the
  * keyword-spotting network this way because its input is dense).  DEVICE

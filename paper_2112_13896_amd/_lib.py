@@ -39,6 +39,12 @@ SIGNATURES = {
     "cs_mrs_kwta_chain2": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
                                 _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp,
                                 _vp, _vp]),
+    "cs_conv2d_dense_kwta_chain3": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i,
+                                         _vp, _i, _i, _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _i,
+                                         _i, _i, _i, _i, _vp, _i, _i, _vp, _i, _vp, _i, _i,
+                                         _vp, _vp, _vp, _i,
+                                         _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i,
+                                         _vp, _i, _i, _vp, _vp, _vp]),
     "cs_mrs_kwta_chain3": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
                                 _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _i,
                                 _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i,

@@ -55,19 +55,21 @@ struct DenseArgs {
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 
-template <int POOL, typename TO>
-__global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __restrict__ x,
-                                                       const uint16_t* __restrict__ aug,
-                                                       const int32_t* __restrict__ bias,
-                                                       int32_t* __restrict__ y,
-                                                       TO* __restrict__ out, ListOut lo,
-                                                       ConvGeom geo, DenseArgs da) {
+// The workgroup body for workgroup index blk, BD (>= 512) threads.
+template <int POOL, typename TO, int BD>
+__device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
+                                           const uint16_t* __restrict__ aug,
+                                           const int32_t* __restrict__ bias,
+                                           int32_t* __restrict__ y, TO* __restrict__ out,
+                                           const ListOut& lo, const ConvGeom& geo,
+                                           const DenseArgs& da, uint32_t blk) {
+  static_assert(BD >= 512 && BD % 64 == 0, "the weight staging takes 512 threads");
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int Hp = geo.Ho / POOL, Wp = geo.Wo / POOL;
   const int C = geo.C, W = geo.W;
-  const uint32_t img = fdiv(blockIdx.x, da.fd_timg);
-  const int pr0 = (int)(blockIdx.x - img * (uint32_t)da.tiles_img) * da.TPR;
+  const uint32_t img = fdiv(blk, da.fd_timg);
+  const int pr0 = (int)(blk - img * (uint32_t)da.tiles_img) * da.TPR;
   const int npr = min(da.TPR, Hp - pr0);
   const int nitems = npr * Wp;
   const int64_t item0 = ((int64_t)img * Hp + pr0) * Wp;
@@ -93,8 +95,8 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) bch[nt] = bias ? bias[16 * nt + col] : 0;
   {
-    static_assert(DENSE_BD == 64 * 8, "one thread per (channel, 4 slots)");
-    const int wch = tid >> 3, wk0 = (tid & 7) * 4;
+    // threads 0 .. 511: one per (channel, 4 slots)
+    const int wch = (tid & 511) >> 3, wk0 = (tid & 7) * 4;
     uint32_t wb4[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -107,25 +109,25 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       const uint4* src = reinterpret_cast<const uint4*>(ximg + (int64_t)iy0 * W * C);
       uint4* dst = reinterpret_cast<uint4*>(rows);
       const int n16 = nbytes / 16;                         // >= 1
-      for (int b0 = 0; b0 < n16; b0 += DENSE_BD * 2) {
+      for (int b0 = 0; b0 < n16; b0 += BD * 2) {
         uint4 v[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int e = b0 + u * DENSE_BD + tid;
+          const int e = b0 + u * BD + tid;
           v[u] = src[e < n16 ? e : n16 - 1];               // in range: no branch
         }
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int e = b0 + u * DENSE_BD + tid;
+          const int e = b0 + u * BD + tid;
           if (e < n16) dst[e] = v[u];
         }
       }
     } else
-    for (int b0 = 0; b0 < nbytes; b0 += DENSE_BD * DENSE_STAGE) {
+    for (int b0 = 0; b0 < nbytes; b0 += BD * DENSE_STAGE) {
       int8_t v[DENSE_STAGE];
 #pragma unroll
       for (int u = 0; u < DENSE_STAGE; ++u) {
-        const int e = b0 + u * DENSE_BD + tid;
+        const int e = b0 + u * BD + tid;
         const int r = (int)fdiv((uint32_t)e, da.fd_rowb);
         const int cb = e - r * rowb;
         const int px = (int)fdiv((uint32_t)cb, da.fd_c);
@@ -136,14 +138,14 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       }
 #pragma unroll
       for (int u = 0; u < DENSE_STAGE; ++u) {
-        const int e = b0 + u * DENSE_BD + tid;
+        const int e = b0 + u * BD + tid;
         if (e < nbytes) rows[e] = v[u];
       }
     }
     uint32_t w4 = 0u;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w4 |= (wk0 + i < da.R ? wb4[i] & 0xFFu : 0u) << (8 * i);
-    reinterpret_cast<uint32_t*>(wt)[tid] = w4;               // wt + wch * 32 + wk0
+    if (tid < 512) reinterpret_cast<uint32_t*>(wt)[tid] = w4;   // wt + wch * 32 + wk0
     if (tid < 32) {
       // slot kk = (ky * KW + kx) * C + c: byte offset from a window's corner
       const int kk = tid;
@@ -172,7 +174,7 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
   const int ostride = da.ostride;
   constexpr int IPM = 16 / (POOL * POOL);                  // items per M tile
   const int mtiles = (nitems + IPM - 1) / IPM;
-  for (int mt = wv; mt < mtiles; mt += DENSE_BD / 64) {
+  for (int mt = wv; mt < mtiles; mt += BD / 64) {
     // this lane's im2col row: item and sub-pixel (past the tile's last item
     // the last item is gathered again; its results are not stored)
     const int r = lane & 15;
@@ -222,7 +224,7 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
   const int c_out = 64;
   if (da.write_sums) {
     const int tot = nitems * c_out;
-    for (int e = tid; e < tot; e += DENSE_BD) {
+    for (int e = tid; e < tot; e += BD) {
       const int it = (int)fdiv((uint32_t)e, da.fd_cout);
       y[item0 * c_out + e] = otile[it * ostride + (e - it * c_out)];
     }
@@ -235,15 +237,15 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
     TO* tl_val = reinterpret_cast<TO*>(smem + da.off_lval);
     switch (da.kmode) {
       case 1:
-        kwta_quad_items<int32_t, TO, 8, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
+        kwta_quad_items<int32_t, TO, 8, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
                                         tl_val, lo.cap, lo.cnt);
         break;
       case 2:
-        kwta_quad_items<int32_t, TO, 16, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 16, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
       default:
-        kwta_quad_items<int32_t, TO, 32, DENSE_BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 32, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
     }
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
     if (lo.idx) {
       using OV = typename ChunkVal<TO>::type;
       const int cq = lo.cap >> 2;
-      for (int e = tid; e < nitems * cq; e += DENSE_BD) {
+      for (int e = tid; e < nitems * cq; e += BD) {
         const int it = (int)fdiv((uint32_t)e, da.fd_ochunks);
         const int j = e - it * cq;
         const int64_t gofs = (item0 + it) * lo.cap + 4 * j;
@@ -261,7 +263,7 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       }
     } else {
       const bool none = da.k == 0;
-      for (int e = tid; e < nitems * c_out; e += DENSE_BD) {
+      for (int e = tid; e < nitems * c_out; e += BD) {
         const int it = (int)fdiv((uint32_t)e, da.fd_cout);
         const int ch = e - it * c_out;
         const int32_t a = otile[it * ostride + ch];
@@ -272,6 +274,16 @@ __global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __rest
       }
     }
   }
+}
+
+template <int POOL, typename TO>
+__global__ __launch_bounds__(DENSE_BD) void conv_dense_mfma(const int8_t* __restrict__ x,
+                                                       const uint16_t* __restrict__ aug,
+                                                       const int32_t* __restrict__ bias,
+                                                       int32_t* __restrict__ y,
+                                                       TO* __restrict__ out, ListOut lo,
+                                                       ConvGeom geo, DenseArgs da) {
+  dense_body<POOL, TO, DENSE_BD>(x, aug, bias, y, out, lo, geo, da, blockIdx.x);
 }
 
 }  // namespace cs

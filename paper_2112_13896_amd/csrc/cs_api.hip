@@ -13,6 +13,7 @@
 #include "conv_dense_mfma.h"
 #include "cs.h"
 #include "kwta_kernels.h"
+#include "mrs_chain.h"
 #include "mrs_fused.h"
 #include "mrs_reorder.h"
 #include "mrs_kernels.h"
@@ -1182,6 +1183,57 @@ int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, i
   return launch_status();
 }
 
+// LDS layout and arguments of the first-layer matrix-core kernel for
+// workgroups of tpr pooled rows (fewer while the layout exceeds budget); the
+// layer is int8, n == 1, c_out == 64, kh*kw*c_in <= 32, k <= 32 (checked by
+// the callers).  ocap: list capacity, 0 for dense output.
+bool dense_plan(const cs::ConvGeom& geo, const void* x, int w, int pad, int k, int shift,
+                int keep_sums, int ocap, int osz, int tpr, size_t budget, cs::DenseArgs* pda,
+                size_t* shmem) {
+  const int pool = geo.pool, Hp = geo.Ho / pool, Wp = geo.Wo / pool;
+  const int c_in = geo.C, kh = geo.KH, kw = geo.KW, stride = geo.S;
+  const bool lists = ocap > 0;
+  cs::DenseArgs& da = *pda;
+  da = cs::DenseArgs{};
+  for (; tpr >= 1; --tpr) {
+    const int rows_in = (tpr * pool - 1) * stride + kh;
+    const size_t items_t = (size_t)tpr * Wp;
+    size_t o = round16((size_t)rows_in * (w + 2 * pad) * c_in);   // zero-padded rows
+    da.off_w = (uint32_t)o;
+    o += 64 * 32 + 32 * 4;                              // weights [64][32] bytes, slot offsets
+    da.off_out = (uint32_t)o;
+    o += round16(items_t * 65 * 4);
+    da.off_sel = (uint32_t)o;
+    o += round16(items_t * 8);
+    da.off_lidx = (uint32_t)o;
+    o += lists ? round16(items_t * ocap * 2) : 0;
+    da.off_lval = (uint32_t)o;
+    o += lists ? round16(items_t * ocap * osz) : 0;
+    if (o <= budget) {
+      *shmem = o;
+      break;
+    }
+  }
+  if (tpr < 1) return false;
+  da.TPR = tpr;
+  da.tiles_img = (Hp + tpr - 1) / tpr;
+  da.R = kh * kw * c_in;
+  da.k = k;
+  da.shift = shift;
+  da.kmode = k <= 8 ? 1 : (k <= 16 ? 2 : 3);
+  da.write_sums = keep_sums;
+  da.ostride = 65;
+  da.fd_wp = cs::make_fastdiv((uint32_t)Wp);
+  da.fd_timg = cs::make_fastdiv((uint32_t)da.tiles_img);
+  da.fd_cout = cs::make_fastdiv(64u);
+  da.fd_ochunks = cs::make_fastdiv((uint32_t)(lists ? ocap / 4 : 1));
+  da.fd_rowb = cs::make_fastdiv((uint32_t)((w + 2 * pad) * c_in));
+  da.vec_rows = pad == 0 && (w * c_in) % 16 == 0 && aligned(x, 16) ? 1 : 0;
+  da.fd_c = cs::make_fastdiv((uint32_t)c_in);
+  da.fd_kw = cs::make_fastdiv((uint32_t)kw);
+  return true;
+}
+
 int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
                          int stride, int pad, const void* aug, int c_out, int n, const void* bias,
                          int pool, void* y, int keep_sums, int k, cs_dtype ot, int shift, void* out,
@@ -1211,45 +1263,10 @@ int cs_conv2d_dense_kwta(cs_dtype xt, const void* x, int b, int h, int w, int c_
     // matrix-core kernel: pooled rows per workgroup for about 512 workgroups
     int tiles = (int)((512 + b - 1) / b);
     tiles = tiles < 1 ? 1 : (tiles > Hp ? Hp : tiles);
-    int tpr = (Hp + tiles - 1) / tiles;
-    size_t shmem = 0;
     cs::DenseArgs da{};
-    for (; tpr >= 1; --tpr) {
-      const int rows_in = (tpr * pool - 1) * stride + kh;
-      const size_t items_t = (size_t)tpr * Wp;
-      size_t o = round16((size_t)rows_in * (w + 2 * pad) * c_in);   // zero-padded rows
-      da.off_w = (uint32_t)o;
-      o += 64 * 32 + 32 * 4;                              // weights [64][32] bytes, slot offsets
-      da.off_out = (uint32_t)o;
-      o += round16(items_t * 65 * 4);
-      da.off_sel = (uint32_t)o;
-      o += round16(items_t * 8);
-      da.off_lidx = (uint32_t)o;
-      o += lists ? round16(items_t * ocap * 2) : 0;
-      da.off_lval = (uint32_t)o;
-      o += lists ? round16(items_t * ocap * osz) : 0;
-      if (o <= kFusedLds) {
-        shmem = o;
-        break;
-      }
-    }
-    if (tpr >= 1) {
-      da.TPR = tpr;
-      da.tiles_img = (Hp + tpr - 1) / tpr;
-      da.R = R;
-      da.k = k;
-      da.shift = shift;
-      da.kmode = k <= 8 ? 1 : (k <= 16 ? 2 : 3);
-      da.write_sums = keep_sums;
-      da.ostride = 65;
-      da.fd_wp = cs::make_fastdiv((uint32_t)Wp);
-      da.fd_timg = cs::make_fastdiv((uint32_t)da.tiles_img);
-      da.fd_cout = cs::make_fastdiv(64u);
-      da.fd_ochunks = cs::make_fastdiv((uint32_t)(lists ? ocap / 4 : 1));
-      da.fd_rowb = cs::make_fastdiv((uint32_t)((w + 2 * pad) * c_in));
-      da.vec_rows = pad == 0 && (w * c_in) % 16 == 0 && aligned(x, 16) ? 1 : 0;
-      da.fd_c = cs::make_fastdiv((uint32_t)c_in);
-      da.fd_kw = cs::make_fastdiv((uint32_t)kw);
+    size_t shmem = 0;
+    if (dense_plan(geo, x, w, pad, k, shift, keep_sums, lists ? ocap : 0, osz,
+                   (Hp + tiles - 1) / tiles, kFusedLds, &da, &shmem)) {
       const int64_t nb = (int64_t)b * da.tiles_img;
       if (nb < INT32_MAX) {
         const dim3 grid((unsigned)nb), block(cs::DENSE_BD);
@@ -1546,4 +1563,110 @@ int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const
   return cs_mrs_kwta_chain2(xt, oidx, oval, ocnt, ocap, b, hp, wp, c_out, hp, wp, 1, 0, aug2,
                             c_out2, n2, bias2, 1, y2, keep_sums, k2, ot, shift2, oidx2, oval2,
                             ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, stream);
+}
+
+template <int POOL, int KW>
+void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const SamplePlan& sp,
+                        size_t shmem, hipStream_t s, const void* x, const void* aug0,
+                        const void* bias0, void* y0, const cs::ListOut& lo0,
+                        const cs::ConvGeom& geo0, const void* aug, const void* bias, void* y,
+                        const cs::ListOut& lo, const cs::ConvGeom& geo, const void* aug2,
+                        const void* bias2, void* y2, const cs::ListOut& lo2,
+                        const cs::ConvGeom& geo2, const cs::NextLayer& nx) {
+  hipLaunchKernelGGL((cs::dense_scatter_sample<POOL, KW>), dim3((unsigned)geo0.B),
+                     dim3(cs::SCAT_BD), shmem, s, static_cast<const int8_t*>(x),
+                     static_cast<const uint16_t*>(aug0), static_cast<const int32_t*>(bias0),
+                     static_cast<int32_t*>(y0), lo0, geo0, da, static_cast<const uint16_t*>(aug),
+                     static_cast<const int32_t*>(bias), static_cast<int32_t*>(y), lo, geo, scp.sc,
+                     static_cast<const uint16_t*>(aug2), static_cast<const int32_t*>(bias2),
+                     static_cast<int32_t*>(y2), lo2, geo2, sp.sa, nx);
+}
+
+int cs_conv2d_dense_kwta_chain3(
+    cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw, int stride, int pad,
+    const void* aug, int c_out, int n, const void* bias, int pool, void* y, int keep_sums, int k,
+    cs_dtype ot, int shift, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap, int kh2, int kw2,
+    int stride2, int pad2, const void* aug2, int c_out2, int n2, const void* bias2, int pool2,
+    void* y2, int k2, int shift2, uint16_t* oidx2, void* oval2, int32_t* ocnt2, int ocap2,
+    const void* aug3, int c_out3, int n3, const void* bias3, void* y3, int k3, int shift3,
+    uint16_t* oidx3, void* oval3, int32_t* ocnt3, int ocap3, const void* aug4, int c_out4, int n4,
+    const void* bias4, void* y4, void* stream) {
+  if (xt != CS_I8 || ot != CS_I8) return CS_ERR_DTYPE;
+  if (!x || !aug || !y || !oidx || !oval || !ocnt) return CS_ERR_ARG;
+  if (!aug2 || !y2 || !oidx2 || !oval2 || !ocnt2 || !aug3 || !y3 || !oidx3 || !oval3 || !ocnt3 ||
+      !aug4 || !y4)
+    return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0 || shift < 0 || shift > 31 || k2 < 0 ||
+      shift2 < 0 || shift2 > 31 || k3 < 0 || shift3 < 0 || shift3 > 31)
+    return CS_ERR_ARG;
+  if (ocap < 1 || ocap2 < 1 || ocap3 < 1 || c_out2 < 1 || n2 < 1 || c_out3 < 1 || n3 < 1 ||
+      c_out4 < 1 || n4 < 1)
+    return CS_ERR_SHAPE;
+  cs::ConvGeom geo0;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo0);
+  if (st != CS_OK) return st;
+  if (k > c_out || ocap < k) return CS_ERR_SHAPE;
+  const int R = kh * kw * c_in;
+  if (n != 1 || c_out != 64 || R > 32) return CS_ERR_SHAPE;
+  const int hp0 = geo0.Ho / pool, wp0 = geo0.Wo / pool;
+  cs::ConvGeom geo;
+  st = conv_geometry(b, hp0, wp0, c_out, kh2, kw2, stride2, pad2, c_out2, n2, pool2, &geo);
+  if (st != CS_OK) return st;
+  if (k2 > c_out2 || c_out2 > CS_MAX_KWTA_ROW || ocap2 < k2) return CS_ERR_SHAPE;
+  const int hp = geo.Ho / pool2, wp = geo.Wo / pool2;
+  cs::ConvGeom geo2;
+  st = conv_geometry(b, hp, wp, c_out2, hp, wp, 1, 0, c_out3, n3, 1, &geo2);
+  if (st != CS_OK) return st;
+  if (k3 > c_out3 || c_out3 > CS_MAX_KWTA_ROW || ocap3 < k3) return CS_ERR_SHAPE;
+  if (n4 > CS_MAX_N || c_out4 % n4 != 0) return CS_ERR_SHAPE;
+  geo.cap = ocap;
+  geo2.cap = ocap2;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  // one kernel: each phase one workgroup per image (the first layer's tile
+  // and the second's band are the whole image), within one compute unit's LDS
+  const bool lists_ok = ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, 4);
+  cs::DenseArgs da{};
+  size_t sh0 = 0;
+  ScatterPlan scp;
+  SamplePlan sp;
+  if (k <= 32 && lists_ok && aligned(aug, 16) && (pool == 1 || pool == 2) &&
+      (int64_t)b * hp0 * wp0 * 64 < INT32_MAX &&
+      dense_plan(geo0, x, w, pad, k, shift, keep_sums, ocap, 1, hp0, kCuLds, &da, &sh0) &&
+      da.tiles_img == 1 && !sample_plan(geo, xt, k2, shift2, keep_sums, &sp) &&
+      scatter_plan(geo, xt, aug2, k2, shift2, keep_sums, &scp) && scp.sc.bands == 1 &&
+      scp.blocks == b && scp.gpl == 2 && scp.m == 1 &&
+      sample_plan(geo2, xt, k3, shift3, keep_sums, &sp)) {
+    const cs::NextLayer nx{static_cast<const uint16_t*>(aug4), static_cast<const int32_t*>(bias4),
+                           static_cast<int32_t*>(y4), c_out4 / n4, n4, c_out4,
+                           (uint32_t)round16(sp.shmem)};
+    const size_t sh2 = (size_t)nx.off_acc + round16((size_t)c_out4 * 4);
+    const size_t shmem = std::max(sh0, std::max(scp.shmem, sh2));
+    if (shmem <= kCuLds) {
+      const cs::ListOut lo0{oidx, oval, ocnt, ocap};
+      const cs::ListOut lo{oidx2, oval2, ocnt2, ocap2};
+      const cs::ListOut lo2{oidx3, oval3, ocnt3, ocap3};
+#define CS_DC(P_, K_)                                                                          \
+  launch_dense_chain<P_, K_>(da, scp, sp, shmem, s, x, aug, bias, y, lo0, geo0, aug2, bias2, y2, \
+                             lo, geo, aug3, bias3, y3, lo2, geo2, nx)
+      if (pool == 2) {
+        if (geo.KW == 3) CS_DC(2, 3);
+        else if (geo.KW == 5) CS_DC(2, 5);
+        else CS_DC(2, 7);
+      } else {
+        if (geo.KW == 3) CS_DC(1, 3);
+        else if (geo.KW == 5) CS_DC(1, 5);
+        else CS_DC(1, 7);
+      }
+#undef CS_DC
+      return launch_status();
+    }
+  }
+  // otherwise: the first layer, then the three-layer tail on its lists
+  st = cs_conv2d_dense_kwta(xt, x, b, h, w, c_in, kh, kw, stride, pad, aug, c_out, n, bias, pool, y,
+                            keep_sums, k, ot, shift, nullptr, oidx, oval, ocnt, ocap, stream);
+  if (st != CS_OK) return st;
+  return cs_mrs_kwta_chain3(xt, oidx, oval, ocnt, ocap, b, hp0, wp0, c_out, kh2, kw2, stride2, pad2,
+                            aug2, c_out2, n2, bias2, pool2, y2, keep_sums, k2, ot, shift2, oidx2,
+                            oval2, ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, k3, shift3, oidx3,
+                            oval3, ocnt3, ocap3, aug4, c_out4, n4, bias4, y4, stream);
 }

@@ -1,0 +1,41 @@
+// A whole keyword-spotting-shaped chain in one launch, one workgroup per
+// image (Figure 10: every layer's winners go on with their indices; Section
+// 4: the first layer runs sparse-dense on the dense input):
+//  1. the dense-input first layer on the matrix cores (dense_body: conv, 2x2
+//     pool, k-WTA, requantisation) over the whole image, its lists written;
+//  2. after a workgroup barrier, the input-stationary layer (scatter_body) on
+//     those lists, its k-WTA lists written;
+//  3. after another barrier, the layer whose window is the whole pooled map
+//     (sample_body) on them, with the last linear layer on its winners.
+// The barriers' workgroup-scope release/acquire order each phase's global
+// stores before the next phase's loads; the lists come back from L2 of the
+// same compute unit.  Each phase lays out the dynamic LDS its own way from
+// offset 0 (the launch reserves the largest).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "conv_dense_mfma.h"
+#include "mrs_sample.h"
+#include "mrs_scatter.h"
+
+namespace cs {
+
+template <int POOL, int KW>
+__global__ __launch_bounds__(SCAT_BD) void dense_scatter_sample(
+    const int8_t* __restrict__ x, const uint16_t* __restrict__ aug0,
+    const int32_t* __restrict__ bias0, int32_t* __restrict__ y0, ListOut lo0, ConvGeom geo0,
+    DenseArgs da, const uint16_t* __restrict__ aug, const int32_t* __restrict__ bias,
+    int32_t* __restrict__ y, ListOut lo, ConvGeom geo, ScatterArgs sc,
+    const uint16_t* __restrict__ aug2, const int32_t* __restrict__ bias2,
+    int32_t* __restrict__ y2, ListOut lo2, ConvGeom geo2, SampleArgs sa2, NextLayer nx) {
+  dense_body<POOL, int8_t, SCAT_BD>(x, aug0, bias0, y0, nullptr, lo0, geo0, da, blockIdx.x);
+  __syncthreads();
+  scatter_body<int8_t, KW, 2, 1>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt, aug, bias,
+                                 y, nullptr, lo, geo, sc, blockIdx.x);
+  __syncthreads();
+  sample_body<int8_t, int32_t, int8_t>(lo.idx, static_cast<const int8_t*>(lo.val), lo.cnt, aug2,
+                                       bias2, y2, nullptr, lo2, geo2, sa2, nx, blockIdx.x);
+}
+
+}  // namespace cs

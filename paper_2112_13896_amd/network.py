@@ -26,7 +26,9 @@ their indices"):
     layer with one output vector per sample, runs in that layer's call
     (cs_mrs_kwta_chain2: the winners feed it on chip) unless fuse_tail is off;
     when that pair reads a conv layer's lists as a window over its whole
-    pooled map, the three run in the conv layer's call (cs_mrs_kwta_chain3).
+    pooled map, the three run in the conv layer's call (cs_mrs_kwta_chain3),
+    and when that conv layer reads a dense-input first layer's lists, all
+    four run in the first layer's call (cs_conv2d_dense_kwta_chain3).
 A linear layer that follows a conv layer reads the conv output's per-pixel
 lists as a convolution whose window is the whole h x w map: its slots
 (h, w, c) in NHWC flatten order are exactly the window's taps-major slots.
@@ -66,6 +68,7 @@ class Plan:
     cap_out: int             # capacity of the emitted lists
     fuse_next: bool = False  # the next (last) layer runs in this layer's call
     fuse_next2: bool = False  # the next two (last) layers run in this layer's call
+    fuse_next3: bool = False  # the next three (last) layers run in this layer's call
 
 
 @dataclass
@@ -170,6 +173,15 @@ class Network:
                     tuple(a.geo) == tuple(c.out_shape) and a.kh == c.out_shape[1] and
                     a.kw == c.out_shape[2] and a.stride == 1 and a.pad == 0 and a.pool == 1):
                 c.fuse_next2 = True
+        # a dense-input first layer whose lists feed those three: all four in
+        # one call (cs_conv2d_dense_kwta_chain3)
+        if self.fuse_tail and nl == 4 and self.plans[1].fuse_next2:
+            d = self.plans[0]
+            sd = self.packed[0].spec
+            int8 = self.packed[0].aug.dtype == torch.int16
+            if (int8 and d.dense_kernel and sd.k is not None and sd.shift is not None and
+                    d.emit_lists and self.plans[1].in_lists):
+                d.fuse_next3 = True
 
     def make_buffers(self) -> Buffers:
         B = Buffers()
@@ -224,6 +236,21 @@ class Network:
         lists_out = B.lists[li] if pl.emit_lists else None
         out = None if pl.emit_lists else B.out[li]
         calls = []
+        if pl.dense_kernel and pl.fuse_next3:
+            # one call: this layer and the three after it on its lists
+            q, r, t = self.packed[li + 1], self.packed[li + 2], self.packed[li + 3]
+            pq = self.plans[li + 1]
+            bq = pq.geo[0]
+            calls.append((f"{s.name}.dense_kwta+{q.spec.name}.mrs_kwta+{r.spec.name}.mrs_kwta+"
+                          f"{t.spec.name}.mrs", lambda: ops.conv2d_dense_kwta_chain3(
+                x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, k=s.k,
+                shift=shift, aug2=q.aug, kh2=pq.kh, kw2=pq.kw, n2=q.spec.n, stride2=pq.stride,
+                pad2=pq.pad, bias2=q.bias, pool2=pq.pool, k2=q.spec.k, shift2=q.spec.shift,
+                aug3=r.aug, n3=r.spec.n, bias3=r.bias, k3=r.spec.k, shift3=r.spec.shift,
+                aug4=t.aug, n4=t.spec.n, bias4=t.bias, keep_sums=self.keep_sums, y=acc,
+                lists=lists_out, y2=B.acc[li + 1], lists2=B.lists[li + 1],
+                y3=B.acc[li + 2].reshape(bq, -1), lists3=B.lists[li + 2], y4=B.acc[li + 3])))
+            return calls
         if pl.dense_kernel:
             if s.k is not None:
                 # sparse-dense variant with k-WTA: dense activations, no
@@ -236,7 +263,8 @@ class Network:
                 calls.append((f"{s.name}.mrs", lambda: ops.conv2d_dense(
                     x, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad, p.bias, pl.pool, out=acc)))
             return calls
-        if ((li > 0 and (self.plans[li - 1].fuse_next or self.plans[li - 1].fuse_next2)) or
+        if ((li > 0 and (self.plans[li - 1].fuse_next or self.plans[li - 1].fuse_next2 or
+                         self.plans[li - 1].fuse_next3)) or
                 (li > 1 and self.plans[li - 2].fuse_next2)):
             return []                                   # run by an earlier layer's call
         if pl.in_lists:

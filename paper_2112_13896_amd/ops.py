@@ -294,6 +294,53 @@ def mrs_kwta_chain3(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in
     return y, lists, y2, lists2, y3
 
 
+def conv2d_dense_kwta_chain3(x: torch.Tensor, aug, kh: int, kw: int, n: int, stride: int = 1,
+                             pad: int = 0, bias=None, pool: int = 1, *, k: int, shift: int,
+                             aug2, kh2: int, kw2: int, n2: int, stride2: int = 1, pad2: int = 0,
+                             bias2=None, pool2: int = 1, k2: int, shift2: int, aug3, n3: int,
+                             bias3=None, k3: int, shift3: int, aug4, n4: int, bias4=None,
+                             keep_sums: bool = True, y=None, lists=None, y2=None, lists2=None,
+                             y3=None, lists3=None, y4=None):
+    """The dense-input int8 first layer with k-WTA lists, then the three layers
+    of mrs_kwta_chain3 on them (cs_conv2d_dense_kwta_chain3).  Returns
+    (y, lists, y2, lists2, y3, lists3, y4)."""
+    if x.dim() != 4 or x.dtype != torch.int8:
+        raise ValueError("x must be int8 NHWC")
+    b, h, w, c_in = x.shape
+    dev = x.device
+    pa, c_out = _aug(aug, torch.int8, n)
+    pa2, c_out2 = _aug(aug2, torch.int8, n2)
+    pa3, c_out3 = _aug(aug3, torch.int8, n3)
+    pa4, c_out4 = _aug(aug4, torch.int8, n4)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    s1 = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    ho2, wo2 = conv_out(s1[1], kh2, stride2, pad2), conv_out(s1[2], kw2, stride2, pad2)
+    s2 = (b, max(ho2, 0) // pool2, max(wo2, 0) // pool2, c_out2)
+    r1, r2 = s1[0] * s1[1] * s1[2], s2[0] * s2[1] * s2[2]
+    y = torch.empty(s1, dtype=torch.int32, device=dev) if y is None else y
+    y2 = torch.empty(s2, dtype=torch.int32, device=dev) if y2 is None else y2
+    y3 = torch.empty((b, c_out3), dtype=torch.int32, device=dev) if y3 is None else y3
+    y4 = torch.empty((b, c_out4), dtype=torch.int32, device=dev) if y4 is None else y4
+    for t, nm, m in ((y, "y", r1 * c_out), (y2, "y2", r2 * c_out2), (y3, "y3", b * c_out3),
+                     (y4, "y4", b * c_out4)):
+        if t.dtype != torch.int32 or t.numel() != m:
+            raise ValueError(f"{nm} does not match its layer's output")
+    lists = _list_buffers(r1, list_capacity(k), dev, lists)
+    lists2 = _list_buffers(r2, list_capacity(k2), dev, lists2)
+    lists3 = _list_buffers(b, list_capacity(k3), dev, lists3)
+    (oi, ov, oc), (oi2, ov2, oc2), (oi3, ov3, oc3) = lists, lists2, lists3
+    check("cs_conv2d_dense_kwta_chain3", lib().cs_conv2d_dense_kwta_chain3(
+        CS_I8, _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n, _opt(bias, "bias"),
+        pool, _dev(y, "y"), 1 if keep_sums else 0, k, CS_I8, shift, _dev(oi, "oidx"),
+        _dev(ov, "oval"), _dev(oc, "ocnt"), oi.shape[1],
+        kh2, kw2, stride2, pad2, pa2, c_out2, n2, _opt(bias2, "bias2"), pool2, _dev(y2, "y2"),
+        k2, shift2, _dev(oi2, "oidx2"), _dev(ov2, "oval2"), _dev(oc2, "ocnt2"), oi2.shape[1],
+        pa3, c_out3, n3, _opt(bias3, "bias3"), _dev(y3, "y3"), k3, shift3, _dev(oi3, "oidx3"),
+        _dev(ov3, "oval3"), _dev(oc3, "ocnt3"), oi3.shape[1],
+        pa4, c_out4, n4, _opt(bias4, "bias4"), _dev(y4, "y4"), _stream()))
+    return y, lists, y2, lists2, y3, lists3, y4
+
+
 def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: int, pad: int,
              c_out: int, n: int, pool: int = 1, k: int = -1) -> dict:
     """The launch plan the library picks for a layer (host only)."""

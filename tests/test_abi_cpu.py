@@ -389,6 +389,34 @@ def test_chain3_validation(L):
     assert call(ocap2=0) == CS_ERR_SHAPE
 
 
+def test_dense_chain3_validation(L):
+    f = L.cs_conv2d_dense_kwta_chain3
+    ok = dict(xt=CS_I8, x=FAKE, b=4, h=32, w=32, c_in=1, kh=5, kw=5, stride=1, pad=0, aug=FAKE,
+              c_out=64, n=1, bias=None, pool=2, y=FAKE, keep_sums=0, k=8, ot=CS_I8, shift=11,
+              oidx=FAKE, oval=FAKE, ocnt=FAKE, ocap=8, kh2=5, kw2=5, stride2=1, pad2=0, aug2=FAKE,
+              c_out2=64, n2=16, bias2=None, pool2=2, y2=FAKE, k2=8, shift2=9, oidx2=FAKE,
+              oval2=FAKE, ocnt2=FAKE, ocap2=8, aug3=FAKE, c_out3=1500, n3=20, bias3=None, y3=FAKE,
+              k3=75, shift3=8, oidx3=FAKE, oval3=FAKE, ocnt3=FAKE, ocap3=76, aug4=FAKE, c_out4=12,
+              n4=1, bias4=None, y4=FAKE, stream=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(*a.values())
+    assert call(xt=CS_F32) == CS_ERR_DTYPE
+    assert call(ot=CS_I32) == CS_ERR_DTYPE
+    for name in ("x", "aug", "oidx", "aug2", "oidx2", "y3", "ocnt3", "aug4", "y4"):
+        assert call(**{name: None}) == CS_ERR_ARG, name
+    assert call(k3=-1) == CS_ERR_ARG
+    assert call(shift3=32) == CS_ERR_ARG
+    assert call(n=2) == CS_ERR_SHAPE                # the first layer is dense (n == 1)
+    assert call(c_out=32, c_out2=32) == CS_ERR_SHAPE   # the first layer has 64 outputs
+    assert call(kh=7, kw=7) == CS_ERR_SHAPE         # 49 slots > 32
+    assert call(k=9) == CS_ERR_SHAPE                # more winners than the first list holds
+    assert call(k3=80) == CS_ERR_SHAPE
+    assert call(n4=5) == CS_ERR_SHAPE               # 5 does not divide 12
+
+
 def test_mrs_and_linear_validation(L):
     m = L.cs_mrs_conv2d
     base = [CS_F32, FAKE, FAKE, FAKE, 4, 2, 8, 8, 4, 3, 3, 1, 1, FAKE, 8, 4, None, 1, FAKE, None]

@@ -66,19 +66,20 @@ def test_int_config_bit_exact(cid):
 
 
 def test_tail_fusion_matches_two_launches():
-    """Config 2's last three layers (conv2 with k-WTA, linear1 with k-WTA over
-    conv2's whole map, the output layer on its winners) in one call
-    (cs_mrs_kwta_chain3) and as three calls: the same bits in every buffer,
-    two launches fewer."""
+    """Config 2's four layers (conv1 on the dense input, conv2 with k-WTA,
+    linear1 with k-WTA over conv2's whole map, the output layer on its
+    winners) in one call (cs_conv2d_dense_kwta_chain3) and as four calls: the
+    same bits in every buffer, three launches fewer."""
     cfg = CONFIGS[2]
     inp = generate(cfg)
     fused = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
     plain = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, fuse_tail=False)
     assert fused.plans[-2].fuse_next and not plain.plans[-2].fuse_next
     assert fused.plans[-3].fuse_next2 and not plain.plans[-3].fuse_next2
+    assert fused.plans[0].fuse_next3 and not plain.plans[0].fuse_next3
     names_f, names_p = fused.kernel_names(), plain.kernel_names()
-    assert len(names_f) == len(names_p) - 2
-    assert "conv2.mrs_kwta+linear1.mrs_kwta+output.mrs" in names_f
+    assert len(names_f) == len(names_p) - 3
+    assert names_f == ["conv1.dense_kwta+conv2.mrs_kwta+linear1.mrs_kwta+output.mrs"]
     x = dev(inp["x"])
     fused.forward(x)
     plain.forward(x)

@@ -446,3 +446,69 @@ def test_chain3_matches_separate_calls(case):
     if pool == 2:
         ref = o.maxpool2x2_nhwc(ref)
     assert np.array_equal(host(got[0]).astype(np.int64), ref), "first layer sums"
+
+
+# ------------------------------------------------------------- four-layer chain
+# (b, h, w, c_in), kh, kw, pad, pool, k, shift | kh2, pad2, c_out2, n2, pool2, k2, shift2 |
+# c_out3, n3, k3, shift3 | c_out4, n4 | ties
+DENSE_CHAIN_CASES = [
+    # keyword-spotting shape at a small batch: one kernel
+    ((5, 32, 32, 1), 5, 5, 0, 2, 8, 11, 5, 0, 64, 16, 2, 8, 9, 1500, 20, 75, 8, 12, 1, False),
+    # no first pool, 3x3 pad 1 twice, ties in the first layer: one kernel
+    ((3, 12, 12, 2), 3, 3, 1, 1, 8, 0, 3, 1, 64, 8, 2, 6, 5, 100, 4, 10, 5, 10, 2, True),
+    # 128 channels in the second layer: the two-call fallback
+    ((2, 16, 16, 1), 5, 5, 0, 2, 8, 11, 3, 1, 128, 16, 1, 12, 7, 200, 8, 20, 6, 8, 1, False),
+]
+
+
+@pytest.mark.parametrize("case", DENSE_CHAIN_CASES,
+                         ids=[f"{c[0]}-{c[1]}x{c[2]}-p{c[4]}-to{c[9]}" for c in DENSE_CHAIN_CASES])
+def test_dense_chain3_matches_separate_calls(case):
+    """cs_conv2d_dense_kwta_chain3 against cs_conv2d_dense_kwta followed by
+    cs_mrs_kwta_chain3 on its lists: the same bits in every output."""
+    (shape, kh, kw, pad, pool, k, shift, kh2, pad2, c_out2, n2, pool2, k2, shift2, c_out3, n3,
+     k3, shift3, c_out4, n4, ties) = case
+    r = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    b, h, w, c_in = shape
+    if ties:
+        x = r.integers(0, 2, size=shape).astype(np.int8)
+        W1 = np.sign(r.integers(-127, 128, size=(64, kh, kw, c_in))).astype(np.int8)
+        W1[W1 == 0] = 1
+    else:
+        x = r.integers(-127, 128, size=shape).astype(np.int8)
+        W1 = r.integers(-127, 128, size=(64, kh, kw, c_in)).astype(np.int8)
+        W1[W1 == 0] = 1
+    ho1, wo1 = (h + 2 * pad - kh + 1) // pool, (w + 2 * pad - kw + 1) // pool
+    ho2, wo2 = (ho1 + 2 * pad2 - kh2 + 1) // pool2, (wo1 + 2 * pad2 - kh2 + 1) // pool2
+    W2 = weights(r, c_out2, kh2, kh2, 64, n2, "i8")
+    W3 = weights(r, c_out3, ho2, wo2, c_out2, n3, "i8")
+    W4 = weights(r, c_out4, 1, 1, c_out3, n4, "i8")
+    b1, b2, b3, b4 = (dev(r.integers(-1000, 1001, size=m).astype(np.int32))
+                      for m in (64, c_out2, c_out3, c_out4))
+    a1, a2, a3, a4 = (ops.aug_to_device(ops.pack(Wx.reshape(Wx.shape[0], -1), nx)[0])
+                      for Wx, nx in ((W1, 1), (W2, n2), (W3, n3), (W4, n4)))
+    xd = dev(x)
+    got = ops.conv2d_dense_kwta_chain3(
+        xd, a1, kh, kw, 1, 1, pad, b1, pool, k=k, shift=shift, aug2=a2, kh2=kh2, kw2=kh2, n2=n2,
+        pad2=pad2, bias2=b2, pool2=pool2, k2=k2, shift2=shift2, aug3=a3, n3=n3, bias3=b3, k3=k3,
+        shift3=shift3, aug4=a4, n4=n4, bias4=b4, keep_sums=True)
+    y, lists = ops.conv2d_dense_kwta(xd, a1, kh, kw, 1, 1, pad, b1, pool, k=k,
+                                     out_dtype=torch.int8, shift=shift, keep_sums=True,
+                                     cap=ops.list_capacity(k))
+    rest = ops.mrs_kwta_chain3(*lists, (b, ho1, wo1, 64), a2, kh2, kh2, n2, 1, pad2, b2, pool2,
+                               k=k2, shift=shift2, aug2=a3, n2=n3, bias2=b3, k2=k3,
+                               shift2=shift3, aug3=a4, n3=n4, bias3=b4, keep_sums=True)
+    torch.cuda.synchronize()
+    want = (y, lists) + tuple(rest)
+    for i, nm in ((0, "y"), (2, "y2"), (4, "y3"), (6, "y4")):
+        assert np.array_equal(host(got[i]).reshape(-1), host(want[i]).reshape(-1)), nm
+    for i, nm in ((1, "lists"), (3, "lists2"), (5, "lists3")):
+        gi, gv, gc = (host(t) for t in got[i])
+        ei, ev, ec = (host(t) for t in want[i])
+        assert np.array_equal(gc, ec), nm + " counts"
+        live = np.arange(gi.shape[1])[None, :] < ec[:, None]
+        assert np.array_equal(gi[live], ei[live]) and np.array_equal(gv[live], ev[live]), nm
+    ref = o.conv2d_nhwc(x, W1, 1, pad, host(b1))
+    if pool == 2:
+        ref = o.maxpool2x2_nhwc(ref)
+    assert np.array_equal(host(got[0]).astype(np.int64), ref), "first layer sums"

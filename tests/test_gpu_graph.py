@@ -56,11 +56,12 @@ def test_graph_replay_matches_eager(cid):
         torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("cid,overlap", [(2, False), (2, True), (3, True), (5, True)])
-def test_multi_pass_graph_matches_eager(cid, overlap):
+@pytest.mark.parametrize("cid,mode", [(2, "sequential"), (2, "alternate"), (3, "overlapped"),
+                                      (3, "alternate"), (5, "overlapped")])
+def test_multi_pass_graph_matches_eager(cid, mode):
     """The benchmark's graph of several passes over rotating buffer sets (seven
     passes over three sets, so sets are written again inside one replay), in
-    the sequential and the two-stream schedule: after each replay every set
+    each of the three schedules: after each replay every set
     holds the eager pass's bits for its own input."""
     from bench import capture_passes
     cfg = CONFIGS[cid]
@@ -88,7 +89,7 @@ def test_multi_pass_graph_matches_eager(cid, overlap):
             if lst is not None:
                 for t in lst:
                     t.fill_(-1)
-    g = capture_passes(net, xs, sets, 7, overlap=overlap)
+    g = capture_passes(net, xs, sets, 7, mode)
     for rep in range(3):
         g.replay()
         torch.cuda.synchronize()
