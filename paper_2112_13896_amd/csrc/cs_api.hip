@@ -954,7 +954,8 @@ int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
   const int nb = (int)(nb64 < 65536 ? nb64 : 65536);
   const dim3 grid(nb), block(64 * cs::KWTA_WAVE_WAVES);
 #define CS_KWTA_WAVE(MM)                                                                  \
-  hipLaunchKernelGGL((cs::kwta_wave<TI, TO, MM>), grid, block, 0, stream, in, rows, c, k, out, \
+  hipLaunchKernelGGL((cs::kwta_wave<TI, TO, MM>), grid, block,                                  \
+                     (size_t)cs::KWTA_WAVE_WAVES * cs::WAVE_HIST * 4, stream, in, rows, c, k, out, \
                      shift, lo)
   if (m <= 1) CS_KWTA_WAVE(1);
   else if (m <= 2) CS_KWTA_WAVE(2);

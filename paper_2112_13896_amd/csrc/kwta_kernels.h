@@ -69,16 +69,22 @@ struct ListOut {
   int cap;
 };
 
-// k-th largest of a row's keys, searched by one wavefront: lane l holds keys
-// key[j] of elements j*64 + l (elements >= c are not part of the row).  The
-// search starts below the bits all keys share (from the row's min and max)
-// and fixes one bit per step, MSB first: T | bit is kept while at least k keys
-// are >= it, counted with a ballot per key.  No memory traffic; the result is
-// wavefront-uniform.  Requires 1 <= k < c.  Returns T; *need = k - #{key > T},
-// the number of keys equal to T that win (the lowest indices).
+// Radix select over a wavefront's keys: key[j] is element j*64 + lane of the
+// row, elements >= c are not part of it, 0 < k < c.  Returns the k-th largest
+// key T and sets *need to k minus the number of keys above T (the keys equal
+// to T that win).  Keys are offset by the row minimum, then 9-bit digits are
+// resolved from the top, as many passes as the offset range has bits / 9:
+// each pass counts the keys that share the digits found so far into 512 LDS
+// bins (the others into a spare bin per lane), and one inclusive scan over the
+// lanes (lane l holds bins 8(63 - l) .. + 7, the highest first) finds the bin
+// of the k-th.  hist: WAVE_HIST words of LDS owned by the wavefront.
+constexpr int WAVE_BINS = 512;
+constexpr int WAVE_HIST = WAVE_BINS + 64;
+
 template <int M>
-__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[M], int c, int k,
-                                                     int* need) {
+__device__ __forceinline__ uint32_t wave_kth_radix(const uint32_t (&key)[M], int c, int k,
+                                                   int* need, uint32_t* hist) {
+  typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
   const int lane = threadIdx.x & 63;
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
@@ -90,26 +96,63 @@ __device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[M], i
   }
   kmin = wave_min_u32(kmin);
   kmax = wave_max_u32(kmax);
-  const uint32_t diff = kmin ^ kmax;
-  uint32_t T = kmax;
-  if (diff != 0u) {
-    const int hb = 31 - __builtin_clz(diff);
-    const uint32_t low = hb == 31 ? 0xFFFFFFFFu : ((2u << hb) - 1u);
-    T = kmax & ~low;                                   // the shared prefix, zeros below
-    for (int b = hb; b >= 0; --b) {
-      const uint32_t cand = T | (1u << b);
-      int cnt = 0;
-#pragma unroll
-      for (int j = 0; j < M; ++j)                      // keys outside the row are 0 < cand
-        if (j * 64 < c) cnt += __popcll(__ballot(key[j] >= cand));
-      if (cnt >= k) T = cand;
-    }
+  const uint32_t range = kmax - kmin;
+  if (range == 0u) {
+    *need = k;
+    return kmin;
   }
-  int gt = 0;
+  uint32_t ok[M];
 #pragma unroll
-  for (int j = 0; j < M; ++j) gt += __popcll(__ballot(j * 64 + lane < c && key[j] > T));
-  *need = k - gt;
-  return T;
+  for (int j = 0; j < M; ++j) ok[j] = key[j] - kmin;
+  int rem = 32 - __builtin_clz(range);
+  int passes = (rem + 8) / 9;
+  uint32_t prefix = 0u;
+  int nd = k;
+  const u4_t z = {0u, 0u, 0u, 0u};
+  reinterpret_cast<u4_t*>(hist)[2 * lane] = z;
+  reinterpret_cast<u4_t*>(hist)[2 * lane + 1] = z;
+  const int spare = WAVE_BINS + lane;
+  for (; passes > 0; --passes) {                                   // uniform
+    const int width = (rem + passes - 1) / passes;
+    const int sh = rem - width;
+    const uint32_t hi = rem >= 32 ? 0u : (0xFFFFFFFFu << rem);
+    const uint32_t lob = rem >= 32 ? 0u : (prefix << rem);
+    wave_lds_order();
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const bool in = j * 64 + lane < c && (ok[j] & hi) == lob;
+      const int bin = in ? (int)__builtin_amdgcn_ubfe(ok[j], (uint32_t)sh, (uint32_t)width) : spare;
+      __hip_atomic_fetch_add(hist + bin, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    wave_lds_order();
+    const int b0 = 8 * (63 - lane);
+    const u4_t h0 = reinterpret_cast<const u4_t*>(hist + b0)[0];
+    const u4_t h1 = reinterpret_cast<const u4_t*>(hist + b0)[1];
+    reinterpret_cast<u4_t*>(hist + b0)[0] = z;                     // the next pass's bins
+    reinterpret_cast<u4_t*>(hist + b0)[1] = z;
+    const uint32_t hb[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+    int ls = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) ls += (int)hb[q];
+    const int incl = (int)wave_incl_scan((uint32_t)ls, 0u, OpAdd{});
+    const int above = incl - ls;
+    int run = above, bin = b0, found = 0;
+#pragma unroll
+    for (int q = 7; q >= 0; --q) {
+      const bool hit = !found && run + (int)hb[q] >= nd;
+      bin = hit ? b0 + q : bin;
+      run = (!found && !hit) ? run + (int)hb[q] : run;
+      found |= hit;
+    }
+    const uint64_t fb = __ballot(above < nd && nd <= incl);        // exactly one lane
+    const int f = __ffsll((unsigned long long)fb) - 1;
+    prefix = (prefix << width) | (uint32_t)__builtin_amdgcn_readlane(bin, f);
+    nd -= __builtin_amdgcn_readlane(run, f);
+    rem = sh;
+  }
+  wave_lds_order();                                                // before the bins are reused
+  *need = nd;
+  return prefix + kmin;
 }
 
 constexpr int KWTA_LANE_ROWS = 128;   // rows (threads) per block of kwta_lane
@@ -240,7 +283,7 @@ __global__ __launch_bounds__(KWTA_LANE_ROWS) void kwta_lane(const TI* __restrict
 template <typename TI, typename TO, int M>
 __device__ __forceinline__ void kwta_wave_row(const TI (&v)[M], int c, int k, int shift,
                                               const ListOut& lo, TO* __restrict__ out,
-                                              int64_t row) {
+                                              int64_t row, uint32_t* hist) {
   const int lane = threadIdx.x & 63;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
   const bool all_win = (k >= c);
@@ -250,7 +293,7 @@ __device__ __forceinline__ void kwta_wave_row(const TI (&v)[M], int c, int k, in
   for (int j = 0; j < M; ++j) key[j] = j * 64 + lane < c ? order_key(v[j]) : 0u;
   int need = 0;
   uint32_t thr = 0u;
-  if (!all_win && !none_win) thr = wave_kth_largest<M>(key, c, k, &need);
+  if (!all_win && !none_win) thr = wave_kth_radix<M>(key, c, k, &need, hist);
   // ranks of the ties in index order (element index = j*64 + lane)
   int run = 0, lrun = 0;
 #pragma unroll
@@ -478,8 +521,10 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
                                                                   int64_t rows, int c, int k,
                                                                   TO* __restrict__ out,
                                                                   int shift, ListOut lo) {
+  extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem) + wv * WAVE_HIST;   // this wavefront's bins
   for (int64_t row = (int64_t)blockIdx.x * KWTA_WAVE_WAVES + wv; row < rows;
        row += (int64_t)gridDim.x * KWTA_WAVE_WAVES) {            // uniform across the wave
     TI v[M];
@@ -488,7 +533,7 @@ __global__ __launch_bounds__(64 * KWTA_WAVE_WAVES) void kwta_wave(const TI* __re
       const int e = j * 64 + lane;
       v[j] = e < c ? in[row * c + e] : TI(0);
     }
-    kwta_wave_row<TI, TO, M>(v, c, k, shift, lo, out, row);
+    kwta_wave_row<TI, TO, M>(v, c, k, shift, lo, out, row, hist);
   }
 }
 
