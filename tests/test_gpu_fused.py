@@ -402,6 +402,8 @@ CHAIN3_CASES = [
     ((3, 6, 7, 32), 5, 3, 3, 1, 96, 8, 1, 7, 0, 200, 8, 20, 0, 10, 2, True),
     # an image wider than one band: the two-call fallback
     ((2, 64, 64, 16), 3, 3, 3, 1, 32, 4, 2, 4, 6, 64, 4, 10, 4, 8, 1, False),
+    # k = 0 in the first layer: empty lists into the second (its sums are its bias)
+    ((2, 10, 10, 16), 4, 3, 3, 1, 32, 4, 2, 0, 6, 64, 8, 10, 4, 8, 1, False),
 ]
 
 
@@ -458,6 +460,8 @@ DENSE_CHAIN_CASES = [
     ((3, 12, 12, 2), 3, 3, 1, 1, 8, 0, 3, 1, 64, 8, 2, 6, 5, 100, 4, 10, 5, 10, 2, True),
     # 128 channels in the second layer: the two-call fallback
     ((2, 16, 16, 1), 5, 5, 0, 2, 8, 11, 3, 1, 128, 16, 1, 12, 7, 200, 8, 20, 6, 8, 1, False),
+    # every output of the third layer wins (k3 = c_out3); no pool in the second
+    ((2, 12, 12, 1), 3, 3, 1, 2, 4, 6, 3, 1, 64, 8, 1, 8, 5, 16, 4, 16, 5, 4, 1, False),
 ]
 
 
