@@ -137,6 +137,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
     for (int s = 0; s < KMAX; ++s) top[s] = 0u;
     const bool search = live && k > 0 && k < c;
     if (search) {
+      // the first block, sorted, is the list; later blocks are merged into it
       for (int i0 = i_lo; i0 < i_hi; i0 += KMAX) {
         uint32_t blk[KMAX];
 #pragma unroll
@@ -146,7 +147,12 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
           blk[j] = i < i_hi ? kx : 0u;
         }
         bitonic_sort_desc<KMAX>(blk);
-        top_merge_desc<KMAX>(top, blk);
+        if (i0 == i_lo) {
+#pragma unroll
+          for (int j = 0; j < KMAX; ++j) top[j] = blk[j];
+        } else {
+          top_merge_desc<KMAX>(top, blk);
+        }
       }
     }
     // merge with the neighbour at distance 1, then 2 (all four lanes end equal);
