@@ -365,6 +365,23 @@ __device__ __forceinline__ void bitonic_sort_desc(uint32_t (&a)[N]) {
         }
       }
 }
+// Eight keys: a 19-comparator network of depth 6 (Knuth, The Art of Computer
+// Programming vol. 3, 5.3.4) in place of the 24 of the bitonic sort; by the
+// 0-1 principle it sorts any input (all 256 0-1 inputs checked).
+template <>
+__device__ __forceinline__ void bitonic_sort_desc<8>(uint32_t (&a)[8]) {
+  auto ce = [&](int i, int j) {
+    const uint32_t x = a[i], y = a[j];
+    a[i] = x > y ? x : y;
+    a[j] = x > y ? y : x;
+  };
+  ce(0, 2); ce(1, 3); ce(4, 6); ce(5, 7);
+  ce(0, 4); ce(1, 5); ce(2, 6); ce(3, 7);
+  ce(0, 1); ce(2, 3); ce(4, 5); ce(6, 7);
+  ce(2, 4); ce(3, 5);
+  ce(1, 4); ce(3, 6);
+  ce(1, 2); ce(3, 4); ce(5, 6);
+}
 template <int N>
 __device__ __forceinline__ void bitonic_clean_desc(uint32_t (&a)[N]) {
 #pragma unroll
