@@ -56,8 +56,10 @@ def run_chain(layers, x: np.ndarray, Ws, bs, inputs=None) -> list:
 
 
 def requant_shift(winner_values: np.ndarray) -> int:
-    """max(0, ceil(log2(max|winner| / 127))): the smallest arithmetic shift
-    that brings every winner into the int8 range [-127, 127]."""
+    """The smallest s >= 0 with max|winner| >> s <= 127: the smallest
+    arithmetic shift that brings every winner into the int8 range [-127, 127]
+    (equal to max(0, bit_length(max|winner|) - 7); at max|winner| = 255 it is
+    1, where ceil(log2(255 / 127)) would give 2)."""
     m = int(np.abs(np.asarray(winner_values, dtype=np.int64)).max()) if np.size(winner_values) else 0
     s = 0
     while (m >> s) > 127:

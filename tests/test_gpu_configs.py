@@ -136,16 +136,6 @@ def test_config_launch_paths(cid, layer, path):
     assert plan["path"] == path, plan
 
 
-def test_config_product_counts_match_closed_form():
-    """Products the MRS kernel performs = sum over (non-zero x, set) pairs; with
-    complementary covering sets this equals the oracle's pair count."""
-    cfg = CONFIGS[1]
-    inp = generate(cfg)
-    W = inp["W"][0]
-    spec = cfg.layers[0]
-    assert o.pair_count_linear(inp["x"], W) == int((inp["x"] != 0).sum()) * spec.groups
-
-
 def test_repeated_forward_identical():
     cfg = CONFIGS[3]
     inp = generate(cfg, batch=4)

@@ -419,11 +419,45 @@ def test_packed_product_equals_dense():
     b = r.integers(-1000, 1001, size=24).astype(np.int32)
     val, kid, _ = o.pack(W, 4)
     y = np.tile(b.astype(np.int64), (5, 1))
+    products = 0
     for bi in range(5):
         for i in np.nonzero(x[bi])[0]:
             for g in range(6):
                 y[bi, g * 4 + kid[i, g]] += int(x[bi, i]) * int(val[i, g])
+                products += 1
     assert np.array_equal(o.linear(x, W, b), y)
+    # Figure 1 / Section 3.2: one product per (non-zero activation, non-zero
+    # weight) pair and no other; with covering sets that is nnz(x) * G
+    assert products == o.pair_count_linear(x, W) == int((x != 0).sum()) * 6
+
+
+@pytest.mark.parametrize("cid", [1, 3, 5])
+def test_config_product_counts_match_closed_form(cid):
+    """The products a sparse-sparse layer needs (the oracle's pair count) equal
+    the closed form: sum over rows of nnz(x) * G (covering sets), summed over
+    the output pixels' windows for a convolution."""
+    cfg = CONFIGS[cid]
+    inp = generate(cfg, batch=2)
+    spec = cfg.layers[0]
+    x = inp["x"]
+    W = inp["W"][0]
+    if spec.kind == "linear":
+        assert o.pair_count_linear(x, W.reshape(spec.c_out, -1)) == \
+            int((x != 0).sum()) * spec.groups
+    else:
+        B, H, Wd, C = x.shape
+        nnz = (x != 0).sum(axis=3)
+        Ho = (H + 2 * spec.pad - spec.kh) // spec.stride + 1
+        Wo = (Wd + 2 * spec.pad - spec.kw) // spec.stride + 1
+        win = 0
+        for ho in range(Ho):
+            for wo in range(Wo):
+                for ky in range(spec.kh):
+                    for kx in range(spec.kw):
+                        hy, wx = ho * spec.stride + ky - spec.pad, wo * spec.stride + kx - spec.pad
+                        if 0 <= hy < H and 0 <= wx < Wd:
+                            win += int(nnz[:, hy, wx].sum())
+        assert o.pair_count_conv(x, W, spec.stride, spec.pad) == win * spec.groups
 
 
 # ---------------------------------------------------------------- configs

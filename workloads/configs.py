@@ -70,9 +70,9 @@ class Config:
         return SEED_BASE + self.cid
 
 
-# Requantisation shifts (int chains).  Each is max(0, ceil(log2(max|winner| /
-# 127))) over the seeded batch of the layer's k-WTA winners, computed once from
-# the CPU reference run and frozen here; the script that derives them lives in
+# Requantisation shifts (int chains).  Each is the smallest s >= 0 with
+# max|winner| >> s <= 127 over the seeded batch of the layer's k-WTA winners,
+# computed once from the CPU reference run and frozen here; the script that derives them lives in
 # tests/golden/ and a CPU test re-derives and compares them.
 _C2_S1, _C2_S2, _C2_S3 = 11, 9, 9
 _C5_S1 = 9
