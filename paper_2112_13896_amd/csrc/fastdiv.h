@@ -1,8 +1,10 @@
 // Division of unsigned 32-bit numbers by a divisor fixed at launch: one
 // multiply-high, one add and one shift instead of the ~30-instruction
-// software division the GPU otherwise runs (the round-up reciprocal method:
-// m = floor(2^32 (2^s - d) / d) + 1 with s = ceil(log2 d), then
-// floor(n / d) = (mulhi(n, m) + n) >> s, the add done in 64 bits).
+// software division the GPU otherwise runs.  This is the round-up reciprocal
+// method for division by invariant integers of T. Granlund and P. L.
+// Montgomery, "Division by Invariant Integers using Multiplication", PLDI
+// 1994 (Section 4): m = floor(2^32 (2^s - d) / d) + 1 with s = ceil(log2 d),
+// then floor(n / d) = (mulhi(n, m) + n) >> s, the add done in 64 bits.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

@@ -15,12 +15,14 @@
 //    keeps a descending top-K list by insertion (a max/min exchange per slot,
 //    no branches), which yields T;
 //  * kwta_wave  (row <= 2048): one wavefront owns a row, each lane holds up to
-//    M keys in registers.  T is found MSB-first, one bit per step below the
-//    bits every key of the row shares, counting the keys above a candidate
-//    with ballots (the threshold search of Section 3.3.3 and Figure 10,
-//    refined bit by bit so it is exact for 32-bit keys).  No LDS histogram:
-//    sums that cluster (many equal to the bias) would pile its atomics onto
-//    a few bins.  Ties are ranked with a ballot + popcount in index order.
+//    M keys in registers.  T is found by a radix select, most significant
+//    digit first, in 9-bit digits over the bits below those every key of the
+//    row shares: each pass builds a 512-bin histogram of the current digit in
+//    the wavefront's own LDS bins (the histogram threshold search of Section
+//    3.3.3 and Figure 10, repeated digit by digit so it is exact for 32-bit
+//    keys), a DPP scan from the top bin finds the digit holding the k-th key,
+//    and keys outside the prefix found so far go to a spare bin.  Ties are
+//    ranked with a ballot + popcount in index order.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

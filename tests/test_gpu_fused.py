@@ -22,9 +22,10 @@ import pytest
 import torch
 
 from oracle import cs_oracle as o
+from oracle import networks
 from paper_2112_13896_amd import ops
 from tests.gpu_util import assert_f32_close, check_kwta_f32, dev, host, pool_S
-from workloads import complementary_weights
+from workloads import LayerSpec, complementary_weights
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +63,27 @@ def dense_from_lists(idx, val, cnt, c):
         assert (np.diff(ii) > 0).all(), f"row {row}: list indices not ascending"
         out[row, ii] = val[row, :m]
     return out
+
+
+def check_chain_against_oracle(layers, x, Ws, bs, sums, lists):
+    """Every layer of a fused int8 chain against networks.run_chain (the
+    oracle's dense layers in Table 1's order): the sums after pool bit for bit,
+    and each k-WTA layer's list (counts, ascending indices, requantised values)
+    equal to the oracle's requantised winners with zero values left out.
+    `sums[l]` is the GPU's sums tensor of layer l, `lists[l]` its (idx, val,
+    cnt) or None for a layer without k-WTA."""
+    ref = networks.run_chain(layers, x, Ws, bs)
+    for li, (spec, r) in enumerate(zip(layers, ref)):
+        acc = r["acc"].reshape(-1, spec.c_out)
+        got = host(sums[li]).reshape(acc.shape).astype(np.int64)
+        assert np.array_equal(got, acc), f"layer {li} ({spec.name}): sums differ from the oracle"
+        if lists[li] is None:
+            continue
+        gi, gv, gc = (host(t) for t in lists[li])
+        want = np.asarray(r["out"], dtype=np.int64).reshape(-1, spec.c_out)
+        assert np.array_equal(gc, (want != 0).sum(axis=1)), f"layer {li}: list counts"
+        dense = dense_from_lists(gi, gv, gc, spec.c_out).astype(np.int64)
+        assert np.array_equal(dense, want), f"layer {li} ({spec.name}): lists differ from the oracle"
 
 
 # dtype, (b, h, w, c_in), nnz, kh, kw, stride, pad, c_out, n, pool, k, bias, shift,
@@ -409,8 +431,9 @@ CHAIN3_CASES = [
 
 @pytest.mark.parametrize("case", CHAIN3_CASES, ids=[f"{c[0]}-{c[1]}x{c[2]}-to{c[10]}" for c in CHAIN3_CASES])
 def test_chain3_matches_separate_calls(case):
-    """cs_mrs_kwta_chain3 against cs_mrs_kwta_conv2d followed by
-    cs_mrs_kwta_chain2 on its lists: the same bits in every output."""
+    """cs_mrs_kwta_chain3 against the oracle at every layer (sums, lists), and
+    against cs_mrs_kwta_conv2d followed by cs_mrs_kwta_chain2 on its lists:
+    the same bits in every output."""
     (shape, nnz, kh, kw, pad, c_out, n, pool, k, shift, c_out2, n2, k2, shift2, c_out3, n3,
      ties) = case
     r = np.random.default_rng(zlib.crc32(repr(case).encode()))
@@ -443,11 +466,17 @@ def test_chain3_matches_separate_calls(case):
         assert np.array_equal(gc, ec), nm + " counts"
         live = np.arange(gi.shape[1])[None, :] < ec[:, None]
         assert np.array_equal(gi[live], ei[live]) and np.array_equal(gv[live], ev[live]), nm
-    # the sums of the first layer against the oracle, so that both sides are pinned
-    ref = o.conv2d_nhwc(x, W1, 1, pad, host(b1))
-    if pool == 2:
-        ref = o.maxpool2x2_nhwc(ref)
-    assert np.array_equal(host(got[0]).astype(np.int64), ref), "first layer sums"
+    # every layer against the oracle: conv (pool, k-WTA, requant) -> a window
+    # over the whole pooled map (the NHWC flatten of a linear layer) -> linear
+    layers = (
+        LayerSpec("conv", "conv", c_in, c_out, n=n, kh=kh, kw=kw, pad=pad, pool=pool, k=k,
+                  shift=shift, bias=True),
+        LayerSpec("map", "linear", hp * wp * c_out, c_out2, n=n2, k=k2, shift=shift2, bias=True),
+        LayerSpec("last", "linear", c_out2, c_out3, n=n3, bias=True),
+    )
+    check_chain_against_oracle(layers, x, [W1, W2.reshape(c_out2, -1), W3.reshape(c_out3, -1)],
+                               [host(b1), host(b2), host(b3)], [got[0], got[2], got[4]],
+                               [got[1], got[3], None])
 
 
 # ------------------------------------------------------------- four-layer chain
@@ -468,8 +497,9 @@ DENSE_CHAIN_CASES = [
 @pytest.mark.parametrize("case", DENSE_CHAIN_CASES,
                          ids=[f"{c[0]}-{c[1]}x{c[2]}-p{c[4]}-to{c[9]}" for c in DENSE_CHAIN_CASES])
 def test_dense_chain3_matches_separate_calls(case):
-    """cs_conv2d_dense_kwta_chain3 against cs_conv2d_dense_kwta followed by
-    cs_mrs_kwta_chain3 on its lists: the same bits in every output."""
+    """cs_conv2d_dense_kwta_chain3 against the oracle at every layer (sums,
+    lists), and against cs_conv2d_dense_kwta followed by cs_mrs_kwta_chain3 on
+    its lists: the same bits in every output."""
     (shape, kh, kw, pad, pool, k, shift, kh2, pad2, c_out2, n2, pool2, k2, shift2, c_out3, n3,
      k3, shift3, c_out4, n4, ties) = case
     r = np.random.default_rng(zlib.crc32(repr(case).encode()))
@@ -512,7 +542,18 @@ def test_dense_chain3_matches_separate_calls(case):
         assert np.array_equal(gc, ec), nm + " counts"
         live = np.arange(gi.shape[1])[None, :] < ec[:, None]
         assert np.array_equal(gi[live], ei[live]) and np.array_equal(gv[live], ev[live]), nm
-    ref = o.conv2d_nhwc(x, W1, 1, pad, host(b1))
-    if pool == 2:
-        ref = o.maxpool2x2_nhwc(ref)
-    assert np.array_equal(host(got[0]).astype(np.int64), ref), "first layer sums"
+    # every layer against the oracle: dense conv (pool, k-WTA, requant) -> conv
+    # (pool, k-WTA, requant) -> a window over the whole map -> linear
+    layers = (
+        LayerSpec("conv1", "conv", c_in, 64, n=1, kh=kh, kw=kw, pad=pad, pool=pool, k=k,
+                  shift=shift, bias=True),
+        LayerSpec("conv2", "conv", 64, c_out2, n=n2, kh=kh2, kw=kh2, pad=pad2, pool=pool2, k=k2,
+                  shift=shift2, bias=True),
+        LayerSpec("map", "linear", ho2 * wo2 * c_out2, c_out3, n=n3, k=k3, shift=shift3,
+                  bias=True),
+        LayerSpec("last", "linear", c_out3, c_out4, n=n4, bias=True),
+    )
+    check_chain_against_oracle(
+        layers, x, [W1, W2, W3.reshape(c_out3, -1), W4.reshape(c_out4, -1)],
+        [host(b1), host(b2), host(b3), host(b4)], [got[0], got[2], got[4], got[6]],
+        [got[1], got[3], got[5], None])

@@ -29,7 +29,7 @@ def snapshot(net, bufs):
     return outs, sums
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 5])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_graph_replay_matches_eager(cid):
     cfg = CONFIGS[cid]
     inp = generate(cfg)
@@ -57,7 +57,7 @@ def test_graph_replay_matches_eager(cid):
 
 
 @pytest.mark.parametrize("cid,mode", [(2, "sequential"), (2, "alternate"), (3, "overlapped"),
-                                      (3, "alternate"), (5, "overlapped")])
+                                      (3, "alternate"), (4, "alternate"), (5, "overlapped")])
 def test_multi_pass_graph_matches_eager(cid, mode):
     """The benchmark's graph of several passes over rotating buffer sets (seven
     passes over three sets, so sets are written again inside one replay), in
@@ -98,3 +98,20 @@ def test_multi_pass_graph_matches_eager(cid, mode):
             for li in range(len(net.packed)):
                 assert np.array_equal(got[li], want[j][li]), f"replay {rep} set {j} layer {li}"
         torch.zeros(1 << 20, device="cuda").add_(1)      # unrelated eager work between replays
+
+
+@pytest.mark.parametrize("cid", [3, 4])
+def test_repeated_forward_identical_full_size(cid):
+    """fp32 chains at their full batch: two eager passes over the same input
+    give the same bits in every layer (no summation order depends on timing)."""
+    cfg = CONFIGS[cid]
+    inp = generate(cfg)
+    net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch)
+    x = dev(inp["x"])
+    net.forward(x)
+    a_outs, a_sums = snapshot(net, net.bufs)
+    net.forward(x)
+    b_outs, b_sums = snapshot(net, net.bufs)
+    for li in range(len(cfg.layers)):
+        assert np.array_equal(a_outs[li], b_outs[li]), f"layer {li} output"
+        assert np.array_equal(a_sums[li], b_sums[li]), f"layer {li} sums"
