@@ -237,6 +237,33 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
               void* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * cs_conv2d_noalloc - cs_conv2d for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation and result, bit for bit, but the
+ * compaction lists go to a scratch area the library holds instead of a
+ * workspace the caller passes in.
+ *
+ *  Arguments as cs_conv2d without ws / ws_bytes (linear layers: b = batch,
+ *  h = w = kh = kw = stride = 1, pad = 0, pool = 1).
+ *  Scratch: a static device array of CS_NOALLOC_SCRATCH_BYTES per GPU, part
+ *  of the library's code object, held from the library's load until the
+ *  process ends; its address is looked up once per device on the first call
+ *  made with that device current.  Nothing is allocated, freed or cleared by
+ *  a call; every scratch byte the kernels read was written earlier in the
+ *  same call.  All calls on one GPU share that GPU's scratch, so calls whose
+ *  execution overlaps on one GPU (concurrent streams, host threads) race and
+ *  must be serialised by the caller.
+ *  Errors: as cs_conv2d; CS_ERR_WORKSPACE when the lists of the b*h*w input
+ *  rows need more than CS_NOALLOC_SCRATCH_BYTES (cs_workspace_bytes(1, xt,
+ *  b*h*w, c_in) is that need); CS_ERR_DEVICE if the scratch address cannot be
+ *  obtained.
+ */
+#define CS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int cs_conv2d_noalloc(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                      int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                      int pool, void* y, void* stream);
+
+/*
  * cs_mrs_kwta_chain2 - two layers of a chain's tail: a layer with k-WTA whose
  * output is one vector per sample (a linear layer, or a conv whose pooled map
  * is 1 x 1), then a linear layer without k-WTA on its requantised winners

@@ -23,6 +23,7 @@ CS_I8, CS_I32, CS_F32 = 0, 1, 2
 CS_MAX_ROW = 65535
 CS_MAX_N = 32
 CS_MAX_KWTA_ROW = 2048
+CS_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 # name -> (restype, argtypes), in the order of include/cs.h
 _c = ctypes
@@ -62,6 +63,8 @@ SIGNATURES = {
     "cs_linear": (_i, [_i, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _sz, _vp]),
     "cs_conv2d": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i, _vp, _vp,
                        _sz, _vp]),
+    "cs_conv2d_noalloc": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
+                               _vp, _vp]),
     "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                              _vp, _vp]),
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),

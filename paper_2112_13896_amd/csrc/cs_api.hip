@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <mutex>
 
 #include "compact_kernels.h"
 #include "conv_dense_mfma.h"
@@ -21,6 +22,13 @@
 #include "mrs_rows.h"
 #include "mrs_scatter.h"
 #include "mrs_tiled.h"
+
+// Scratch of cs_conv2d_noalloc: the compaction lists it would otherwise take
+// from a caller's workspace.  A device-side array of the code object (one copy
+// per GPU, at that GPU's own address), held until the process ends; host code
+// never passes its name to a kernel, only the address noalloc_scratch() looks
+// up with hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[CS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -928,6 +936,33 @@ WsLayout ws_layout(cs_dtype xt, int64_t rows, int c_in) {
   return l;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char* g_scratch[kMaxDevices] = {};
+
+// The device address of the current device's scratch, looked up on the first
+// call with that device current and kept per device.
+int noalloc_scratch(unsigned char** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return CS_ERR_DEVICE;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return CS_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return CS_ERR_DEVICE;
+    }
+    if (reinterpret_cast<uintptr_t>(p) % kAlign != 0) return CS_ERR_DEVICE;
+    g_scratch[dev] = static_cast<unsigned char*>(p);
+  }
+  *out = g_scratch[dev];
+  return CS_OK;
+}
+
 // ---------------------------------------------------------------- k-WTA
 template <typename TI, typename TO>
 int kwta_dispatch(const TI* in, int64_t rows, int c, int k, TO* out, int shift,
@@ -1125,6 +1160,29 @@ int cs_conv2d(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh,
   if (!ws || ws_bytes < l.total) return CS_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return CS_ERR_WORKSPACE;
   auto* base = static_cast<unsigned char*>(ws);
+  auto* idx = reinterpret_cast<uint16_t*>(base + l.idx_off);
+  void* lv = base + l.val_off;
+  auto* cnt = reinterpret_cast<int32_t*>(base + l.cnt_off);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
+  if (r != CS_OK) return r;
+  return mrs_launch(xt, idx, lv, cnt, geo, aug, bias, y, s);
+}
+
+int cs_conv2d_noalloc(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,
+                      int stride, int pad, const void* aug, int c_out, int n, const void* bias,
+                      int pool, void* y, void* stream) {
+  if (!is_act_dtype(xt)) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !aug || !y) return CS_ERR_ARG;
+  const int64_t rows = (int64_t)b * h * w;
+  const WsLayout l = ws_layout(xt, rows, c_in);
+  if (l.total > CS_NOALLOC_SCRATCH_BYTES) return CS_ERR_WORKSPACE;
+  unsigned char* base = nullptr;
+  const int sst = noalloc_scratch(&base);
+  if (sst != CS_OK) return sst;
   auto* idx = reinterpret_cast<uint16_t*>(base + l.idx_off);
   void* lv = base + l.val_off;
   auto* cnt = reinterpret_cast<int32_t*>(base + l.cnt_off);

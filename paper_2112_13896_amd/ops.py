@@ -377,6 +377,27 @@ def workspace(op: int, dtype: torch.dtype, rows: int, c_in: int, device) -> torc
     return torch.empty((nbytes,), dtype=torch.uint8, device=device)
 
 
+def conv2d_noalloc(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
+                   stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None,
+                   pool: int = 1, out: torch.Tensor | None = None) -> torch.Tensor:
+    """conv2d without a workspace argument: the library's own scratch holds the
+    compaction lists (cs_conv2d_noalloc; nothing is allocated when `out` is
+    given).  Calls that overlap on one GPU race on that scratch."""
+    if x.dim() != 4:
+        raise ValueError("x must be NHWC")
+    b, h, w, c_in = x.shape
+    pa, c_out = _aug(aug, x.dtype, n)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    ydt = torch.int32 if x.dtype == torch.int8 else torch.float32
+    if out is None:
+        out = torch.empty((b, max(ho, 0) // pool, max(wo, 0) // pool, c_out), dtype=ydt,
+                          device=x.device)
+    check("cs_conv2d_noalloc", lib().cs_conv2d_noalloc(
+        _dt(x), _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n,
+        _opt(bias, "bias"), pool, _dev(out, "out"), _stream()))
+    return out
+
+
 def conv2d(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
            stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
            ws: torch.Tensor | None = None, out: torch.Tensor | None = None) -> torch.Tensor:

@@ -146,6 +146,29 @@ def test_conv2d_validation(L):
     assert f(*conv_args(ws=FAKE_WS + 8)) == CS_ERR_WORKSPACE   # misaligned
 
 
+def test_conv2d_noalloc_validation(L):
+    """Host checks of the entry point without a workspace, including the
+    scratch limit; all are refused before any HIP call."""
+    f = L.cs_conv2d_noalloc
+
+    def args(**kw):
+        a = conv_args(**kw)
+        del a[17:19]                                  # no ws, ws_bytes
+        return a
+    assert f(*args(xt=CS_I32)) == CS_ERR_DTYPE
+    assert f(*args(b=0)) == CS_ERR_ARG
+    assert f(*args(n=3)) == CS_ERR_SHAPE
+    assert f(*args(pool=2, h=7, w=7)) == CS_ERR_SHAPE
+    assert f(*args(x=None)) == CS_ERR_ARG
+    assert f(*args(y=None)) == CS_ERR_ARG
+    # lists of more rows than the scratch holds
+    per_row = 64 * (2 + 4) + 4
+    rows = _lib.CS_NOALLOC_SCRATCH_BYTES // per_row + 4096
+    assert L.cs_workspace_bytes(1, CS_F32, rows, 64) > _lib.CS_NOALLOC_SCRATCH_BYTES
+    assert f(*args(xt=CS_F32, b=1, h=rows, w=1, c_in=64, kh=1, kw=1, pad=0, c_out=64,
+                   n=8)) == CS_ERR_WORKSPACE
+
+
 def test_conv2d_dense_validation(L):
     f = L.cs_conv2d_dense
     ok = dict(xt=CS_I8, x=FAKE, b=2, h=32, w=32, c_in=1, kh=5, kw=5, stride=1, pad=0, aug=FAKE,
