@@ -1,32 +1,36 @@
 #!/usr/bin/env python3
 """Throughput of the Complementary Sparsity sparse-sparse layer chain on one GPU.
 
-    python bench.py [--steps K] [--warmup W] [--config C]
+    python bench.py [--steps K] [--warmup W] [--config C] [--also 1,3,4,5]
 
 A step is one pass of the whole chain over one batch: per layer, compaction
 of the activations into (index, value) lists (dense inputs only),
 multiply-route-sum (+ bias, + 2x2 max-pool), k-WTA (+ int8 requantisation)
 emitting the next layer's lists; where a layer's packed table fits one
 workgroup the last three are one kernel and the sums never reach HBM.  Inputs
-are resident in HBM when the timed region starts; the chain rotates among
-buffer sets (input + every intermediate) totalling more than 512 MiB, so a
-step does not find the previous step's data in the 256 MiB Infinity Cache.
-The K timed passes (K <= 256; else one pass per buffer set) are recorded once
-into a HIP graph (a serving loop's batches in one launch), pass i on buffer set
-i mod sets, in three schedules: one after another; each pass's first kernel
-on one stream and the rest on a second, so that the next batch's first kernel
-runs beside the current batch's later ones; or whole passes on the two streams
-in turn, so that one batch's last workgroups and the next one's first overlap
-(a buffer set is written again only after the passes that read it).  The
-fastest in a few warm-up replays is timed (`schedule`), so the step time is
-the kernels' time, not Python's or the graph launch's overhead; the same K
-passes with one graph launch each (no overlap) are timed after and reported
-beside it.  Per-kernel durations (and the roofline of the dominant kernel) come
-from graphs holding 20 launches of that one kernel, timed with HIP events on
-the replaying stream.
+are resident in HBM when the timed region starts.
+
+Cache-cold protocol: the chain rotates among buffer sets (input + every
+intermediate), as many as make the bytes one pass touches (the sum of its
+launches' algorithmic bytes) times the number of sets exceed 512 MiB, so a set
+comes round again only after twice the 256 MiB Infinity Cache of other data;
+and a 512 MiB buffer is written before every timed region.  The K timed passes
+(K <= 256; else one pass per buffer set) are recorded once into a HIP graph (a
+serving loop's batches in one launch), pass i on buffer set i mod sets, in
+three schedules: one after another; each pass's first kernel on one stream and
+the rest on a second, so the next batch's first kernel runs beside the current
+batch's later ones; or whole passes on the two streams in turn.  The fastest
+in a few warm-up replays is timed (`schedule`); the same K passes with one
+graph launch each are timed after and reported beside it.  Per-kernel
+durations (and the roofline of the dominant kernel) come from graphs holding
+one launch of that kernel per buffer set, each replay after the scrub, timed
+with HIP events on the replaying stream.
 
 Default workload: the keyword-spotting CNN of Table 1 (config 2, int8, batch
-256).  Prints ONE JSON line on stdout; progress goes to stderr.
+256), then the other workloads (`--also`), each reported under "workloads"
+with its step time and every kernel's duration and HBM fraction.  Prints ONE
+JSON line on stdout; progress goes to stderr.  `--eager-passes N` only runs N
+eager passes (for profiler runs); `--calibrate-copy MIB` times a device copy.
 """
 from __future__ import annotations
 
@@ -71,9 +75,14 @@ def conv_products(cnt_map: np.ndarray, pl, groups: int) -> int:
 
 def layer_costs(net, bufs, cfg) -> dict:
     """Algorithmic bytes (and products) per launch of every kernel, from the
-    actual non-zero counts of this batch."""
+    actual non-zero counts of this batch.  "bytes" is what the launch must move
+    (its inputs, the packed table, the bias and what it writes: lists or dense
+    outputs); "bytes_dense_out" counts a layer as if it wrote its dense sums
+    after pooling instead (lists or dense input in + table + bias + 4 B per
+    output), the per-layer form of the multiply-route-sum byte count."""
     import torch
     costs = {}
+    dense8 = {}
     for li, (p, pl) in enumerate(zip(net.packed, net.plans)):
         s = p.spec
         is_int = p.aug.dtype == torch.int16          # int8 weights/activations
@@ -95,6 +104,7 @@ def layer_costs(net, bufs, cfg) -> dict:
             if not pl.in_lists:
                 costs[f"{s.name}.compact"] = {"bytes": rows * c * es + lists}
             mrs_bytes = lists + table + bias + out_elems * 4
+        dense8[s.name] = mrs_bytes
         prods = conv_products(cnt.reshape(b, h, w), pl, s.c_out // s.n)
         if s.k is not None and pl.dense_kernel:
             # one launch: dense input, weights, the k-WTA output (lists or dense)
@@ -106,7 +116,8 @@ def layer_costs(net, bufs, cfg) -> dict:
                 obytes = out_elems * ob
             sums = out_elems * 4 if net.keep_sums else 0
             costs[f"{s.name}.dense_kwta"] = {"bytes": rows * c * es + table + bias + sums + obytes,
-                                             "products": prods, "int": is_int}
+                                             "products": prods, "int": is_int,
+                                             "bytes_dense_out": mrs_bytes}
             continue
         if s.k is not None and not pl.dense_kernel:
             # one launch: lists in, table, bias, the k-WTA output (lists or
@@ -119,9 +130,10 @@ def layer_costs(net, bufs, cfg) -> dict:
                 obytes = out_elems * ob
             sums = out_elems * 4 if net.keep_sums else 0
             costs[f"{s.name}.mrs_kwta"] = {"bytes": mrs_bytes - out_elems * 4 + sums + obytes,
-                                           "products": prods, "int": is_int}
+                                           "products": prods, "int": is_int,
+                                           "bytes_dense_out": mrs_bytes}
             continue
-        costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods,
+        costs[f"{s.name}.mrs"] = {"bytes": mrs_bytes, "products": prods, "bytes_dense_out": mrs_bytes,
                                   "int": is_int, "lists_in": 0 if pl.dense_kernel else lists}
         if s.k is not None:
             if pl.emit_lists:
@@ -131,37 +143,38 @@ def layer_costs(net, bufs, cfg) -> dict:
             else:
                 ob = 1 if s.shift is not None else 4
                 costs[f"{s.name}.kwta"] = {"bytes": out_elems * (4 + ob)}
-    # a call that runs two layers (a layer and the last layer on its winners):
-    # both layers' bytes, less the second one's list reads (they stay on chip)
+    # a call that runs several layers: all their bytes, less the later layers'
+    # reads of lists that stay on chip
+    names = [p.spec.name for p in net.packed]
     for li, pl in enumerate(net.plans):
         if pl.fuse_next2:
-            # three layers: all their bytes, less the last one's list reads
-            # (on chip); the middle layer reads the first one's lists back
-            c = costs[f"{net.packed[li].spec.name}.mrs_kwta"]
-            a = costs[f"{net.packed[li + 1].spec.name}.mrs_kwta"]
-            z = costs[f"{net.packed[li + 2].spec.name}.mrs"]
-            costs[f"{net.packed[li].spec.name}.mrs_kwta+{net.packed[li + 1].spec.name}.mrs_kwta+"
-                  f"{net.packed[li + 2].spec.name}.mrs"] = {
+            c = costs[f"{names[li]}.mrs_kwta"]
+            a = costs[f"{names[li + 1]}.mrs_kwta"]
+            z = costs[f"{names[li + 2]}.mrs"]
+            costs[f"{names[li]}.mrs_kwta+{names[li + 1]}.mrs_kwta+{names[li + 2]}.mrs"] = {
                 "bytes": c["bytes"] + a["bytes"] + z["bytes"] - z["lists_in"],
-                "products": c["products"] + a["products"] + z["products"], "int": c["int"]}
+                "products": c["products"] + a["products"] + z["products"], "int": c["int"],
+                "bytes_dense_out": sum(dense8[names[li + i]] for i in range(3))}
     for li, pl in enumerate(net.plans):
         if pl.fuse_next3:
             # the dense first layer and the three-layer tail: bytes of both;
             # the products counted are the routed ones (VALU work), the first
             # layer's dense multiply-adds run on the matrix cores
-            names = [net.packed[li + i].spec.name for i in range(4)]
-            d = costs[f"{names[0]}.dense_kwta"]
-            t = costs[f"{names[1]}.mrs_kwta+{names[2]}.mrs_kwta+{names[3]}.mrs"]
-            costs[f"{names[0]}.dense_kwta+{names[1]}.mrs_kwta+{names[2]}.mrs_kwta+{names[3]}.mrs"] = {
+            d = costs[f"{names[li]}.dense_kwta"]
+            t = costs[f"{names[li + 1]}.mrs_kwta+{names[li + 2]}.mrs_kwta+{names[li + 3]}.mrs"]
+            costs[f"{names[li]}.dense_kwta+{names[li + 1]}.mrs_kwta+{names[li + 2]}.mrs_kwta+"
+                  f"{names[li + 3]}.mrs"] = {
                 "bytes": d["bytes"] + t["bytes"], "products": t["products"], "int": t["int"],
-                "mfma_macs": d["products"]}
+                "mfma_macs": d["products"],
+                "bytes_dense_out": sum(dense8[names[li + i]] for i in range(4))}
     for li, pl in enumerate(net.plans):
         if pl.fuse_next:
-            a = costs[f"{net.packed[li].spec.name}.mrs_kwta"]
-            z = costs[f"{net.packed[li + 1].spec.name}.mrs"]
-            costs[f"{net.packed[li].spec.name}.mrs_kwta+{net.packed[li + 1].spec.name}.mrs"] = {
+            a = costs[f"{names[li]}.mrs_kwta"]
+            z = costs[f"{names[li + 1]}.mrs"]
+            costs[f"{names[li]}.mrs_kwta+{names[li + 1]}.mrs"] = {
                 "bytes": a["bytes"] + z["bytes"] - z["lists_in"],
-                "products": a["products"] + z["products"], "int": a["int"]}
+                "products": a["products"] + z["products"], "int": a["int"],
+                "bytes_dense_out": dense8[names[li]] + dense8[names[li + 1]]}
     return costs
 
 
@@ -225,6 +238,9 @@ def dense_macs(cfg) -> int:
 def roofline_for(name: str, cost: dict, ms: float) -> dict:
     sec = ms * 1e-3
     gbs = cost["bytes"] / sec / 1e9
+    extra = {}
+    if "bytes_dense_out" in cost:
+        extra["hbm_frac_dense_out"] = round(cost["bytes_dense_out"] / sec / 1e9 / HBM_PEAK_GBS, 4)
     if "products" in cost:
         # ridge: products per byte above which the VALU roof is the lower one
         if cost["int"]:
@@ -238,12 +254,14 @@ def roofline_for(name: str, cost: dict, ms: float) -> dict:
             ach = ops / sec / 1e12
             return {"bound": "alu", "achieved": round(ach, 3), "peak": peak_ops,
                     "unit": "TOP/s" if cost["int"] else "TFLOP/s", "frac": round(ach / peak_ops, 4),
-                    "traffic": None, "kernel": name, "algorithmic_bytes": cost["bytes"],
-                    "products": cost["products"], "hbm_gbs": round(gbs, 1),
+                    "traffic": None, "kernel": name, "us": round(ms * 1e3, 2),
+                    "algorithmic_bytes": cost["bytes"], "products": cost["products"],
+                    "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), **extra,
                     **({"mfma_macs": cost["mfma_macs"]} if "mfma_macs" in cost else {})}
     return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": name,
-            "algorithmic_bytes": cost["bytes"], **({"products": cost["products"]} if "products" in cost else {})}
+            "us": round(ms * 1e3, 2), "algorithmic_bytes": cost["bytes"], **extra,
+            **({"products": cost["products"]} if "products" in cost else {})}
 
 
 def load_traffic(kernel: str, workload: str):
@@ -263,15 +281,18 @@ def load_traffic(kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(cfg, inp, seconds: float) -> dict:
-    """The CPU oracle (as it stands) on the whole batch, repeated until about
-    `seconds` of work; samples/s over all repetitions."""
-    from oracle import networks
+def cpu_model() -> str:
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_rate(cfg, inp, seconds: float):
+    from oracle import networks
     reps, t0 = 0, time.perf_counter()
     while True:
         networks.run_chain(cfg.layers, inp["x"], inp["W"], inp["b"])
@@ -279,10 +300,32 @@ def cpu_baseline(cfg, inp, seconds: float) -> dict:
         el = time.perf_counter() - t0
         if el >= seconds or reps >= 50:
             break
-    return {"value": round(reps * cfg.batch / el, 2), "unit": "samples/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{reps} x full batch of {cfg.batch} ({cfg.name}), float64 numpy oracle, "
-                      f"{el:.1f} s on {os.cpu_count()} host CPUs (BLAS threads {threads})"}
+    return reps, el
+
+
+def cpu_baseline(cfg, inp, seconds: float) -> dict:
+    """The CPU oracle (as it stands) on whole batches of the workload, repeated
+    for about `seconds`: once with the BLAS threads numpy starts with (all
+    host cores), once on one core (one BLAS thread, the process pinned to
+    one CPU).  samples/s over all repetitions."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    reps, el = _oracle_rate(cfg, inp, seconds)
+    res = {"value": round(reps * cfg.batch / el, 2), "unit": "samples/s", "cores": int(threads),
+           "kind": "oracle", "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+           "sample": f"{reps} x full batch of {cfg.batch} ({cfg.name}), float64 numpy oracle, "
+                     f"{el:.1f} s, BLAS threads {threads}"}
+    aff = os.sched_getaffinity(0)
+    try:
+        os.sched_setaffinity(0, {min(aff)})
+        with threadpool_limits(limits=1):
+            reps1, el1 = _oracle_rate(cfg, inp, seconds)
+    finally:
+        os.sched_setaffinity(0, aff)
+    res["one_core"] = {"value": round(reps1 * cfg.batch / el1, 2), "unit": "samples/s",
+                       "cores": 1, "sample": f"{reps1} x full batch of {cfg.batch}, {el1:.1f} s, "
+                                             "one BLAS thread, pinned to one CPU"}
+    return res
 
 
 def ab_reorder(cfg, inp, x, kernel_ms, breakdown) -> dict:
@@ -317,78 +360,70 @@ def ab_reorder(cfg, inp, x, kernel_ms, breakdown) -> dict:
             "routed_us": round(routed * 1e3, 2), "table_entries_per_output": int(table.shape[1])}
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, help="workload id (default 2: keyword-spotting CNN)")
-    ap.add_argument("--rotate-mib", type=float, default=512.0)
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--ab-reorder", action="store_true",
-                    help="also time the first layer by reordering the activations instead of "
-                         "routing the products (fp32 dense-input 64-channel layers)")
-    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
-                    help="only copy a MIB-sized device buffer --steps times (reference kernel "
-                         "for scaling the HBM byte counters)")
-    args = ap.parse_args()
+MALL_MIB = 256.0                    # MI355X Infinity Cache (last-level cache)
+SET_MEM_CAP = 24 << 30              # most device memory the rotating buffer sets may take
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
-              "the sparse-sparse path shards over samples with no exchange, so N GPUs run N "
-              "independent copies of this measurement.", file=sys.stderr)
-        return 2
 
+def scrub(buf) -> None:
+    """Write a buffer twice the size of the last-level cache, so that no
+    earlier launch's data is still cached (outside every timed region)."""
+    buf.fill_(1)
+
+
+def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0,
+            ab: bool = False) -> dict:
+    """One workload: the whole chain, K timed passes, per-kernel durations.
+
+    Buffer sets (input + every intermediate) rotate; their number is chosen
+    from the bytes one pass actually touches (the sum of its launches'
+    algorithmic bytes) so that a set is reused only after more than
+    `rotate_mib` of other data, and a 512 MiB scrub precedes every timed
+    region, so no pass finds its data in the 256 MiB Infinity Cache or in L2."""
     import torch
 
     from paper_2112_13896_amd.network import Network
-    from workloads import CONFIGS, generate
+    from workloads import generate
 
-    if not torch.cuda.is_available():
-        log("bench.py needs a GPU")
-        return 1
-    if args.calibrate_copy > 0:
-        nbytes = int(args.calibrate_copy * 2 ** 20) // 16 * 16
-        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        el = time.perf_counter() - t0
-        print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes,
-                          "launches": args.steps,
-                          "GB/s": round(2 * nbytes * args.steps / el / 1e9, 1)}), flush=True)
-        return 0
-    cfg = CONFIGS[args.config]
     log(f"bench: workload {cfg.name}, batch {cfg.batch}")
     inp = generate(cfg)
     net = Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch, keep_sums=False)
-    per_set = net.bufs.nbytes() + inp["x"].nbytes
-    nsets = max(8, math.ceil(args.rotate_mib * 2 ** 20 / per_set))
+    x0 = torch.from_numpy(inp["x"]).cuda()
+    net.forward(x0, net.bufs)
+    torch.cuda.synchronize()
+    costs = layer_costs(net, net.bufs, cfg)
+    names0 = [nm for li in range(len(net.packed)) for nm, _ in net.launches(
+        li, x0 if li == 0 else None, net.bufs)]
+    touched = sum(costs[nm]["bytes"] for nm in names0 if nm in costs)
+    alloc = net.bufs.nbytes() + inp["x"].nbytes
+    nsets = max(8, math.ceil(rotate_mib * 2 ** 20 / max(touched, 1)))
+    nsets = max(2, min(nsets, 512, SET_MEM_CAP // max(alloc, 1)))
     sets = [net.bufs] + [net.make_buffers() for _ in range(nsets - 1)]
-    xs = [torch.from_numpy(inp["x"]).cuda() for _ in range(nsets)]
-    log(f"bench: {nsets} rotating buffer sets of {per_set / 2 ** 20:.1f} MiB")
-
-    for i in range(args.warmup):
+    # a different input per set: the batch rolled by j samples (same work)
+    xs = [x0] + [torch.from_numpy(np.roll(inp["x"], j, axis=0)).cuda() for j in range(1, nsets)]
+    log(f"bench: {nsets} rotating buffer sets, {touched / 2 ** 20:.2f} MiB touched per pass "
+        f"({alloc / 2 ** 20:.1f} MiB allocated per set)")
+    for j in range(nsets):                           # every set holds a whole pass's data
+        net.forward(xs[j], sets[j])
+    torch.cuda.synchronize()
+    scrub_buf = torch.empty(int(2 * MALL_MIB * 2 ** 20) // 4, dtype=torch.int32, device="cuda")
+    if eager_only:
+        # profiler mode: eager passes only (every launch a plain dispatch)
+        t0 = time.perf_counter()
+        for i in range(eager_only):
+            net.forward(xs[i % nsets], sets[i % nsets])
+        torch.cuda.synchronize()
+        return {"workload": cfg.name, "eager_passes": eager_only,
+                "ms_per_pass_eager": round((time.perf_counter() - t0) * 1e3 / eager_only, 4)}
+    for i in range(warmup):
         net.forward(xs[i % nsets], sets[i % nsets])
     torch.cuda.synchronize()
-    # one HIP graph per buffer set: a step is one replay (every layer's kernels,
-    # no per-launch host work)
+    # one HIP graph per buffer set: one pass per replay
     graphs = [net.capture(xs[j], sets[j]) for j in range(nsets)]
-    # and one graph of the passes over all the sets in turn, two streams:
-    # a pass's first launch on the capture stream, the rest on a second
-    # stream after it, so that the next pass's first launch (another buffer
-    # set) can run beside the rest of this one
-    gsteps = args.steps if args.steps <= 256 else nsets
+    # the timed steps: one graph of all the passes, pass i on set i % nsets,
+    # in the fastest of three schedules
+    gsteps = steps if steps <= 256 else nsets
     g_mode = {m: capture_passes(net, xs, sets, gsteps, m)
               for m in ("sequential", "overlapped", "alternate")}
-    for i in range(args.warmup):
-        graphs[i % nsets].replay()
-    # the faster of the two schedules of the all-sets graph (a few replays each)
     sched = {}
     for name, g in g_mode.items():
         g.replay()
@@ -400,49 +435,56 @@ def main() -> int:
         sched[name] = time.perf_counter() - t0
     schedule = min(sched, key=sched.get)
     g_all = g_mode[schedule]
-    log(f"bench: schedule {schedule} ({', '.join(f'{k} {v * 1e6 / (3 * gsteps):.1f} us' for k, v in sched.items())} per step)")
+    log(f"bench: schedule {schedule} ("
+        + ", ".join(f"{k} {v * 1e6 / (3 * gsteps):.1f} us" for k, v in sched.items())
+        + " per step, cache-warm)")
 
-    # per-kernel durations: each launch recorded KREP times into a graph of its
-    # own, replayed with HIP events on the replaying stream around it
-    def kernel_ms(call, reps=4):
+    scrub(scrub_buf)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps // gsteps):
+        g_all.replay()
+    for i in range(steps % gsteps):
+        graphs[i % nsets].replay()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    # the same steps with one graph launch each
+    scrub(scrub_buf)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        graphs[i % nsets].replay()
+    torch.cuda.synchronize()
+    ms_step_1 = (time.perf_counter() - t0) * 1e3 / steps
+
+    # per-kernel durations, cache-cold: a graph of one launch of the kernel per
+    # buffer set (min(nsets, 32) sets), timed with HIP events on the replaying
+    # stream, each replay after a scrub
+    per_set = [dict(nc for li in range(len(net.packed)) for nc in net.launches(
+        li, xs[j] if li == 0 else None, sets[j])) for j in range(nsets)]
+    nk = min(nsets, 32)
+
+    def kernel_ms(name, reps=4):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            for _ in range(KREP):
-                call()
+            for j in range(nk):
+                per_set[j][name]()
         g.replay()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
+        tot = 0.0
         for _ in range(reps):
+            scrub(scrub_buf)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
             g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / (reps * KREP)
+            e1.record()
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1)
+        return tot / (reps * nk)
 
-    launches = [nc for li in range(len(net.packed)) for nc in net.launches(
-        li, xs[0] if li == 0 else None, sets[0])]
-    breakdown = {name: kernel_ms(call) for name, call in launches}
+    breakdown = {name: kernel_ms(name) for name in names0}
     dominant = max(breakdown, key=breakdown.get)
-    costs = layer_costs(net, sets[0], cfg)
-    log("bench: per-kernel ms " + ", ".join(f"{k}={v:.4f}" for k, v in breakdown.items()))
-
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps // gsteps):
-        g_all.replay()
-    for i in range(args.steps % gsteps):
-        graphs[i % nsets].replay()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / args.steps
-    samples_s = cfg.batch / (ms_step * 1e-3)
-    # the same steps with one graph launch each
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        graphs[i % nsets].replay()
-    torch.cuda.synchronize()
-    ms_step_1 = (time.perf_counter() - t0) * 1e3 / args.steps
-    # the dominant kernel again, right after the timed steps
-    dom_ms = kernel_ms(dict(launches)[dominant], reps=max(4, args.steps // KREP))
+    log("bench: per-kernel ms (cold) " + ", ".join(f"{k}={v:.4f}" for k, v in breakdown.items()))
+    dom_ms = kernel_ms(dominant, reps=max(4, steps // 4))
     roof = roofline_for(dominant, costs[dominant], dom_ms)
     roof["traffic"] = load_traffic(dominant, cfg.name)
     kernels = {}
@@ -450,25 +492,128 @@ def main() -> int:
         c = costs.get(k, {})
         e = {"us": round(ms * 1e3, 2)}
         if "bytes" in c:
-            e["GB/s"] = round(c["bytes"] / (ms * 1e-3) / 1e9, 1)
+            e["bytes"] = c["bytes"]
+            e["hbm_frac"] = round(c["bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        if "bytes_dense_out" in c:
+            e["bytes_dense_out"] = c["bytes_dense_out"]
+            e["hbm_frac_dense_out"] = round(c["bytes_dense_out"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
         if "products" in c:
             e["Gproducts/s"] = round(c["products"] / (ms * 1e-3) / 1e9, 1)
         kernels[k] = e
+    rec = {"workload": cfg.name, "batch": cfg.batch, "steps": steps,
+           "ms_per_step": round(ms_step, 4), "samples_per_s": round(cfg.batch / (ms_step * 1e-3), 1),
+           "dense_equiv_gmac_per_s": round(dense_macs(cfg) / (ms_step * 1e-3) / 1e9, 1),
+           "ms_per_step_one_launch_per_step": round(ms_step_1, 4), "schedule": schedule,
+           "buffer_sets": nsets, "touched_bytes_per_pass": int(touched),
+           "roofline": roof, "kernels": kernels}
+    if ab:
+        rec["ab_reorder"] = ab_reorder(cfg, inp, xs[0], lambda call: _time_call(call),
+                                       breakdown)
+    rec["_inp"] = inp
+    return rec
+
+
+def _time_call(call, reps=4) -> float:
+    import torch
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(KREP):
+            call()
+    g.replay()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / (reps * KREP)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload id (default 2: keyword-spotting CNN)")
+    ap.add_argument("--also", default="1,3,4,5",
+                    help="other workloads measured after the headline one and reported in "
+                         "\"workloads\" (comma-separated ids; empty for none)")
+    ap.add_argument("--rotate-mib", type=float, default=512.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager-passes", type=int, default=0, metavar="N",
+                    help="profiler mode: only N eager passes of the workload (no graphs, no timing)")
+    ap.add_argument("--ab-reorder", action="store_true",
+                    help="also time the first layer by reordering the activations instead of "
+                         "routing the products (fp32 dense-input 64-channel layers)")
+    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer --steps times (reference kernel "
+                         "for scaling the HBM byte counters, and the copy ceiling)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
+              "the sparse-sparse path shards over samples with no exchange, so N GPUs run N "
+              "independent copies of this measurement.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from workloads import CONFIGS
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        return 1
+    if args.calibrate_copy > 0:
+        nbytes = int(args.calibrate_copy * 2 ** 20) // 16 * 16
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        sec = e0.elapsed_time(e1) * 1e-3
+        print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes,
+                          "launches": args.steps,
+                          "GB/s": round(2 * nbytes * args.steps / sec / 1e9, 1)}), flush=True)
+        return 0
+    cfg = CONFIGS[args.config]
+    if args.eager_passes:
+        print(json.dumps(measure(cfg, args.steps, args.warmup, args.rotate_mib,
+                                 eager_only=args.eager_passes)), flush=True)
+        return 0
+    head = measure(cfg, args.steps, args.warmup, args.rotate_mib, ab=args.ab_reorder)
+    inp = head.pop("_inp")
     res = {
-        "metric": METRIC, "value": round(samples_s, 1), "unit": "samples/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "metric": METRIC, "value": head["samples_per_s"], "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "i8*i8->i32" if cfg.dtype == "i8" else "f32",
         "data": "synthetic (seeded; stands in for the paper's dataset)",
         "config": {"workload": cfg.name, "batch": cfg.batch, "layers": [s.name for s in cfg.layers]},
-        "dense_equiv_gmac_per_s": round(dense_macs(cfg) / (ms_step * 1e-3) / 1e9, 1),
-        "ms_per_step_one_launch_per_step": round(ms_step_1, 4),
-        "schedule": schedule,
-        "roofline": roof,
-        "kernels": kernels,
+        "dense_equiv_gmac_per_s": head["dense_equiv_gmac_per_s"],
+        "ms_per_step_one_launch_per_step": head["ms_per_step_one_launch_per_step"],
+        "schedule": head["schedule"],
+        "buffer_sets": head["buffer_sets"],
+        "touched_bytes_per_pass": head["touched_bytes_per_pass"],
+        "roofline": head["roofline"],
+        "kernels": head["kernels"],
     }
-    if args.ab_reorder:
-        res["ab_reorder"] = ab_reorder(cfg, inp, xs[0], kernel_ms, breakdown)
+    if "ab_reorder" in head:
+        res["ab_reorder"] = head["ab_reorder"]
+    others = [int(c) for c in args.also.split(",") if c.strip() and int(c) != args.config]
+    if others:
+        res["workloads"] = {}
+        for cid in others:
+            sub = measure(CONFIGS[cid], min(args.steps, 20), min(args.warmup, 5), args.rotate_mib)
+            sub.pop("_inp")
+            res["workloads"][sub.pop("workload")] = sub
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)
