@@ -196,7 +196,13 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
  *          whose window is the whole unpadded input map, output 1 x 1, no
  *          pool - a linear layer; 4 input-stationary int8 convolution; 5 one
  *          wavefront per item: a 1x1 layer with many items and a k-WTA over
- *          rows of more than 128 or k > 32); for paths 3 and
+ *          rows of more than 128 or k > 32; 6 fp32 layer without pooling,
+ *          sets and kernels per set powers of two, n <= 16, c_out <= 256:
+ *          tiles complete in the channel dimension with the packed table
+ *          streamed through LDS in blocks of rows, k-WTA in the epilogue);
+ *          for path 6: [1] k-WTA selection (1-3 four lanes per row with
+ *          top-8/16/32 lists, 4 sixteen lanes per row), [2] table rows per block, [3] blocks, [6]
+ *          workgroups, [7] LDS bytes, [8] sets per lane; for paths 3 and
  *          5: [6] workgroups, [7] LDS bytes per workgroup, [8] entry slices
  *          per packed set; for path 4: [2] output rows per band, [6]
  *          workgroups, [7] LDS bytes, [8] sets per lane; for path 2: [1] tile mode (0 rows of

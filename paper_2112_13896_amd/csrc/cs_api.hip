@@ -14,6 +14,7 @@
 #include "conv_dense_mfma.h"
 #include "cs.h"
 #include "kwta_kernels.h"
+#include "mrs_blocks.h"
 #include "mrs_chain.h"
 #include "mrs_fused.h"
 #include "mrs_reorder.h"
@@ -457,6 +458,150 @@ int launch_fused(const FusedPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stre
   return launch_status();
 }
 
+// ------------------------------------------------ fp32 layers, table in row blocks
+// A fp32 layer without pooling whose sets and kernels per set are powers of
+// two: tiles of pixels complete in the channel dimension, the packed table
+// streamed through LDS in blocks of rows, k-WTA over rows of up to 256
+// channels in the epilogue (mrs_blocks.h).
+struct BlocksPlan {
+  cs::BlocksArgs ba;
+  int gb;
+  int64_t blocks;
+  size_t shmem;
+};
+
+int ilog2_exact(int64_t v) {                    // log2 of a power of two, else -1
+  if (v < 1) return -1;
+  int l = 0;
+  while ((1LL << l) < v) ++l;
+  return (1LL << l) == v ? l : -1;
+}
+
+// ocap: capacity of the output lists (0: dense output or sums only); lvec:
+// the output lists take 8-byte index and 16-byte value stores.
+bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const void* y, int k,
+                 int write_sums, int ocap, bool lvec, BlocksPlan* pl) {
+  if (xt != CS_F32 || geo.pool != 1) return false;
+  const int n = geo.n, G = geo.G;
+  const int log2n = ilog2_exact(n), log2G = ilog2_exact(G);
+  if (log2n < 0 || log2G < 1 || n > 16 || geo.c_out > 256) return false;
+  if (geo.cap % 4 != 0 || !aligned(aug, 16) || !aligned(y, 4)) return false;
+  const int T = geo.KH * geo.KW;
+  const int64_t R = (int64_t)T * geo.C;
+  const int64_t items = (int64_t)geo.B * geo.Ho * geo.Wo;
+  const int64_t in_rows = (int64_t)geo.B * geo.H * geo.W;
+  if (items * geo.c_out >= INT32_MAX || in_rows * geo.cap >= INT32_MAX || R * G >= INT32_MAX)
+    return false;
+  // sets per lane: two (four when the lane count per pixel would pass 64)
+  int gb = G >= 2 ? 2 : 1;
+  while (gb < 4 && G / gb > 64) gb *= 2;
+  if (gb * n > 64 || G / gb > cs::BLK_BD) return false;   // offsets fit 16 bits
+  const int U = G / gb;
+  // rows per block: the whole table if it fits one workgroup's share of LDS
+  // (two workgroups per compute unit); else blocks of at most BLK_ENTRIES
+  // entries (the next block waits in registers), double-buffered when two
+  // fit, else one buffer refilled between two barriers: whole taps if a tap
+  // fits, else a channel range dividing C
+  const int tstride = G;                                  // 8-byte entries per row
+  const size_t acc_b = (size_t)gb * n * cs::BLK_BD * 4;
+  const size_t budget = kCuLds / 2;
+  const size_t fixed = acc_b + round16((size_t)geo.c_out * 4);
+  auto lds_for = [&](int64_t rows, int nbuf) {
+    return fixed + nbuf * round16((size_t)rows * tstride * 8);
+  };
+  const int max_rows = cs::BLK_ENTRIES / G;
+  int64_t RB = 0;
+  int tpb = 0, cblocks = 0, nbuf = 1;
+  if (lds_for(R, 1) <= budget) {
+    RB = R;
+    tpb = T;
+  } else if (geo.C <= max_rows && lds_for(geo.C, 1) <= budget) {
+    tpb = max_rows / geo.C;
+    if (tpb > T) tpb = T;
+    while (tpb > 1 && lds_for((int64_t)tpb * geo.C, 1) > budget) --tpb;
+    RB = (int64_t)tpb * geo.C;
+    nbuf = lds_for(RB, 2) <= budget ? 2 : 1;
+  } else {
+    RB = geo.C < max_rows ? geo.C : max_rows;
+    while (RB >= 4 && (geo.C % RB != 0 || lds_for(RB, 1) > budget)) --RB;
+    if (RB < 4) return false;
+    cblocks = (int)(geo.C / RB);
+    nbuf = lds_for(RB, 2) <= budget ? 2 : 1;
+  }
+  const int64_t nblocks = (R + RB - 1) / RB;
+  if (nblocks == 1) nbuf = 1;
+  const size_t tb = round16((size_t)RB * tstride * 8);
+  cs::BlocksArgs& ba = pl->ba;
+  ba.log2U = ilog2_exact(U);
+  ba.P = cs::BLK_BD / U;
+  ba.items = (int)items;
+  ba.RB = (int)RB;
+  ba.nblocks = (int)nblocks;
+  ba.tpb = tpb;
+  ba.cblocks = cblocks;
+  ba.tstride = tstride;
+  ba.nbuf = nbuf;
+  ba.log2n = log2n;
+  ba.log2G = log2G;
+  ba.k = k;
+  ba.write_sums = write_sums;
+  // k-WTA: four lanes per row (the gather kernel's selection) for rows of at
+  // most 128 channels and k <= 32, else sixteen lanes per row
+  const bool quad = k >= 0 && geo.c_out <= 128 && k <= 32 && (ocap == 0 || (ocap % 4 == 0 && lvec));
+  ba.kmode = !quad ? 4 : (k <= 8 ? 1 : (k <= 16 ? 2 : 3));
+  ba.kp = geo.c_out <= 64 ? 4 : (geo.c_out <= 128 ? 8 : 16);
+  ba.ostride = geo.c_out + 1;                             // odd: conflict-free row reads
+  ba.off_t0 = (uint32_t)acc_b;
+  ba.off_t1 = (uint32_t)(acc_b + (nbuf - 1) * tb);
+  ba.off_bias = (uint32_t)(acc_b + nbuf * tb);
+  size_t end = ba.off_bias + round16((size_t)geo.c_out * 4);
+  // the four-lane epilogue's tile, selections and lists over the table blocks
+  const int P = cs::BLK_BD / U;
+  ba.off_out = (uint32_t)acc_b;
+  ba.off_sel = ba.off_out + (uint32_t)round16((size_t)P * ba.ostride * 4);
+  ba.off_lidx = ba.off_sel + (uint32_t)round16((size_t)P * 8);
+  ba.off_lval = ba.off_lidx + (uint32_t)round16((size_t)P * ocap * 2);
+  const size_t epi_end = ba.off_lval + round16((size_t)P * ocap * 4);
+  if (quad && epi_end > ba.off_bias) {
+    // the epilogue region would reach the bias: put the bias after it
+    ba.off_bias = (uint32_t)round16(epi_end);
+    end = ba.off_bias + round16((size_t)geo.c_out * 4);
+  }
+  ba.fd_wo = cs::make_fastdiv((uint32_t)geo.Wo);
+  ba.fd_ho = cs::make_fastdiv((uint32_t)geo.Ho);
+  ba.fd_kw = cs::make_fastdiv((uint32_t)geo.KW);
+  ba.fd_cout = cs::make_fastdiv((uint32_t)geo.c_out);
+  ba.fd_ochunks = cs::make_fastdiv((uint32_t)(ocap >= 4 ? ocap / 4 : 1));
+  pl->gb = gb;
+  pl->shmem = end;
+  pl->blocks = (items + ba.P - 1) / ba.P;
+  return pl->shmem <= kBlockLds * 2 && pl->blocks < INT32_MAX;
+}
+
+int launch_blocks(const BlocksPlan& pl, hipStream_t stream, const uint16_t* idx,
+                  const void* lval, const int32_t* cnt, const void* aug, const void* bias,
+                  void* y, void* out, const cs::ListOut& lo, const cs::ConvGeom& geo) {
+  const dim3 grid((unsigned)pl.blocks), block(cs::BLK_BD);
+  const float* lv = static_cast<const float*>(lval);
+  const uint2* pa = static_cast<const uint2*>(aug);
+  const float* bs = static_cast<const float*>(bias);
+  float* yy = static_cast<float*>(y);
+  float* oo = static_cast<float*>(out);
+#define CS_BLOCKS(GB_, CH_)                                                              \
+  hipLaunchKernelGGL((cs::mrs_blocks_f32<float, GB_, CH_>), grid, block, pl.shmem, stream, idx, \
+                     lv, cnt, pa, bs, yy, oo, lo, geo, pl.ba)
+  const bool ch = pl.ba.tpb == 0;
+  if (pl.gb == 1) {
+    if (ch) CS_BLOCKS(1, true); else CS_BLOCKS(1, false);
+  } else if (pl.gb == 2) {
+    if (ch) CS_BLOCKS(2, true); else CS_BLOCKS(2, false);
+  } else {
+    if (ch) CS_BLOCKS(4, true); else CS_BLOCKS(4, false);
+  }
+#undef CS_BLOCKS
+  return launch_status();
+}
+
 // ------------------------------------------------ one sample per workgroup
 // A layer whose output is one vector per sample (a linear layer, or a
 // convolution whose window is the whole unpadded input map) runs with one
@@ -844,6 +989,10 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
     return launch_rows(rp, CS_I32, stream, idx, lval, cnt, aug, bias, y, nullptr,
                        cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   if (lists_vectorisable(xt, idx, lval, geo.cap)) {
+    BlocksPlan bp;
+    if (blocks_plan(geo, xt, aug, y, -1, 1, 0, false, &bp))
+      return launch_blocks(bp, stream, idx, lval, cnt, aug, bias, y, nullptr,
+                           cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
     FusedPlan fp;
     if (fused_plan(geo, xt, aug, y, -1, 0, 1, 0, 0, &fp))
       return launch_fused(fp, xt, xt, stream, idx, lval, cnt, aug, bias, y, nullptr,
@@ -1065,6 +1214,12 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
     if (rows_plan(geo, xt, aug, k, shift, keep_sums, &rp))
       return launch_rows(rp, ot, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
+  if (lists_vectorisable(xt, idx, lval, cap)) {
+    BlocksPlan bp;
+    const bool lvec = lists && aligned(oidx, 8) && aligned(oval, 16);
+    if (blocks_plan(geo, xt, aug, y, k, keep_sums, lists ? ocap : 0, lvec, &bp))
+      return launch_blocks(bp, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
   if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
     FusedPlan fp;
     if (fused_plan(geo, xt, aug, y, k, shift, keep_sums, lists ? ocap : 0, osz, &fp))
@@ -1117,6 +1272,18 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
     info[6] = rp.blocks;
     info[7] = (int64_t)rp.shmem;
     info[8] = rp.cpl;
+    return CS_OK;
+  }
+  BlocksPlan bp;
+  if (cap % 4 == 0 && blocks_plan(geo, xt, nullptr, nullptr, k, 1, k >= 0 ? (k + 3) / 4 * 4 : 0,
+                                  true, &bp)) {
+    info[1] = bp.ba.kmode;
+    info[0] = 6;
+    info[2] = bp.ba.RB;
+    info[3] = bp.ba.nblocks;
+    info[6] = bp.blocks;
+    info[7] = (int64_t)bp.shmem;
+    info[8] = bp.gb;
     return CS_OK;
   }
   FusedPlan fp;

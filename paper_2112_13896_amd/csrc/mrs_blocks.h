@@ -1,0 +1,550 @@
+// One fp32 layer in one kernel: Multiply, Route and Sum (Section 3.2 steps
+// 3-5) with the packed table streamed through LDS in blocks of rows, then
+// bias, k-WTA (Section 3.3.3) and the winners written as the next layer's
+// (index, value) lists (Figure 10) or densely.
+//
+//  * tile: P consecutive output pixels per workgroup, complete in the channel
+//    dimension (every set), so k-WTA needs no round trip through HBM;
+//  * lanes: (pixel, unit of GB sets), the U = G / GB lanes of a pixel
+//    adjacent (they read the same list entries);
+//  * table: the augmented tensor (value + Kernel ID per slot, Section 3.3.1)
+//    is staged in blocks of RB slot rows - whole taps, or a channel range of
+//    one tap - as a value array and an array of 16-bit accumulator offsets
+//    (the Kernel ID already turned into the byte offset of its accumulator
+//    row), double-buffered: the next block's loads are in flight while the
+//    current block is used, one barrier per block.  A block's slots are
+//    visited in list order (a list is in ascending channel order), so a lane
+//    keeps its place in a tap's list from one channel block to the next;
+//  * Route / Sum: the accumulators of a lane are LDS columns acc[j*n + kid]
+//    [lane] (a bank is a function of the lane only).  fp32 has no fast LDS
+//    atomic here, so each product is a read-add-write of the lane's own
+//    column; the four entries of a list chunk are done together (all reads,
+//    then the writes in entry order), and an entry whose Kernel ID equals an
+//    earlier one of the chunk adds onto that entry's new value instead of
+//    the value read - the same sums, in the same order, as one entry after
+//    another, without a round trip per product;
+//  * epilogue: one wavefront per pixel row, each lane holding KPL
+//    consecutive channels; the k-th largest order-preserving key is found bit
+//    by bit (counts of keys >= a candidate by ballot), ties go to the lower
+//    index, and the list positions come from wavefront prefix sums.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fastdiv.h"
+#include "kwta_kernels.h"
+#include "mrs_fused.h"
+#include "mrs_kernels.h"
+#include "wave_ops.h"
+
+namespace cs {
+
+constexpr int BLK_BD = 256;       // threads per workgroup
+constexpr int BLK_STAGE = 8;      // 16-byte table loads per thread per block (at most)
+constexpr int BLK_ENTRIES = BLK_BD * BLK_STAGE * 2;   // table entries per block (at most)
+
+struct BlocksArgs {
+  int log2U;          // lanes per pixel = G / GB (a power of two)
+  int P;              // pixels per tile = BLK_BD / U
+  int items;          // output pixels B * Ho * Wo (no pooling)
+  int RB;             // slot rows per block
+  int nblocks;        // ceil(R / RB)
+  int tpb;            // taps per block (RB = tpb * C), or 0: a block is a channel range
+  int cblocks;        // channel blocks per tap (C / RB) when tpb == 0
+  int tstride;        // 8-byte entries per staged row (G + padding)
+  int nbuf;           // table buffers: 2 (the next block is stored beside the
+                      // one in use) or 1 (stored after a barrier)
+  int log2n;          // kernels per set n = 1 << log2n
+  int log2G;          // sets G = 1 << log2G
+  int k;              // k-WTA winners per row; -1: sums only
+  int write_sums;     // 1: the sums (bias added) are written to y
+  int kmode;          // k-WTA: 1/2/3 four lanes per row with top-8/16/32 lists
+                      // (rows <= 128, k <= 32); 4: sixteen lanes per row
+  int ostride;        // row stride of the sum tile (four lanes per row)
+  int kp;             // channels per lane with sixteen lanes per row (4, 8 or 16)
+  uint32_t off_t0, off_t1, off_bias;   // LDS byte offsets
+  uint32_t off_out, off_sel, off_lidx, off_lval;       // epilogue (over the table blocks)
+  FastDiv fd_wo, fd_ho, fd_kw, fd_cout, fd_ochunks;
+};
+
+// The four entries of a list chunk (indices and values), read as two vectors.
+struct BChunk {
+  uint2 idx;
+  float4 val;
+};
+
+__device__ __forceinline__ float bchunk_val(const float4& v, int e) {
+  return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
+}
+__device__ __forceinline__ int bchunk_idx(const uint2& ii, int e) {
+  const uint32_t wd = e < 2 ? ii.x : ii.y;
+  return (int)((e & 1) ? (wd >> 16) : (wd & 0xFFFFu));
+}
+
+// Stage table rows [r0, r1) of the augmented tensor ([R][G] {value, kid})
+// into a block of rows of `tstride` 8-byte entries {value, offset}: the
+// offset of (row, set s) is the byte offset of the lane's accumulator row
+// (s mod GB) * n + kid, i.e. ((s mod GB) * n + kid) * BLK_BD * 4, so one LDS
+// read gives a lane its sets' weights and where their products go.
+template <int GB>
+struct BlockStage {
+  uint4 v[BLK_STAGE];
+  __device__ __forceinline__ void load(const uint2* __restrict__ aug, int r0, int r1, int G) {
+    const int npair = (r1 - r0) * G / 2;                 // 16-byte loads (G even)
+    const uint4* src = reinterpret_cast<const uint4*>(aug + (size_t)r0 * G);
+#pragma unroll
+    for (int u = 0; u < BLK_STAGE; ++u) {
+      const int e = u * BLK_BD + (int)threadIdx.x;
+      v[u] = src[e < npair ? e : npair - 1];             // in range: npair >= 1
+    }
+  }
+  // rows [r0, r1) as loaded, placed from staged row row0 on
+  __device__ __forceinline__ void store(unsigned char* smem, uint32_t off_t, int row0, int nrows,
+                                        int log2G, int tstride, int log2n) const {
+    const int G = 1 << log2G;
+    uint2* tab = reinterpret_cast<uint2*>(smem + off_t);
+    const int npair = nrows * G / 2;
+    const uint32_t nm = (1u << log2n) - 1u;                // a Kernel ID is < n
+#pragma unroll
+    for (int u = 0; u < BLK_STAGE; ++u) {
+      const int e = u * BLK_BD + (int)threadIdx.x;
+      if (e < npair) {
+        const int e2 = 2 * e;
+        const int row = row0 + (e2 >> log2G), s = e2 & (G - 1);   // s even: one row
+        const uint32_t o0 = (((uint32_t)(s % GB) << log2n) + (v[u].y & nm)) * (BLK_BD * 4);
+        const uint32_t o1 = (((uint32_t)((s + 1) % GB) << log2n) + (v[u].w & nm)) * (BLK_BD * 4);
+        *reinterpret_cast<uint4*>(tab + row * tstride + s) = make_uint4(v[u].x, o0, v[u].z, o1);
+      }
+    }
+  }
+};
+
+// One list chunk against the staged block, GB sets of the lane.  Entry e is
+// live when e in [e_lo, e_hi); a dead entry reads row 0 and adds a zero.
+// Route + Sum: the entries go in pairs; both reads of a pair are issued, then
+// the two writes in entry order, the second entry adding onto the first's new
+// value when their accumulators are the same (equal offsets <=> equal Kernel
+// IDs) - the same sums, in the same order, as one entry after another.
+template <int GB>
+__device__ __forceinline__ void blk_chunk(const BChunk& ch, int e_lo, int e_hi, int row_add,
+                                          const uint2* tab, int tstride, int set0,
+                                          unsigned char* accb) {
+  float x[4];
+  uint2 te[4][GB];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool ok = e >= e_lo && e < e_hi;
+    const int r = ok ? bchunk_idx(ch.idx, e) + row_add : 0;
+    x[e] = ok ? bchunk_val(ch.val, e) : 0.f;
+    const uint2* tp = tab + __umul24(r, tstride) + set0;
+    if constexpr (GB == 1) {
+      te[e][0] = tp[0];
+    } else if constexpr (GB == 2) {
+      const uint4 q = *reinterpret_cast<const uint4*>(tp);
+      te[e][0] = make_uint2(q.x, q.y);
+      te[e][1] = make_uint2(q.z, q.w);
+    } else {
+      const uint4 q0 = *reinterpret_cast<const uint4*>(tp);
+      const uint4 q1 = *reinterpret_cast<const uint4*>(tp + 2);
+      te[e][0] = make_uint2(q0.x, q0.y);
+      te[e][1] = make_uint2(q0.z, q0.w);
+      te[e][2] = make_uint2(q1.x, q1.y);
+      te[e][3] = make_uint2(q1.z, q1.w);
+    }
+  }
+#pragma unroll
+  for (int pr = 0; pr < 4; pr += 2) {
+    float a[2][GB];
+#pragma unroll
+    for (int j = 0; j < GB; ++j) {
+      a[0][j] = *reinterpret_cast<const float*>(accb + te[pr][j].y);
+      a[1][j] = *reinterpret_cast<const float*>(accb + te[pr + 1][j].y);
+    }
+#pragma unroll
+    for (int j = 0; j < GB; ++j) {
+      const float v0 = __builtin_fmaf(x[pr], __uint_as_float(te[pr][j].x), a[0][j]);
+      const float b1 = te[pr + 1][j].y == te[pr][j].y ? v0 : a[1][j];
+      const float v1 = __builtin_fmaf(x[pr + 1], __uint_as_float(te[pr + 1][j].x), b1);
+      *reinterpret_cast<float*>(accb + te[pr][j].y) = v0;
+      *reinterpret_cast<float*>(accb + te[pr + 1][j].y) = v1;
+    }
+  }
+}
+
+// A tap's list count and first BLK_SPEC chunks, loaded ahead of their use.
+// Every load is issued unconditionally (a tap outside the image reads list
+// row 0, a chunk past the row's capacity reads the row's last chunk), so the
+// compiler's wait counts stay exact and a later load never waits for them.
+constexpr int BLK_SPEC = 3;
+struct TapPre {
+  int off;                 // list row offset, or -1: the tap is outside the image
+  int cnt;
+  BChunk ch[BLK_SPEC];
+};
+
+__device__ __forceinline__ void tap_prefetch(TapPre& tp, const uint16_t* __restrict__ lidx,
+                                             const float* __restrict__ lval,
+                                             const int32_t* __restrict__ lcnt, const ConvGeom& geo,
+                                             bool live, int bb, int ho, int wo, int t, int j0,
+                                             const FastDiv& fd_kw) {
+  const int ky = (int)fdiv((uint32_t)t, fd_kw), kx = t - ky * geo.KW;
+  const int hy = ho * geo.S + ky - geo.P, wx = wo * geo.S + kx - geo.P;
+  const bool ok = live && t < geo.KH * geo.KW && hy >= 0 && hy < geo.H && wx >= 0 && wx < geo.W;
+  const int q = ok ? (bb * geo.H + hy) * geo.W + wx : 0;   // < 2^31 (host)
+  const int base = q * geo.cap;
+  tp.off = ok ? base : -1;
+  tp.cnt = lcnt[q];
+  const int c4 = j0 & ~3;
+#pragma unroll
+  for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
+    const int pos = min(c4 + 4 * s2, geo.cap - 4);
+    tp.ch[s2].idx = *reinterpret_cast<const uint2*>(lidx + base + pos);
+    tp.ch[s2].val = *reinterpret_cast<const float4*>(lval + base + pos);
+  }
+}
+
+// Entries e of chunk `ch` (list positions c4 + e) with e in [lo, m - c4) and,
+// in channel mode, a channel below c_hi: processed; returns the chunk entry
+// where the lane stopped (4 when it went through the chunk).
+template <int GB, bool CH>
+__device__ __forceinline__ int blk_chunk_upto(const BChunk& ch, int lo, int m, int c4, int c_hi,
+                                              int row_add, const uint2* tab, int tstride, int set0,
+                                              unsigned char* accb) {
+  const int hi = m - c4 < 4 ? m - c4 : 4;
+  int stop = hi;
+  if constexpr (CH) {
+#pragma unroll
+    for (int e = 3; e >= 0; --e)
+      if (e < hi && bchunk_idx(ch.idx, e) >= c_hi) stop = e;   // the list ascends
+  }
+  blk_chunk<GB>(ch, lo, stop, row_add, tab, tstride, set0, accb);
+  return stop < hi ? stop : 4;
+}
+
+// The entries of one tap's list from position j0 on (and, in channel mode,
+// below channel c_hi), the first chunks already in `tp`; the rest are read
+// one chunk ahead.  Returns the list position where the lane stopped.
+template <int GB, bool CH>
+__device__ __forceinline__ int blk_tap(const TapPre& tp, const uint16_t* __restrict__ lidx,
+                                       const float* __restrict__ lval, int cap, int j0, int c_hi,
+                                       int row_add, const uint2* tab, int tstride, int set0,
+                                       unsigned char* accb) {
+  if (tp.off < 0) return j0;
+  const int m = min(tp.cnt, cap);
+  int c4 = j0 & ~3;
+  int lo = j0 - c4;
+#pragma unroll
+  for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
+    if (c4 >= m) return m;
+    const int st = blk_chunk_upto<GB, CH>(tp.ch[s2], lo, m, c4, c_hi, row_add, tab, tstride,
+                                          set0, accb);
+    if (st < 4) return c4 + st;
+    c4 += 4;
+    lo = 0;
+  }
+  if (c4 >= m) return m;
+  const uint16_t* li = lidx + tp.off;
+  const float* lv = lval + tp.off;
+  BChunk cur;
+  cur.idx = *reinterpret_cast<const uint2*>(li + c4);
+  cur.val = *reinterpret_cast<const float4*>(lv + c4);
+  while (true) {
+    const int pn = min(c4 + 4, cap - 4);                 // next chunk, in the row
+    BChunk nxt;
+    nxt.idx = *reinterpret_cast<const uint2*>(li + pn);
+    nxt.val = *reinterpret_cast<const float4*>(lv + pn);
+    const int st = blk_chunk_upto<GB, CH>(cur, 0, m, c4, c_hi, row_add, tab, tstride, set0,
+                                          accb);
+    if (st < 4) return c4 + st;
+    c4 += 4;
+    if (c4 >= m) return m;
+    cur = nxt;
+  }
+}
+
+// k-WTA with sixteen lanes per row (rows of up to 256 channels, any k): lane
+// l of a row holds channels l*KP .. l*KP+KP-1 (read from the accumulator
+// columns, bias added), the k-th largest key is found bit by bit with
+// sixteen-lane counts, stopping as soon as the keys at or above the prefix
+// are exactly k (their minimum is then the k-th largest); ties go to the
+// lower index; winners are written as lists (non-zero values, ascending
+// index) or densely.  Four rows per wavefront at a time.
+template <typename TO, int GB, int KP>
+__device__ __forceinline__ void blk_kwta16(const float* acc, const float* bias_s, int item0,
+                                           int nrows, int P, int log2U, int log2n, int c_out,
+                                           int k, int write_sums, float* __restrict__ y,
+                                           TO* __restrict__ out, const ListOut& lo) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int l16 = lane & 15;
+  const int n = 1 << log2n;
+  for (int r0 = wv * 4; r0 < P; r0 += BLK_BD / 16) {
+    const int r = r0 + (lane >> 4);
+    const bool live_r = r < nrows;
+    const int64_t row = (int64_t)item0 + r;
+    float v[KP];
+    uint32_t key[KP];
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      const int o = l16 * KP + j;
+      const bool ok = live_r && o < c_out;
+      float sv = 0.f;
+      if (ok) {
+        const int g = o >> log2n, kk = o & (n - 1);
+        sv = acc[((g % GB) * n + kk) * BLK_BD + (r << log2U) + g / GB] + bias_s[o];
+        if (write_sums) y[row * c_out + o] = sv;
+      }
+      v[j] = sv;
+      key[j] = ok ? order_key(sv) : 0u;                 // 0: below every real key
+    }
+    if (k < 0) continue;
+    uint32_t thr = 0u;
+    int need = 0;
+    if (k > 0 && k < c_out) {
+      uint32_t pre = 0u;
+      int cntp = c_out;
+      bool done = !live_r;
+      for (int bit = 31; bit >= 0; --bit) {
+        if (__ballot(!done) == 0ull) break;             // every row of the wavefront found
+        const uint32_t cand = pre | (1u << bit);
+        uint32_t c = 0;
+#pragma unroll
+        for (int j = 0; j < KP; ++j) c += key[j] >= cand ? 1u : 0u;
+        c = row16_reduce(c, OpAdd{});
+        if (!done) {
+          if ((int)c >= k) {
+            pre = cand;
+            cntp = (int)c;
+          }
+          if (cntp == k) done = true;
+        }
+      }
+      // the k-th largest key: the least key at or above the prefix
+      uint32_t mn = 0xFFFFFFFFu;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) mn = (key[j] >= pre && key[j] < mn) ? key[j] : mn;
+      thr = row16_reduce(mn, OpMin{});
+      uint32_t gt = 0;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) gt += key[j] > thr ? 1u : 0u;
+      gt = row16_reduce(gt, OpAdd{});
+      need = k - (int)gt;
+    }
+    // ties in index order: this lane's first tie has rank (ties of the lanes before)
+    int eq = 0;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_out && key[j] == thr) ? 1 : 0;
+    int tie_rank = row16_incl_sum(eq) - eq;
+    bool win[KP];
+    int wcount = 0;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      const int o = l16 * KP + j;
+      const bool ok = live_r && o < c_out;
+      bool w;
+      if (!ok || k == 0) {
+        w = false;
+      } else if (k >= c_out) {
+        w = true;
+      } else if (key[j] > thr) {
+        w = true;
+      } else if (key[j] == thr) {
+        w = tie_rank < need;
+        ++tie_rank;
+      } else {
+        w = false;
+      }
+      win[j] = w;
+      wcount += (lo.idx ? (w && v[j] != 0.f) : w) ? 1 : 0;
+    }
+    if (lo.idx) {
+      const int incl = row16_incl_sum(wcount);
+      int pos = incl - wcount;
+      if (live_r) {
+        uint16_t* oi = lo.idx + row * lo.cap;
+        TO* ov = static_cast<TO*>(lo.val) + row * lo.cap;
+#pragma unroll
+        for (int j = 0; j < KP; ++j) {
+          if (win[j] && v[j] != 0.f) {
+            oi[pos] = (uint16_t)(l16 * KP + j);
+            ov[pos] = (TO)v[j];
+            ++pos;
+          }
+        }
+        if (l16 == 15) lo.cnt[row] = incl;
+      }
+    } else if (live_r) {
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        const int o = l16 * KP + j;
+        if (o < c_out) out[row * c_out + o] = win[j] ? (TO)v[j] : TO(0);
+      }
+    }
+  }
+}
+
+template <typename TO, int GB, bool CH>
+__global__ __launch_bounds__(BLK_BD) void mrs_blocks_f32(const uint16_t* __restrict__ lidx,
+                                                         const float* __restrict__ lval,
+                                                         const int32_t* __restrict__ lcnt,
+                                                         const uint2* __restrict__ aug,
+                                                         const float* __restrict__ bias,
+                                                         float* __restrict__ y,
+                                                         TO* __restrict__ out, ListOut lo,
+                                                         ConvGeom geo, BlocksArgs ba) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int n = 1 << ba.log2n;
+  const int G = geo.G;
+  const int C = geo.C;
+  const int T_ = geo.KH * geo.KW;
+  const int R = T_ * C;
+  const int c_out = geo.c_out;
+  const int U = 1 << ba.log2U;
+  const int ps = tid >> ba.log2U;                        // pixel slot of the lane
+  const int u = tid & (U - 1);                           // unit: sets u*GB .. u*GB+GB-1
+  const int item0 = (int)blockIdx.x * ba.P;
+  const int item = item0 + ps;
+  const bool live = item < ba.items;
+  int bb = 0, ho = 0, wo = 0;
+  if (live) {
+    const uint32_t t1 = fdiv((uint32_t)item, ba.fd_wo);
+    wo = item - (int)(t1 * ba.fd_wo.d);
+    const uint32_t t2 = fdiv(t1, ba.fd_ho);
+    ho = (int)(t1 - t2 * ba.fd_ho.d);
+    bb = (int)t2;
+  }
+  float* acc = reinterpret_cast<float*>(smem);           // [GB * n][BLK_BD]
+  unsigned char* accb = smem + tid * 4;                  // this lane's column
+  float* bias_s = reinterpret_cast<float*>(smem + ba.off_bias);
+  // the first tap's count and first chunks, then the table while they fly
+  TapPre cur;
+  tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
+#pragma unroll
+  for (int j = 0; j < GB * 16; ++j)
+    if (j < (GB << ba.log2n)) acc[j * BLK_BD + tid] = 0.f;
+  for (int o = tid; o < c_out; o += BLK_BD) bias_s[o] = bias ? bias[o] : 0.f;
+
+  // the first block, in passes of BLK_ENTRIES entries (a single block may be
+  // larger than what one pass holds in registers)
+  BlockStage<GB> st;
+  {
+    const int rb0 = min(R, ba.RB);
+    const int rpp = BLK_ENTRIES >> ba.log2G;              // rows per pass
+    for (int rs = 0; rs < rb0; rs += rpp) {
+      const int re = min(rb0, rs + rpp);
+      st.load(aug, rs, re, G);
+      st.store(smem, ba.off_t0, rs, re - rs, ba.log2G, ba.tstride, ba.log2n);
+    }
+  }
+  __syncthreads();
+
+  int cursor = 0;                                        // place in the current tap's list
+  for (int blk = 0; blk < ba.nblocks; ++blk) {
+    const int r0n = (blk + 1) * ba.RB;
+    const bool has_next = blk + 1 < ba.nblocks;
+    const bool odd = ba.nbuf == 2 && (blk & 1);
+    const uint2* tab = reinterpret_cast<const uint2*>(smem + (odd ? ba.off_t1 : ba.off_t0));
+    // the next table block's loads (issued after the prefetched list data)
+    if (has_next) st.load(aug, r0n, min(R, r0n + ba.RB), G);
+    if constexpr (!CH) {
+      // whole taps t0 .. t1-1; the next tap (of this block or the next one)
+      // is prefetched while one is processed
+      const int t0 = blk * ba.tpb, t1 = min(T_, t0 + ba.tpb);
+      for (int t = t0; t < t1; ++t) {
+        TapPre nxt;
+        tap_prefetch(nxt, lidx, lval, lcnt, geo, live, bb, ho, wo, t + 1, 0, ba.fd_kw);
+        blk_tap<GB, false>(cur, lidx, lval, geo.cap, 0, C, (t - t0) * C, tab, ba.tstride, u * GB,
+                           accb);
+        cur = nxt;
+      }
+    } else {
+      // one tap, the channels [c_lo, c_hi): the lane goes on in the tap's
+      // list where the previous block stopped
+      const int t0 = blk / ba.cblocks;
+      const int c_lo = (blk - t0 * ba.cblocks) * ba.RB;
+      if (c_lo == 0) cursor = 0;
+      cursor = blk_tap<GB, true>(cur, lidx, lval, geo.cap, cursor, c_lo + ba.RB, -c_lo, tab,
+                                 ba.tstride, u * GB, accb);
+      // the next block's list data, in flight across the barrier
+      const int tn = (blk + 1) / ba.cblocks;
+      tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
+                   tn == t0 ? cursor : 0, ba.fd_kw);
+    }
+    if (has_next) {
+      if (ba.nbuf == 1) __syncthreads();                 // every lane is done with the block
+      st.store(smem, odd || ba.nbuf == 1 ? ba.off_t0 : ba.off_t1, 0, min(R, r0n + ba.RB) - r0n,
+               ba.log2G, ba.tstride, ba.log2n);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue
+  const int nrows = min(ba.P, ba.items - item0);         // live rows of the tile
+  if (ba.kmode == 4 || ba.k < 0) {
+    if (ba.kp == 4)
+      blk_kwta16<TO, GB, 4>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+                            ba.write_sums, y, out, lo);
+    else if (ba.kp == 8)
+      blk_kwta16<TO, GB, 8>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+                            ba.write_sums, y, out, lo);
+    else
+      blk_kwta16<TO, GB, 16>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+                             ba.write_sums, y, out, lo);
+    return;
+  }
+  // four lanes per row: the sums (bias added) into a row-major tile with an
+  // odd row stride over the table blocks, then the selection of the gather
+  // kernel's epilogue
+  const int ostride = ba.ostride;
+  float* otile = reinterpret_cast<float*>(smem + ba.off_out);
+  for (int e = tid; e < nrows * c_out; e += BLK_BD) {
+    const int r = (int)fdiv((uint32_t)e, ba.fd_cout), o = e - r * c_out;
+    const int g = o >> ba.log2n, kk = o & (n - 1);
+    const float sv = acc[((g % GB) * n + kk) * BLK_BD + (r << ba.log2U) + g / GB] + bias_s[o];
+    otile[r * ostride + o] = sv;
+    if (ba.write_sums) y[(int64_t)item0 * c_out + e] = sv;
+  }
+  __syncthreads();
+  const FastDiv one{1u, 0u, 0u};
+  const SlotMap sm{0, 1, 0, nrows, one};
+  const RowMap rm{0, 1, 0, 0, 0, 0, 0, (int64_t)item0, one};
+  uint2* sel = reinterpret_cast<uint2*>(smem + ba.off_sel);
+  uint16_t* tl_idx = lo.idx ? reinterpret_cast<uint16_t*>(smem + ba.off_lidx) : nullptr;
+  TO* tl_val = reinterpret_cast<TO*>(smem + ba.off_lval);
+  if (ba.kmode == 1)
+    kwta_quad_items<float, TO, 8, BLK_BD>(otile, ostride, sm, rm, c_out, ba.k, 0, sel, tl_idx,
+                                          tl_val, lo.cap, lo.cnt);
+  else if (ba.kmode == 2)
+    kwta_quad_items<float, TO, 16, BLK_BD>(otile, ostride, sm, rm, c_out, ba.k, 0, sel, tl_idx,
+                                           tl_val, lo.cap, lo.cnt);
+  else
+    kwta_quad_items<float, TO, 32, BLK_BD>(otile, ostride, sm, rm, c_out, ba.k, 0, sel, tl_idx,
+                                           tl_val, lo.cap, lo.cnt);
+  __syncthreads();
+  if (lo.idx) {
+    // the tile's lists, 4 entries per store (cap % 4 == 0); entries past a
+    // row's count are copied too and are not part of the output
+    const int cq = lo.cap >> 2;
+    for (int e = tid; e < nrows * cq; e += BLK_BD) {
+      const int it = (int)fdiv((uint32_t)e, ba.fd_ochunks);
+      const int j = e - it * cq;
+      const int64_t g = ((int64_t)item0 + it) * lo.cap + 4 * j;
+      *reinterpret_cast<uint2*>(lo.idx + g) = reinterpret_cast<const uint2*>(tl_idx)[it * cq + j];
+      *reinterpret_cast<float4*>(static_cast<TO*>(lo.val) + g) =
+          reinterpret_cast<const float4*>(tl_val)[it * cq + j];
+    }
+  } else {
+    const bool none = ba.k == 0;
+    for (int e = tid; e < nrows * c_out; e += BLK_BD) {
+      const int it = (int)fdiv((uint32_t)e, ba.fd_cout);
+      const int ch = e - it * c_out;
+      const float a = otile[it * ostride + ch];
+      const uint2 sv = sel[it];
+      const uint32_t key = order_key(a);
+      const bool win = !none && (key > sv.x || (key == sv.x && ch <= (int)sv.y));
+      out[(int64_t)item0 * c_out + e] = win ? (TO)a : TO(0);
+    }
+  }
+}
+
+}  // namespace cs

@@ -348,8 +348,12 @@ def mrs_plan(dtype: torch.dtype, cap: int, in_shape, kh: int, kw: int, stride: i
     info = (ctypes.c_int64 * 11)()
     check("cs_mrs_plan", lib().cs_mrs_plan(_TORCH_DT[dtype], cap, b, h, w, c_in, kh, kw, stride,
                                            pad, c_out, n, pool, k, info))
-    path = ("simple", "tiled", "fused", "sample", "scatter", "rows")[info[0]]
+    path = ("simple", "tiled", "fused", "sample", "scatter", "rows", "blocks")[info[0]]
     kwta = None if k < 0 else ("separate" if info[10] else "fused")
+    if path == "blocks":
+        return {"path": path, "kwta": kwta, "select": info[1], "rows_per_block": info[2],
+                "table_blocks": info[3], "blocks": info[6], "lds": info[7],
+                "sets_per_lane": info[8]}
     if path == "rows":
         return {"path": path, "kwta": kwta, "blocks": info[6], "lds": info[7],
                 "channels_per_lane": info[8]}

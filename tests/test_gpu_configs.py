@@ -118,8 +118,8 @@ def test_fp32_config_layerwise(cid):
 
 @pytest.mark.parametrize("cid,layer,path", [(1, "linear", "sample"), (2, "conv2", "scatter"),
                                              (2, "linear1", "sample"), (2, "output", "sample"),
-                                             (3, "conv3x3", "fused"), (4, "conv1x1", "tiled"),
-                                             (4, "conv3x3", "tiled"), (5, "expand", "rows"),
+                                             (3, "conv3x3", "blocks"), (4, "conv1x1", "blocks"),
+                                             (4, "conv3x3", "blocks"), (5, "expand", "rows"),
                                              (5, "project", "rows")])
 def test_config_launch_paths(cid, layer, path):
     """Which kernel runs each layer at full size (the benchmark's launches)."""

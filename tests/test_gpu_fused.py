@@ -93,10 +93,11 @@ CASES = [
     ("i8", (3, 14, 14, 64), 8, 5, 5, 1, 0, 64, 16, 2, 8, False, 9, "lists", ("scatter", None)),
     # the same layer with stride 2: the gather kernel (rectangle tiles)
     ("i8", (2, 17, 17, 64), 8, 5, 5, 2, 2, 64, 16, 1, 8, False, 9, "lists", ("fused", 1)),
-    # 3x3 pad 1, ragged image against the tiles, fp32 dense output
-    ("f32", (2, 19, 13, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "dense", ("fused", 1)),
-    # wide image: column tiles
-    ("f32", (1, 9, 150, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "lists", ("fused", 1)),
+    # 3x3 pad 1, ragged image against the tiles, fp32 dense output: the
+    # table-block kernel (one block), the last tile part-full
+    ("f32", (2, 19, 13, 64), 7, 3, 3, 1, 1, 64, 8, 1, 8, False, None, "dense", ("blocks", None)),
+    # wide image, 6 sets (not a power of two): the gather kernel, column tiles
+    ("f32", (1, 9, 150, 64), 7, 3, 3, 1, 1, 48, 8, 1, 8, False, None, "lists", ("fused", 1)),
     # 1x1 expand: rows of items, bias, requantised lists, ragged last tile
     ("i8", (2, 7, 9, 96), 12, 1, 1, 1, 0, 576, 8, 1, 72, True, 9, "lists", ("fused", 0)),
     # linear, int32 dense output, bias: one workgroup per sample
@@ -104,9 +105,11 @@ CASES = [
     ("i8", (29, 1, 1, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("sample", None)),
     # dense kernels (n = 1), one accumulator per set in registers
     ("i8", (3, 4, 5, 300), 40, 1, 1, 1, 0, 12, 1, 1, 3, False, None, "lists", ("fused", 0)),
-    ("f32", (3, 6, 5, 40), 9, 3, 3, 1, 1, 16, 1, 1, 5, True, None, "dense", ("fused", 1)),
+    ("f32", (3, 6, 5, 40), 9, 3, 3, 1, 1, 16, 1, 1, 5, True, None, "dense", ("blocks", None)),
+    ("f32", (3, 6, 5, 40), 9, 3, 3, 1, 1, 12, 1, 1, 5, True, None, "dense", ("fused", 1)),
     # stride 2, odd input
-    ("f32", (2, 17, 17, 32), 5, 3, 3, 2, 1, 32, 4, 1, 4, False, None, "lists", ("fused", 1)),
+    ("f32", (2, 17, 17, 32), 5, 3, 3, 2, 1, 32, 4, 1, 4, False, None, "lists", ("blocks", None)),
+    ("f32", (2, 17, 17, 32), 5, 3, 3, 2, 1, 24, 4, 1, 4, False, None, "lists", ("fused", 1)),
     # 5x5 pad 2 with pool, odd number of sets (one set per lane)
     ("f32", (2, 12, 10, 16), 4, 5, 5, 1, 2, 24, 8, 2, 6, True, None, "dense", ("fused", 1)),
     # k = 0 and k = c_out
@@ -115,7 +118,7 @@ CASES = [
     # ties everywhere: +-1 weights, all-one inputs
     ("i8", (4, 9, 9, 64), 8, 3, 3, 1, 1, 64, 16, 1, 8, False, 0, "lists", ("scatter", None)),
     # lists that do not fit the LDS budget: some pixels are read from global memory
-    ("f32", (2, 24, 24, 128), 100, 3, 3, 1, 1, 16, 4, 1, 4, False, None, "lists", ("fused", 1)),
+    ("f32", (2, 24, 24, 128), 100, 3, 3, 1, 1, 12, 4, 1, 4, False, None, "lists", ("fused", 1)),
     # c_out not a multiple of 4, odd set count (one set per lane): input-stationary
     ("i8", (3, 6, 6, 24), 5, 3, 3, 1, 1, 6, 2, 1, 2, True, 2, "lists", ("scatter", None)),
     # the same with stride 2: two kernels (sums, then k-WTA)
@@ -142,8 +145,19 @@ CASES = [
     ("i8", (2, 48, 48, 128), 100, 1, 1, 1, 0, 1000, 8, 1, 120, True, None, "dense", ("rows", None)),
     ("i8", (1, 70, 70, 64), 3, 1, 1, 1, 0, 256, 32, 1, 0, False, 9, "lists", ("rows", None)),
     ("i8", (1, 70, 70, 64), 3, 1, 1, 1, 0, 256, 32, 1, 256, True, None, "dense", ("rows", None)),
-    # the same shape in fp32: the gather kernel's sums, then a k-WTA kernel
-    ("f32", (4, 32, 32, 64), 7, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "dense", ("fused", 0)),
+    # the same shape in fp32: the table-block kernel, k-WTA over 256 channels
+    ("f32", (4, 32, 32, 64), 7, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "dense", ("blocks", None)),
+    # fp32 table-block kernel: a 3x3 layer whose taps are split into channel
+    # blocks (the stage-3 3x3 shape), a 1x1 layer over 1024 channels in 8
+    # channel blocks (lists continue from block to block), k = 0, k = c_out,
+    # 64 channels in 4 sets, 128 channels with two keys per lane
+    ("f32", (2, 9, 9, 256), 26, 3, 3, 1, 1, 256, 16, 1, 26, False, None, "lists", ("blocks", None)),
+    ("f32", (2, 7, 5, 1024), 102, 1, 1, 1, 0, 256, 16, 1, 26, True, None, "lists", ("blocks", None)),
+    ("f32", (2, 7, 5, 1024), 102, 1, 1, 1, 0, 256, 16, 1, 0, False, None, "lists", ("blocks", None)),
+    ("f32", (2, 6, 6, 256), 26, 3, 3, 1, 1, 256, 16, 1, 256, True, None, "dense", ("blocks", None)),
+    ("f32", (3, 10, 10, 64), 7, 3, 3, 1, 1, 64, 16, 1, 8, True, None, "lists", ("blocks", None)),
+    ("f32", (2, 8, 9, 96), 9, 3, 3, 1, 1, 128, 4, 1, 20, False, None, "lists", ("blocks", None)),
+    ("f32", (2, 7, 7, 64), 7, 3, 3, 1, 1, 128, 4, 1, 16, True, None, "dense", ("blocks", None)),
     # a table too large for LDS, one output vector per sample: one workgroup
     # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
     ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
@@ -294,14 +308,14 @@ def test_rows_sums_only(case):
 def test_fused_partial_staging_plan():
     """The budget case above really leaves pixels unstaged: its lists need
     more chunks than the LDS list budget of a tile."""
-    plan = ops.mrs_plan(torch.float32, 128, (2, 24, 24, 128), 3, 3, 1, 1, 16, 4, 1, 4)
+    plan = ops.mrs_plan(torch.float32, 128, (2, 24, 24, 128), 3, 3, 1, 1, 12, 4, 1, 4)
     assert plan["path"] == "fused"
     need = plan["npix_cap"] * 25                 # 100 entries per pixel = 25 chunks
     assert plan["list_cap"] < need, plan
 
 
 def test_fused_column_tiles_plan():
-    plan = ops.mrs_plan(torch.float32, 64, (1, 9, 150, 64), 3, 3, 1, 1, 64, 8, 1, 8)
+    plan = ops.mrs_plan(torch.float32, 64, (1, 9, 150, 64), 3, 3, 1, 1, 48, 8, 1, 8)
     assert plan["path"] == "fused" and plan["tile_mode"] == 1
     assert 0 < plan["tile_cols"] < 150, plan
 
