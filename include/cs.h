@@ -201,7 +201,10 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
  *          tiles complete in the channel dimension with the packed table
  *          streamed through LDS in blocks of rows, k-WTA in the epilogue);
  *          for path 6: [1] k-WTA selection (1-3 four lanes per row with
- *          top-8/16/32 lists, 4 sixteen lanes per row), [2] table rows per block, [3] blocks, [6]
+ *          top-8/16/32 lists, 4 sixteen lanes per row, 5 the lanes that
+ *          summed a pixel, on their own accumulators, bit by bit, 6-8 the
+ *          same four lanes with top-8/16/32 lists), [2] table rows per
+ *          block, [3] blocks, [6]
  *          workgroups, [7] LDS bytes, [8] sets per lane; for paths 3 and
  *          5: [6] workgroups, [7] LDS bytes per workgroup, [8] entry slices
  *          per packed set; for path 4: [2] output rows per band, [6]

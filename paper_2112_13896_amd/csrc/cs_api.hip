@@ -466,6 +466,7 @@ int launch_fused(const FusedPlan& pl, cs_dtype xt, cs_dtype ot, hipStream_t stre
 struct BlocksPlan {
   cs::BlocksArgs ba;
   int gb;
+  bool own;              // k-WTA on the lanes' own accumulator columns
   int64_t blocks;
   size_t shmem;
 };
@@ -479,8 +480,11 @@ int ilog2_exact(int64_t v) {                    // log2 of a power of two, else 
 
 // ocap: capacity of the output lists (0: dense output or sums only); lvec:
 // the output lists take 8-byte index and 16-byte value stores.
-bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const void* y, int k,
-                 int write_sums, int ocap, bool lvec, BlocksPlan* pl) {
+// cus: compute units of the device (sizes the grid of a one-block table), or
+// 0 when only planning.
+bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const void* y,
+                 const void* out, int k, int write_sums, int ocap, bool lvec, int cus,
+                 BlocksPlan* pl) {
   if (xt != CS_F32 || geo.pool != 1) return false;
   const int n = geo.n, G = geo.G;
   const int log2n = ilog2_exact(n), log2G = ilog2_exact(G);
@@ -505,7 +509,7 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
   const int tstride = G;                                  // 8-byte entries per row
   const size_t acc_b = (size_t)gb * n * cs::BLK_BD * 4;
   const size_t budget = kCuLds / 2;
-  const size_t fixed = acc_b + round16((size_t)geo.c_out * 4);
+  const size_t fixed = acc_b;
   auto lds_for = [&](int64_t rows, int nbuf) {
     return fixed + nbuf * round16((size_t)rows * tstride * 8);
   };
@@ -553,8 +557,7 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
   ba.ostride = geo.c_out + 1;                             // odd: conflict-free row reads
   ba.off_t0 = (uint32_t)acc_b;
   ba.off_t1 = (uint32_t)(acc_b + (nbuf - 1) * tb);
-  ba.off_bias = (uint32_t)(acc_b + nbuf * tb);
-  size_t end = ba.off_bias + round16((size_t)geo.c_out * 4);
+  size_t end = acc_b + nbuf * tb;
   // the four-lane epilogue's tile, selections and lists over the table blocks
   const int P = cs::BLK_BD / U;
   ba.off_out = (uint32_t)acc_b;
@@ -562,10 +565,24 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
   ba.off_lidx = ba.off_sel + (uint32_t)round16((size_t)P * 8);
   ba.off_lval = ba.off_lidx + (uint32_t)round16((size_t)P * ocap * 2);
   const size_t epi_end = ba.off_lval + round16((size_t)P * ocap * 4);
-  if (quad && epi_end > ba.off_bias) {
-    // the epilogue region would reach the bias: put the bias after it
-    ba.off_bias = (uint32_t)round16(epi_end);
-    end = ba.off_bias + round16((size_t)geo.c_out * 4);
+  if (quad && epi_end > end) end = epi_end;
+  // k-WTA on the lanes' own accumulator columns: a pixel's lanes in one DPP
+  // row (U <= 16), 4..32 channels per lane, 16-byte aligned dense rows
+  const int kp_own = gb * n;
+  pl->own = U <= 16 && kp_own >= 4 && kp_own <= 32 && (kp_own & (kp_own - 1)) == 0 &&
+            aligned(y, 16) && aligned(out, 16);
+  if (pl->own) {
+    // a pixel's four lanes hold its four quarters: the four-lane selection
+    // in place (a quad selection record per pixel in LDS), else bit by bit
+    const bool quad_own = U == 4 && gb == 2 && tpb > 0 && k >= 0 && k <= 32 &&
+                          geo.c_out == 4 * kp_own;
+    ba.kmode = quad_own ? (k <= 8 ? 6 : (k <= 16 ? 7 : 8)) : 5;
+    if (quad_own) {
+      ba.off_sel = (uint32_t)round16(acc_b + nbuf * tb);
+      end = ba.off_sel + round16((size_t)P * 8);
+    } else {
+      end = acc_b + nbuf * tb;
+    }
   }
   ba.fd_wo = cs::make_fastdiv((uint32_t)geo.Wo);
   ba.fd_ho = cs::make_fastdiv((uint32_t)geo.Ho);
@@ -574,8 +591,20 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
   ba.fd_ochunks = cs::make_fastdiv((uint32_t)(ocap >= 4 ? ocap / 4 : 1));
   pl->gb = gb;
   pl->shmem = end;
-  pl->blocks = (items + ba.P - 1) / ba.P;
-  return pl->shmem <= kBlockLds * 2 && pl->blocks < INT32_MAX;
+  const int64_t ntiles = (items + ba.P - 1) / ba.P;
+  ba.ntiles = (int)ntiles;
+  pl->blocks = ntiles;
+  if (nblocks == 1) {
+    // the table is staged once per workgroup: as many workgroups as fit at
+    // once (by LDS), each looping over tiles
+    if (cus > 0) {
+      int64_t per_cu = (int64_t)(kCuLds / (end > 0 ? end : 1));
+      if (per_cu > 8) per_cu = 8;
+      if (per_cu < 1) per_cu = 1;
+      if (pl->blocks > per_cu * cus) pl->blocks = per_cu * cus;
+    }
+  }
+  return pl->shmem <= kBlockLds * 2 && ntiles < INT32_MAX;
 }
 
 int launch_blocks(const BlocksPlan& pl, hipStream_t stream, const uint16_t* idx,
@@ -587,17 +616,41 @@ int launch_blocks(const BlocksPlan& pl, hipStream_t stream, const uint16_t* idx,
   const float* bs = static_cast<const float*>(bias);
   float* yy = static_cast<float*>(y);
   float* oo = static_cast<float*>(out);
-#define CS_BLOCKS(GB_, CH_)                                                              \
-  hipLaunchKernelGGL((cs::mrs_blocks_f32<float, GB_, CH_>), grid, block, pl.shmem, stream, idx, \
-                     lv, cnt, pa, bs, yy, oo, lo, geo, pl.ba)
+#define CS_BLOCKS(GB_, CH_, KP_, QK_)                                                    \
+  hipLaunchKernelGGL((cs::mrs_blocks_f32<float, GB_, CH_, KP_, QK_>), grid, block, pl.shmem,  \
+                     stream, idx, lv, cnt, pa, bs, yy, oo, lo, geo, pl.ba)
+#define CS_BLOCKS_KP(GB_, CH_)                                                           \
+  do {                                                                                  \
+    const int kp = pl.own ? GB_ * geo.n : 0;                                            \
+    if (kp == 4) CS_BLOCKS(GB_, CH_, 4, 0);                                             \
+    else if (kp == 8) CS_BLOCKS(GB_, CH_, 8, 0);                                        \
+    else if (kp == 16) CS_BLOCKS(GB_, CH_, 16, 0);                                      \
+    else if (kp == 32) CS_BLOCKS(GB_, CH_, 32, 0);                                      \
+    else CS_BLOCKS(GB_, CH_, 0, 0);                                                     \
+  } while (0)
+// the four-lane selection in place: two sets per lane, whole-tap blocks
+#define CS_BLOCKS_QUAD(KP_)                                                              \
+  do {                                                                                  \
+    if (pl.ba.kmode == 6) CS_BLOCKS(2, false, KP_, 8);                                  \
+    else if (pl.ba.kmode == 7) CS_BLOCKS(2, false, KP_, 16);                            \
+    else CS_BLOCKS(2, false, KP_, 32);                                                  \
+  } while (0)
   const bool ch = pl.ba.tpb == 0;
-  if (pl.gb == 1) {
-    if (ch) CS_BLOCKS(1, true); else CS_BLOCKS(1, false);
+  if (pl.own && pl.ba.kmode >= 6) {
+    const int kp = 2 * geo.n;
+    if (kp == 4) CS_BLOCKS_QUAD(4);
+    else if (kp == 8) CS_BLOCKS_QUAD(8);
+    else if (kp == 16) CS_BLOCKS_QUAD(16);
+    else CS_BLOCKS_QUAD(32);
+  } else if (pl.gb == 1) {
+    if (ch) CS_BLOCKS_KP(1, true); else CS_BLOCKS_KP(1, false);
   } else if (pl.gb == 2) {
-    if (ch) CS_BLOCKS(2, true); else CS_BLOCKS(2, false);
+    if (ch) CS_BLOCKS_KP(2, true); else CS_BLOCKS_KP(2, false);
   } else {
-    if (ch) CS_BLOCKS(4, true); else CS_BLOCKS(4, false);
+    if (ch) CS_BLOCKS_KP(4, true); else CS_BLOCKS_KP(4, false);
   }
+#undef CS_BLOCKS_QUAD
+#undef CS_BLOCKS_KP
 #undef CS_BLOCKS
   return launch_status();
 }
@@ -990,7 +1043,10 @@ int mrs_launch(cs_dtype xt, const uint16_t* idx, const void* lval, const int32_t
                        cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
   if (lists_vectorisable(xt, idx, lval, geo.cap)) {
     BlocksPlan bp;
-    if (blocks_plan(geo, xt, aug, y, -1, 1, 0, false, &bp))
+    int cus = 0;
+    const int dst = device_cus(&cus);
+    if (dst != CS_OK) return dst;
+    if (blocks_plan(geo, xt, aug, y, nullptr, -1, 1, 0, false, cus, &bp))
       return launch_blocks(bp, stream, idx, lval, cnt, aug, bias, y, nullptr,
                            cs::ListOut{nullptr, nullptr, nullptr, 0}, geo);
     FusedPlan fp;
@@ -1217,7 +1273,12 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
   if (lists_vectorisable(xt, idx, lval, cap)) {
     BlocksPlan bp;
     const bool lvec = lists && aligned(oidx, 8) && aligned(oval, 16);
-    if (blocks_plan(geo, xt, aug, y, k, keep_sums, lists ? ocap : 0, lvec, &bp))
+    int cus = 0;
+    if (xt == CS_F32) {
+      const int dst = device_cus(&cus);
+      if (dst != CS_OK) return dst;
+    }
+    if (blocks_plan(geo, xt, aug, y, out, k, keep_sums, lists ? ocap : 0, lvec, cus, &bp))
       return launch_blocks(bp, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
   }
   if (lists_ok && lists_vectorisable(xt, idx, lval, cap)) {
@@ -1275,8 +1336,8 @@ int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int
     return CS_OK;
   }
   BlocksPlan bp;
-  if (cap % 4 == 0 && blocks_plan(geo, xt, nullptr, nullptr, k, 1, k >= 0 ? (k + 3) / 4 * 4 : 0,
-                                  true, &bp)) {
+  if (cap % 4 == 0 && blocks_plan(geo, xt, nullptr, nullptr, nullptr, k, 1,
+                                  k >= 0 ? (k + 3) / 4 * 4 : 0, true, 0, &bp)) {
     info[1] = bp.ba.kmode;
     info[0] = 6;
     info[2] = bp.ba.RB;

@@ -47,6 +47,7 @@ struct BlocksArgs {
   int log2U;          // lanes per pixel = G / GB (a power of two)
   int P;              // pixels per tile = BLK_BD / U
   int items;          // output pixels B * Ho * Wo (no pooling)
+  int ntiles;         // tiles of P pixels; workgroups loop over them
   int RB;             // slot rows per block
   int nblocks;        // ceil(R / RB)
   int tpb;            // taps per block (RB = tpb * C), or 0: a block is a channel range
@@ -58,11 +59,13 @@ struct BlocksArgs {
   int log2G;          // sets G = 1 << log2G
   int k;              // k-WTA winners per row; -1: sums only
   int write_sums;     // 1: the sums (bias added) are written to y
-  int kmode;          // k-WTA: 1/2/3 four lanes per row with top-8/16/32 lists
-                      // (rows <= 128, k <= 32); 4: sixteen lanes per row
+  int kmode;          // k-WTA on a copied tile: 1/2/3 four lanes per row with
+                      // top-8/16/32 lists (rows <= 128, k <= 32), 4 sixteen
+                      // lanes per row; on the lanes' own columns: 5 bit by bit,
+                      // 6/7/8 four lanes (a pixel's quad) with top-8/16/32 lists
   int ostride;        // row stride of the sum tile (four lanes per row)
   int kp;             // channels per lane with sixteen lanes per row (4, 8 or 16)
-  uint32_t off_t0, off_t1, off_bias;   // LDS byte offsets
+  uint32_t off_t0, off_t1;   // LDS byte offsets of the table buffers
   uint32_t off_out, off_sel, off_lidx, off_lval;       // epilogue (over the table blocks)
   FastDiv fd_wo, fd_ho, fd_kw, fd_cout, fd_ochunks;
 };
@@ -270,9 +273,9 @@ __device__ __forceinline__ int blk_tap(const TapPre& tp, const uint16_t* __restr
 // lower index; winners are written as lists (non-zero values, ascending
 // index) or densely.  Four rows per wavefront at a time.
 template <typename TO, int GB, int KP>
-__device__ __forceinline__ void blk_kwta16(const float* acc, const float* bias_s, int item0,
-                                           int nrows, int P, int log2U, int log2n, int c_out,
-                                           int k, int write_sums, float* __restrict__ y,
+__device__ __forceinline__ void blk_kwta16(const float* acc, int item0, int nrows, int P,
+                                           int log2U, int log2n, int c_out, int k,
+                                           int write_sums, float* __restrict__ y,
                                            TO* __restrict__ out, const ListOut& lo) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int l16 = lane & 15;
@@ -290,7 +293,7 @@ __device__ __forceinline__ void blk_kwta16(const float* acc, const float* bias_s
       float sv = 0.f;
       if (ok) {
         const int g = o >> log2n, kk = o & (n - 1);
-        sv = acc[((g % GB) * n + kk) * BLK_BD + (r << log2U) + g / GB] + bias_s[o];
+        sv = acc[((g % GB) * n + kk) * BLK_BD + (r << log2U) + g / GB];
         if (write_sums) y[row * c_out + o] = sv;
       }
       v[j] = sv;
@@ -382,125 +385,39 @@ __device__ __forceinline__ void blk_kwta16(const float* acc, const float* bias_s
   }
 }
 
-template <typename TO, int GB, bool CH>
-__global__ __launch_bounds__(BLK_BD) void mrs_blocks_f32(const uint16_t* __restrict__ lidx,
-                                                         const float* __restrict__ lval,
-                                                         const int32_t* __restrict__ lcnt,
-                                                         const uint2* __restrict__ aug,
-                                                         const float* __restrict__ bias,
-                                                         float* __restrict__ y,
-                                                         TO* __restrict__ out, ListOut lo,
-                                                         ConvGeom geo, BlocksArgs ba) {
-  extern __shared__ __align__(16) unsigned char smem[];
+// The epilogue on a tile copied from the accumulator columns (any lane
+// layout): k-WTA with sixteen lanes per row, or with four lanes per row on a
+// row-major tile (the gather kernel's selection) followed by the lists'
+// copy-out; sums only when k < 0.
+template <typename TO, int GB>
+__device__ __forceinline__ void blk_epilogue_tile(unsigned char* smem, const float* acc,
+                                                  int item0, int c_out, float* __restrict__ y,
+                                                  TO* __restrict__ out, const ListOut& lo,
+                                                  const BlocksArgs& ba) {
   const int tid = threadIdx.x;
   const int n = 1 << ba.log2n;
-  const int G = geo.G;
-  const int C = geo.C;
-  const int T_ = geo.KH * geo.KW;
-  const int R = T_ * C;
-  const int c_out = geo.c_out;
-  const int U = 1 << ba.log2U;
-  const int ps = tid >> ba.log2U;                        // pixel slot of the lane
-  const int u = tid & (U - 1);                           // unit: sets u*GB .. u*GB+GB-1
-  const int item0 = (int)blockIdx.x * ba.P;
-  const int item = item0 + ps;
-  const bool live = item < ba.items;
-  int bb = 0, ho = 0, wo = 0;
-  if (live) {
-    const uint32_t t1 = fdiv((uint32_t)item, ba.fd_wo);
-    wo = item - (int)(t1 * ba.fd_wo.d);
-    const uint32_t t2 = fdiv(t1, ba.fd_ho);
-    ho = (int)(t1 - t2 * ba.fd_ho.d);
-    bb = (int)t2;
-  }
-  float* acc = reinterpret_cast<float*>(smem);           // [GB * n][BLK_BD]
-  unsigned char* accb = smem + tid * 4;                  // this lane's column
-  float* bias_s = reinterpret_cast<float*>(smem + ba.off_bias);
-  // the first tap's count and first chunks, then the table while they fly
-  TapPre cur;
-  tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
-#pragma unroll
-  for (int j = 0; j < GB * 16; ++j)
-    if (j < (GB << ba.log2n)) acc[j * BLK_BD + tid] = 0.f;
-  for (int o = tid; o < c_out; o += BLK_BD) bias_s[o] = bias ? bias[o] : 0.f;
-
-  // the first block, in passes of BLK_ENTRIES entries (a single block may be
-  // larger than what one pass holds in registers)
-  BlockStage<GB> st;
-  {
-    const int rb0 = min(R, ba.RB);
-    const int rpp = BLK_ENTRIES >> ba.log2G;              // rows per pass
-    for (int rs = 0; rs < rb0; rs += rpp) {
-      const int re = min(rb0, rs + rpp);
-      st.load(aug, rs, re, G);
-      st.store(smem, ba.off_t0, rs, re - rs, ba.log2G, ba.tstride, ba.log2n);
-    }
-  }
-  __syncthreads();
-
-  int cursor = 0;                                        // place in the current tap's list
-  for (int blk = 0; blk < ba.nblocks; ++blk) {
-    const int r0n = (blk + 1) * ba.RB;
-    const bool has_next = blk + 1 < ba.nblocks;
-    const bool odd = ba.nbuf == 2 && (blk & 1);
-    const uint2* tab = reinterpret_cast<const uint2*>(smem + (odd ? ba.off_t1 : ba.off_t0));
-    // the next table block's loads (issued after the prefetched list data)
-    if (has_next) st.load(aug, r0n, min(R, r0n + ba.RB), G);
-    if constexpr (!CH) {
-      // whole taps t0 .. t1-1; the next tap (of this block or the next one)
-      // is prefetched while one is processed
-      const int t0 = blk * ba.tpb, t1 = min(T_, t0 + ba.tpb);
-      for (int t = t0; t < t1; ++t) {
-        TapPre nxt;
-        tap_prefetch(nxt, lidx, lval, lcnt, geo, live, bb, ho, wo, t + 1, 0, ba.fd_kw);
-        blk_tap<GB, false>(cur, lidx, lval, geo.cap, 0, C, (t - t0) * C, tab, ba.tstride, u * GB,
-                           accb);
-        cur = nxt;
-      }
-    } else {
-      // one tap, the channels [c_lo, c_hi): the lane goes on in the tap's
-      // list where the previous block stopped
-      const int t0 = blk / ba.cblocks;
-      const int c_lo = (blk - t0 * ba.cblocks) * ba.RB;
-      if (c_lo == 0) cursor = 0;
-      cursor = blk_tap<GB, true>(cur, lidx, lval, geo.cap, cursor, c_lo + ba.RB, -c_lo, tab,
-                                 ba.tstride, u * GB, accb);
-      // the next block's list data, in flight across the barrier
-      const int tn = (blk + 1) / ba.cblocks;
-      tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
-                   tn == t0 ? cursor : 0, ba.fd_kw);
-    }
-    if (has_next) {
-      if (ba.nbuf == 1) __syncthreads();                 // every lane is done with the block
-      st.store(smem, odd || ba.nbuf == 1 ? ba.off_t0 : ba.off_t1, 0, min(R, r0n + ba.RB) - r0n,
-               ba.log2G, ba.tstride, ba.log2n);
-    }
-    __syncthreads();
-  }
-
-  // ---- epilogue
   const int nrows = min(ba.P, ba.items - item0);         // live rows of the tile
+  __syncthreads();                                       // every lane's sums are in LDS
   if (ba.kmode == 4 || ba.k < 0) {
     if (ba.kp == 4)
-      blk_kwta16<TO, GB, 4>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+      blk_kwta16<TO, GB, 4>(acc, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
                             ba.write_sums, y, out, lo);
     else if (ba.kp == 8)
-      blk_kwta16<TO, GB, 8>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+      blk_kwta16<TO, GB, 8>(acc, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
                             ba.write_sums, y, out, lo);
     else
-      blk_kwta16<TO, GB, 16>(acc, bias_s, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
+      blk_kwta16<TO, GB, 16>(acc, item0, nrows, ba.P, ba.log2U, ba.log2n, c_out, ba.k,
                              ba.write_sums, y, out, lo);
     return;
   }
-  // four lanes per row: the sums (bias added) into a row-major tile with an
-  // odd row stride over the table blocks, then the selection of the gather
-  // kernel's epilogue
+  // four lanes per row: the sums into a row-major tile with an odd row stride
+  // over the table blocks (no longer read), then the gather kernel's selection
   const int ostride = ba.ostride;
   float* otile = reinterpret_cast<float*>(smem + ba.off_out);
   for (int e = tid; e < nrows * c_out; e += BLK_BD) {
     const int r = (int)fdiv((uint32_t)e, ba.fd_cout), o = e - r * c_out;
     const int g = o >> ba.log2n, kk = o & (n - 1);
-    const float sv = acc[((g % GB) * n + kk) * BLK_BD + (r << ba.log2U) + g / GB] + bias_s[o];
+    const float sv = acc[((g % GB) * n + kk) * BLK_BD + (r << ba.log2U) + g / GB];
     otile[r * ostride + o] = sv;
     if (ba.write_sums) y[(int64_t)item0 * c_out + e] = sv;
   }
@@ -543,6 +460,301 @@ __global__ __launch_bounds__(BLK_BD) void mrs_blocks_f32(const uint16_t* __restr
       const uint32_t key = order_key(a);
       const bool win = !none && (key > sv.x || (key == sv.x && ch <= (int)sv.y));
       out[(int64_t)item0 * c_out + e] = win ? (TO)a : TO(0);
+    }
+  }
+}
+
+// Reductions and prefix sums over aligned groups of U = 1 << log2U lanes
+// (U <= 16, inside one DPP row): xor 1 and xor 2 within quads, then the
+// half-row mirror (joins the two quads of an 8-lane group) and the row mirror
+// (joins the two halves of a 16-lane row).  Every lane of the wavefront must
+// take part; every lane of a group ends with the group's result.
+template <typename Op>
+__device__ __forceinline__ uint32_t group_reduce(uint32_t v, int log2U, Op op) {
+  if (log2U >= 1) v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));
+  if (log2U >= 2) v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));
+  if (log2U >= 3) v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));
+  if (log2U >= 4) v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));
+  return v;
+}
+// Inclusive prefix sum over the group, lane position p = lane & (U - 1):
+// row shifts by 1, 2, 4, 8 taken only from lanes of the same group.
+__device__ __forceinline__ int group_incl_sum(int v, int log2U, int p) {
+  if (log2U >= 1) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false); v += p >= 1 ? t : 0; }
+  if (log2U >= 2) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false); v += p >= 2 ? t : 0; }
+  if (log2U >= 3) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false); v += p >= 4 ? t : 0; }
+  if (log2U >= 4) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false); v += p >= 8 ? t : 0; }
+  return v;
+}
+
+// k-WTA over the U lanes of each pixel, the lanes that computed its sums: lane
+// u holds channels u*KP .. u*KP+KP-1 (KP = GB * n) in its own accumulator
+// column, bias included, so no other lane's data is read and no barrier is
+// needed.  The k-th largest key is found bit by bit with group counts,
+// stopping as soon as the keys at or above the prefix are exactly k (their
+// minimum is then the k-th largest); ties go to the lower index; winners are
+// written as lists (non-zero values, ascending index) or densely.
+template <typename TO, int KP>
+__device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_t row, bool live,
+                                             int c_out, int k, int write_sums,
+                                             float* __restrict__ y, TO* __restrict__ out,
+                                             const ListOut& lo) {
+  const int tid = threadIdx.x;
+  const int p = tid & ((1 << log2U) - 1);                // lane position in the group
+  const int o0 = p * KP;                                 // first channel of the lane
+  float v[KP];
+  uint32_t key[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    v[j] = acc[j * BLK_BD + tid];
+    key[j] = live ? order_key(v[j]) : 0u;                // 0: below every real key
+  }
+  if (write_sums && live) {
+    float* yr = y + row * c_out + o0;                    // 16-byte aligned (host)
+#pragma unroll
+    for (int j = 0; j < KP; j += 4)
+      *reinterpret_cast<float4*>(yr + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+  }
+  if (k < 0) return;
+  uint32_t thr = 0u;
+  int need = 0;
+  if (k > 0 && k < c_out) {
+    uint32_t pre = 0u;
+    int cntp = c_out;
+    bool done = !live;
+    for (int bit = 31; bit >= 0; --bit) {
+      if (__ballot(!done) == 0ull) break;               // every row of the wavefront found
+      const uint32_t cand = pre | (1u << bit);
+      uint32_t c = 0;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) c += key[j] >= cand ? 1u : 0u;
+      c = group_reduce(c, log2U, OpAdd{});
+      if (!done) {
+        if ((int)c >= k) {
+          pre = cand;
+          cntp = (int)c;
+        }
+        if (cntp == k) done = true;
+      }
+    }
+    // the k-th largest key: the least key at or above the prefix
+    uint32_t mn = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) mn = (key[j] >= pre && key[j] < mn) ? key[j] : mn;
+    thr = group_reduce(mn, log2U, OpMin{});
+    uint32_t gt = 0;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) gt += key[j] > thr ? 1u : 0u;
+    gt = group_reduce(gt, log2U, OpAdd{});
+    need = k - (int)gt;
+  }
+  // ties in index order: this lane's first tie has rank (ties of the lanes before)
+  int eq = 0;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_out && key[j] == thr) ? 1 : 0;
+  int tie_rank = group_incl_sum(eq, log2U, p) - eq;
+  uint32_t winm = 0;                                    // bit j: channel o0 + j wins
+  int wcount = 0;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    bool w;
+    if (!live || k == 0) {
+      w = false;
+    } else if (k >= c_out) {
+      w = true;
+    } else if (key[j] > thr) {
+      w = true;
+    } else if (key[j] == thr) {
+      w = tie_rank < need;
+      ++tie_rank;
+    } else {
+      w = false;
+    }
+    winm |= w ? 1u << j : 0u;
+    wcount += (lo.idx ? (w && v[j] != 0.f) : w) ? 1 : 0;
+  }
+  if (lo.idx) {
+    const int incl = group_incl_sum(wcount, log2U, p);
+    int pos = incl - wcount;
+    if (live) {
+      uint16_t* oi = lo.idx + row * lo.cap;
+      TO* ov = static_cast<TO*>(lo.val) + row * lo.cap;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        if (((winm >> j) & 1u) && v[j] != 0.f) {
+          oi[pos] = (uint16_t)(o0 + j);
+          ov[pos] = (TO)v[j];
+          ++pos;
+        }
+      }
+      if (p == (1 << log2U) - 1) lo.cnt[row] = incl;
+    }
+  } else if (live) {
+    TO* orow = out + row * c_out + o0;
+#pragma unroll
+    for (int j = 0; j < KP; j += 4)
+      *reinterpret_cast<float4*>(orow + j) =
+          make_float4((winm >> j) & 1u ? v[j] : 0.f, (winm >> (j + 1)) & 1u ? v[j + 1] : 0.f,
+                      (winm >> (j + 2)) & 1u ? v[j + 2] : 0.f, (winm >> (j + 3)) & 1u ? v[j + 3] : 0.f);
+  }
+}
+
+// KP: channels per lane (GB * n) when the k-WTA runs on the lanes' own
+// accumulator columns; 0: the selection of ba.kmode on a copied tile.  Up to
+// 16 channels per lane the registers are held to three wavefronts per SIMD.
+// QK: with the four-lane selection in place (kmode 6-8), its list length
+// (8, 16 or 32); 0 otherwise.
+template <typename TO, int GB, bool CH, int KP, int QK>
+__global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_blocks_f32(const uint16_t* __restrict__ lidx,
+                                                         const float* __restrict__ lval,
+                                                         const int32_t* __restrict__ lcnt,
+                                                         const uint2* __restrict__ aug,
+                                                         const float* __restrict__ bias,
+                                                         float* __restrict__ y,
+                                                         TO* __restrict__ out, ListOut lo,
+                                                         ConvGeom geo, BlocksArgs ba) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int n = 1 << ba.log2n;
+  const int G = geo.G;
+  const int C = geo.C;
+  const int T_ = geo.KH * geo.KW;
+  const int R = T_ * C;
+  const int c_out = geo.c_out;
+  const int U = 1 << ba.log2U;
+  const int ps = tid >> ba.log2U;                        // pixel slot of the lane
+  const int u = tid & (U - 1);                           // unit: sets u*GB .. u*GB+GB-1
+  const int nacc = GB << ba.log2n;                       // the lane's channels u*nacc ..
+  float* acc = reinterpret_cast<float*>(smem);           // [GB * n][BLK_BD]
+  unsigned char* accb = smem + tid * 4;                  // this lane's column
+  const bool one_block = ba.nblocks == 1;
+  BlockStage<GB> st;
+  auto stage_first = [&]() {
+    // the first block, in passes of BLK_ENTRIES entries (a single block may
+    // be larger than what one pass holds in registers)
+    const int rb0 = min(R, ba.RB);
+    const int rpp = BLK_ENTRIES >> ba.log2G;              // rows per pass
+    for (int rs = 0; rs < rb0; rs += rpp) {
+      const int re = min(rb0, rs + rpp);
+      st.load(aug, rs, re, G);
+      st.store(smem, ba.off_t0, rs, re - rs, ba.log2G, ba.tstride, ba.log2n);
+    }
+  };
+  // a table of one block is staged once for all the workgroup's tiles
+  if (one_block) {
+    stage_first();
+    __syncthreads();
+  }
+  for (int tile = blockIdx.x; tile < ba.ntiles; tile += gridDim.x) {
+    const int item0 = tile * ba.P;
+    const int item = item0 + ps;
+    const bool live = item < ba.items;
+    int bb = 0, ho = 0, wo = 0;
+    if (live) {
+      const uint32_t t1 = fdiv((uint32_t)item, ba.fd_wo);
+      wo = item - (int)(t1 * ba.fd_wo.d);
+      const uint32_t t2 = fdiv(t1, ba.fd_ho);
+      ho = (int)(t1 - t2 * ba.fd_ho.d);
+      bb = (int)t2;
+    }
+    // the first tap's count and first chunks, then the table while they fly
+    TapPre cur;
+    tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
+    // accumulators start at the bias of their channels
+#pragma unroll
+    for (int j = 0; j < GB * 16; ++j)
+      if (j < nacc) acc[j * BLK_BD + tid] = bias ? bias[u * nacc + j] : 0.f;
+    if (!one_block) {
+      stage_first();
+      __syncthreads();
+    }
+
+    int cursor = 0;                                      // place in the current tap's list
+    for (int blk = 0; blk < ba.nblocks; ++blk) {
+      const int r0n = (blk + 1) * ba.RB;
+      const bool has_next = blk + 1 < ba.nblocks;
+      const bool odd = ba.nbuf == 2 && (blk & 1);
+      const uint2* tab = reinterpret_cast<const uint2*>(smem + (odd ? ba.off_t1 : ba.off_t0));
+      // the next table block's loads (issued after the prefetched list data)
+      if (has_next) st.load(aug, r0n, min(R, r0n + ba.RB), G);
+      if constexpr (!CH) {
+        // whole taps t0 .. t1-1; the next tap (of this block or the next
+        // one) is prefetched while one is processed
+        const int t0 = blk * ba.tpb, t1 = min(T_, t0 + ba.tpb);
+        for (int t = t0; t < t1; ++t) {
+          TapPre nxt;
+          tap_prefetch(nxt, lidx, lval, lcnt, geo, live, bb, ho, wo, t + 1, 0, ba.fd_kw);
+          blk_tap<GB, false>(cur, lidx, lval, geo.cap, 0, C, (t - t0) * C, tab, ba.tstride,
+                             u * GB, accb);
+          cur = nxt;
+        }
+      } else {
+        // one tap, the channels [c_lo, c_hi): the lane goes on in the tap's
+        // list where the previous block stopped
+        const int t0 = blk / ba.cblocks;
+        const int c_lo = (blk - t0 * ba.cblocks) * ba.RB;
+        if (c_lo == 0) cursor = 0;
+        cursor = blk_tap<GB, true>(cur, lidx, lval, geo.cap, cursor, c_lo + ba.RB, -c_lo, tab,
+                                   ba.tstride, u * GB, accb);
+        // the next block's list data, in flight across the barrier
+        const int tn = (blk + 1) / ba.cblocks;
+        tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
+                     tn == t0 ? cursor : 0, ba.fd_kw);
+      }
+      if (has_next) {
+        if (ba.nbuf == 1) __syncthreads();               // every lane is done with the block
+        st.store(smem, odd || ba.nbuf == 1 ? ba.off_t0 : ba.off_t1, 0,
+                 min(R, r0n + ba.RB) - r0n, ba.log2G, ba.tstride, ba.log2n);
+      }
+      if (!one_block) __syncthreads();
+    }
+
+    // ---- epilogue
+    if constexpr (KP > 0) {
+      // the lanes' own columns: no barrier, the next tile starts right after
+      if constexpr (QK > 0) {
+        // a pixel's four lanes are a quad holding its four quarters: the
+        // gather kernel's four-lane selection reads them in place and writes
+        // the lists straight to their rows
+        const FastDiv one{1u, 0u, 0u};
+        const RowMap rm{0, 1, 0, 0, 0, 0, 0, (int64_t)item0, one};
+        uint2* sel = reinterpret_cast<uint2*>(smem + ba.off_sel);
+        uint16_t* gi = lo.idx ? lo.idx + (int64_t)item0 * lo.cap : nullptr;
+        TO* gv = lo.idx ? static_cast<TO*>(lo.val) + (int64_t)item0 * lo.cap : nullptr;
+        kwta_quad_item<float, TO, QK, BLK_BD>(acc + tid, 0, ps, live, rm, c_out, ba.k, 0, sel, gi,
+                                              gv, lo.cap, lo.cnt);
+        if (live && (ba.write_sums || !lo.idx)) {
+          wave_lds_order();                              // sel of this quad, written by lane 0
+          const uint2 sv = sel[ps];
+          const int o0 = u * KP;
+          float* yr = y + (int64_t)item * c_out + o0;
+          TO* orow = out + (int64_t)item * c_out + o0;
+#pragma unroll
+          for (int j = 0; j < KP; j += 4) {
+            float a4[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) a4[e] = acc[(j + e) * BLK_BD + tid];
+            if (ba.write_sums)
+              *reinterpret_cast<float4*>(yr + j) = make_float4(a4[0], a4[1], a4[2], a4[3]);
+            if (!lo.idx) {
+              float w4[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t key = order_key(a4[e]);
+                const bool win = ba.k > 0 && (key > sv.x || (key == sv.x && o0 + j + e <= (int)sv.y));
+                w4[e] = win ? a4[e] : 0.f;
+              }
+              *reinterpret_cast<float4*>(orow + j) = make_float4(w4[0], w4[1], w4[2], w4[3]);
+            }
+          }
+        }
+      } else {
+        blk_kwta_own<TO, KP>(acc, ba.log2U, (int64_t)item, live, c_out, ba.k, ba.write_sums, y,
+                             out, lo);
+      }
+    } else {
+      blk_epilogue_tile<TO, GB>(smem, acc, item0, c_out, y, out, lo, ba);
+      __syncthreads();                                   // before the accumulators are reused
     }
   }
 }

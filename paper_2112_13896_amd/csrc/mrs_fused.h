@@ -119,7 +119,10 @@ struct RowMap {
 // or -1).  Rows are read with an odd stride (bank-conflict free).
 // One item (tile slot `it`) per quad; every lane of the wavefront takes part
 // (the DPP exchanges), `live` quads write.
-template <typename A, typename TO, int KMAX>
+// ES: element stride of the row (1: a row-major tile; other: the quad's lanes
+// read their quarters from LDS columns of that stride, `otile` then being the
+// lane's own column and ostride unused).
+template <typename A, typename TO, int KMAX, int ES = 1>
 __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int it, bool live,
                                                const RowMap& rm, int c, int k, int shift,
                                                uint2* sel, uint16_t* tl_idx, TO* tl_val, int cap,
@@ -129,7 +132,9 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
   const int L = (c + 3) >> 2;                          // row quarter of a lane
   const int i_lo = qd * L, i_hi = min(c, i_lo + L);
   {
-    const A* v = otile + (live ? it : 0) * ostride;
+    // element i of the row (i_lo <= i < i_hi) is vq[(i - i_lo) * ES]
+    const A* vq = ES == 1 ? otile + (live ? it : 0) * ostride + i_lo : otile;
+    auto v = [&](int i) -> A { return vq[(i - i_lo) * ES]; };
     // --- the threshold: per-lane top-KMAX of the quarter, merged over the quad
     // (keys past the quarter are 0: a 0 never changes the k-th largest)
     uint32_t top[KMAX];
@@ -143,7 +148,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
 #pragma unroll
         for (int j = 0; j < KMAX; ++j) {
           const int i = i0 + j;
-          const uint32_t kx = order_key(v[i < i_hi ? i : i_hi - 1]);
+          const uint32_t kx = order_key(v(i < i_hi ? i : i_hi - 1));
           blk[j] = i < i_hi ? kx : 0u;
         }
         bitonic_sort_desc<KMAX>(blk);
@@ -186,7 +191,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
 #pragma unroll
         for (int j = 0; j < BK; ++j) {
           const int i = i0 + j;
-          const uint32_t key = order_key(v[i < i_hi ? i : i_hi - 1]);
+          const uint32_t key = order_key(v(i < i_hi ? i : i_hi - 1));
           const uint32_t bit = i < i_hi ? 1u << (i - i_lo) : 0u;
           gtm |= key > thr ? bit : 0u;
           eqm |= key == thr ? bit : 0u;
@@ -210,7 +215,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
     uint32_t putm = 0u;
     for (uint32_t w = gtm | tm; w != 0u; w &= w - 1u) {
       const int j = __builtin_ctz(w);
-      putm |= kwta_out<A, TO>(v[i_lo + j], shift) != TO(0) ? 1u << j : 0u;
+      putm |= kwta_out<A, TO>(v(i_lo + j), shift) != TO(0) ? 1u << j : 0u;
     }
     const int win_l = __popc(putm);
     const int pos0 = quad_excl_sum(win_l, qd);           // list position of the first winner
@@ -229,7 +234,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
         for (uint32_t w = putm; w != 0u; w &= w - 1u) {
           const int i = i_lo + __builtin_ctz(w);
           tl_idx[it * cap + pos] = (uint16_t)i;
-          tl_val[it * cap + pos] = kwta_out<A, TO>(v[i], shift);
+          tl_val[it * cap + pos] = kwta_out<A, TO>(v(i), shift);
           ++pos;
         }
       }

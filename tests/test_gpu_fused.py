@@ -158,6 +158,9 @@ CASES = [
     ("f32", (3, 10, 10, 64), 7, 3, 3, 1, 1, 64, 16, 1, 8, True, None, "lists", ("blocks", None)),
     ("f32", (2, 8, 9, 96), 9, 3, 3, 1, 1, 128, 4, 1, 20, False, None, "lists", ("blocks", None)),
     ("f32", (2, 7, 7, 64), 7, 3, 3, 1, 1, 128, 4, 1, 16, True, None, "dense", ("blocks", None)),
+    # 256 sets of one kernel (64 lanes per pixel): k-WTA on a copied tile, 16 lanes per row
+    ("f32", (2, 5, 6, 32), 5, 3, 3, 1, 1, 256, 1, 1, 40, True, None, "lists", ("blocks", None)),
+    ("f32", (2, 5, 6, 32), 5, 3, 3, 1, 1, 256, 1, 1, 40, False, None, "dense", ("blocks", None)),
     # a table too large for LDS, one output vector per sample: one workgroup
     # per sample (keyword-spotting linear1: the 5x5x64 map as a whole-map conv)
     ("i8", (8, 5, 5, 64), 8, 5, 5, 1, 0, 1500, 20, 1, 75, False, 8, "lists", ("sample", None)),
