@@ -11,6 +11,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "wave_ops.h"
+
 namespace cs {
 
 constexpr int COMPACT_BATCH = 8;   // 64-element chunks of a row in flight together
@@ -92,6 +94,97 @@ __global__ __launch_bounds__(256) void compact_narrow(const T* __restrict__ x, i
       val[row * c + pos] = v;
     }
     if (j == 0 && row < rows) cnt[row] = __popcll(m);
+  }
+}
+
+// Rows whose length is a multiple of E = 16 / sizeof(T) elements (16-byte
+// rows, 16-byte aligned base): each lane loads E consecutive elements with one
+// 16-byte load.  A row takes NL = c / E lanes; rows of NL <= 16 lanes are
+// packed 64 / L to a wavefront in aligned groups of L = NL rounded up to a
+// power of two, longer rows take a whole wavefront each and go through the
+// row 64 vectors at a time.  A lane loads only when its row exists and its
+// vector lies inside the row (v < NL), so every address read is inside x;
+// every position written is below the row's non-zero count <= c.  A lane's
+// non-zeros go to the positions after those of the lanes before it in the
+// row (a group prefix sum of the per-lane counts by DPP row shifts), in index
+// order.
+template <typename T>
+struct Vec16;
+template <>
+struct Vec16<float> {
+  static constexpr int E = 4;
+  using type = float4;
+  static __device__ __forceinline__ float get(const float4& v, int e) {
+    return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
+  }
+};
+template <>
+struct Vec16<int8_t> {
+  static constexpr int E = 16;
+  using type = int4;
+  static __device__ __forceinline__ int8_t get(const int4& v, int e) {
+    const int w = e < 4 ? v.x : (e < 8 ? v.y : (e < 12 ? v.z : v.w));
+    return (int8_t)(w >> (8 * (e & 3)));
+  }
+};
+
+// Inclusive prefix sum over aligned groups of 1 << lg lanes (lg <= 4, one DPP
+// row) or the whole wavefront (lg == 6); p = the lane's place in its group.
+__device__ __forceinline__ int compact_group_incl(int v, int lg, int p) {
+  if (lg == 6) return (int)wave_incl_scan((uint32_t)v, 0u, OpAdd{});
+  if (lg >= 1) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false); v += p >= 1 ? t : 0; }
+  if (lg >= 2) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false); v += p >= 2 ? t : 0; }
+  if (lg >= 3) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false); v += p >= 4 ? t : 0; }
+  if (lg >= 4) { const int t = __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false); v += p >= 8 ? t : 0; }
+  return v;
+}
+
+// lg: log2 of the lanes per row group (0..4, or 6: one row per wavefront).
+template <typename T>
+__global__ __launch_bounds__(256) void compact_vec(const T* __restrict__ x, int64_t rows, int c,
+                                                   int lg, uint16_t* __restrict__ idx,
+                                                   T* __restrict__ val,
+                                                   int32_t* __restrict__ cnt) {
+  using V = Vec16<T>;
+  constexpr int E = V::E;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int NL = c / E;                                   // vectors per row (c % E == 0)
+  const int L = 1 << lg;
+  const int rpw = 64 >> lg;                               // rows per wavefront (lg == 6: 1)
+  const int sub = lane >> lg, p = lane & (L - 1);
+  const int last = L - 1;
+  for (int64_t r0 = wave * rpw; r0 < rows; r0 += nwaves * rpw) {
+    const int64_t row = r0 + sub;
+    const bool rv = row < rows;
+    const T* xr = x + (rv ? row : 0) * c;
+    uint16_t* ir = idx + (rv ? row : 0) * c;
+    T* vr = val + (rv ? row : 0) * c;
+    int run = 0;
+    for (int v0 = 0; v0 < NL; v0 += L) {                  // uniform: one pass unless lg == 6
+      const int vi = v0 + p;
+      const bool ld = rv && vi < NL;
+      typename V::type q{};
+      if (ld) q = reinterpret_cast<const typename V::type*>(xr)[vi];
+      uint32_t nzm = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) nzm |= (ld && V::get(q, e) != T(0)) ? 1u << e : 0u;
+      const int nl = __popc(nzm);
+      const int incl = compact_group_incl(nl, lg, p);
+      int pos = run + incl - nl;
+      if (ld) {
+        for (uint32_t m = nzm; m != 0u; m &= m - 1u) {
+          const int e = __builtin_ctz(m);
+          ir[pos] = (uint16_t)(vi * E + e);
+          vr[pos] = V::get(q, e);
+          ++pos;
+        }
+      }
+      // the group's total: its last lane's inclusive sum
+      run += lg == 6 ? __builtin_amdgcn_readlane(incl, 63) : __shfl(incl, (lane & ~last) + last, 64);
+    }
+    if (rv && p == 0) cnt[row] = run;
   }
 }
 

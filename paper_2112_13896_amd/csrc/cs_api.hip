@@ -54,9 +54,45 @@ int blocks_for(int64_t threads, int bd, int64_t cap = 1 << 20) {
 }
 
 // ---------------------------------------------------------------- compaction
+int device_cus(int* cus);
+
+// The vectorised compaction's lanes per row group (log2): 16-byte rows of at
+// most 16 vectors share a wavefront in power-of-two groups, longer ones take a
+// wavefront each; -1 when the rows are not whole 16-byte vectors or x is not
+// 16-byte aligned.
+int compact_vec_lg(cs_dtype xt, const void* x, int c) {
+  const int E = xt == CS_I8 ? 16 : 4;
+  if (c % E != 0 || reinterpret_cast<uintptr_t>(x) % 16 != 0) return -1;
+  const int nl = c / E;
+  if (nl > 16) return 6;
+  int lg = 0;
+  while ((1 << lg) < nl) ++lg;
+  return lg;
+}
+
 int compact_checked(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* idx, void* val,
                     int32_t* cnt, hipStream_t stream) {
   if (rows == 0) return CS_OK;
+  const int lg = compact_vec_lg(xt, x, c);
+  if (lg >= 0) {
+    int cus = 0;
+    const int dst = device_cus(&cus);
+    if (dst != CS_OK) return dst;
+    const int64_t rpw = 64 >> lg;                          // rows per wavefront
+    const int64_t waves = (rows + rpw - 1) / rpw;
+    int64_t blocks = (waves + 3) / 4;                      // 4 wavefronts per workgroup
+    const int64_t cap = (int64_t)cus * 16;                 // at most 64 wavefronts per CU
+    if (blocks > cap) blocks = cap;
+    if (xt == CS_I8)
+      hipLaunchKernelGGL(cs::compact_vec<int8_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         static_cast<const int8_t*>(x), rows, c, lg, idx,
+                         static_cast<int8_t*>(val), cnt);
+    else
+      hipLaunchKernelGGL(cs::compact_vec<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         static_cast<const float*>(x), rows, c, lg, idx, static_cast<float*>(val),
+                         cnt);
+    return launch_status();
+  }
   if (c >= 64) {
     const int64_t threads = rows * 64;
     const int grid = blocks_for(threads, 256, 65536);

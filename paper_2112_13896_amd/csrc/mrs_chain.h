@@ -10,7 +10,11 @@
 // The barriers' workgroup-scope release/acquire order each phase's global
 // stores before the next phase's loads; the lists come back from L2 of the
 // same compute unit.  Each phase lays out the dynamic LDS its own way from
-// offset 0 (the launch reserves the largest).
+// offset 0 (the launch reserves the largest, about 62 KB).  The registers are
+// held to 64 per lane (eight wavefronts per SIMD), so that two workgroups -
+// two images, from one batch or from the next batch launched on another
+// stream - share a compute unit and fill each other's latency-bound phases;
+// a single launch is slower that way, a stream of batches faster.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -22,7 +26,7 @@
 namespace cs {
 
 template <int POOL, int KW>
-__global__ __launch_bounds__(SCAT_BD) void dense_scatter_sample(
+__global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(
     const int8_t* __restrict__ x, const uint16_t* __restrict__ aug0,
     const int32_t* __restrict__ bias0, int32_t* __restrict__ y0, ListOut lo0, ConvGeom geo0,
     DenseArgs da, const uint16_t* __restrict__ aug, const int32_t* __restrict__ bias,
