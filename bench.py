@@ -14,7 +14,7 @@ Cache-cold protocol: the chain rotates among buffer sets (input + every
 intermediate), as many as make the bytes one pass touches (the sum of its
 launches' algorithmic bytes) times the number of sets exceed 512 MiB, so a set
 comes round again only after twice the 256 MiB Infinity Cache of other data;
-and a 512 MiB buffer is written before every timed region.  The K timed passes
+and a 512 MiB buffer is read before every timed region.  The K timed passes
 (K <= 256; else one pass per buffer set) are recorded once into a HIP graph (a
 serving loop's batches in one launch), pass i on buffer set i mod sets, in
 three schedules: one after another; each pass's first kernel on one stream and
@@ -365,9 +365,11 @@ SET_MEM_CAP = 24 << 30              # most device memory the rotating buffer set
 
 
 def scrub(buf) -> None:
-    """Write a buffer twice the size of the last-level cache, so that no
-    earlier launch's data is still cached (outside every timed region)."""
-    buf.fill_(1)
+    """Read a buffer twice the size of the last-level cache, so that no
+    earlier launch's data is still cached (outside every timed region).  A
+    read leaves clean lines behind: a write would leave the caches full of
+    dirty lines whose write-back the next kernel would pay for."""
+    buf.sum()
 
 
 def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0,
@@ -377,8 +379,9 @@ def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0
     Buffer sets (input + every intermediate) rotate; their number is chosen
     from the bytes one pass actually touches (the sum of its launches'
     algorithmic bytes) so that a set is reused only after more than
-    `rotate_mib` of other data, and a 512 MiB scrub precedes every timed
-    region, so no pass finds its data in the 256 MiB Infinity Cache or in L2."""
+    `rotate_mib` of other data, and a 512 MiB read (the scrub) precedes every
+    timed region, so no pass finds its data in the 256 MiB Infinity Cache or
+    in L2."""
     import torch
 
     from paper_2112_13896_amd.network import Network
@@ -405,7 +408,7 @@ def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0
     for j in range(nsets):                           # every set holds a whole pass's data
         net.forward(xs[j], sets[j])
     torch.cuda.synchronize()
-    scrub_buf = torch.empty(int(2 * MALL_MIB * 2 ** 20) // 4, dtype=torch.int32, device="cuda")
+    scrub_buf = torch.ones(int(2 * MALL_MIB * 2 ** 20) // 4, dtype=torch.int32, device="cuda")
     if eager_only:
         # profiler mode: eager passes only (every launch a plain dispatch)
         t0 = time.perf_counter()

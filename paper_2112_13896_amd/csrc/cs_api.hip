@@ -78,7 +78,7 @@ int compact_checked(cs_dtype xt, const void* x, int64_t rows, int c, uint16_t* i
     int cus = 0;
     const int dst = device_cus(&cus);
     if (dst != CS_OK) return dst;
-    const int64_t rpw = 64 >> lg;                          // rows per wavefront
+    const int64_t rpw = 64 >> lg;                          // rows per wavefront (lg 6: one)
     const int64_t waves = (rows + rpw - 1) / rpw;
     int64_t blocks = (waves + 3) / 4;                      // 4 wavefronts per workgroup
     const int64_t cap = (int64_t)cus * 16;                 // at most 64 wavefronts per CU

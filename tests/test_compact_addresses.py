@@ -25,11 +25,35 @@ def host_lg(c, E):
     return lg
 
 
+UN = 1            # vector rounds per wavefront round
+
+
+def put(nl_of, q, lanes_ld, vi_of, run, lg, rows_of, idx, val, c, E):
+    """compact_put for all 64 lanes: writes the lists, returns each lane's
+    group total."""
+    L = 1 << lg
+    tot = np.zeros(64, dtype=np.int64)
+    for lane in range(64):
+        p = lane & (L - 1)
+        g0 = lane - p
+        incl = int(nl_of[g0:lane + 1].sum())
+        pos = run[lane] + incl - nl_of[lane]
+        if lane in lanes_ld:
+            row = rows_of[lane]
+            for e in np.flatnonzero(q[lane] != 0):
+                assert 0 <= pos < c                      # inside the row's list
+                idx[row, pos] = vi_of[lane] * E + e
+                val[row, pos] = q[lane][e]
+                pos += 1
+        tot[lane] = int(nl_of[g0:g0 + L].sum())
+    return tot
+
+
 def model(x, E, cus=256):
     rows, c = x.shape
     lg = host_lg(c, E)
     assert lg >= 0
-    rpw = 64 >> lg
+    rpw = 1 if lg == 6 else (64 >> lg) * UN            # rows per wavefront round (host)
     waves = -(-rows // rpw)
     blocks = min(-(-waves // 4), cus * 16)
     nwaves = blocks * 4
@@ -40,49 +64,56 @@ def model(x, E, cus=256):
     cnt = np.full(rows, -1, dtype=np.int64)
     flat = x.reshape(-1)
     loads = []
+
+    def load(row, vi):
+        a = row * c + vi * E                            # element address of the 16-byte load
+        assert 0 <= a and a + E <= rows * c
+        loads.append(a)
+        return flat[a:a + E]
+
     for w in range(nwaves):
-        for r0 in range(w * rpw, rows, nwaves * rpw):
-            run = np.zeros(64, dtype=np.int64)
-            for v0 in range(0, NL, L):
-                nl = np.zeros(64, dtype=np.int64)
-                q = {}
-                for lane in range(64):
-                    sub, p = lane >> lg, lane & (L - 1)
-                    row = r0 + sub
-                    vi = v0 + p
-                    if row < rows and vi < NL:
-                        a = row * c + vi * E          # element address of the 16-byte load
-                        loads.append(a)
-                        assert 0 <= a and a + E <= rows * c
-                        q[lane] = flat[a:a + E]
-                        nl[lane] = int((q[lane] != 0).sum())
-                for lane in range(64):
-                    sub, p = lane >> lg, lane & (L - 1)
-                    row = r0 + sub
-                    g0 = lane - p
-                    incl = int(nl[g0:lane + 1].sum())
-                    pos = run[lane] + incl - nl[lane]
-                    if lane in q:
-                        for e in np.flatnonzero(q[lane] != 0):
-                            assert 0 <= pos < c          # inside the row's list
-                            idx[row, pos] = (v0 + p) * E + e
-                            val[row, pos] = q[lane][e]
-                            pos += 1
-                for lane in range(64):
-                    p = lane & (L - 1)
-                    g0 = lane - p
-                    run[lane] += int(nl[g0:g0 + L].sum())
-            for lane in range(64):
-                sub, p = lane >> lg, lane & (L - 1)
-                if r0 + sub < rows and p == 0:
-                    cnt[r0 + sub] = run[lane]
+        if lg <= 4:
+            g = 64 >> lg
+            for r0 in range(w * g * UN, rows, nwaves * g * UN):
+                for u in range(UN):
+                    q, nl, rows_of, vi_of = {}, np.zeros(64, dtype=np.int64), {}, {}
+                    for lane in range(64):
+                        sub, p = lane >> lg, lane & (L - 1)
+                        row = r0 + u * g + sub
+                        if row < rows and p < NL:
+                            q[lane] = load(row, p)
+                            nl[lane] = int((q[lane] != 0).sum())
+                            rows_of[lane], vi_of[lane] = row, p
+                    tot = put(nl, q, q, vi_of, np.zeros(64, dtype=np.int64), lg, rows_of, idx,
+                              val, c, E)
+                    for lane in range(64):
+                        sub, p = lane >> lg, lane & (L - 1)
+                        row = r0 + u * g + sub
+                        if row < rows and p == 0:
+                            cnt[row] = tot[lane]
+        else:
+            for row in range(w, rows, nwaves):
+                run = np.zeros(64, dtype=np.int64)
+                for v0 in range(0, NL, 64 * UN):
+                    for u in range(UN):
+                        q, nl, rows_of, vi_of = {}, np.zeros(64, dtype=np.int64), {}, {}
+                        for lane in range(64):
+                            vi = v0 + u * 64 + lane
+                            if vi < NL:
+                                q[lane] = load(row, vi)
+                                nl[lane] = int((q[lane] != 0).sum())
+                                rows_of[lane], vi_of[lane] = row, vi
+                        run = run + put(nl, q, q, vi_of, run, 6, rows_of, idx, val, c, E)
+                cnt[row] = run[0]
     return idx, val, cnt, loads
 
 
 @pytest.mark.parametrize("rows,c,dtype,nnz", [
     (37, 96, np.int8, 12),        # 6 vectors per row, groups of 8 lanes, 8 rows per wavefront
     (29, 64, np.float32, 7),      # 16 lanes per row, 4 rows per wavefront, partial last wavefront
-    (5, 1024, np.float32, 102),   # one row per wavefront, 4 passes of 64 vectors
+    (5, 1024, np.float32, 102),   # one row per wavefront, 4 rounds of 64 vectors
+    (3, 2048, np.float32, 300),   # one row per wavefront, 8 rounds (two batches of 4)
+    (300, 64, np.float32, 7),     # several row groups per wavefront round
     (7, 512, np.int8, 64),        # 32 vectors: one row per wavefront, lanes past the row idle
     (11, 16, np.int8, 16),        # one vector per row (a full row), 64 rows per wavefront
     (3, 4, np.float32, 2),        # one vector per row
