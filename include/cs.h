@@ -54,7 +54,8 @@ typedef enum {
   CS_ERR_DTYPE = -3,      /* unsupported dtype or dtype combination              */
   CS_ERR_COLLISION = -4,  /* cs_pack: two kernels of one set share a slot        */
   CS_ERR_WORKSPACE = -5,  /* workspace missing or smaller than required          */
-  CS_ERR_DEVICE = -6      /* HIP launch or runtime error                         */
+  CS_ERR_DEVICE = -6,     /* HIP launch or runtime error                         */
+  CS_ERR_UNSUPPORTED = -7 /* not available in this build of the library          */
 } cs_status;
 
 typedef enum { CS_I8 = 0, CS_I32 = 1, CS_F32 = 2 } cs_dtype;
@@ -560,6 +561,26 @@ int cs_kwta_lists(cs_dtype it, const void* in, int64_t rows, int c, int k, cs_dt
  * xt.  Returns 0 for invalid arguments.  Host only.
  */
 size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in);
+
+/*
+ * cs_product_count - the number of weight x activation products the
+ * multiply-route-sum kernels have formed on the current device since the
+ * last reset (Section 3.2 and Figure 1: only pairs of a non-zero activation
+ * and a non-zero packed weight are multiplied, so the work falls with the
+ * product of the two densities).  Only the counting build of the library
+ * (libcs_count.so, compiled with CS_COUNT_PRODUCTS) keeps the count: each
+ * kernel adds the products of its live list entries to one device counter.
+ * The dense-input matrix-core layers are not counted (they are dense
+ * contractions, not routed products).
+ *
+ *  count  out (host, may be NULL): the count, read after the device has
+ *         finished all work queued before the call.
+ *  reset  non-zero: set the counter to 0 after reading it.
+ *
+ * Synchronises the current device.  Errors: CS_ERR_UNSUPPORTED in the
+ * product build (libcs.so), CS_ERR_DEVICE.
+ */
+int cs_product_count(unsigned long long* count, int reset);
 
 /* cs_status_str - static, never-NULL description of a status code. */
 const char* cs_status_str(int status);

@@ -9,6 +9,8 @@ import ctypes
 import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs.so")
+# the same library with the product counter compiled in (tests only)
+COUNT_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs_count.so")
 
 CS_OK = 0
 CS_ERR_ARG = -1
@@ -17,6 +19,7 @@ CS_ERR_DTYPE = -3
 CS_ERR_COLLISION = -4
 CS_ERR_WORKSPACE = -5
 CS_ERR_DEVICE = -6
+CS_ERR_UNSUPPORTED = -7
 
 CS_I8, CS_I32, CS_F32 = 0, 1, 2
 
@@ -70,6 +73,7 @@ SIGNATURES = {
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),
     "cs_kwta_lists": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp]),
     "cs_workspace_bytes": (_sz, [_i, _i, _i64, _i]),
+    "cs_product_count": (_i, [_c.POINTER(_c.c_ulonglong), _i]),
     "cs_status_str": (_c.c_char_p, [_i]),
 }
 
@@ -81,22 +85,54 @@ class CSError(RuntimeError):
 
 
 _LIB = None
+_LOADED = {}
+
+
+def _load(path: str) -> ctypes.CDLL:
+    if path not in _LOADED:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with "
+                               "`python -m paper_2112_13896_amd.build`")
+        L = ctypes.CDLL(path)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _LOADED[path] = L
+    return _LOADED[path]
 
 
 def lib() -> ctypes.CDLL:
     """The loaded library (raises if it is not built)."""
     global _LIB
     if _LIB is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
-                               "`python -m paper_2112_13896_amd.build`")
-        L = ctypes.CDLL(LIB_PATH)
-        for name, (res, args) in SIGNATURES.items():
-            f = getattr(L, name)
-            f.restype = res
-            f.argtypes = args
-        _LIB = L
+        _LIB = _load(LIB_PATH)
     return _LIB
+
+
+class counting_library:
+    """Context manager: every call made through the binding inside it goes to
+    the counting build (libcs_count.so), whose kernels count the products they
+    form (read with product_count()).  Tests only."""
+
+    def __enter__(self):
+        global _LIB
+        self._prev = _LIB
+        _LIB = _load(COUNT_LIB_PATH)
+        return self
+
+    def __exit__(self, *exc):
+        global _LIB
+        _LIB = self._prev
+        return False
+
+
+def product_count(reset: bool = False) -> int:
+    """cs_product_count of the library in use (raises CSError with
+    CS_ERR_UNSUPPORTED outside the counting build)."""
+    v = ctypes.c_ulonglong(0)
+    check("cs_product_count", lib().cs_product_count(ctypes.byref(v), int(bool(reset))))
+    return int(v.value)
 
 
 def status_str(status: int) -> str:

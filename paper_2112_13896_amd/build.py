@@ -3,7 +3,8 @@
     python -m paper_2112_13896_amd.build
 
 Compiles the HIP kernels and C ABI (csrc/cs_api.hip) and the host pack
-routine (csrc/cs_pack.cpp) with hipcc.  Packed-fp32 instruction generation is
+routine (csrc/cs_pack.cpp) with hipcc, once as the product library and once
+with the product counter compiled in (libcs_count.so, used by tests).  Packed-fp32 instruction generation is
 switched off for all device code.
 """
 from __future__ import annotations
@@ -18,6 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libcs.so")
+COUNT_LIB = os.path.join(HERE, "libcs_count.so")
 ARCH = "gfx950"
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -47,23 +49,42 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
-def build(verbose: bool = False, extra: list | None = None) -> str:
-    """Compile libcs.so (always recompiles).  Returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Wall", "-Wno-unused-command-line-argument", *DEVICE_FLAGS, "-I", INCLUDE, "-I", CSRC,
-           *(extra or []), "-o", tmp, *sources()]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {r.returncode}")
+def _cmd(out: str, extra: list) -> list:
+    return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+            "-Wall", "-Wno-unused-command-line-argument", *DEVICE_FLAGS, "-I", INCLUDE, "-I", CSRC,
+            *extra, "-o", out, *sources()]
+
+
+def build(verbose: bool = False, extra: list | None = None, counting: bool = True) -> str:
+    """Compile libcs.so (always recompiles) and, with `counting`, the counting
+    build libcs_count.so (every multiply-route-sum kernel counts the products
+    it forms; tests only), the two compilations side by side.  Returns the
+    path of libcs.so."""
+    jobs = [(LIB, list(extra or []))]
+    if counting:
+        jobs.append((COUNT_LIB, list(extra or []) + ["-DCS_COUNT_PRODUCTS"]))
+    procs = []
+    for out, ex in jobs:
+        cmd = _cmd(out + ".tmp", ex)
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((out, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
+                                            text=True)))
+    failed = None
     noise = "is not a recognized feature for this target"
-    msgs = [ln for ln in (r.stdout + r.stderr).splitlines() if noise not in ln and ln.strip()]
-    if msgs and verbose:
-        print("\n".join(msgs))
-    os.replace(tmp, LIB)
+    for out, p in procs:
+        text = p.communicate()[0]
+        if p.returncode != 0:
+            sys.stderr.write(text)
+            failed = failed or f"hipcc failed with exit code {p.returncode} ({os.path.basename(out)})"
+            continue
+        msgs = [ln for ln in text.splitlines() if noise not in ln and ln.strip()]
+        if msgs and verbose:
+            print("\n".join(msgs))
+    if failed:
+        raise RuntimeError(failed)
+    for out, _ in procs:
+        os.replace(out + ".tmp", out)
     return LIB
 
 

@@ -1993,3 +1993,30 @@ int cs_conv2d_dense_kwta_chain3(
                             oval2, ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, k3, shift3, oidx3,
                             oval3, ocnt3, ocap3, aug4, c_out4, n4, bias4, y4, stream);
 }
+
+extern "C" int cs_product_count(unsigned long long* count, int reset) {
+#ifdef CS_COUNT_PRODUCTS
+  unsigned long long v = 0;
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpyFromSymbol(&v, HIP_SYMBOL(cs_products_formed), sizeof(v), 0,
+                          hipMemcpyDeviceToHost) != hipSuccess) {
+    (void)hipGetLastError();
+    return CS_ERR_DEVICE;
+  }
+  if (count) *count = v;
+  if (reset) {
+    const unsigned long long zero = 0;
+    if (hipMemcpyToSymbol(HIP_SYMBOL(cs_products_formed), &zero, sizeof(zero), 0,
+                          hipMemcpyHostToDevice) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+      (void)hipGetLastError();
+      return CS_ERR_DEVICE;
+    }
+  }
+  return CS_OK;
+#else
+  if (count) *count = 0;
+  (void)reset;
+  return CS_ERR_UNSUPPORTED;
+#endif
+}

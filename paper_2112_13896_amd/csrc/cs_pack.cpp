@@ -263,6 +263,7 @@ extern "C" const char* cs_status_str(int status) {
     case CS_ERR_COLLISION: return "two kernels of one packed set share a slot";
     case CS_ERR_WORKSPACE: return "workspace missing or too small";
     case CS_ERR_DEVICE: return "HIP device error";
+    case CS_ERR_UNSUPPORTED: return "not available in this build of the library";
     default: return "unknown status";
   }
 }

@@ -132,6 +132,7 @@ template <int GB>
 __device__ __forceinline__ void blk_chunk(const BChunk& ch, int e_lo, int e_hi, int row_add,
                                           const uint2* tab, int tstride, int set0,
                                           unsigned char* accb) {
+  CS_COUNT_PRODUCTS_ADD((e_hi - e_lo) * GB);
   float x[4];
   uint2 te[4][GB];
 #pragma unroll
@@ -645,7 +646,13 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
     stage_first();
     __syncthreads();
   }
-  for (int tile = blockIdx.x; tile < ba.ntiles; tile += gridDim.x) {
+  // workgroups go to the eight XCDs in turn (workgroup b to XCD b mod 8), each
+  // XCD with its own L2: renumber them so the workgroups of one XCD take
+  // neighbouring tiles, whose windows share input rows
+  const int nx = gridDim.x >> 3;
+  const int wg = (gridDim.x & 7) == 0 ? (int)(blockIdx.x & 7) * nx + (int)(blockIdx.x >> 3)
+                                      : (int)blockIdx.x;
+  for (int tile = wg; tile < ba.ntiles; tile += gridDim.x) {
     const int item0 = tile * ba.P;
     const int item = item0 + ps;
     const bool live = item < ba.items;

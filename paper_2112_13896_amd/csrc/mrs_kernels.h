@@ -25,6 +25,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "count_products.h"
+
 namespace cs {
 
 struct ConvGeom {

@@ -175,6 +175,7 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
         for (int q = 0; q < ra.qf; ++q) {                           // uniform
           const int g = lane + 64 * q;
           if (g < G) {                                              // all lanes but in a last partial group
+            CS_COUNT_PRODUCTS_ADD(min(ROWS_BATCH, nb - e));
             uint32_t w[ROWS_BATCH];
 #pragma unroll
             for (int u = 0; u < ROWS_BATCH; ++u)
@@ -205,6 +206,7 @@ __global__ __launch_bounds__(ROWS_BD) void mrs_rows(const uint16_t* __restrict__
               const int el = e + s + S * u;
               en[u] = ent[el < nb ? el : 64];
             }
+            CS_COUNT_PRODUCTS_ADD(min(ROWS_BATCH, (nb - e - s + S - 1) / S));
             uint32_t w[ROWS_BATCH];
 #pragma unroll
             for (int u = 0; u < ROWS_BATCH; ++u)

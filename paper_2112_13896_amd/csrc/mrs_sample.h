@@ -210,6 +210,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
         xb[4 * q + 3] = v4.w;
       }
       E te[SAMPLE_BATCH];
+      CS_COUNT_PRODUCTS_ADD(min(SAMPLE_BATCH, ee - e));
 #pragma unroll
       for (int j = 0; j < SAMPLE_BATCH; ++j)
         te[j] = aug[(int64_t)(e + j < ee ? er[j] : 0) * G + g];    // row 0 past the end
@@ -422,6 +423,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
       for (int j = 0; j < SAMPLE_KEYS; ++j) {
         const int32_t ov = (int32_t)kwta_out<A, TO>(rv[j], sa.shift);
         if (wins[j] && ov != 0) {
+          CS_COUNT_PRODUCTS_ADD(nx.G);
           if (nx.G <= NX_MAXG) {
 #pragma unroll
             for (int g = 0; g < NX_MAXG; ++g) {

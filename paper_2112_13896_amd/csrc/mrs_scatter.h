@@ -223,6 +223,7 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
 #pragma unroll
       for (int kx = 0; kx < KW; ++kx) {
         if (vy && xk[kx] != 0) {
+          CS_COUNT_PRODUCTS_ADD(GPL);
           const uint32_t wk = w[kx];
           const uint32_t ob = rb + (uint32_t)((KW - 1 - kx) * col_b);
           __hip_atomic_fetch_add(reinterpret_cast<int*>(accb + ob + ((wk >> 8) & 0xFFu)),

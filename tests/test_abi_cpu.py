@@ -43,10 +43,23 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for code in range(0, -7, -1):
+    for code in range(0, -8, -1):
         s = _lib.status_str(code)
         assert s and s != "unknown status"
     assert _lib.status_str(5) == "unknown status"
+
+
+def test_counting_build_exports_every_declared_symbol():
+    """The counting build (libcs_count.so) is the same ABI; in the product
+    build the counter is absent and says so without touching a device."""
+    C = _lib._load(_lib.COUNT_LIB_PATH)
+    for nm in declared_functions():
+        assert hasattr(C, nm)
+    v = ctypes.c_ulonglong(7)
+    assert _lib.lib().cs_product_count(ctypes.byref(v), 1) == _lib.CS_ERR_UNSUPPORTED
+    assert v.value == 0
+    with pytest.raises(_lib.CSError):
+        _lib.product_count()
 
 
 @pytest.mark.parametrize("dtype", ["int8", "float32"])
