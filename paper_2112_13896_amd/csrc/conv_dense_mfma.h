@@ -55,8 +55,9 @@ struct DenseArgs {
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 
-// The workgroup body for workgroup index blk, BD (>= 512) threads.
-template <int POOL, typename TO, int BD>
+// The workgroup body for workgroup index blk, BD (>= 512) threads.  KM: the
+// k-WTA selection (da.kmode) fixed at compile time, or 0: chosen at run time.
+template <int POOL, typename TO, int BD, int KM = 0>
 __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
                                            const uint16_t* __restrict__ aug,
                                            const int32_t* __restrict__ bias,
@@ -235,7 +236,7 @@ __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
     uint2* sel = reinterpret_cast<uint2*>(smem + da.off_sel);
     uint16_t* tl_idx = lo.idx ? reinterpret_cast<uint16_t*>(smem + da.off_lidx) : nullptr;
     TO* tl_val = reinterpret_cast<TO*>(smem + da.off_lval);
-    switch (da.kmode) {
+    switch (KM > 0 ? KM : da.kmode) {
       case 1:
         kwta_quad_items<int32_t, TO, 8, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
                                         tl_val, lo.cap, lo.cnt);

@@ -1888,7 +1888,7 @@ int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const
                             ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, stream);
 }
 
-template <int POOL, int KW>
+template <int POOL, int KW, int KM>
 void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const SamplePlan& sp,
                         size_t shmem, hipStream_t s, const void* x, const void* aug0,
                         const void* bias0, void* y0, const cs::ListOut& lo0,
@@ -1896,13 +1896,28 @@ void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const S
                         const cs::ListOut& lo, const cs::ConvGeom& geo, const void* aug2,
                         const void* bias2, void* y2, const cs::ListOut& lo2,
                         const cs::ConvGeom& geo2, const cs::NextLayer& nx) {
-  hipLaunchKernelGGL((cs::dense_scatter_sample<POOL, KW>), dim3((unsigned)geo0.B),
-                     dim3(cs::SCAT_BD), shmem, s, static_cast<const int8_t*>(x),
-                     static_cast<const uint16_t*>(aug0), static_cast<const int32_t*>(bias0),
-                     static_cast<int32_t*>(y0), lo0, geo0, da, static_cast<const uint16_t*>(aug),
-                     static_cast<const int32_t*>(bias), static_cast<int32_t*>(y), lo, geo, scp.sc,
-                     static_cast<const uint16_t*>(aug2), static_cast<const int32_t*>(bias2),
-                     static_cast<int32_t*>(y2), lo2, geo2, sp.sa, nx);
+  const cs::ChainArgs a{static_cast<const int8_t*>(x),
+                        static_cast<const uint16_t*>(aug0),
+                        static_cast<const int32_t*>(bias0),
+                        static_cast<int32_t*>(y0),
+                        lo0,
+                        geo0,
+                        da,
+                        static_cast<const uint16_t*>(aug),
+                        static_cast<const int32_t*>(bias),
+                        static_cast<int32_t*>(y),
+                        lo,
+                        geo,
+                        scp.sc,
+                        static_cast<const uint16_t*>(aug2),
+                        static_cast<const int32_t*>(bias2),
+                        static_cast<int32_t*>(y2),
+                        lo2,
+                        geo2,
+                        sp.sa,
+                        nx};
+  hipLaunchKernelGGL((cs::dense_scatter_sample<POOL, KW, KM>), dim3((unsigned)geo0.B),
+                     dim3(cs::SCAT_BD), shmem, s, a);
 }
 
 int cs_conv2d_dense_kwta_chain3(
@@ -1968,9 +1983,15 @@ int cs_conv2d_dense_kwta_chain3(
       const cs::ListOut lo0{oidx, oval, ocnt, ocap};
       const cs::ListOut lo{oidx2, oval2, ocnt2, ocap2};
       const cs::ListOut lo2{oidx3, oval3, ocnt3, ocap3};
-#define CS_DC(P_, K_)                                                                          \
-  launch_dense_chain<P_, K_>(da, scp, sp, shmem, s, x, aug, bias, y, lo0, geo0, aug2, bias2, y2, \
-                             lo, geo, aug3, bias3, y3, lo2, geo2, nx)
+#define CS_DC3(P_, K_, M_)                                                                     \
+  launch_dense_chain<P_, K_, M_>(da, scp, sp, shmem, s, x, aug, bias, y, lo0, geo0, aug2, bias2, \
+                                 y2, lo, geo, aug3, bias3, y3, lo2, geo2, nx)
+#define CS_DC(P_, K_)                                   \
+  do {                                                  \
+    if (da.kmode == 1) CS_DC3(P_, K_, 1);               \
+    else if (da.kmode == 2) CS_DC3(P_, K_, 2);          \
+    else CS_DC3(P_, K_, 3);                             \
+  } while (0)
       if (pool == 2) {
         if (geo.KW == 3) CS_DC(2, 3);
         else if (geo.KW == 5) CS_DC(2, 5);
@@ -1981,6 +2002,7 @@ int cs_conv2d_dense_kwta_chain3(
         else CS_DC(1, 7);
       }
 #undef CS_DC
+#undef CS_DC3
       return launch_status();
     }
   }

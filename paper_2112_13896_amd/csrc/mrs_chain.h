@@ -25,21 +25,72 @@
 
 namespace cs {
 
-template <int POOL, int KW>
-__global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(
-    const int8_t* __restrict__ x, const uint16_t* __restrict__ aug0,
-    const int32_t* __restrict__ bias0, int32_t* __restrict__ y0, ListOut lo0, ConvGeom geo0,
-    DenseArgs da, const uint16_t* __restrict__ aug, const int32_t* __restrict__ bias,
-    int32_t* __restrict__ y, ListOut lo, ConvGeom geo, ScatterArgs sc,
-    const uint16_t* __restrict__ aug2, const int32_t* __restrict__ bias2,
-    int32_t* __restrict__ y2, ListOut lo2, ConvGeom geo2, SampleArgs sa2, NextLayer nx) {
-  dense_body<POOL, int8_t, SCAT_BD>(x, aug0, bias0, y0, nullptr, lo0, geo0, da, blockIdx.x);
+// The arguments of the three phases, passed as one value.
+struct ChainArgs {
+  const int8_t* x;
+  const uint16_t* aug0;
+  const int32_t* bias0;
+  int32_t* y0;
+  ListOut lo0;
+  ConvGeom geo0;
+  DenseArgs da;
+  const uint16_t* aug;
+  const int32_t* bias;
+  int32_t* y;
+  ListOut lo;
+  ConvGeom geo;
+  ScatterArgs sc;
+  const uint16_t* aug2;
+  const int32_t* bias2;
+  int32_t* y2;
+  ListOut lo2;
+  ConvGeom geo2;
+  SampleArgs sa2;
+  NextLayer nx;
+};
+
+// The kernel's argument segment, as a pointer the compiler cannot see
+// through: the scalar loads of a phase's arguments stay in that phase instead
+// of being hoisted to the kernel's start, where the three phases' arguments
+// would all be live at once (more than the scalar registers left at eight
+// wavefronts per SIMD, so they were spilled).
+__device__ __forceinline__ const ChainArgs* chain_args() {
+  auto p = __builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(p));
+  return (const ChainArgs*)p;
+}
+
+// KM: the first layer's k-WTA selection (its kmode), fixed at compile time.
+template <int POOL, int KW, int KM>
+__global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
+  {
+    const ChainArgs* a = chain_args();
+    const ListOut lo0 = a->lo0;
+    const ConvGeom geo0 = a->geo0;
+    const DenseArgs da = a->da;
+    dense_body<POOL, int8_t, SCAT_BD, KM>(a->x, a->aug0, a->bias0, a->y0, nullptr, lo0, geo0, da,
+                                      blockIdx.x);
+  }
   __syncthreads();
-  scatter_body<int8_t, KW, 2, 1>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt, aug, bias,
-                                 y, nullptr, lo, geo, sc, blockIdx.x);
+  {
+    const ChainArgs* a = chain_args();
+    const ListOut lo0 = a->lo0, lo = a->lo;
+    const ConvGeom geo = a->geo;
+    const ScatterArgs sc = a->sc;
+    scatter_body<int8_t, KW, 2, 1>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt, a->aug,
+                                   a->bias, a->y, nullptr, lo, geo, sc, blockIdx.x);
+  }
   __syncthreads();
-  sample_body<int8_t, int32_t, int8_t>(lo.idx, static_cast<const int8_t*>(lo.val), lo.cnt, aug2,
-                                       bias2, y2, nullptr, lo2, geo2, sa2, nx, blockIdx.x);
+  {
+    const ChainArgs* a = chain_args();
+    const ListOut lo = a->lo, lo2 = a->lo2;
+    const ConvGeom geo2 = a->geo2;
+    const SampleArgs sa2 = a->sa2;
+    const NextLayer nx = a->nx;
+    sample_body<int8_t, int32_t, int8_t>(lo.idx, static_cast<const int8_t*>(lo.val), lo.cnt,
+                                         a->aug2, a->bias2, a->y2, nullptr, lo2, geo2, sa2, nx,
+                                         blockIdx.x);
+  }
 }
 
 }  // namespace cs

@@ -339,7 +339,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
   // this before its adds); the packed rows of the keys that can win (key >=
   // T) are loaded now, their latency hidden behind the scan and the lists
   int32_t* acc2 = reinterpret_cast<int32_t*>(smem + nx.off_acc);
-  uint16_t pw[SAMPLE_KEYS][NX_MAXG];
+  uint32_t pw[SAMPLE_KEYS][NX_MAXG / 2];                // two 16-bit entries per register
   if (nx.aug != nullptr) {
     for (int o = tid; o < nx.c_out; o += SAMPLE_BD) acc2[o] = 0;
     if (nx.G <= NX_MAXG) {
@@ -348,7 +348,9 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
         if (i0 + j < c_out && key[j] >= thr) {
           const uint16_t* r = nx.aug + (int64_t)(i0 + j) * nx.G;
 #pragma unroll
-          for (int g = 0; g < NX_MAXG; ++g) pw[j][g] = g < nx.G ? r[g] : (uint16_t)0;
+          for (int g = 0; g < NX_MAXG; g += 2)
+            pw[j][g / 2] = (g < nx.G ? (uint32_t)r[g] : 0u) |
+                           ((g + 1 < nx.G ? (uint32_t)r[g + 1] : 0u) << 16);
         }
       }
     }
@@ -427,7 +429,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
           if (nx.G <= NX_MAXG) {
 #pragma unroll
             for (int g = 0; g < NX_MAXG; ++g) {
-              const uint32_t w = pw[j][g];
+              const uint32_t w = (pw[j][g / 2] >> (16 * (g & 1))) & 0xFFFFu;
               if (g < nx.G)
                 __hip_atomic_fetch_add(acc2 + g * nx.n + (int)(w >> 8),
                                        ov * (int)(int8_t)(w & 0xFFu), __ATOMIC_RELAXED,
