@@ -107,10 +107,15 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
     pval[u] = lval[lbase + ec];
   }
   // the table copied as it is ([tap][c][set] 16-bit entries), Kernel IDs
-  // turned into byte offsets kid * 4 (kid < 32, so the byte holds it)
+  // turned into byte offsets kid * 4 (kid < 32, so the byte holds it); with
+  // two sets per lane the second set's byte is (n + kid) * 4, its channel's
+  // offset from the first set's channel 0 (n + kid < 64)
   const int gpc = G / GPL;
   {
-    auto kid4 = [](uint32_t w) { return (w & 0x00FF00FFu) | ((w & 0x1F001F00u) << 2); };
+    const uint32_t hi_add = GPL == 2 ? (uint32_t)n << 26 : 0u;
+    auto kid4 = [hi_add](uint32_t w) {
+      return ((w & 0x00FF00FFu) | ((w & 0x1F001F00u) << 2)) + hi_add;
+    };
     const int nw = geo.KH * KW * C * G / 2;                         // words; R*G even (host)
     const int n16 = nw / 4;                                         // 16-byte pieces
     const su32x4* src = reinterpret_cast<const su32x4*>(aug);
@@ -203,8 +208,12 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
     int xk[KW];
 #pragma unroll
     for (int kx = 0; kx < KW; ++kx) xk[kx] = (unsigned)(lx + P - kx) < (unsigned)Wo ? x : 0;
-    // byte offset of (row dy - ky, column lx + P - (KW-1)) plus the set's channels
-    const int colb = (lx + P - (KW - 1)) * col_b + g * n * 4;
+    // byte offsets of the outputs (row dy - wlo, column lx + P - kx) plus the
+    // set's channels, one per tap column; one tap row lower is row_b less
+    uint32_t bk[KW];
+#pragma unroll
+    for (int kx = 0; kx < KW; ++kx)
+      bk[kx] = acc_b + (uint32_t)((dy - wlo) * row_b + (lx + P - kx) * col_b + g * n * 4);
     const unsigned char* tp0 = tabb + (uint32_t)((ch * G + g) * 2);
     // the table words of a tap row are read one row ahead, before the atomics
     // of the current row (LDS operations complete in order, so a read issued
@@ -216,25 +225,28 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
       for (int kx = 0; kx < KW; ++kx) w[kx] = *reinterpret_cast<const TW*>(rp + kx * tap_b);
     };
     // lanes whose output is outside the band or the map are masked off (the
-    // LDS cycles an atomic costs grow with its active lanes)
+    // LDS cycles an atomic costs grow with its active lanes); the entry's
+    // Kernel-ID bytes are the offsets within the output pixel
     auto add_row = [&](const uint32_t (&w)[KW], int ky) {
       const bool vy = ky >= klo && ky <= khi;
-      const uint32_t rb = acc_b + (uint32_t)((dy - ky) * row_b + colb);
 #pragma unroll
       for (int kx = 0; kx < KW; ++kx) {
         if (vy && xk[kx] != 0) {
           CS_COUNT_PRODUCTS_ADD(GPL);
           const uint32_t wk = w[kx];
-          const uint32_t ob = rb + (uint32_t)((KW - 1 - kx) * col_b);
-          __hip_atomic_fetch_add(reinterpret_cast<int*>(accb + ob + ((wk >> 8) & 0xFFu)),
+          __hip_atomic_fetch_add(reinterpret_cast<int*>(accb + bk[kx] + ((wk >> 8) & 0xFFu)),
                                  __mul24(xk[kx], (int)(int8_t)(wk & 0xFFu)), __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_WORKGROUP);
           if constexpr (GPL == 2)
-            __hip_atomic_fetch_add(
-                reinterpret_cast<int*>(accb + ob + (uint32_t)(n * 4) + (wk >> 24)),
-                __mul24(xk[kx], (int)(int8_t)((wk >> 16) & 0xFFu)), __ATOMIC_RELAXED,
-                __HIP_MEMORY_SCOPE_WORKGROUP);
+            __hip_atomic_fetch_add(reinterpret_cast<int*>(accb + bk[kx] + (wk >> 24)),
+                                   __mul24(xk[kx], (int)(int8_t)((wk >> 16) & 0xFFu)),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
+      }
+#pragma unroll
+      for (int kx = 0; kx < KW; ++kx) {
+        bk[kx] -= (uint32_t)row_b;
+        asm volatile("" : "+v"(bk[kx]));   // kept per lane: one add per atomic address
       }
     };
     uint32_t wa[KW], wb[KW];
