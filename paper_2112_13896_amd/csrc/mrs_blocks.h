@@ -9,24 +9,30 @@
 //    adjacent (they read the same list entries);
 //  * table: the augmented tensor (value + Kernel ID per slot, Section 3.3.1)
 //    is staged in blocks of RB slot rows - whole taps, or a channel range of
-//    one tap - as a value array and an array of 16-bit accumulator offsets
-//    (the Kernel ID already turned into the byte offset of its accumulator
-//    row), double-buffered: the next block's loads are in flight while the
-//    current block is used, one barrier per block.  A block's slots are
-//    visited in list order (a list is in ascending channel order), so a lane
-//    keeps its place in a tap's list from one channel block to the next;
+//    one tap - as 8-byte entries {value, accumulator offset} (the Kernel ID
+//    already turned into the byte offset of its accumulator row), so one LDS
+//    read gives a lane its sets' weights and where their products go.  A
+//    table of one block is staged once per workgroup (persistent workgroups
+//    loop over tiles); larger ones are double-buffered when two blocks fit:
+//    the next block's loads are in flight while the current block is used,
+//    one barrier per block.  A block's slots are visited in list order (a
+//    list is in ascending channel order), so a lane keeps its place in a
+//    tap's list from one channel block to the next;
 //  * Route / Sum: the accumulators of a lane are LDS columns acc[j*n + kid]
-//    [lane] (a bank is a function of the lane only).  fp32 has no fast LDS
-//    atomic here, so each product is a read-add-write of the lane's own
-//    column; the four entries of a list chunk are done together (all reads,
-//    then the writes in entry order), and an entry whose Kernel ID equals an
-//    earlier one of the chunk adds onto that entry's new value instead of
-//    the value read - the same sums, in the same order, as one entry after
-//    another, without a round trip per product;
-//  * epilogue: one wavefront per pixel row, each lane holding KPL
-//    consecutive channels; the k-th largest order-preserving key is found bit
-//    by bit (counts of keys >= a candidate by ballot), ties go to the lower
-//    index, and the list positions come from wavefront prefix sums.
+//    [lane] (a bank is a function of the lane only), starting at the bias.
+//    fp32 has no fast LDS atomic here, so each product is a read-add-write of
+//    the lane's own column; the entries of a list chunk go in pairs (both
+//    reads, then the writes in entry order), and the second entry of a pair
+//    whose Kernel ID equals the first's adds onto the first's new value
+//    instead of the value read - the same sums, in the same order, as one
+//    entry after another;
+//  * epilogue, when a pixel's lanes hold all its channels in their own
+//    columns: the k-WTA runs on those columns with no barrier - four lanes
+//    per pixel (a quad) with the gather kernels' sorted top-8/16/32 lists and
+//    bit masks, or a bit-by-bit search of the k-th largest key with group
+//    counts; otherwise the sums are copied to a tile and selected there (four
+//    or sixteen lanes per row).  Ties go to the lower index; the winners are
+//    written as lists (non-zero values, ascending index) or densely.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
