@@ -360,6 +360,64 @@ def ab_reorder(cfg, inp, x, kernel_ms, breakdown) -> dict:
             "routed_us": round(routed * 1e3, 2), "table_entries_per_output": int(table.shape[1])}
 
 
+def ab_units(net, cfg, unit: int) -> list:
+    """k-WTA in units of `unit` channels (Section 5's [64:64] modules) on every
+    fp32 layer that reads lists: the one-kernel layer
+    (cs_mrs_kwta_units_conv2d, lists out) against the same result from
+    separate launches (sums, k-WTA on the unit view, compaction of the masked
+    output into lists).  Warm timings (20-launch graphs)."""
+    import torch
+    from paper_2112_13896_amd import ops
+
+    out = []
+    for li, (p, pl) in enumerate(zip(net.packed, net.plans)):
+        s = p.spec
+        if (net.packed[0].aug.dtype == torch.int16 or not pl.in_lists or s.k is None
+                or s.kind != "conv" or s.c_out % unit or pl.pool != 1):
+            continue
+        ku = -(-s.k * unit // s.c_out)                    # winners per unit, rounded up
+        idx, lval, cnt = net.bufs.lists[li - 1]
+        b, h, w, c = pl.geo
+        bias = p.bias
+        y = torch.empty_like(net.bufs.acc[li])
+        y4 = y.reshape(b, -1, 1, s.c_out) if y.dim() == 2 else y
+        rows = y.numel() // s.c_out
+        dense = torch.empty_like(y)
+        cap = ops.list_capacity(ku * (s.c_out // unit))
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device="cuda"),
+                 torch.empty((rows, cap), dtype=torch.float32, device="cuda"),
+                 torch.empty((rows,), dtype=torch.int32, device="cuda"))
+        clists = (torch.empty((rows, s.c_out), dtype=torch.int16, device="cuda"),
+                  torch.empty((rows, s.c_out), dtype=torch.float32, device="cuda"),
+                  torch.empty((rows,), dtype=torch.int32, device="cuda"))
+
+        def fused():
+            ops.mrs_kwta_units_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n,
+                                      pl.stride, pl.pad, bias, 1, k=ku, unit=unit, y=y4,
+                                      keep_sums=False, lists=lists)
+
+        def sums():
+            ops.mrs_conv2d(idx, lval, cnt, pl.geo, p.aug, pl.kh, pl.kw, s.n, pl.stride, pl.pad,
+                           bias, 1, out=y4)
+
+        def kw():
+            ops.kwta(y.reshape(-1, unit), ku, out=dense.reshape(-1, unit))
+
+        def comp():
+            ops.compact_into(dense.reshape(rows, s.c_out), *clists)
+        fused()
+        sums(); kw(); comp()
+        torch.cuda.synchronize()
+        t = {nm: _time_call(f) * 1e3 for nm, f in
+             (("fused", fused), ("sums", sums), ("kwta", kw), ("compact", comp))}
+        out.append({"layer": s.name, "unit": unit, "k_per_unit": ku,
+                    "one_kernel_us": round(t["fused"], 2),
+                    "separate_us": {"sums": round(t["sums"], 2), "kwta_units": round(t["kwta"], 2),
+                                    "compact": round(t["compact"], 2),
+                                    "total": round(t["sums"] + t["kwta"] + t["compact"], 2)}})
+    return out
+
+
 MALL_MIB = 256.0                    # MI355X Infinity Cache (last-level cache)
 SET_MEM_CAP = 24 << 30              # most device memory the rotating buffer sets may take
 
@@ -373,7 +431,7 @@ def scrub(buf) -> None:
 
 
 def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0,
-            ab: bool = False) -> dict:
+            ab: bool = False, ab_unit: int = 0) -> dict:
     """One workload: the whole chain, K timed passes, per-kernel durations.
 
     Buffer sets (input + every intermediate) rotate; their number is chosen
@@ -512,6 +570,8 @@ def measure(cfg, steps: int, warmup: int, rotate_mib: float, eager_only: int = 0
     if ab:
         rec["ab_reorder"] = ab_reorder(cfg, inp, xs[0], lambda call: _time_call(call),
                                        breakdown)
+    if ab_unit:
+        rec["ab_units"] = ab_units(net, cfg, ab_unit)
     rec["_inp"] = inp
     return rec
 
@@ -549,6 +609,9 @@ def main() -> int:
     ap.add_argument("--ab-reorder", action="store_true",
                     help="also time the first layer by reordering the activations instead of "
                          "routing the products (fp32 dense-input 64-channel layers)")
+    ap.add_argument("--ab-units", type=int, default=0, metavar="UNIT",
+                    help="also time k-WTA in units of UNIT channels on the fp32 layers that "
+                         "read lists: one kernel against sums + unit k-WTA + compaction")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
                     help="only copy a MIB-sized device buffer --steps times (reference kernel "
                          "for scaling the HBM byte counters, and the copy ceiling)")
@@ -590,7 +653,8 @@ def main() -> int:
         print(json.dumps(measure(cfg, args.steps, args.warmup, args.rotate_mib,
                                  eager_only=args.eager_passes)), flush=True)
         return 0
-    head = measure(cfg, args.steps, args.warmup, args.rotate_mib, ab=args.ab_reorder)
+    head = measure(cfg, args.steps, args.warmup, args.rotate_mib, ab=args.ab_reorder,
+                   ab_unit=args.ab_units)
     inp = head.pop("_inp")
     res = {
         "metric": METRIC, "value": head["samples_per_s"], "unit": "samples/s", "n_gpus": 1,
@@ -607,8 +671,9 @@ def main() -> int:
         "roofline": head["roofline"],
         "kernels": head["kernels"],
     }
-    if "ab_reorder" in head:
-        res["ab_reorder"] = head["ab_reorder"]
+    for key in ("ab_reorder", "ab_units"):
+        if key in head:
+            res[key] = head[key]
     others = [int(c) for c in args.also.split(",") if c.strip() and int(c) != args.config]
     if others:
         res["workloads"] = {}

@@ -186,6 +186,34 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
                        void* oval, int32_t* ocnt, int ocap, void* stream);
 
 /*
+ * cs_mrs_kwta_units_conv2d - cs_mrs_kwta_conv2d with the k-WTA applied in
+ * units: every `unit` consecutive channels of an output pixel keep their own
+ * k winners (Section 5: channels partitioned into independent modules, each
+ * with its own k-WTA; the ResNet-50 stages use units of 64 channels).  fp32
+ * only (unit == c_out: exactly cs_mrs_kwta_conv2d, any dtype, ot = the sums'
+ * dtype).  DEVICE memory.  One kernel when the layer runs on the table-block
+ * kernel with the selection on the lanes' own accumulators (no pooling,
+ * power-of-two sets and kernels per set, n <= 16, c_out <= 256, a unit a
+ * power-of-two number of a pixel's lanes); otherwise cs_mrs_conv2d and
+ * cs_kwta on the [rows * c_out / unit][unit] view of y, dense output only.
+ *
+ *  xt .. keep_sums, out  as cs_mrs_kwta_conv2d (xt == CS_F32, output fp32).
+ *  k       winners per unit, 0 <= k <= unit; ties go to the lower channel index.
+ *  unit    channels per unit, dividing c_out.
+ *  oidx, oval, ocnt, ocap  one list per output pixel with the winners of all
+ *          its units in ascending channel order; ocap >= k * c_out / unit.
+ *  Errors: CS_ERR_ARG, CS_ERR_DTYPE (xt != CS_F32 with unit != c_out),
+ *  CS_ERR_SHAPE (unit does not divide c_out, k > unit, ocap too small, or
+ *  lists asked for a layer the single kernel does not take), CS_ERR_DEVICE.
+ */
+int cs_mrs_kwta_units_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval,
+                             const int32_t* cnt, int cap, int b, int h, int w, int c_in, int kh,
+                             int kw, int stride, int pad, const void* aug, int c_out, int n,
+                             const void* bias, int pool, void* y, int keep_sums, int k, int unit,
+                             void* out, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap,
+                             void* stream);
+
+/*
  * cs_mrs_plan - how cs_mrs_conv2d / cs_mrs_kwta_conv2d would run a layer with
  * these sizes (operands assumed aligned as torch allocates them).  Host only;
  * no HIP call.  For tests and tuning.

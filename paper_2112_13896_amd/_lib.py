@@ -38,6 +38,9 @@ SIGNATURES = {
                            _vp, _i, _vp, _vp]),
     "cs_mrs_kwta_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,
                                 _vp, _i, _vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),
+    "cs_mrs_kwta_units_conv2d": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp,
+                                      _i, _i, _vp, _i, _vp, _i, _i, _i, _vp, _vp, _vp, _vp, _i,
+                                      _vp]),
     "cs_mrs_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
                          _c.POINTER(_i64)]),
     "cs_mrs_kwta_chain2": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i,

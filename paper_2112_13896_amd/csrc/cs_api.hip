@@ -518,10 +518,12 @@ int ilog2_exact(int64_t v) {                    // log2 of a power of two, else 
 // the output lists take 8-byte index and 16-byte value stores.
 // cus: compute units of the device (sizes the grid of a one-block table), or
 // 0 when only planning.
+// unit: channels per k-WTA unit (k winners in each), 0 or c_out: the whole row
 bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const void* y,
                  const void* out, int k, int write_sums, int ocap, bool lvec, int cus,
-                 BlocksPlan* pl) {
+                 BlocksPlan* pl, int unit = 0) {
   if (xt != CS_F32 || geo.pool != 1) return false;
+  if (unit <= 0) unit = geo.c_out;
   const int n = geo.n, G = geo.G;
   const int log2n = ilog2_exact(n), log2G = ilog2_exact(G);
   if (log2n < 0 || log2G < 1 || n > 16 || geo.c_out > 256) return false;
@@ -607,11 +609,16 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
   const int kp_own = gb * n;
   pl->own = U <= 16 && kp_own >= 4 && kp_own <= 32 && (kp_own & (kp_own - 1)) == 0 &&
             aligned(y, 16) && aligned(out, 16);
+  // k-WTA units narrower than the row: only on the lanes' own columns, a unit
+  // being a power-of-two number of a pixel's lanes
+  const int log2Us = unit % kp_own == 0 ? ilog2_exact(unit / kp_own) : -1;
+  if (unit != geo.c_out && (!pl->own || log2Us < 0 || log2Us > ilog2_exact(U))) return false;
+  ba.log2Us = pl->own ? (log2Us >= 0 ? log2Us : ilog2_exact(U)) : ilog2_exact(U);
   if (pl->own) {
     // a pixel's four lanes hold its four quarters: the four-lane selection
     // in place (a quad selection record per pixel in LDS), else bit by bit
     const bool quad_own = U == 4 && gb == 2 && tpb > 0 && k >= 0 && k <= 32 &&
-                          geo.c_out == 4 * kp_own;
+                          geo.c_out == 4 * kp_own && unit == geo.c_out;
     ba.kmode = quad_own ? (k <= 8 ? 6 : (k <= 16 ? 7 : 8)) : 5;
     if (quad_own) {
       ba.off_sel = (uint32_t)round16(acc_b + nbuf * tb);
@@ -1334,6 +1341,52 @@ int cs_mrs_kwta_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval, const
                          static_cast<int8_t*>(out), shift, s, lo);
   return kwta_dispatch(static_cast<const int32_t*>(y), rows, c_out, k, static_cast<int32_t*>(out),
                        0, s, lo);
+}
+
+int cs_mrs_kwta_units_conv2d(cs_dtype xt, const uint16_t* idx, const void* lval,
+                             const int32_t* cnt, int cap, int b, int h, int w, int c_in, int kh,
+                             int kw, int stride, int pad, const void* aug, int c_out, int n,
+                             const void* bias, int pool, void* y, int keep_sums, int k, int unit,
+                             void* out, uint16_t* oidx, void* oval, int32_t* ocnt, int ocap,
+                             void* stream) {
+  if (unit == c_out)
+    return cs_mrs_kwta_conv2d(xt, idx, lval, cnt, cap, b, h, w, c_in, kh, kw, stride, pad, aug,
+                              c_out, n, bias, pool, y, keep_sums, k,
+                              xt == CS_I8 ? CS_I32 : CS_F32, 0, out, oidx, oval, ocnt, ocap,
+                              stream);
+  if (xt != CS_F32) return CS_ERR_DTYPE;
+  cs::ConvGeom geo;
+  int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, pool, &geo);
+  if (st != CS_OK) return st;
+  if (cap < 1 || unit < 1 || c_out % unit != 0) return CS_ERR_SHAPE;
+  if (!idx || !lval || !cnt || !aug || !y) return CS_ERR_ARG;
+  if ((keep_sums != 0 && keep_sums != 1) || k < 0) return CS_ERR_ARG;
+  if (k > unit || unit > CS_MAX_KWTA_ROW) return CS_ERR_SHAPE;
+  const bool lists = oidx != nullptr;
+  if (lists == (out != nullptr)) return CS_ERR_ARG;        // exactly one output form
+  if (lists && (!oval || !ocnt || ocap < 1)) return CS_ERR_ARG;
+  const int kall = k * (c_out / unit);                      // winners per output pixel
+  if (lists && ocap < kall) return CS_ERR_SHAPE;
+  geo.cap = cap;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const cs::ListOut lo{oidx, oval, ocnt, lists ? ocap : 0};
+  if (lists_vectorisable(xt, idx, lval, cap)) {
+    BlocksPlan bp;
+    const bool lvec = lists && aligned(oidx, 8) && aligned(oval, 16);
+    int cus = 0;
+    const int dst = device_cus(&cus);
+    if (dst != CS_OK) return dst;
+    if (blocks_plan(geo, xt, aug, y, out, k, keep_sums, lists ? ocap : 0, lvec, cus, &bp, unit))
+      return launch_blocks(bp, s, idx, lval, cnt, aug, bias, y, out, lo, geo);
+  }
+  // two kernels: the sums into y, then k-WTA on the [rows * c_out / unit][unit]
+  // view of y (dense output only)
+  if (lists) return CS_ERR_SHAPE;
+  st = mrs_launch(xt, idx, lval, cnt, geo, aug, bias, y, s);
+  if (st != CS_OK) return st;
+  const int64_t rows = (int64_t)b * (geo.Ho / pool) * (geo.Wo / pool) * (c_out / unit);
+  return kwta_dispatch(static_cast<const float*>(y), rows, unit, k, static_cast<float*>(out), 0, s,
+                       cs::ListOut{nullptr, nullptr, nullptr, 0});
 }
 
 int cs_mrs_plan(cs_dtype xt, int cap, int b, int h, int w, int c_in, int kh, int kw, int stride,

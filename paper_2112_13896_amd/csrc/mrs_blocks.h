@@ -71,6 +71,8 @@ struct BlocksArgs {
                       // 6/7/8 four lanes (a pixel's quad) with top-8/16/32 lists
   int ostride;        // row stride of the sum tile (four lanes per row)
   int kp;             // channels per lane with sixteen lanes per row (4, 8 or 16)
+  int log2Us;         // on the lanes' own columns: lanes per k-WTA unit (k winners
+                      // per unit of KP << log2Us channels; log2U: the whole row)
   uint32_t off_t0, off_t1;   // LDS byte offsets of the table buffers
   uint32_t off_out, off_sel, off_lidx, off_lval;       // epilogue (over the table blocks)
   FastDiv fd_wo, fd_ho, fd_kw, fd_cout, fd_ochunks;
@@ -497,17 +499,22 @@ __device__ __forceinline__ int group_incl_sum(int v, int log2U, int p) {
 // k-WTA over the U lanes of each pixel, the lanes that computed its sums: lane
 // u holds channels u*KP .. u*KP+KP-1 (KP = GB * n) in its own accumulator
 // column, bias included, so no other lane's data is read and no barrier is
-// needed.  The k-th largest key is found bit by bit with group counts,
-// stopping as soon as the keys at or above the prefix are exactly k (their
-// minimum is then the k-th largest); ties go to the lower index; winners are
-// written as lists (non-zero values, ascending index) or densely.
+// needed.  The row is split into units of Us = 1 << log2Us lanes (KP * Us
+// channels; Us = U: the whole row), each keeping its own k winners (the k-WTA
+// in units of Section 5's channel partitioning).  The k-th largest key of a
+// unit is found bit by bit with group counts, stopping as soon as the keys at
+// or above the prefix are exactly k (their minimum is then the k-th largest);
+// ties go to the lower index; the winners of the whole row are written as one
+// list (non-zero values, ascending index) or densely.
 template <typename TO, int KP>
-__device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_t row, bool live,
-                                             int c_out, int k, int write_sums,
-                                             float* __restrict__ y, TO* __restrict__ out,
-                                             const ListOut& lo) {
+__device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int log2Us,
+                                             int64_t row, bool live, int c_out, int k,
+                                             int write_sums, float* __restrict__ y,
+                                             TO* __restrict__ out, const ListOut& lo) {
   const int tid = threadIdx.x;
   const int p = tid & ((1 << log2U) - 1);                // lane position in the group
+  const int ps = p & ((1 << log2Us) - 1);                // lane position in its unit
+  const int c_unit = KP << log2Us;                       // channels per k-WTA unit
   const int o0 = p * KP;                                 // first channel of the lane
   float v[KP];
   uint32_t key[KP];
@@ -525,9 +532,9 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_
   if (k < 0) return;
   uint32_t thr = 0u;
   int need = 0;
-  if (k > 0 && k < c_out) {
+  if (k > 0 && k < c_unit) {
     uint32_t pre = 0u;
-    int cntp = c_out;
+    int cntp = c_unit;
     bool done = !live;
     for (int bit = 31; bit >= 0; --bit) {
       if (__ballot(!done) == 0ull) break;               // every row of the wavefront found
@@ -535,7 +542,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_
       uint32_t c = 0;
 #pragma unroll
       for (int j = 0; j < KP; ++j) c += key[j] >= cand ? 1u : 0u;
-      c = group_reduce(c, log2U, OpAdd{});
+      c = group_reduce(c, log2Us, OpAdd{});
       if (!done) {
         if ((int)c >= k) {
           pre = cand;
@@ -548,18 +555,19 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_
     uint32_t mn = 0xFFFFFFFFu;
 #pragma unroll
     for (int j = 0; j < KP; ++j) mn = (key[j] >= pre && key[j] < mn) ? key[j] : mn;
-    thr = group_reduce(mn, log2U, OpMin{});
+    thr = group_reduce(mn, log2Us, OpMin{});
     uint32_t gt = 0;
 #pragma unroll
     for (int j = 0; j < KP; ++j) gt += key[j] > thr ? 1u : 0u;
-    gt = group_reduce(gt, log2U, OpAdd{});
+    gt = group_reduce(gt, log2Us, OpAdd{});
     need = k - (int)gt;
   }
-  // ties in index order: this lane's first tie has rank (ties of the lanes before)
+  // ties in index order: this lane's first tie has rank (ties of the unit's
+  // lanes before)
   int eq = 0;
 #pragma unroll
-  for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_out && key[j] == thr) ? 1 : 0;
-  int tie_rank = group_incl_sum(eq, log2U, p) - eq;
+  for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_unit && key[j] == thr) ? 1 : 0;
+  int tie_rank = group_incl_sum(eq, log2Us, ps) - eq;
   uint32_t winm = 0;                                    // bit j: channel o0 + j wins
   int wcount = 0;
 #pragma unroll
@@ -567,7 +575,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int64_
     bool w;
     if (!live || k == 0) {
       w = false;
-    } else if (k >= c_out) {
+    } else if (k >= c_unit) {
       w = true;
     } else if (key[j] > thr) {
       w = true;
@@ -762,8 +770,8 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
           }
         }
       } else {
-        blk_kwta_own<TO, KP>(acc, ba.log2U, (int64_t)item, live, c_out, ba.k, ba.write_sums, y,
-                             out, lo);
+        blk_kwta_own<TO, KP>(acc, ba.log2U, ba.log2Us, (int64_t)item, live, c_out, ba.k,
+                             ba.write_sums, y, out, lo);
       }
     } else {
       blk_epilogue_tile<TO, GB>(smem, acc, item0, c_out, y, out, lo, ba);

@@ -194,6 +194,48 @@ def mrs_kwta_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in
     return y, result
 
 
+def mrs_kwta_units_conv2d(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape,
+                          aug, kh: int, kw: int, n: int, stride: int = 1, pad: int = 0,
+                          bias=None, pool: int = 1, *, k: int, unit: int,
+                          y: torch.Tensor | None = None, keep_sums: bool = True,
+                          cap: int | None = None, lists=None, out: torch.Tensor | None = None):
+    """One fp32 layer with k-WTA in units (cs_mrs_kwta_units_conv2d): every
+    `unit` consecutive channels of an output pixel keep their own k winners.
+    Returns (y, result) as mrs_kwta_conv2d."""
+    b, h, w, c_in = in_shape
+    pa, c_out = _aug(aug, lval.dtype, n)
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    acc_dt = torch.int32 if lval.dtype == torch.int8 else torch.float32
+    oshape = (b, max(ho, 0) // pool, max(wo, 0) // pool, c_out)
+    rows = oshape[0] * oshape[1] * oshape[2]
+    if y is None:
+        y = torch.empty(oshape, dtype=acc_dt, device=lval.device)
+    if lists is None and cap is not None:
+        lists = (torch.empty((rows, cap), dtype=torch.int16, device=lval.device),
+                 torch.empty((rows, cap), dtype=acc_dt, device=lval.device),
+                 torch.empty((rows,), dtype=torch.int32, device=lval.device))
+    if lists is not None:
+        oi, ov, oc = lists
+        if oi.dtype != torch.int16 or ov.dtype != acc_dt or oc.dtype != torch.int32:
+            raise TypeError("list buffer dtypes do not match")
+        if oi.shape != ov.shape or oi.dim() != 2 or oi.shape[0] != rows or oc.shape != (rows,):
+            raise ValueError("list buffer shapes do not match the output")
+        args = (None, _dev(oi, "oidx"), _dev(ov, "oval"), _dev(oc, "ocnt"), oi.shape[1])
+        result = lists
+    else:
+        if out is None:
+            out = torch.empty(oshape, dtype=acc_dt, device=lval.device)
+        if out.dtype != acc_dt or out.numel() != rows * c_out:
+            raise ValueError("out does not match the output")
+        args = (_dev(out, "out"), None, None, None, 0)
+        result = out
+    check("cs_mrs_kwta_units_conv2d", lib().cs_mrs_kwta_units_conv2d(
+        _dt(lval), _dev(idx, "idx"), _dev(lval, "lval"), _dev(cnt, "cnt"), idx.shape[-1],
+        b, h, w, c_in, kh, kw, stride, pad, pa, c_out, n, _opt(bias, "bias"), pool,
+        _dev(y, "y"), 1 if keep_sums else 0, k, unit, *args, _stream()))
+    return y, result
+
+
 def mrs_kwta_chain2(idx: torch.Tensor, lval: torch.Tensor, cnt: torch.Tensor, in_shape, aug,
                     kh: int, kw: int, n: int, stride: int = 1, pad: int = 0, bias=None,
                     pool: int = 1, *, k: int, shift: int, aug2, n2: int, bias2=None,

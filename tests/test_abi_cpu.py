@@ -473,6 +473,33 @@ def test_mrs_and_linear_validation(L):
     assert lin(CS_F32, FAKE, 16, 512, None, 64, 8, None, FAKE, FAKE_WS, 1 << 30, None) == CS_ERR_ARG
 
 
+def test_units_validation(L):
+    """cs_mrs_kwta_units_conv2d rejects bad arguments on the host, before any
+    device call."""
+    u = L.cs_mrs_kwta_units_conv2d
+    #      xt      idx   lval  cnt  cap b  h  w  cin kh kw s  p  aug   c_out n  bias pool y
+    base = [CS_F32, FAKE, FAKE, FAKE, 8, 2, 8, 8, 16, 3, 3, 1, 1, FAKE, 64, 8, None, 1, FAKE,
+            1, 4, 16, None, FAKE, FAKE, FAKE, 16, None]
+    #       keep k unit out  oidx oval  ocnt  ocap stream
+
+    def call(**kw):
+        a = list(base)
+        pos = {"xt": 0, "idx": 1, "cap": 4, "c_out": 14, "k": 20, "unit": 21, "out": 22,
+               "oidx": 23, "ocap": 26}
+        for key, v in kw.items():
+            a[pos[key]] = v
+        return u(*a)
+    assert call(unit=24) == CS_ERR_SHAPE                        # does not divide c_out
+    assert call(k=17) == CS_ERR_SHAPE                           # k > unit
+    assert call(ocap=15) == CS_ERR_SHAPE                        # 4 units x 4 winners
+    assert call(xt=CS_I8) == CS_ERR_DTYPE                       # units: fp32 only
+    assert call(idx=None) == CS_ERR_ARG
+    assert call(out=FAKE) == CS_ERR_ARG                         # both output forms
+    assert call(oidx=None) == CS_ERR_ARG                        # neither output form
+    assert call(cap=0) == CS_ERR_SHAPE
+    assert call(unit=0) == CS_ERR_SHAPE
+
+
 def test_kwta_validation(L):
     k = L.cs_kwta
     assert k(CS_I8, FAKE, 4, 64, 8, CS_I8, 0, FAKE, None) == CS_ERR_DTYPE
