@@ -418,6 +418,50 @@ def ab_units(net, cfg, unit: int) -> list:
     return out
 
 
+def ab_stem(batch: int = 32) -> dict:
+    """A ResNet-50 stem with block Complementary Sparsity (Section 5: a pixel's
+    RGB values one block; 7x7, stride 2, pad 3, 64 outputs, n = 4: 75 % of
+    the weights zero) on a dense int8 224x224x3 batch: the sparse-dense block
+    kernel (cs_conv2d_dense_blocks, one dot product and one routed add per
+    tap and set) against the routed path on the compacted input (cs_conv2d).
+    Synthetic seeded data; warm timings (20-launch graphs); the two sums must
+    be equal."""
+    import torch
+    from paper_2112_13896_amd import ops
+    from workloads import block_complementary_weights
+
+    r = np.random.default_rng(2112_13896 + 50)
+    h = w = 224
+    c, kh, n, c_out = 3, 7, 4, 64
+    mask = block_complementary_weights(r, r, c_out, kh * kh * c, n, c) != 0
+    W = np.where(mask, r.integers(1, 128, size=mask.shape) * r.choice([-1, 1], size=mask.shape),
+                 0).astype(np.int8)
+    aug, kidb, _ = ops.pack_blocks(W, n, c)
+    ad, kd = ops.aug_to_device(aug), torch.from_numpy(kidb).cuda()
+    x = torch.from_numpy(r.integers(-127, 128, size=(batch, h, w, c)).astype(np.int8)).cuda()
+    ho = (h + 6 - kh) // 2 + 1
+    y1 = torch.empty((batch, ho, ho, c_out), dtype=torch.int32, device="cuda")
+    y2 = torch.empty_like(y1)
+    rows = batch * h * w
+    ws = torch.empty(ops.workspace_bytes(1, torch.int8, rows, c), dtype=torch.uint8, device="cuda")
+
+    def blocks():
+        ops.conv2d_dense_blocks(x, ad, kd, kh, kh, n, 2, 3, None, out=y1)
+
+    def routed():
+        ops.conv2d(x, ad, kh, kh, n, 2, 3, None, ws=ws, out=y2)
+    blocks()
+    routed()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(y1, y2))
+    tb, tr = _time_call(blocks) * 1e3, _time_call(routed) * 1e3
+    nbytes = x.numel() + y1.numel() * 4 + aug.nbytes + kidb.nbytes
+    return {"layer": "stem 7x7/2, 3 -> 64, n = 4, blocks of 3 (RGB)", "batch": batch,
+            "input": [h, w, c], "equal_sums": same, "dense_blocks_us": round(tb, 2),
+            "routed_us": round(tr, 2), "dense_blocks_hbm_frac": round(
+                nbytes / (tb * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}
+
+
 MALL_MIB = 256.0                    # MI355X Infinity Cache (last-level cache)
 SET_MEM_CAP = 24 << 30              # most device memory the rotating buffer sets may take
 
@@ -612,6 +656,9 @@ def main() -> int:
     ap.add_argument("--ab-units", type=int, default=0, metavar="UNIT",
                     help="also time k-WTA in units of UNIT channels on the fp32 layers that "
                          "read lists: one kernel against sums + unit k-WTA + compaction")
+    ap.add_argument("--ab-stem", action="store_true",
+                    help="also time a block-CS ResNet-50 stem (dense int8 224x224x3, batch 32): "
+                         "the sparse-dense block kernel against the routed path")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
                     help="only copy a MIB-sized device buffer --steps times (reference kernel "
                          "for scaling the HBM byte counters, and the copy ceiling)")
@@ -674,6 +721,8 @@ def main() -> int:
     for key in ("ab_reorder", "ab_units"):
         if key in head:
             res[key] = head[key]
+    if args.ab_stem:
+        res["ab_stem"] = ab_stem()
     others = [int(c) for c in args.also.split(",") if c.strip() and int(c) != args.config]
     if others:
         res["workloads"] = {}

@@ -397,6 +397,32 @@ int cs_conv2d_dense_kwta_chain3(
     const void* bias4, void* y4, void* stream);
 
 /*
+ * cs_conv2d_dense_blocks - the sparse-dense variant with block Complementary
+ * Sparsity (Section 3.1: complementary patterns made of blocks; Section 5: a
+ * stem whose block is one input pixel's RGB values; Section 4: a first layer
+ * on dense input runs sparse-dense).  DEVICE memory, int8 activations and
+ * weights, int32 sums.  A block is one tap's c_in channels: the c_in products
+ * of a (tap, set) pair are summed first (one 4-way int8 dot product) and the
+ * sum is routed once by the block's Kernel ID, so an output pixel costs
+ * kh*kw*(c_out/n) dot products and routed adds.  No compaction, no workspace.
+ *
+ *  x       device NHWC [b][h][w][c_in] int8, dense; 1 <= c_in <= 4.
+ *  aug     device [kh*kw*c_in][c_out/n] uint16 (cs_pack_blocks with b = c_in:
+ *          value in the low byte).
+ *  kidb    device [kh*kw][c_out/n] uint8: each block's Kernel ID (< n), as
+ *          cs_pack_blocks writes it.
+ *  bias    device int32 [c_out] or NULL.
+ *  y       device NHWC [b][ho][wo][c_out] int32 out: the sums plus bias.
+ *  Errors: CS_ERR_ARG, CS_ERR_SHAPE (c_in > 4, c_out/n sets too many for one
+ *  workgroup, the input under one tile - kh rows of (P-1)*stride + kw
+ *  pixels, P = 256 / lanes per pixel output pixels - over 1024 pixels, or
+ *  the tile's LDS over 64 KB), CS_ERR_DEVICE.
+ */
+int cs_conv2d_dense_blocks(const int8_t* x, int b, int h, int w, int c_in, int kh, int kw,
+                           int stride, int pad, const uint16_t* aug, const uint8_t* kidb,
+                           int c_out, int n, const int32_t* bias, int32_t* y, void* stream);
+
+/*
  * cs_conv2d_dense - the sparse-dense variant (Section 3.1: Combine, Multiply,
  * Route, Sum with dense activations; Section 4 runs the first layer of the
  * keyword-spotting network this way because its input is dense).  DEVICE

@@ -71,6 +71,8 @@ SIGNATURES = {
                        _sz, _vp]),
     "cs_conv2d_noalloc": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                                _vp, _vp]),
+    "cs_conv2d_dense_blocks": (_i, [_vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _i, _i, _vp,
+                                    _vp, _vp]),
     "cs_conv2d_dense": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _i,
                              _vp, _vp]),
     "cs_kwta": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp]),

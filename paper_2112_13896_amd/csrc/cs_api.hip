@@ -11,6 +11,7 @@
 #include <mutex>
 
 #include "compact_kernels.h"
+#include "conv_dense_blocks.h"
 #include "conv_dense_mfma.h"
 #include "cs.h"
 #include "kwta_kernels.h"
@@ -1507,6 +1508,77 @@ int cs_conv2d_noalloc(cs_dtype xt, const void* x, int b, int h, int w, int c_in,
   int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
   if (r != CS_OK) return r;
   return mrs_launch(xt, idx, lv, cnt, geo, aug, bias, y, s);
+}
+
+int cs_conv2d_dense_blocks(const int8_t* x, int b, int h, int w, int c_in, int kh, int kw,
+                           int stride, int pad, const uint16_t* aug, const uint8_t* kidb,
+                           int c_out, int n, const int32_t* bias, int32_t* y, void* stream) {
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, n, 1, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !aug || !kidb || !y) return CS_ERR_ARG;
+  if (c_in > 4) return CS_ERR_SHAPE;                       // a block is one v_dot4
+  const int G = c_out / n;
+  const int GB = G % 2 == 0 ? 2 : 1;
+  const int U = G / GB;
+  if (U > cs::DB_BD) return CS_ERR_SHAPE;
+  const int P = cs::DB_BD / U;
+  const int64_t items64 = (int64_t)b * geo.Ho * geo.Wo;
+  if (items64 * c_out >= ((int64_t)1 << 40) || items64 >= INT32_MAX ||
+      (int64_t)b * h >= INT32_MAX)
+    return CS_ERR_SHAPE;
+  cs::DenseBlocksArgs da;
+  da.GB = GB;
+  da.U = U;
+  da.P = P;
+  da.nseg = (geo.Wo + P - 1) / P;
+  const int64_t ntiles = (int64_t)b * geo.Ho * da.nseg;
+  if (ntiles >= INT32_MAX) return CS_ERR_SHAPE;
+  da.ntiles = (int)ntiles;
+  da.SW = (P - 1) * stride + kw;
+  if ((int64_t)kh * da.SW > (int64_t)cs::DB_PRE * cs::DB_BD) return CS_ERR_SHAPE;
+  const size_t acc_b = (size_t)GB * n * cs::DB_BD * 4;
+  const size_t xs_b = round16((size_t)kh * da.SW * 4);
+  const bool pk = c_in <= 3;                                // one-word table entries
+  const size_t tab_b = (size_t)kh * kw * G * (pk ? 4 : 8);
+  da.off_x = (uint32_t)acc_b;
+  da.off_t = (uint32_t)(acc_b + xs_b);
+  const size_t shmem = acc_b + xs_b + tab_b;
+  if (shmem > kBlockLds) return CS_ERR_SHAPE;
+  da.fd_nseg = cs::make_fastdiv((uint32_t)da.nseg);
+  da.fd_ho = cs::make_fastdiv((uint32_t)geo.Ho);
+  da.fd_sw = cs::make_fastdiv((uint32_t)da.SW);
+  // persistent: as many workgroups as fit at once (LDS and 32 wavefronts per CU)
+  int cus = 0;
+  const int dst = device_cus(&cus);
+  if (dst != CS_OK) return dst;
+  int64_t per_cu = (int64_t)(kCuLds / shmem);
+  if (per_cu > 8) per_cu = 8;
+  if (per_cu < 1) per_cu = 1;
+  const int64_t nb = ntiles < per_cu * cus ? ntiles : per_cu * cus;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+#define CS_DB3(KW_, GB_, PK_)                                                               \
+  hipLaunchKernelGGL((cs::conv_dense_blocks<KW_, GB_, PK_>), dim3((unsigned)nb),             \
+                     dim3(cs::DB_BD), shmem, s, x, aug, kidb, bias, y, geo, da)
+#define CS_DB(KW_, GB_)         \
+  do {                          \
+    if (pk) CS_DB3(KW_, GB_, true); \
+    else CS_DB3(KW_, GB_, false);   \
+  } while (0)
+  if (GB == 2) {
+    if (kw == 7) CS_DB(7, 2);
+    else if (kw == 5) CS_DB(5, 2);
+    else if (kw == 3) CS_DB(3, 2);
+    else CS_DB(0, 2);
+  } else {
+    if (kw == 7) CS_DB(7, 1);
+    else if (kw == 5) CS_DB(5, 1);
+    else if (kw == 3) CS_DB(3, 1);
+    else CS_DB(0, 1);
+  }
+#undef CS_DB
+#undef CS_DB3
+  return launch_status();
 }
 
 int cs_conv2d_dense(cs_dtype xt, const void* x, int b, int h, int w, int c_in, int kh, int kw,

@@ -465,6 +465,29 @@ def conv2d(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
     return out
 
 
+def conv2d_dense_blocks(x: torch.Tensor, aug: torch.Tensor, kidb: torch.Tensor, kh: int,
+                        kw: int, n: int, stride: int = 1, pad: int = 0,
+                        bias: torch.Tensor | None = None,
+                        out: torch.Tensor | None = None) -> torch.Tensor:
+    """Sparse-dense int8 conv with block CS, a block being one pixel's c_in <= 4
+    channels (cs_conv2d_dense_blocks); aug and kidb as ops.pack_blocks gives
+    them with b = c_in (on the device)."""
+    if x.dim() != 4 or x.dtype != torch.int8:
+        raise ValueError("x must be int8 NHWC")
+    b, h, w, c_in = x.shape
+    pa, c_out = _aug(aug, x.dtype, n)
+    if kidb.dtype != torch.uint8 or tuple(kidb.shape) != (kh * kw, c_out // n):
+        raise ValueError("kidb must be uint8 [kh*kw][c_out/n]")
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    if out is None:
+        out = torch.empty((b, max(ho, 0), max(wo, 0), c_out), dtype=torch.int32,
+                          device=x.device)
+    check("cs_conv2d_dense_blocks", lib().cs_conv2d_dense_blocks(
+        _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, pa, _dev(kidb, "kidb"), c_out, n,
+        _opt(bias, "bias"), _dev(out, "out"), _stream()))
+    return out
+
+
 def conv2d_dense(x: torch.Tensor, aug: torch.Tensor, kh: int, kw: int, n: int,
                  stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None, pool: int = 1,
                  out: torch.Tensor | None = None) -> torch.Tensor:

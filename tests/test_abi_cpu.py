@@ -500,6 +500,27 @@ def test_units_validation(L):
     assert call(unit=0) == CS_ERR_SHAPE
 
 
+def test_dense_blocks_validation(L):
+    """cs_conv2d_dense_blocks rejects bad arguments on the host."""
+    f = L.cs_conv2d_dense_blocks
+    #       x     b  h   w   c  kh kw s  p  aug   kidb  c_out n bias y     stream
+    base = [FAKE, 2, 32, 32, 3, 7, 7, 2, 3, FAKE, FAKE, 64, 4, None, FAKE, None]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+    assert call(4, 5) == CS_ERR_SHAPE                           # a block is at most 4 channels
+    assert call(12, 3) == CS_ERR_SHAPE                          # n does not divide c_out
+    assert call(0, None) == CS_ERR_ARG
+    assert call(10, None) == CS_ERR_ARG                         # no block Kernel IDs
+    assert call(14, None) == CS_ERR_ARG
+    assert call(2, 0) == CS_ERR_ARG
+    assert call(5, 40) == CS_ERR_SHAPE                          # window larger than the map
+    # a 31 x 31 window with 32 sets: its table does not fit a workgroup's LDS
+    assert f(FAKE, 2, 64, 64, 3, 31, 31, 1, 3, FAKE, FAKE, 64, 2, None, FAKE, None) == CS_ERR_SHAPE
+
+
 def test_kwta_validation(L):
     k = L.cs_kwta
     assert k(CS_I8, FAKE, 4, 64, 8, CS_I8, 0, FAKE, None) == CS_ERR_DTYPE
