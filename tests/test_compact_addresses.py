@@ -118,6 +118,8 @@ def model(x, E, cus=256):
     (11, 16, np.int8, 16),        # one vector per row (a full row), 64 rows per wavefront
     (3, 4, np.float32, 2),        # one vector per row
     (9, 96, np.float32, 30),      # 24 vectors: one row per wavefront
+    (3, 65532, np.float32, 2000), # the widest fp32 row that is whole vectors: 16383 of them
+    (2, 4096, np.int8, 300),      # 256 vectors of 16 int8
 ])
 def test_compact_vec_model(rows, c, dtype, nnz):
     r = np.random.default_rng(rows * 1000 + c)

@@ -56,6 +56,24 @@ def test_compact(dtype, c):
             assert np.array_equal(val_h[ri, :n], vv)
 
 
+@pytest.mark.parametrize("dtype", ["i8", "f32"])
+@pytest.mark.parametrize("c", [4096, 65532, 65535])
+def test_compact_widest_rows(dtype, c):
+    """Rows up to the widest the 16-bit list indices allow (CS_MAX_ROW): the
+    vector path (width a multiple of the vector) and the chunked one."""
+    r = rng(c + 3)
+    for rows, dens in [(1, 0.3), (3, 0.02), (9, 0.9)]:
+        x = random_rows(r, rows, c, dens, dtype)
+        idx, val, cnt = ops.compact(dev(x))
+        idx_h = host(idx).view(np.uint16)
+        val_h, cnt_h = host(val), host(cnt)
+        for ri, (ii, vv) in enumerate(o.compact_rows(x)):
+            n = cnt_h[ri]
+            assert n == len(ii), (ri, n, len(ii))
+            assert np.array_equal(idx_h[ri, :n], ii)
+            assert np.array_equal(val_h[ri, :n], vv)
+
+
 def test_compact_empty():
     x = torch.zeros((0, 64), dtype=torch.int8, device="cuda")
     idx, val, cnt = ops.compact(x)
