@@ -462,6 +462,51 @@ def ab_stem(batch: int = 32) -> dict:
                 nbytes / (tb * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}
 
 
+def ab_channels(batch: int = 32) -> dict:
+    """Complementary Sparsity overlaid in the channel dimension (Section 3.1)
+    on a ResNet-50 stage-1-shaped layer (56x56, 3x3 pad 1, 48 -> 64 channels,
+    n = 3: every filter's three-channel groups overlaid, 1/3 of its weights
+    non-zero; dense input): the int8 kernel (cs_conv2d_channels) against the
+    fp32 reordering kernel the overlay ran on before (cs_conv2d_reorder_kwta,
+    every output winning so that both give the sums).  Synthetic seeded data;
+    warm timings (20-launch graphs)."""
+    import torch
+    from paper_2112_13896_amd import ops
+    from workloads import channel_complementary_weights
+
+    r = np.random.default_rng(2112_13896 + 60)
+    h = w = 56
+    c, kh, n, c_out = 48, 3, 3, 64
+    Wf = channel_complementary_weights(r, r, c_out, kh, kh, c, n)
+    mask = Wf != 0
+    W8 = np.where(mask, r.integers(1, 128, size=mask.shape) * r.choice([-1, 1], size=mask.shape),
+                  0).astype(np.int8)
+    p8, _ = ops.pack_channels(W8, n)
+    t8 = torch.from_numpy(ops.channel_table(p8, kh, kh, c, c_out, n, 1)).cuda()
+    pf, _ = ops.pack_channels(Wf, n)
+    tf = torch.from_numpy(ops.reorder_table_channels(pf, kh, kh, c, c_out, n)).cuda()
+    x8 = torch.from_numpy(r.integers(-127, 128, size=(batch, h, w, c)).astype(np.int8)).cuda()
+    xf = torch.from_numpy(np.abs(r.normal(size=(batch, h, w, c))).astype(np.float32)).cuda()
+    y8 = torch.empty((batch, h, w, c_out), dtype=torch.int32, device="cuda")
+    yf = torch.empty((batch, h, w, c_out), dtype=torch.float32, device="cuda")
+    of = torch.empty_like(yf)
+
+    def i8():
+        ops.conv2d_channels(x8, t8, kh, kh, c_out, n, 1, 1, None, out=y8)
+
+    def f32():
+        ops.conv2d_reorder_kwta(xf, tf, kh, kh, 1, None, k=c_out, y=yf, keep_sums=False, out=of)
+    i8()
+    f32()
+    torch.cuda.synchronize()
+    t8us, tfus = _time_call(i8) * 1e3, _time_call(f32) * 1e3
+    nbytes = x8.numel() + y8.numel() * 4 + t8.numel() * 4
+    return {"layer": "3x3 pad 1, 48 -> 64, n = 3 channel overlay, 56x56", "batch": batch,
+            "int8_channels_us": round(t8us, 2), "fp32_reorder_us": round(tfus, 2),
+            "int8_hbm_frac": round(nbytes / (t8us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "slots_per_filter": int(kh * kh * c // n)}
+
+
 MALL_MIB = 256.0                    # MI355X Infinity Cache (last-level cache)
 SET_MEM_CAP = 24 << 30              # most device memory the rotating buffer sets may take
 
@@ -659,6 +704,9 @@ def main() -> int:
     ap.add_argument("--ab-stem", action="store_true",
                     help="also time a block-CS ResNet-50 stem (dense int8 224x224x3, batch 32): "
                          "the sparse-dense block kernel against the routed path")
+    ap.add_argument("--ab-channels", action="store_true",
+                    help="also time a channel-overlaid layer (56x56, 3x3, 48 -> 64, n = 3, batch "
+                         "32): the int8 channel kernel against the fp32 reordering kernel")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
                     help="only copy a MIB-sized device buffer --steps times (reference kernel "
                          "for scaling the HBM byte counters, and the copy ceiling)")
@@ -723,6 +771,8 @@ def main() -> int:
             res[key] = head[key]
     if args.ab_stem:
         res["ab_stem"] = ab_stem()
+    if args.ab_channels:
+        res["ab_channels"] = ab_channels()
     others = [int(c) for c in args.also.split(",") if c.strip() and int(c) != args.config]
     if others:
         res["workloads"] = {}

@@ -515,9 +515,11 @@ int cs_pack_blocks(cs_dtype wt, const void* w, int d_out, int r, int n, int b, v
  * slice whose slots keep the weight and the channel ID (which slice, 0..n-1).
  * Offline, HOST memory only, no HIP call.
  *
- *  wt      CS_F32.  w host [c_out][kh][kw][c_in] dense filters (0 = absent).
+ *  wt      CS_F32 or CS_I8.  w host [c_out][kh][kw][c_in] dense filters (0 =
+ *          absent).
  *  n       channels per group, 1 <= n <= CS_MAX_N, dividing c_in.
- *  packed  host [c_out][c_in/n][kh][kw] cs_aug_f32 out (kid = channel ID):
+ *  packed  host [c_out][c_in/n][kh][kw] out, cs_aug_f32 (CS_F32) or uint16
+ *          (CS_I8: value byte | channel ID << 8) entries, kid = channel ID:
  *          value = w[o][y][x][q*n + cid] for the one channel of group q that
  *          is non-zero at (y, x); holes hold 0, 0.
  *  holes   out (may be NULL): packed slots no channel uses.
@@ -528,6 +530,50 @@ int cs_pack_blocks(cs_dtype wt, const void* w, int d_out, int r, int n, int b, v
  */
 int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, int kw, int c_in, int n,
                      void* packed, int64_t* holes, int* bad_o, int* bad_i);
+
+/*
+ * cs_channel_table - the table cs_conv2d_channels reads for an int8
+ * channel-overlaid layer (cs_pack_channels, CS_I8) run with stride `stride`.
+ * Offline, HOST memory only, no HIP call.  Filter o's row holds, with S =
+ * (c_in/n)*kh*kw packed slots and S4 = ceil(S/4): first 4*S4 offsets, slot
+ * i = (q*kh + y)*kw + x at [i] (padding slots 0): off = (y*sw + x)*cp + q*n +
+ * cid, the byte offset of the slot's input (tap (y, x), channel q*n + cid)
+ * from the first input pixel of an output pixel's window in the kernel's
+ * staged tile (sw = 63*stride + kw pixels per staged row, cp = c_in bytes per
+ * pixel when c_in/4 is odd, else c_in + 4); then S4 words, word j holding the
+ * weights of slots 4j .. 4j+3 in its bytes (0 for padding slots).
+ *
+ *  packed  host [c_out][c_in/n][kh][kw] uint16 (cs_pack_channels, CS_I8).
+ *  table   host int32 [c_out][5 * S4] out.
+ *  Errors: CS_ERR_ARG (null pointers, sizes < 1, a channel ID >= n),
+ *  CS_ERR_SHAPE (n does not divide c_in, c_in not a multiple of 4, n >
+ *  CS_MAX_N, the staged tile reaching 2^23 bytes).
+ */
+int cs_channel_table(const uint16_t* packed, int kh, int kw, int c_in, int c_out, int n,
+                     int stride, int32_t* table);
+
+/*
+ * cs_conv2d_channels - an int8 dense-input conv layer with Complementary
+ * Sparsity overlaid in the channel dimension (Section 3.1): every output is
+ * the dot product of its filter's packed slots with the input gathered at
+ * each slot's channel (q*n + channel ID) - no routing, the products of a
+ * filter all go to its own output.  DEVICE memory (except the scalars).
+ * Output tiles of 64 pixels of one output row, one pixel per lane, the
+ * filters split over the four wavefronts of a workgroup; the tile's input
+ * rows staged in LDS with the pixel stride of cs_channel_table.
+ *
+ *  x       device NHWC [b][h][w][c_in] int8, dense, 4-byte aligned; c_in a
+ *          multiple of 4.
+ *  table   device copy of cs_channel_table's table for this stride.
+ *  c_out   16, 32, 64 or 128; n as packed.
+ *  bias    device int32 [c_out] or NULL.
+ *  y       device NHWC [b][ho][wo][c_out] int32 out (16-byte aligned): sums + bias.
+ *  Errors: CS_ERR_ARG, CS_ERR_SHAPE (c_out, c_in or n unsupported, the staged
+ *  tile over 64 KB of LDS), CS_ERR_DEVICE.
+ */
+int cs_conv2d_channels(const int8_t* x, int b, int h, int w, int c_in, int kh, int kw, int stride,
+                       int pad, const int32_t* table, int c_out, int n, const int32_t* bias,
+                       int32_t* y, void* stream);
 
 /*
  * cs_reorder_table_channels - cs_reorder_table for a channel-overlaid layer

@@ -63,6 +63,8 @@ SIGNATURES = {
                             _c.POINTER(_i)]),
     "cs_pack_channels": (_i, [_i, _vp, _i, _i, _i, _i, _i, _vp, _c.POINTER(_i64), _c.POINTER(_i),
                               _c.POINTER(_i)]),
+    "cs_channel_table": (_i, [_vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "cs_conv2d_channels": (_i, [_vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _vp, _vp]),
     "cs_reorder_table_channels": (_i, [_vp, _i, _i, _i, _i, _i, _c.POINTER(_i), _vp]),
     "cs_conv2d_reorder_kwta": (_i, [_i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _i, _vp, _vp,
                                     _i, _i, _i, _vp, _vp, _vp, _vp, _i, _vp]),

@@ -11,6 +11,7 @@
 #include <mutex>
 
 #include "compact_kernels.h"
+#include "conv_channels.h"
 #include "conv_dense_blocks.h"
 #include "conv_dense_mfma.h"
 #include "cs.h"
@@ -1508,6 +1509,46 @@ int cs_conv2d_noalloc(cs_dtype xt, const void* x, int b, int h, int w, int c_in,
   int r = compact_checked(xt, x, rows, c_in, idx, lv, cnt, s);
   if (r != CS_OK) return r;
   return mrs_launch(xt, idx, lv, cnt, geo, aug, bias, y, s);
+}
+
+int cs_conv2d_channels(const int8_t* x, int b, int h, int w, int c_in, int kh, int kw, int stride,
+                       int pad, const int32_t* table, int c_out, int n, const int32_t* bias,
+                       int32_t* y, void* stream) {
+  cs::ConvGeom geo;
+  const int st = conv_geometry(b, h, w, c_in, kh, kw, stride, pad, c_out, 1, 1, &geo);
+  if (st != CS_OK) return st;
+  if (!x || !table || !y || n < 1) return CS_ERR_ARG;
+  if (n > CS_MAX_N || c_in % n != 0 || c_in % 4 != 0) return CS_ERR_SHAPE;
+  if (c_out != 16 && c_out != 32 && c_out != 64 && c_out != 128) return CS_ERR_SHAPE;
+  if (!aligned(x, 4) || !aligned(y, 16)) return CS_ERR_ARG;
+  cs::ChannelArgs ca;
+  ca.S4 = ((c_in / n) * kh * kw + 3) / 4;
+  ca.SW = 63 * stride + kw;
+  ca.CP = (c_in / 4) % 2 == 1 ? c_in : c_in + 4;
+  const size_t shmem = round16((size_t)kh * ca.SW * ca.CP);
+  if (shmem > kBlockLds) return CS_ERR_SHAPE;
+  ca.nseg = (geo.Wo + cs::CH_P - 1) / cs::CH_P;
+  const int64_t ntiles = (int64_t)b * geo.Ho * ca.nseg;
+  if (ntiles >= INT32_MAX || (int64_t)b * h * w * c_in >= ((int64_t)1 << 40)) return CS_ERR_SHAPE;
+  ca.ntiles = (int)ntiles;
+  ca.fd_nseg = cs::make_fastdiv((uint32_t)ca.nseg);
+  ca.fd_ho = cs::make_fastdiv((uint32_t)geo.Ho);
+  int cus = 0;
+  const int dst = device_cus(&cus);
+  if (dst != CS_OK) return dst;
+  int64_t per_cu = (int64_t)(kCuLds / shmem);
+  if (per_cu > 8) per_cu = 8;
+  const int64_t nb = ntiles < per_cu * cus ? ntiles : per_cu * cus;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+#define CS_CH(FW_)                                                                        \
+  hipLaunchKernelGGL((cs::conv_channels_i8<FW_>), dim3((unsigned)nb), dim3(cs::CH_BD), shmem, s, \
+                     x, table, bias, y, geo, ca)
+  if (c_out == 16) CS_CH(4);
+  else if (c_out == 32) CS_CH(8);
+  else if (c_out == 64) CS_CH(16);
+  else CS_CH(32);
+#undef CS_CH
+  return launch_status();
 }
 
 int cs_conv2d_dense_blocks(const int8_t* x, int b, int h, int w, int c_in, int kh, int kw,

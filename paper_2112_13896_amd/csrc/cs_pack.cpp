@@ -177,20 +177,20 @@ extern "C" int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, i
   if (bad_i) *bad_i = -1;
   if (holes) *holes = 0;
   if (!w || !packed || c_out < 1 || kh < 1 || kw < 1 || c_in < 1 || n < 1) return CS_ERR_ARG;
-  if (wt != CS_F32) return CS_ERR_DTYPE;
+  if (wt != CS_F32 && wt != CS_I8) return CS_ERR_DTYPE;
   if (n > CS_MAX_N || c_in % n != 0) return CS_ERR_SHAPE;
-  const float* W = static_cast<const float*>(w);
-  cs_aug_f32* P = static_cast<cs_aug_f32*>(packed);
   const int Q = c_in / n;
   int64_t nh = 0;
   for (int o = 0; o < c_out; ++o)
     for (int q = 0; q < Q; ++q)
       for (int y = 0; y < kh; ++y)
         for (int x = 0; x < kw; ++x) {
-          const float* wp = W + (((int64_t)o * kh + y) * kw + x) * c_in + q * n;
+          const int64_t wi = (((int64_t)o * kh + y) * kw + x) * c_in + q * n;
           int owner = -1;
           for (int j = 0; j < n; ++j) {
-            if (wp[j] != 0.f) {
+            const bool nz = wt == CS_F32 ? static_cast<const float*>(w)[wi + j] != 0.f
+                                         : static_cast<const int8_t*>(w)[wi + j] != 0;
+            if (nz) {
               if (owner >= 0) {
                 if (bad_o) *bad_o = o;
                 if (bad_i) *bad_i = (q * kh + y) * kw + x;
@@ -199,12 +199,45 @@ extern "C" int cs_pack_channels(cs_dtype wt, const void* w, int c_out, int kh, i
               owner = j;
             }
           }
-          cs_aug_f32& e = P[(((int64_t)o * Q + q) * kh + y) * kw + x];
-          e.value = owner >= 0 ? wp[owner] : 0.f;
-          e.kid = owner >= 0 ? (uint32_t)owner : 0u;
+          const int64_t pi = (((int64_t)o * Q + q) * kh + y) * kw + x;
+          if (wt == CS_F32) {
+            cs_aug_f32& e = static_cast<cs_aug_f32*>(packed)[pi];
+            e.value = owner >= 0 ? static_cast<const float*>(w)[wi + owner] : 0.f;
+            e.kid = owner >= 0 ? (uint32_t)owner : 0u;
+          } else {
+            const uint8_t v = owner >= 0 ? (uint8_t)static_cast<const int8_t*>(w)[wi + owner] : 0;
+            static_cast<uint16_t*>(packed)[pi] =
+                (uint16_t)(v | (owner >= 0 ? (uint32_t)owner << 8 : 0u));
+          }
           nh += owner < 0 ? 1 : 0;
         }
   if (holes) *holes = nh;
+  return CS_OK;
+}
+
+extern "C" int cs_channel_table(const uint16_t* packed, int kh, int kw, int c_in, int c_out, int n,
+                                int stride, int32_t* table) {
+  if (!packed || !table || kh < 1 || kw < 1 || c_in < 1 || c_out < 1 || n < 1 || stride < 1)
+    return CS_ERR_ARG;
+  if (n > CS_MAX_N || c_in % n != 0 || c_in % 4 != 0) return CS_ERR_SHAPE;
+  const int Q = c_in / n, S = Q * kh * kw, S4 = (S + 3) / 4;
+  const int64_t sw = (int64_t)63 * stride + kw;            // staged pixels per row
+  const int64_t cp = (c_in / 4) % 2 == 1 ? c_in : c_in + 4; // staged bytes per pixel
+  if ((int64_t)kh * sw * cp >= ((int64_t)1 << 23)) return CS_ERR_SHAPE;
+  for (int o = 0; o < c_out; ++o) {
+    int32_t* row = table + (int64_t)o * 5 * S4;             // offsets [4*S4], weights [S4]
+    for (int i = 0; i < 5 * S4; ++i) row[i] = 0;            // padding slots: offset 0, weight 0
+    for (int q = 0; q < Q; ++q)
+      for (int y = 0; y < kh; ++y)
+        for (int x = 0; x < kw; ++x) {
+          const int si = (q * kh + y) * kw + x;
+          const uint16_t e = packed[(int64_t)o * S + si];
+          const int cid = e >> 8;
+          if (cid >= n) return CS_ERR_ARG;
+          row[si] = (int32_t)((y * sw + x) * cp + q * n + cid);
+          row[4 * S4 + si / 4] |= (int32_t)((uint32_t)(e & 0xFFu) << (8 * (si % 4)));
+        }
+  }
   return CS_OK;
 }
 

@@ -599,24 +599,59 @@ def pack_blocks(W: np.ndarray, n: int, b: int):
 
 def pack_channels(W4: np.ndarray, n: int):
     """Combine along the channel dimension on the host (cs_pack_channels):
-    W4 fp32 [c_out][kh][kw][c_in] -> (packed uint32 [c_out][c_in/n][kh][kw][2]
-    holding (value bits, channel ID), holes).  Raises CSError
+    W4 [c_out][kh][kw][c_in] fp32 -> (packed uint32 [c_out][c_in/n][kh][kw][2]
+    holding (value bits, channel ID), holes); int8 -> packed uint16
+    [c_out][c_in/n][kh][kw] (value byte | channel ID << 8).  Raises CSError
     (CS_ERR_COLLISION) with .bad = (o, slot) on a collision."""
-    W4 = np.ascontiguousarray(W4, dtype=np.float32)
+    i8 = np.asarray(W4).dtype == np.int8
+    W4 = np.ascontiguousarray(W4, dtype=np.int8 if i8 else np.float32)
     if W4.ndim != 4:
         raise ValueError("W4 must be [c_out][kh][kw][c_in]")
     c_out, kh, kw, c_in = W4.shape
     q = c_in // n if n > 0 else 0
-    packed = np.zeros((c_out, max(q, 1), kh, kw, 2), dtype=np.uint32)
+    if i8:
+        packed = np.zeros((c_out, max(q, 1), kh, kw), dtype=np.uint16)
+    else:
+        packed = np.zeros((c_out, max(q, 1), kh, kw, 2), dtype=np.uint32)
     holes = ctypes.c_int64(0)
     bo, bi = ctypes.c_int(0), ctypes.c_int(0)
-    st = lib().cs_pack_channels(CS_F32, W4.ctypes.data, c_out, kh, kw, c_in, n, packed.ctypes.data,
-                                ctypes.byref(holes), ctypes.byref(bo), ctypes.byref(bi))
+    st = lib().cs_pack_channels(CS_I8 if i8 else CS_F32, W4.ctypes.data, c_out, kh, kw, c_in, n,
+                                packed.ctypes.data, ctypes.byref(holes), ctypes.byref(bo),
+                                ctypes.byref(bi))
     if st != _lib.CS_OK:
         err = _lib.CSError("cs_pack_channels", st)
         err.bad = (bo.value, bi.value)
         raise err
     return packed, int(holes.value)
+
+
+def channel_table(packed: np.ndarray, kh: int, kw: int, c_in: int, c_out: int, n: int,
+                  stride: int = 1) -> np.ndarray:
+    """cs_channel_table: an int8 channel-overlaid layer's table for
+    conv2d_channels at this stride, int32 [c_out][5 * ceil((c_in/n)*kh*kw / 4)]."""
+    packed = np.ascontiguousarray(packed, dtype=np.uint16)
+    s4 = ((c_in // n) * kh * kw + 3) // 4
+    table = np.zeros((c_out, 5 * s4), dtype=np.int32)
+    check("cs_channel_table", lib().cs_channel_table(packed.ctypes.data, kh, kw, c_in, c_out, n,
+                                                      stride, table.ctypes.data))
+    return table
+
+
+def conv2d_channels(x: torch.Tensor, table: torch.Tensor, kh: int, kw: int, c_out: int, n: int,
+                    stride: int = 1, pad: int = 0, bias: torch.Tensor | None = None,
+                    out: torch.Tensor | None = None) -> torch.Tensor:
+    """int8 dense-input conv with the channel-dimension overlay (cs_conv2d_channels);
+    table: device copy of channel_table(...) for this stride."""
+    if x.dim() != 4 or x.dtype != torch.int8:
+        raise ValueError("x must be int8 NHWC")
+    b, h, w, c_in = x.shape
+    ho, wo = conv_out(h, kh, stride, pad), conv_out(w, kw, stride, pad)
+    if out is None:
+        out = torch.empty((b, max(ho, 0), max(wo, 0), c_out), dtype=torch.int32, device=x.device)
+    check("cs_conv2d_channels", lib().cs_conv2d_channels(
+        _dev(x, "x"), b, h, w, c_in, kh, kw, stride, pad, _dev(table, "table"), c_out, n,
+        _opt(bias, "bias"), _dev(out, "out"), _stream()))
+    return out
 
 
 def reorder_table_channels(packed: np.ndarray, kh: int, kw: int, c_in: int, c_out: int,

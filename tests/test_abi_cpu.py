@@ -340,6 +340,89 @@ def test_reorder_table_channels_sums_match_oracle():
                                    o.conv2d_nhwc(x, W4, 1, pad, None), rtol=1e-12, atol=1e-12)
 
 
+def _int8_channel_weights(r, c_out, kh, kw, c, n):
+    from workloads import channel_complementary_weights
+    mask = channel_complementary_weights(r, r, c_out, kh, kw, c, n) != 0
+    vals = r.integers(1, 128, size=mask.shape) * r.choice([-1, 1], size=mask.shape)
+    return np.where(mask, vals, 0).astype(np.int8)
+
+
+def _channel_eval(x, table, kh, kw, stride, pad, c_out):
+    """The int8 channel kernel's indexing on the CPU: per 64-pixel segment of
+    an output row, the staged tile [kh][63*stride + kw][cp] bytes (zero
+    outside the image); output pixel p of the segment reads byte
+    p*stride*cp + off of it for every slot offset of its filter's row and
+    multiplies it by the slot's weight byte (little-endian in the weight
+    words after the offsets)."""
+    b, h, w, c = x.shape
+    ho, wo = (h + 2 * pad - kh) // stride + 1, (w + 2 * pad - kw) // stride + 1
+    sw = 63 * stride + kw
+    cp = c if (c // 4) % 2 == 1 else c + 4
+    s4 = table.shape[1] // 5
+    off = table[:, :4 * s4].astype(np.int64)
+    wt = np.ascontiguousarray(table[:, 4 * s4:]).view(np.uint8).reshape(c_out, 4 * s4)
+    wt = wt.view(np.int8).astype(np.int64)
+    y = np.zeros((b, ho, wo, c_out), dtype=np.int64)
+    for bi in range(b):
+        for oy in range(ho):
+            for ox0 in range(0, wo, 64):
+                tile = np.zeros((kh, sw, cp), dtype=np.int64)
+                for ky in range(kh):
+                    iy = oy * stride - pad + ky
+                    for px in range(sw):
+                        ix = ox0 * stride - pad + px
+                        if 0 <= iy < h and 0 <= ix < w:
+                            tile[ky, px, :c] = x[bi, iy, ix]
+                flat = tile.reshape(-1)
+                for p_ in range(min(64, wo - ox0)):
+                    g = flat[p_ * stride * cp + off]          # [c_out][S]
+                    y[bi, oy, ox0 + p_] = (g * wt).sum(axis=1)
+    return y
+
+
+def test_channel_table_int8_matches_oracle():
+    """int8 channel-dimension overlay: cs_pack_channels (CS_I8) matches the
+    oracle's pack, and its cs_channel_table, read the way cs_conv2d_channels
+    reads it, gives the oracle's convolution of the dense filters exactly."""
+    r = np.random.default_rng(17)
+    for shape, kh, stride, pad, n, c_out in [((1, 9, 11, 12), 3, 1, 1, 3, 16),
+                                             ((2, 10, 9, 24), 3, 2, 1, 3, 32),
+                                             ((1, 8, 70, 8), 1, 1, 0, 1, 16)]:
+        W4 = _int8_channel_weights(r, c_out, kh, kh, shape[3], n)
+        packed, holes = ops.pack_channels(W4, n)
+        val, cid, oh = o.pack_channels(W4, n)
+        assert packed.dtype == np.uint16 and holes == oh
+        assert np.array_equal((packed & 0xFF).astype(np.uint8).view(np.int8), val)
+        assert np.array_equal(packed >> 8, cid.astype(np.uint16))
+        t = ops.channel_table(packed, kh, kh, shape[3], c_out, n, stride)
+        x = r.integers(-127, 128, size=shape).astype(np.int8)
+        assert np.array_equal(_channel_eval(x, t, kh, kh, stride, pad, c_out),
+                              o.conv2d_nhwc(x, W4, stride, pad, None))
+
+
+def test_channels_validation(L):
+    f = L.cs_conv2d_channels
+    #       x     b  h   w   c   kh kw s  p  table c_out n  bias  y     stream
+    base = [FAKE, 2, 16, 16, 48, 3, 3, 1, 1, FAKE, 64, 3, None, FAKE, None]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+    assert call(4, 50) == CS_ERR_SHAPE                          # c_in not a multiple of 4
+    assert call(11, 5) == CS_ERR_SHAPE                          # n does not divide c_in
+    assert call(10, 48) == CS_ERR_SHAPE                         # c_out not 16/32/64/128
+    assert call(0, None) == CS_ERR_ARG
+    assert call(9, None) == CS_ERR_ARG
+    assert call(13, FAKE + 4) == CS_ERR_ARG                     # y not 16-byte aligned
+    t = L.cs_channel_table
+    assert t(None, 3, 3, 48, 64, 3, 1, FAKE) == CS_ERR_ARG
+    bad = np.zeros((64, 16, 3, 3), dtype=np.uint16)
+    bad[0, 0, 0, 0] = 3 << 8                                    # channel ID 3 with n = 3
+    out = np.zeros((64, 5 * 36), dtype=np.int32)
+    assert t(bad.ctypes.data, 3, 3, 48, 64, 3, 1, out.ctypes.data) == CS_ERR_ARG
+
+
 def test_reorder_validation(L):
     f = L.cs_reorder_table
     sm = ctypes.c_int(0)
@@ -348,7 +431,7 @@ def test_reorder_validation(L):
     assert f(FAKE, 3, 3, 64, 64, 40, ctypes.byref(sm), None) == CS_ERR_SHAPE  # n > CS_MAX_N
     pc = L.cs_pack_channels
     hz = ctypes.c_int64(0)
-    assert pc(CS_I8, FAKE, 4, 3, 3, 6, 3, FAKE, ctypes.byref(hz), None, None) == CS_ERR_DTYPE
+    assert pc(CS_I32, FAKE, 4, 3, 3, 6, 3, FAKE, ctypes.byref(hz), None, None) == CS_ERR_DTYPE
     assert pc(CS_F32, None, 4, 3, 3, 6, 3, FAKE, None, None, None) == CS_ERR_ARG
     assert pc(CS_F32, FAKE, 4, 3, 3, 6, 4, FAKE, None, None, None) == CS_ERR_SHAPE   # 4 does not divide 6
     tc = L.cs_reorder_table_channels
