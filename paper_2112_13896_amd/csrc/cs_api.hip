@@ -163,6 +163,16 @@ int device_cus(int* cus) {
 
 constexpr size_t kBlockLds = 64 * 1024;   // LDS budget of one workgroup
 constexpr size_t kCuLds = 160 * 1024;     // LDS of one compute unit (gfx950)
+// LDS is given to a workgroup in units of 1,280 bytes (measured: three
+// workgroups of 53,760 bytes run together on a compute unit, three of 54,016
+// bytes do not)
+constexpr size_t kLdsGranule = 1280;
+
+// Workgroups of `shmem` bytes of LDS that fit on one compute unit at once.
+inline int64_t lds_wgs_per_cu(size_t shmem) {
+  const size_t g = (shmem + kLdsGranule - 1) / kLdsGranule * kLdsGranule;
+  return g == 0 ? 8 : (int64_t)(kCuLds / g);
+}
 
 // First version: one lane per (output item, set), packed kernels read from
 // global memory.  Used when the lists cannot be read four entries at a time
@@ -643,7 +653,7 @@ bool blocks_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, const vo
     // the table is staged once per workgroup: as many workgroups as fit at
     // once (by LDS), each looping over tiles
     if (cus > 0) {
-      int64_t per_cu = (int64_t)(kCuLds / (end > 0 ? end : 1));
+      int64_t per_cu = lds_wgs_per_cu(end);
       if (per_cu > 8) per_cu = 8;
       if (per_cu < 1) per_cu = 1;
       if (pl->blocks > per_cu * cus) pl->blocks = per_cu * cus;
@@ -985,7 +995,7 @@ bool rows_plan(const cs::ConvGeom& geo, cs_dtype xt, const void* aug, int k, int
   for (int w : {16, 8, 4}) {
     const size_t sh = rows_shmem(*pl, w, geo.c_out);
     if (sh <= kCuLds)
-      return rows_layout(pl, w, std::min<int>(32, (int)(kCuLds / sh) * w), geo.c_out);
+      return rows_layout(pl, w, std::min<int>(32, (int)lds_wgs_per_cu(sh) * w), geo.c_out);
   }
   return false;
 }
@@ -1146,7 +1156,7 @@ int mrs_launch_tiled(cs_dtype xt, const uint16_t* idx, const void* lval, const i
   ta.fd_kw = cs::make_fastdiv((uint32_t)geo.KW);
   const size_t tab_bytes = ((size_t)R * Gs * esz + 15) / 16 * 16;
   const size_t shmem = (size_t)gb * nacc * cs::MRS_BD * 4 + tab_bytes + (size_t)Gs * nacc * 4;
-  int bpc = (int)(kCuLds / shmem);
+  int bpc = (int)lds_wgs_per_cu(shmem);
   bpc = bpc < 1 ? 1 : (bpc > 8 ? 8 : bpc);              // 8 x 256 threads fill a compute unit
   const int64_t grid_lanes = (int64_t)cus * bpc * cs::MRS_BD;
   const int64_t units = items * (geo.G / gb);
@@ -1536,7 +1546,7 @@ int cs_conv2d_channels(const int8_t* x, int b, int h, int w, int c_in, int kh, i
   int cus = 0;
   const int dst = device_cus(&cus);
   if (dst != CS_OK) return dst;
-  int64_t per_cu = (int64_t)(kCuLds / shmem);
+  int64_t per_cu = lds_wgs_per_cu(shmem);
   if (per_cu > 8) per_cu = 8;
   const int64_t nb = ntiles < per_cu * cus ? ntiles : per_cu * cus;
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1593,7 +1603,7 @@ int cs_conv2d_dense_blocks(const int8_t* x, int b, int h, int w, int c_in, int k
   int cus = 0;
   const int dst = device_cus(&cus);
   if (dst != CS_OK) return dst;
-  int64_t per_cu = (int64_t)(kCuLds / shmem);
+  int64_t per_cu = lds_wgs_per_cu(shmem);
   if (per_cu > 8) per_cu = 8;
   if (per_cu < 1) per_cu = 1;
   const int64_t nb = ntiles < per_cu * cus ? ntiles : per_cu * cus;

@@ -678,13 +678,22 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       ho = (int)(t1 - t2 * ba.fd_ho.d);
       bb = (int)t2;
     }
+    // accumulators start at the bias of their channels (KP > 0: nacc == KP);
+    // the bias loads are issued together and before the list prefetch, so
+    // their one wait does not cover the list loads
+    {
+      constexpr int NJ = KP > 0 ? KP : GB * 16;
+      float bv[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        bv[j] = (bias && (KP > 0 || j < nacc)) ? bias[u * nacc + j] : 0.f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (KP > 0 || j < nacc) acc[j * BLK_BD + tid] = bv[j];
+    }
     // the first tap's count and first chunks, then the table while they fly
     TapPre cur;
     tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
-    // accumulators start at the bias of their channels
-#pragma unroll
-    for (int j = 0; j < GB * 16; ++j)
-      if (j < nacc) acc[j * BLK_BD + tid] = bias ? bias[u * nacc + j] : 0.f;
     if (!one_block) {
       stage_first();
       __syncthreads();
