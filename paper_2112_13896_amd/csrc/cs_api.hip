@@ -671,24 +671,31 @@ int launch_blocks(const BlocksPlan& pl, hipStream_t stream, const uint16_t* idx,
   const float* bs = static_cast<const float*>(bias);
   float* yy = static_cast<float*>(y);
   float* oo = static_cast<float*>(out);
-#define CS_BLOCKS(GB_, CH_, KP_, QK_)                                                    \
-  hipLaunchKernelGGL((cs::mrs_blocks_f32<float, GB_, CH_, KP_, QK_>), grid, block, pl.shmem,  \
+#define CS_BLOCKS(GB_, CH_, KP_, QK_, QD_)                                               \
+  hipLaunchKernelGGL((cs::mrs_blocks_f32<float, GB_, CH_, KP_, QK_, QD_>), grid, block, pl.shmem, \
                      stream, idx, lv, cnt, pa, bs, yy, oo, lo, geo, pl.ba)
+// a pixel's lanes fill whole quads (U >= 4): the quads share the list loads
+#define CS_BLOCKS_QD(GB_, CH_, KP_)                                                      \
+  do {                                                                                  \
+    if (pl.ba.log2U >= 2) CS_BLOCKS(GB_, CH_, KP_, 0, true);                            \
+    else CS_BLOCKS(GB_, CH_, KP_, 0, false);                                            \
+  } while (0)
 #define CS_BLOCKS_KP(GB_, CH_)                                                           \
   do {                                                                                  \
     const int kp = pl.own ? GB_ * geo.n : 0;                                            \
-    if (kp == 4) CS_BLOCKS(GB_, CH_, 4, 0);                                             \
-    else if (kp == 8) CS_BLOCKS(GB_, CH_, 8, 0);                                        \
-    else if (kp == 16) CS_BLOCKS(GB_, CH_, 16, 0);                                      \
-    else if (kp == 32) CS_BLOCKS(GB_, CH_, 32, 0);                                      \
-    else CS_BLOCKS(GB_, CH_, 0, 0);                                                     \
+    if (kp == 4) CS_BLOCKS_QD(GB_, CH_, 4);                                             \
+    else if (kp == 8) CS_BLOCKS_QD(GB_, CH_, 8);                                        \
+    else if (kp == 16) CS_BLOCKS_QD(GB_, CH_, 16);                                      \
+    else if (kp == 32) CS_BLOCKS_QD(GB_, CH_, 32);                                      \
+    else CS_BLOCKS_QD(GB_, CH_, 0);                                                     \
   } while (0)
-// the four-lane selection in place: two sets per lane, whole-tap blocks
+// the four-lane selection in place: two sets per lane, whole-tap blocks, four
+// lanes per pixel
 #define CS_BLOCKS_QUAD(KP_)                                                              \
   do {                                                                                  \
-    if (pl.ba.kmode == 6) CS_BLOCKS(2, false, KP_, 8);                                  \
-    else if (pl.ba.kmode == 7) CS_BLOCKS(2, false, KP_, 16);                            \
-    else CS_BLOCKS(2, false, KP_, 32);                                                  \
+    if (pl.ba.kmode == 6) CS_BLOCKS(2, false, KP_, 8, true);                            \
+    else if (pl.ba.kmode == 7) CS_BLOCKS(2, false, KP_, 16, true);                      \
+    else CS_BLOCKS(2, false, KP_, 32, true);                                            \
   } while (0)
   const bool ch = pl.ba.tpb == 0;
   if (pl.own && pl.ba.kmode >= 6) {
@@ -706,6 +713,7 @@ int launch_blocks(const BlocksPlan& pl, hipStream_t stream, const uint16_t* idx,
   }
 #undef CS_BLOCKS_QUAD
 #undef CS_BLOCKS_KP
+#undef CS_BLOCKS_QD
 #undef CS_BLOCKS
   return launch_status();
 }

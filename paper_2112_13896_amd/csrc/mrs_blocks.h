@@ -183,18 +183,29 @@ __device__ __forceinline__ void blk_chunk(const BChunk& ch, int e_lo, int e_hi, 
   }
 }
 
-// A tap's list count and first BLK_SPEC chunks, loaded ahead of their use.
-// Every load is issued unconditionally (a tap outside the image reads list
-// row 0, a chunk past the row's capacity reads the row's last chunk), so the
-// compiler's wait counts stay exact and a later load never waits for them.
+// A tap's list count and first list entries, loaded ahead of their use.
+// QD false: the lane loads the first BLK_SPEC chunks itself.  QD true (a
+// pixel's lanes fill whole quads, U >= 4): the four lanes of a quad load one
+// chunk each - lane p the chunk at (j0 rounded down to 4) + 4p - and pass them
+// round with DPP, so a wavefront issues one load per array for sixteen
+// entries of its sixteen pixels instead of one per chunk and lane.  Every
+// load is issued unconditionally (a tap outside the image reads list row 0, a
+// chunk past the row's capacity reads the row's last chunk, which is then
+// never used), so the compiler's wait counts stay exact and a later load
+// never waits for them.
 constexpr int BLK_SPEC = 3;
+// Whole-tap mode: the list data of the next BLK_DEPTH taps is in flight while
+// a tap is processed.
+constexpr int BLK_DEPTH = 1;
+template <bool QD>
 struct TapPre {
   int off;                 // list row offset, or -1: the tap is outside the image
   int cnt;
-  BChunk ch[BLK_SPEC];
+  BChunk ch[QD ? 1 : BLK_SPEC];
 };
 
-__device__ __forceinline__ void tap_prefetch(TapPre& tp, const uint16_t* __restrict__ lidx,
+template <bool QD>
+__device__ __forceinline__ void tap_prefetch(TapPre<QD>& tp, const uint16_t* __restrict__ lidx,
                                              const float* __restrict__ lval,
                                              const int32_t* __restrict__ lcnt, const ConvGeom& geo,
                                              bool live, int bb, int ho, int wo, int t, int j0,
@@ -207,12 +218,40 @@ __device__ __forceinline__ void tap_prefetch(TapPre& tp, const uint16_t* __restr
   tp.off = ok ? base : -1;
   tp.cnt = lcnt[q];
   const int c4 = j0 & ~3;
+  if constexpr (QD) {
+    const int pos = min(c4 + 4 * (int)(threadIdx.x & 3), geo.cap - 4);
+    tp.ch[0].idx = *reinterpret_cast<const uint2*>(lidx + base + pos);
+    tp.ch[0].val = *reinterpret_cast<const float4*>(lval + base + pos);
+  } else {
 #pragma unroll
-  for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
-    const int pos = min(c4 + 4 * s2, geo.cap - 4);
-    tp.ch[s2].idx = *reinterpret_cast<const uint2*>(lidx + base + pos);
-    tp.ch[s2].val = *reinterpret_cast<const float4*>(lval + base + pos);
+    for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
+      const int pos = min(c4 + 4 * s2, geo.cap - 4);
+      tp.ch[s2].idx = *reinterpret_cast<const uint2*>(lidx + base + pos);
+      tp.ch[s2].val = *reinterpret_cast<const float4*>(lval + base + pos);
+    }
   }
+}
+
+// Lane s's chunk of the quad (s a constant after unrolling): a DPP broadcast
+// within each quad, whose four lanes are active together (they serve one
+// pixel, so they take the same branches).
+__device__ __forceinline__ uint32_t quad_bcast(uint32_t v, int s) {
+  switch (s) {
+    case 0: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x00, 0xF, 0xF, false);
+    case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x55, 0xF, 0xF, false);
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xAA, 0xF, 0xF, false);
+    default: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xFF, 0xF, 0xF, false);
+  }
+}
+__device__ __forceinline__ BChunk quad_bcast(const BChunk& c, int s) {
+  BChunk r;
+  r.idx.x = quad_bcast(c.idx.x, s);
+  r.idx.y = quad_bcast(c.idx.y, s);
+  r.val.x = __uint_as_float(quad_bcast(__float_as_uint(c.val.x), s));
+  r.val.y = __uint_as_float(quad_bcast(__float_as_uint(c.val.y), s));
+  r.val.z = __uint_as_float(quad_bcast(__float_as_uint(c.val.z), s));
+  r.val.w = __uint_as_float(quad_bcast(__float_as_uint(c.val.w), s));
+  return r;
 }
 
 // Entries e of chunk `ch` (list positions c4 + e) with e in [lo, m - c4) and,
@@ -235,9 +274,10 @@ __device__ __forceinline__ int blk_chunk_upto(const BChunk& ch, int lo, int m, i
 
 // The entries of one tap's list from position j0 on (and, in channel mode,
 // below channel c_hi), the first chunks already in `tp`; the rest are read
-// one chunk ahead.  Returns the list position where the lane stopped.
-template <int GB, bool CH>
-__device__ __forceinline__ int blk_tap(const TapPre& tp, const uint16_t* __restrict__ lidx,
+// ahead (QD false: one chunk, QD true: the quad's next sixteen entries).
+// Returns the list position where the lane stopped.
+template <int GB, bool CH, bool QD>
+__device__ __forceinline__ int blk_tap(const TapPre<QD>& tp, const uint16_t* __restrict__ lidx,
                                        const float* __restrict__ lval, int cap, int j0, int c_hi,
                                        int row_add, const uint2* tab, int tstride, int set0,
                                        unsigned char* accb) {
@@ -245,32 +285,59 @@ __device__ __forceinline__ int blk_tap(const TapPre& tp, const uint16_t* __restr
   const int m = min(tp.cnt, cap);
   int c4 = j0 & ~3;
   int lo = j0 - c4;
-#pragma unroll
-  for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
-    if (c4 >= m) return m;
-    const int st = blk_chunk_upto<GB, CH>(tp.ch[s2], lo, m, c4, c_hi, row_add, tab, tstride,
-                                          set0, accb);
-    if (st < 4) return c4 + st;
-    c4 += 4;
-    lo = 0;
-  }
-  if (c4 >= m) return m;
   const uint16_t* li = lidx + tp.off;
   const float* lv = lval + tp.off;
-  BChunk cur;
-  cur.idx = *reinterpret_cast<const uint2*>(li + c4);
-  cur.val = *reinterpret_cast<const float4*>(lv + c4);
-  while (true) {
-    const int pn = min(c4 + 4, cap - 4);                 // next chunk, in the row
-    BChunk nxt;
-    nxt.idx = *reinterpret_cast<const uint2*>(li + pn);
-    nxt.val = *reinterpret_cast<const float4*>(lv + pn);
-    const int st = blk_chunk_upto<GB, CH>(cur, 0, m, c4, c_hi, row_add, tab, tstride, set0,
-                                          accb);
-    if (st < 4) return c4 + st;
-    c4 += 4;
+  if constexpr (QD) {
+    BChunk mine = tp.ch[0];                              // entries g0 + 4p .. of the quad
+    int g0 = c4;
+    while (true) {
+      const bool more = g0 + 16 < m;                     // the same in the quad
+      BChunk nmine;
+      if (more) {
+        const int pos = min(g0 + 16 + 4 * (int)(threadIdx.x & 3), cap - 4);
+        nmine.idx = *reinterpret_cast<const uint2*>(li + pos);
+        nmine.val = *reinterpret_cast<const float4*>(lv + pos);
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2) {
+        if (c4 >= m) return m;
+        const BChunk cs = quad_bcast(mine, s2);
+        const int st = blk_chunk_upto<GB, CH>(cs, lo, m, c4, c_hi, row_add, tab, tstride, set0,
+                                              accb);
+        if (st < 4) return c4 + st;
+        c4 += 4;
+        lo = 0;
+      }
+      if (!more) return m;
+      mine = nmine;
+      g0 += 16;
+    }
+  } else {
+#pragma unroll
+    for (int s2 = 0; s2 < BLK_SPEC; ++s2) {
+      if (c4 >= m) return m;
+      const int st = blk_chunk_upto<GB, CH>(tp.ch[s2], lo, m, c4, c_hi, row_add, tab, tstride,
+                                            set0, accb);
+      if (st < 4) return c4 + st;
+      c4 += 4;
+      lo = 0;
+    }
     if (c4 >= m) return m;
-    cur = nxt;
+    BChunk cur;
+    cur.idx = *reinterpret_cast<const uint2*>(li + c4);
+    cur.val = *reinterpret_cast<const float4*>(lv + c4);
+    while (true) {
+      const int pn = min(c4 + 4, cap - 4);               // next chunk, in the row
+      BChunk nxt;
+      nxt.idx = *reinterpret_cast<const uint2*>(li + pn);
+      nxt.val = *reinterpret_cast<const float4*>(lv + pn);
+      const int st = blk_chunk_upto<GB, CH>(cur, 0, m, c4, c_hi, row_add, tab, tstride, set0,
+                                            accb);
+      if (st < 4) return c4 + st;
+      c4 += 4;
+      if (c4 >= m) return m;
+      cur = nxt;
+    }
   }
 }
 
@@ -618,8 +685,9 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
 // accumulator columns; 0: the selection of ba.kmode on a copied tile.  Up to
 // 16 channels per lane the registers are held to three wavefronts per SIMD.
 // QK: with the four-lane selection in place (kmode 6-8), its list length
-// (8, 16 or 32); 0 otherwise.
-template <typename TO, int GB, bool CH, int KP, int QK>
+// (8, 16 or 32); 0 otherwise.  QD: a pixel's lanes fill whole quads (U >= 4),
+// whose lanes share the list loads.
+template <typename TO, int GB, bool CH, int KP, int QK, bool QD>
 __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_blocks_f32(const uint16_t* __restrict__ lidx,
                                                          const float* __restrict__ lval,
                                                          const int32_t* __restrict__ lcnt,
@@ -691,9 +759,15 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       for (int j = 0; j < NJ; ++j)
         if (KP > 0 || j < nacc) acc[j * BLK_BD + tid] = bv[j];
     }
-    // the first tap's count and first chunks, then the table while they fly
-    TapPre cur;
-    tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
+    // the first taps' counts and first chunks, then the table while they fly
+    // (q[0] is the tap processed next; channel mode uses q[0] only)
+    TapPre<QD> q[BLK_DEPTH];
+    tap_prefetch(q[0], lidx, lval, lcnt, geo, live, bb, ho, wo, 0, 0, ba.fd_kw);
+    if constexpr (!CH) {
+#pragma unroll
+      for (int d = 1; d < BLK_DEPTH; ++d)
+        tap_prefetch(q[d], lidx, lval, lcnt, geo, live, bb, ho, wo, d, 0, ba.fd_kw);
+    }
     if (!one_block) {
       stage_first();
       __syncthreads();
@@ -708,15 +782,17 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       // the next table block's loads (issued after the prefetched list data)
       if (has_next) st.load(aug, r0n, min(R, r0n + ba.RB), G);
       if constexpr (!CH) {
-        // whole taps t0 .. t1-1; the next tap (of this block or the next
-        // one) is prefetched while one is processed
+        // whole taps t0 .. t1-1; the taps BLK_DEPTH ahead (of this block
+        // or the next ones) are in flight while one is processed
         const int t0 = blk * ba.tpb, t1 = min(T_, t0 + ba.tpb);
         for (int t = t0; t < t1; ++t) {
-          TapPre nxt;
-          tap_prefetch(nxt, lidx, lval, lcnt, geo, live, bb, ho, wo, t + 1, 0, ba.fd_kw);
-          blk_tap<GB, false>(cur, lidx, lval, geo.cap, 0, C, (t - t0) * C, tab, ba.tstride,
+          TapPre<QD> nxt;
+          tap_prefetch(nxt, lidx, lval, lcnt, geo, live, bb, ho, wo, t + BLK_DEPTH, 0, ba.fd_kw);
+          blk_tap<GB, false, QD>(q[0], lidx, lval, geo.cap, 0, C, (t - t0) * C, tab, ba.tstride,
                              u * GB, accb);
-          cur = nxt;
+#pragma unroll
+          for (int d = 0; d + 1 < BLK_DEPTH; ++d) q[d] = q[d + 1];
+          q[BLK_DEPTH - 1] = nxt;
         }
       } else {
         // one tap, the channels [c_lo, c_hi): the lane goes on in the tap's
@@ -724,11 +800,11 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
         const int t0 = blk / ba.cblocks;
         const int c_lo = (blk - t0 * ba.cblocks) * ba.RB;
         if (c_lo == 0) cursor = 0;
-        cursor = blk_tap<GB, true>(cur, lidx, lval, geo.cap, cursor, c_lo + ba.RB, -c_lo, tab,
+        cursor = blk_tap<GB, true, QD>(q[0], lidx, lval, geo.cap, cursor, c_lo + ba.RB, -c_lo, tab,
                                    ba.tstride, u * GB, accb);
         // the next block's list data, in flight across the barrier
         const int tn = (blk + 1) / ba.cblocks;
-        tap_prefetch(cur, lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
+        tap_prefetch(q[0], lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
                      tn == t0 ? cursor : 0, ba.fd_kw);
       }
       if (has_next) {
