@@ -563,6 +563,34 @@ __device__ __forceinline__ int group_incl_sum(int v, int log2U, int p) {
   return v;
 }
 
+// Clamped 16-bit subtraction and minimum on two halves at once (integer
+// packed operations; written out so that the compiler keeps them packed
+// instead of turning them into one compare per half).
+__device__ __forceinline__ uint32_t pk_sub_sat_u16(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+__device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+
+// How many of the 2N 16-bit values packed in h are below c16: per half,
+// min(c16 -sat value, 1) is 1 exactly then; four independent packed sums.
+template <int N>
+__device__ __forceinline__ uint32_t below16(const uint32_t (&h)[N], uint32_t c16) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t c2 = c16 | (c16 << 16);
+  u16x2 acc[4] = {{0, 0}, {0, 0}, {0, 0}, {0, 0}};
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    acc[i & 3] += __builtin_bit_cast(u16x2, pk_min_u16(pk_sub_sat_u16(c2, h[i]), 0x00010001u));
+  const u16x2 t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  return (uint32_t)t.x + (uint32_t)t.y;
+}
+
 // k-WTA over the U lanes of each pixel, the lanes that computed its sums: lane
 // u holds channels u*KP .. u*KP+KP-1 (KP = GB * n) in its own accumulator
 // column, bias included, so no other lane's data is read and no barrier is
@@ -571,8 +599,11 @@ __device__ __forceinline__ int group_incl_sum(int v, int log2U, int p) {
 // in units of Section 5's channel partitioning).  The k-th largest key of a
 // unit is found bit by bit with group counts, stopping as soon as the keys at
 // or above the prefix are exactly k (their minimum is then the k-th largest);
-// ties go to the lower index; the winners of the whole row are written as one
-// list (non-zero values, ascending index) or densely.
+// the counts of the upper sixteen bits compare the keys' high halves and those
+// of the lower sixteen the low halves of the keys that share the prefix's high
+// half, two halves per packed instruction.  Ties go to the lower index; the
+// winners of the whole row are written as one list (non-zero values,
+// ascending index) or densely.
 template <typename TO, int KP>
 __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int log2Us,
                                              int64_t row, bool live, int c_out, int k,
@@ -603,12 +634,9 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     uint32_t pre = 0u;
     int cntp = c_unit;
     bool done = !live;
-    for (int bit = 31; bit >= 0; --bit) {
-      if (__ballot(!done) == 0ull) break;               // every row of the wavefront found
-      const uint32_t cand = pre | (1u << bit);
-      uint32_t c = 0;
-#pragma unroll
-      for (int j = 0; j < KP; ++j) c += key[j] >= cand ? 1u : 0u;
+    // one step of the search: the unit's keys at or above pre | bit, from
+    // this lane's count c (every lane of a unit takes part in the reduction)
+    auto step = [&](uint32_t cand, uint32_t c) {
       c = group_reduce(c, log2Us, OpAdd{});
       if (!done) {
         if ((int)c >= k) {
@@ -616,6 +644,37 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
           cntp = (int)c;
         }
         if (cntp == k) done = true;
+      }
+    };
+    // bits 31..16 on the keys' high halves, two to a register (a candidate's
+    // low half is 0 there, so key >= cand is a compare of the high halves)
+    {
+      uint32_t hp[KP / 2];
+#pragma unroll
+      for (int i = 0; i < KP / 2; ++i) hp[i] = (key[2 * i] >> 16) | (key[2 * i + 1] & 0xFFFF0000u);
+      for (int bit = 31; bit >= 16; --bit) {
+        if (__ballot(!done) == 0ull) break;              // every unit of the wavefront found
+        const uint32_t cand = pre | (1u << bit);
+        step(cand, (uint32_t)KP - below16(hp, cand >> 16));
+      }
+    }
+    // bits 15..0: only keys whose high half is the prefix's compete, on their
+    // low halves (the others hold 0, below every candidate, whose low half is
+    // at least 1); keys with a larger high half count in every step
+    if (__ballot(!done) != 0ull) {
+      const uint32_t ph = pre >> 16;
+      uint32_t lp[KP / 2];
+      uint32_t above = 0;
+#pragma unroll
+      for (int i = 0; i < KP / 2; ++i) {
+        const uint32_t k0 = key[2 * i], k1 = key[2 * i + 1];
+        lp[i] = ((k0 >> 16) == ph ? (k0 & 0xFFFFu) : 0u) | ((k1 >> 16) == ph ? (k1 << 16) : 0u);
+        above += ((k0 >> 16) > ph ? 1u : 0u) + ((k1 >> 16) > ph ? 1u : 0u);
+      }
+      for (int bit = 15; bit >= 0; --bit) {
+        if (__ballot(!done) == 0ull) break;
+        const uint32_t cand = pre | (1u << bit);
+        step(cand, above + (uint32_t)KP - below16(lp, cand & 0xFFFFu));
       }
     }
     // the k-th largest key: the least key at or above the prefix
