@@ -681,6 +681,73 @@ def _time_call(call, reps=4) -> float:
     return e0.elapsed_time(e1) / (reps * KREP)
 
 
+CHAIN_PHASES = ("conv1 staging", "conv1 products (MFMA)", "conv1 k-WTA", "conv1 lists out",
+                "conv2 staging", "conv2 products (routed adds)", "conv2 pool + k-WTA + lists",
+                "linear1 staging", "linear1 products", "linear1 sums", "linear1 threshold",
+                "linear1 winners + lists", "output layer")
+
+
+def phase_report(cids) -> dict:
+    """Per-phase times from the stamping build (libcs_stamps.so): for the
+    one-kernel keyword-spotting chain, the mean time of each phase per
+    workgroup, with one pass at a time on one stream and with passes
+    alternating on two streams (two images per CU, as the benchmark's graph
+    runs them); for the table-block layers, the mean time per tile of its
+    set-up + products and of its epilogue.  Eager launches, warm caches."""
+    import torch
+    from paper_2112_13896_amd import _lib
+    from paper_2112_13896_amd.network import Network
+    from workloads import CONFIGS, generate
+
+    out = {}
+    with _lib.stamping_library():
+        for cid in cids:
+            cfg = CONFIGS[cid]
+            inp = generate(cfg)
+            nets = [Network(cfg.layers, inp["W"], inp["b"], cfg.in_shape, cfg.batch,
+                            keep_sums=False) for _ in range(2)]
+            x = torch.from_numpy(inp["x"]).cuda()
+            for n in nets:
+                n.forward(x)
+            torch.cuda.synchronize()
+            rec = {}
+            for li in range(len(cfg.layers)):
+                for name, call in nets[0].launches(li, x if li == 0 else None):
+                    if "mrs" not in name:
+                        continue
+                    _lib.phase_stamps(reset=True)
+                    for _ in range(20):
+                        call()
+                    acc, khz = _lib.phase_stamps(reset=True)
+                    us = lambda a, b, c: round((acc[b] - acc[a]) / max(acc[c], 1) / khz * 1e3, 2)
+                    if acc[15]:
+                        rec[name] = {"workgroups": acc[15] // 20, "one stream": {
+                            "workgroup us": us(0, 13, 15),
+                            **{CHAIN_PHASES[i]: us(i, i + 1, 15) for i in range(13)}}}
+                        # two passes at a time, on two streams (separate buffers)
+                        side = torch.cuda.Stream()
+                        calls = [c for nm2, c in nets[1].launches(li, x if li == 0 else None)
+                                 if nm2 == name]
+                        torch.cuda.synchronize()
+                        for i in range(20):
+                            if i % 2:
+                                with torch.cuda.stream(side):
+                                    calls[0]()
+                            else:
+                                call()
+                        acc, khz = _lib.phase_stamps(reset=True)
+                        rec[name]["two streams"] = {
+                            "workgroup us": us(0, 13, 15),
+                            **{CHAIN_PHASES[i]: us(i, i + 1, 15) for i in range(13)}}
+                    elif acc[31]:
+                        rec[name] = {"tiles": acc[31] // 20,
+                                     "tile set-up + products us": us(16, 17, 31),
+                                     "epilogue us": us(17, 18, 31)}
+            out[cfg.name] = rec
+            torch.cuda.synchronize()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -707,6 +774,9 @@ def main() -> int:
     ap.add_argument("--ab-channels", action="store_true",
                     help="also time a channel-overlaid layer (56x56, 3x3, 48 -> 64, n = 3, batch "
                          "32): the int8 channel kernel against the fp32 reordering kernel")
+    ap.add_argument("--phase-stamps", default="", metavar="IDS",
+                    help="only report per-phase times of the given workloads (comma-separated "
+                         "ids) from the stamping build libcs_stamps.so")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MIB",
                     help="only copy a MIB-sized device buffer --steps times (reference kernel "
                          "for scaling the HBM byte counters, and the copy ceiling)")
@@ -742,6 +812,10 @@ def main() -> int:
         print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes,
                           "launches": args.steps,
                           "GB/s": round(2 * nbytes * args.steps / sec / 1e9, 1)}), flush=True)
+        return 0
+    if args.phase_stamps:
+        ids = [int(c) for c in args.phase_stamps.split(",") if c.strip()]
+        print(json.dumps({"phase_stamps": phase_report(ids)}), flush=True)
         return 0
     cfg = CONFIGS[args.config]
     if args.eager_passes:

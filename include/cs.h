@@ -682,6 +682,28 @@ size_t cs_workspace_bytes(int op, cs_dtype xt, int64_t rows, int c_in);
  */
 int cs_product_count(unsigned long long* count, int reset);
 
+/*
+ * cs_phase_stamps - per-phase wall-clock sums of the stamping build of the
+ * library (libcs_stamps.so, compiled with CS_PHASE_STAMPS; a measurement
+ * aid: where the time of a layer kernel goes).  At the end of each phase of
+ * the one-kernel keyword-spotting chain and of each tile of the table-block
+ * kernel, thread 0 of the workgroup adds the constant-rate wall clock to the
+ * phase's slot, and at each start one to the count slot (chain: slots 0-13
+ * in phase order, count 15; table-block kernel: 16 tile start, 17 products,
+ * 18 epilogue, count 31).  (slot[b] - slot[a]) / count / clock is the mean
+ * time from point a to point b.
+ *
+ *  acc        out (host): the first n slots, read after the device has
+ *             finished all work queued before the call; n in 0..32.
+ *  reset      non-zero: set every slot to 0 after reading.
+ *  clock_khz  out (host, may be NULL): the wall clock's rate in kHz.
+ *
+ * Synchronises the current device.  Errors: CS_ERR_ARG (n outside 0..32, or
+ * acc NULL with n > 0), CS_ERR_UNSUPPORTED outside the stamping build,
+ * CS_ERR_DEVICE.
+ */
+int cs_phase_stamps(unsigned long long* acc, int n, int reset, int* clock_khz);
+
 /* cs_status_str - static, never-NULL description of a status code. */
 const char* cs_status_str(int status);
 

@@ -11,6 +11,7 @@ import os
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs.so")
 # the same library with the product counter compiled in (tests only)
 COUNT_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs_count.so")
+STAMP_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcs_stamps.so")
 
 CS_OK = 0
 CS_ERR_ARG = -1
@@ -81,6 +82,7 @@ SIGNATURES = {
     "cs_kwta_lists": (_i, [_i, _vp, _i64, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp]),
     "cs_workspace_bytes": (_sz, [_i, _i, _i64, _i]),
     "cs_product_count": (_i, [_c.POINTER(_c.c_ulonglong), _i]),
+    "cs_phase_stamps": (_i, [_c.POINTER(_c.c_ulonglong), _i, _i, _c.POINTER(_c.c_int)]),
     "cs_status_str": (_c.c_char_p, [_i]),
 }
 
@@ -132,6 +134,28 @@ class counting_library:
         global _LIB
         _LIB = self._prev
         return False
+
+
+class stamping_library(counting_library):
+    """Context manager: calls inside it go to the stamping build
+    (libcs_stamps.so), whose layer kernels add up wall-clock stamps at their
+    phase boundaries (read with phase_stamps())."""
+
+    def __enter__(self):
+        global _LIB
+        self._prev = _LIB
+        _LIB = _load(STAMP_LIB_PATH)
+        return self
+
+
+def phase_stamps(reset: bool = False):
+    """cs_phase_stamps of the library in use: (the 32 slot sums, the wall
+    clock's rate in kHz); raises CSError with CS_ERR_UNSUPPORTED outside the
+    stamping build."""
+    acc = (ctypes.c_ulonglong * 32)()
+    khz = ctypes.c_int(0)
+    check("cs_phase_stamps", lib().cs_phase_stamps(acc, 32, int(bool(reset)), ctypes.byref(khz)))
+    return [int(v) for v in acc], int(khz.value)
 
 
 def product_count(reset: bool = False) -> int:

@@ -20,6 +20,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libcs.so")
 COUNT_LIB = os.path.join(HERE, "libcs_count.so")
+STAMP_LIB = os.path.join(HERE, "libcs_stamps.so")
 ARCH = "gfx950"
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -56,13 +57,15 @@ def _cmd(out: str, extra: list) -> list:
 
 
 def build(verbose: bool = False, extra: list | None = None, counting: bool = True) -> str:
-    """Compile libcs.so (always recompiles) and, with `counting`, the counting
-    build libcs_count.so (every multiply-route-sum kernel counts the products
-    it forms; tests only), the two compilations side by side.  Returns the
+    """Compile libcs.so (always recompiles) and, with `counting`, the two
+    instrumented builds: libcs_count.so (every multiply-route-sum kernel counts
+    the products it forms; tests only) and libcs_stamps.so (phase stamps; the
+    benchmark's phase report), the compilations side by side.  Returns the
     path of libcs.so."""
     jobs = [(LIB, list(extra or []))]
     if counting:
         jobs.append((COUNT_LIB, list(extra or []) + ["-DCS_COUNT_PRODUCTS"]))
+        jobs.append((STAMP_LIB, list(extra or []) + ["-DCS_PHASE_STAMPS"]))
     procs = []
     for out, ex in jobs:
         cmd = _cmd(out + ".tmp", ex)

@@ -156,6 +156,7 @@ __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
     }
   }
   __syncthreads();
+  CS_STAMP(1);
   // B operands: lane holds channel 16*nt + lane%16, slots 8*(lane/16) .. +7
   int64_t bop[4];
 #pragma unroll
@@ -220,6 +221,7 @@ __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
     }
   }
   __syncthreads();
+  CS_STAMP(2);
 
   // ---- output: the sums, and/or k-WTA as in the fused sparse layer
   const int c_out = 64;
@@ -251,6 +253,7 @@ __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
         break;
     }
     __syncthreads();
+    CS_STAMP(3);
     if (lo.idx) {
       using OV = typename ChunkVal<TO>::type;
       const int cq = lo.cap >> 2;

@@ -2200,6 +2200,43 @@ int cs_conv2d_dense_kwta_chain3(
                             oval3, ocnt3, ocap3, aug4, c_out4, n4, bias4, y4, stream);
 }
 
+extern "C" int cs_phase_stamps(unsigned long long* acc, int n, int reset, int* clock_khz) {
+#ifdef CS_PHASE_STAMPS
+  if (n < 0 || n > 32 || (n > 0 && !acc)) return CS_ERR_ARG;
+  unsigned long long v[32] = {0};
+  int dev = 0;
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpyFromSymbol(v, HIP_SYMBOL(cs_phase_acc), sizeof(v), 0, hipMemcpyDeviceToHost) !=
+          hipSuccess ||
+      hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return CS_ERR_DEVICE;
+  }
+  for (int i = 0; i < n; ++i) acc[i] = v[i];
+  if (clock_khz &&
+      hipDeviceGetAttribute(clock_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return CS_ERR_DEVICE;
+  }
+  if (reset) {
+    const unsigned long long zero[32] = {0};
+    if (hipMemcpyToSymbol(HIP_SYMBOL(cs_phase_acc), zero, sizeof(zero), 0,
+                          hipMemcpyHostToDevice) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+      (void)hipGetLastError();
+      return CS_ERR_DEVICE;
+    }
+  }
+  return CS_OK;
+#else
+  (void)acc;
+  (void)n;
+  (void)reset;
+  if (clock_khz) *clock_khz = 0;
+  return CS_ERR_UNSUPPORTED;
+#endif
+}
+
 extern "C" int cs_product_count(unsigned long long* count, int reset) {
 #ifdef CS_COUNT_PRODUCTS
   unsigned long long v = 0;

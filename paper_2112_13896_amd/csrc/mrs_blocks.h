@@ -794,6 +794,8 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
   const int wg = (gridDim.x & 7) == 0 ? (int)(blockIdx.x & 7) * nx + (int)(blockIdx.x >> 3)
                                       : (int)blockIdx.x;
   for (int tile = wg; tile < ba.ntiles; tile += gridDim.x) {
+    CS_STAMP_COUNT(31);
+    CS_STAMP(16);
     const int item0 = tile * ba.P;
     const int item = item0 + ps;
     const bool live = item < ba.items;
@@ -875,6 +877,7 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
     }
 
     // ---- epilogue
+    CS_STAMP(17);
     if constexpr (KP > 0) {
       // the lanes' own columns: no barrier, the next tile starts right after
       if constexpr (QK > 0) {
@@ -921,6 +924,7 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       blk_epilogue_tile<TO, GB>(smem, acc, item0, c_out, y, out, lo, ba);
       __syncthreads();                                   // before the accumulators are reused
     }
+    CS_STAMP(18);
   }
 }
 

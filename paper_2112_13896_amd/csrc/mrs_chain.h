@@ -63,6 +63,8 @@ __device__ __forceinline__ const ChainArgs* chain_args() {
 // KM: the first layer's k-WTA selection (its kmode), fixed at compile time.
 template <int POOL, int KW, int KM>
 __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
+  CS_STAMP_COUNT(15);
+  CS_STAMP(0);
   {
     const ChainArgs* a = chain_args();
     const ListOut lo0 = a->lo0;
@@ -72,6 +74,7 @@ __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
                                       blockIdx.x);
   }
   __syncthreads();
+  CS_STAMP(4);
   {
     const ChainArgs* a = chain_args();
     const ListOut lo0 = a->lo0, lo = a->lo;
@@ -81,6 +84,7 @@ __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
                                    a->bias, a->y, nullptr, lo, geo, sc, blockIdx.x);
   }
   __syncthreads();
+  CS_STAMP(7);
   {
     const ChainArgs* a = chain_args();
     const ListOut lo = a->lo, lo2 = a->lo2;
@@ -91,6 +95,10 @@ __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
                                          a->aug2, a->bias2, a->y2, nullptr, lo2, geo2, sa2, nx,
                                          blockIdx.x);
   }
+#ifdef CS_PHASE_STAMPS
+  __syncthreads();
+#endif
+  CS_STAMP(13);
 }
 
 }  // namespace cs

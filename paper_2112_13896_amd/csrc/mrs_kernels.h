@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "count_products.h"
+#include "phase_stamps.h"
 
 namespace cs {
 

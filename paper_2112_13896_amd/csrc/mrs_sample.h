@@ -182,6 +182,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
     }
   }
   __syncthreads();
+  CS_STAMP(8);
 
   // ---- multiply, route, sum: job (s, g) takes the entries [s*per, s*per +
   // per) (per a multiple of 4: 16-byte LDS reads), all its table loads of a
@@ -222,6 +223,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
     }
   }
   __syncthreads();
+  CS_STAMP(9);
   // ---- the slices' sums + bias (channel g*n + kid sits at acc[s][kid][g]),
   // and the row's smallest and largest keys
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
@@ -254,6 +256,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
     kmax = wmm[SAMPLE_BD / 64 + w] > kmax ? wmm[SAMPLE_BD / 64 + w] : kmax;
   }
 
+  CS_STAMP(10);
   // ---- k-WTA over the row: thread t holds keys [KEYS*t, KEYS*t + KEYS),
   // offset by the row's smallest key (order kept, fewer significant bits)
   const int i0 = tid * SAMPLE_KEYS;
@@ -356,6 +359,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
     }
   }
 
+  CS_STAMP(11);
   // ---- one scan: keys above the threshold (with a non-zero output, for
   // lists) and keys equal to it, packed as two 16-bit counts
   int gt_t = 0, eq_t = 0;
@@ -416,6 +420,7 @@ __device__ __forceinline__ void sample_body(const uint16_t* __restrict__ lidx,
       eq_before += eq ? 1 : 0;
     }
   }
+  CS_STAMP(12);
   // ---- the next layer on the winners: a winner (channel i, output v) adds
   // v * value to the next layer's output g*n + kid for every set g of its
   // packed row i (integer sums: exact in any order)

@@ -171,6 +171,7 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
   }
   for (int e = SCAT_PRE * SCAT_BD + tid; e < ne; e += SCAT_BD) put(e, lidx[lbase + e], lval[lbase + e]);
   __syncthreads();
+  CS_STAMP(5);
 
   // ---- multiply, route, sum
   const int njobs = tot * gpc;
@@ -263,6 +264,7 @@ __device__ __forceinline__ void scatter_body(const uint16_t* __restrict__ lidx,
     }
   }
   __syncthreads();
+  CS_STAMP(6);
 
   // ---- epilogue: 16 lanes per pooled item, KPL consecutive channels per lane
   constexpr int KPL = 4 * M;                                        // c_out <= 64 * M (host)

@@ -62,6 +62,25 @@ def test_counting_build_exports_every_declared_symbol():
         _lib.product_count()
 
 
+def test_stamping_build_exports_every_declared_symbol():
+    """The stamping build (libcs_stamps.so) is the same ABI; the other builds
+    have no phase stamps and say so without touching a device, and the
+    argument check comes first in the stamping build."""
+    S = _lib._load(_lib.STAMP_LIB_PATH)
+    for nm in declared_functions():
+        assert hasattr(S, nm)
+    acc = (ctypes.c_ulonglong * 32)()
+    khz = ctypes.c_int(5)
+    assert _lib.lib().cs_phase_stamps(acc, 32, 0, ctypes.byref(khz)) == _lib.CS_ERR_UNSUPPORTED
+    assert khz.value == 0
+    C = _lib._load(_lib.COUNT_LIB_PATH)
+    assert C.cs_phase_stamps(acc, 32, 0, None) == _lib.CS_ERR_UNSUPPORTED
+    assert S.cs_phase_stamps(acc, 33, 0, None) == _lib.CS_ERR_ARG
+    assert S.cs_phase_stamps(None, 4, 0, None) == _lib.CS_ERR_ARG
+    with pytest.raises(_lib.CSError):
+        _lib.phase_stamps()
+
+
 @pytest.mark.parametrize("dtype", ["int8", "float32"])
 def test_pack_matches_oracle(dtype):
     r = np.random.default_rng(3)
