@@ -743,6 +743,11 @@ def phase_report(cids) -> dict:
                         rec[name] = {"tiles": acc[31] // 20,
                                      "tile set-up + products us": us(16, 17, 31),
                                      "epilogue us": us(17, 18, 31)}
+                        if acc[19] and acc[20]:
+                            # the selection on the lanes' own columns, in parts
+                            rec[name].update({"epilogue: threshold search us": us(17, 19, 31),
+                                              "epilogue: threshold, ties, masks us": us(19, 20, 31),
+                                              "epilogue: output us": us(20, 18, 31)})
             out[cfg.name] = rec
             torch.cuda.synchronize()
     return out

@@ -677,6 +677,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
         step(cand, above + (uint32_t)KP - below16(lp, cand & 0xFFFFu));
       }
     }
+    CS_STAMP(19);
     // the k-th largest key: the least key at or above the prefix
     uint32_t mn = 0xFFFFFFFFu;
 #pragma unroll
@@ -714,6 +715,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     winm |= w ? 1u << j : 0u;
     wcount += (lo.idx ? (w && v[j] != 0.f) : w) ? 1 : 0;
   }
+  CS_STAMP(20);
   if (lo.idx) {
     const int incl = group_incl_sum(wcount, log2U, p);
     int pos = incl - wcount;

@@ -13,7 +13,8 @@
 // 6 conv2 products, 7 conv2 pool + k-WTA + lists, 8 linear1 staged,
 // 9 linear1 products, 10 linear1 sums, 11 linear1 threshold, 12 linear1
 // lists, 13 end (output layer), 15 count; the table-block kernel 16 tile
-// start, 17 products, 18 epilogue, 31 count.
+// start, 17 products, 18 epilogue, 31 count, and in its k-WTA on the lanes'
+// own columns 19 threshold search, 20 winner masks.
 #pragma once
 
 #ifdef CS_PHASE_STAMPS
