@@ -742,6 +742,8 @@ def phase_report(cids) -> dict:
                     elif acc[31]:
                         rec[name] = {"tiles": acc[31] // 20,
                                      "tile set-up + products us": us(16, 17, 31),
+                                     "of it: products (table blocks in LDS) us":
+                                         round(acc[21] / max(acc[31], 1) / khz * 1e3, 2),
                                      "epilogue us": us(17, 18, 31)}
                         if acc[19] and acc[20]:
                             # the selection on the lanes' own columns, in parts

@@ -690,9 +690,10 @@ int cs_product_count(unsigned long long* count, int reset);
  * kernel, thread 0 of the workgroup adds the constant-rate wall clock to the
  * phase's slot, and at each start one to the count slot (chain: slots 0-13
  * in phase order, count 15; table-block kernel: 16 tile start, 17 products,
- * 18 epilogue, count 31, and inside its k-WTA on the lanes' own columns 19
- * threshold search, 20 winner masks).  (slot[b] - slot[a]) / count / clock is
- * the mean time from point a to point b.
+ * 18 epilogue, count 31, inside its k-WTA on the lanes' own columns 19
+ * threshold search, 20 winner masks, and 21 the summed time of a tile's table
+ * blocks' products).  (slot[b] - slot[a]) / count / clock is the mean time
+ * from point a to point b, slot[21] / count / clock a mean duration.
  *
  *  acc        out (host): the first n slots, read after the device has
  *             finished all work queued before the call; n in 0..32.

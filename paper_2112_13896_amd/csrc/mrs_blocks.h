@@ -809,19 +809,16 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       ho = (int)(t1 - t2 * ba.fd_ho.d);
       bb = (int)t2;
     }
-    // accumulators start at the bias of their channels (KP > 0: nacc == KP);
-    // the bias loads are issued together and before the list prefetch, so
-    // their one wait does not cover the list loads
-    {
-      constexpr int NJ = KP > 0 ? KP : GB * 16;
-      float bv[NJ];
+    // accumulators start at the bias of their channels (KP > 0: nacc == KP):
+    // the bias loads are issued together, then the first taps' list loads,
+    // and only then are the accumulators written, so the two latencies
+    // overlap (the wait before the writes covers the bias loads, and every
+    // store issued before them: the vector memory counter counts both)
+    constexpr int NJ = KP > 0 ? KP : GB * 16;
+    float bv[NJ];
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        bv[j] = (bias && (KP > 0 || j < nacc)) ? bias[u * nacc + j] : 0.f;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        if (KP > 0 || j < nacc) acc[j * BLK_BD + tid] = bv[j];
-    }
+    for (int j = 0; j < NJ; ++j)
+      bv[j] = (bias && (KP > 0 || j < nacc)) ? bias[u * nacc + j] : 0.f;
     // the first taps' counts and first chunks, then the table while they fly
     // (q[0] is the tap processed next; channel mode uses q[0] only)
     TapPre<QD> q[BLK_DEPTH];
@@ -831,12 +828,16 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       for (int d = 1; d < BLK_DEPTH; ++d)
         tap_prefetch(q[d], lidx, lval, lcnt, geo, live, bb, ho, wo, d, 0, ba.fd_kw);
     }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (KP > 0 || j < nacc) acc[j * BLK_BD + tid] = bv[j];
     if (!one_block) {
       stage_first();
       __syncthreads();
     }
 
     int cursor = 0;                                      // place in the current tap's list
+    unsigned long long blk_time = 0;                     // stamping build: the blocks' products
     for (int blk = 0; blk < ba.nblocks; ++blk) {
       const int r0n = (blk + 1) * ba.RB;
       const bool has_next = blk + 1 < ba.nblocks;
@@ -844,6 +845,7 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
       const uint2* tab = reinterpret_cast<const uint2*>(smem + (odd ? ba.off_t1 : ba.off_t0));
       // the next table block's loads (issued after the prefetched list data)
       if (has_next) st.load(aug, r0n, min(R, r0n + ba.RB), G);
+      const unsigned long long blk_t0 = CS_CLOCK();
       if constexpr (!CH) {
         // whole taps t0 .. t1-1; the taps BLK_DEPTH ahead (of this block
         // or the next ones) are in flight while one is processed
@@ -870,6 +872,7 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
         tap_prefetch(q[0], lidx, lval, lcnt, geo, live, bb, ho, wo, has_next ? tn : T_,
                      tn == t0 ? cursor : 0, ba.fd_kw);
       }
+      blk_time += CS_CLOCK() - blk_t0;
       if (has_next) {
         if (ba.nbuf == 1) __syncthreads();               // every lane is done with the block
         st.store(smem, odd || ba.nbuf == 1 ? ba.off_t0 : ba.off_t1, 0,
@@ -880,6 +883,7 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
 
     // ---- epilogue
     CS_STAMP(17);
+    CS_STAMP_ADD(21, blk_time);
     if constexpr (KP > 0) {
       // the lanes' own columns: no barrier, the next tile starts right after
       if constexpr (QK > 0) {

@@ -13,8 +13,10 @@
 // 6 conv2 products, 7 conv2 pool + k-WTA + lists, 8 linear1 staged,
 // 9 linear1 products, 10 linear1 sums, 11 linear1 threshold, 12 linear1
 // lists, 13 end (output layer), 15 count; the table-block kernel 16 tile
-// start, 17 products, 18 epilogue, 31 count, and in its k-WTA on the lanes'
-// own columns 19 threshold search, 20 winner masks.
+// start, 17 products, 18 epilogue, 31 count, in its k-WTA on the lanes' own
+// columns 19 threshold search, 20 winner masks, and 21 the time of a tile
+// spent in the table blocks' products (measured per block with CS_CLOCK, added
+// once per tile: an atomic per block would itself take part of the time).
 #pragma once
 
 #ifdef CS_PHASE_STAMPS
@@ -27,11 +29,20 @@ __device__ unsigned long long cs_phase_acc[32];
   do {                                                                                  \
     if (threadIdx.x == 0) atomicAdd(&cs_phase_acc[(i)], 1ull);                          \
   } while (0)
+#define CS_CLOCK() ((unsigned long long)wall_clock64())
+#define CS_STAMP_ADD(i, v)                                                               \
+  do {                                                                                  \
+    if (threadIdx.x == 0) atomicAdd(&cs_phase_acc[(i)], (unsigned long long)(v));       \
+  } while (0)
 #else
 #define CS_STAMP(i) \
   do {              \
   } while (0)
 #define CS_STAMP_COUNT(i) \
   do {                    \
+  } while (0)
+#define CS_CLOCK() 0ull
+#define CS_STAMP_ADD(i, v) \
+  do {                     \
   } while (0)
 #endif
