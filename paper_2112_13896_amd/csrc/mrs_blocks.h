@@ -576,19 +576,43 @@ __device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
   asm("v_pk_min_u16 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
   return d;
 }
+__device__ __forceinline__ uint32_t pk_add_u16(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_pk_add_u16 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
 
 // How many of the 2N 16-bit values packed in h are below c16: per half,
-// min(c16 -sat value, 1) is 1 exactly then; four independent packed sums.
+// min(c16 -sat value, 1) is 1 exactly then; the 0/1 halves are added in a
+// tree (the adds written out too, so the compiler does not turn the tree
+// into one long chain of dependent adds).
 template <int N>
 __device__ __forceinline__ uint32_t below16(const uint32_t (&h)[N], uint32_t c16) {
-  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
   const uint32_t c2 = c16 | (c16 << 16);
-  u16x2 acc[4] = {{0, 0}, {0, 0}, {0, 0}, {0, 0}};
+  uint32_t m[N];
 #pragma unroll
-  for (int i = 0; i < N; ++i)
-    acc[i & 3] += __builtin_bit_cast(u16x2, pk_min_u16(pk_sub_sat_u16(c2, h[i]), 0x00010001u));
-  const u16x2 t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-  return (uint32_t)t.x + (uint32_t)t.y;
+  for (int i = 0; i < N; ++i) m[i] = pk_min_u16(pk_sub_sat_u16(c2, h[i]), 0x00010001u);
+#pragma unroll
+  for (int w = 1; w < N; w *= 2)
+#pragma unroll
+    for (int i = 0; i + w < N; i += 2 * w) m[i] = pk_add_u16(m[i], m[i + w]);
+  return (m[0] & 0xFFFFu) + (m[0] >> 16);
+}
+
+// Sum over the aligned groups of 2^log2U lanes (log2U <= 4) without
+// branches: each of the four DPP steps adds its partner's value masked by
+// mk[s] (all ones when the group spans that step, else zero), the masks
+// made once by group_masks.
+__device__ __forceinline__ void group_masks(int log2U, uint32_t (&mk)[4]) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) mk[s] = log2U > s ? 0xFFFFFFFFu : 0u;
+}
+__device__ __forceinline__ uint32_t group_sum_nb(uint32_t v, const uint32_t (&mk)[4]) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false) & mk[0];
+  v += (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false) & mk[1];
+  v += (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false) & mk[2];
+  v += (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false) & mk[3];
+  return v;
 }
 
 // k-WTA over the U lanes of each pixel, the lanes that computed its sums: lane
@@ -636,8 +660,10 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     bool done = !live;
     // one step of the search: the unit's keys at or above pre | bit, from
     // this lane's count c (every lane of a unit takes part in the reduction)
+    uint32_t mk[4];
+    group_masks(log2Us, mk);
     auto step = [&](uint32_t cand, uint32_t c) {
-      c = group_reduce(c, log2Us, OpAdd{});
+      c = group_sum_nb(c, mk);
       if (!done) {
         if ((int)c >= k) {
           pre = cand;
