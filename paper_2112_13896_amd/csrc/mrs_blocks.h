@@ -563,9 +563,10 @@ __device__ __forceinline__ int group_incl_sum(int v, int log2U, int p) {
   return v;
 }
 
-// Clamped 16-bit subtraction and minimum on two halves at once (integer
-// packed operations; written out so that the compiler keeps them packed
-// instead of turning them into one compare per half).
+// Clamped 16-bit subtraction, minimum and sum on two halves at once (integer
+// packed operations), and 32-bit minimum and sum: written out so that the
+// compiler keeps them as they are instead of turning a minimum with 1 into a
+// compare (one chain through VCC) or a tree of sums into one chain.
 __device__ __forceinline__ uint32_t pk_sub_sat_u16(uint32_t a, uint32_t b) {
   uint32_t d;
   asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(d) : "v"(a), "v"(b));
@@ -574,6 +575,16 @@ __device__ __forceinline__ uint32_t pk_sub_sat_u16(uint32_t a, uint32_t b) {
 __device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
   uint32_t d;
   asm("v_pk_min_u16 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+__device__ __forceinline__ uint32_t min_u32(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_min_u32 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+__device__ __forceinline__ uint32_t add_u32(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_add_u32 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
   return d;
 }
 __device__ __forceinline__ uint32_t pk_add_u16(uint32_t a, uint32_t b) {
@@ -606,6 +617,18 @@ __device__ __forceinline__ uint32_t below16(const uint32_t (&h)[N], uint32_t c16
 __device__ __forceinline__ void group_masks(int log2U, uint32_t (&mk)[4]) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) mk[s] = log2U > s ? 0xFFFFFFFFu : 0u;
+}
+__device__ __forceinline__ uint32_t group_min_nb(uint32_t v, const uint32_t (&mk)[4]) {
+  uint32_t t;
+  t = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false) | ~mk[0];
+  v = t < v ? t : v;
+  t = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false) | ~mk[1];
+  v = t < v ? t : v;
+  t = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false) | ~mk[2];
+  v = t < v ? t : v;
+  t = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false) | ~mk[3];
+  v = t < v ? t : v;
+  return v;
 }
 __device__ __forceinline__ uint32_t group_sum_nb(uint32_t v, const uint32_t (&mk)[4]) {
   v += (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false) & mk[0];
@@ -704,16 +727,30 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
       }
     }
     CS_STAMP(19);
-    // the k-th largest key: the least key at or above the prefix
-    uint32_t mn = 0xFFFFFFFFu;
+    // the k-th largest key: the least key at or above the prefix.  key - pre
+    // wraps the keys below the prefix above every key at or above it, so the
+    // least of the differences (a tree of minima, then the group's) is the
+    // least key at or above the prefix minus the prefix; the unit has cntp
+    // >= k > 0 such keys
+    uint32_t d[KP];
 #pragma unroll
-    for (int j = 0; j < KP; ++j) mn = (key[j] >= pre && key[j] < mn) ? key[j] : mn;
-    thr = group_reduce(mn, log2Us, OpMin{});
-    uint32_t gt = 0;
+    for (int j = 0; j < KP; ++j) d[j] = key[j] - pre;
 #pragma unroll
-    for (int j = 0; j < KP; ++j) gt += key[j] > thr ? 1u : 0u;
-    gt = group_reduce(gt, log2Us, OpAdd{});
-    need = k - (int)gt;
+    for (int w = 1; w < KP; w *= 2)
+#pragma unroll
+      for (int j = 0; j + w < KP; j += 2 * w) d[j] = d[j] < d[j + w] ? d[j] : d[j + w];
+    thr = group_min_nb(d[0], mk) + pre;
+    // keys above the threshold: the cntp keys at or above the prefix are the
+    // threshold's copies and the keys above it; the copies are counted with
+    // min(key ^ thr, 1), 0 exactly for a copy (a tree of sums, no compares)
+#pragma unroll
+    for (int j = 0; j < KP; ++j) d[j] = min_u32(key[j] ^ thr, 1u);
+#pragma unroll
+    for (int w = 1; w < KP; w *= 2)
+#pragma unroll
+      for (int j = 0; j + w < KP; j += 2 * w) d[j] = add_u32(d[j], d[j + w]);
+    const uint32_t eq_unit = group_sum_nb((uint32_t)KP - d[0], mk);
+    need = k - (cntp - (int)eq_unit);
   }
   // ties in index order: this lane's first tie has rank (ties of the unit's
   // lanes before)
