@@ -370,10 +370,14 @@ int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const
  * (input shape b x hp x wp x c_out, where hp x wp is the first layer's pooled
  * map).  The result is that of those two calls.  When the first layer's
  * matrix-core kernel can take a whole image per workgroup and the three-layer
- * tail runs in one kernel (cs_mrs_kwta_chain3's condition), all four layers
- * run in one kernel, one workgroup per image, the phases separated by
- * workgroup barriers and the lists between them read back from L2; otherwise
- * the two calls run back to back on `stream`.  DEVICE memory.
+ * tail runs in one kernel (cs_mrs_kwta_chain3's condition, or: the second
+ * layer has eight list slots per pixel (ocap == 8), a square 3x3 or 5x5
+ * window, four sets (c_out2 == 4 * n2 <= 64), the first layer pools 2x2 and
+ * the second layer's output map fits in LDS, which runs it output-stationary),
+ * all four layers run in one kernel, one workgroup per image, the phases
+ * separated by workgroup barriers and the lists between them read back from
+ * L2; otherwise the two calls run back to back on `stream`.  The result does
+ * not depend on the path (integer sums).  DEVICE memory.
  *
  *  xt .. ocap   the first layer as cs_conv2d_dense_kwta (xt == ot == CS_I8,
  *          list output oidx/oval/ocnt/ocap, no dense out).

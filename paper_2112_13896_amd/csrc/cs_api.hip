@@ -2072,8 +2072,55 @@ int cs_mrs_kwta_chain3(cs_dtype xt, const uint16_t* idx, const void* lval, const
                             ocnt2, ocap2, aug3, c_out3, n3, bias3, y3, stream);
 }
 
-template <int POOL, int KW, int KM>
-void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const SamplePlan& sp,
+// The output-stationary second layer of the dense chain: 64 input channels
+// with eight list slots each, a square 3x3 or 5x5 window at stride 1, four
+// sets (c_out = 4n <= 64), the whole output map in LDS as blocks of 64
+// pixels, one wavefront per (tap row, block).
+struct GatherPlan {
+  cs::GatherArgs ga;
+  size_t shmem;
+};
+
+bool gather_plan(const cs::ConvGeom& geo, const void* aug, int k, int shift, int write_sums,
+                 GatherPlan* pl) {
+  if (geo.C != cs::GATH_C || geo.cap != cs::GATH_CAP || geo.S != 1 || geo.KH != geo.KW) return false;
+  if ((geo.KW != 3 && geo.KW != 5) || geo.G != 4 || geo.c_out > 64 || !aligned(aug, 4)) return false;
+  if (geo.pool != 1 && geo.pool != 2) return false;
+  const int64_t npix = (int64_t)geo.H * geo.W;
+  const int64_t nout = (int64_t)geo.Ho * geo.Wo;
+  if (npix < 1 || npix > cs::GATH_BD || nout < 1) return false;
+  const int NH = (int)((nout + 63) / 64);
+  if (geo.KW * NH > cs::GATH_BD / 64) return false;
+  const int nitems = (geo.Ho / geo.pool) * (geo.Wo / geo.pool);
+  if (nitems < 1) return false;
+  const size_t o_tab = (size_t)NH * cs::GATH_BLK_B;
+  const size_t o_ent = o_tab + (size_t)(geo.G / 2) * geo.KW * geo.KW * cs::GATH_C * 4;
+  const size_t o_cnt = o_ent + (size_t)npix * cs::GATH_CAP * 2;
+  const size_t o_bias = o_cnt + round16((size_t)npix * 4);
+  const size_t o_pt = o_bias + round16((size_t)geo.c_out * 4);
+  const size_t total = o_pt + round16((size_t)nitems * (geo.c_out + 1) * 4);
+  if (total > kCuLds) return false;
+  cs::GatherArgs& ga = pl->ga;
+  ga.NH = NH;
+  ga.nitems = nitems;
+  ga.k = k;
+  ga.shift = shift;
+  ga.write_sums = write_sums;
+  ga.off_tab = (uint32_t)o_tab;
+  ga.off_ent = (uint32_t)o_ent;
+  ga.off_cnt = (uint32_t)o_cnt;
+  ga.off_bias = (uint32_t)o_bias;
+  ga.off_pt = (uint32_t)o_pt;
+  ga.fd_wo = cs::make_fastdiv((uint32_t)geo.Wo);
+  ga.fd_wp = cs::make_fastdiv((uint32_t)(geo.Wo / geo.pool));
+  ga.fd_items = cs::make_fastdiv((uint32_t)nitems);
+  pl->shmem = total;
+  return true;
+}
+
+template <int POOL, int KW, int KM, bool GA>
+void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const GatherPlan& gp,
+                        const SamplePlan& sp,
                         size_t shmem, hipStream_t s, const void* x, const void* aug0,
                         const void* bias0, void* y0, const cs::ListOut& lo0,
                         const cs::ConvGeom& geo0, const void* aug, const void* bias, void* y,
@@ -2093,6 +2140,7 @@ void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const S
                         lo,
                         geo,
                         scp.sc,
+                        gp.ga,
                         static_cast<const uint16_t*>(aug2),
                         static_cast<const int32_t*>(bias2),
                         static_cast<int32_t*>(y2),
@@ -2100,8 +2148,12 @@ void launch_dense_chain(const cs::DenseArgs& da, const ScatterPlan& scp, const S
                         geo2,
                         sp.sa,
                         nx};
-  hipLaunchKernelGGL((cs::dense_scatter_sample<POOL, KW, KM>), dim3((unsigned)geo0.B),
-                     dim3(cs::SCAT_BD), shmem, s, a);
+  if constexpr (GA)
+    hipLaunchKernelGGL((cs::dense_gather_sample<POOL, KW, KM>), dim3((unsigned)geo0.B),
+                       dim3(cs::GATH_BD), shmem, s, a);
+  else
+    hipLaunchKernelGGL((cs::dense_scatter_sample<POOL, KW, KM>), dim3((unsigned)geo0.B),
+                       dim3(cs::SCAT_BD), shmem, s, a);
 }
 
 int cs_conv2d_dense_kwta_chain3(
@@ -2149,27 +2201,35 @@ int cs_conv2d_dense_kwta_chain3(
   const bool lists_ok = ocap % 4 == 0 && aligned(oidx, 8) && aligned(oval, 4);
   cs::DenseArgs da{};
   size_t sh0 = 0;
-  ScatterPlan scp;
+  ScatterPlan scp{};
+  GatherPlan gp{};
   SamplePlan sp;
+  bool ga = false;
   if (k <= 32 && lists_ok && aligned(aug, 16) && (pool == 1 || pool == 2) &&
       (int64_t)b * hp0 * wp0 * 64 < INT32_MAX &&
       dense_plan(geo0, x, w, pad, k, shift, keep_sums, ocap, 1, hp0, kCuLds, &da, &sh0) &&
       da.tiles_img == 1 && !sample_plan(geo, xt, k2, shift2, keep_sums, &sp) &&
-      scatter_plan(geo, xt, aug2, k2, shift2, keep_sums, &scp) && scp.sc.bands == 1 &&
-      scp.blocks == b && scp.gpl == 2 && scp.m == 1 &&
+      ((ga = pool == 2 && gather_plan(geo, aug2, k2, shift2, keep_sums, &gp)) ||
+       (scatter_plan(geo, xt, aug2, k2, shift2, keep_sums, &scp) && scp.sc.bands == 1 &&
+        scp.blocks == b && scp.gpl == 2 && scp.m == 1)) &&
       sample_plan(geo2, xt, k3, shift3, keep_sums, &sp)) {
     const cs::NextLayer nx{static_cast<const uint16_t*>(aug4), static_cast<const int32_t*>(bias4),
                            static_cast<int32_t*>(y4), c_out4 / n4, n4, c_out4,
                            (uint32_t)round16(sp.shmem)};
     const size_t sh2 = (size_t)nx.off_acc + round16((size_t)c_out4 * 4);
-    const size_t shmem = std::max(sh0, std::max(scp.shmem, sh2));
+    const size_t shmem = std::max(sh0, std::max(ga ? gp.shmem : scp.shmem, sh2));
     if (shmem <= kCuLds) {
       const cs::ListOut lo0{oidx, oval, ocnt, ocap};
       const cs::ListOut lo{oidx2, oval2, ocnt2, ocap2};
       const cs::ListOut lo2{oidx3, oval3, ocnt3, ocap3};
-#define CS_DC3(P_, K_, M_)                                                                     \
-  launch_dense_chain<P_, K_, M_>(da, scp, sp, shmem, s, x, aug, bias, y, lo0, geo0, aug2, bias2, \
-                                 y2, lo, geo, aug3, bias3, y3, lo2, geo2, nx)
+#define CS_DC4(P_, K_, M_, G_)                                                                  \
+  launch_dense_chain<P_, K_, M_, G_>(da, scp, gp, sp, shmem, s, x, aug, bias, y, lo0, geo0, aug2, \
+                                     bias2, y2, lo, geo, aug3, bias3, y3, lo2, geo2, nx)
+#define CS_DC3(P_, K_, M_)                                              \
+  do {                                                                  \
+    if (P_ == 2 && K_ <= 5 && ga) CS_DC4(P_, K_, M_, (P_ == 2 && K_ <= 5)); \
+    else CS_DC4(P_, K_, M_, false);                                     \
+  } while (0)
 #define CS_DC(P_, K_)                                   \
   do {                                                  \
     if (da.kmode == 1) CS_DC3(P_, K_, 1);               \
@@ -2187,6 +2247,7 @@ int cs_conv2d_dense_kwta_chain3(
       }
 #undef CS_DC
 #undef CS_DC3
+#undef CS_DC4
       return launch_status();
     }
   }

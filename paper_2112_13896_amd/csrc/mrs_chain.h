@@ -3,8 +3,10 @@
 // 4: the first layer runs sparse-dense on the dense input):
 //  1. the dense-input first layer on the matrix cores (dense_body: conv, 2x2
 //     pool, k-WTA, requantisation) over the whole image, its lists written;
-//  2. after a workgroup barrier, the input-stationary layer (scatter_body) on
-//     those lists, its k-WTA lists written;
+//  2. after a workgroup barrier, the second layer on those lists, its k-WTA
+//     lists written: output-stationary (gather_body: 64 input channels, eight
+//     list slots, a square window, four sets, every output pixel in LDS) or
+//     else input-stationary (scatter_body);
 //  3. after another barrier, the layer whose window is the whole pooled map
 //     (sample_body) on them, with the last linear layer on its winners.
 // The barriers' workgroup-scope release/acquire order each phase's global
@@ -20,6 +22,7 @@
 #include <stdint.h>
 
 #include "conv_dense_mfma.h"
+#include "mrs_gather.h"
 #include "mrs_sample.h"
 #include "mrs_scatter.h"
 
@@ -40,6 +43,7 @@ struct ChainArgs {
   ListOut lo;
   ConvGeom geo;
   ScatterArgs sc;
+  GatherArgs ga;
   const uint16_t* aug2;
   const int32_t* bias2;
   int32_t* y2;
@@ -60,9 +64,10 @@ __device__ __forceinline__ const ChainArgs* chain_args() {
   return (const ChainArgs*)p;
 }
 
-// KM: the first layer's k-WTA selection (its kmode), fixed at compile time.
-template <int POOL, int KW, int KM>
-__global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
+// KM: the first layer's k-WTA selection (its kmode), fixed at compile time;
+// GA: the second layer output-stationary (four sets).
+template <int POOL, int KW, int KM, bool GA>
+__device__ __forceinline__ void dense_chain_body() {
   CS_STAMP_COUNT(15);
   CS_STAMP(0);
   {
@@ -79,9 +84,15 @@ __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
     const ChainArgs* a = chain_args();
     const ListOut lo0 = a->lo0, lo = a->lo;
     const ConvGeom geo = a->geo;
-    const ScatterArgs sc = a->sc;
-    scatter_body<int8_t, KW, 2, 1>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt, a->aug,
-                                   a->bias, a->y, nullptr, lo, geo, sc, blockIdx.x);
+    if constexpr (GA) {
+      const GatherArgs ga = a->ga;
+      gather_body<int8_t, KW, 4>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt, a->aug,
+                                 a->bias, a->y, nullptr, lo, geo, ga, blockIdx.x);
+    } else {
+      const ScatterArgs sc = a->sc;
+      scatter_body<int8_t, KW, 2, 1>(lo0.idx, static_cast<const int8_t*>(lo0.val), lo0.cnt,
+                                     a->aug, a->bias, a->y, nullptr, lo, geo, sc, blockIdx.x);
+    }
   }
   __syncthreads();
   CS_STAMP(7);
@@ -99,6 +110,16 @@ __global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
   __syncthreads();
 #endif
   CS_STAMP(13);
+}
+
+template <int POOL, int KW, int KM>
+__global__ __launch_bounds__(SCAT_BD, 8) void dense_scatter_sample(ChainArgs) {
+  dense_chain_body<POOL, KW, KM, false>();
+}
+
+template <int POOL, int KW, int KM>
+__global__ __launch_bounds__(SCAT_BD, 8) void dense_gather_sample(ChainArgs) {
+  dense_chain_body<POOL, KW, KM, true>();
 }
 
 }  // namespace cs

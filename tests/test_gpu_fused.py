@@ -500,8 +500,13 @@ def test_chain3_matches_separate_calls(case):
 # (b, h, w, c_in), kh, kw, pad, pool, k, shift | kh2, pad2, c_out2, n2, pool2, k2, shift2 |
 # c_out3, n3, k3, shift3 | c_out4, n4 | ties
 DENSE_CHAIN_CASES = [
-    # keyword-spotting shape at a small batch: one kernel
+    # keyword-spotting shape at a small batch: one kernel (second layer output-stationary)
     ((5, 32, 32, 1), 5, 5, 0, 2, 8, 11, 5, 0, 64, 16, 2, 8, 9, 1500, 20, 75, 8, 12, 1, False),
+    # output-stationary second layer with padding, no second pool, one 64-pixel
+    # block, ties in the first layer
+    ((3, 16, 16, 1), 3, 3, 1, 2, 8, 0, 3, 1, 64, 16, 1, 8, 3, 100, 4, 10, 5, 10, 2, True),
+    # output-stationary with 48 outputs (four sets of 12) and three pixel blocks
+    ((2, 28, 28, 1), 5, 5, 2, 2, 8, 10, 3, 1, 48, 12, 2, 6, 8, 60, 6, 12, 6, 12, 1, False),
     # no first pool, 3x3 pad 1 twice, ties in the first layer: one kernel
     ((3, 12, 12, 2), 3, 3, 1, 1, 8, 0, 3, 1, 64, 8, 2, 6, 5, 100, 4, 10, 5, 10, 2, True),
     # 128 channels in the second layer: the two-call fallback
