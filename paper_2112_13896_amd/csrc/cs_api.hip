@@ -2084,7 +2084,7 @@ struct GatherPlan {
 bool gather_plan(const cs::ConvGeom& geo, const void* aug, int k, int shift, int write_sums,
                  GatherPlan* pl) {
   if (geo.C != cs::GATH_C || geo.cap != cs::GATH_CAP || geo.S != 1 || geo.KH != geo.KW) return false;
-  if ((geo.KW != 3 && geo.KW != 5) || geo.G != 4 || geo.c_out > 64 || !aligned(aug, 4)) return false;
+  if ((geo.KW != 3 && geo.KW != 5) || geo.G != 4 || geo.c_out > 64 || !aligned(aug, 16)) return false;
   if (geo.pool != 1 && geo.pool != 2) return false;
   const int64_t npix = (int64_t)geo.H * geo.W;
   const int64_t nout = (int64_t)geo.Ho * geo.Wo;

@@ -81,7 +81,7 @@ __device__ __forceinline__ void gather_body(const uint16_t* __restrict__ lidx,
   int* pt = reinterpret_cast<int*>(smem + ga.off_pt);              // [nitems][c_out + 1]
 
   // ---- global loads issued together: counts, entries (two per thread and
-  // round), table pieces
+  // round), table pieces (16 bytes per thread and round)
   int c = 0;
   if (tid < npix) c = lcnt[prow0 + tid];
   const int npairs = npix * (GATH_CAP / 2);                        // entry pairs
@@ -99,20 +99,43 @@ __device__ __forceinline__ void gather_body(const uint16_t* __restrict__ lidx,
   }
   // the table: word (tap*C + channel)*NPR + pr of the packed tensor holds
   // sets 2pr, 2pr + 1; each 16-bit half's Kernel ID becomes the output
-  // channel (2pr + half)*n + min(kid, n - 1) (< 64)
-  {
-    const int nw = T * GATH_C * NPR;                               // words
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(aug);
-    for (int e = tid; e < nw; e += GATH_BD) {
-      const uint32_t w = src[e];
-      const int r = NPR == 2 ? (e >> 1) : e, pr = NPR == 2 ? (e & 1) : 0;
-      const uint32_t k0 = (w >> 8) & 0xFFu, k1 = w >> 24;
-      const uint32_t c0 = (uint32_t)(2 * pr * n) + (k0 < (uint32_t)n ? k0 : (uint32_t)(n - 1));
-      const uint32_t c1 = (uint32_t)((2 * pr + 1) * n) + (k1 < (uint32_t)n ? k1 : (uint32_t)(n - 1));
-      tab[pr * T * GATH_C + r] = (w & 0x00FF00FFu) | c0 << 8 | c1 << 24;
+  // channel (2pr + half)*n + min(kid, n - 1) (< 64).  Piece m (16 bytes) is
+  // words 4m .. 4m + 3: rows 4m/NPR .. of pair (word mod NPR).
+  constexpr int N16 = T * GATH_C * NPR / 4;                        // pieces
+  constexpr int TPRE = (N16 + GATH_BD - 1) / GATH_BD;
+  const su32x4* src = reinterpret_cast<const su32x4*>(aug);
+  su32x4 tv[TPRE];
+#pragma unroll
+  for (int u = 0; u < TPRE; ++u) {
+    const int m = u * GATH_BD + tid;
+    tv[u] = src[m < N16 ? m : N16 - 1];
+  }
+  auto chan = [n](uint32_t w, int pr) -> uint32_t {
+    const uint32_t k0 = (w >> 8) & 0xFFu, k1 = w >> 24;
+    const uint32_t c0 = (uint32_t)(2 * pr * n) + (k0 < (uint32_t)n ? k0 : (uint32_t)(n - 1));
+    const uint32_t c1 = (uint32_t)((2 * pr + 1) * n) + (k1 < (uint32_t)n ? k1 : (uint32_t)(n - 1));
+    return (w & 0x00FF00FFu) | c0 << 8 | c1 << 24;
+  };
+  for (int o = tid; o < c_out; o += GATH_BD) bias_s[o] = bias ? bias[o] : 0;
+#pragma unroll
+  for (int u = 0; u < TPRE; ++u) {
+    const int m = u * GATH_BD + tid;
+    if (m < N16) {
+      const su32x4 v = tv[u];
+      if constexpr (NPR == 2) {
+        // rows 2m, 2m + 1: (pair 0, pair 1) words (x, y) and (z, w)
+        *reinterpret_cast<uint2*>(tab + 2 * m) = make_uint2(chan(v.x, 0), chan(v.z, 0));
+        *reinterpret_cast<uint2*>(tab + T * GATH_C + 2 * m) = make_uint2(chan(v.y, 1), chan(v.w, 1));
+      } else {
+        su32x4 o;
+        o.x = chan(v.x, 0);
+        o.y = chan(v.y, 0);
+        o.z = chan(v.z, 0);
+        o.w = chan(v.w, 0);
+        reinterpret_cast<su32x4*>(tab)[m] = o;
+      }
     }
   }
-  for (int o = tid; o < c_out; o += GATH_BD) bias_s[o] = bias ? bias[o] : 0;
   {
     su32x4* a4 = reinterpret_cast<su32x4*>(accb);
     const su32x4 z = {0u, 0u, 0u, 0u};
