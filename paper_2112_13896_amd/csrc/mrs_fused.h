@@ -151,6 +151,9 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
           const uint32_t kx = order_key(v(i < i_hi ? i : i_hi - 1));
           blk[j] = i < i_hi ? kx : 0u;
         }
+        // the block's reads leave together (left to itself the scheduler
+        // waits for each read before issuing the next)
+        __builtin_amdgcn_sched_barrier(0);
         bitonic_sort_desc<KMAX>(blk);
         if (i0 == i_lo) {
 #pragma unroll
@@ -188,13 +191,19 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
     uint32_t gtm = 0u, eqm = 0u;
     if (live && k > 0) {
       for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
+        uint32_t kb[BK];
 #pragma unroll
         for (int j = 0; j < BK; ++j) {
           const int i = i0 + j;
-          const uint32_t key = order_key(v(i < i_hi ? i : i_hi - 1));
+          kb[j] = order_key(v(i < i_hi ? i : i_hi - 1));
+        }
+        __builtin_amdgcn_sched_barrier(0);               // the batch's reads leave together
+#pragma unroll
+        for (int j = 0; j < BK; ++j) {
+          const int i = i0 + j;
           const uint32_t bit = i < i_hi ? 1u << (i - i_lo) : 0u;
-          gtm |= key > thr ? bit : 0u;
-          eqm |= key == thr ? bit : 0u;
+          gtm |= kb[j] > thr ? bit : 0u;
+          eqm |= kb[j] == thr ? bit : 0u;
         }
       }
     }
