@@ -187,23 +187,27 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
       need = k - gt;
     }
     // --- the lane's quarter as bit masks (bit j: element i_lo + j; c <= 128,
-    // so a quarter has at most 32 elements): keys above T and keys equal to T
-    uint32_t gtm = 0u, eqm = 0u;
+    // so a quarter has at most 32 elements): keys above T, keys equal to T,
+    // and (list output) elements whose output value is non-zero
+    uint32_t gtm = 0u, eqm = 0u, nzm = 0u;
+    const bool lists = tl_idx != nullptr;
     if (live && k > 0) {
       for (int i0 = i_lo; i0 < i_hi; i0 += BK) {
-        uint32_t kb[BK];
+        A vb[BK];
 #pragma unroll
         for (int j = 0; j < BK; ++j) {
           const int i = i0 + j;
-          kb[j] = order_key(v(i < i_hi ? i : i_hi - 1));
+          vb[j] = v(i < i_hi ? i : i_hi - 1);
         }
         __builtin_amdgcn_sched_barrier(0);               // the batch's reads leave together
 #pragma unroll
         for (int j = 0; j < BK; ++j) {
           const int i = i0 + j;
           const uint32_t bit = i < i_hi ? 1u << (i - i_lo) : 0u;
-          gtm |= kb[j] > thr ? bit : 0u;
-          eqm |= kb[j] == thr ? bit : 0u;
+          const uint32_t key = order_key(vb[j]);
+          gtm |= key > thr ? bit : 0u;
+          eqm |= key == thr ? bit : 0u;
+          if (lists) nzm |= kwta_out<A, TO>(vb[j], shift) != TO(0) ? bit : 0u;
         }
       }
     }
@@ -221,11 +225,7 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
     }
     int last_tie = tm ? i_lo + 31 - __builtin_clz(tm) : -1;
     // winners with a non-zero output value: their list positions
-    uint32_t putm = 0u;
-    for (uint32_t w = gtm | tm; w != 0u; w &= w - 1u) {
-      const int j = __builtin_ctz(w);
-      putm |= kwta_out<A, TO>(v(i_lo + j), shift) != TO(0) ? 1u << j : 0u;
-    }
+    const uint32_t putm = (gtm | tm) & nzm;
     const int win_l = __popc(putm);
     const int pos0 = quad_excl_sum(win_l, qd);           // list position of the first winner
     // the last winning tie of the row: the largest over the quad
