@@ -759,7 +759,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
   for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_unit && key[j] == thr) ? 1 : 0;
   int tie_rank = group_incl_sum(eq, log2Us, ps) - eq;
   uint32_t winm = 0;                                    // bit j: channel o0 + j wins
-  int wcount = 0;
+  uint32_t putm = 0;                                    // ... and has a non-zero value
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     bool w;
@@ -776,8 +776,9 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
       w = false;
     }
     winm |= w ? 1u << j : 0u;
-    wcount += (lo.idx ? (w && v[j] != 0.f) : w) ? 1 : 0;
+    putm |= (w && v[j] != 0.f) ? 1u << j : 0u;
   }
+  const int wcount = __popc(lo.idx ? putm : winm);
   CS_STAMP(20);
   if (lo.idx) {
     const int incl = group_incl_sum(wcount, log2U, p);
@@ -785,13 +786,13 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     if (live) {
       uint16_t* oi = lo.idx + row * lo.cap;
       TO* ov = static_cast<TO*>(lo.val) + row * lo.cap;
-#pragma unroll
-      for (int j = 0; j < KP; ++j) {
-        if (((winm >> j) & 1u) && v[j] != 0.f) {
-          oi[pos] = (uint16_t)(o0 + j);
-          ov[pos] = (TO)v[j];
-          ++pos;
-        }
+      // one pass per winner of the lane (a few), the value read back from
+      // the lane's own column, instead of KP predicated slots
+      for (uint32_t w = putm; w != 0u; w &= w - 1u) {
+        const int j = __builtin_ctz(w);
+        oi[pos] = (uint16_t)(o0 + j);
+        ov[pos] = (TO)acc[j * BLK_BD + threadIdx.x];
+        ++pos;
       }
       if (p == (1 << log2U) - 1) lo.cnt[row] = incl;
     }
