@@ -618,6 +618,24 @@ __device__ __forceinline__ void group_masks(int log2U, uint32_t (&mk)[4]) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) mk[s] = log2U > s ? 0xFFFFFFFFu : 0u;
 }
+// In-place transpose of a 32 x 32 bit matrix held as 32 words: afterwards
+// bit j of a[b] is bit b of the original a[j] (five stages of block swaps,
+// each row pair by two shifts and two bit-field selects).
+__device__ __forceinline__ void bit_transpose32(uint32_t (&a)[32]) {
+  constexpr uint32_t M[5] = {0x0000FFFFu, 0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
+#pragma unroll
+  for (int st = 0; st < 5; ++st) {
+    const int w = 16 >> st;
+    const uint32_t m = M[st];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      if (j & w) continue;
+      const uint32_t x = a[j], y = a[j + w];
+      a[j] = (x & m) | ((y << w) & ~m);
+      a[j + w] = ((x >> w) & m) | (y & ~m);
+    }
+  }
+}
 __device__ __forceinline__ uint32_t group_min_nb(uint32_t v, const uint32_t (&mk)[4]) {
   uint32_t t;
   t = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false) | ~mk[0];
@@ -695,6 +713,52 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
         if (cntp == k) done = true;
       }
     };
+    if constexpr (KP == 32) {
+      // bit-sliced: plane b holds bit b of the lane's 32 keys (bit j: key
+      // j), so a step's count is the keys already above the prefix plus one
+      // bit count of the planes' AND with the keys that still match it
+      uint32_t sl[32];
+#pragma unroll
+      for (int j = 0; j < 32; ++j) sl[j] = key[j];
+      bit_transpose32(sl);
+      uint32_t match = 0xFFFFFFFFu, above = 0u;
+      // the group masks as vector values (an AND each, instead of selects on
+      // scalar conditions the compiler spills at this register pressure)
+      uint32_t mv[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        mv[q] = mk[q];
+        asm volatile("" : "+v"(mv[q]));
+      }
+      // each step branch-free: a unit still searching takes bit b when at
+      // least k keys are at or above the candidate, else the matching keys
+      // with bit b set are above the prefix from now on (k as a vector value:
+      // the scalar one is a spilled argument, reloaded every step)
+      int kv = k;
+      asm volatile("" : "+v"(kv));
+#pragma unroll
+      for (int bit = 31; bit >= 0; --bit) {
+        if (__ballot(!done) == 0ull) break;              // every unit of the wavefront found
+        const uint32_t hit = match & sl[bit];
+        const uint32_t nh = (uint32_t)__popc(hit);
+        uint32_t c = above + nh;
+        if (log2Us == 3) {
+          // units of eight lanes: three DPP adds with no masks
+          c += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)c, 0xB1, 0xF, 0xF, false);
+          c += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)c, 0x4E, 0xF, 0xF, false);
+          c += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)c, 0x141, 0xF, 0xF, false);
+        } else {
+          c = group_sum_nb(c, mv);
+        }
+        const bool take = !done && (int)c >= kv;
+        const bool drop = !done && (int)c < kv;
+        pre = take ? (pre | (1u << bit)) : pre;
+        cntp = take ? (int)c : cntp;
+        match = take ? hit : (drop ? (match & ~sl[bit]) : match);
+        above = drop ? above + nh : above;
+        done = done || cntp == kv;
+      }
+    } else {
     // bits 31..16 on the keys' high halves, two to a register (a candidate's
     // low half is 0 there, so key >= cand is a compare of the high halves)
     {
@@ -725,6 +789,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
         const uint32_t cand = pre | (1u << bit);
         step(cand, above + (uint32_t)KP - below16(lp, cand & 0xFFFFu));
       }
+    }
     }
     CS_STAMP(19);
     // the k-th largest key: the least key at or above the prefix.  key - pre
