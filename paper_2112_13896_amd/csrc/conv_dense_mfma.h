@@ -240,15 +240,15 @@ __device__ __forceinline__ void dense_body(const int8_t* __restrict__ x,
     TO* tl_val = reinterpret_cast<TO*>(smem + da.off_lval);
     switch (KM > 0 ? KM : da.kmode) {
       case 1:
-        kwta_quad_items<int32_t, TO, 8, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
+        kwta_quad_items<int32_t, TO, 8, BD, 64>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel, tl_idx,
                                         tl_val, lo.cap, lo.cnt);
         break;
       case 2:
-        kwta_quad_items<int32_t, TO, 16, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 16, BD, 64>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
       default:
-        kwta_quad_items<int32_t, TO, 32, BD>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
+        kwta_quad_items<int32_t, TO, 32, BD, 64>(otile, ostride, sm, rm, c_out, da.k, da.shift, sel,
                                          tl_idx, tl_val, lo.cap, lo.cnt);
         break;
     }

@@ -1024,8 +1024,12 @@ __global__ __launch_bounds__(BLK_BD, (KP > 0 && KP <= 16) ? 3 : 2) void mrs_bloc
         uint2* sel = reinterpret_cast<uint2*>(smem + ba.off_sel);
         uint16_t* gi = lo.idx ? lo.idx + (int64_t)item0 * lo.cap : nullptr;
         TO* gv = lo.idx ? static_cast<TO*>(lo.val) + (int64_t)item0 * lo.cap : nullptr;
-        kwta_quad_item<float, TO, QK, BLK_BD>(acc + tid, 0, ps, live, rm, c_out, ba.k, 0, sel, gi,
-                                              gv, lo.cap, lo.cnt);
+        if (c_out == 64)                                  // 16 channels per lane, known
+          kwta_quad_item<float, TO, QK, BLK_BD, 64>(acc + tid, 0, ps, live, rm, c_out, ba.k, 0,
+                                                    sel, gi, gv, lo.cap, lo.cnt);
+        else
+          kwta_quad_item<float, TO, QK, BLK_BD>(acc + tid, 0, ps, live, rm, c_out, ba.k, 0, sel,
+                                                gi, gv, lo.cap, lo.cnt);
         if (live && (ba.write_sums || !lo.idx)) {
           wave_lds_order();                              // sel of this quad, written by lane 0
           const uint2 sv = sel[ps];

@@ -121,12 +121,15 @@ struct RowMap {
 // (the DPP exchanges), `live` quads write.
 // ES: element stride of the row (1: a row-major tile; other: the quad's lanes
 // read their quarters from LDS columns of that stride, `otile` then being the
-// lane's own column and ostride unused).
-template <typename A, typename TO, int KMAX, int ES = 1>
+// lane's own column and ostride unused).  CC: the row length when the caller
+// knows it at compile time (c is then ignored; the quarters' bounds checks
+// fold away and the block loops unroll), 0: c.
+template <typename A, typename TO, int KMAX, int ES = 1, int CC = 0>
 __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int it, bool live,
                                                const RowMap& rm, int c, int k, int shift,
                                                uint2* sel, uint16_t* tl_idx, TO* tl_val, int cap,
                                                int32_t* gcnt) {
+  if constexpr (CC > 0) c = CC;
   constexpr int BK = 16;                               // keys read per batch (loads issued together)
   const int qd = threadIdx.x & 3;
   const int L = (c + 3) >> 2;                          // row quarter of a lane
@@ -254,14 +257,14 @@ __device__ __forceinline__ void kwta_quad_item(const A* otile, int ostride, int 
 }
 
 // All the tile's slots, one per quad of the workgroup's BD threads.
-template <typename A, typename TO, int KMAX, int BD = MRS_BD>
+template <typename A, typename TO, int KMAX, int BD = MRS_BD, int CC = 0>
 __device__ void kwta_quad_items(const A* otile, int ostride, const SlotMap& sm, const RowMap& rm,
                                 int c, int k, int shift, uint2* sel, uint16_t* tl_idx,
                                 TO* tl_val, int cap, int32_t* gcnt) {
   const int nsl = (sm.nslots + 3) & ~3;
   for (int base = 0; base < ((nsl + BD / 4 - 1) / (BD / 4)) * (BD / 4); base += BD / 4) {
     const int it = base + (threadIdx.x >> 2);
-    kwta_quad_item<A, TO, KMAX>(otile, ostride, it, sm.live(it), rm, c, k, shift, sel, tl_idx,
+    kwta_quad_item<A, TO, KMAX, 1, CC>(otile, ostride, it, sm.live(it), rm, c, k, shift, sel, tl_idx,
                                 tl_val, cap, gcnt);
   }
 }
