@@ -695,6 +695,9 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
   if (k < 0) return;
   uint32_t thr = 0u;
   int need = 0;
+  // KP == 32: the search leaves the winners as masks (bit j: key j) — keys
+  // above the final prefix, and keys that still match it
+  uint32_t gtm32 = 0u, eqm32 = 0u;
   if (k > 0 && k < c_unit) {
     uint32_t pre = 0u;
     int cntp = c_unit;
@@ -721,7 +724,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
 #pragma unroll
       for (int j = 0; j < 32; ++j) sl[j] = key[j];
       bit_transpose32(sl);
-      uint32_t match = 0xFFFFFFFFu, above = 0u;
+      uint32_t match = 0xFFFFFFFFu, above = 0u, above_m = 0u;
       // the group masks as vector values (an AND each, instead of selects on
       // scalar conditions the compiler spills at this register pressure)
       uint32_t mv[4];
@@ -756,8 +759,14 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
         cntp = take ? (int)c : cntp;
         match = take ? hit : (drop ? (match & ~sl[bit]) : match);
         above = drop ? above + nh : above;
+        above_m = drop ? (above_m | hit) : above_m;
         done = done || cntp == kv;
       }
+      // keys above the prefix are above the k-th largest; the matching ones
+      // are its copies when the search ran to bit 0, else (cntp == k) keys
+      // that all win
+      gtm32 = above_m;
+      eqm32 = match;
     } else {
     // bits 31..16 on the keys' high halves, two to a register (a candidate's
     // low half is 0 there, so key >= cand is a compare of the high halves)
@@ -792,6 +801,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     }
     }
     CS_STAMP(19);
+    if constexpr (KP != 32) {
     // the k-th largest key: the least key at or above the prefix.  key - pre
     // wraps the keys below the prefix above every key at or above it, so the
     // least of the differences (a tree of minima, then the group's) is the
@@ -816,15 +826,44 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
       for (int j = 0; j + w < KP; j += 2 * w) d[j] = add_u32(d[j], d[j + w]);
     const uint32_t eq_unit = group_sum_nb((uint32_t)KP - d[0], mk);
     need = k - (cntp - (int)eq_unit);
+    }
   }
+  uint32_t winm = 0;                                    // bit j: channel o0 + j wins
+  uint32_t putm = 0;                                    // ... and has a non-zero value
+  if constexpr (KP == 32) {
+    // need = k minus the unit's keys above; the first `need` matching keys
+    // of the unit in index order win (every lane takes part in the sums)
+    uint32_t mk2[4];
+    group_masks(log2Us, mk2);
+    const int nabove = (int)group_sum_nb((uint32_t)__popc(gtm32), mk2);
+    const int eq_l = __popc(eqm32);
+    const int tie0 = group_incl_sum(eq_l, log2Us, ps) - eq_l;
+    int m = k - nabove - tie0;
+    m = m < 0 ? 0 : (m > eq_l ? eq_l : m);
+    uint32_t tm = m >= eq_l ? eqm32 : 0u;
+    if (m > 0 && m < eq_l) {                            // a tie split at this lane (rare)
+      for (uint32_t e2 = eqm32; m > 0; --m) {
+        const uint32_t lb = e2 & (0u - e2);
+        tm |= lb;
+        e2 ^= lb;
+      }
+    }
+    winm = (!live || k == 0) ? 0u : (k >= c_unit ? 0xFFFFFFFFu : (gtm32 | tm));
+    putm = winm;
+    if (lo.idx) {
+      // winners whose value is exactly zero are left out of the list
+      for (uint32_t w = winm; w != 0u; w &= w - 1u) {
+        const int j = __builtin_ctz(w);
+        if (acc[j * BLK_BD + threadIdx.x] == 0.f) putm &= ~(1u << j);
+      }
+    }
+  } else {
   // ties in index order: this lane's first tie has rank (ties of the unit's
   // lanes before)
   int eq = 0;
 #pragma unroll
   for (int j = 0; j < KP; ++j) eq += (k > 0 && k < c_unit && key[j] == thr) ? 1 : 0;
   int tie_rank = group_incl_sum(eq, log2Us, ps) - eq;
-  uint32_t winm = 0;                                    // bit j: channel o0 + j wins
-  uint32_t putm = 0;                                    // ... and has a non-zero value
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     bool w;
@@ -842,6 +881,7 @@ __device__ __forceinline__ void blk_kwta_own(const float* acc, int log2U, int lo
     }
     winm |= w ? 1u << j : 0u;
     putm |= (w && v[j] != 0.f) ? 1u << j : 0u;
+  }
   }
   const int wcount = __popc(lo.idx ? putm : winm);
   CS_STAMP(20);
