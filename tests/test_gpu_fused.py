@@ -255,6 +255,45 @@ def test_fused_layer(case):
         assert near <= max(1, out.shape[0] // 100)
 
 
+@pytest.mark.parametrize("mode", ["lists", "dense"])
+@pytest.mark.parametrize("shape,kh", [((2, 6, 6, 256), 3), ((2, 7, 5, 1024), 1)])
+def test_blocks_f32_exact_ties(shape, kh, mode):
+    """The fp32 table-block layer with 32 channels per lane when many sums are
+    equal: integer-valued inputs, +-1 weights and an integer bias make every
+    sum an exact integer, with ties at the k-th largest in most pixels, so the
+    threshold search runs to its last bit and the tied channels are taken in
+    index order.  The sums and the k-WTA must equal the oracle's exactly."""
+    c_in = shape[3]
+    c_out, n, k, nnz = 256, 16, 26, 26 if kh == 3 else 102
+    pad = 1 if kh == 3 else 0
+    r = np.random.default_rng(4242 + kh)
+    rows = int(np.prod(shape[:3]))
+    x = np.zeros((rows, c_in), dtype=np.float32)
+    for i in range(rows):
+        pos = r.choice(c_in, size=nnz, replace=False)
+        x[i, pos] = r.integers(1, 3, size=nnz).astype(np.float32)
+    x = x.reshape(shape)
+    W = np.sign(weights(r, c_out, kh, kh, c_in, n, "f32")).astype(np.float32)
+    bias = r.integers(-2, 3, size=c_out).astype(np.float32)
+    aug, _ = ops.pack(W.reshape(c_out, -1), n)
+    xd = dev(x)
+    idx, lv, cnt = ops.compact(xd.reshape(-1, c_in))
+    plan = ops.mrs_plan(torch.float32, c_in, shape, kh, kh, 1, pad, c_out, n, 1, k)
+    assert plan["path"] == "blocks", plan
+    cap = ops.list_capacity(k) if mode == "lists" else None
+    y, res = ops.mrs_kwta_conv2d(idx, lv, cnt, shape, ops.aug_to_device(aug), kh, kh, n, 1, pad,
+                                 dev(bias), 1, k=k, keep_sums=True, cap=cap)
+    torch.cuda.synchronize()
+    ref = o.conv2d_nhwc(x, W, 1, pad, bias).reshape(-1, c_out)
+    assert np.array_equal(host(y).reshape(-1, c_out).astype(np.float64), ref), "sums"
+    srt = -np.sort(-ref, axis=1)
+    assert (srt[:, k - 1] == srt[:, k]).mean() > 0.5, "too few ties at the threshold"
+    want = np.where(o.kwta_winners(ref, k), ref, 0.0)
+    out = (dense_from_lists(*(host(t) for t in res), c_out) if mode == "lists"
+           else host(res).reshape(-1, c_out))
+    assert np.array_equal(out.astype(np.float64), want), "k-WTA output"
+
+
 @pytest.mark.parametrize("dtype", ["i8", "f32"])
 def test_sample_sums_only(dtype):
     """cs_mrs_conv2d (no k-WTA) of a large-table linear layer takes the
